@@ -1,0 +1,429 @@
+"""Pins of the CPU oracle against things other than itself (CPU only).
+
+Each check ties one oracle function to a published value, an exact rational
+computation, a library routine (numpy / torch on the CPU), a closed form or a
+brute force over tiny inputs, so that a dropped term, wrong sign, wrong index
+or transposed operand in the oracle fails here.
+"""
+import itertools
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+M64 = (1 << 64) - 1
+GAMMA = 0x9E3779B97F4A7C15
+
+
+def _vectors():
+    vals = []
+    with open(os.path.join(GOLDEN, "splitmix64_seed1234567.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            if line.startswith("seed"):
+                seed = int(line.split()[1])
+                continue
+            vals.append(int(line))
+    return seed, vals
+
+
+# --------------------------------------------------------------------------- mix64
+
+
+def test_mix64_matches_published_splitmix64_vectors():
+    seed, vals = _vectors()
+    s = seed
+    for v in vals:
+        s = (s + GAMMA) & M64
+        assert O.mix64(s) == v
+
+
+def _unxorshift(y, k):
+    x = y
+    sh = k
+    while sh < 64:
+        x ^= y >> sh
+        sh += k
+    return x & M64
+
+
+def mix64_inverse(z):
+    """Inverse of the splitmix64 output function, step by step."""
+    z = _unxorshift(z, 31)
+    z = (z * pow(0x94D049BB133111EB, -1, 1 << 64)) & M64
+    z = _unxorshift(z, 27)
+    z = (z * pow(0xBF58476D1CE4E5B9, -1, 1 << 64)) & M64
+    z = _unxorshift(z, 30)
+    return z
+
+
+def test_mix64_is_a_bijection():
+    g = np.random.default_rng(1)
+    for x in g.integers(0, 2**63, size=200, dtype=np.int64).tolist() + [0, 1, M64]:
+        assert mix64_inverse(O.mix64(x)) == x
+
+
+# --------------------------------------------------------------------------- row init
+
+
+def _round_f32(fr: Fraction) -> np.float32:
+    """Exact round-to-nearest-even of a rational to fp32."""
+    f = np.float32(float(fr))
+    cands = {f, np.nextafter(f, np.float32(np.inf)), np.nextafter(f, np.float32(-np.inf))}
+    best = None
+    for c in cands:
+        d = abs(Fraction(float(c)) - fr)
+        key = (d, int(np.array(c, dtype=np.float32).view(np.uint32)) & 1)
+        if best is None or key < best[0]:
+            best = (key, c)
+    return best[1]
+
+
+def _key_for_stream_state(seed, z):
+    """The key whose per-row hash stream starts at splitmix64 state z."""
+    k = mix64_inverse(z) ^ O.mix64(seed)
+    return k - (1 << 64) if k >= (1 << 63) else k
+
+
+@pytest.mark.parametrize("seed", [0, 2509, 0xDEADBEEFCAFEF00D])
+def test_init_row_is_splitmix64_stream_on_unit_interval(seed):
+    # With lo=0, hi=1 element j is exactly the top 24 bits of the (j+1)-th
+    # splitmix64 output from the key's stream state, divided by 2^24.
+    s0, vals = _vectors()
+    key = _key_for_stream_state(seed, s0)
+    w = O.init_row(seed, key, len(vals), 0.0, 1.0)
+    expect = np.array([(v >> 40) / float(1 << 24) for v in vals], dtype=np.float32)
+    assert np.array_equal(w, expect)
+
+
+def test_init_row_single_rounding_on_symmetric_interval():
+    s0, vals = _vectors()
+    seed = 77
+    key = _key_for_stream_state(seed, s0)
+    lo, hi = np.float32(-0.01), np.float32(0.01)
+    span = np.float32(hi - lo)
+    w = O.init_row(seed, key, len(vals), float(lo), float(hi))
+    for j, v in enumerate(vals):
+        u = Fraction(v >> 40, 1 << 24)
+        exact = u * Fraction(float(span)) + Fraction(float(lo))
+        assert w[j] == _round_f32(exact), j
+
+
+def test_init_row_distribution_and_sensitivity():
+    D = 16
+    keys = np.arange(-4000, 4000, 3, dtype=np.int64)
+    W = np.stack([O.init_row(5, int(k), D, -0.01, 0.01) for k in keys])
+    assert W.min() >= -0.01 and W.max() <= np.float32(0.01)
+    # uniform on [-0.01, 0.01]: mean 0, variance 0.02^2/12, per element position
+    assert abs(W.mean()) < 2e-4
+    assert abs(W.var() / (0.02**2 / 12) - 1) < 0.05
+    for j in range(D):
+        assert abs(W[:, j].mean()) < 1.2e-3
+    # adjacent elements uncorrelated; different seed / key give different rows
+    c = np.corrcoef(W[:, :-1].ravel(), W[:, 1:].ravel())[0, 1]
+    assert abs(c) < 0.05
+    assert not np.array_equal(O.init_row(5, 10, D, -0.01, 0.01), O.init_row(6, 10, D, -0.01, 0.01))
+    assert not np.array_equal(O.init_row(5, 10, D, -0.01, 0.01), O.init_row(5, 11, D, -0.01, 0.01))
+    assert np.array_equal(O.init_row(5, 10, D, -0.01, 0.01), O.init_row(5, 10, D, -0.01, 0.01))
+
+
+# --------------------------------------------------------------------------- bf16
+
+
+def test_bf16_roundtrip_exhaustive():
+    for h in range(1 << 16):
+        x = O.bf16_to_f32(h)
+        if np.isnan(x):
+            assert O.bf16_rne(x) == 0x7FC0
+        else:
+            assert O.bf16_rne(x) == h
+
+
+def test_bf16_rne_matches_torch_including_ties():
+    g = np.random.default_rng(3)
+    bits = g.integers(0, 1 << 32, size=20000, dtype=np.uint64).astype(np.uint32)
+    # force exact ties (low 16 bits 0x8000) and near-ties on a third of them
+    bits[::3] = (bits[::3] & 0xFFFF0000) | 0x8000
+    bits[1::7] = (bits[1::7] & 0xFFFF0000) | 0x7FFF
+    x = bits.view(np.float32)
+    x = x[np.isfinite(x)]
+    ref = torch.from_numpy(x.copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    got = np.array([O.bf16_rne(float(v)) for v in x], dtype=np.uint16)
+    assert np.array_equal(got, ref)
+
+
+# --------------------------------------------------------------------------- dedup
+
+
+def _first_occurrence_unique(seq):
+    _, idx = np.unique(seq, return_index=True)
+    return seq[np.sort(idx)]
+
+
+def test_dedup_brute_force_all_sequences_over_4_keys():
+    alphabet = np.array([7, -3, 0, 2**62], dtype=np.int64)
+    for n in range(0, 5):
+        for combo in itertools.product(range(4), repeat=n):
+            seq = alphabet[list(combo)] if n else np.zeros(0, dtype=np.int64)
+            st, u, inv = O.dedup(seq)
+            assert st == O.OK
+            assert np.array_equal(u, _first_occurrence_unique(seq))
+            assert np.array_equal(u[inv], seq)
+
+
+def test_dedup_invariants_large():
+    g = np.random.default_rng(11)
+    seq = g.zipf(1.3, size=50000).astype(np.int64) * 1_000_003 - 7
+    st, u, inv = O.dedup(seq)
+    assert st == O.OK
+    assert np.array_equal(u[inv], seq)                       # reconstruction
+    assert len(np.unique(u)) == len(u)                       # distinct
+    assert np.array_equal(np.sort(u), np.unique(seq))        # same set as numpy
+    first = np.full(len(u), len(seq))
+    np.minimum.at(first, inv, np.arange(len(seq)))
+    assert np.all(np.diff(first) > 0)                        # first-occurrence order
+
+
+def test_dedup_rejects_reserved_keys():
+    for bad in (np.iinfo(np.int64).min, np.iinfo(np.int64).min + 1):
+        st, _, _ = O.dedup(np.array([1, bad, 2], dtype=np.int64))
+        assert st == O.EKEY
+    st, u, _ = O.dedup(np.array([np.iinfo(np.int64).max, 0, -1], dtype=np.int64))
+    assert st == O.OK and len(u) == 3
+
+
+# --------------------------------------------------------------------------- find-or-insert
+
+
+def test_find_or_insert_invariants():
+    T = O.Table(8, seed=9)
+    g = np.random.default_rng(2)
+    keys = g.integers(-50, 50, size=300).astype(np.int64)
+    st, rows, nn = T.find_or_insert(keys)
+    assert st == O.OK
+    U = len(np.unique(keys))
+    assert nn == U and T.size() == U
+    # same key -> same row, distinct keys -> distinct rows, rows in [0, live)
+    for k in np.unique(keys):
+        assert len(set(rows[keys == k])) == 1
+    assert len(set(rows.tolist())) == U and rows.min() == 0 and rows.max() == U - 1
+    # new rows are numbered in first-occurrence order
+    assert np.array_equal(rows[np.sort(np.unique(keys, return_index=True)[1])], np.arange(U))
+    # re-inserting inserts nothing and returns the same rows
+    st2, rows2, nn2 = T.find_or_insert(keys[::-1])
+    assert nn2 == 0 and np.array_equal(rows2, rows[::-1])
+    # present set equals the inserted set; rows hold their init values, state zero
+    ek, er = T.export()
+    assert np.array_equal(np.sort(ek), np.unique(keys))
+    found, w, s = T.read_rows(np.unique(keys))
+    assert found == U and np.all(s == 0)
+    for k, wr in zip(np.unique(keys), w):
+        assert np.array_equal(wr, O.init_row(9, int(k), 8, -0.01, 0.01))
+
+
+def test_find_or_insert_bounded_table_efull_and_ekey():
+    T = O.Table(4, max_live=3)
+    st, rows, nn = T.find_or_insert(np.array([5, 6, 5, 7, 8, 9, 6], dtype=np.int64))
+    assert st == O.EFULL and nn == 3
+    assert rows.tolist() == [0, 1, 0, 2, -1, -1, 1]
+    st, _, _ = T.find_or_insert(np.array([np.iinfo(np.int64).min], dtype=np.int64))
+    assert st == O.EKEY
+
+
+def test_bf16_table_rows_are_rounded_init():
+    T = O.Table(8, row_dtype=O.BF16, seed=4)
+    T.find_or_insert(np.array([1, 2, 3], dtype=np.int64))
+    _, w, _ = T.read_rows(np.array([1, 2, 3], dtype=np.int64))
+    for k, wr in zip([1, 2, 3], w):
+        ref = torch.from_numpy(O.init_row(4, k, 8, -0.01, 0.01)).to(torch.bfloat16).float().numpy()
+        assert np.array_equal(wr, ref)
+
+
+# --------------------------------------------------------------------------- pooling
+
+
+def _tiny_batch(g, n_bags, max_len, vocab, allow_empty=True):
+    lens = g.integers(0 if allow_empty else 1, max_len + 1, size=n_bags)
+    off = np.zeros(n_bags + 1, dtype=np.int64)
+    np.cumsum(lens, out=off[1:])
+    vals = (g.zipf(1.4, size=int(off[-1])) % vocab).astype(np.int64) * 31 + 5
+    return vals, off
+
+
+@pytest.mark.parametrize("row_dtype", [O.F32, O.BF16])
+@pytest.mark.parametrize("mode", [O.SUM, O.MEAN])
+def test_pooling_matches_torch_embedding_bag(mode, row_dtype):
+    g = np.random.default_rng(5 + mode + 10 * row_dtype)
+    vals, off = _tiny_batch(g, 60, 9, 40)
+    D = 12
+    T = O.Table(D, row_dtype=row_dtype, seed=3)
+    r = T.forward(vals, off, mode)
+    assert r["status"] == O.OK
+    # dense weight from the rows the oracle holds, indexed by unique position
+    _, W, _ = T.read_rows(r["unique"])
+    idx = torch.from_numpy(r["inverse"].astype(np.int64))
+    ref = torch.nn.functional.embedding_bag(idx, torch.from_numpy(W.astype(np.float64)),
+                                            torch.from_numpy(off[:-1]), mode=["sum", "mean"][mode])
+    np.testing.assert_allclose(r["out"], ref.numpy(), rtol=0, atol=1e-15)
+    # a bag of length one is its row, bit-exact; total mass = sum_u count_u * w_u
+    lens = np.diff(off)
+    for gi in np.nonzero(lens == 1)[0][:5]:
+        assert np.array_equal(r["out"][gi], W[r["inverse"][off[gi]]].astype(np.float64))
+    if mode == O.SUM:
+        cnt = np.bincount(r["inverse"], minlength=r["U"])
+        np.testing.assert_allclose(r["out"].sum(0), (cnt[:, None] * W.astype(np.float64)).sum(0), atol=1e-12)
+    assert np.all(r["out"][lens == 0] == 0)
+
+
+def test_padded_gather_and_mask():
+    g = np.random.default_rng(8)
+    vals, off = _tiny_batch(g, 20, 12, 25)
+    L, D = 8, 4
+    T = O.Table(D, row_dtype=O.BF16, opt=O.ADAM, seed=1)
+    r = T.forward(vals, off, O.NONE, pad_len=L)
+    _, W, _ = T.read_rows(r["unique"])
+    lens = np.diff(off)
+    for gi in range(len(lens)):
+        for t in range(L):
+            if t < lens[gi]:
+                assert r["mask"][gi, t] == 1
+                assert np.array_equal(r["out"][gi, t], W[r["inverse"][off[gi] + t]])
+            else:
+                assert r["mask"][gi, t] == 0 and np.all(r["out"][gi, t] == 0)
+
+
+# --------------------------------------------------------------------------- backward
+
+
+@pytest.mark.parametrize("mode", [O.SUM, O.MEAN])
+def test_backward_matches_torch_autograd(mode):
+    g = np.random.default_rng(21 + mode)
+    vals, off = _tiny_batch(g, 50, 10, 30)
+    D = 6
+    T = O.Table(D, seed=2)
+    r = T.forward(vals, off, mode)
+    _, W, _ = T.read_rows(r["unique"])
+    G = g.standard_normal((len(off) - 1, D)).astype(np.float32)
+    gu = O.backward(off, r["inverse"], r["U"], D, mode, 0, G)
+    Wt = torch.from_numpy(W.astype(np.float64)).requires_grad_(True)
+    out = torch.nn.functional.embedding_bag(torch.from_numpy(r["inverse"].astype(np.int64)), Wt,
+                                            torch.from_numpy(off[:-1]), mode=["sum", "mean"][mode])
+    out.backward(torch.from_numpy(G.astype(np.float64)))
+    np.testing.assert_allclose(gu, Wt.grad.numpy(), rtol=1e-13, atol=1e-13)
+
+
+def test_backward_adjoint_identity_padded_and_nan_masked():
+    g = np.random.default_rng(4)
+    vals, off = _tiny_batch(g, 30, 14, 20)
+    L, D = 10, 3
+    st, u, inv = O.dedup(vals)
+    U = len(u)
+    W = g.standard_normal((U, D))
+    G = g.standard_normal((len(off) - 1, L, D)).astype(np.float32)
+    # forward as a linear map of W (padded copy), then <fwd(W), G> = <W, bwd(G)>
+    lens = np.diff(off)
+    fw = np.zeros((len(off) - 1, L, D))
+    for gi in range(len(lens)):
+        for t in range(min(lens[gi], L)):
+            fw[gi, t] = W[inv[off[gi] + t]]
+    Gn = G.copy()
+    Gn[np.arange(L)[None, :] >= lens[:, None]] = np.nan      # masked slots
+    gu = O.backward(off, inv, U, D, O.NONE, L, Gn)
+    assert np.all(np.isfinite(gu))
+    lhs = float((fw * G.astype(np.float64)).sum())
+    rhs = float((W * gu).sum())
+    assert abs(lhs - rhs) <= 1e-12 * max(1.0, abs(lhs))
+
+
+# --------------------------------------------------------------------------- optimizer
+
+
+def test_first_step_closed_form_adagrad_and_adam():
+    D = 5
+    grads = np.array([[0.5, -2.0, 1e-3, 0.0, 7.0]], dtype=np.float32)
+    for opt in (O.ADAGRAD, O.ADAM):
+        T = O.Table(D, opt=opt, seed=1)
+        _, rows, _ = T.find_or_insert(np.array([42], dtype=np.int64))
+        _, w0, _ = T.read_rows(np.array([42], dtype=np.int64))
+        lr, eps = 0.01, 1e-8
+        T.optimizer(rows, grads, lr, eps)
+        _, w1, s = T.read_rows(np.array([42], dtype=np.int64))
+        gd = grads.astype(np.float64)
+        expect = w0.astype(np.float64) - lr * gd / (np.abs(gd) + eps)
+        np.testing.assert_allclose(w1, expect, rtol=0, atol=2e-9)
+        if opt == O.ADAGRAD:
+            np.testing.assert_array_equal(s[:, 0], (gd * gd).astype(np.float32))
+
+
+def test_adagrad_matches_torch_multi_step_lazy():
+    D, V = 4, 6
+    g = np.random.default_rng(31)
+    T = O.Table(D, opt=O.ADAGRAD, seed=7)
+    keys = np.arange(V, dtype=np.int64) * 11
+    _, rows, _ = T.find_or_insert(keys)
+    _, W0, _ = T.read_rows(keys)
+    p = torch.nn.Parameter(torch.from_numpy(W0.astype(np.float64)))
+    opt = torch.optim.Adagrad([p], lr=0.05, eps=1e-8, initial_accumulator_value=0.0)
+    for step in range(5):
+        touched = np.sort(g.choice(V, size=3, replace=False))
+        G = g.standard_normal((3, D)).astype(np.float32)
+        T.optimizer(rows[touched], G, 0.05, 1e-8)
+        dense = torch.zeros(V, D, dtype=torch.float64)
+        dense[touched] = torch.from_numpy(G.astype(np.float64))
+        p.grad = dense
+        opt.step()
+    _, W, _ = T.read_rows(keys)
+    np.testing.assert_allclose(W, p.detach().numpy(), rtol=1e-6, atol=1e-8)
+
+
+def test_adam_matches_torch_sparse_adam_multi_step_lazy():
+    D, V = 4, 7
+    g = np.random.default_rng(32)
+    T = O.Table(D, opt=O.ADAM, seed=8)
+    keys = np.arange(V, dtype=np.int64) + 1000
+    _, rows, _ = T.find_or_insert(keys)
+    _, W0, _ = T.read_rows(keys)
+    p = torch.nn.Parameter(torch.from_numpy(W0.astype(np.float64)))
+    opt = torch.optim.SparseAdam([p], lr=1e-3, betas=(0.9, 0.999), eps=1e-8)
+    untouched_before = None
+    for step in range(6):
+        touched = np.sort(g.choice(V, size=3, replace=False))
+        G = g.standard_normal((3, D)).astype(np.float32)
+        if step == 2:
+            G[0] = 0.0  # touched with a zero gradient still counts as touched
+        _, before, sb = T.read_rows(keys)
+        T.optimizer(rows[touched], G, 1e-3, 1e-8, 0.9, 0.999)
+        _, after, sa = T.read_rows(keys)
+        others = np.setdiff1d(np.arange(V), touched)
+        assert np.array_equal(before[others], after[others]) and np.array_equal(sb[others], sa[others])
+        idx = torch.from_numpy(touched.astype(np.int64))[None, :]
+        p.grad = torch.sparse_coo_tensor(idx, torch.from_numpy(G.astype(np.float64)), (V, D))
+        opt.step()
+    _, W, _ = T.read_rows(keys)
+    assert T.t == 6
+    np.testing.assert_allclose(W, p.detach().numpy(), rtol=1e-5, atol=1e-9)
+
+
+def test_step_is_forward_backward_optimizer():
+    g = np.random.default_rng(41)
+    vals, off = _tiny_batch(g, 40, 6, 25)
+    D = 8
+    G = g.standard_normal((len(off) - 1, D)).astype(np.float32)
+    A = O.Table(D, opt=O.ADAM, seed=3)
+    B = O.Table(D, opt=O.ADAM, seed=3)
+    ra = A.step(vals, off, O.MEAN, G, 1e-3)
+    rb = B.forward(vals, off, O.MEAN)
+    gu = O.backward(off, rb["inverse"], rb["U"], D, O.MEAN, 0, G)
+    B.optimizer(rb["rows"], gu.astype(np.float32), 1e-3)
+    assert ra["U"] == rb["U"] and ra["n_new"] == rb["n_new"] == rb["U"]
+    np.testing.assert_array_equal(ra["out"], rb["out"])
+    _, wa, sa = A.read_rows(rb["unique"])
+    _, wb, sb = B.read_rows(rb["unique"])
+    assert np.array_equal(wa, wb) and np.array_equal(sa, sb)
