@@ -1,0 +1,279 @@
+"""Benchmark of the sparse embedding step on one MI355X.
+
+One step = lookup_pool_fwd (dedup, IDMap find-or-insert with row init, fused
+gather + pool) + lookup_pool_bwd_opt (per-unique gradient sums fused with the
+row-sparse optimizer) over one batch of synthetic input already resident in
+HBM.  Default workload: 26 single-hot categorical features, each its own
+logical table (fused into one physical table), dim 64 fp32 rows with Adam
+state, batch 65536, table pre-populated with 90% of the vocabulary.
+
+Prints ONE JSON line (rank 0, N = 1):
+  value       = ID occurrences per second over the timed steps (whole job)
+  gbps        = algorithmic bytes per step / step time
+  roofline    = the dominant kernel's algorithmic bytes / its HIP-event time
+  cpu_baseline= the CPU oracle timed on a bounded sample of the same workload
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "embedding step IDs/sec (fwd+bwd+opt) and achieved HBM GB/s vs peak, 1 MI355X"
+HBM_PEAK_GBPS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU time of the oracle sample")
+    ap.add_argument("--unfused", action="store_true", help="lookup_pool_bwd + sparse_opt_step instead of the fused call")
+    return ap.parse_args()
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "api.hip", "rs_internal.h"):
+        with open(os.path.join(ROOT, "paper_2509_20883_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def row_bytes(w):
+    R = w.dim * (2 if w.row_dtype == 1 else 4)
+    S = w.dim * 4 * (2 if w.opt == 1 else 1)
+    return R, S
+
+
+def b_alg(w, N, G, U, Nnew):
+    """Algorithmic HBM bytes of one step (every array moved once; rows of
+    duplicate ids counted once)."""
+    R, S = row_bytes(w)
+    if w.mode == 2:
+        L = w.pad_len
+        out = G * L * R + G * L            # padded rows + mask
+        grad = N * R                       # valid positions only (lengths <= L here)
+    else:
+        out = G * w.dim * 4
+        grad = G * w.dim * 4
+    return (8 * N + 8 * (G + 1) + 4 * N + 8 * U + 8 * U + 16 * U + 8 * U + 8 * U + Nnew * (16 + R + S)
+            + 4 * N + R * U + out + grad + 4 * N + 2 * (R + S) * U)
+
+
+def kernel_bytes(w, kernel, N, G, U):
+    """Algorithmic bytes of one launch of the two dominant kernels."""
+    R, S = row_bytes(w)
+    if kernel == "pool":
+        out = G * w.pad_len * R + G * w.pad_len if w.mode == 2 else G * w.dim * 4
+        # offsets, inverse, occ_rank, row ids, seg, unique rows, output, occ_ref + chunk starts
+        return 8 * (G + 1) + 4 * N + 4 * N + 8 * U + 4 * U + R * U + out + 4 * N + 4 * (N // 32)
+    if kernel == "bwd_chunks":
+        grad = N * R if w.mode == 2 else G * w.dim * 4
+        # occ_ref, chunk starts, seg, row ids, upstream grad, row + state read-modify-write
+        return 4 * N + 4 * (N // 32) + 4 * U + 8 * U + grad + 2 * (R + S) * U
+    raise KeyError(kernel)
+
+
+def cpu_baseline(w, target_s):
+    """The oracle as it stands, single-threaded, on consecutive full batches of the
+    workload until about target_s seconds of step time have been measured."""
+    import oracle as O
+    from paper_2509_20883_amd import workloads as W
+
+    ot = O.Table(w.dim, row_dtype=w.row_dtype, opt=w.opt, lo=w.init_lo, hi=w.init_hi, seed=w.table_seed)
+    present = set()
+    ids = secs = 0.0
+    steps = 0
+    while secs < target_s and steps < 50:
+        b = W.make_batch(w, steps)
+        if w.mode == 2:
+            grad = W.make_grad(w, b, steps)
+        else:
+            grad = np.random.default_rng(steps).standard_normal((b.bags, w.dim)).astype(np.float32)
+        # pre-populated keys are materialised lazily, on first sight (untimed)
+        if w.prepop != "none":
+            uk = np.unique(b.values)
+            uk = uk[[k not in present for k in uk.tolist()]] if present else uk
+            if w.prepop == "frac90":
+                member = np.zeros(uk.size, dtype=bool)
+                fid = uk >> 40
+                for f in np.unique(fid):
+                    sel = fid == f
+                    member[sel] = W.prepop_member(w, int(f), uk[sel] & ((1 << 40) - 1))
+                ot.find_or_insert(uk[member])
+            elif w.prepop == "all":
+                ot.find_or_insert(uk)
+            present.update(uk.tolist())
+        t0 = time.perf_counter()
+        ot.step(b.values, b.offsets, w.mode, grad, w.lr, w.eps, w.beta1, w.beta2, pad_len=w.pad_len)
+        secs += time.perf_counter() - t0
+        ids += b.n
+        steps += 1
+    return {"value": ids / secs, "unit": "IDs/s", "cores": 1, "kind": "oracle",
+            "sample": f"{steps} consecutive full steps (batch {w.batch} x {w.n_features} features, "
+                      f"{int(ids)} ids), {secs:.1f} s of single-threaded step time"}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(json.dumps({"error": "single-GPU build: run with --gpus 1 (the multi-GPU path is a design only)"}))
+        sys.exit(2)
+    import torch
+
+    from paper_2509_20883_amd import recis as R
+    from paper_2509_20883_amd import workloads as W
+
+    torch.cuda.set_device(0)
+    w = W.workload(a.workload)
+    dev = torch.device("cuda", 0)
+    t_setup = time.time()
+    table = R.Table(w.dim, w.row_dtype, w.opt, w.init_lo, w.init_hi, w.table_seed, w.capacity_slots, w.max_load,
+                    w.block_rows, auto_grow=True)
+    for keys in W.prepop_keys(w):
+        table.find_or_insert(torch.from_numpy(keys).to(dev))
+    live0 = table.size()
+    nsteps = a.warmup + a.steps
+    batches, grads = [], []
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2509)
+    for s in range(nsteps):
+        b = W.make_batch(w, s)
+        batches.append((torch.from_numpy(b.values).to(dev), torch.from_numpy(b.offsets).to(dev), b.n, b.bags))
+        if w.mode == 2:
+            shape = (b.bags, w.pad_len, w.dim)
+            gdt = torch.bfloat16 if w.row_dtype == 1 else torch.float32
+        else:
+            shape, gdt = (b.bags, w.dim), torch.float32
+        grads.append(torch.randn(shape, generator=gen, device=dev, dtype=torch.float32).to(gdt))
+    ctxs = [R.Ctx() for _ in range(nsteps)]
+    maxb = max(b[3] for b in batches)
+    if w.mode == 2:
+        odt = torch.bfloat16 if w.row_dtype == 1 else torch.float32
+        out = torch.empty(maxb, w.pad_len, w.dim, dtype=odt, device=dev)
+        mask = torch.empty(maxb, w.pad_len, dtype=torch.uint8, device=dev)
+    else:
+        out = torch.empty(maxb, w.dim, dtype=torch.float32, device=dev)
+        mask = None
+    for c, (v, o, n, g) in zip(ctxs, batches):
+        c.ensure(table.workspace_bytes(n, g, w.pad_len), dev)
+    gu = None
+    if a.unfused:
+        gu = torch.empty(max(b[2] for b in batches), w.dim, dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    setup_s = time.time() - t_setup
+
+    def step(i):
+        v, o, n, g = batches[i]
+        ob = out[:g]
+        mb = mask[:g] if mask is not None else None
+        table.forward(v, o, w.mode, pad_len=w.pad_len, ctx=ctxs[i], out=ob, mask=mb)
+        if a.unfused:
+            table.backward(ctxs[i], grads[i], gu)
+            table.optimizer_step(ctxs[i], gu, w.lr, w.eps, w.beta1, w.beta2)
+        else:
+            table.backward_optimizer(ctxs[i], grads[i], w.lr, w.eps, w.beta1, w.beta2)
+
+    # untimed pass over the warm-up steps with per-kernel events: find the dominant kernel
+    names = ["dedup_local", "dedup_compact", "idmap_probe", "idmap_insert", "pool", "bwd_chunks", "bwd_straddle"]
+    if a.unfused:
+        names.append("opt")
+    prof = {k: [] for k in names}
+    for i in range(a.warmup):
+        evs = {k: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for k in names}
+        for k, (e0, e1) in evs.items():
+            table.set_kernel_events(k, e0, e1)
+        step(i)
+        torch.cuda.synchronize()
+        for k, (e0, e1) in evs.items():
+            prof[k].append(e0.elapsed_time(e1))
+    for k in names:
+        table.set_kernel_events(k, None, None)
+    dom = max(("pool", "bwd_chunks"), key=lambda k: float(np.mean(prof[k])) if prof[k] else 0.0)
+
+    # timed region: K steps, the dominant kernel bracketed by HIP events on the step's stream
+    dom_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(a.steps)]
+    torch.cuda.synchronize()
+    e_start, e_stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e_start.record()
+    for j in range(a.steps):
+        table.set_kernel_events(dom, *dom_ev[j])
+        step(a.warmup + j)
+    e_stop.record()
+    torch.cuda.synchronize()
+    table.set_kernel_events(dom, None, None)
+    total_ms = e_start.elapsed_time(e_stop)
+    table.check()
+
+    # per-step sizes (read after the timed region)
+    tot_ids = tot_bytes = dom_bytes = 0
+    Us, news = [], []
+    for j in range(a.steps):
+        i = a.warmup + j
+        sc = ctxs[i].scalars().cpu().numpy()
+        U, Nnew = int(sc[0]), int(sc[1])
+        _, _, n, g = batches[i]
+        tot_ids += n
+        tot_bytes += b_alg(w, n, g, U, Nnew)
+        dom_bytes += kernel_bytes(w, dom, n, g, U)
+        Us.append(U)
+        news.append(Nnew)
+    dom_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in dom_ev]))
+    ms_per_step = total_ms / a.steps
+    gbps = tot_bytes / (total_ms * 1e-3) / 1e9
+    achieved = dom_bytes / a.steps / (dom_ms * 1e-3) / 1e9
+
+    traffic = None
+    tpath = os.path.join(ROOT, "profiles", f"traffic_workload{a.workload}_{dom}.json")
+    if os.path.exists(tpath):
+        with open(tpath) as fh:
+            tj = json.load(fh)
+        if tj.get("kernel_source_hash") == kernel_source_hash():
+            traffic = tj.get("bytes_per_launch")
+
+    res = {
+        "metric": METRIC,
+        "value": tot_ids / (total_ms * 1e-3),
+        "unit": "IDs/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if w.row_dtype == 0 else "bf16-storage/f32-math",
+        "data": "synthetic (seeded Zipf ids, N(0,1) upstream grads; inputs resident in HBM)",
+        "config": {**W.describe(w), "live_rows_at_start": live0, "U_mean": float(np.mean(Us)),
+                   "new_per_step_mean": float(np.mean(news)), "bwd": "unfused" if a.unfused else "fused"},
+        "gbps": gbps,
+        "hbm_frac": gbps / HBM_PEAK_GBPS,
+        "bytes_alg_per_step": tot_bytes / a.steps,
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic, "kernel_ms": dom_ms,
+                     "kernel_bytes_alg": dom_bytes / a.steps},
+        "kernel_ms_warmup": {k: float(np.mean(v)) for k, v in prof.items() if v},
+        "setup_s": setup_s,
+    }
+    if not a.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, a.cpu_seconds)
+        res["cpu_baseline"]["gpu_speedup"] = res["value"] / res["cpu_baseline"]["value"]
+    table.close()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

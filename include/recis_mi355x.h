@@ -1,0 +1,249 @@
+/*
+ * recis_mi355x.h — C ABI of the MI355X (gfx950) sparse embedding step.
+ *
+ * The library implements the sparse component's per-step hot path described
+ * by RecIS (arXiv 2509.20883): the two-tier dynamic embedding store (an IDMap
+ * from feature id to an offset, and Blocks holding embedding rows together
+ * with their optimizer state; "Optimization for Memory Bound", "Moving to
+ * GPU"), its forward workflow (dedup, one IDMap lookup per id, read the row,
+ * pool it: sum / mean / padded copy — "Reduction Operations", "Gather"), and
+ * its backward workflow (per-id gradient aggregation using the offsets kept
+ * from the forward pass, then a row-sparse Adagrad / Adam update of the rows
+ * and their state in place — "Backward Update", "Optimizer", "Scatter").
+ *
+ * Conventions shared by every entry point
+ *  - All array arguments are DEVICE pointers owned by the caller, unless a
+ *    comment says "host".  The table object (IDMap + Blocks + dedup scratch)
+ *    is owned by the library.
+ *  - Every call that takes an `rs_stream` only enqueues work on that HIP
+ *    stream (a hipStream_t; NULL = the null stream) and returns without
+ *    waiting, except where a comment says it synchronizes.  Calls on one
+ *    table must be issued in stream order from one host thread: the table's
+ *    scratch and counters are shared by its calls.
+ *  - Sizes and counts that depend on the data (the number of unique ids U,
+ *    the number of inserted ids) stay on the device; buffers are sized by
+ *    the upper bound n.
+ *  - Every call returns an rs_status; no C++ exception crosses the ABI.  A
+ *    message for the last non-OK status of the calling thread is returned by
+ *    rs_last_error().  Errors the kernels detect (a reserved key, a full
+ *    table) are latched in the table and returned by the next synchronizing
+ *    call (ht_size, ht_reserve, ht_destroy, rs_table_check).
+ *  - Keys are opaque int64.  INT64_MIN (empty) and INT64_MIN+1 (tombstone)
+ *    are reserved; a key equal to either is rejected with RS_EKEY and does
+ *    not take part in the step.
+ */
+#ifndef RECIS_MI355X_H
+#define RECIS_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RS_VERSION 1
+
+typedef enum {
+  RS_OK = 0,
+  RS_EINVAL = 1, /* an argument the host can check is invalid              */
+  RS_ENOMEM = 2, /* the allocator returned NULL                            */
+  RS_EFULL = 3,  /* auto_grow is off and an insert found no room; the keys
+                    that did not fit get row -1 and are skipped downstream  */
+  RS_EKEY = 4,   /* a reserved key was in the input                        */
+  RS_EHIP = 5    /* a HIP runtime call failed                               */
+} rs_status;
+
+typedef enum { RS_POOL_SUM = 0, RS_POOL_MEAN = 1, RS_POOL_NONE = 2 } rs_pool;
+typedef enum { RS_F32 = 0, RS_BF16 = 1 } rs_dtype;
+typedef enum { RS_ADAGRAD = 0, RS_ADAM = 1 } rs_optim;
+
+typedef struct rs_table rs_table; /* opaque, library-owned */
+typedef void* rs_stream;          /* hipStream_t */
+
+/* Device-memory allocator used for every table allocation (IDMap, Blocks,
+ * scratch).  NULL as the allocator argument means hipMalloc / hipFree.  A
+ * free callback is only invoked after the table's work has completed. */
+typedef struct {
+  void* (*alloc)(size_t bytes, void* ctx);
+  void (*free)(void* ptr, void* ctx);
+  void* ctx;
+} rs_allocator;
+
+/* Table descriptor (the Embedding Engine's KV table; all ids in one table
+ * share one dim, the "merge same-dim tables" layout of Load Balancing). */
+typedef struct {
+  int32_t dim;            /* D: 8, 16, 32, 64, 128 or 256                         */
+  int32_t row_dtype;      /* rs_dtype of stored rows; optimizer state is fp32      */
+  int32_t optimizer;      /* rs_optim: fixes the state held beside each row        */
+  float init_lo, init_hi; /* new rows draw uniform values in [lo, hi]              */
+  uint64_t seed;          /* row-init seed: a new key's row is a pure function
+                             of (seed, key)                                      */
+  int64_t capacity_slots; /* IDMap slots, a power of two >= 16                     */
+  float max_load;         /* IDMap load limit, in (0, 0.9]                          */
+  int64_t block_rows;     /* rows per Blocks chunk, a power of two >= 64           */
+  int32_t auto_grow;      /* 1: rehash the IDMap (x2) and add Blocks on demand;
+                             0: inserts beyond max_load*capacity fail (RS_EFULL) */
+  int32_t reserved0;
+} rs_table_desc;
+
+/* Optimizer hyper-parameters.  Adagrad uses lr, eps; Adam uses all four.
+ * Given in double: the kernels take fp32 constants that the library derives
+ * in double (lr, eps, beta, 1 - beta, bias corrections), so 1 - beta2 does
+ * not inherit the fp32 rounding error of beta2. */
+typedef struct {
+  double lr, eps, beta1, beta2;
+} rs_opt_params;
+
+/* Forward context: the caller provides the workspace; lookup_pool_fwd fills
+ * the rest.  It holds the forward offsets the backward needs ("retained
+ * forward-pass offsets"), so the workspace, the offsets array and this struct
+ * must stay alive and unmodified until the matching lookup_pool_bwd /
+ * sparse_opt_step / lookup_pool_bwd_opt has been enqueued. */
+typedef struct {
+  /* in */
+  void* workspace;        /* device, >= lookup_workspace_bytes(n, bags, pad_len, t) bytes */
+  size_t workspace_bytes;
+  /* out: device pointers into the workspace, valid after lookup_pool_fwd */
+  int64_t* unique;   /* [n] unique keys, first-occurrence order; first U valid          */
+  int32_t* inverse;  /* [n] occurrence -> index into unique (-1 for a rejected key)     */
+  int64_t* rows;     /* [n] Blocks row of unique[u] (-1 if it could not be inserted)    */
+  int64_t* scalars;  /* [4] U, inserted this call, occurrences kept, live rows before   */
+  /* library-private (retained forward state) */
+  const int64_t* offsets;
+  const rs_table* table;
+  int64_t n, bags, pad_len;
+  int32_t mode, dim;
+  int64_t priv[16];
+} rs_ctx;
+
+/* Library version (RS_VERSION). */
+int rs_version(void);
+
+/* Message describing the calling thread's last non-OK status ("" if none). */
+const char* rs_last_error(void);
+
+/* Create a table (IDMap with desc->capacity_slots empty slots, no rows yet)
+ * on the current HIP device.  `alloc` may be NULL.  The stream is used for
+ * the initial clears, which are complete when the call returns.
+ * Errors: RS_EINVAL for a bad descriptor, RS_ENOMEM, RS_EHIP. */
+rs_status ht_create(const rs_table_desc* desc, const rs_allocator* alloc, rs_stream stream,
+                    rs_table** out);
+
+/* Synchronize the device, free everything the table owns, and return any
+ * latched device error.  NULL is accepted (RS_OK). */
+rs_status ht_destroy(rs_table* t);
+
+/* IDMap find-or-insert (the KV store inserts a feature the first time it is
+ * seen).  keys: [n] int64, duplicates allowed.  rows_out: [n] int64, the row
+ * of each key (equal keys get equal rows; -1 for a key that did not fit).
+ * A missing key gets the next free row — new rows are numbered live, live+1,
+ * ... in the first-occurrence order of the new keys — and its row is
+ * initialised: element j = fma(u_j, hi - lo, lo) in fp32 (bf16 rows: rounded
+ * to nearest even) with u_j = (splitmix64 output j+1 from state
+ * mix(key ^ mix(seed))) >> 40 times 2^-24; optimizer state = 0.
+ * n_inserted_dev: device int64 scalar receiving the number inserted (may be NULL).
+ * May synchronize the stream when the table has to grow. */
+rs_status ht_find_or_insert(rs_table* t, const int64_t* keys, int64_t n, int64_t* rows_out,
+                            int64_t* n_inserted_dev, rs_stream stream);
+
+/* IDMap find only: rows_out[i] = row of keys[i], or -1 if absent.  Inserts nothing. */
+rs_status ht_find(rs_table* t, const int64_t* keys, int64_t n, int64_t* rows_out, rs_stream stream);
+
+/* Synchronize the stream and return the number of live keys (host pointer);
+ * returns (and clears) any latched device error. */
+rs_status ht_size(rs_table* t, int64_t* live_host, rs_stream stream);
+
+/* Synchronize the stream and return (and clear) any latched device error. */
+rs_status rs_table_check(rs_table* t, rs_stream stream);
+
+/* Current IDMap capacity in slots (host pointer).  No synchronization. */
+rs_status ht_capacity(const rs_table* t, int64_t* slots_host);
+
+/* Copy every (key, row) pair out of the IDMap, in slot order, into keys[cap]
+ * and rows[cap]; n_dev (device int64) receives the live count, which may
+ * exceed cap (then only cap pairs are written). */
+rs_status ht_export(rs_table* t, int64_t* keys, int64_t* rows, int64_t cap, int64_t* n_dev,
+                    rs_stream stream);
+
+/* Read rows by row id: w_out [n, D] fp32 (bf16 rows widened exactly),
+ * state_out [n, S, D] fp32 with S = 1 (Adagrad accumulator) or 2 (Adam m, v);
+ * either may be NULL.  Rows outside [0, live) give NaN. */
+rs_status ht_read_rows(rs_table* t, const int64_t* rows, int64_t n, float* w_out, float* state_out,
+                       rs_stream stream);
+
+/* Grow the IDMap (rehash into the smallest power-of-two capacity with
+ * live_upper_bound <= max_load * capacity) and the Blocks (to hold
+ * live_upper_bound rows).  Key -> row pairs and row contents are unchanged.
+ * Synchronizes; returns (and clears) any latched device error. */
+rs_status ht_reserve(rs_table* t, int64_t live_upper_bound, rs_stream stream);
+
+/* Workspace bytes lookup_pool_fwd needs for n ids in `bags` bags (pad_len is
+ * used by RS_POOL_NONE, else ignored) on table t. */
+size_t lookup_workspace_bytes(int64_t n, int64_t bags, int64_t pad_len, const rs_table* t);
+
+/* Forward: dedup + find-or-insert + fused gather/pool.
+ * values [n] int64, offsets [bags+1] int64 (CSR: offsets[0] = 0,
+ * nondecreasing, offsets[bags] = n; bag g = feature-major f*B + b).
+ *  RS_POOL_SUM : out fp32 [bags, D], out[g] = sum of the rows of bag g
+ *  RS_POOL_MEAN: out fp32 [bags, D], the sum divided by the bag length; an
+ *                empty bag gives 0
+ *  RS_POOL_NONE: out [bags, pad_len, D] in the row dtype, out[g][t] = row of
+ *                the t-th id of bag g for t < min(len, pad_len), else 0;
+ *                mask uint8 [bags, pad_len] = (t < len).  Ids past pad_len
+ *                are looked up (and inserted) but not copied.
+ * New keys are inserted (and initialised) before the gather.
+ * validate != 0 also checks the CSR offsets on the host (copies them back:
+ * slow, synchronizing).  Errors: RS_EINVAL (sizes, workspace, mode),
+ * RS_ENOMEM / RS_EHIP; device-detected errors are latched. */
+rs_status lookup_pool_fwd(rs_table* t, const int64_t* values, const int64_t* offsets, int64_t n,
+                          int64_t bags, int32_t mode, int64_t pad_len, void* out, uint8_t* mask,
+                          rs_ctx* ctx, int32_t validate, rs_stream stream);
+
+/* Backward: per-unique gradient sums.  grad_out has the forward output's
+ * shape: fp32 [bags, D] (sum, mean) or [bags, pad_len, D] in the row dtype
+ * (none; positions with mask 0 are never read).
+ * grad_unique [n, D] fp32: row u (< U) receives
+ *   sum over occurrences i of unique u of scale(bag(i)) * grad_out[bag(i)]
+ * (scale 1 for sum, 1/len for mean; padded: grad_out[g][t] for t < pad_len). */
+rs_status lookup_pool_bwd(rs_table* t, const rs_ctx* ctx, const void* grad_out, float* grad_unique,
+                          rs_stream stream);
+
+/* Row-sparse optimizer on the U rows touched by ctx's forward (every unique
+ * key of the step, even one whose gradient is zero); untouched rows and their
+ * state are not read or written.
+ *   Adagrad: acc += g*g;  w -= lr * g / (sqrt(acc) + eps)
+ *   Adam:    t += 1 (once per call, table-global);  m = b1*m + (1-b1)*g;
+ *            v = b2*v + (1-b2)*g*g;  w -= lr * (m/(1-b1^t)) / (sqrt(v/(1-b2^t)) + eps)
+ * Arithmetic in fp32; bf16 rows are widened, updated, and rounded to nearest
+ * even.  grad_unique [n, D] fp32 as written by lookup_pool_bwd. */
+rs_status sparse_opt_step(rs_table* t, const rs_ctx* ctx, const float* grad_unique,
+                          const rs_opt_params* p, rs_stream stream);
+
+/* lookup_pool_bwd followed by sparse_opt_step in one pass: the per-unique
+ * gradient is applied to its row as soon as it is complete and never written
+ * out.  Same results as the two calls (up to fp32 summation order). */
+rs_status lookup_pool_bwd_opt(rs_table* t, const rs_ctx* ctx, const void* grad_out,
+                              const rs_opt_params* p, rs_stream stream);
+
+/* Kernel timing hook: from now on, hipEvent_t `start` / `stop` are recorded on
+ * the call's stream immediately before / after every launch of the named
+ * kernel (NULL, NULL clears it).  For measurement only. */
+typedef enum {
+  RS_K_DEDUP_LOCAL = 0,
+  RS_K_DEDUP_COMPACT = 1,
+  RS_K_IDMAP_PROBE = 2,
+  RS_K_IDMAP_INSERT = 3,
+  RS_K_POOL = 4,
+  RS_K_BWD_CHUNKS = 5,
+  RS_K_BWD_STRADDLE = 6,
+  RS_K_OPT = 7,
+  RS_K_COUNT = 8
+} rs_kernel_id;
+rs_status rs_set_kernel_events(rs_table* t, int32_t kernel, void* start_event, void* stop_event);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RECIS_MI355X_H */

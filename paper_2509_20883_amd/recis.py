@@ -1,0 +1,285 @@
+"""Python binding of librecis_mi355x.so (ctypes; argument marshalling only).
+
+Every step of the embedding path runs in the library's HIP kernels; PyTorch is
+used here only for device memory and the current HIP stream.  There is no
+fallback: if the library is not built, or no GPU is present, calls raise.
+
+Names follow the C ABI (include/recis_mi355x.h): ht_create, ht_find_or_insert,
+lookup_pool_fwd, lookup_pool_bwd, sparse_opt_step, lookup_pool_bwd_opt.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional, Tuple
+
+import torch
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "librecis_mi355x.so")
+HEADER = os.path.join(os.path.dirname(PKG), "include", "recis_mi355x.h")
+
+OK, EINVAL, ENOMEM, EFULL, EKEY, EHIP = 0, 1, 2, 3, 4, 5
+STATUS_NAMES = {0: "RS_OK", 1: "RS_EINVAL", 2: "RS_ENOMEM", 3: "RS_EFULL", 4: "RS_EKEY", 5: "RS_EHIP"}
+SUM, MEAN, NONE = 0, 1, 2
+F32, BF16 = 0, 1
+ADAGRAD, ADAM = 0, 1
+KERNELS = {"dedup_local": 0, "dedup_compact": 1, "idmap_probe": 2, "idmap_insert": 3, "pool": 4,
+           "bwd_chunks": 5, "bwd_straddle": 6, "opt": 7}
+
+
+class RecisError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+class TableDesc(C.Structure):
+    _fields_ = [("dim", C.c_int32), ("row_dtype", C.c_int32), ("optimizer", C.c_int32),
+                ("init_lo", C.c_float), ("init_hi", C.c_float), ("seed", C.c_uint64),
+                ("capacity_slots", C.c_int64), ("max_load", C.c_float), ("block_rows", C.c_int64),
+                ("auto_grow", C.c_int32), ("reserved0", C.c_int32)]
+
+
+class OptParams(C.Structure):
+    _fields_ = [("lr", C.c_double), ("eps", C.c_double), ("beta1", C.c_double), ("beta2", C.c_double)]
+
+
+class RsCtx(C.Structure):
+    _fields_ = [("workspace", C.c_void_p), ("workspace_bytes", C.c_size_t),
+                ("unique", C.c_void_p), ("inverse", C.c_void_p), ("rows", C.c_void_p),
+                ("scalars", C.c_void_p), ("offsets", C.c_void_p), ("table", C.c_void_p),
+                ("n", C.c_int64), ("bags", C.c_int64), ("pad_len", C.c_int64),
+                ("mode", C.c_int32), ("dim", C.c_int32), ("priv", C.c_int64 * 16)]
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RecisError(EHIP, f"{LIB_PATH} is not built; run paper_2509_20883_amd/build.py")
+    L = C.CDLL(LIB_PATH)
+    p, i32, i64 = C.c_void_p, C.c_int32, C.c_int64
+    sig = {
+        "rs_version": (C.c_int, []),
+        "rs_last_error": (C.c_char_p, []),
+        "ht_create": (C.c_int, [C.POINTER(TableDesc), p, p, C.POINTER(p)]),
+        "ht_destroy": (C.c_int, [p]),
+        "ht_find_or_insert": (C.c_int, [p, p, i64, p, p, p]),
+        "ht_find": (C.c_int, [p, p, i64, p, p]),
+        "ht_size": (C.c_int, [p, C.POINTER(i64), p]),
+        "rs_table_check": (C.c_int, [p, p]),
+        "ht_capacity": (C.c_int, [p, C.POINTER(i64)]),
+        "ht_export": (C.c_int, [p, p, p, i64, p, p]),
+        "ht_read_rows": (C.c_int, [p, p, i64, p, p, p]),
+        "ht_reserve": (C.c_int, [p, i64, p]),
+        "lookup_workspace_bytes": (C.c_size_t, [i64, i64, i64, p]),
+        "lookup_pool_fwd": (C.c_int, [p, p, p, i64, i64, i32, i64, p, p, C.POINTER(RsCtx), i32, p]),
+        "lookup_pool_bwd": (C.c_int, [p, C.POINTER(RsCtx), p, p, p]),
+        "sparse_opt_step": (C.c_int, [p, C.POINTER(RsCtx), p, C.POINTER(OptParams), p]),
+        "lookup_pool_bwd_opt": (C.c_int, [p, C.POINTER(RsCtx), p, C.POINTER(OptParams), p]),
+        "rs_set_kernel_events": (C.c_int, [p, i32, p, p]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = L
+    return L
+
+
+def _check(st: int):
+    if st != OK:
+        raise RecisError(st, lib().rs_last_error().decode())
+
+
+def _stream() -> C.c_void_p:
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _dev(t: torch.Tensor, dtype: torch.dtype) -> torch.Tensor:
+    if not t.is_cuda:
+        raise RecisError(EINVAL, "tensors must be on the GPU")
+    if t.dtype != dtype:
+        raise RecisError(EINVAL, f"expected {dtype}, got {t.dtype}")
+    return t.contiguous()
+
+
+class Ctx:
+    """Forward context: the caller-owned workspace plus the rs_ctx struct."""
+
+    def __init__(self):
+        self.ws: Optional[torch.Tensor] = None
+        self.c = RsCtx()
+        self.keep = ()
+
+    def ensure(self, nbytes: int, device):
+        if self.ws is None or self.ws.numel() < nbytes:
+            self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        self.c.workspace = self.ws.data_ptr()
+        self.c.workspace_bytes = self.ws.numel()
+
+    def _view(self, ptr: int, count: int, dtype: torch.dtype) -> torch.Tensor:
+        off = ptr - self.ws.data_ptr()
+        es = torch.empty(0, dtype=dtype).element_size()
+        return self.ws[off:off + count * es].view(dtype)
+
+    def scalars(self) -> torch.Tensor:
+        """Device int64[4]: U, inserted, occurrences kept, live rows before."""
+        return self._view(self.c.scalars, 4, torch.int64)
+
+    def unique(self, U: int) -> torch.Tensor:
+        return self._view(self.c.unique, U, torch.int64)
+
+    def inverse(self) -> torch.Tensor:
+        return self._view(self.c.inverse, self.c.n, torch.int32)
+
+    def rows(self, U: int) -> torch.Tensor:
+        return self._view(self.c.rows, U, torch.int64)
+
+
+class Table:
+    """A dynamic embedding table (IDMap + Blocks) on the current GPU."""
+
+    def __init__(self, dim: int, row_dtype: int = F32, optimizer: int = ADAGRAD, init_lo: float = -0.01,
+                 init_hi: float = 0.01, seed: int = 0, capacity_slots: int = 1 << 17, max_load: float = 0.75,
+                 block_rows: int = 1 << 16, auto_grow: bool = True):
+        d = TableDesc(dim, row_dtype, optimizer, init_lo, init_hi, seed & 0xFFFFFFFFFFFFFFFF, capacity_slots,
+                      max_load, block_rows, int(bool(auto_grow)), 0)
+        h = C.c_void_p()
+        _check(lib().ht_create(C.byref(d), None, _stream(), C.byref(h)))
+        self.h = h
+        self.dim, self.row_dtype, self.optimizer = dim, row_dtype, optimizer
+        self.nstate = 2 if optimizer == ADAM else 1
+        self.device = torch.device("cuda", torch.cuda.current_device())
+
+    def close(self):
+        if getattr(self, "h", None) and self.h.value:
+            st = lib().ht_destroy(self.h)
+            self.h = C.c_void_p()
+            _check(st)
+
+    def __del__(self):
+        try:
+            if getattr(self, "h", None) and self.h.value and _lib is not None:
+                _lib.ht_destroy(self.h)
+                self.h = C.c_void_p()
+        except Exception:
+            pass
+
+    # ---------------------------------------------------------------- IDMap
+    def find_or_insert(self, keys: torch.Tensor) -> Tuple[torch.Tensor, torch.Tensor]:
+        k = _dev(keys, torch.int64)
+        rows = torch.empty_like(k)
+        nins = torch.zeros(1, dtype=torch.int64, device=k.device)
+        _check(lib().ht_find_or_insert(self.h, _ptr(k), k.numel(), _ptr(rows), _ptr(nins), _stream()))
+        return rows, nins
+
+    def find(self, keys: torch.Tensor) -> torch.Tensor:
+        k = _dev(keys, torch.int64)
+        rows = torch.empty_like(k)
+        _check(lib().ht_find(self.h, _ptr(k), k.numel(), _ptr(rows), _stream()))
+        return rows
+
+    def size(self) -> int:
+        v = C.c_int64()
+        _check(lib().ht_size(self.h, C.byref(v), _stream()))
+        return v.value
+
+    def check(self):
+        _check(lib().rs_table_check(self.h, _stream()))
+
+    def capacity(self) -> int:
+        v = C.c_int64()
+        _check(lib().ht_capacity(self.h, C.byref(v)))
+        return v.value
+
+    def reserve(self, live_upper_bound: int):
+        _check(lib().ht_reserve(self.h, live_upper_bound, _stream()))
+
+    def export(self) -> Tuple[torch.Tensor, torch.Tensor]:
+        live = self.size()
+        keys = torch.empty(max(live, 1), dtype=torch.int64, device=self.device)
+        rows = torch.empty(max(live, 1), dtype=torch.int64, device=self.device)
+        nd = torch.zeros(1, dtype=torch.int64, device=self.device)
+        _check(lib().ht_export(self.h, _ptr(keys), _ptr(rows), live, _ptr(nd), _stream()))
+        return keys[:live], rows[:live]
+
+    def read_rows(self, rows: torch.Tensor) -> Tuple[torch.Tensor, torch.Tensor]:
+        r = _dev(rows, torch.int64)
+        w = torch.empty(r.numel(), self.dim, dtype=torch.float32, device=r.device)
+        s = torch.empty(r.numel(), self.nstate, self.dim, dtype=torch.float32, device=r.device)
+        _check(lib().ht_read_rows(self.h, _ptr(r), r.numel(), _ptr(w), _ptr(s), _stream()))
+        return w, s
+
+    # ---------------------------------------------------------------- step
+    def workspace_bytes(self, n: int, bags: int, pad_len: int = 0) -> int:
+        return int(lib().lookup_workspace_bytes(n, bags, pad_len, self.h))
+
+    def forward(self, values: torch.Tensor, offsets: torch.Tensor, mode: int, pad_len: int = 0,
+                ctx: Optional[Ctx] = None, out: Optional[torch.Tensor] = None,
+                mask: Optional[torch.Tensor] = None, validate: bool = False):
+        v = _dev(values, torch.int64)
+        o = _dev(offsets, torch.int64)
+        n, bags = v.numel(), o.numel() - 1
+        ctx = ctx or Ctx()
+        ctx.ensure(self.workspace_bytes(n, bags, pad_len), v.device)
+        if mode == NONE:
+            odt = torch.bfloat16 if self.row_dtype == BF16 else torch.float32
+            if out is None:
+                out = torch.empty(bags, pad_len, self.dim, dtype=odt, device=v.device)
+            if mask is None:
+                mask = torch.empty(bags, pad_len, dtype=torch.uint8, device=v.device)
+        elif out is None:
+            out = torch.empty(bags, self.dim, dtype=torch.float32, device=v.device)
+        ctx.keep = (v, o)
+        _check(lib().lookup_pool_fwd(self.h, _ptr(v), _ptr(o), n, bags, mode, pad_len, _ptr(out), _ptr(mask),
+                                     C.byref(ctx.c), int(validate), _stream()))
+        return out, mask, ctx
+
+    def _grad(self, ctx: Ctx, grad_out: torch.Tensor) -> torch.Tensor:
+        c = ctx.c
+        if c.mode == NONE:
+            want, dt = c.bags * c.pad_len * self.dim, (torch.bfloat16 if self.row_dtype == BF16 else torch.float32)
+        else:
+            want, dt = c.bags * self.dim, torch.float32
+        if grad_out.numel() != want or grad_out.dtype != dt or not grad_out.is_cuda:
+            raise RecisError(EINVAL, f"grad_out must be a GPU {dt} tensor with {want} elements")
+        return grad_out.contiguous()
+
+    def backward(self, ctx: Ctx, grad_out: torch.Tensor, grad_unique: Optional[torch.Tensor] = None):
+        g = self._grad(ctx, grad_out)
+        if grad_unique is None:
+            grad_unique = torch.empty(max(ctx.c.n, 1), self.dim, dtype=torch.float32, device=g.device)
+        _check(lib().lookup_pool_bwd(self.h, C.byref(ctx.c), _ptr(g), _ptr(grad_unique), _stream()))
+        return grad_unique
+
+    def optimizer_step(self, ctx: Ctx, grad_unique: torch.Tensor, lr: float, eps: float = 1e-8,
+                       beta1: float = 0.9, beta2: float = 0.999):
+        p = OptParams(lr, eps, beta1, beta2)
+        _check(lib().sparse_opt_step(self.h, C.byref(ctx.c), _ptr(grad_unique), C.byref(p), _stream()))
+
+    def backward_optimizer(self, ctx: Ctx, grad_out: torch.Tensor, lr: float, eps: float = 1e-8,
+                           beta1: float = 0.9, beta2: float = 0.999):
+        g = self._grad(ctx, grad_out)
+        p = OptParams(lr, eps, beta1, beta2)
+        _check(lib().lookup_pool_bwd_opt(self.h, C.byref(ctx.c), _ptr(g), C.byref(p), _stream()))
+
+    def set_kernel_events(self, kernel: str, start, stop):
+        """Record torch.cuda.Event `start` / `stop` around every launch of `kernel`."""
+        if start is not None:
+            # torch creates the underlying hipEvent_t on first record()
+            start.record()
+            stop.record()
+        s = None if start is None else C.c_void_p(start.cuda_event)
+        e = None if stop is None else C.c_void_p(stop.cuda_event)
+        _check(lib().rs_set_kernel_events(self.h, KERNELS[kernel], s, e))

@@ -1,0 +1,282 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle, on the GPU.
+
+Sizes: every workload at its reduced size (batch / 32, vocabulary / 100) spans
+many tiles and has ragged tails; the single-feature workload runs at full size.
+Full-size sampled checks of the benchmarked workload are in test_gpu_fullsize.py.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2509_20883_amd import recis as R
+from paper_2509_20883_amd import workloads as W
+from tests import parity as P
+
+pytestmark = pytest.mark.gpu
+
+I64_MIN = np.iinfo(np.int64).min
+I64_MAX = np.iinfo(np.int64).max
+
+
+def _log(*a):
+    print(*a, flush=True)
+
+
+# --------------------------------------------------------------------------- IDMap
+
+
+def test_find_or_insert_matches_oracle():
+    _log("find_or_insert small")
+    w = W.workload(0)
+    gt, ot = P.gpu_table(w), P.oracle_table(w)
+    g = np.random.default_rng(1)
+    for rep in range(3):
+        keys = (g.zipf(1.2, size=5000) % 3000).astype(np.int64) * 7919 - 100000 * rep
+        rows, nins = gt.find_or_insert(P.to_dev(keys))
+        st, rref, nref = ot.find_or_insert(keys)
+        assert st == O.OK
+        assert np.array_equal(rows.cpu().numpy(), rref)
+        assert int(nins.item()) == nref
+    assert gt.size() == ot.size()
+    ek, er = gt.export()
+    rk, rr = ot.export()
+    o1, o2 = np.argsort(ek.cpu().numpy()), np.argsort(rk)
+    assert np.array_equal(ek.cpu().numpy()[o1], rk[o2])
+    assert np.array_equal(er.cpu().numpy()[o1], rr[o2])
+    # rows hold their initial values bit-exactly, state zero
+    keys = rk[:500]
+    wg, sg = gt.read_rows(gt.find(P.to_dev(keys)))
+    _, wr, sr = ot.read_rows(keys)
+    assert np.array_equal(wg.cpu().numpy(), wr) and np.all(sg.cpu().numpy() == 0)
+    # re-inserting inserts nothing
+    _, nins = gt.find_or_insert(P.to_dev(keys))
+    assert int(nins.item()) == 0
+    gt.close()
+
+
+@pytest.mark.parametrize("dim,dtype,opt", [(8, O.BF16, O.ADAGRAD), (32, O.BF16, O.ADAM), (256, O.F32, O.ADAM),
+                                           (128, O.BF16, O.ADAM), (64, O.F32, O.ADAGRAD)])
+def test_row_init_bit_exact_all_layouts(dim, dtype, opt):
+    _log("row init", dim, dtype, opt)
+    gt = R.Table(dim, dtype, opt, -0.05, 0.03, seed=12345, capacity_slots=1 << 12, block_rows=64)
+    ot = O.Table(dim, row_dtype=dtype, opt=opt, lo=-0.05, hi=0.03, seed=12345)
+    keys = np.array([0, -1, 1, I64_MAX, I64_MIN + 2, 2**40 + 5, -(2**62)] + list(range(100, 400)), dtype=np.int64)
+    rows, _ = gt.find_or_insert(P.to_dev(keys))
+    _, rref, _ = ot.find_or_insert(keys)
+    assert np.array_equal(rows.cpu().numpy(), rref)
+    wg, sg = gt.read_rows(rows)
+    _, wr, sr = ot.read_rows(keys)
+    assert np.array_equal(wg.cpu().numpy(), wr)
+    assert np.array_equal(sg.cpu().numpy(), sr)
+    gt.close()
+
+
+def test_reserved_key_rejected():
+    _log("reserved key")
+    gt = R.Table(16)
+    keys = P.to_dev(np.array([1, I64_MIN, 2, I64_MIN + 1, 1], dtype=np.int64))
+    rows, _ = gt.find_or_insert(keys)
+    with pytest.raises(R.RecisError) as e:
+        gt.check()
+    assert e.value.status == R.EKEY
+    r = rows.cpu().numpy()
+    assert r[1] == -1 and r[3] == -1 and r[0] == r[4] and r[0] != r[2]
+    assert gt.size() == 2
+    gt.close()
+
+
+def test_bounded_table_efull_matches_oracle():
+    _log("efull")
+    gt = R.Table(16, capacity_slots=16, max_load=0.5, auto_grow=False, block_rows=64)
+    ot = O.Table(16, max_live=8)
+    keys = np.arange(20, dtype=np.int64) * 3 + 1
+    keys = np.concatenate([keys[:5], keys[:5], keys[5:]])
+    rows, nins = gt.find_or_insert(P.to_dev(keys))
+    st, rref, nref = ot.find_or_insert(keys)
+    assert st == O.EFULL
+    with pytest.raises(R.RecisError) as e:
+        gt.check()
+    assert e.value.status == R.EFULL
+    assert np.array_equal(rows.cpu().numpy(), rref)
+    assert int(nins.item()) == nref == 8
+    gt.close()
+
+
+def test_rehash_keeps_contents():
+    _log("rehash")
+    w = W.workload(0)
+    gt = P.gpu_table(w, capacity_slots=1 << 10)
+    g = np.random.default_rng(5)
+    keys = np.unique(g.integers(-2**62, 2**62, size=700, dtype=np.int64))
+    rows, _ = gt.find_or_insert(P.to_dev(keys))
+    w_before, _ = gt.read_rows(rows)
+    ek0, er0 = [x.cpu().numpy() for x in gt.export()]
+    cap0 = gt.capacity()
+    gt.reserve(50_000)
+    assert gt.capacity() > cap0
+    ek1, er1 = [x.cpu().numpy() for x in gt.export()]
+    o0, o1 = np.argsort(ek0), np.argsort(ek1)
+    assert np.array_equal(ek0[o0], ek1[o1]) and np.array_equal(er0[o0], er1[o1])
+    assert np.array_equal(gt.find(P.to_dev(keys)).cpu().numpy(), rows.cpu().numpy())
+    w_after, _ = gt.read_rows(rows)
+    assert torch.equal(w_before, w_after)
+    # auto-grow through many inserts from a tiny table
+    more = np.unique(g.integers(-2**62, 2**62, size=20000, dtype=np.int64))
+    r2, _ = gt.find_or_insert(P.to_dev(more))
+    assert gt.size() == len(np.union1d(keys, more))
+    assert np.array_equal(gt.find(P.to_dev(more)).cpu().numpy(), r2.cpu().numpy())
+    gt.close()
+
+
+# --------------------------------------------------------------------------- step parity
+
+
+@pytest.mark.parametrize("k", [0, 1, 2, 3, 4])
+def test_step_parity_workloads(k):
+    w = W.workload(k, mini=(k != 0))
+    _log("step parity", w.name, "mini" if w.mini else "full")
+    gt, ot = P.gpu_table(w), P.oracle_table(w)
+    P.prepopulate(w, gt, ot)
+    steps = 3 if k in (0, 4) else 2
+    for step in range(steps):
+        b = W.make_batch(w, step)
+        grad = W.make_grad(w, b, step, nan_in_masked=(w.mode == O.NONE))
+        U, nn = P.run_step_parity(w, gt, ot, b, grad, step)
+        _log(f"  step {step}: N={b.n} bags={b.bags} U={U} new={nn}")
+    gt.check()
+    assert gt.size() == ot.size()
+    gt.close()
+
+
+def _fused_vs_unfused(w, b, grad):
+    ga, gb = P.gpu_table(w), P.gpu_table(w)
+    P.prepopulate(w, ga)
+    P.prepopulate(w, gb)
+    pad = w.pad_len if w.mode == O.NONE else 0
+    gdev = P.to_dev(grad)
+    if w.mode == O.NONE and w.row_dtype == O.BF16:
+        gdev = gdev.to(torch.bfloat16)
+    _, _, ca = ga.forward(P.to_dev(b.values), P.to_dev(b.offsets), w.mode, pad_len=pad)
+    _, _, cb = gb.forward(P.to_dev(b.values), P.to_dev(b.offsets), w.mode, pad_len=pad)
+    U = int(ca.scalars()[0].item())
+    w0, s0 = [x.cpu().numpy() for x in ga.read_rows(ca.rows(U))]
+    gu = ga.backward(ca, gdev)
+    ga.optimizer_step(ca, gu, w.lr, w.eps, w.beta1, w.beta2)
+    gb.backward_optimizer(cb, gdev, w.lr, w.eps, w.beta1, w.beta2)
+    wa, sa = [x.cpu().numpy() for x in ga.read_rows(ca.rows(U))]
+    wb, sb = [x.cpu().numpy() for x in gb.read_rows(cb.rows(U))]
+    ga.check()
+    gb.check()
+    # the two paths may sum a key's gradient in a different order: allow the
+    # gradient tolerance, propagated through the update
+    inv = ca.inverse().cpu().numpy()
+    gfin = np.where(np.isfinite(grad), grad, 0).astype(np.float32)
+    gabs = O.backward(b.offsets, inv, U, w.dim, w.mode, pad, np.abs(gfin))
+    bounds = P.opt_bounds(w.opt, w.row_dtype, w0, s0, gu[:U].cpu().numpy(), 2e-5 * gabs, w.lr, w.eps,
+                          w.beta1, w.beta2, 1, wa)
+    ga.close()
+    gb.close()
+    return wa, sa, wb, sb, bounds
+
+
+@pytest.mark.parametrize("k", [0, 2, 3])
+def test_fused_bwd_opt_equals_two_calls(k):
+    w = W.workload(k, mini=(k != 0))
+    _log("fused vs unfused", w.name)
+    b = W.make_batch(w, 0)
+    grad = W.make_grad(w, b, 0)
+    wa, sa, wb, sb, bounds = _fused_vs_unfused(w, b, grad)
+    P.assert_opt_close(wb, sb, wa, sa, bounds, what="fused vs unfused")
+
+
+# --------------------------------------------------------------------------- edge cases
+
+
+def _custom_batch_parity(w, values, offsets, steps=1, seed=0):
+    gt, ot = P.gpu_table(w), P.oracle_table(w)
+    b = W.Batch(values=np.asarray(values, dtype=np.int64), offsets=np.asarray(offsets, dtype=np.int64),
+                n_features=1, batch=len(offsets) - 1)
+    g = np.random.default_rng(seed)
+    for step in range(steps):
+        if w.mode == O.NONE:
+            grad = W.bf16_representable(g.standard_normal((b.bags, w.pad_len, w.dim)).astype(np.float32))
+        else:
+            grad = g.standard_normal((b.bags, w.dim)).astype(np.float32)
+        P.run_step_parity(w, gt, ot, b, grad, step)
+    gt.check()
+    gt.close()
+
+
+def test_empty_batch_and_empty_bags():
+    _log("empty")
+    w = W.workload(0)
+    _custom_batch_parity(w, [], [0, 0, 0, 0])
+    _custom_batch_parity(w, [5, 6, 5], [0, 0, 2, 2, 3, 3])
+    w2 = W.workload(2, mini=True)
+    _custom_batch_parity(w2, [5, 6, 5, 9], [0, 0, 3, 3, 4])
+
+
+def test_hot_key_spanning_many_chunks():
+    _log("hot key")
+    w = W.workload(0)
+    n = 200_000
+    vals = np.full(n, 42, dtype=np.int64)
+    vals[::1000] = np.arange(200) + 1000           # a few other keys between the hot ones
+    off = np.concatenate([np.arange(0, n, 7), [n]]).astype(np.int64)
+    _custom_batch_parity(w, vals, off, steps=2)
+
+
+def test_all_distinct_and_extreme_keys():
+    _log("distinct / extreme keys")
+    w = W.workload(0)
+    g = np.random.default_rng(9)
+    vals = np.unique(g.integers(-2**63 + 2, 2**63 - 1, size=30000, dtype=np.int64))
+    g.shuffle(vals)
+    vals = np.concatenate([[0, -1, I64_MAX, I64_MIN + 2], vals])
+    off = np.concatenate([np.arange(0, len(vals), 3), [len(vals)]]).astype(np.int64)
+    _custom_batch_parity(w, vals, off)
+
+
+def test_padded_bag_longer_than_pad_len():
+    _log("padded truncation")
+    w = W.workload(3, mini=True)
+    g = np.random.default_rng(4)
+    lens = np.array([0, 1, w.pad_len, w.pad_len + 37, 5, 2 * w.pad_len])
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    vals = (g.zipf(1.2, size=int(off[-1])) % 500).astype(np.int64)
+    _custom_batch_parity(w, vals, off, steps=2)
+
+
+def test_integer_outputs_deterministic():
+    _log("determinism")
+    w = W.workload(2, mini=True)
+    b = W.make_batch(w, 0)
+    res = []
+    for rep in range(2):
+        gt = P.gpu_table(w)
+        _, _, ctx = gt.forward(P.to_dev(b.values), P.to_dev(b.offsets), w.mode)
+        U = int(ctx.scalars()[0].item())
+        res.append((ctx.unique(U).cpu().numpy().copy(), ctx.inverse().cpu().numpy().copy(),
+                    ctx.rows(U).cpu().numpy().copy()))
+        gt.close()
+    for a, b2 in zip(res[0], res[1]):
+        assert np.array_equal(a, b2)
+
+
+def test_resize_during_growing_run_matches_oracle():
+    _log("growing run with resizes")
+    w = W.workload(4, mini=True)
+    w.capacity_slots = 1 << 16            # rehashes while pre-populating ...
+    w.fresh_per_step = 100_000            # ... and again between the steps
+    gt, ot = P.gpu_table(w), P.oracle_table(w)
+    P.prepopulate(w, gt, ot)
+    caps = [gt.capacity()]
+    assert caps[0] > 1 << 16
+    for step in range(3):
+        b = W.make_batch(w, step)
+        grad = W.make_grad(w, b, step)
+        P.run_step_parity(w, gt, ot, b, grad, step)
+        caps.append(gt.capacity())
+    assert caps[-1] > caps[0]
+    gt.close()
