@@ -41,12 +41,32 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU time of the oracle sample")
     ap.add_argument("--unfused", action="store_true", help="lookup_pool_bwd + sparse_opt_step instead of the fused call")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy 5 times (scales HBM byte counters)")
     return ap.parse_args()
+
+
+def copy_calibration():
+    """A plain copy kernel of known size: 1 GiB read + 1 GiB written per launch."""
+    import torch
+
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 5
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "ms": ms, "GBps": 2 * n / (ms * 1e-3) / 1e9}))
 
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("kernels.hip", "api.hip", "rs_internal.h"):
+    for f in ("dedup_idmap.hip", "pool.hip", "backward.hip", "api.hip", "rs_internal.h", "device_common.h"):
         with open(os.path.join(ROOT, "paper_2509_20883_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -73,17 +93,30 @@ def b_alg(w, N, G, U, Nnew):
             + 4 * N + R * U + out + grad + 4 * N + 2 * (R + S) * U)
 
 
-def kernel_bytes(w, kernel, N, G, U):
-    """Algorithmic bytes of one launch of the two dominant kernels."""
+def key_stats(values: np.ndarray, long_threshold: int = 32):
+    """Host-side split of a batch into short keys (<= 32 occurrences) and hot keys."""
+    _, cnt = np.unique(values, return_counts=True)
+    hot = cnt > long_threshold
+    return {"U": int(cnt.size), "U_short": int((~hot).sum()), "N_short": int(cnt[~hot].sum()),
+            "U_long": int(hot.sum()), "N_long": int(cnt[hot].sum())}
+
+
+def kernel_bytes(w, kernel, N, G, ks):
+    """Algorithmic bytes of one launch of the two largest kernels (each array
+    element the kernel must touch, counted once; rows of duplicate ids once)."""
     R, S = row_bytes(w)
+    U = ks["U"]
     if kernel == "pool":
         out = G * w.pad_len * R + G * w.pad_len if w.mode == 2 else G * w.dim * 4
-        # offsets, inverse, occ_rank, row ids, seg, unique rows, output, occ_ref + chunk starts
-        return 8 * (G + 1) + 4 * N + 4 * N + 8 * U + 4 * U + R * U + out + 4 * N + 4 * (N // 32)
-    if kernel == "bwd_chunks":
-        grad = N * R if w.mode == 2 else G * w.dim * 4
-        # occ_ref, chunk starts, seg, row ids, upstream grad, row + state read-modify-write
-        return 4 * N + 4 * (N // 32) + 4 * U + 8 * U + grad + 2 * (R + S) * U
+        # offsets, inverse, occurrence ranks, row ids, segment descriptors,
+        # unique rows, output, occurrence list
+        return 8 * (G + 1) + 4 * N + 4 * N + 8 * U + 16 * U + R * U + out + 4 * N
+    if kernel == "bwd_short":
+        Us, Ns = ks["U_short"], ks["N_short"]
+        gr = R if w.mode == 2 else w.dim * 4
+        # segment descriptors, row ids, occurrence list, one upstream gradient
+        # row per occurrence, row + state read-modify-write
+        return 16 * U + 8 * Us + 4 * Ns + gr * Ns + 2 * (R + S) * Us
     raise KeyError(kernel)
 
 
@@ -129,6 +162,9 @@ def cpu_baseline(w, target_s):
 
 def main():
     a = parse()
+    if a.copy_calibration:
+        copy_calibration()
+        return
     if a.gpus != 1:
         print(json.dumps({"error": "single-GPU build: run with --gpus 1 (the multi-GPU path is a design only)"}))
         sys.exit(2)
@@ -150,8 +186,10 @@ def main():
     batches, grads = [], []
     gen = torch.Generator(device=dev)
     gen.manual_seed(2509)
+    host_values = []
     for s in range(nsteps):
         b = W.make_batch(w, s)
+        host_values.append(b.values)
         batches.append((torch.from_numpy(b.values).to(dev), torch.from_numpy(b.offsets).to(dev), b.n, b.bags))
         if w.mode == 2:
             shape = (b.bags, w.pad_len, w.dim)
@@ -188,7 +226,7 @@ def main():
             table.backward_optimizer(ctxs[i], grads[i], w.lr, w.eps, w.beta1, w.beta2)
 
     # untimed pass over the warm-up steps with per-kernel events: find the dominant kernel
-    names = ["dedup_local", "dedup_compact", "idmap_probe", "idmap_insert", "pool", "bwd_chunks", "bwd_straddle"]
+    names = ["dedup_local", "rank_probe", "compact_insert", "init_rows", "pool", "bwd_short", "bwd_long"]
     if a.unfused:
         names.append("opt")
     prof = {k: [] for k in names}
@@ -202,7 +240,7 @@ def main():
             prof[k].append(e0.elapsed_time(e1))
     for k in names:
         table.set_kernel_events(k, None, None)
-    dom = max(("pool", "bwd_chunks"), key=lambda k: float(np.mean(prof[k])) if prof[k] else 0.0)
+    dom = max(("pool", "bwd_short"), key=lambda k: float(np.mean(prof[k])) if prof[k] else 0.0)
 
     # timed region: K steps, the dominant kernel bracketed by HIP events on the step's stream
     dom_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(a.steps)]
@@ -228,7 +266,7 @@ def main():
         _, _, n, g = batches[i]
         tot_ids += n
         tot_bytes += b_alg(w, n, g, U, Nnew)
-        dom_bytes += kernel_bytes(w, dom, n, g, U)
+        dom_bytes += kernel_bytes(w, dom, n, g, key_stats(host_values[i]))
         Us.append(U)
         news.append(Nnew)
     dom_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in dom_ev]))

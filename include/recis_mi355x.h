@@ -61,9 +61,12 @@ typedef enum { RS_ADAGRAD = 0, RS_ADAM = 1 } rs_optim;
 typedef struct rs_table rs_table; /* opaque, library-owned */
 typedef void* rs_stream;          /* hipStream_t */
 
-/* Device-memory allocator used for every table allocation (IDMap, Blocks,
- * scratch).  NULL as the allocator argument means hipMalloc / hipFree.  A
- * free callback is only invoked after the table's work has completed. */
+/* Device-memory allocator used for the table's IDMap, dedup scratch and
+ * internal workspace.  NULL as the allocator argument means hipMalloc /
+ * hipFree.  A free callback is only invoked after the table's work has
+ * completed.  The Blocks (rows + optimizer state) are physical chunks
+ * (hipMemCreate) mapped into one reserved virtual range, so that rows never
+ * move when the table grows; they do not go through the allocator. */
 typedef struct {
   void* (*alloc)(size_t bytes, void* ctx);
   void (*free)(void* ptr, void* ctx);
@@ -81,7 +84,8 @@ typedef struct {
                              of (seed, key)                                      */
   int64_t capacity_slots; /* IDMap slots, a power of two >= 16                     */
   float max_load;         /* IDMap load limit, in (0, 0.9]                          */
-  int64_t block_rows;     /* rows per Blocks chunk, a power of two >= 64           */
+  int64_t block_rows;     /* rows per Blocks chunk (the unit of growth), a power
+                             of two >= 64                                        */
   int32_t auto_grow;      /* 1: rehash the IDMap (x2) and add Blocks on demand;
                              0: inserts beyond max_load*capacity fail (RS_EFULL) */
   int32_t reserved0;
@@ -230,15 +234,16 @@ rs_status lookup_pool_bwd_opt(rs_table* t, const rs_ctx* ctx, const void* grad_o
  * the call's stream immediately before / after every launch of the named
  * kernel (NULL, NULL clears it).  For measurement only. */
 typedef enum {
-  RS_K_DEDUP_LOCAL = 0,
-  RS_K_DEDUP_COMPACT = 1,
-  RS_K_IDMAP_PROBE = 2,
-  RS_K_IDMAP_INSERT = 3,
-  RS_K_POOL = 4,
-  RS_K_BWD_CHUNKS = 5,
-  RS_K_BWD_STRADDLE = 6,
-  RS_K_OPT = 7,
-  RS_K_COUNT = 8
+  RS_K_DEDUP_LOCAL = 0,    /* tile dedup + scratch set                          */
+  RS_K_RANK_PROBE = 1,     /* first occurrences + IDMap probe                   */
+  RS_K_COMPACT_INSERT = 2, /* unique ids, segments, rows, IDMap inserts         */
+  RS_K_INIT_ROWS = 3,      /* initial rows of inserted keys                     */
+  RS_K_POOL = 4,           /* gather + pool (and the occurrence list)           */
+  RS_K_BWD_SHORT = 5,      /* per-key gradient sum (+ optimizer), short keys    */
+  RS_K_BWD_LONG = 6,       /* hot keys: unit partial sums + finish (two kernels) */
+  RS_K_OPT = 7,            /* optimizer from grad_unique (two-call path)        */
+  RS_K_OCC = 8,            /* per-occurrence rows, list positions, inverse      */
+  RS_K_COUNT = 9
 } rs_kernel_id;
 rs_status rs_set_kernel_events(rs_table* t, int32_t kernel, void* start_event, void* stop_event);
 

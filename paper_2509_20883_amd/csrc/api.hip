@@ -43,23 +43,19 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
 
-int ilog2(int64_t x) {
-  int r = 0;
-  while ((int64_t(1) << r) < x) ++r;
-  return r;
-}
-
 // Workspace layout of one forward: every array sized by the upper bound n.
 struct Layout {
-  size_t slot_of, occ_rank, inverse, unique, uslot, ucount, seg, rows, isnew, occ_ref, chunk_u, bsum, scal,
-      gpart, total;
+  size_t slot_of, occ_rank, inverse, occ_row, occ_pos, unique, useg, rows, new_list, occ_ref, long_u, long_start,
+      units, bsum, scal, gpart, total;
+  int64_t ntiles;
 };
 
 Layout make_layout(int64_t n, int dim) {
   const size_t n1 = static_cast<size_t>(n > 0 ? n : 1);
-  const size_t nch = n1 / kChunk + 2;
-  const size_t nb = n1 / kScanTile + 2;
+  const size_t nlong = n1 / kLong + 1;             // keys with > kLong occurrences
+  const size_t nunit = 2 * (n1 / kUnit) + 2;       // >= sum over them of ceil(count / kUnit)
   Layout L{};
+  L.ntiles = static_cast<int64_t>(n1 / kRankTile + 2);
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -69,17 +65,19 @@ Layout make_layout(int64_t n, int dim) {
   L.slot_of = take(4 * n1);
   L.occ_rank = take(4 * n1);
   L.inverse = take(4 * n1);
+  L.occ_row = take(8 * n1);
+  L.occ_pos = take(4 * n1);
   L.unique = take(8 * n1);
-  L.uslot = take(4 * n1);
-  L.ucount = take(4 * n1);
-  L.seg = take(4 * (n1 + 1));
+  L.useg = take(sizeof(Seg) * n1);
   L.rows = take(8 * n1);
-  L.isnew = take(4 * n1);
+  L.new_list = take(4 * n1);
   L.occ_ref = take(4 * n1);
-  L.chunk_u = take(4 * nch);
-  L.bsum = take(4 * nb);
+  L.long_u = take(4 * nlong);
+  L.long_start = take(4 * nlong);
+  L.units = take(sizeof(Unit) * nunit);
+  L.bsum = take(4 * 3 * static_cast<size_t>(L.ntiles));
   L.scal = take(8 * kCScalars);
-  L.gpart = take(4 * nch * static_cast<size_t>(dim));
+  L.gpart = take(4 * nlong * static_cast<size_t>(dim));
   L.total = off;
   return L;
 }
@@ -90,17 +88,20 @@ Work make_work(void* base, const Layout& L) {
   w.slot_of = reinterpret_cast<int32_t*>(b + L.slot_of);
   w.occ_rank = reinterpret_cast<int32_t*>(b + L.occ_rank);
   w.inverse = reinterpret_cast<int32_t*>(b + L.inverse);
+  w.occ_row = reinterpret_cast<int64_t*>(b + L.occ_row);
+  w.occ_pos = reinterpret_cast<int32_t*>(b + L.occ_pos);
   w.unique = reinterpret_cast<int64_t*>(b + L.unique);
-  w.uslot = reinterpret_cast<int32_t*>(b + L.uslot);
-  w.ucount = reinterpret_cast<int32_t*>(b + L.ucount);
-  w.seg = reinterpret_cast<int32_t*>(b + L.seg);
+  w.useg = reinterpret_cast<Seg*>(b + L.useg);
   w.rows = reinterpret_cast<int64_t*>(b + L.rows);
-  w.isnew = reinterpret_cast<int32_t*>(b + L.isnew);
+  w.new_list = reinterpret_cast<int32_t*>(b + L.new_list);
   w.occ_ref = reinterpret_cast<int32_t*>(b + L.occ_ref);
-  w.chunk_u = reinterpret_cast<int32_t*>(b + L.chunk_u);
+  w.long_u = reinterpret_cast<int32_t*>(b + L.long_u);
+  w.long_start = reinterpret_cast<int32_t*>(b + L.long_start);
+  w.units = reinterpret_cast<Unit*>(b + L.units);
   w.bsum = reinterpret_cast<int32_t*>(b + L.bsum);
   w.scal = reinterpret_cast<int64_t*>(b + L.scal);
   w.gpart = reinterpret_cast<float*>(b + L.gpart);
+  w.ntiles = L.ntiles;
   return w;
 }
 
@@ -129,19 +130,20 @@ struct rs_table {
   Slot* slots = nullptr;
   int64_t cap = 0;
   int64_t limit = 0;  // floor(max_load * cap)
-  // Blocks
-  std::vector<uint8_t*> blocks;
-  uint8_t** d_blocks = nullptr;
+  // Blocks: physical chunks (hipMemCreate) mapped back to back into one
+  // reserved virtual range, so rows never move when the table grows
+  uint8_t* va_base = nullptr;
+  size_t va_size = 0;
+  size_t mapped = 0;      // bytes mapped so far
+  size_t chunk_bytes = 0; // block_rows * stride, rounded up to the mapping granularity
+  std::vector<hipMemGenericAllocationHandle_t> chunks;
   int64_t stride = 0;
-  int block_shift = 0;
   int64_t rows_prov = 0;
   // device scalars
   int64_t* d_scal = nullptr;
   // dedup scratch
-  unsigned long long* s_key = nullptr;
-  unsigned int* s_first = nullptr;
-  unsigned int* s_cnt = nullptr;
-  int32_t* s_uid = nullptr;
+  ScratchSlot* s_slot = nullptr;
+  ScratchAux* s_aux = nullptr;
   int64_t s_cap = 0;
   // host view of the live count: an upper bound, refreshed from an
   // asynchronous read-back when one has completed
@@ -178,9 +180,7 @@ struct rs_table {
     TableDev t;
     t.slots = slots;
     t.cap_mask = static_cast<uint64_t>(cap - 1);
-    t.store.blocks = d_blocks;
-    t.store.shift = block_shift;
-    t.store.mask = d.block_rows - 1;
+    t.store.base = va_base;
     t.store.stride = stride;
     t.scal = d_scal;
     t.dim = d.dim;
@@ -191,7 +191,7 @@ struct rs_table {
     t.span = d.init_hi - d.init_lo;  // fp32 subtraction
     return t;
   }
-  Scratch scratch() const { return Scratch{s_key, s_first, s_cnt, s_uid, static_cast<uint64_t>(s_cap - 1)}; }
+  Scratch scratch() const { return Scratch{s_slot, s_aux, static_cast<uint64_t>(s_cap - 1)}; }
   hipEvent_t* ev(int k) { return (kev[k][0] || kev[k][1]) ? kev[k] : nullptr; }
 };
 
@@ -221,41 +221,50 @@ rs_status ensure_scratch(rs_table* t, int64_t n, hipStream_t s) {
   while (want < 2 * n) want <<= 1;
   if (t->s_cap >= want) return RS_OK;
   RS_HIP(hipStreamSynchronize(s));
-  t->release(t->s_key);
-  t->release(t->s_first);
-  t->release(t->s_cnt);
-  t->release(t->s_uid);
-  t->s_key = static_cast<unsigned long long*>(t->alloc(8 * want));
-  t->s_first = static_cast<unsigned int*>(t->alloc(4 * want));
-  t->s_cnt = static_cast<unsigned int*>(t->alloc(4 * want));
-  t->s_uid = static_cast<int32_t*>(t->alloc(4 * want));
-  if (!t->s_key || !t->s_first || !t->s_cnt || !t->s_uid) {
+  t->release(t->s_slot);
+  t->release(t->s_aux);
+  t->s_slot = static_cast<ScratchSlot*>(t->alloc(sizeof(ScratchSlot) * want));
+  t->s_aux = static_cast<ScratchAux*>(t->alloc(sizeof(ScratchAux) * want));
+  if (!t->s_slot || !t->s_aux) {
     t->s_cap = 0;
     return fail(RS_ENOMEM, "allocation of the dedup scratch failed");
   }
   t->s_cap = want;
-  RS_HIP(hipMemsetAsync(t->s_key, 0, 8 * want, s));
-  RS_HIP(hipMemsetAsync(t->s_first, 0xFF, 4 * want, s));
-  RS_HIP(hipMemsetAsync(t->s_cnt, 0, 4 * want, s));
+  // empty slot = {key 0, first 0xFFFFFFFF, cnt 0}
+  RS_HIP(launch_scratch_clear(t->s_slot, want, s));
   return RS_OK;
 }
 
-// Add Blocks chunks until `rows` rows fit.
+// Map Blocks chunks until `rows` rows fit.
 rs_status provision_rows(rs_table* t, int64_t rows, hipStream_t s) {
   if (rows <= t->rows_prov) return RS_OK;
-  const int64_t br = t->d.block_rows;
-  const int64_t need_blocks = (rows + br - 1) / br;
-  if (need_blocks > kMaxBlocks) return fail(RS_ENOMEM, "too many Blocks chunks (raise block_rows)");
-  const size_t first_new = t->blocks.size();
-  while (static_cast<int64_t>(t->blocks.size()) < need_blocks) {
-    void* p = t->alloc(static_cast<size_t>(br) * static_cast<size_t>(t->stride));
-    if (!p) return fail(RS_ENOMEM, "allocation of a Blocks chunk failed");
-    t->blocks.push_back(static_cast<uint8_t*>(p));
+  const size_t need = static_cast<size_t>(rows) * static_cast<size_t>(t->stride);
+  if (need > t->va_size) return fail(RS_ENOMEM, "table rows exceed the reserved Blocks address range");
+  hipMemAllocationProp prop = {};
+  prop.type = hipMemAllocationTypePinned;
+  prop.location.type = hipMemLocationTypeDevice;
+  prop.location.id = t->device;
+  hipMemAccessDesc acc = {};
+  acc.location.type = hipMemLocationTypeDevice;
+  acc.location.id = t->device;
+  acc.flags = hipMemAccessFlagsProtReadWrite;
+  while (t->mapped < need) {
+    const size_t bytes = std::min(t->chunk_bytes, t->va_size - t->mapped);
+    hipMemGenericAllocationHandle_t h;
+    if (hipMemCreate(&h, bytes, &prop, 0) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(RS_ENOMEM, "hipMemCreate of a Blocks chunk failed");
+    }
+    if (hipMemMap(t->va_base + t->mapped, bytes, 0, h, 0) != hipSuccess ||
+        hipMemSetAccess(t->va_base + t->mapped, bytes, &acc, 1) != hipSuccess) {
+      (void)hipGetLastError();
+      (void)hipMemRelease(h);
+      return fail(RS_EHIP, "mapping a Blocks chunk failed");
+    }
+    t->chunks.push_back(h);
+    t->mapped += bytes;
   }
-  // entries past the old count are read by no kernel yet: a plain copy is safe
-  RS_HIP(hipMemcpy(t->d_blocks + first_new, t->blocks.data() + first_new,
-                   sizeof(uint8_t*) * (t->blocks.size() - first_new), hipMemcpyHostToDevice));
-  t->rows_prov = static_cast<int64_t>(t->blocks.size()) * br;
+  t->rows_prov = static_cast<int64_t>(t->mapped / static_cast<size_t>(t->stride));
   return set_scalar(t, kTRowCap, t->rows_prov, s);
 }
 
@@ -313,32 +322,33 @@ void start_readback(rs_table* t, hipStream_t s) {
 
 // Dedup `values` into w, then find-or-insert the unique keys (growing the
 // table first when it may not have room).
-rs_status dedup_and_insert(rs_table* t, const int64_t* values, int64_t n, const Work& w, hipStream_t s) {
+rs_status dedup_and_insert(rs_table* t, const int64_t* values, int64_t n, const Work& w, bool occ_lists,
+                           hipStream_t s) {
   rs_status st = ensure_scratch(t, n, s);
   if (st != RS_OK) return st;
   const Scratch sc = t->scratch();
-  RS_HIP(launch_dedup(values, n, sc, w, reinterpret_cast<int*>(t->d_scal + kTErr), t->ev(RS_K_DEDUP_LOCAL),
-                      t->ev(RS_K_DEDUP_COMPACT), s));
-  RS_HIP(launch_seg_scan(w, n, sc, t->d.dim, s));
+  RS_HIP(launch_dedup_probe(values, n, sc, t->dev(), w, t->ev(RS_K_DEDUP_LOCAL), t->ev(RS_K_RANK_PROBE), s));
   refresh_bound(t);
   const int64_t bound = t->live_bound + n;
   if (bound > t->limit || bound > t->rows_prov) {
     // exact decision: read back U and live (one synchronization)
     RS_HIP(hipStreamSynchronize(s));
-    int64_t U = 0, live = 0;
-    RS_HIP(hipMemcpy(&U, w.scal + kCU, sizeof(int64_t), hipMemcpyDeviceToHost));
-    RS_HIP(hipMemcpy(&live, t->d_scal + kTLive, sizeof(int64_t), hipMemcpyDeviceToHost));
+    // the 3-way scan already reserved rows for the keys not found (or as
+    // many as fitted): read the request and the live count before it
+    int64_t req = 0, live0 = 0;
+    RS_HIP(hipMemcpy(&req, w.scal + kCNewReq, sizeof(int64_t), hipMemcpyDeviceToHost));
+    RS_HIP(hipMemcpy(&live0, w.scal + kCBaseLive, sizeof(int64_t), hipMemcpyDeviceToHost));
     t->rb_pending = false;
-    t->live_bound = live;
-    st = grow_for(t, live + U, s);
+    st = grow_for(t, live0 + req, s);
     if (st != RS_OK) return st;
-    t->live_bound = live + U;
+    // redo the reservation against the grown table
+    RS_HIP(launch_rereserve(w, t->dev(), s));
+    t->live_bound = live0 + req;
   } else {
     t->live_bound = bound;
   }
-  const TableDev td = t->dev();
-  RS_HIP(launch_idmap_probe(td, w, n, t->ev(RS_K_IDMAP_PROBE), s));
-  RS_HIP(launch_idmap_insert(td, w, n, t->ev(RS_K_IDMAP_INSERT), s));
+  RS_HIP(launch_compact_insert(values, n, sc, t->dev(), w, occ_lists, t->ev(RS_K_COMPACT_INSERT),
+                               t->ev(RS_K_INIT_ROWS), t->ev(RS_K_OCC), s));
   start_readback(t, s);
   return RS_OK;
 }
@@ -407,13 +417,11 @@ rs_status ht_create(const rs_table_desc* d, const rs_allocator* a, rs_stream str
     return fail(RS_EHIP, "hipGetDevice failed");
   }
   t->stride = static_cast<int64_t>(d->dim) * (t->wbytes() + 4 * t->nstate());
-  t->block_shift = ilog2(d->block_rows);
   t->cap = d->capacity_slots;
   t->limit = static_cast<int64_t>(std::floor(static_cast<double>(d->max_load) * static_cast<double>(t->cap)));
   t->slots = static_cast<Slot*>(t->alloc(sizeof(Slot) * static_cast<size_t>(t->cap)));
-  t->d_blocks = static_cast<uint8_t**>(t->alloc(sizeof(uint8_t*) * kMaxBlocks));
   t->d_scal = static_cast<int64_t*>(t->alloc(sizeof(int64_t) * kTScalars));
-  if (!t->slots || !t->d_blocks || !t->d_scal) {
+  if (!t->slots || !t->d_scal) {
     ht_destroy(t);
     return fail(RS_ENOMEM, "table allocation failed");
   }
@@ -425,13 +433,35 @@ rs_status ht_create(const rs_table_desc* d, const rs_allocator* a, rs_stream str
       break;
     }
     if (hipMemsetAsync(t->slots, 0, sizeof(Slot) * static_cast<size_t>(t->cap), s) != hipSuccess ||
-        hipMemsetAsync(t->d_blocks, 0, sizeof(uint8_t*) * kMaxBlocks, s) != hipSuccess ||
+
         hipMemsetAsync(t->d_scal, 0, sizeof(int64_t) * kTScalars, s) != hipSuccess) {
       st = fail(RS_EHIP, "initial clear failed");
       break;
     }
     st = set_scalar(t, kTLimit, t->limit, s);
     if (st != RS_OK) break;
+    // reserve the Blocks address range: as many bytes as the device has
+    hipMemAllocationProp prop = {};
+    prop.type = hipMemAllocationTypePinned;
+    prop.location.type = hipMemLocationTypeDevice;
+    prop.location.id = t->device;
+    size_t gran = 0, total = 0;
+    if (hipMemGetAllocationGranularity(&gran, &prop, hipMemAllocationGranularityRecommended) != hipSuccess ||
+        hipDeviceTotalMem(&total, t->device) != hipSuccess || gran == 0) {
+      st = fail(RS_EHIP, "querying the virtual-memory granularity failed");
+      break;
+    }
+    const size_t want = static_cast<size_t>(d->block_rows) * static_cast<size_t>(t->stride);
+    t->chunk_bytes = (want + gran - 1) / gran * gran;
+    t->va_size = (total + t->chunk_bytes - 1) / t->chunk_bytes * t->chunk_bytes;
+    void* va = nullptr;
+    if (hipMemAddressReserve(&va, t->va_size, 0, nullptr, 0) != hipSuccess) {
+      (void)hipGetLastError();
+      t->va_size = 0;
+      st = fail(RS_ENOMEM, "reserving the Blocks address range failed");
+      break;
+    }
+    t->va_base = static_cast<uint8_t*>(va);
     if (hipStreamSynchronize(s) != hipSuccess) st = fail(RS_EHIP, "hipStreamSynchronize failed");
   } while (false);
   if (st != RS_OK) {
@@ -448,13 +478,12 @@ rs_status ht_destroy(rs_table* t) {
   if (hipDeviceSynchronize() != hipSuccess) st = fail(RS_EHIP, "hipDeviceSynchronize failed");
   if (st == RS_OK && t->d_scal) st = take_latched(t);
   t->release(t->slots);
-  for (uint8_t* b : t->blocks) t->release(b);
-  t->release(t->d_blocks);
+  if (t->mapped) (void)hipMemUnmap(t->va_base, t->mapped);
+  for (hipMemGenericAllocationHandle_t h : t->chunks) (void)hipMemRelease(h);
+  if (t->va_base) (void)hipMemAddressFree(t->va_base, t->va_size);
   t->release(t->d_scal);
-  t->release(t->s_key);
-  t->release(t->s_first);
-  t->release(t->s_cnt);
-  t->release(t->s_uid);
+  t->release(t->s_slot);
+  t->release(t->s_aux);
   t->release(t->iws);
   if (t->h_pin) (void)hipHostFree(t->h_pin);
   if (t->rb_ev) (void)hipEventDestroy(t->rb_ev);
@@ -470,7 +499,7 @@ size_t lookup_workspace_bytes(int64_t n, int64_t /*bags*/, int64_t /*pad_len*/, 
 rs_status ht_find_or_insert(rs_table* t, const int64_t* keys, int64_t n, int64_t* rows_out, int64_t* n_inserted_dev,
                             rs_stream stream) {
   if (!t) return fail(RS_EINVAL, "null table");
-  if (n < 0 || n > (int64_t(1) << 30)) return fail(RS_EINVAL, "n must be in [0, 2^30]");
+  if (n < 0 || n > (int64_t(1) << 29)) return fail(RS_EINVAL, "n must be in [0, 2^29]");
   if (n > 0 && (!keys || !rows_out)) return fail(RS_EINVAL, "null keys or rows_out");
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (n == 0) {
@@ -486,7 +515,7 @@ rs_status ht_find_or_insert(rs_table* t, const int64_t* keys, int64_t n, int64_t
     if (!t->iws) return fail(RS_ENOMEM, "allocation of the insert workspace failed");
   }
   const Work w = make_work(t->iws, L);
-  rs_status st = dedup_and_insert(t, keys, n, w, s);
+  rs_status st = dedup_and_insert(t, keys, n, w, false, s);
   if (st != RS_OK) return st;
   RS_HIP(launch_map_rows(w, n, rows_out, n_inserted_dev, s));
   return RS_OK;
@@ -564,7 +593,7 @@ rs_status lookup_pool_fwd(rs_table* t, const int64_t* values, const int64_t* off
                           int32_t mode, int64_t pad_len, void* out, uint8_t* mask, rs_ctx* ctx, int32_t validate,
                           rs_stream stream) {
   if (!t || !ctx) return fail(RS_EINVAL, "null table or context");
-  if (n < 0 || n > (int64_t(1) << 30)) return fail(RS_EINVAL, "n must be in [0, 2^30]");
+  if (n < 0 || n > (int64_t(1) << 29)) return fail(RS_EINVAL, "n must be in [0, 2^29]");
   if (bags < 0 || bags >= (int64_t(1) << 31)) return fail(RS_EINVAL, "bags must be in [0, 2^31)");
   if (mode != RS_POOL_SUM && mode != RS_POOL_MEAN && mode != RS_POOL_NONE) return fail(RS_EINVAL, "bad pooling mode");
   if (mode == RS_POOL_NONE) {
@@ -596,7 +625,7 @@ rs_status lookup_pool_fwd(rs_table* t, const int64_t* values, const int64_t* off
   ctx->pad_len = mode == RS_POOL_NONE ? pad_len : 0;
   ctx->mode = mode;
   ctx->dim = t->d.dim;
-  rs_status st = dedup_and_insert(t, values, n, w, s);
+  rs_status st = dedup_and_insert(t, values, n, w, true, s);
   if (st != RS_OK) return st;
   RS_HIP(launch_pool(t->dev(), w, offsets, n, bags, mode, ctx->pad_len, out, mask, t->ev(RS_K_POOL), s));
   ctx->table = t;
@@ -608,8 +637,8 @@ rs_status lookup_pool_bwd(rs_table* t, const rs_ctx* ctx, const void* grad_out, 
   if (st != RS_OK) return st;
   if (ctx->n > 0 && (!grad_out || !grad_unique)) return fail(RS_EINVAL, "null gradient");
   const Work w = ctx_work(ctx);
-  RS_HIP(launch_bwd(t->dev(), w, ctx->offsets, ctx->n, ctx->bags, ctx->mode, ctx->pad_len, grad_out, grad_unique,
-                    nullptr, t->ev(RS_K_BWD_CHUNKS), t->ev(RS_K_BWD_STRADDLE), static_cast<hipStream_t>(stream)));
+  RS_HIP(launch_bwd(t->dev(), w, ctx->offsets, ctx->n, ctx->mode, grad_out, grad_unique, nullptr,
+                    t->ev(RS_K_BWD_SHORT), t->ev(RS_K_BWD_LONG), static_cast<hipStream_t>(stream)));
   return RS_OK;
 }
 
@@ -633,8 +662,8 @@ rs_status lookup_pool_bwd_opt(rs_table* t, const rs_ctx* ctx, const void* grad_o
   if (ctx->n > 0 && !grad_out) return fail(RS_EINVAL, "null gradient");
   const OptArgs o = make_opt(t, p);
   const Work w = ctx_work(ctx);
-  RS_HIP(launch_bwd(t->dev(), w, ctx->offsets, ctx->n, ctx->bags, ctx->mode, ctx->pad_len, grad_out, nullptr, &o,
-                    t->ev(RS_K_BWD_CHUNKS), t->ev(RS_K_BWD_STRADDLE), static_cast<hipStream_t>(stream)));
+  RS_HIP(launch_bwd(t->dev(), w, ctx->offsets, ctx->n, ctx->mode, grad_out, nullptr, &o, t->ev(RS_K_BWD_SHORT),
+                    t->ev(RS_K_BWD_LONG), static_cast<hipStream_t>(stream)));
   return RS_OK;
 }
 

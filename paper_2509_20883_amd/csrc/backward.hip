@@ -1,0 +1,324 @@
+// Backward + row-sparse optimizer kernels of the sparse embedding step (gfx950).
+//
+// RecIS backward workflow: the embedding gradients and the offsets kept from
+// the forward pass update the optimizer state and the parameters in the
+// Blocks directly ("Backward Update"; SparseAdam-style optimizers update the
+// touched rows only).  The gradient of a unique key is the sum over its
+// occurrences of the upstream gradient row of the occurrence's bag (scaled
+// by 1/len for mean pooling; one position's row for the padded copy).
+//
+// The forward wrote, per unique key, a contiguous segment of the occurrence
+// list.  Two strategies reduce it, as the paper's reduction operators pick a
+// mapping by conflict rate ("reduce easy" / "reduce hard"):
+//   k_bwd_short       a key with <= kLong occurrences: one lane group sums
+//                     its segment and, fused, applies the optimizer to its row
+//                     (the row and its state are prefetched while the
+//                     gradient rows are being read)
+//   k_bwd_long        a hot key: its segment is cut into units (kUnit
+//                     positions, more for the hottest keys so a key has at
+//                     most kMaxUnits units) spread over the whole GPU; the
+//                     partial sums of a wavefront's units of one key are
+//                     combined by shuffles and added into the key's partial
+//                     row with fp32 atomics (one per element per wavefront)
+//   k_bwd_long_finish applies the optimizer from the partial rows
+// Without the optimizer (lookup_pool_bwd) the same kernels write grad_unique.
+#include "device_common.h"
+
+namespace rs {
+
+// Optimizer state of E consecutive elements [lane*E, lane*E + E) of a row.
+template <typename WT, int E>
+struct RowFrag {
+  float w[E], s1[E], s2[E];
+  __device__ inline void load(const uint8_t* row, int lane, int dim, int nstate) {
+    load_vals<WT, E>(reinterpret_cast<const WT*>(row) + lane * E, w);
+    const float* p = reinterpret_cast<const float*>(row + static_cast<int64_t>(dim) * sizeof(WT)) + lane * E;
+    load_vals<float, E>(p, s1);
+    if (nstate == 2) load_vals<float, E>(p + dim, s2);
+  }
+  // Adagrad: acc += g^2; w -= lr g / (sqrt(acc) + eps).
+  // Adam:    m = b1 m + (1-b1) g; v = b2 v + (1-b2) g^2; w -= lr (m/bc1) / (sqrt(v/bc2) + eps).
+  __device__ inline void update_store(uint8_t* row, int lane, int dim, const float (&g)[E], const OptArgs& o) {
+    float* p = reinterpret_cast<float*>(row + static_cast<int64_t>(dim) * sizeof(WT)) + lane * E;
+    if (o.opt == 0) {
+#pragma unroll
+      for (int k = 0; k < E; ++k) {
+        s1[k] = s1[k] + g[k] * g[k];
+        w[k] = w[k] - o.lr * g[k] / (__builtin_sqrtf(s1[k]) + o.eps);
+      }
+      store_vals<float, E>(p, s1);
+    } else {
+#pragma unroll
+      for (int k = 0; k < E; ++k) {
+        s1[k] = o.beta1 * s1[k] + o.omb1 * g[k];
+        s2[k] = o.beta2 * s2[k] + o.omb2 * g[k] * g[k];
+        w[k] = w[k] - o.lr * (s1[k] / o.bc1) / (__builtin_sqrtf(s2[k] / o.bc2) + o.eps);
+      }
+      store_vals<float, E>(p, s1);
+      store_vals<float, E>(p + dim, s2);
+    }
+    store_vals<WT, E>(reinterpret_cast<WT*>(row) + lane * E, w);
+  }
+};
+
+// Sum of the gradient rows of occurrence-list positions [p0, p0 + cnt),
+// cnt <= kUnit.  The lanes of the group load the positions' gradient-row
+// indices together (one round trip), share them by shuffles, and then read
+// the gradient rows kBatch at a time.
+template <typename GT, int E, int LANES, int MODE>
+__device__ inline void sum_positions(const Work& w, const GT* __restrict__ grad, const int64_t* __restrict__ offsets,
+                                     int p0, int cnt, int lane, float (&acc)[E]) {
+  constexpr int D = LANES * E;
+  constexpr int NR = (kUnit + LANES - 1) / LANES;  // positions per lane
+  constexpr int kBatch = E == 4 ? 16 : 8;          // gradient rows in flight
+  int myref[NR];
+#pragma unroll
+  for (int k = 0; k < NR; ++k) {
+    const int q = k * LANES + lane;
+    myref[k] = q < cnt ? w.occ_ref[p0 + q] : -1;
+  }
+#pragma unroll
+  for (int q0 = 0; q0 < kUnit; q0 += kBatch) {
+    if (q0 >= cnt) break;
+    int ref[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int q = q0 + j;
+      const int r = LANES > 1 ? __shfl(myref[q / LANES], q % LANES, LANES) : myref[q];
+      ref[j] = q < cnt ? r : -1;
+    }
+    float x[kBatch][E];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      if (ref[j] >= 0) {
+        load_vals<GT, E>(grad + static_cast<int64_t>(ref[j]) * D + lane * E, x[j]);
+      } else {
+#pragma unroll
+        for (int k = 0; k < E; ++k) x[j][k] = 0.f;
+      }
+    }
+    if (MODE == 1) {
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        if (ref[j] < 0) continue;
+        const float sc = 1.0f / static_cast<float>(offsets[ref[j] + 1] - offsets[ref[j]]);
+#pragma unroll
+        for (int k = 0; k < E; ++k) x[j][k] *= sc;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j)
+#pragma unroll
+      for (int k = 0; k < E; ++k) acc[k] += x[j][k];
+  }
+}
+
+template <typename WT, typename GT, int LANES, int MODE, bool FUSED>
+__global__ __launch_bounds__(kBlock) void k_bwd_short(TableDev t, Work w, const int64_t* __restrict__ offsets,
+                                                      const GT* __restrict__ grad, float* __restrict__ grad_unique,
+                                                      OptArgs o) {
+  constexpr int E = 16 / static_cast<int>(sizeof(GT));
+  constexpr int GPB = kBlock / LANES;
+  constexpr int D = LANES * E;
+  const int lane = threadIdx.x % LANES;
+  const int grp = threadIdx.x / LANES;
+  const int64_t U = w.scal[kCU];
+  for (int64_t u = static_cast<int64_t>(blockIdx.x) * GPB + grp; u < U; u += static_cast<int64_t>(gridDim.x) * GPB) {
+    const Seg sg = w.useg[u];
+    if (sg.count > kLong) continue;  // a hot key: k_bwd_long
+    RowFrag<WT, E> fr;
+    uint8_t* rp = nullptr;
+    if (FUSED && sg.row >= 0) {
+      rp = t.store.row(sg.row);
+      fr.load(rp, lane, D, t.nstate);  // in flight while the gradients are read
+    }
+    float acc[E];
+#pragma unroll
+    for (int k = 0; k < E; ++k) acc[k] = 0.f;
+    sum_positions<GT, E, LANES, MODE>(w, grad, offsets, sg.start, sg.count, lane, acc);
+    if (FUSED) {
+      if (rp) fr.update_store(rp, lane, D, acc, o);
+    } else {
+      store_vals<float, E>(grad_unique + u * D + lane * E, acc);
+    }
+  }
+}
+
+// One lane group per backward unit of a hot key.  Units of one key are
+// consecutive, so the groups of a wavefront usually share the key: their
+// partial sums are then combined by cross-group shuffles and one group adds
+// the wavefront's sum into the key's partial row (one atomic per element per
+// wavefront, not per unit).
+template <typename GT, int LANES, int MODE>
+__global__ __launch_bounds__(kBlock) void k_bwd_long(Work w, const int64_t* __restrict__ offsets,
+                                                     const GT* __restrict__ grad) {
+  constexpr int E = 16 / static_cast<int>(sizeof(GT));
+  constexpr int GPW = kWave / LANES;  // lane groups per wavefront
+  constexpr int D = LANES * E;
+  const int lane = threadIdx.x % LANES;
+  const int gw = (threadIdx.x % kWave) / LANES;  // group within the wavefront
+  const int64_t units = w.scal[kCNUnits];
+  const int64_t waves = static_cast<int64_t>(gridDim.x) * (kBlock / kWave);
+  for (int64_t wb = (static_cast<int64_t>(blockIdx.x) * (kBlock / kWave) + threadIdx.x / kWave) * GPW; wb < units;
+       wb += waves * GPW) {  // the trip count is uniform across the wavefront
+    const int64_t unit = wb + gw;
+    int li = -1;
+    float acc[E];
+#pragma unroll
+    for (int q = 0; q < E; ++q) acc[q] = 0.f;
+    if (unit < units) {
+      const Unit un = w.units[unit];
+      li = un.li;
+      for (int p = un.p0; p < un.p1; p += kUnit) sum_positions<GT, E, LANES, MODE>(w, grad, offsets, p, min(kUnit, un.p1 - p), lane, acc);
+    }
+    int li0 = li;
+#pragma unroll
+    for (int off = LANES; off < kWave; off <<= 1) li0 = max(li0, __shfl_xor(li0, off, kWave));
+    const bool same = __all(li == li0 || li < 0);
+    if (same && GPW > 1) {
+#pragma unroll
+      for (int off = LANES; off < kWave; off <<= 1)
+#pragma unroll
+        for (int q = 0; q < E; ++q) acc[q] += __shfl_xor(acc[q], off, kWave);
+      if (gw == 0 && li0 >= 0) {
+        float* gp = w.gpart + static_cast<int64_t>(li0) * D + lane * E;
+#pragma unroll
+        for (int q = 0; q < E; ++q) unsafeAtomicAdd(gp + q, acc[q]);
+      }
+    } else if (li >= 0) {
+      float* gp = w.gpart + static_cast<int64_t>(li) * D + lane * E;
+#pragma unroll
+      for (int q = 0; q < E; ++q) unsafeAtomicAdd(gp + q, acc[q]);
+    }
+  }
+}
+
+template <typename WT, int E, int LANES, bool FUSED>
+__global__ __launch_bounds__(kBlock) void k_bwd_long_finish(TableDev t, Work w, float* __restrict__ grad_unique,
+                                                            OptArgs o) {
+  constexpr int GPB = kBlock / LANES;
+  constexpr int D = LANES * E;
+  const int lane = threadIdx.x % LANES;
+  const int grp = threadIdx.x / LANES;
+  const int64_t nlong = w.scal[kCNLong];
+  for (int64_t li = static_cast<int64_t>(blockIdx.x) * GPB + grp; li < nlong;
+       li += static_cast<int64_t>(gridDim.x) * GPB) {
+    const int u = w.long_u[li];
+    float acc[E];
+    load_vals<float, E>(w.gpart + li * D + lane * E, acc);
+    if (FUSED) {
+      const int64_t r = w.useg[u].row;
+      if (r < 0) continue;
+      uint8_t* rp = t.store.row(r);
+      RowFrag<WT, E> fr;
+      fr.load(rp, lane, D, t.nstate);
+      fr.update_store(rp, lane, D, acc, o);
+    } else {
+      store_vals<float, E>(grad_unique + static_cast<int64_t>(u) * D + lane * E, acc);
+    }
+  }
+}
+
+template <typename WT, typename GT, int LANES, int MODE, bool FUSED>
+static hipError_t bwd_launch(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, const void* grad,
+                             float* gu, const OptArgs& o, hipEvent_t* ev_s, hipEvent_t* ev_l, hipStream_t s) {
+  constexpr int E = 16 / static_cast<int>(sizeof(GT));
+  constexpr int GPB = kBlock / LANES;
+  const GT* g = static_cast<const GT*>(grad);
+  if (ev_s && ev_s[0]) (void)hipEventRecord(ev_s[0], s);
+  k_bwd_short<WT, GT, LANES, MODE, FUSED><<<grid_for(n, GPB, 1 << 17), kBlock, 0, s>>>(t, w, offsets, g, gu, o);
+  if (ev_s && ev_s[1]) (void)hipEventRecord(ev_s[1], s);
+  if (ev_l && ev_l[0]) (void)hipEventRecord(ev_l[0], s);
+  k_bwd_long<GT, LANES, MODE><<<grid_for(2 * (n / kUnit) + 2, GPB, 1 << 16), kBlock, 0, s>>>(w, offsets, g);
+  k_bwd_long_finish<WT, E, LANES, FUSED><<<grid_for(n / kLong + 1, GPB, 1 << 16), kBlock, 0, s>>>(t, w, gu, o);
+  if (ev_l && ev_l[1]) (void)hipEventRecord(ev_l[1], s);
+  return hipGetLastError();
+}
+
+template <typename WT, typename GT, int MODE, bool FUSED>
+static hipError_t bwd_dim(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, const void* grad,
+                          float* gu, const OptArgs& o, hipEvent_t* es, hipEvent_t* el, hipStream_t s) {
+  constexpr int E = 16 / static_cast<int>(sizeof(GT));
+  switch (t.dim / E) {
+    case 1: return bwd_launch<WT, GT, 1, MODE, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
+    case 2: return bwd_launch<WT, GT, 2, MODE, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
+    case 4: return bwd_launch<WT, GT, 4, MODE, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
+    case 8: return bwd_launch<WT, GT, 8, MODE, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
+    case 16: return bwd_launch<WT, GT, 16, MODE, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
+    case 32: return bwd_launch<WT, GT, 32, MODE, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
+    case 64: return bwd_launch<WT, GT, 64, MODE, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <typename WT, bool FUSED>
+static hipError_t bwd_mode(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int mode,
+                           const void* grad, float* gu, const OptArgs& o, hipEvent_t* es, hipEvent_t* el,
+                           hipStream_t s) {
+  if (mode == 2) return bwd_dim<WT, WT, 0, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
+  if (mode == 1) return bwd_dim<WT, float, 1, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
+  return bwd_dim<WT, float, 0, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
+}
+
+hipError_t launch_bwd(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int mode, const void* grad,
+                      float* grad_unique, const OptArgs* opt, hipEvent_t* ev_short, hipEvent_t* ev_long,
+                      hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const OptArgs o = opt ? *opt : OptArgs{0, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 1.f, 1.f};
+  if (opt)
+    return t.row_dtype ? bwd_mode<uint16_t, true>(t, w, offsets, n, mode, grad, grad_unique, o, ev_short, ev_long, s)
+                       : bwd_mode<float, true>(t, w, offsets, n, mode, grad, grad_unique, o, ev_short, ev_long, s);
+  return t.row_dtype ? bwd_mode<uint16_t, false>(t, w, offsets, n, mode, grad, grad_unique, o, ev_short, ev_long, s)
+                     : bwd_mode<float, false>(t, w, offsets, n, mode, grad, grad_unique, o, ev_short, ev_long, s);
+}
+
+// ---------------------------------------------------------------------------
+// optimizer from a written grad_unique (the two-call path)
+// ---------------------------------------------------------------------------
+
+template <typename WT, int LANES>
+__global__ __launch_bounds__(kBlock) void k_opt(TableDev t, Work w, const float* __restrict__ grad_unique, OptArgs o) {
+  constexpr int E = 4;
+  constexpr int GPB = kBlock / LANES;
+  constexpr int D = LANES * E;
+  const int lane = threadIdx.x % LANES;
+  const int grp = threadIdx.x / LANES;
+  const int64_t U = w.scal[kCU];
+  for (int64_t u = static_cast<int64_t>(blockIdx.x) * GPB + grp; u < U; u += static_cast<int64_t>(gridDim.x) * GPB) {
+    const int64_t r = w.useg[u].row;
+    if (r < 0) continue;
+    uint8_t* rp = t.store.row(r);
+    RowFrag<WT, E> fr;
+    fr.load(rp, lane, D, t.nstate);
+    float g[E];
+    load_vals<float, E>(grad_unique + u * D + lane * E, g);
+    fr.update_store(rp, lane, D, g, o);
+  }
+}
+
+template <typename WT>
+static hipError_t opt_dim(const TableDev& t, const Work& w, int64_t n, const float* gu, const OptArgs& o,
+                          hipStream_t s) {
+  switch (t.dim / 4) {
+    case 2: k_opt<WT, 2><<<grid_for(n, kBlock / 2, 1 << 16), kBlock, 0, s>>>(t, w, gu, o); break;
+    case 4: k_opt<WT, 4><<<grid_for(n, kBlock / 4, 1 << 16), kBlock, 0, s>>>(t, w, gu, o); break;
+    case 8: k_opt<WT, 8><<<grid_for(n, kBlock / 8, 1 << 16), kBlock, 0, s>>>(t, w, gu, o); break;
+    case 16: k_opt<WT, 16><<<grid_for(n, kBlock / 16, 1 << 16), kBlock, 0, s>>>(t, w, gu, o); break;
+    case 32: k_opt<WT, 32><<<grid_for(n, kBlock / 32, 1 << 16), kBlock, 0, s>>>(t, w, gu, o); break;
+    case 64: k_opt<WT, 64><<<grid_for(n, kBlock / 64, 1 << 16), kBlock, 0, s>>>(t, w, gu, o); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_opt(const TableDev& t, const Work& w, int64_t n, const float* grad_unique, const OptArgs& opt,
+                      hipEvent_t* ev, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (ev && ev[0]) (void)hipEventRecord(ev[0], s);
+  const hipError_t e =
+      t.row_dtype ? opt_dim<uint16_t>(t, w, n, grad_unique, opt, s) : opt_dim<float>(t, w, n, grad_unique, opt, s);
+  if (ev && ev[1]) (void)hipEventRecord(ev[1], s);
+  return e;
+}
+
+}  // namespace rs

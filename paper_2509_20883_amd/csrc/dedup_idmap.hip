@@ -1,0 +1,642 @@
+// Dedup and IDMap kernels of the sparse embedding step (gfx950).
+//
+// RecIS keeps a two-tier store: an IDMap from feature id to an offset and
+// Blocks holding the rows ("Optimization for Memory Bound"); ids are
+// deduplicated before the lookup ("ids partition").  One forward runs:
+//   k_dedup_local    per 1024-occurrence tile: LDS dedup, then one global
+//                    scratch insert per distinct key of the tile (atomicMin of
+//                    its first position, atomicAdd of its count; the value the
+//                    atomicAdd returns ranks the tile's occurrences of the key)
+//   k_rank_probe     first occurrences probe the IDMap; tile sums of
+//                    (first occurrences, their counts, keys not found)
+//   k_scan3          one block scans the three tile-sum arrays and reserves
+//                    the rows of the new keys
+//   k_compact_insert unique ids in first-occurrence order, occurrence-list
+//                    segments, rows; new keys claim an IDMap slot
+//   k_init_rows      lane groups write the initial rows of the new keys
+//   k_occ            per occurrence: unique id (inverse), row, position in the
+//                    occurrence list, hot-key backward units; releases the
+//                    scratch slots
+#include "device_common.h"
+
+namespace rs {
+
+// ---------------------------------------------------------------------------
+// open addressing (linear probing)
+// ---------------------------------------------------------------------------
+
+// Row of an encoded key, or -1 when the probe reaches an empty slot.  Reads
+// kProbeBatch consecutive slots per round trip.
+__device__ inline int64_t idmap_lookup(const TableDev& t, unsigned long long e) {
+  uint64_t h = idmap_hash(e) & t.cap_mask;
+  for (uint64_t probed = 0; probed <= t.cap_mask; probed += kProbeBatch) {
+    Slot sl[kProbeBatch];
+#pragma unroll
+    for (int k = 0; k < kProbeBatch; ++k) sl[k] = t.slots[(h + k) & t.cap_mask];
+#pragma unroll
+    for (int k = 0; k < kProbeBatch; ++k) {
+      if (sl[k].key == e) return sl[k].row;
+      if (sl[k].key == kEncEmpty) return -1;
+    }
+    h = (h + kProbeBatch) & t.cap_mask;
+  }
+  return -1;
+}
+
+// Claim the slot of an encoded key (its own if present, else the first empty
+// one on its probe sequence); returns the slot index or -1 if the table is full.
+// A stale read of an empty slot only costs a failed compare-and-swap.
+__device__ inline int64_t idmap_claim(const TableDev& t, unsigned long long e) {
+  uint64_t h = idmap_hash(e) & t.cap_mask;
+  for (uint64_t probed = 0; probed <= t.cap_mask; ++probed) {
+    const unsigned long long cur = t.slots[h].key;
+    if (cur == e) return static_cast<int64_t>(h);
+    if (cur == kEncEmpty) {
+      const unsigned long long old = atomicCAS(&t.slots[h].key, kEncEmpty, e);
+      if (old == kEncEmpty || old == e) return static_cast<int64_t>(h);
+    }
+    h = (h + 1) & t.cap_mask;
+  }
+  return -1;
+}
+
+// Slot of an encoded key in the scratch set: read first, compare-and-swap only
+// an empty slot (a hot key, already present, costs no atomic here).
+__device__ inline int64_t scratch_claim(const Scratch& sc, unsigned long long e) {
+  uint64_t h = scratch_hash(e) & sc.mask;
+  for (uint64_t probed = 0; probed <= sc.mask; ++probed) {
+    unsigned long long cur = sc.slot[h].key;
+    if (cur == kEncEmpty) cur = atomicCAS(&sc.slot[h].key, kEncEmpty, e);
+    if (cur == kEncEmpty || cur == e) return static_cast<int64_t>(h);
+    h = (h + 1) & sc.mask;
+  }
+  return -1;
+}
+
+// ---------------------------------------------------------------------------
+// pass 1: tile-local dedup in LDS, then the global scratch set
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kBlock) void k_dedup_local(const int64_t* __restrict__ values, int64_t n, Scratch sc,
+                                                        int32_t* __restrict__ slot_of, int32_t* __restrict__ occ_rank,
+                                                        int* err) {
+  __shared__ unsigned long long lkey[kDedupLdsSlots];
+  __shared__ unsigned int lmin[kDedupLdsSlots];
+  __shared__ unsigned int lcnt[kDedupLdsSlots];
+  __shared__ int lgs[kDedupLdsSlots];
+  __shared__ unsigned int lbase[kDedupLdsSlots];
+  const int tid = threadIdx.x;
+  for (int s = tid; s < kDedupLdsSlots; s += kBlock) {
+    lkey[s] = kEncEmpty;
+    lmin[s] = 0xFFFFFFFFu;
+    lcnt[s] = 0u;
+  }
+  __syncthreads();
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kDedupTile;
+  unsigned long long e[kDedupItems];
+#pragma unroll
+  for (int k = 0; k < kDedupItems; ++k) {
+    const int64_t i = base + k * kBlock + tid;
+    e[k] = i < n ? (static_cast<unsigned long long>(values[i]) ^ kSign) : kEncEmpty;
+  }
+  int ls[kDedupItems];
+  unsigned int lr[kDedupItems];
+#pragma unroll
+  for (int k = 0; k < kDedupItems; ++k) {
+    const int64_t i = base + k * kBlock + tid;
+    ls[k] = -1;
+    lr[k] = 0;
+    if (i >= n) continue;
+    if (e[k] <= kEncTomb) {
+      atomicOr(err, kErrKey);
+      continue;
+    }
+    unsigned int h = static_cast<unsigned int>(mix64(e[k]) >> 40) & (kDedupLdsSlots - 1);
+    while (true) {  // at most kDedupTile keys in twice as many slots: terminates
+      const unsigned long long old = atomicCAS(&lkey[h], kEncEmpty, e[k]);
+      if (old == kEncEmpty || old == e[k]) break;
+      h = (h + 1) & (kDedupLdsSlots - 1);
+    }
+    atomicMin(&lmin[h], static_cast<unsigned int>(i));
+    lr[k] = atomicAdd(&lcnt[h], 1u);
+    ls[k] = static_cast<int>(h);
+  }
+  __syncthreads();
+  // Each thread owns 8 LDS slots.  Their first scratch reads are issued
+  // together; an existing key needs no compare-and-swap, and its first
+  // position needs no atomicMin when the stored one is already smaller (it
+  // only ever decreases, so a stale read errs on the side of the atomic).
+  constexpr int kOwn = kDedupLdsSlots / kBlock;
+  unsigned long long ke[kOwn];
+  int64_t gs[kOwn];
+  ScratchSlot cur[kOwn];
+#pragma unroll
+  for (int j = 0; j < kOwn; ++j) {
+    ke[j] = lkey[tid + j * kBlock];
+    gs[j] = -1;
+  }
+#pragma unroll
+  for (int j = 0; j < kOwn; ++j)
+    if (ke[j] != kEncEmpty) cur[j] = sc.slot[scratch_hash(ke[j]) & sc.mask];
+#pragma unroll
+  for (int j = 0; j < kOwn; ++j) {
+    if (ke[j] == kEncEmpty) continue;
+    const uint64_t h = scratch_hash(ke[j]) & sc.mask;
+    if (cur[j].key == ke[j]) {
+      gs[j] = static_cast<int64_t>(h);
+    } else if (cur[j].key == kEncEmpty) {
+      const unsigned long long old = atomicCAS(&sc.slot[h].key, kEncEmpty, ke[j]);
+      if (old == kEncEmpty || old == ke[j]) {
+        gs[j] = static_cast<int64_t>(h);
+        cur[j].first = 0xFFFFFFFFu;  // not read: always take the atomicMin
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kOwn; ++j) {
+    if (ke[j] == kEncEmpty || gs[j] >= 0) continue;
+    gs[j] = scratch_claim(sc, ke[j]);
+    cur[j].first = 0xFFFFFFFFu;
+    if (gs[j] < 0) atomicOr(err, kErrScratch);
+  }
+  unsigned int gb[kOwn];
+#pragma unroll
+  for (int j = 0; j < kOwn; ++j) {
+    gb[j] = 0;
+    if (gs[j] < 0) continue;
+    const int s = tid + j * kBlock;
+    if (cur[j].first > lmin[s]) atomicMin(&sc.slot[gs[j]].first, lmin[s]);
+    gb[j] = atomicAdd(&sc.slot[gs[j]].cnt, lcnt[s]);
+  }
+#pragma unroll
+  for (int j = 0; j < kOwn; ++j) {
+    const int s = tid + j * kBlock;
+    lgs[s] = static_cast<int>(gs[j]);
+    lbase[s] = gb[j];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kDedupItems; ++k) {
+    const int64_t i = base + k * kBlock + tid;
+    if (i >= n) continue;
+    const int g = ls[k] >= 0 ? lgs[ls[k]] : -1;
+    const bool cand = g >= 0 && lmin[ls[k]] == static_cast<unsigned int>(i);
+    slot_of[i] = g < 0 ? -1 : (g | (cand ? kCandBit : 0));
+    occ_rank[i] = g >= 0 ? static_cast<int>(lbase[ls[k]] + lr[k]) : 0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// pass 2: first occurrences probe the IDMap; tile sums
+// ---------------------------------------------------------------------------
+
+__device__ inline void load4(const int32_t* __restrict__ p, int64_t i0, int64_t n, int (&v)[4]) {
+  if (i0 + 4 <= n) {
+    const int4 a = *reinterpret_cast<const int4*>(p + i0);
+    v[0] = a.x;
+    v[1] = a.y;
+    v[2] = a.z;
+    v[3] = a.w;
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = (i0 + k < n) ? p[i0 + k] : -1;
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_rank_probe(TableDev t, Scratch sc, const int32_t* __restrict__ slot_of,
+                                                       int64_t n, int32_t* __restrict__ bsum, int64_t ntiles) {
+  __shared__ int sh[kBlock / kWave + 1];
+  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kRankTile + threadIdx.x * kRankItems;
+  int s[4];
+  load4(slot_of, i0, n, s);
+  bool f[4];
+  ScratchSlot ss[4];
+  int c = 0, cf = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const bool cand = s[k] >= 0 && (s[k] & kCandBit);
+    if (cand) ss[k] = sc.slot[s[k] & kSlotMask];
+    f[k] = cand && ss[k].first == static_cast<unsigned int>(i0 + k);
+    if (f[k]) {
+      cf += 1;
+      c += static_cast<int>(ss[k].cnt);
+    }
+  }
+  int nw = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (!f[k]) continue;
+    const int64_t r = idmap_lookup(t, ss[k].key);
+    sc.aux[s[k] & kSlotMask].row = r;
+    nw += r < 0;
+  }
+  const int a = block_sum<kBlock>(cf | (nw << 16), sh);
+  __syncthreads();
+  const int b = block_sum<kBlock>(c, sh);
+  if (threadIdx.x == 0) {
+    bsum[blockIdx.x] = a & 0xFFFF;
+    bsum[ntiles + blockIdx.x] = b;
+    bsum[2 * ntiles + blockIdx.x] = a >> 16;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// one-block scan of the three tile-sum arrays; row reservation
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(1024) void k_scan3(int32_t* __restrict__ bsum, int64_t nb, int64_t ntiles,
+                                                int64_t* cscal, int64_t* tscal) {
+  __shared__ int sh[1024 / kWave + 1];
+  const int64_t per = (nb + 1023) / 1024;
+  const int64_t lo = min(nb, static_cast<int64_t>(threadIdx.x) * per);
+  const int64_t hi = min(nb, lo + per);
+  int64_t totals[3];
+#pragma unroll
+  for (int a = 0; a < 3; ++a) {
+    int32_t* p = bsum + a * ntiles;
+    int local = 0;
+    for (int64_t k = lo; k < hi; ++k) local += p[k];
+    int tot;
+    int run = block_excl_scan<1024>(local, sh, tot);
+    for (int64_t k = lo; k < hi; ++k) {
+      const int v = p[k];
+      p[k] = run;
+      run += v;
+    }
+    totals[a] = tot;
+  }
+  if (threadIdx.x != 0) return;
+  cscal[kCU] = totals[0];
+  cscal[kCValid] = totals[1];
+  cscal[kCNewReq] = totals[2];
+  cscal[kCNLong] = 0;
+  cscal[kCNUnits] = 0;
+  const int64_t live = tscal[kTLive];
+  const int64_t lim = min(tscal[kTLimit], tscal[kTRowCap]);
+  const int64_t room = lim > live ? lim - live : 0;
+  const int64_t ins = totals[2] < room ? totals[2] : room;
+  cscal[kCNew] = ins;
+  cscal[kCBaseLive] = live;
+  cscal[kCTrunc] = totals[2] > room ? 1 : 0;
+  tscal[kTLive] = live + ins;
+}
+
+// After the host grew the table: reserve again from the same live count.
+__global__ void k_rereserve(int64_t* cscal, int64_t* tscal) {
+  const int64_t live = cscal[kCBaseLive], req = cscal[kCNewReq];
+  const int64_t lim = min(tscal[kTLimit], tscal[kTRowCap]);
+  const int64_t room = lim > live ? lim - live : 0;
+  const int64_t ins = req < room ? req : room;
+  cscal[kCNew] = ins;
+  cscal[kCTrunc] = req > room ? 1 : 0;
+  tscal[kTLive] = live + ins;
+}
+
+__global__ void k_scratch_clear(ScratchSlot* slots, int64_t n) {
+  for (int64_t i = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * kBlock)
+    slots[i] = ScratchSlot{kEncEmpty, 0xFFFFFFFFu, 0u};
+}
+
+hipError_t launch_scratch_clear(ScratchSlot* slots, int64_t n, hipStream_t s) {
+  k_scratch_clear<<<grid_for(n, kBlock, 65536), kBlock, 0, s>>>(slots, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_rereserve(const Work& w, const TableDev& t, hipStream_t s) {
+  k_rereserve<<<1, 1, 0, s>>>(w.scal, t.scal);
+  return hipGetLastError();
+}
+
+hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const Scratch& sc, const TableDev& t, const Work& w,
+                              hipEvent_t* ev_local, hipEvent_t* ev_probe, hipStream_t s) {
+  if (n <= 0) {
+    (void)hipMemsetAsync(w.scal, 0, sizeof(int64_t) * kCScalars, s);
+    return hipGetLastError();
+  }
+  const int64_t nb = (n + kRankTile - 1) / kRankTile;
+  if (ev_local && ev_local[0]) (void)hipEventRecord(ev_local[0], s);
+  k_dedup_local<<<grid_for(n, kDedupTile, 1ll << 31), kBlock, 0, s>>>(values, n, sc, w.slot_of, w.occ_rank,
+                                                                     reinterpret_cast<int*>(t.scal + kTErr));
+  if (ev_local && ev_local[1]) (void)hipEventRecord(ev_local[1], s);
+  if (ev_probe && ev_probe[0]) (void)hipEventRecord(ev_probe[0], s);
+  k_rank_probe<<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, sc, w.slot_of, n, w.bsum, w.ntiles);
+  if (ev_probe && ev_probe[1]) (void)hipEventRecord(ev_probe[1], s);
+  k_scan3<<<1, 1024, 0, s>>>(w.bsum, nb, w.ntiles, w.scal, t.scal);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// pass 3: unique ids, segments, rows, IDMap inserts
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kBlock) void k_compact_insert(TableDev t, Scratch sc, Work w,
+                                                           const int64_t* __restrict__ values, int64_t n) {
+  __shared__ int sh[kBlock / kWave + 1];
+  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kRankTile + threadIdx.x * kRankItems;
+  int s[4];
+  load4(w.slot_of, i0, n, s);
+  bool f[4];
+  ScratchSlot ss[4];
+  int64_t r[4];
+  int cf = 0, cc = 0, cn = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const bool cand = s[k] >= 0 && (s[k] & kCandBit);
+    s[k] &= kSlotMask;
+    if (cand) ss[k] = sc.slot[s[k]];
+    f[k] = cand && ss[k].first == static_cast<unsigned int>(i0 + k);
+    r[k] = f[k] ? sc.aux[s[k]].row : 0;
+    cf += f[k];
+    cc += f[k] ? static_cast<int>(ss[k].cnt) : 0;
+    cn += (f[k] && r[k] < 0);
+  }
+  int tot;
+  const int ex_a = block_excl_scan<kBlock>(cf | (cn << 16), sh, tot);
+  const int ex_c = block_excl_scan<kBlock>(cc, sh, tot);
+  const int b = blockIdx.x;
+  int uid = w.bsum[b] + (ex_a & 0xFFFF);
+  int start = w.bsum[w.ntiles + b] + ex_c;
+  int64_t nr = w.bsum[2 * w.ntiles + b] + (ex_a >> 16);
+  const int64_t inserted = w.scal[kCNew];
+  const int64_t live0 = w.scal[kCBaseLive];
+  if (blockIdx.x == 0 && threadIdx.x == 0 && w.scal[kCTrunc]) atomicOr(reinterpret_cast<int*>(&t.scal[kTErr]), kErrFull);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (!f[k]) continue;
+    const int c = static_cast<int>(ss[k].cnt);
+    w.unique[uid] = values[i0 + k];
+    int li = -1, ush = 0;
+    if (c > kLong) {
+      li = static_cast<int>(atomicAdd(reinterpret_cast<unsigned long long*>(&w.scal[kCNLong]), 1ull));
+      while ((c - 1) >> (ush + kUnitLog2) >= kMaxUnits) ++ush;  // ceil(c / (kUnit << ush)) <= kMaxUnits
+      const int usz = kUnit << ush;
+      const int units = (c + usz - 1) / usz;
+      const int us = static_cast<int>(
+          atomicAdd(reinterpret_cast<unsigned long long*>(&w.scal[kCNUnits]), static_cast<unsigned long long>(units)));
+      w.long_u[li] = uid;
+      w.long_start[li] = us;
+      float4* gp = reinterpret_cast<float4*>(w.gpart + static_cast<int64_t>(li) * t.dim);
+      for (int j = 0; j < t.dim / 4; ++j) gp[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    int64_t row = r[k];
+    if (row < 0) {
+      if (nr < inserted) {
+        const int64_t slot = idmap_claim(t, ss[k].key);
+        if (slot >= 0) {
+          row = live0 + nr;
+          t.slots[slot].row = row;
+          w.new_list[nr] = uid;
+        } else {
+          atomicOr(reinterpret_cast<int*>(&t.scal[kTErr]), kErrProbe);
+        }
+      }
+      ++nr;
+    }
+    w.rows[uid] = row;
+    w.useg[uid] = Seg{row, start, c};
+    ScratchAux ax;
+    ax.row = row;
+    ax.start = start;
+    ax.uid = uid;
+    ax.count = c;
+    ax.long_idx = li;
+    ax.unit_shift = ush;
+    ax.pad = 0;
+    sc.aux[s[k]] = ax;
+    ++uid;
+    start += c;
+  }
+}
+
+// The initial value of element j of a new key's row: 24 bits of the
+// (j+1)-th splitmix64 output from state mix(key ^ mix(seed)), mapped
+// exactly onto [0, 1), then one fp32 fused multiply-add onto [lo, hi].
+__device__ inline float init_value(uint64_t z, int j, float lo, float span) {
+  const uint64_t h = mix64(z + static_cast<uint64_t>(j + 1) * 0x9E3779B97F4A7C15ull);
+  const float u = static_cast<float>(h >> 40) * 0x1.0p-24f;
+  return __builtin_fmaf(u, span, lo);
+}
+
+// Lane groups of 16 write the rows of the inserted keys: w from the init
+// formula, optimizer state zero, 16 bytes per lane per store.
+__global__ __launch_bounds__(kBlock) void k_init_rows(TableDev t, Work w) {
+  constexpr int G = 16;
+  const int lane = threadIdx.x % G, grp = threadIdx.x / G;
+  const int64_t inserted = w.scal[kCNew];
+  const int chunks = static_cast<int>(t.store.stride / 16);
+  const int wbytes = t.dim * (t.row_dtype ? 2 : 4);
+  for (int64_t q = static_cast<int64_t>(blockIdx.x) * (kBlock / G) + grp; q < inserted;
+       q += static_cast<int64_t>(gridDim.x) * (kBlock / G)) {
+    const int u = w.new_list[q];
+    const int64_t row = w.useg[u].row;
+    const uint64_t z = mix64(static_cast<uint64_t>(w.unique[u]) ^ mix64(t.seed));
+    uint8_t* rp = t.store.row(row);
+    for (int ch = lane; ch < chunks; ch += G) {
+      const int off = ch * 16;
+      uint4 val = make_uint4(0u, 0u, 0u, 0u);
+      if (off < wbytes) {
+        if (t.row_dtype == 0) {
+          const int j0 = off / 4;
+          val = make_uint4(__float_as_uint(init_value(z, j0, t.lo, t.span)),
+                           __float_as_uint(init_value(z, j0 + 1, t.lo, t.span)),
+                           __float_as_uint(init_value(z, j0 + 2, t.lo, t.span)),
+                           __float_as_uint(init_value(z, j0 + 3, t.lo, t.span)));
+        } else {
+          const int j0 = off / 2;
+          uint32_t h[4];
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            h[k] = static_cast<uint32_t>(f32_to_bf16(init_value(z, j0 + 2 * k, t.lo, t.span))) |
+                   (static_cast<uint32_t>(f32_to_bf16(init_value(z, j0 + 2 * k + 1, t.lo, t.span))) << 16);
+          val = make_uint4(h[0], h[1], h[2], h[3]);
+        }
+      }
+      *reinterpret_cast<uint4*>(rp + off) = val;
+    }
+  }
+}
+
+// The per-occurrence pass: inverse[i] = unique id of occurrence i (-1 for a
+// rejected key), and the occurrence of rank 0 of each key returns its scratch
+// slot to empty, so the scratch never needs a full clear.  For a forward
+// (OCC) it also writes each occurrence's row and its position in the
+// occurrence list, and the descriptor of every backward unit of a hot key.
+template <bool OCC>
+__global__ __launch_bounds__(kBlock) void k_occ(Scratch sc, Work w, int64_t n) {
+  const int64_t i0 = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * 4;
+  if (i0 >= n) return;
+  int s[4], rk[4];
+  load4(w.slot_of, i0, n, s);
+  load4(w.occ_rank, i0, n, rk);
+  ScratchAux a[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (s[k] >= 0) {
+      a[k] = sc.aux[s[k] & kSlotMask];
+    } else {
+      a[k].row = -1;
+      a[k].uid = -1;
+      a[k].start = 0;
+      a[k].long_idx = -1;
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (s[k] < 0 || i0 + k >= n) continue;
+    if (rk[k] == 0) sc.slot[s[k] & kSlotMask] = ScratchSlot{kEncEmpty, 0xFFFFFFFFu, 0u};
+    if (OCC && a[k].long_idx >= 0) {
+      const int sh = a[k].unit_shift;
+      const int usz = kUnit << sh;
+      if ((rk[k] & (usz - 1)) == 0) {
+        const int p = a[k].start + rk[k];
+        w.units[w.long_start[a[k].long_idx] + (rk[k] >> (kUnitLog2 + sh))] =
+            Unit{a[k].long_idx, p, min(p + usz, a[k].start + a[k].count), 0};
+      }
+    }
+  }
+  if (i0 + 4 <= n) {
+    *reinterpret_cast<int4*>(w.inverse + i0) = make_int4(a[0].uid, a[1].uid, a[2].uid, a[3].uid);
+    if (OCC) {
+      *reinterpret_cast<longlong2*>(w.occ_row + i0) = make_longlong2(a[0].row, a[1].row);
+      *reinterpret_cast<longlong2*>(w.occ_row + i0 + 2) = make_longlong2(a[2].row, a[3].row);
+      *reinterpret_cast<int4*>(w.occ_pos + i0) =
+          make_int4(s[0] >= 0 ? a[0].start + rk[0] : -1, s[1] >= 0 ? a[1].start + rk[1] : -1,
+                    s[2] >= 0 ? a[2].start + rk[2] : -1, s[3] >= 0 ? a[3].start + rk[3] : -1);
+    }
+  } else {
+    for (int k = 0; k < 4 && i0 + k < n; ++k) {
+      w.inverse[i0 + k] = a[k].uid;
+      if (OCC) {
+        w.occ_row[i0 + k] = a[k].row;
+        w.occ_pos[i0 + k] = s[k] >= 0 ? a[k].start + rk[k] : -1;
+      }
+    }
+  }
+}
+
+hipError_t launch_compact_insert(const int64_t* values, int64_t n, const Scratch& sc, const TableDev& t, const Work& w,
+                                 bool occ_lists, hipEvent_t* ev_compact, hipEvent_t* ev_init, hipEvent_t* ev_occ,
+                                 hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t nb = (n + kRankTile - 1) / kRankTile;
+  if (ev_compact && ev_compact[0]) (void)hipEventRecord(ev_compact[0], s);
+  k_compact_insert<<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, sc, w, values, n);
+  if (ev_compact && ev_compact[1]) (void)hipEventRecord(ev_compact[1], s);
+  if (ev_init && ev_init[0]) (void)hipEventRecord(ev_init[0], s);
+  k_init_rows<<<grid_for(n, kBlock / 16, 8192), kBlock, 0, s>>>(t, w);
+  if (ev_init && ev_init[1]) (void)hipEventRecord(ev_init[1], s);
+  if (ev_occ && ev_occ[0]) (void)hipEventRecord(ev_occ[0], s);
+  if (occ_lists) k_occ<true><<<grid_for(n, kBlock * 4, 1ll << 31), kBlock, 0, s>>>(sc, w, n);
+  else k_occ<false><<<grid_for(n, kBlock * 4, 1ll << 31), kBlock, 0, s>>>(sc, w, n);
+  if (ev_occ && ev_occ[1]) (void)hipEventRecord(ev_occ[1], s);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// find-or-insert results, find-only lookups, rehash, export, read-back
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kBlock) void k_map_rows(const int32_t* __restrict__ inverse, const int64_t* __restrict__ rows,
+                                                     int64_t n, int64_t* __restrict__ out, const int64_t* cscal,
+                                                     int64_t* n_inserted) {
+  const int64_t i = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  if (i == 0 && n_inserted) *n_inserted = cscal[kCNew];
+  if (i < n) {
+    const int u = inverse[i];
+    out[i] = u >= 0 ? rows[u] : -1;
+  }
+}
+
+hipError_t launch_map_rows(const Work& w, int64_t n, int64_t* rows_out, int64_t* n_inserted, hipStream_t s) {
+  k_map_rows<<<grid_for(n, kBlock, 1ll << 31), kBlock, 0, s>>>(w.inverse, w.rows, n, rows_out, w.scal, n_inserted);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(kBlock) void k_find(TableDev t, const int64_t* __restrict__ keys, int64_t n,
+                                                 int64_t* __restrict__ out) {
+  for (int64_t i = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const unsigned long long e = static_cast<unsigned long long>(keys[i]) ^ kSign;
+    out[i] = e <= kEncTomb ? -1 : idmap_lookup(t, e);
+  }
+}
+
+hipError_t launch_find(const TableDev& t, const int64_t* keys, int64_t n, int64_t* rows_out, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  k_find<<<grid_for(n, kBlock, 16384), kBlock, 0, s>>>(t, keys, n, rows_out);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(kBlock) void k_rehash(const Slot* __restrict__ old, int64_t old_cap, TableDev t) {
+  for (int64_t i = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x; i < old_cap;
+       i += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const Slot sl = old[i];
+    if (sl.key <= kEncTomb) continue;
+    const int64_t slot = idmap_claim(t, sl.key);
+    if (slot >= 0) t.slots[slot].row = sl.row;
+    else atomicOr(reinterpret_cast<int*>(&t.scal[kTErr]), kErrProbe);
+  }
+}
+
+hipError_t launch_rehash(const Slot* old_slots, int64_t old_cap, const TableDev& t, hipStream_t s) {
+  k_rehash<<<grid_for(old_cap, kBlock, 65536), kBlock, 0, s>>>(old_slots, old_cap, t);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(kBlock) void k_export(TableDev t, int64_t cap_slots, int64_t* __restrict__ keys,
+                                                   int64_t* __restrict__ rows, int64_t cap, unsigned long long* counter) {
+  for (int64_t i = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x; i < cap_slots;
+       i += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const Slot sl = t.slots[i];
+    if (sl.key <= kEncTomb) continue;
+    const unsigned long long k = atomicAdd(counter, 1ull);
+    if (static_cast<int64_t>(k) < cap) {
+      keys[k] = static_cast<int64_t>(sl.key ^ kSign);
+      rows[k] = sl.row;
+    }
+  }
+}
+
+__global__ void k_copy_scalar(const int64_t* src, int64_t* dst) { *dst = *src; }
+
+hipError_t launch_export(const TableDev& t, int64_t cap_slots, int64_t* keys, int64_t* rows, int64_t cap,
+                         int64_t* n_dev, hipStream_t s) {
+  (void)hipMemsetAsync(&t.scal[kTExport], 0, sizeof(int64_t), s);
+  k_export<<<grid_for(cap_slots, kBlock, 65536), kBlock, 0, s>>>(
+      t, cap_slots, keys, rows, cap, reinterpret_cast<unsigned long long*>(&t.scal[kTExport]));
+  if (n_dev) k_copy_scalar<<<1, 1, 0, s>>>(&t.scal[kTExport], n_dev);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(kBlock) void k_read_rows(TableDev t, const int64_t* __restrict__ rows, int64_t n,
+                                                      float* __restrict__ w_out, float* __restrict__ state_out) {
+  const int64_t live = t.scal[kTLive];
+  const int64_t total = n * t.dim;
+  for (int64_t idx = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x; idx < total;
+       idx += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const int64_t i = idx / t.dim;
+    const int j = static_cast<int>(idx % t.dim);
+    const int64_t r = rows[i];
+    const bool ok = r >= 0 && r < live;
+    const uint8_t* rp = ok ? t.store.row(r) : nullptr;
+    if (w_out) {
+      float v = __builtin_nanf("");
+      if (ok) v = t.row_dtype ? bf16_to_f32(reinterpret_cast<const uint16_t*>(rp)[j]) : reinterpret_cast<const float*>(rp)[j];
+      w_out[idx] = v;
+    }
+    if (state_out) {
+      const float* sp = ok ? reinterpret_cast<const float*>(rp + static_cast<int64_t>(t.dim) * (t.row_dtype ? 2 : 4)) : nullptr;
+      for (int q = 0; q < t.nstate; ++q) state_out[(i * t.nstate + q) * t.dim + j] = ok ? sp[q * t.dim + j] : __builtin_nanf("");
+    }
+  }
+}
+
+hipError_t launch_read_rows(const TableDev& t, const int64_t* rows, int64_t n, float* w_out, float* state_out,
+                            hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  k_read_rows<<<grid_for(n * t.dim, kBlock, 65536), kBlock, 0, s>>>(t, rows, n, w_out, state_out);
+  return hipGetLastError();
+}
+
+}  // namespace rs

@@ -1,0 +1,187 @@
+// Forward gather + pool kernels of the sparse embedding step (gfx950).
+//
+// RecIS forward workflow: one IDMap lookup per id gives the offset, the row
+// is read at that offset and the rows of a bag are reduced (sum, mean) or
+// copied into a padded sequence ("Forward Pass", "Reduction Operations",
+// "Gather").  The lookup happened in the dedup passes, which also gave every
+// occurrence its row (occ_row) and its position in the occurrence list
+// (occ_pos); these kernels read each occurrence's row with 16-byte vector
+// loads, one lane group of D*sizeof(row)/16 lanes per row, and write the
+// gradient row each position of the occurrence list will read (occ_ref).
+//
+// A lane group handles kBags bags at once: their load chains (offsets ->
+// occurrence row -> row data) are interleaved so a wavefront keeps
+// 4 x (64 / lanes) rows in flight even for single-id bags.
+#include "device_common.h"
+
+namespace rs {
+
+constexpr int kBags = 4;
+
+template <typename WT, int LANES, int MODE>
+__global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64_t* __restrict__ offsets, int64_t n,
+                                                 int64_t bags, float* __restrict__ out) {
+  constexpr int E = 16 / static_cast<int>(sizeof(WT));
+  constexpr int D = LANES * E;
+  constexpr int GPB = kBlock / LANES;
+  const int lane = threadIdx.x % LANES;
+  const int grp = threadIdx.x / LANES;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * GPB * kBags;
+  for (int64_t g0 = (static_cast<int64_t>(blockIdx.x) * GPB + grp) * kBags; g0 < bags; g0 += stride) {
+    int64_t b[kBags], e[kBags];
+    int64_t maxlen = 0;
+#pragma unroll
+    for (int q = 0; q < kBags; ++q) {
+      // CSR bounds clamped to [0, n]: malformed offsets cannot read out of range
+      const bool ok = g0 + q < bags;
+      b[q] = ok ? min(max(offsets[g0 + q], int64_t(0)), n) : 0;
+      e[q] = ok ? min(max(offsets[g0 + q + 1], b[q]), n) : 0;
+      maxlen = max(maxlen, e[q] - b[q]);
+    }
+    float acc[kBags][E];
+#pragma unroll
+    for (int q = 0; q < kBags; ++q)
+#pragma unroll
+      for (int k = 0; k < E; ++k) acc[q][k] = 0.f;
+    for (int64_t tt = 0; tt < maxlen; ++tt) {
+      int64_t r[kBags];
+      int pos[kBags];
+#pragma unroll
+      for (int q = 0; q < kBags; ++q) {
+        const bool act = b[q] + tt < e[q];
+        r[q] = act ? w.occ_row[b[q] + tt] : -1;
+        pos[q] = act ? w.occ_pos[b[q] + tt] : -1;
+      }
+      float x[kBags][E];
+#pragma unroll
+      for (int q = 0; q < kBags; ++q) {
+        if (r[q] >= 0) {
+          load_vals<WT, E>(reinterpret_cast<const WT*>(t.store.row(r[q])) + lane * E, x[q]);
+        } else {
+#pragma unroll
+          for (int k = 0; k < E; ++k) x[q][k] = 0.f;
+        }
+      }
+      if (lane == 0) {
+        // the occurrence's place in its key's segment of the occurrence list
+        // receives the gradient row it will read in the backward
+#pragma unroll
+        for (int q = 0; q < kBags; ++q)
+          if (pos[q] >= 0) w.occ_ref[pos[q]] = static_cast<int>(g0 + q);
+      }
+#pragma unroll
+      for (int q = 0; q < kBags; ++q)
+#pragma unroll
+        for (int k = 0; k < E; ++k) acc[q][k] += x[q][k];
+    }
+#pragma unroll
+    for (int q = 0; q < kBags; ++q) {
+      if (g0 + q >= bags) continue;
+      if (MODE == 1 && e[q] > b[q]) {
+        const float len = static_cast<float>(e[q] - b[q]);
+#pragma unroll
+        for (int k = 0; k < E; ++k) acc[q][k] = acc[q][k] / len;
+      }
+      store_vals<float, E>(out + (g0 + q) * D + lane * E, acc[q]);
+    }
+  }
+}
+
+// Padded copy: block = (bag, TCH positions); a lane group copies TCH / groups
+// positions, with their loads issued together.
+template <typename WT, int LANES>
+__global__ __launch_bounds__(kBlock) void k_pool_none(TableDev t, Work w, const int64_t* __restrict__ offsets,
+                                                      int64_t n, int64_t bags, int64_t L, WT* __restrict__ out,
+                                                      uint8_t* __restrict__ mask) {
+  constexpr int E = 16 / static_cast<int>(sizeof(WT));
+  constexpr int D = LANES * E;
+  constexpr int GPB = kBlock / LANES;
+  constexpr int TCH = GPB > 64 ? GPB : 64;  // positions per block
+  constexpr int K = TCH / GPB;               // positions per lane group
+  const int lane = threadIdx.x % LANES;
+  const int grp = threadIdx.x / LANES;
+  const int64_t nch = (L + TCH - 1) / TCH;
+  for (int64_t blk = blockIdx.x; blk < bags * nch; blk += gridDim.x) {
+    const int64_t g = blk / nch, c = blk % nch;
+    const int64_t b = min(max(offsets[g], int64_t(0)), n);
+    const int64_t len = min(max(offsets[g + 1], b), n) - b;
+    int64_t tp[K], r[K];
+    int pos[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      tp[k] = c * TCH + grp + k * GPB;
+      const bool act = tp[k] < L && tp[k] < len;
+      r[k] = act ? w.occ_row[b + tp[k]] : -1;
+      pos[k] = act ? w.occ_pos[b + tp[k]] : -1;
+    }
+    uint4 v[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+      v[k] = r[k] >= 0 ? *reinterpret_cast<const uint4*>(reinterpret_cast<const WT*>(t.store.row(r[k])) + lane * E)
+                       : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      if (tp[k] >= L) continue;
+      *reinterpret_cast<uint4*>(out + (g * L + tp[k]) * D + lane * E) = v[k];
+      if (lane == 0) {
+        mask[g * L + tp[k]] = tp[k] < len ? 1 : 0;
+        if (pos[k] >= 0) w.occ_ref[pos[k]] = static_cast<int>(g * L + tp[k]);
+      }
+    }
+    if (c == 0 && lane == 0) {
+      // ids past pad_len: in the occurrence list (the key is touched) but
+      // without a gradient row
+      for (int64_t tpos = L + grp; tpos < len; tpos += GPB) {
+        const int pp = w.occ_pos[b + tpos];
+        if (pp >= 0) w.occ_ref[pp] = -1;
+      }
+    }
+  }
+}
+
+template <typename WT, int LANES>
+static hipError_t pool_mode(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int64_t bags,
+                            int mode, int64_t pad_len, void* out, uint8_t* mask, hipStream_t s) {
+  constexpr int GPB = kBlock / LANES;
+  if (mode == 2) {
+    constexpr int TCH = GPB > 64 ? GPB : 64;
+    const int64_t nch = (pad_len + TCH - 1) / TCH;
+    k_pool_none<WT, LANES><<<grid_for(bags * nch, 1, 1 << 20), kBlock, 0, s>>>(t, w, offsets, n, bags, pad_len,
+                                                                             static_cast<WT*>(out), mask);
+  } else if (mode == 1) {
+    k_pool<WT, LANES, 1><<<grid_for(bags, GPB * kBags, 1 << 20), kBlock, 0, s>>>(t, w, offsets, n, bags,
+                                                                                 static_cast<float*>(out));
+  } else {
+    k_pool<WT, LANES, 0><<<grid_for(bags, GPB * kBags, 1 << 20), kBlock, 0, s>>>(t, w, offsets, n, bags,
+                                                                                 static_cast<float*>(out));
+  }
+  return hipGetLastError();
+}
+
+template <typename WT>
+static hipError_t pool_dim(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int64_t bags, int mode,
+                           int64_t pad_len, void* out, uint8_t* mask, hipStream_t s) {
+  constexpr int E = 16 / static_cast<int>(sizeof(WT));
+  switch (t.dim / E) {
+    case 1: return pool_mode<WT, 1>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
+    case 2: return pool_mode<WT, 2>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
+    case 4: return pool_mode<WT, 4>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
+    case 8: return pool_mode<WT, 8>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
+    case 16: return pool_mode<WT, 16>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
+    case 32: return pool_mode<WT, 32>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
+    case 64: return pool_mode<WT, 64>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_pool(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int64_t bags, int mode,
+                       int64_t pad_len, void* out, uint8_t* mask, hipEvent_t* ev, hipStream_t s) {
+  if (bags <= 0) return hipSuccess;
+  if (ev && ev[0]) (void)hipEventRecord(ev[0], s);
+  const hipError_t e = t.row_dtype ? pool_dim<uint16_t>(t, w, offsets, n, bags, mode, pad_len, out, mask, s)
+                                   : pool_dim<float>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
+  if (ev && ev[1]) (void)hipEventRecord(ev[1], s);
+  return e;
+}
+
+}  // namespace rs

@@ -1,6 +1,6 @@
-// Internal declarations shared by the kernels (kernels.hip) and the C ABI
-// host code (api.hip).  gfx950 / CDNA4 only: 64-lane wavefronts, 256-thread
-// blocks, 16-byte vector memory operations.
+// Internal declarations shared by the kernels and the C ABI host code.
+// gfx950 / CDNA4 only: 64-lane wavefronts, 256-thread blocks, 16-byte vector
+// memory operations.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -8,7 +8,7 @@
 
 namespace rs {
 
-constexpr int kBlock = 256;                  // threads per block (4 waves)
+constexpr int kBlock = 256;  // threads per block (4 waves)
 constexpr int kWave = 64;
 constexpr uint64_t kSign = 0x8000000000000000ull;
 
@@ -24,15 +24,26 @@ constexpr int kDedupItems = 4;
 constexpr int kDedupTile = kBlock * kDedupItems;  // 1024 occurrences
 constexpr int kDedupLdsSlots = 2 * kDedupTile;    // load <= 0.5
 
-// Block-tile scans: 8 consecutive items per thread.
-constexpr int kScanItems = 8;
-constexpr int kScanTile = kBlock * kScanItems;    // 2048
+// Tile of the two passes that rank first occurrences (4 consecutive items
+// per thread: many resident waves for these latency-bound passes).
+constexpr int kRankItems = 4;
+constexpr int kRankTile = kBlock * kRankItems;  // 1024
 
-// Backward: the occurrence list (sorted by unique id) is cut into chunks of
-// kChunk positions; a lane group reduces one chunk.
-constexpr int kChunk = 32;
+// Open addressing with linear probing; a lookup reads kProbeBatch
+// consecutive IDMap slots (64 bytes) per round trip.
+constexpr int kProbeBatch = 4;
 
-constexpr int kMaxBlocks = 1 << 16;               // Blocks chunks per table
+// Backward: a key with at most kLong occurrences is reduced by one lane
+// group; a longer ("hot") key is cut into units of kUnit positions whose
+// partial sums are added into a per-key partial row.
+constexpr int kLong = 32;
+constexpr int kUnit = 32;
+constexpr int kUnitLog2 = 5;
+static_assert(kUnit == 1 << kUnitLog2, "kUnit is a power of two");
+// A key with more than kUnit * kMaxUnits occurrences gets units of
+// kUnit << shift positions, so no partial row receives more than kMaxUnits
+// atomic adds per element.
+constexpr int kMaxUnits = 64;
 
 // Latched device error bits.
 enum : int { kErrKey = 1, kErrFull = 2, kErrScratch = 4, kErrProbe = 8 };
@@ -40,7 +51,17 @@ enum : int { kErrKey = 1, kErrFull = 2, kErrScratch = 4, kErrProbe = 8 };
 // Table-resident device scalars.
 enum : int { kTLive = 0, kTLimit = 1, kTRowCap = 2, kTErr = 3, kTExport = 4, kTScalars = 8 };
 // Per-call (context) device scalars.
-enum : int { kCU = 0, kCNew = 1, kCValid = 2, kCBaseLive = 3, kCScalars = 4 };
+enum : int {
+  kCU = 0,         // unique keys
+  kCNew = 1,       // keys inserted
+  kCValid = 2,     // occurrences kept (= sum of per-key counts)
+  kCBaseLive = 3,  // live rows before the insert
+  kCNewReq = 4,    // keys not found (inserted if room)
+  kCNLong = 5,     // keys with more than kLong occurrences
+  kCNUnits = 6,    // backward units of those keys
+  kCTrunc = 7,     // 1 if some keys not found had no room (latched as RS_EFULL)
+  kCScalars = 8
+};
 
 __host__ __device__ inline uint64_t mix64(uint64_t z) {
   z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
@@ -48,7 +69,7 @@ __host__ __device__ inline uint64_t mix64(uint64_t z) {
   return z ^ (z >> 31);
 }
 
-// Slot hash of the IDMap and of the dedup scratch (different salts).
+// Bucket hashes of the IDMap and of the dedup scratch (different salts).
 __device__ inline uint64_t idmap_hash(unsigned long long e) { return mix64(e ^ 0x2545F4914F6CDD1Dull); }
 __device__ inline uint64_t scratch_hash(unsigned long long e) { return mix64(e ^ 0x5BD1E9955BD1E995ull); }
 
@@ -57,21 +78,18 @@ struct alignas(16) Slot {
   long long row;
 };
 
-// Blocks: rows live in fixed-size chunks that never move; a row is
+// Blocks: physical chunks mapped back to back into one reserved virtual
+// range, so rows never move and row r is at base + r * stride; a row is
 // [w: D x row dtype | state0: D x fp32 | state1: D x fp32 (Adam)].
 struct RowStore {
-  uint8_t* const* blocks;  // device array of chunk base pointers
-  int shift;               // log2(block_rows)
-  int64_t mask;            // block_rows - 1
-  int64_t stride;          // bytes per row
-  __device__ inline uint8_t* row(int64_t r) const {
-    return blocks[r >> shift] + (r & mask) * stride;
-  }
+  uint8_t* base;
+  int64_t stride;  // bytes per row
+  __device__ inline uint8_t* row(int64_t r) const { return base + r * stride; }
 };
 
 struct TableDev {
   Slot* slots;
-  uint64_t cap_mask;
+  uint64_t cap_mask;  // slots - 1 (linear probing, slot granularity)
   RowStore store;
   int64_t* scal;  // kT* scalars
   int dim;
@@ -81,30 +99,65 @@ struct TableDev {
   float lo, span;  // init: fma(u, span, lo)
 };
 
+// Per-table dedup scratch: an open-addressing set of one call's keys, as two
+// arrays of structs so that every pass touches one cache sector per key.
+struct alignas(16) ScratchSlot {
+  unsigned long long key;  // encoded key (0: empty)
+  unsigned int first;      // first position of the key in the batch
+  unsigned int cnt;        // occurrences of the key
+};
+struct alignas(32) ScratchAux {
+  long long row;  // IDMap row (found by the probe pass, or assigned)
+  int start;      // first position of the key's segment of the occurrence list
+  int uid;        // unique id (first-occurrence order)
+  int count;      // occurrences
+  int long_idx;   // hot-key index, -1 if count <= kLong
+  int unit_shift; // hot key: backward units of kUnit << unit_shift positions
+  int pad;
+};
 struct Scratch {
-  unsigned long long* key;
-  unsigned int* first;
-  unsigned int* cnt;
-  int32_t* uid;
-  uint64_t mask;
+  ScratchSlot* slot;
+  ScratchAux* aux;
+  uint64_t mask;  // slots - 1
+};
+
+// slot_of[i]: scratch slot of occurrence i; kCandBit marks the occurrence at
+// its tile's first position of the key (only those can be the key's first
+// occurrence in the batch); -1 for a rejected key.
+constexpr int kCandBit = 1 << 30;
+constexpr int kSlotMask = kCandBit - 1;
+
+// Per-unique segment descriptor: the key's row, and where its occurrences
+// start in the occurrence list and how many there are.
+struct alignas(16) Seg {
+  long long row;
+  int start, count;
+};
+
+// Backward unit of a hot key: gradient-list positions [p0, p1), partial row li.
+struct alignas(16) Unit {
+  int li, p0, p1, pad;
 };
 
 // Workspace arrays of one forward (and its backward).
 struct Work {
-  int32_t* slot_of;   // [n] scratch slot per occurrence
-  int32_t* occ_rank;  // [n] rank of the occurrence among those of its key
-  int32_t* inverse;   // [n]
-  int64_t* unique;    // [n]
-  int32_t* uslot;     // [n] scratch slot per unique
-  int32_t* ucount;    // [n] occurrences per unique
-  int32_t* seg;       // [n+1] exclusive scan of ucount
-  int64_t* rows;      // [n]
-  int32_t* isnew;     // [n]
-  int32_t* occ_ref;   // [n] grad row of each position of the occurrence list
-  int32_t* chunk_u;   // [n/kChunk + 1] unique id at the start of each chunk
-  int32_t* bsum;      // [n/kScanTile + 2] tile sums
-  int64_t* scal;      // [kCScalars]
-  float* gpart;       // [(n/kChunk + 1) * D] partial sums of segments crossing chunks
+  int32_t* slot_of;     // [n] scratch slot per occurrence (| kCandBit)
+  int32_t* occ_rank;    // [n] rank of the occurrence among those of its key
+  int32_t* inverse;     // [n]
+  int64_t* occ_row;     // [n] Blocks row of each occurrence (-1: none)
+  int32_t* occ_pos;     // [n] position of each occurrence in the occurrence list
+  int64_t* unique;      // [n]
+  Seg* useg;            // [n]
+  int64_t* rows;        // [n]
+  int32_t* new_list;    // [n] unique id of the k-th inserted key
+  int32_t* occ_ref;     // [n] gradient row of each position of the occurrence list
+  int32_t* long_u;      // [n/kLong + 1] unique id of each hot key
+  int32_t* long_start;  // [n/kLong + 1] first backward unit of each hot key
+  Unit* units;          // [2n/kUnit + 2] backward units of the hot keys
+  int32_t* bsum;        // [3 * ntiles] tile sums: first occurrences, their counts, new keys
+  int64_t* scal;        // [kCScalars]
+  float* gpart;         // [(n/kLong + 1) * D] partial gradient rows of hot keys
+  int64_t ntiles;       // tiles of the rank passes (bsum stride)
 };
 
 struct OptArgs {
@@ -113,34 +166,34 @@ struct OptArgs {
 };
 
 // ---------------------------------------------------------------------------
-// launchers (kernels.hip); all enqueue on `s` and return hipGetLastError()
+// launchers; all enqueue on `s` and return hipGetLastError()
 // ---------------------------------------------------------------------------
-hipError_t launch_fill_u64(unsigned long long* p, unsigned long long v, int64_t n, hipStream_t s);
-
-hipError_t launch_dedup(const int64_t* values, int64_t n, const Scratch& sc, const Work& w,
-                        int* err, hipEvent_t* ev_local, hipEvent_t* ev_compact, hipStream_t s);
-hipError_t launch_seg_scan(const Work& w, int64_t nmax, const Scratch& sc, int dim, hipStream_t s);
-hipError_t launch_idmap_probe(const TableDev& t, const Work& w, int64_t nmax, hipEvent_t* ev,
-                              hipStream_t s);
-hipError_t launch_idmap_insert(const TableDev& t, const Work& w, int64_t nmax, hipEvent_t* ev,
-                               hipStream_t s);
-hipError_t launch_map_rows(const Work& w, int64_t n, int64_t* rows_out, int64_t* n_inserted,
-                           hipStream_t s);
-hipError_t launch_find(const TableDev& t, const int64_t* keys, int64_t n, int64_t* rows_out,
-                       hipStream_t s);
-hipError_t launch_pool(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int64_t bags,
-                       int mode, int64_t pad_len, void* out, uint8_t* mask, hipEvent_t* ev,
-                       hipStream_t s);
-hipError_t launch_bwd(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n,
-                      int64_t bags, int mode, int64_t pad_len, const void* grad, float* grad_unique,
-                      const OptArgs* opt, hipEvent_t* ev_chunks, hipEvent_t* ev_straddle,
-                      hipStream_t s);
-hipError_t launch_opt(const TableDev& t, const Work& w, int64_t n, const float* grad_unique,
-                      const OptArgs& opt, hipEvent_t* ev, hipStream_t s);
+// dedup + IDMap probe of first occurrences + 3-way scan (ends before the insert)
+hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const Scratch& sc, const TableDev& t,
+                              const Work& w, hipEvent_t* ev_local, hipEvent_t* ev_probe, hipStream_t s);
+// unique / segments / rows / IDMap insert / row init, then the per-occurrence
+// pass: inverse[], scratch release and, for a forward (occ_lists), each
+// occurrence's row and list position and the hot keys' backward units
+hipError_t launch_compact_insert(const int64_t* values, int64_t n, const Scratch& sc, const TableDev& t,
+                                 const Work& w, bool occ_lists, hipEvent_t* ev_compact, hipEvent_t* ev_init,
+                                 hipEvent_t* ev_occ, hipStream_t s);
+// set every scratch slot to empty
+hipError_t launch_scratch_clear(ScratchSlot* slots, int64_t n, hipStream_t s);
+// redo the row reservation of the last scan after the table has grown
+hipError_t launch_rereserve(const Work& w, const TableDev& t, hipStream_t s);
+hipError_t launch_map_rows(const Work& w, int64_t n, int64_t* rows_out, int64_t* n_inserted, hipStream_t s);
+hipError_t launch_find(const TableDev& t, const int64_t* keys, int64_t n, int64_t* rows_out, hipStream_t s);
+hipError_t launch_pool(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int64_t bags, int mode,
+                       int64_t pad_len, void* out, uint8_t* mask, hipEvent_t* ev, hipStream_t s);
+hipError_t launch_bwd(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int mode,
+                      const void* grad, float* grad_unique, const OptArgs* opt, hipEvent_t* ev_short,
+                      hipEvent_t* ev_long, hipStream_t s);
+hipError_t launch_opt(const TableDev& t, const Work& w, int64_t n, const float* grad_unique, const OptArgs& opt,
+                      hipEvent_t* ev, hipStream_t s);
 hipError_t launch_rehash(const Slot* old_slots, int64_t old_cap, const TableDev& t, hipStream_t s);
-hipError_t launch_export(const TableDev& t, int64_t cap_slots, int64_t* keys, int64_t* rows,
-                         int64_t cap, int64_t* n_dev, hipStream_t s);
-hipError_t launch_read_rows(const TableDev& t, const int64_t* rows, int64_t n, float* w_out,
-                            float* state_out, hipStream_t s);
+hipError_t launch_export(const TableDev& t, int64_t cap_slots, int64_t* keys, int64_t* rows, int64_t cap,
+                         int64_t* n_dev, hipStream_t s);
+hipError_t launch_read_rows(const TableDev& t, const int64_t* rows, int64_t n, float* w_out, float* state_out,
+                            hipStream_t s);
 
 }  // namespace rs

@@ -24,8 +24,8 @@ STATUS_NAMES = {0: "RS_OK", 1: "RS_EINVAL", 2: "RS_ENOMEM", 3: "RS_EFULL", 4: "R
 SUM, MEAN, NONE = 0, 1, 2
 F32, BF16 = 0, 1
 ADAGRAD, ADAM = 0, 1
-KERNELS = {"dedup_local": 0, "dedup_compact": 1, "idmap_probe": 2, "idmap_insert": 3, "pool": 4,
-           "bwd_chunks": 5, "bwd_straddle": 6, "opt": 7}
+KERNELS = {"dedup_local": 0, "rank_probe": 1, "compact_insert": 2, "init_rows": 3, "pool": 4,
+           "bwd_short": 5, "bwd_long": 6, "opt": 7, "occ": 8}
 
 
 class RecisError(RuntimeError):
