@@ -64,9 +64,13 @@ def copy_calibration():
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "ms": ms, "GBps": 2 * n / (ms * 1e-3) / 1e9}))
 
 
-def kernel_source_hash() -> str:
+KERNEL_SOURCES = {"pool": "pool.hip", "bwd_short": "backward.hip"}
+
+
+def kernel_source_hash(kernel: str) -> str:
+    """Hash of the sources a kernel is built from (its file + the shared headers)."""
     h = hashlib.sha256()
-    for f in ("dedup_idmap.hip", "pool.hip", "backward.hip", "api.hip", "rs_internal.h", "device_common.h"):
+    for f in (KERNEL_SOURCES[kernel], "rs_internal.h", "device_common.h"):
         with open(os.path.join(ROOT, "paper_2509_20883_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -279,7 +283,7 @@ def main():
     if os.path.exists(tpath):
         with open(tpath) as fh:
             tj = json.load(fh)
-        if tj.get("kernel_source_hash") == kernel_source_hash():
+        if tj.get("kernel_source_hash") == kernel_source_hash(dom):
             traffic = tj.get("bytes_per_launch")
 
     res = {
