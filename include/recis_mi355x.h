@@ -139,7 +139,7 @@ rs_status ht_create(const rs_table_desc* desc, const rs_allocator* alloc, rs_str
 rs_status ht_destroy(rs_table* t);
 
 /* IDMap find-or-insert (the KV store inserts a feature the first time it is
- * seen).  keys: [n] int64, duplicates allowed.  rows_out: [n] int64, the row
+ * seen).  keys: [n] int64 (n <= 2^28), duplicates allowed.  rows_out: [n] int64, the row
  * of each key (equal keys get equal rows; -1 for a key that did not fit).
  * A missing key gets the next free row — new rows are numbered live, live+1,
  * ... in the first-occurrence order of the new keys — and its row is
@@ -187,7 +187,7 @@ rs_status ht_reserve(rs_table* t, int64_t live_upper_bound, rs_stream stream);
 size_t lookup_workspace_bytes(int64_t n, int64_t bags, int64_t pad_len, const rs_table* t);
 
 /* Forward: dedup + find-or-insert + fused gather/pool.
- * values [n] int64, offsets [bags+1] int64 (CSR: offsets[0] = 0,
+ * values [n] int64 (n <= 2^28), offsets [bags+1] int64 (CSR: offsets[0] = 0,
  * nondecreasing, offsets[bags] = n; bag g = feature-major f*B + b).
  *  RS_POOL_SUM : out fp32 [bags, D], out[g] = sum of the rows of bag g
  *  RS_POOL_MEAN: out fp32 [bags, D], the sum divided by the bag length; an
@@ -203,6 +203,26 @@ size_t lookup_workspace_bytes(int64_t n, int64_t bags, int64_t pad_len, const rs
 rs_status lookup_pool_fwd(rs_table* t, const int64_t* values, const int64_t* offsets, int64_t n,
                           int64_t bags, int32_t mode, int64_t pad_len, void* out, uint8_t* mask,
                           rs_ctx* ctx, int32_t validate, rs_stream stream);
+
+/* The forward in two halves, for callers that overlap the next batch's id
+ * processing with the current batch's pool and backward on a second stream.
+ *
+ * lookup_prepare: everything of lookup_pool_fwd except the gather + pool:
+ * dedup, IDMap find-or-insert, row init of new keys, and the per-occurrence
+ * bookkeeping, into ctx (same arguments and errors as lookup_pool_fwd
+ * minus out / mask).  It reads and writes only the IDMap, the table's dedup
+ * scratch, the rows of the keys it inserts and ctx -- never a row that
+ * already existed -- so it may run while an earlier batch's
+ * lookup_pool_prepared / backward / optimizer are still running on another
+ * stream.  Prepares of one table must be issued in order on one stream.
+ *
+ * lookup_pool_prepared: the gather + pool of a prepared ctx.  The caller
+ * orders it after the prepare (same stream, or an event) and after the
+ * optimizer of every earlier batch (whose updates it must read).
+ * lookup_pool_fwd = lookup_prepare + lookup_pool_prepared on one stream. */
+rs_status lookup_prepare(rs_table* t, const int64_t* values, const int64_t* offsets, int64_t n, int64_t bags,
+                         int32_t mode, int64_t pad_len, rs_ctx* ctx, int32_t validate, rs_stream stream);
+rs_status lookup_pool_prepared(rs_table* t, rs_ctx* ctx, void* out, uint8_t* mask, rs_stream stream);
 
 /* Backward: per-unique gradient sums.  grad_out has the forward output's
  * shape: fp32 [bags, D] (sum, mean) or [bags, pad_len, D] in the row dtype

@@ -286,8 +286,9 @@ rs_status rehash(rs_table* t, int64_t new_cap, hipStream_t s) {
   return RS_OK;
 }
 
-// Grow (when allowed) so that `live_need` keys fit the IDMap and the Blocks.
-rs_status grow_for(rs_table* t, int64_t live_need, hipStream_t s) {
+// Grow (when allowed) so that `live_need` keys fit the IDMap and the Blocks;
+// `batch` (the ids of the call) sizes the Blocks headroom.
+rs_status grow_for(rs_table* t, int64_t live_need, int64_t batch, hipStream_t s) {
   if (t->d.auto_grow) {
     int64_t c = t->cap;
     while (static_cast<double>(live_need) > static_cast<double>(t->d.max_load) * static_cast<double>(c)) c <<= 1;
@@ -295,7 +296,9 @@ rs_status grow_for(rs_table* t, int64_t live_need, hipStream_t s) {
       rs_status st = rehash(t, c, s);
       if (st != RS_OK) return st;
     }
-    const int64_t headroom = live_need + live_need / 8 + t->d.block_rows;
+    // headroom: a quarter more rows and at least four batches' worth, so the
+    // host's upper bound on live rows rarely forces a synchronization
+    const int64_t headroom = live_need + std::max(live_need / 4, 4 * batch) + t->d.block_rows;
     return provision_rows(t, headroom, s);
   }
   return provision_rows(t, std::min(live_need, t->limit), s);
@@ -339,7 +342,7 @@ rs_status dedup_and_insert(rs_table* t, const int64_t* values, int64_t n, const 
     RS_HIP(hipMemcpy(&req, w.scal + kCNewReq, sizeof(int64_t), hipMemcpyDeviceToHost));
     RS_HIP(hipMemcpy(&live0, w.scal + kCBaseLive, sizeof(int64_t), hipMemcpyDeviceToHost));
     t->rb_pending = false;
-    st = grow_for(t, live0 + req, s);
+    st = grow_for(t, live0 + req, n, s);
     if (st != RS_OK) return st;
     // redo the reservation against the grown table
     RS_HIP(launch_rereserve(w, t->dev(), s));
@@ -377,6 +380,7 @@ OptArgs make_opt(rs_table* t, const rs_opt_params* p) {
 rs_status check_ctx(const rs_table* t, const rs_ctx* c) {
   if (!t || !c) return fail(RS_EINVAL, "null table or context");
   if (c->table != t) return fail(RS_EINVAL, "context was filled by a forward on another table");
+  if (c->priv[0] != 2) return fail(RS_EINVAL, "the context's forward has not been pooled");
   if (c->dim != t->d.dim) return fail(RS_EINVAL, "context dim mismatch");
   return RS_OK;
 }
@@ -499,7 +503,7 @@ size_t lookup_workspace_bytes(int64_t n, int64_t /*bags*/, int64_t /*pad_len*/, 
 rs_status ht_find_or_insert(rs_table* t, const int64_t* keys, int64_t n, int64_t* rows_out, int64_t* n_inserted_dev,
                             rs_stream stream) {
   if (!t) return fail(RS_EINVAL, "null table");
-  if (n < 0 || n > (int64_t(1) << 29)) return fail(RS_EINVAL, "n must be in [0, 2^29]");
+  if (n < 0 || n > (int64_t(1) << 28)) return fail(RS_EINVAL, "n must be in [0, 2^28]");
   if (n > 0 && (!keys || !rows_out)) return fail(RS_EINVAL, "null keys or rows_out");
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (n == 0) {
@@ -589,19 +593,17 @@ rs_status ht_reserve(rs_table* t, int64_t live_upper_bound, rs_stream stream) {
   return take_latched(t);
 }
 
-rs_status lookup_pool_fwd(rs_table* t, const int64_t* values, const int64_t* offsets, int64_t n, int64_t bags,
-                          int32_t mode, int64_t pad_len, void* out, uint8_t* mask, rs_ctx* ctx, int32_t validate,
-                          rs_stream stream) {
+rs_status lookup_prepare(rs_table* t, const int64_t* values, const int64_t* offsets, int64_t n, int64_t bags,
+                         int32_t mode, int64_t pad_len, rs_ctx* ctx, int32_t validate, rs_stream stream) {
   if (!t || !ctx) return fail(RS_EINVAL, "null table or context");
-  if (n < 0 || n > (int64_t(1) << 29)) return fail(RS_EINVAL, "n must be in [0, 2^29]");
+  if (n < 0 || n > (int64_t(1) << 28)) return fail(RS_EINVAL, "n must be in [0, 2^28]");
   if (bags < 0 || bags >= (int64_t(1) << 31)) return fail(RS_EINVAL, "bags must be in [0, 2^31)");
   if (mode != RS_POOL_SUM && mode != RS_POOL_MEAN && mode != RS_POOL_NONE) return fail(RS_EINVAL, "bad pooling mode");
   if (mode == RS_POOL_NONE) {
     if (pad_len <= 0) return fail(RS_EINVAL, "pad_len must be > 0 for RS_POOL_NONE");
     if (bags * pad_len >= (int64_t(1) << 31)) return fail(RS_EINVAL, "bags * pad_len must be < 2^31");
-    if (bags > 0 && !mask) return fail(RS_EINVAL, "null mask");
   }
-  if (!offsets || (n > 0 && !values) || (bags > 0 && !out)) return fail(RS_EINVAL, "null input or output");
+  if (!offsets || (n > 0 && !values)) return fail(RS_EINVAL, "null input");
   const Layout L = make_layout(n, t->d.dim);
   if (!ctx->workspace || ctx->workspace_bytes < L.total) return fail(RS_EINVAL, "workspace missing or too small");
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -614,7 +616,8 @@ rs_status lookup_pool_fwd(rs_table* t, const int64_t* values, const int64_t* off
       if (h[g + 1] < h[g]) return fail(RS_EINVAL, "offsets must be nondecreasing");
   }
   const Work w = make_work(ctx->workspace, L);
-  ctx->table = nullptr;  // published only once the forward has been enqueued
+  ctx->table = nullptr;  // published only once the work has been enqueued
+  ctx->priv[0] = 0;      // 1: prepared, 2: pooled
   ctx->unique = w.unique;
   ctx->inverse = w.inverse;
   ctx->rows = w.rows;
@@ -627,9 +630,31 @@ rs_status lookup_pool_fwd(rs_table* t, const int64_t* values, const int64_t* off
   ctx->dim = t->d.dim;
   rs_status st = dedup_and_insert(t, values, n, w, true, s);
   if (st != RS_OK) return st;
-  RS_HIP(launch_pool(t->dev(), w, offsets, n, bags, mode, ctx->pad_len, out, mask, t->ev(RS_K_POOL), s));
+  ctx->priv[0] = 1;
   ctx->table = t;
   return RS_OK;
+}
+
+rs_status lookup_pool_prepared(rs_table* t, rs_ctx* ctx, void* out, uint8_t* mask, rs_stream stream) {
+  if (!t || !ctx) return fail(RS_EINVAL, "null table or context");
+  if (ctx->table != t || ctx->priv[0] < 1) return fail(RS_EINVAL, "context was not prepared on this table");
+  if (ctx->bags > 0 && !out) return fail(RS_EINVAL, "null output");
+  if (ctx->mode == RS_POOL_NONE && ctx->bags > 0 && !mask) return fail(RS_EINVAL, "null mask");
+  const Work w = ctx_work(ctx);
+  RS_HIP(launch_pool(t->dev(), w, ctx->offsets, ctx->n, ctx->bags, ctx->mode, ctx->pad_len, out, mask,
+                     t->ev(RS_K_POOL), static_cast<hipStream_t>(stream)));
+  ctx->priv[0] = 2;
+  return RS_OK;
+}
+
+rs_status lookup_pool_fwd(rs_table* t, const int64_t* values, const int64_t* offsets, int64_t n, int64_t bags,
+                          int32_t mode, int64_t pad_len, void* out, uint8_t* mask, rs_ctx* ctx, int32_t validate,
+                          rs_stream stream) {
+  if (bags > 0 && !out) return fail(RS_EINVAL, "null output");
+  if (mode == RS_POOL_NONE && bags > 0 && !mask) return fail(RS_EINVAL, "null mask");
+  rs_status st = lookup_prepare(t, values, offsets, n, bags, mode, pad_len, ctx, validate, stream);
+  if (st != RS_OK) return st;
+  return lookup_pool_prepared(t, ctx, out, mask, stream);
 }
 
 rs_status lookup_pool_bwd(rs_table* t, const rs_ctx* ctx, const void* grad_out, float* grad_unique, rs_stream stream) {

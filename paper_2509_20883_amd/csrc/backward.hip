@@ -226,11 +226,14 @@ static hipError_t bwd_launch(const TableDev& t, const Work& w, const int64_t* of
   constexpr int GPB = kBlock / LANES;
   const GT* g = static_cast<const GT*>(grad);
   if (ev_s && ev_s[0]) (void)hipEventRecord(ev_s[0], s);
-  k_bwd_short<WT, GT, LANES, MODE, FUSED><<<grid_for(n, GPB, 1 << 17), kBlock, 0, s>>>(t, w, offsets, g, gu, o);
+  // grid-stride kernels over device-side counts (U, units, hot keys): a grid
+  // of at most kResident blocks keeps every CU busy without dispatching
+  // wavefronts that would find no work
+  k_bwd_short<WT, GT, LANES, MODE, FUSED><<<grid_for(n, GPB, kResident), kBlock, 0, s>>>(t, w, offsets, g, gu, o);
   if (ev_s && ev_s[1]) (void)hipEventRecord(ev_s[1], s);
   if (ev_l && ev_l[0]) (void)hipEventRecord(ev_l[0], s);
-  k_bwd_long<GT, LANES, MODE><<<grid_for(2 * (n / kUnit) + 2, GPB, 1 << 16), kBlock, 0, s>>>(w, offsets, g);
-  k_bwd_long_finish<WT, E, LANES, FUSED><<<grid_for(n / kLong + 1, GPB, 1 << 16), kBlock, 0, s>>>(t, w, gu, o);
+  k_bwd_long<GT, LANES, MODE><<<grid_for(2 * (n / kUnit) + 2, GPB, kResident), kBlock, 0, s>>>(w, offsets, g);
+  k_bwd_long_finish<WT, E, LANES, FUSED><<<grid_for(n / kLong + 1, GPB, kResident), kBlock, 0, s>>>(t, w, gu, o);
   if (ev_l && ev_l[1]) (void)hipEventRecord(ev_l[1], s);
   return hipGetLastError();
 }
@@ -300,12 +303,12 @@ template <typename WT>
 static hipError_t opt_dim(const TableDev& t, const Work& w, int64_t n, const float* gu, const OptArgs& o,
                           hipStream_t s) {
   switch (t.dim / 4) {
-    case 2: k_opt<WT, 2><<<grid_for(n, kBlock / 2, 1 << 16), kBlock, 0, s>>>(t, w, gu, o); break;
-    case 4: k_opt<WT, 4><<<grid_for(n, kBlock / 4, 1 << 16), kBlock, 0, s>>>(t, w, gu, o); break;
-    case 8: k_opt<WT, 8><<<grid_for(n, kBlock / 8, 1 << 16), kBlock, 0, s>>>(t, w, gu, o); break;
-    case 16: k_opt<WT, 16><<<grid_for(n, kBlock / 16, 1 << 16), kBlock, 0, s>>>(t, w, gu, o); break;
-    case 32: k_opt<WT, 32><<<grid_for(n, kBlock / 32, 1 << 16), kBlock, 0, s>>>(t, w, gu, o); break;
-    case 64: k_opt<WT, 64><<<grid_for(n, kBlock / 64, 1 << 16), kBlock, 0, s>>>(t, w, gu, o); break;
+    case 2: k_opt<WT, 2><<<grid_for(n, kBlock / 2, kResident), kBlock, 0, s>>>(t, w, gu, o); break;
+    case 4: k_opt<WT, 4><<<grid_for(n, kBlock / 4, kResident), kBlock, 0, s>>>(t, w, gu, o); break;
+    case 8: k_opt<WT, 8><<<grid_for(n, kBlock / 8, kResident), kBlock, 0, s>>>(t, w, gu, o); break;
+    case 16: k_opt<WT, 16><<<grid_for(n, kBlock / 16, kResident), kBlock, 0, s>>>(t, w, gu, o); break;
+    case 32: k_opt<WT, 32><<<grid_for(n, kBlock / 32, kResident), kBlock, 0, s>>>(t, w, gu, o); break;
+    case 64: k_opt<WT, 64><<<grid_for(n, kBlock / 64, kResident), kBlock, 0, s>>>(t, w, gu, o); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -203,7 +203,7 @@ __device__ inline void load4(const int32_t* __restrict__ p, int64_t i0, int64_t 
   }
 }
 
-__global__ __launch_bounds__(kBlock) void k_rank_probe(TableDev t, Scratch sc, const int32_t* __restrict__ slot_of,
+__global__ __launch_bounds__(kBlock) void k_rank_probe(TableDev t, Scratch sc, int32_t* __restrict__ slot_of,
                                                        int64_t n, int32_t* __restrict__ bsum, int64_t ntiles) {
   __shared__ int sh[kBlock / kWave + 1];
   const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kRankTile + threadIdx.x * kRankItems;
@@ -227,8 +227,20 @@ __global__ __launch_bounds__(kBlock) void k_rank_probe(TableDev t, Scratch sc, c
   for (int k = 0; k < 4; ++k) {
     if (!f[k]) continue;
     const int64_t r = idmap_lookup(t, ss[k].key);
-    sc.aux[s[k] & kSlotMask].row = r;
+    ScratchAux* ax = &sc.aux[s[k] & kSlotMask];
+    ax->row = r;
+    ax->count = static_cast<int>(ss[k].cnt);
     nw += r < 0;
+  }
+  // the first occurrences are marked so the next pass reads only their keys
+  if (cf) {
+    if (i0 + 4 <= n) {
+      *reinterpret_cast<int4*>(slot_of + i0) = make_int4(f[0] ? s[0] | kFirstBit : s[0], f[1] ? s[1] | kFirstBit : s[1],
+                                                          f[2] ? s[2] | kFirstBit : s[2], f[3] ? s[3] | kFirstBit : s[3]);
+    } else {
+      for (int k = 0; k < 4 && i0 + k < n; ++k)
+        if (f[k]) slot_of[i0 + k] = s[k] | kFirstBit;
+    }
   }
   const int a = block_sum<kBlock>(cf | (nw << 16), sh);
   __syncthreads();
@@ -337,19 +349,16 @@ __global__ __launch_bounds__(kBlock) void k_compact_insert(TableDev t, Scratch s
   int s[4];
   load4(w.slot_of, i0, n, s);
   bool f[4];
-  ScratchSlot ss[4];
-  int64_t r[4];
+  ScratchAux ax0[4];
   int cf = 0, cc = 0, cn = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const bool cand = s[k] >= 0 && (s[k] & kCandBit);
+    f[k] = s[k] >= 0 && (s[k] & kFirstBit);
     s[k] &= kSlotMask;
-    if (cand) ss[k] = sc.slot[s[k]];
-    f[k] = cand && ss[k].first == static_cast<unsigned int>(i0 + k);
-    r[k] = f[k] ? sc.aux[s[k]].row : 0;
+    if (f[k]) ax0[k] = sc.aux[s[k]];
     cf += f[k];
-    cc += f[k] ? static_cast<int>(ss[k].cnt) : 0;
-    cn += (f[k] && r[k] < 0);
+    cc += f[k] ? ax0[k].count : 0;
+    cn += (f[k] && ax0[k].row < 0);
   }
   int tot;
   const int ex_a = block_excl_scan<kBlock>(cf | (cn << 16), sh, tot);
@@ -364,7 +373,8 @@ __global__ __launch_bounds__(kBlock) void k_compact_insert(TableDev t, Scratch s
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     if (!f[k]) continue;
-    const int c = static_cast<int>(ss[k].cnt);
+    const int c = ax0[k].count;
+    const unsigned long long ekey = static_cast<unsigned long long>(values[i0 + k]) ^ kSign;
     w.unique[uid] = values[i0 + k];
     int li = -1, ush = 0;
     if (c > kLong) {
@@ -379,10 +389,10 @@ __global__ __launch_bounds__(kBlock) void k_compact_insert(TableDev t, Scratch s
       float4* gp = reinterpret_cast<float4*>(w.gpart + static_cast<int64_t>(li) * t.dim);
       for (int j = 0; j < t.dim / 4; ++j) gp[j] = make_float4(0.f, 0.f, 0.f, 0.f);
     }
-    int64_t row = r[k];
+    int64_t row = ax0[k].row;
     if (row < 0) {
       if (nr < inserted) {
-        const int64_t slot = idmap_claim(t, ss[k].key);
+        const int64_t slot = idmap_claim(t, ekey);
         if (slot >= 0) {
           row = live0 + nr;
           t.slots[slot].row = row;

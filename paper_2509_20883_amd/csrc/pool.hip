@@ -18,6 +18,8 @@ namespace rs {
 
 constexpr int kBags = 4;
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 template <typename WT, int LANES, int MODE>
 __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64_t* __restrict__ offsets, int64_t n,
                                                  int64_t bags, float* __restrict__ out) {
@@ -30,12 +32,29 @@ __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64
   for (int64_t g0 = (static_cast<int64_t>(blockIdx.x) * GPB + grp) * kBags; g0 < bags; g0 += stride) {
     int64_t b[kBags], e[kBags];
     int64_t maxlen = 0;
+    if constexpr (LANES > kBags) {
+      // lanes 0..kBags of the group load offsets[g0 .. g0+kBags] together
+      const int64_t gq = g0 + min(lane, kBags);
+      const int64_t ov = gq <= bags ? offsets[gq] : n;
+#pragma unroll
+      for (int q = 0; q <= kBags; ++q) {
+        const int64_t x = __shfl(ov, q, LANES);
+        if (q < kBags) b[q] = x;
+        if (q > 0) e[q - 1] = x;
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < kBags; ++q) {
+        b[q] = g0 + q < bags ? offsets[g0 + q] : 0;
+        e[q] = g0 + q < bags ? offsets[g0 + q + 1] : 0;
+      }
+    }
 #pragma unroll
     for (int q = 0; q < kBags; ++q) {
       // CSR bounds clamped to [0, n]: malformed offsets cannot read out of range
       const bool ok = g0 + q < bags;
-      b[q] = ok ? min(max(offsets[g0 + q], int64_t(0)), n) : 0;
-      e[q] = ok ? min(max(offsets[g0 + q + 1], b[q]), n) : 0;
+      b[q] = ok ? min(max(b[q], int64_t(0)), n) : 0;
+      e[q] = ok ? min(max(e[q], b[q]), n) : 0;
       maxlen = max(maxlen, e[q] - b[q]);
     }
     float acc[kBags][E];
@@ -82,7 +101,13 @@ __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64
 #pragma unroll
         for (int k = 0; k < E; ++k) acc[q][k] = acc[q][k] / len;
       }
-      store_vals<float, E>(out + (g0 + q) * D + lane * E, acc[q]);
+      // the pooled output is streamed out once: non-temporal stores
+      float* op = out + (g0 + q) * D + lane * E;
+#pragma unroll
+      for (int k = 0; k < E; k += 4) {
+        const f32x4 v = {acc[q][k], acc[q][k + 1], acc[q][k + 2], acc[q][k + 3]};
+        __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(op + k));
+      }
     }
   }
 }

@@ -43,7 +43,11 @@ static_assert(kUnit == 1 << kUnitLog2, "kUnit is a power of two");
 // A key with more than kUnit * kMaxUnits occurrences gets units of
 // kUnit << shift positions, so no partial row receives more than kMaxUnits
 // atomic adds per element.
-constexpr int kMaxUnits = 64;
+constexpr int kMaxUnits = 1024;
+
+// Grid of the grid-stride kernels that loop over a device-side count: 8
+// blocks of 256 threads per CU on 256 CUs.
+constexpr int kResident = 2048;
 
 // Latched device error bits.
 enum : int { kErrKey = 1, kErrFull = 2, kErrScratch = 4, kErrProbe = 8 };
@@ -121,11 +125,13 @@ struct Scratch {
   uint64_t mask;  // slots - 1
 };
 
-// slot_of[i]: scratch slot of occurrence i; kCandBit marks the occurrence at
-// its tile's first position of the key (only those can be the key's first
-// occurrence in the batch); -1 for a rejected key.
+// slot_of[i]: scratch slot of occurrence i (< 2^29 slots); kCandBit marks
+// the occurrence at its tile's first position of the key (only those can be
+// the key's first occurrence in the batch), kFirstBit the key's first
+// occurrence once known; -1 for a rejected key.
 constexpr int kCandBit = 1 << 30;
-constexpr int kSlotMask = kCandBit - 1;
+constexpr int kFirstBit = 1 << 29;
+constexpr int kSlotMask = kFirstBit - 1;
 
 // Per-unique segment descriptor: the key's row, and where its occurrences
 // start in the occurrence list and how many there are.

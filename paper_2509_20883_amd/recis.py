@@ -80,6 +80,8 @@ def lib() -> C.CDLL:
         "ht_reserve": (C.c_int, [p, i64, p]),
         "lookup_workspace_bytes": (C.c_size_t, [i64, i64, i64, p]),
         "lookup_pool_fwd": (C.c_int, [p, p, p, i64, i64, i32, i64, p, p, C.POINTER(RsCtx), i32, p]),
+        "lookup_prepare": (C.c_int, [p, p, p, i64, i64, i32, i64, C.POINTER(RsCtx), i32, p]),
+        "lookup_pool_prepared": (C.c_int, [p, C.POINTER(RsCtx), p, p, p]),
         "lookup_pool_bwd": (C.c_int, [p, C.POINTER(RsCtx), p, p, p]),
         "sparse_opt_step": (C.c_int, [p, C.POINTER(RsCtx), p, C.POINTER(OptParams), p]),
         "lookup_pool_bwd_opt": (C.c_int, [p, C.POINTER(RsCtx), p, C.POINTER(OptParams), p]),
@@ -245,6 +247,35 @@ class Table:
         _check(lib().lookup_pool_fwd(self.h, _ptr(v), _ptr(o), n, bags, mode, pad_len, _ptr(out), _ptr(mask),
                                      C.byref(ctx.c), int(validate), _stream()))
         return out, mask, ctx
+
+    def prepare(self, values: torch.Tensor, offsets: torch.Tensor, mode: int, pad_len: int = 0,
+                ctx: Optional[Ctx] = None, validate: bool = False, stream=None) -> Ctx:
+        """First half of the forward (dedup, find-or-insert, bookkeeping) on `stream`."""
+        v = _dev(values, torch.int64)
+        o = _dev(offsets, torch.int64)
+        n, bags = v.numel(), o.numel() - 1
+        ctx = ctx or Ctx()
+        ctx.ensure(self.workspace_bytes(n, bags, pad_len), v.device)
+        ctx.keep = (v, o)
+        st = C.c_void_p(stream.cuda_stream) if stream is not None else _stream()
+        _check(lib().lookup_prepare(self.h, _ptr(v), _ptr(o), n, bags, mode, pad_len, C.byref(ctx.c),
+                                    int(validate), st))
+        return ctx
+
+    def pool(self, ctx: Ctx, out: Optional[torch.Tensor] = None, mask: Optional[torch.Tensor] = None):
+        """Second half of the forward: gather + pool of a prepared ctx."""
+        c = ctx.c
+        dev = ctx.ws.device
+        if c.mode == NONE:
+            odt = torch.bfloat16 if self.row_dtype == BF16 else torch.float32
+            if out is None:
+                out = torch.empty(c.bags, c.pad_len, self.dim, dtype=odt, device=dev)
+            if mask is None:
+                mask = torch.empty(c.bags, c.pad_len, dtype=torch.uint8, device=dev)
+        elif out is None:
+            out = torch.empty(c.bags, self.dim, dtype=torch.float32, device=dev)
+        _check(lib().lookup_pool_prepared(self.h, C.byref(ctx.c), _ptr(out), _ptr(mask), _stream()))
+        return out, mask
 
     def _grad(self, ctx: Ctx, grad_out: torch.Tensor) -> torch.Tensor:
         c = ctx.c

@@ -280,3 +280,61 @@ def test_resize_during_growing_run_matches_oracle():
         caps.append(gt.capacity())
     assert caps[-1] > caps[0]
     gt.close()
+
+
+def test_pipelined_prepare_matches_serial():
+    """The next batches' lookup_prepare on a second stream, overlapping the
+    current pool + backward, gives the same step results as one stream."""
+    _log("pipelined prepare vs serial")
+    w = W.workload(4, mini=True)
+    steps = 3
+    batches = [W.make_batch(w, s) for s in range(steps)]
+    grads = [P.to_dev(W.make_grad(w, b, s)) for s, b in enumerate(batches)]
+    ga, gb = P.gpu_table(w), P.gpu_table(w)
+    P.prepopulate(w, ga)
+    P.prepopulate(w, gb)
+    outs_a, ctx_a = [], []
+    for s, b in enumerate(batches):
+        out, _, c = ga.forward(P.to_dev(b.values), P.to_dev(b.offsets), w.mode)
+        ga.backward_optimizer(c, grads[s], w.lr, w.eps, w.beta1, w.beta2)
+        outs_a.append(out.clone())
+        ctx_a.append(c)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    ctx_b, ready = [], []
+    for b in batches:
+        c = gb.prepare(P.to_dev(b.values), P.to_dev(b.offsets), w.mode, stream=side)
+        ev = torch.cuda.Event()
+        ev.record(side)
+        ctx_b.append(c)
+        ready.append(ev)
+    outs_b = []
+    for s, (c, ev) in enumerate(zip(ctx_b, ready)):
+        torch.cuda.current_stream().wait_event(ev)
+        out, _ = gb.pool(c)
+        gb.backward_optimizer(c, grads[s], w.lr, w.eps, w.beta1, w.beta2)
+        outs_b.append(out.clone())
+    torch.cuda.synchronize()
+    ga.check()
+    gb.check()
+    for s in range(steps):
+        U = int(ctx_a[s].scalars()[0].item())
+        assert U == int(ctx_b[s].scalars()[0].item())
+        assert torch.equal(ctx_a[s].unique(U), ctx_b[s].unique(U))
+        assert torch.equal(ctx_a[s].inverse(), ctx_b[s].inverse())
+        assert torch.equal(ctx_a[s].rows(U), ctx_b[s].rows(U))
+        # hot-key partial sums use fp32 atomics (order varies): later steps may
+        # differ by an ulp of the updated rows
+        torch.testing.assert_close(outs_b[s], outs_a[s], rtol=1e-4, atol=2e-6)
+    ka, ra = ga.export()
+    kb, rb = gb.export()
+    oa, ob = torch.argsort(ka), torch.argsort(kb)
+    assert torch.equal(ka[oa], kb[ob]) and torch.equal(ra[oa], rb[ob])
+    wa, sa = ga.read_rows(ra[oa])
+    wb, sb = gb.read_rows(rb[ob])
+    torch.testing.assert_close(wb, wa, rtol=1e-4, atol=2e-6)
+    # Adam's m takes (1-beta1) of the gradient: a hot key's gradient summed in
+    # another order differs by ~count ulps of its terms
+    torch.testing.assert_close(sb, sa, rtol=1e-3, atol=1e-4)
+    ga.close()
+    gb.close()
