@@ -1,0 +1,211 @@
+"""Parity at the full sizes of the four synthetic workloads, in the launch
+configuration the benchmark times (lookup_pool_fwd, then the fused
+lookup_pool_bwd_opt, one stream, tables created and pre-populated the same way).
+
+What is compared:
+  - integers over the whole batch, bit-exact: U, the unique ids in
+    first-occurrence order and the inverse (oracle dedup of the full batch),
+    the number of keys inserted (keys absent from the pre-populated set), the
+    rows of the inserted keys (reserved in first-occurrence order after the
+    live ones), and that every unique id's row is what a plain find returns;
+  - pooled / padded outputs of sampled bags: the oracle pools the same bags
+    from rows it initialises itself.  The step is the first after
+    pre-population, so every row still holds its deterministic initial value
+    (a function of seed and id only, paper Sec. "Optimization for Memory
+    Bound": rows are materialised on first sight);
+  - the updated rows and optimizer state of sampled unique ids (random ones,
+    the hottest ones, ids on both sides of the short/long backward split): the
+    oracle sums their gradients over the whole batch in fp64 and applies its
+    own optimizer to its own initial rows.  The GPU's per-unique sums are not
+    exposed by the fused call, so the tolerance adds their allowed error
+    (1e-5 of the summed magnitudes, plus fp32 rounding) to the optimizer bound.
+"""
+from __future__ import annotations
+
+import gc
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2509_20883_amd import workloads as W
+from tests.parity import abs_pooled, assert_opt_close, assert_sum_close, gpu_table, opt_bounds, prepopulate, to_dev
+
+pytestmark = pytest.mark.gpu
+
+SAMPLE = 2048
+LONG_SPLIT = 32  # keys with more occurrences take the hot-key backward
+
+
+def _present(w: W.Workload, keys: np.ndarray, prepop: np.ndarray = None) -> np.ndarray:
+    """Membership of keys in the pre-populated set."""
+    if w.prepop == "none":
+        return np.zeros(keys.size, dtype=bool)
+    if w.prepop == "all":  # every rank of the vocabulary: all batch ids
+        return np.ones(keys.size, dtype=bool)
+    if w.prepop == "frac90":
+        member = np.zeros(keys.size, dtype=bool)
+        fid = keys >> W.ID_BITS
+        for f in np.unique(fid):
+            sel = fid == f
+            member[sel] = W.prepop_member(w, int(f), keys[sel] & W.ID_MASK)
+        return member
+    return np.isin(keys, prepop)
+
+
+def _sample_bags(b: W.Batch, g: np.random.Generator) -> np.ndarray:
+    lens = np.diff(b.offsets)
+    pick = [0, b.bags - 1, int(np.argmax(lens))]
+    if (lens == 0).any():
+        pick.append(int(np.flatnonzero(lens == 0)[0]))
+    pick += g.choice(b.bags, size=min(SAMPLE, b.bags), replace=False).tolist()
+    return np.unique(np.array(pick, dtype=np.int64))
+
+
+def _sample_unique(counts: np.ndarray, g: np.random.Generator) -> np.ndarray:
+    U = counts.size
+    pick = [0, U - 1]
+    pick += np.argsort(-counts, kind="stable")[:16].tolist()  # hottest
+    for c in (LONG_SPLIT - 1, LONG_SPLIT, LONG_SPLIT + 1, LONG_SPLIT + 2):
+        pick += np.flatnonzero(counts == c)[:4].tolist()
+    pick += g.choice(U, size=min(SAMPLE, U), replace=False).tolist()
+    return np.unique(np.array(pick, dtype=np.int64))
+
+
+def _sub_batch(b: W.Batch, bags: np.ndarray):
+    lens = np.diff(b.offsets)[bags]
+    off = np.zeros(bags.size + 1, dtype=np.int64)
+    np.cumsum(lens, out=off[1:])
+    vals = np.concatenate([b.values[b.offsets[i]:b.offsets[i + 1]] for i in bags]) if off[-1] else \
+        np.zeros(0, dtype=np.int64)
+    return vals.astype(np.int64), off
+
+
+def _oracle(w: W.Workload) -> O.Table:
+    return O.Table(w.dim, row_dtype=w.row_dtype, opt=w.opt, lo=w.init_lo, hi=w.init_hi, seed=w.table_seed)
+
+
+def _check_integers(w, gt, ctx, b, live0, prepop):
+    sc = ctx.scalars().cpu().numpy()
+    U, n_new = int(sc[0]), int(sc[1])
+    st, u_ref, inv_ref = O.dedup(b.values)
+    assert st == O.OK
+    assert U == u_ref.size, f"U {U} vs {u_ref.size}"
+    uniq = ctx.unique(U).cpu().numpy()
+    assert np.array_equal(uniq, u_ref), "unique ids differ"
+    inv = ctx.inverse().cpu().numpy()
+    assert np.array_equal(inv, inv_ref), "inverse differs"
+    new = ~_present(w, u_ref, prepop)
+    assert n_new == int(new.sum()), f"inserted {n_new} vs {int(new.sum())}"
+    rows = ctx.rows(U).cpu().numpy()
+    assert np.array_equal(rows[new], live0 + np.arange(n_new)), "rows of inserted keys"
+    assert (rows[~new] >= 0).all() and (rows[~new] < live0).all(), "rows of present keys"
+    found = gt.find(to_dev(u_ref)).cpu().numpy()
+    assert np.array_equal(found, rows), "lookup rows differ from a plain find"
+    assert gt.size() == live0 + n_new
+    return U, uniq, inv, rows
+
+
+def _check_outputs(w, b, out, mask, g):
+    bags = _sample_bags(b, g)
+    vals, off = _sub_batch(b, bags)
+    ot = _oracle(w)
+    pad = w.pad_len if w.mode == O.NONE else 0
+    ref = ot.forward(vals, off, w.mode, pad_len=pad)
+    assert ref["status"] == O.OK
+    sel = torch.from_numpy(bags).cuda()
+    if w.mode == O.NONE:
+        o = out.index_select(0, sel).float().cpu().numpy()
+        assert np.array_equal(o, ref["out"].astype(np.float32)), "padded gather of sampled bags differs"
+        assert np.array_equal(mask.index_select(0, sel).cpu().numpy(), ref["mask"]), "mask differs"
+        lens = np.diff(b.offsets)
+        want = (np.arange(w.pad_len)[None, :] < lens[:, None]).astype(np.uint8)
+        assert np.array_equal(mask.cpu().numpy(), want), "mask of the full batch"
+    else:
+        _, w_ref, _ = ot.read_rows(ref["unique"])
+        scale = abs_pooled(w_ref, ref["inverse"], off, w.mode)
+        assert_sum_close(out.index_select(0, sel).cpu().numpy(), ref["out"], scale, what="pooled (sampled bags)")
+
+
+def _check_update(w, b, grad, uniq, inv, sel, w0, s0, w1, s1):
+    U = uniq.size
+    remap = np.full(U, -1, dtype=np.int32)
+    remap[sel] = np.arange(sel.size, dtype=np.int32)
+    inv_s = np.where(inv >= 0, remap[np.maximum(inv, 0)], -1).astype(np.int32)
+    pad = w.pad_len if w.mode == O.NONE else 0
+    gu = O.backward(b.offsets, inv_s, sel.size, w.dim, w.mode, pad, grad)
+    gfin = np.where(np.isfinite(grad), grad, 0).astype(np.float32)
+    gabs = O.backward(b.offsets, inv_s, sel.size, w.dim, w.mode, pad, np.abs(gfin))
+    ot = _oracle(w)
+    st, rows_o, _ = ot.find_or_insert(uniq[sel])
+    assert st == O.OK
+    _, w0_ref, s0_ref = ot.read_rows(uniq[sel])
+    assert np.array_equal(w0, w0_ref) and np.array_equal(s0, s0_ref), "rows before the update differ"
+    g32 = gu.astype(np.float32)
+    ot.optimizer(rows_o, g32, w.lr, w.eps, w.beta1, w.beta2)
+    _, w1_ref, s1_ref = ot.read_rows(uniq[sel])
+    dg = 1e-5 * gabs + np.abs(gu) * 2.0 ** -23
+    bounds = opt_bounds(w.opt, w.row_dtype, w0, s0, g32, dg, w.lr, w.eps, w.beta1, w.beta2, ot.t, w1_ref)
+    assert_opt_close(w1, s1, w1_ref, s1_ref, bounds, what="fused backward + optimizer (sampled ids)")
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4])
+def test_fullsize_step(k):
+    """One full-size step of workload k (first step after pre-population)."""
+    w = W.workload(k)
+    g = np.random.default_rng(9000 + k)
+    gt = gpu_table(w)
+    try:
+        prepopulate(w, gt)
+        prepop = np.concatenate(list(W.prepop_keys(w))) if w.prepop == "pool" else None
+        live0 = gt.size()
+        b = W.make_batch(w, 0)
+        grad = W.make_grad(w, b, 0)
+        v, off = to_dev(b.values), to_dev(b.offsets)
+        gdev = to_dev(grad)
+        if w.mode == O.NONE and w.row_dtype == O.BF16:
+            gdev = gdev.to(torch.bfloat16)
+        out, mask, ctx = gt.forward(v, off, w.mode, pad_len=w.pad_len if w.mode == O.NONE else 0)
+        torch.cuda.synchronize()
+        U, uniq, inv, rows = _check_integers(w, gt, ctx, b, live0, prepop)
+        counts = np.bincount(inv[inv >= 0], minlength=U)
+        sel = _sample_unique(counts, g)
+        rsel = to_dev(rows[sel])
+        w0, s0 = (x.cpu().numpy() for x in gt.read_rows(rsel))
+        gt.backward_optimizer(ctx, gdev, w.lr, w.eps, w.beta1, w.beta2)
+        w1, s1 = (x.cpu().numpy() for x in gt.read_rows(rsel))
+        gt.check()
+        _check_outputs(w, b, out, mask, g)
+        _check_update(w, b, grad, uniq, inv, sel, w0, s0, w1, s1)
+    finally:
+        gt.close()
+        gc.collect()
+        torch.cuda.empty_cache()
+
+
+def test_fullsize_growing_steps():
+    """Consecutive full-size steps of the growing-table workload: each step's
+    integer results against the oracle's dedup and the set of keys seen so far."""
+    w = W.workload(4)
+    gt = gpu_table(w)
+    try:
+        prepopulate(w, gt)
+        seen = np.sort(np.concatenate(list(W.prepop_keys(w))))
+        ctx = None
+        for step in range(3):
+            live0 = gt.size()
+            b = W.make_batch(w, step)
+            grad = to_dev(W.make_grad(w, b, step))
+            out, _, ctx = gt.forward(to_dev(b.values), to_dev(b.offsets), w.mode, ctx=ctx)
+            torch.cuda.synchronize()
+            U, uniq, _, _ = _check_integers(w, gt, ctx, b, live0, seen)
+            gt.backward_optimizer(ctx, grad, w.lr, w.eps, w.beta1, w.beta2)
+            torch.cuda.synchronize()
+            assert np.isfinite(out.cpu().numpy()).all()
+            seen = np.union1d(seen, uniq)
+        gt.check()
+    finally:
+        gt.close()
+        gc.collect()
+        torch.cuda.empty_cache()
