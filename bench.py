@@ -100,12 +100,22 @@ def b_alg(w, N, G, U, Nnew):
             + 4 * N + R * U + out + grad + 4 * N + 2 * (R + S) * U)
 
 
+def unit_count(c: int, unit: int = 32, max_units: int = 1024) -> int:
+    """Backward units of a hot key with c occurrences (unit << shift positions, at most max_units)."""
+    sh = 0
+    while ((c - 1) >> (sh + 5)) >= max_units:
+        sh += 1
+    usz = unit << sh
+    return (c + usz - 1) // usz
+
+
 def key_stats(values: np.ndarray, long_threshold: int = 32):
     """Host-side split of a batch into short keys (<= 32 occurrences) and hot keys."""
     _, cnt = np.unique(values, return_counts=True)
     hot = cnt > long_threshold
     return {"U": int(cnt.size), "U_short": int((~hot).sum()), "N_short": int(cnt[~hot].sum()),
-            "U_long": int(hot.sum()), "N_long": int(cnt[hot].sum())}
+            "U_long": int(hot.sum()), "N_long": int(cnt[hot].sum()),
+            "units": int(sum(unit_count(int(c)) for c in cnt[hot]))}
 
 
 def kernel_bytes(w, kernel, N, G, ks):
@@ -121,9 +131,9 @@ def kernel_bytes(w, kernel, N, G, ks):
     if kernel == "bwd_short":
         Us, Ns = ks["U_short"], ks["N_short"]
         gr = R if w.mode == 2 else w.dim * 4
-        # segment descriptors, row ids, occurrence list, one upstream gradient
-        # row per occurrence, row + state read-modify-write
-        return 16 * U + 8 * Us + 4 * Ns + gr * Ns + 2 * (R + S) * Us
+        # segment descriptors, occurrence list, one upstream gradient row per
+        # occurrence, row + state read-modify-write
+        return 16 * U + 4 * Ns + gr * Ns + 2 * (R + S) * Us
     raise KeyError(kernel)
 
 
@@ -235,7 +245,7 @@ def main():
     side = torch.cuda.Stream(device=dev)  # default priority
 
     # untimed pass over the warm-up steps with per-kernel events: find the dominant kernel
-    names = ["dedup_local", "rank_probe", "compact_insert", "init_rows", "pool", "bwd_short", "bwd_long"]
+    names = ["dedup_local", "rank_probe", "compact_insert", "occ", "pool", "bwd_short", "bwd_long"]
     if a.unfused:
         names.append("opt")
     prof = {k: [] for k in names}

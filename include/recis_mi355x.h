@@ -257,12 +257,13 @@ typedef enum {
   RS_K_DEDUP_LOCAL = 0,    /* tile dedup + scratch set                          */
   RS_K_RANK_PROBE = 1,     /* first occurrences + IDMap probe                   */
   RS_K_COMPACT_INSERT = 2, /* unique ids, segments, rows, IDMap inserts         */
-  RS_K_INIT_ROWS = 3,      /* initial rows of inserted keys                     */
+  RS_K_INIT_ROWS = 3,      /* same launch as RS_K_OCC (it writes the new rows)  */
   RS_K_POOL = 4,           /* gather + pool (and the occurrence list)           */
   RS_K_BWD_SHORT = 5,      /* per-key gradient sum (+ optimizer), short keys    */
   RS_K_BWD_LONG = 6,       /* hot keys: unit partial sums + finish (two kernels) */
   RS_K_OPT = 7,            /* optimizer from grad_unique (two-call path)        */
-  RS_K_OCC = 8,            /* per-occurrence rows, list positions, inverse      */
+  RS_K_OCC = 8,            /* per-occurrence rows, list positions, inverse; the
+                              same launch writes the rows of inserted keys      */
   RS_K_COUNT = 9
 } rs_kernel_id;
 rs_status rs_set_kernel_events(rs_table* t, int32_t kernel, void* start_event, void* stop_event);

@@ -75,9 +75,9 @@ Layout make_layout(int64_t n, int dim) {
   L.long_u = take(4 * nlong);
   L.long_start = take(4 * nlong);
   L.units = take(sizeof(Unit) * nunit);
-  L.bsum = take(4 * 3 * static_cast<size_t>(L.ntiles));
+  L.bsum = take(4 * 5 * static_cast<size_t>(L.ntiles));
   L.scal = take(8 * kCScalars);
-  L.gpart = take(4 * nlong * static_cast<size_t>(dim));
+  L.gpart = take(4 * nunit * static_cast<size_t>(dim));
   L.total = off;
   return L;
 }
@@ -145,13 +145,16 @@ struct rs_table {
   ScratchSlot* s_slot = nullptr;
   ScratchAux* s_aux = nullptr;
   int64_t s_cap = 0;
-  // host view of the live count: an upper bound, refreshed from an
-  // asynchronous read-back when one has completed
+  // host view of the live count: an upper bound.  Every insert call gets a
+  // 16-bit tag; its scan kernel stores (tag << 48) | exact live count into
+  // h_pin[0], and bound_after[tag % kTags] remembers the host's bound right
+  // after that call was enqueued, so a published count refreshes the bound
+  // by the calls enqueued since (bound_after[.] = -1: no refresh from it).
+  static constexpr int kTags = 64;
   int64_t live_bound = 0;
   int64_t* h_pin = nullptr;
-  hipEvent_t rb_ev = nullptr;
-  bool rb_pending = false;
-  int64_t rb_bound = 0;
+  int64_t tag = 0;
+  int64_t bound_after[kTags];
   int64_t adam_t = 0;
   // internal workspace for ht_find_or_insert
   void* iws = nullptr;
@@ -304,23 +307,29 @@ rs_status grow_for(rs_table* t, int64_t live_need, int64_t batch, hipStream_t s)
   return provision_rows(t, std::min(live_need, t->limit), s);
 }
 
+// Lower the host's bound on live rows with the newest count a scan kernel
+// has published (calls enqueued after it keep their share of the bound).
 void refresh_bound(rs_table* t) {
-  if (t->rb_pending && hipEventQuery(t->rb_ev) == hipSuccess) {
-    t->rb_pending = false;
-    const int64_t exact = *t->h_pin;
-    t->live_bound = exact + (t->live_bound - t->rb_bound);
-  }
+  const int64_t v = __atomic_load_n(t->h_pin, __ATOMIC_ACQUIRE);
+  const int64_t tag = (v >> 48) & 0xFFFF;
+  if (tag == 0 || ((t->tag - tag) & 0xFFFF) >= rs_table::kTags) return;
+  const int64_t after = t->bound_after[tag % rs_table::kTags];
+  if (after < 0) return;
+  const int64_t exact = v & ((int64_t(1) << 48) - 1);
+  t->live_bound = std::min(t->live_bound, exact + (t->live_bound - after));
 }
 
-void start_readback(rs_table* t, hipStream_t s) {
-  if (t->rb_pending) return;
-  if (hipMemcpyAsync(t->h_pin, t->d_scal + kTLive, sizeof(int64_t), hipMemcpyDeviceToHost, s) != hipSuccess ||
-      hipEventRecord(t->rb_ev, s) != hipSuccess) {
-    (void)hipGetLastError();
-    return;
-  }
-  t->rb_pending = true;
-  t->rb_bound = t->live_bound;
+// The bound becomes exact (after a synchronization): counts published for
+// earlier calls can no longer refresh it.
+void reset_bound(rs_table* t, int64_t exact) {
+  t->live_bound = exact;
+  for (int64_t& b : t->bound_after) b = -1;
+}
+
+int64_t next_tag(rs_table* t) {
+  t->tag = (t->tag & 0xFFFF) == 0xFFFF ? 1 : t->tag + 1;  // tags 1..65535 (0: nothing published)
+  t->bound_after[t->tag % rs_table::kTags] = -1;
+  return t->tag;
 }
 
 // Dedup `values` into w, then find-or-insert the unique keys (growing the
@@ -330,29 +339,33 @@ rs_status dedup_and_insert(rs_table* t, const int64_t* values, int64_t n, const 
   rs_status st = ensure_scratch(t, n, s);
   if (st != RS_OK) return st;
   const Scratch sc = t->scratch();
-  RS_HIP(launch_dedup_probe(values, n, sc, t->dev(), w, t->ev(RS_K_DEDUP_LOCAL), t->ev(RS_K_RANK_PROBE), s));
+  const int64_t tag = next_tag(t);
+  RS_HIP(launch_dedup_probe(values, n, sc, t->dev(), w, t->h_pin, tag, t->ev(RS_K_DEDUP_LOCAL),
+                            t->ev(RS_K_RANK_PROBE), s));
   refresh_bound(t);
   const int64_t bound = t->live_bound + n;
   if (bound > t->limit || bound > t->rows_prov) {
     // exact decision: read back U and live (one synchronization)
     RS_HIP(hipStreamSynchronize(s));
-    // the 3-way scan already reserved rows for the keys not found (or as
-    // many as fitted): read the request and the live count before it
+    // the scan already reserved rows for the keys not found (or as many as
+    // fitted): read the request and the live count before it
     int64_t req = 0, live0 = 0;
     RS_HIP(hipMemcpy(&req, w.scal + kCNewReq, sizeof(int64_t), hipMemcpyDeviceToHost));
     RS_HIP(hipMemcpy(&live0, w.scal + kCBaseLive, sizeof(int64_t), hipMemcpyDeviceToHost));
-    t->rb_pending = false;
     st = grow_for(t, live0 + req, n, s);
     if (st != RS_OK) return st;
-    // redo the reservation against the grown table
-    RS_HIP(launch_rereserve(w, t->dev(), s));
-    t->live_bound = live0 + req;
+    // redo the reservation against the grown table (published under a new
+    // tag: the scan's count may predate the growth)
+    reset_bound(t, live0 + req);
+    const int64_t tag2 = next_tag(t);
+    RS_HIP(launch_rereserve(w, t->dev(), t->h_pin, tag2, s));
+    t->bound_after[tag2 % rs_table::kTags] = t->live_bound;
   } else {
     t->live_bound = bound;
+    t->bound_after[tag % rs_table::kTags] = t->live_bound;
   }
   RS_HIP(launch_compact_insert(values, n, sc, t->dev(), w, occ_lists, t->ev(RS_K_COMPACT_INSERT),
                                t->ev(RS_K_INIT_ROWS), t->ev(RS_K_OCC), s));
-  start_readback(t, s);
   return RS_OK;
 }
 
@@ -431,11 +444,12 @@ rs_status ht_create(const rs_table_desc* d, const rs_allocator* a, rs_stream str
   }
   rs_status st = RS_OK;
   do {
-    if (hipHostMalloc(reinterpret_cast<void**>(&t->h_pin), sizeof(int64_t) * 8, hipHostMallocDefault) != hipSuccess ||
-        hipEventCreateWithFlags(&t->rb_ev, hipEventDisableTiming) != hipSuccess) {
-      st = fail(RS_EHIP, "pinned read-back buffer or event creation failed");
+    if (hipHostMalloc(reinterpret_cast<void**>(&t->h_pin), sizeof(int64_t) * 8, hipHostMallocDefault) != hipSuccess) {
+      st = fail(RS_EHIP, "pinned read-back buffer allocation failed");
       break;
     }
+    t->h_pin[0] = 0;
+    for (int64_t& b : t->bound_after) b = -1;
     if (hipMemsetAsync(t->slots, 0, sizeof(Slot) * static_cast<size_t>(t->cap), s) != hipSuccess ||
 
         hipMemsetAsync(t->d_scal, 0, sizeof(int64_t) * kTScalars, s) != hipSuccess) {
@@ -490,7 +504,6 @@ rs_status ht_destroy(rs_table* t) {
   t->release(t->s_aux);
   t->release(t->iws);
   if (t->h_pin) (void)hipHostFree(t->h_pin);
-  if (t->rb_ev) (void)hipEventDestroy(t->rb_ev);
   delete t;
   return st;
 }
@@ -538,8 +551,7 @@ rs_status ht_size(rs_table* t, int64_t* live_host, rs_stream stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   RS_HIP(hipStreamSynchronize(s));
   RS_HIP(hipMemcpy(live_host, t->d_scal + kTLive, sizeof(int64_t), hipMemcpyDeviceToHost));
-  t->rb_pending = false;
-  t->live_bound = *live_host;
+  reset_bound(t, *live_host);
   return take_latched(t);
 }
 

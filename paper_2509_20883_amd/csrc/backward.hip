@@ -16,11 +16,10 @@
 //                     gradient rows are being read)
 //   k_bwd_long        a hot key: its segment is cut into units (kUnit
 //                     positions, more for the hottest keys so a key has at
-//                     most kMaxUnits units) spread over the whole GPU; the
-//                     partial sums of a wavefront's units of one key are
-//                     combined by shuffles and added into the key's partial
-//                     row with fp32 atomics (one per element per wavefront)
-//   k_bwd_long_finish applies the optimizer from the partial rows
+//                     most kMaxUnits units) spread over the whole GPU; each
+//                     unit writes its partial sum row (no atomics)
+//   k_bwd_long_finish one block per hot key sums the partial rows of its
+//                     units in a fixed order and applies the optimizer
 // Without the optimizer (lookup_pool_bwd) the same kernels write grad_unique.
 #include "device_common.h"
 
@@ -113,17 +112,19 @@ __device__ inline void sum_positions(const Work& w, const GT* __restrict__ grad,
   }
 }
 
+// Keys with at most kLong occurrences, one lane group each; block `blk` of
+// `nblk` takes every nblk-th group of keys.
 template <typename WT, typename GT, int LANES, int MODE, bool FUSED>
-__global__ __launch_bounds__(kBlock) void k_bwd_short(TableDev t, Work w, const int64_t* __restrict__ offsets,
-                                                      const GT* __restrict__ grad, float* __restrict__ grad_unique,
-                                                      OptArgs o) {
+__device__ inline void bwd_short(const TableDev& t, const Work& w, const int64_t* __restrict__ offsets,
+                                 const GT* __restrict__ grad, float* __restrict__ grad_unique, const OptArgs& o,
+                                 int64_t blk, int64_t nblk) {
   constexpr int E = 16 / static_cast<int>(sizeof(GT));
   constexpr int GPB = kBlock / LANES;
   constexpr int D = LANES * E;
   const int lane = threadIdx.x % LANES;
   const int grp = threadIdx.x / LANES;
   const int64_t U = w.scal[kCU];
-  for (int64_t u = static_cast<int64_t>(blockIdx.x) * GPB + grp; u < U; u += static_cast<int64_t>(gridDim.x) * GPB) {
+  for (int64_t u = blk * GPB + grp; u < U; u += nblk * GPB) {
     const Seg sg = w.useg[u];
     if (sg.count > kLong) continue;  // a hot key: k_bwd_long
     RowFrag<WT, E> fr;
@@ -144,53 +145,42 @@ __global__ __launch_bounds__(kBlock) void k_bwd_short(TableDev t, Work w, const 
   }
 }
 
-// One lane group per backward unit of a hot key.  Units of one key are
-// consecutive, so the groups of a wavefront usually share the key: their
-// partial sums are then combined by cross-group shuffles and one group adds
-// the wavefront's sum into the key's partial row (one atomic per element per
-// wavefront, not per unit).
+// One lane group per backward unit of a hot key: the unit's partial sum is
+// written to its own partial row.
 template <typename GT, int LANES, int MODE>
-__global__ __launch_bounds__(kBlock) void k_bwd_long(Work w, const int64_t* __restrict__ offsets,
-                                                     const GT* __restrict__ grad) {
+__device__ inline void bwd_units(const Work& w, const int64_t* __restrict__ offsets, const GT* __restrict__ grad,
+                                 int64_t blk, int64_t nblk) {
   constexpr int E = 16 / static_cast<int>(sizeof(GT));
-  constexpr int GPW = kWave / LANES;  // lane groups per wavefront
+  constexpr int GPB = kBlock / LANES;
   constexpr int D = LANES * E;
   const int lane = threadIdx.x % LANES;
-  const int gw = (threadIdx.x % kWave) / LANES;  // group within the wavefront
+  const int grp = threadIdx.x / LANES;
   const int64_t units = w.scal[kCNUnits];
-  const int64_t waves = static_cast<int64_t>(gridDim.x) * (kBlock / kWave);
-  for (int64_t wb = (static_cast<int64_t>(blockIdx.x) * (kBlock / kWave) + threadIdx.x / kWave) * GPW; wb < units;
-       wb += waves * GPW) {  // the trip count is uniform across the wavefront
-    const int64_t unit = wb + gw;
-    int li = -1;
+  for (int64_t unit = blk * GPB + grp; unit < units; unit += nblk * GPB) {
+    const Unit un = w.units[unit];
     float acc[E];
 #pragma unroll
     for (int q = 0; q < E; ++q) acc[q] = 0.f;
-    if (unit < units) {
-      const Unit un = w.units[unit];
-      li = un.li;
-      for (int p = un.p0; p < un.p1; p += kUnit) sum_positions<GT, E, LANES, MODE>(w, grad, offsets, p, min(kUnit, un.p1 - p), lane, acc);
-    }
-    int li0 = li;
-#pragma unroll
-    for (int off = LANES; off < kWave; off <<= 1) li0 = max(li0, __shfl_xor(li0, off, kWave));
-    const bool same = __all(li == li0 || li < 0);
-    if (same && GPW > 1) {
-#pragma unroll
-      for (int off = LANES; off < kWave; off <<= 1)
-#pragma unroll
-        for (int q = 0; q < E; ++q) acc[q] += __shfl_xor(acc[q], off, kWave);
-      if (gw == 0 && li0 >= 0) {
-        float* gp = w.gpart + static_cast<int64_t>(li0) * D + lane * E;
-#pragma unroll
-        for (int q = 0; q < E; ++q) unsafeAtomicAdd(gp + q, acc[q]);
-      }
-    } else if (li >= 0) {
-      float* gp = w.gpart + static_cast<int64_t>(li) * D + lane * E;
-#pragma unroll
-      for (int q = 0; q < E; ++q) unsafeAtomicAdd(gp + q, acc[q]);
-    }
+    for (int p = un.p0; p < un.p1; p += kUnit)
+      sum_positions<GT, E, LANES, MODE>(w, grad, offsets, p, min(kUnit, un.p1 - p), lane, acc);
+    store_vals<float, E>(w.gpart + unit * D + lane * E, acc);
   }
+}
+
+// The two strategies run as consecutive launches (interleaving their blocks
+// in one launch measured slower: the hot-key units' scattered gradient reads
+// then compete with the short keys' row updates).
+template <typename WT, typename GT, int LANES, int MODE, bool FUSED>
+__global__ __launch_bounds__(kBlock) void k_bwd_short(TableDev t, Work w, const int64_t* __restrict__ offsets,
+                                                      const GT* __restrict__ grad, float* __restrict__ grad_unique,
+                                                      OptArgs o) {
+  bwd_short<WT, GT, LANES, MODE, FUSED>(t, w, offsets, grad, grad_unique, o, blockIdx.x, gridDim.x);
+}
+
+template <typename GT, int LANES, int MODE>
+__global__ __launch_bounds__(kBlock) void k_bwd_long(Work w, const int64_t* __restrict__ offsets,
+                                                     const GT* __restrict__ grad) {
+  bwd_units<GT, LANES, MODE>(w, offsets, grad, blockIdx.x, gridDim.x);
 }
 
 template <typename WT, int E, int LANES, bool FUSED>
@@ -198,24 +188,56 @@ __global__ __launch_bounds__(kBlock) void k_bwd_long_finish(TableDev t, Work w, 
                                                             OptArgs o) {
   constexpr int GPB = kBlock / LANES;
   constexpr int D = LANES * E;
+  __shared__ float red[GPB][D];
   const int lane = threadIdx.x % LANES;
   const int grp = threadIdx.x / LANES;
   const int64_t nlong = w.scal[kCNLong];
-  for (int64_t li = static_cast<int64_t>(blockIdx.x) * GPB + grp; li < nlong;
-       li += static_cast<int64_t>(gridDim.x) * GPB) {
+  for (int64_t li = blockIdx.x; li < nlong; li += gridDim.x) {
     const int u = w.long_u[li];
-    float acc[E];
-    load_vals<float, E>(w.gpart + li * D + lane * E, acc);
-    if (FUSED) {
-      const int64_t r = w.useg[u].row;
-      if (r < 0) continue;
-      uint8_t* rp = t.store.row(r);
-      RowFrag<WT, E> fr;
-      fr.load(rp, lane, D, t.nstate);
-      fr.update_store(rp, lane, D, acc, o);
-    } else {
-      store_vals<float, E>(grad_unique + static_cast<int64_t>(u) * D + lane * E, acc);
+    const Seg sg = w.useg[u];
+    const int nu = unit_count(sg.count);
+    const int64_t u0 = w.long_start[li];
+    RowFrag<WT, E> fr;
+    uint8_t* rp = nullptr;
+    if (FUSED && grp == 0 && sg.row >= 0) {
+      rp = t.store.row(sg.row);
+      fr.load(rp, lane, D, t.nstate);  // in flight while the partial rows are read
     }
+    float acc[E];
+#pragma unroll
+    for (int q = 0; q < E; ++q) acc[q] = 0.f;
+    for (int j = grp; j < nu; j += 2 * GPB) {
+      float x[E], y[E];
+      load_vals<float, E>(w.gpart + (u0 + j) * D + lane * E, x);
+      const bool two = j + GPB < nu;
+      if (two) load_vals<float, E>(w.gpart + (u0 + j + GPB) * D + lane * E, y);
+#pragma unroll
+      for (int q = 0; q < E; ++q) acc[q] += x[q];
+      if (two) {
+#pragma unroll
+        for (int q = 0; q < E; ++q) acc[q] += y[q];
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < E; ++q) red[grp][lane * E + q] = acc[q];
+    __syncthreads();
+    for (int h = GPB / 2; h >= 1; h >>= 1) {
+      if (grp < h) {
+#pragma unroll
+        for (int q = 0; q < E; ++q) red[grp][lane * E + q] += red[grp + h][lane * E + q];
+      }
+      __syncthreads();
+    }
+    if (grp == 0) {
+#pragma unroll
+      for (int q = 0; q < E; ++q) acc[q] = red[0][lane * E + q];
+      if (FUSED) {
+        if (rp) fr.update_store(rp, lane, D, acc, o);
+      } else {
+        store_vals<float, E>(grad_unique + static_cast<int64_t>(u) * D + lane * E, acc);
+      }
+    }
+    __syncthreads();  // red is reused by the block's next key
   }
 }
 
@@ -225,15 +247,15 @@ static hipError_t bwd_launch(const TableDev& t, const Work& w, const int64_t* of
   constexpr int E = 16 / static_cast<int>(sizeof(GT));
   constexpr int GPB = kBlock / LANES;
   const GT* g = static_cast<const GT*>(grad);
+  // grid-stride loops over device-side counts (U, units, hot keys): a grid
+  // of at most kResident blocks per strategy keeps every CU busy without
+  // dispatching wavefronts that would find no work
   if (ev_s && ev_s[0]) (void)hipEventRecord(ev_s[0], s);
-  // grid-stride kernels over device-side counts (U, units, hot keys): a grid
-  // of at most kResident blocks keeps every CU busy without dispatching
-  // wavefronts that would find no work
   k_bwd_short<WT, GT, LANES, MODE, FUSED><<<grid_for(n, GPB, kResident), kBlock, 0, s>>>(t, w, offsets, g, gu, o);
   if (ev_s && ev_s[1]) (void)hipEventRecord(ev_s[1], s);
   if (ev_l && ev_l[0]) (void)hipEventRecord(ev_l[0], s);
   k_bwd_long<GT, LANES, MODE><<<grid_for(2 * (n / kUnit) + 2, GPB, kResident), kBlock, 0, s>>>(w, offsets, g);
-  k_bwd_long_finish<WT, E, LANES, FUSED><<<grid_for(n / kLong + 1, GPB, kResident), kBlock, 0, s>>>(t, w, gu, o);
+  k_bwd_long_finish<WT, E, LANES, FUSED><<<grid_for(n / kLong + 1, 1, 4 * kResident), kBlock, 0, s>>>(t, w, gu, o);
   if (ev_l && ev_l[1]) (void)hipEventRecord(ev_l[1], s);
   return hipGetLastError();
 }

@@ -8,15 +8,16 @@
 //                    its first position, atomicAdd of its count; the value the
 //                    atomicAdd returns ranks the tile's occurrences of the key)
 //   k_rank_probe     first occurrences probe the IDMap; tile sums of
-//                    (first occurrences, their counts, keys not found)
-//   k_scan3          one block scans the three tile-sum arrays and reserves
+//                    (first occurrences, their counts, keys not found, hot
+//                    keys, backward units of the hot keys)
+//   k_scan5          one block scans the five tile-sum arrays and reserves
 //                    the rows of the new keys
 //   k_compact_insert unique ids in first-occurrence order, occurrence-list
 //                    segments, rows; new keys claim an IDMap slot
-//   k_init_rows      lane groups write the initial rows of the new keys
-//   k_occ            per occurrence: unique id (inverse), row, position in the
+//   k_occ_init       per occurrence: unique id (inverse), row, position in the
 //                    occurrence list, hot-key backward units; releases the
-//                    scratch slots
+//                    scratch slots.  Its other blocks write the initial rows
+//                    of the new keys
 #include "device_common.h"
 
 namespace rs {
@@ -25,11 +26,11 @@ namespace rs {
 // open addressing (linear probing)
 // ---------------------------------------------------------------------------
 
-// Row of an encoded key, or -1 when the probe reaches an empty slot.  Reads
+// Row of an encoded key, or -1 when the probe reaches an empty slot; the
+// probe starts `done` slots into the key's sequence (at slot h).  Reads
 // kProbeBatch consecutive slots per round trip.
-__device__ inline int64_t idmap_lookup(const TableDev& t, unsigned long long e) {
-  uint64_t h = idmap_hash(e) & t.cap_mask;
-  for (uint64_t probed = 0; probed <= t.cap_mask; probed += kProbeBatch) {
+__device__ inline int64_t idmap_lookup_at(const TableDev& t, unsigned long long e, uint64_t h, uint64_t done) {
+  for (uint64_t probed = done; probed <= t.cap_mask; probed += kProbeBatch) {
     Slot sl[kProbeBatch];
 #pragma unroll
     for (int k = 0; k < kProbeBatch; ++k) sl[k] = t.slots[(h + k) & t.cap_mask];
@@ -43,19 +44,30 @@ __device__ inline int64_t idmap_lookup(const TableDev& t, unsigned long long e) 
   return -1;
 }
 
+__device__ inline int64_t idmap_lookup(const TableDev& t, unsigned long long e) {
+  return idmap_lookup_at(t, e, idmap_hash(e) & t.cap_mask, 0);
+}
+
 // Claim the slot of an encoded key (its own if present, else the first empty
-// one on its probe sequence); returns the slot index or -1 if the table is full.
-// A stale read of an empty slot only costs a failed compare-and-swap.
+// one on its probe sequence); returns the slot index or -1 if the table is
+// full.  Reads kProbeBatch slot keys per round trip; a stale read of an
+// empty slot only costs a failed compare-and-swap (slots are never emptied
+// during a call, so a slot read as occupied stays occupied).
 __device__ inline int64_t idmap_claim(const TableDev& t, unsigned long long e) {
   uint64_t h = idmap_hash(e) & t.cap_mask;
-  for (uint64_t probed = 0; probed <= t.cap_mask; ++probed) {
-    const unsigned long long cur = t.slots[h].key;
-    if (cur == e) return static_cast<int64_t>(h);
-    if (cur == kEncEmpty) {
-      const unsigned long long old = atomicCAS(&t.slots[h].key, kEncEmpty, e);
-      if (old == kEncEmpty || old == e) return static_cast<int64_t>(h);
+  for (uint64_t probed = 0; probed <= t.cap_mask; probed += kProbeBatch) {
+    unsigned long long k[kProbeBatch];
+#pragma unroll
+    for (int q = 0; q < kProbeBatch; ++q) k[q] = t.slots[(h + q) & t.cap_mask].key;
+    for (int q = 0; q < kProbeBatch; ++q) {
+      const uint64_t hq = (h + q) & t.cap_mask;
+      if (k[q] == e) return static_cast<int64_t>(hq);
+      if (k[q] == kEncEmpty) {
+        const unsigned long long old = atomicCAS(&t.slots[hq].key, kEncEmpty, e);
+        if (old == kEncEmpty || old == e) return static_cast<int64_t>(hq);
+      }
     }
-    h = (h + 1) & t.cap_mask;
+    h = (h + kProbeBatch) & t.cap_mask;
   }
   return -1;
 }
@@ -73,6 +85,37 @@ __device__ inline int64_t scratch_claim(const Scratch& sc, unsigned long long e)
   return -1;
 }
 
+// Exclusive block scan of five values per thread at once (two barriers).
+template <int NT>
+__device__ inline void block_excl_scan5(const int (&v)[5], int (&ex)[5], int (&tot)[5], int (*sh)[5]) {
+  const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+  int inc[5];
+#pragma unroll
+  for (int a = 0; a < 5; ++a) inc[a] = wave_incl_scan(v[a]);
+  if (lane == kWave - 1) {
+#pragma unroll
+    for (int a = 0; a < 5; ++a) sh[wid][a] = inc[a];
+  }
+  __syncthreads();
+  if (threadIdx.x < 5) {
+    const int a = threadIdx.x;
+    int run = 0;
+    for (int w = 0; w < NT / kWave; ++w) {
+      const int t = sh[w][a];
+      sh[w][a] = run;
+      run += t;
+    }
+    sh[NT / kWave][a] = run;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int a = 0; a < 5; ++a) {
+    ex[a] = sh[wid][a] + inc[a] - v[a];
+    tot[a] = sh[NT / kWave][a];
+  }
+  __syncthreads();
+}
+
 // ---------------------------------------------------------------------------
 // pass 1: tile-local dedup in LDS, then the global scratch set
 // ---------------------------------------------------------------------------
@@ -80,41 +123,43 @@ __device__ inline int64_t scratch_claim(const Scratch& sc, unsigned long long e)
 __global__ __launch_bounds__(kBlock) void k_dedup_local(const int64_t* __restrict__ values, int64_t n, Scratch sc,
                                                         int32_t* __restrict__ slot_of, int32_t* __restrict__ occ_rank,
                                                         int* err) {
+  // lkey: the key, then (read only by the slot's owner in between) its
+  // scratch slot; lcnt: the count, then the global rank base of the tile's
+  // occurrences of the key
   __shared__ unsigned long long lkey[kDedupLdsSlots];
   __shared__ unsigned int lmin[kDedupLdsSlots];
   __shared__ unsigned int lcnt[kDedupLdsSlots];
-  __shared__ int lgs[kDedupLdsSlots];
-  __shared__ unsigned int lbase[kDedupLdsSlots];
+  __shared__ short ldense[kDedupTile];  // the tile's distinct keys: dense index -> LDS slot
+  __shared__ int sh[kBlock / kWave + 1];
   const int tid = threadIdx.x;
   for (int s = tid; s < kDedupLdsSlots; s += kBlock) {
     lkey[s] = kEncEmpty;
     lmin[s] = 0xFFFFFFFFu;
     lcnt[s] = 0u;
   }
-  __syncthreads();
+  // every load is issued before the first wait (n > 0: indices are clamped)
   const int64_t base = static_cast<int64_t>(blockIdx.x) * kDedupTile;
-  unsigned long long e[kDedupItems];
+  int64_t raw[kDedupItems];
 #pragma unroll
-  for (int k = 0; k < kDedupItems; ++k) {
-    const int64_t i = base + k * kBlock + tid;
-    e[k] = i < n ? (static_cast<unsigned long long>(values[i]) ^ kSign) : kEncEmpty;
-  }
+  for (int k = 0; k < kDedupItems; ++k) raw[k] = values[min(base + k * kBlock + tid, n - 1)];
+  __syncthreads();
   int ls[kDedupItems];
   unsigned int lr[kDedupItems];
 #pragma unroll
   for (int k = 0; k < kDedupItems; ++k) {
     const int64_t i = base + k * kBlock + tid;
+    const unsigned long long e = static_cast<unsigned long long>(raw[k]) ^ kSign;
     ls[k] = -1;
     lr[k] = 0;
     if (i >= n) continue;
-    if (e[k] <= kEncTomb) {
+    if (e <= kEncTomb) {
       atomicOr(err, kErrKey);
       continue;
     }
-    unsigned int h = static_cast<unsigned int>(mix64(e[k]) >> 40) & (kDedupLdsSlots - 1);
+    unsigned int h = static_cast<unsigned int>(mix64(e) >> 40) & (kDedupLdsSlots - 1);
     while (true) {  // at most kDedupTile keys in twice as many slots: terminates
-      const unsigned long long old = atomicCAS(&lkey[h], kEncEmpty, e[k]);
-      if (old == kEncEmpty || old == e[k]) break;
+      const unsigned long long old = atomicCAS(&lkey[h], kEncEmpty, e);
+      if (old == kEncEmpty || old == e) break;
       h = (h + 1) & (kDedupLdsSlots - 1);
     }
     atomicMin(&lmin[h], static_cast<unsigned int>(i));
@@ -122,67 +167,86 @@ __global__ __launch_bounds__(kBlock) void k_dedup_local(const int64_t* __restric
     ls[k] = static_cast<int>(h);
   }
   __syncthreads();
-  // Each thread owns 8 LDS slots.  Their first scratch reads are issued
-  // together; an existing key needs no compare-and-swap, and its first
-  // position needs no atomicMin when the stored one is already smaller (it
-  // only ever decreases, so a stale read errs on the side of the atomic).
+  // Dense list of the occupied slots, so a wavefront's global phase runs as
+  // few rounds as the tile has distinct keys per thread (not one per slot).
   constexpr int kOwn = kDedupLdsSlots / kBlock;
-  unsigned long long ke[kOwn];
-  int64_t gs[kOwn];
-  ScratchSlot cur[kOwn];
+  int occ = 0;
 #pragma unroll
-  for (int j = 0; j < kOwn; ++j) {
-    ke[j] = lkey[tid + j * kBlock];
-    gs[j] = -1;
-  }
+  for (int j = 0; j < kOwn; ++j) occ += lkey[tid * kOwn + j] != kEncEmpty;
+  int d;
+  int at = block_excl_scan<kBlock>(occ, sh, d);
 #pragma unroll
   for (int j = 0; j < kOwn; ++j)
-    if (ke[j] != kEncEmpty) cur[j] = sc.slot[scratch_hash(ke[j]) & sc.mask];
+    if (lkey[tid * kOwn + j] != kEncEmpty) ldense[at++] = static_cast<short>(tid * kOwn + j);
+  __syncthreads();
+  // Global phase, each step issued for all of a thread's keys before its
+  // results are waited for: read the key's scratch slot; claim it with a
+  // compare-and-swap if empty (a hot key, already present, costs no atomic);
+  // lower the stored first position if this tile's is smaller (it only ever
+  // decreases, so a stale read errs on the side of the atomic); add the
+  // tile's count, whose old value is the rank base of the tile's occurrences.
+  constexpr int kPer = kDedupTile / kBlock;
+  int sl[kPer];
+  unsigned long long ke[kPer];
+  ScratchSlot cur[kPer];
 #pragma unroll
-  for (int j = 0; j < kOwn; ++j) {
-    if (ke[j] == kEncEmpty) continue;
-    const uint64_t h = scratch_hash(ke[j]) & sc.mask;
-    if (cur[j].key == ke[j]) {
-      gs[j] = static_cast<int64_t>(h);
-    } else if (cur[j].key == kEncEmpty) {
-      const unsigned long long old = atomicCAS(&sc.slot[h].key, kEncEmpty, ke[j]);
-      if (old == kEncEmpty || old == ke[j]) {
-        gs[j] = static_cast<int64_t>(h);
-        cur[j].first = 0xFFFFFFFFu;  // not read: always take the atomicMin
-      }
+  for (int r = 0; r < kPer; ++r) {
+    const int q = tid + r * kBlock;
+    sl[r] = q < d ? ldense[q] : -1;
+    ke[r] = sl[r] >= 0 ? lkey[sl[r]] : kEncEmpty;
+  }
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) cur[r] = sc.slot[scratch_hash(ke[r]) & sc.mask];  // idle lanes: one shared line
+  int64_t gs[kPer];
+  unsigned long long old[kPer];
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) {
+    old[r] = cur[r].key;
+    if (sl[r] >= 0 && cur[r].key == kEncEmpty)
+      old[r] = atomicCAS(&sc.slot[scratch_hash(ke[r]) & sc.mask].key, kEncEmpty, ke[r]);
+  }
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) {
+    gs[r] = -1;
+    if (sl[r] < 0) continue;
+    if (old[r] == ke[r] || old[r] == kEncEmpty) {
+      gs[r] = static_cast<int64_t>(scratch_hash(ke[r]) & sc.mask);
+      if (old[r] == kEncEmpty) cur[r].first = 0xFFFFFFFFu;  // claimed here: always take the atomicMin
     }
   }
 #pragma unroll
-  for (int j = 0; j < kOwn; ++j) {
-    if (ke[j] == kEncEmpty || gs[j] >= 0) continue;
-    gs[j] = scratch_claim(sc, ke[j]);
-    cur[j].first = 0xFFFFFFFFu;
-    if (gs[j] < 0) atomicOr(err, kErrScratch);
+  for (int r = 0; r < kPer; ++r) {
+    if (sl[r] < 0 || gs[r] >= 0) continue;
+    gs[r] = scratch_claim(sc, ke[r]);  // collision: probe on (rare)
+    cur[r].first = 0xFFFFFFFFu;
+    if (gs[r] < 0) atomicOr(err, kErrScratch);
   }
-  unsigned int gb[kOwn];
+  unsigned int mn[kPer], cn[kPer], gb[kPer];
 #pragma unroll
-  for (int j = 0; j < kOwn; ++j) {
-    gb[j] = 0;
-    if (gs[j] < 0) continue;
-    const int s = tid + j * kBlock;
-    if (cur[j].first > lmin[s]) atomicMin(&sc.slot[gs[j]].first, lmin[s]);
-    gb[j] = atomicAdd(&sc.slot[gs[j]].cnt, lcnt[s]);
+  for (int r = 0; r < kPer; ++r) {
+    mn[r] = sl[r] >= 0 ? lmin[sl[r]] : 0u;
+    cn[r] = sl[r] >= 0 ? lcnt[sl[r]] : 0u;
   }
 #pragma unroll
-  for (int j = 0; j < kOwn; ++j) {
-    const int s = tid + j * kBlock;
-    lgs[s] = static_cast<int>(gs[j]);
-    lbase[s] = gb[j];
+  for (int r = 0; r < kPer; ++r)
+    if (gs[r] >= 0 && cur[r].first > mn[r]) atomicMin(&sc.slot[gs[r]].first, mn[r]);
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) gb[r] = gs[r] >= 0 ? atomicAdd(&sc.slot[gs[r]].cnt, cn[r]) : 0u;
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) {
+    if (sl[r] < 0) continue;
+    lkey[sl[r]] = static_cast<unsigned long long>(gs[r]);
+    lcnt[sl[r]] = gb[r];
   }
   __syncthreads();
 #pragma unroll
   for (int k = 0; k < kDedupItems; ++k) {
     const int64_t i = base + k * kBlock + tid;
     if (i >= n) continue;
-    const int g = ls[k] >= 0 ? lgs[ls[k]] : -1;
+    const int g = ls[k] >= 0 ? static_cast<int>(static_cast<long long>(lkey[ls[k]])) : -1;
     const bool cand = g >= 0 && lmin[ls[k]] == static_cast<unsigned int>(i);
     slot_of[i] = g < 0 ? -1 : (g | (cand ? kCandBit : 0));
-    occ_rank[i] = g >= 0 ? static_cast<int>(lbase[ls[k]] + lr[k]) : 0;
+    occ_rank[i] = g >= 0 ? static_cast<int>(lcnt[ls[k]] + lr[k]) : 0;
   }
 }
 
@@ -205,28 +269,60 @@ __device__ inline void load4(const int32_t* __restrict__ p, int64_t i0, int64_t 
 
 __global__ __launch_bounds__(kBlock) void k_rank_probe(TableDev t, Scratch sc, int32_t* __restrict__ slot_of,
                                                        int64_t n, int32_t* __restrict__ bsum, int64_t ntiles) {
-  __shared__ int sh[kBlock / kWave + 1];
+  __shared__ int sh[kBlock / kWave + 1][5];
   const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kRankTile + threadIdx.x * kRankItems;
   int s[4];
   load4(slot_of, i0, n, s);
+  // every load of a step is issued before its results are waited for: the
+  // scratch slots of the tile-local firsts (other lanes read one shared
+  // slot), then the first IDMap probe batch of every first occurrence
   bool f[4];
   ScratchSlot ss[4];
-  int c = 0, cf = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const bool cand = s[k] >= 0 && (s[k] & kCandBit);
-    if (cand) ss[k] = sc.slot[s[k] & kSlotMask];
-    f[k] = cand && ss[k].first == static_cast<unsigned int>(i0 + k);
+    ss[k] = sc.slot[cand ? (s[k] & kSlotMask) : 0];
+    f[k] = cand;
+  }
+  int c = 0, cf = 0, nl = 0, nu = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    f[k] = f[k] && ss[k].first == static_cast<unsigned int>(i0 + k);
     if (f[k]) {
+      const int ck = static_cast<int>(ss[k].cnt);
       cf += 1;
-      c += static_cast<int>(ss[k].cnt);
+      c += ck;
+      if (ck > kLong) {
+        nl += 1;
+        nu += unit_count(ck);
+      }
     }
+  }
+  uint64_t h[4];
+  Slot pb[4][kProbeBatch];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    h[k] = f[k] ? idmap_hash(ss[k].key) & t.cap_mask : 0;
+#pragma unroll
+    for (int q = 0; q < kProbeBatch; ++q) pb[k][q] = t.slots[(h[k] + q) & t.cap_mask];
   }
   int nw = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     if (!f[k]) continue;
-    const int64_t r = idmap_lookup(t, ss[k].key);
+    int64_t r = -1;
+    bool done = false;
+#pragma unroll
+    for (int q = 0; q < kProbeBatch; ++q) {
+      if (done) continue;
+      if (pb[k][q].key == ss[k].key) {
+        r = pb[k][q].row;
+        done = true;
+      } else if (pb[k][q].key == kEncEmpty) {
+        done = true;
+      }
+    }
+    if (!done) r = idmap_lookup_at(t, ss[k].key, (h[k] + kProbeBatch) & t.cap_mask, kProbeBatch);
     ScratchAux* ax = &sc.aux[s[k] & kSlotMask];
     ax->row = r;
     ax->count = static_cast<int>(ss[k].cnt);
@@ -242,59 +338,76 @@ __global__ __launch_bounds__(kBlock) void k_rank_probe(TableDev t, Scratch sc, i
         if (f[k]) slot_of[i0 + k] = s[k] | kFirstBit;
     }
   }
-  const int a = block_sum<kBlock>(cf | (nw << 16), sh);
-  __syncthreads();
-  const int b = block_sum<kBlock>(c, sh);
-  if (threadIdx.x == 0) {
-    bsum[blockIdx.x] = a & 0xFFFF;
-    bsum[ntiles + blockIdx.x] = b;
-    bsum[2 * ntiles + blockIdx.x] = a >> 16;
-  }
+  const int v[5] = {cf, c, nw, nl, nu};
+  int ex[5], tot[5];
+  block_excl_scan5<kBlock>(v, ex, tot, sh);
+  if (threadIdx.x < 5) bsum[threadIdx.x * ntiles + blockIdx.x] = tot[threadIdx.x];
 }
 
 // ---------------------------------------------------------------------------
-// one-block scan of the three tile-sum arrays; row reservation
+// one-block scan of the five tile-sum arrays; row reservation
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(1024) void k_scan3(int32_t* __restrict__ bsum, int64_t nb, int64_t ntiles,
-                                                int64_t* cscal, int64_t* tscal) {
-  __shared__ int sh[1024 / kWave + 1];
-  const int64_t per = (nb + 1023) / 1024;
-  const int64_t lo = min(nb, static_cast<int64_t>(threadIdx.x) * per);
-  const int64_t hi = min(nb, lo + per);
-  int64_t totals[3];
+__device__ inline void publish_live(int64_t* h_live, int64_t tag, int64_t live) {
+  // one 8-byte store to pinned host memory: (call tag << 48) | live rows
+  if (h_live) {
+    *reinterpret_cast<volatile int64_t*>(h_live) = (tag << 48) | live;
+    __threadfence_system();
+  }
+}
+
+// One block scans the five tile-sum arrays (thread t owns R consecutive
+// tiles of each round of 1024 R tiles; all 5 R loads in flight together).
+template <int R>
+__global__ __launch_bounds__(1024) void k_scan5(int32_t* __restrict__ bsum, int64_t nb, int64_t ntiles,
+                                                int64_t* cscal, int64_t* tscal, int64_t* h_live, int64_t tag) {
+  __shared__ int sh[1024 / kWave + 1][5];
+  int64_t carry[5] = {0, 0, 0, 0, 0};
+  for (int64_t r0 = 0; r0 < nb; r0 += 1024 * R) {
+    const int64_t lo = r0 + static_cast<int64_t>(threadIdx.x) * R;
+    int v[5][R];
 #pragma unroll
-  for (int a = 0; a < 3; ++a) {
-    int32_t* p = bsum + a * ntiles;
-    int local = 0;
-    for (int64_t k = lo; k < hi; ++k) local += p[k];
-    int tot;
-    int run = block_excl_scan<1024>(local, sh, tot);
-    for (int64_t k = lo; k < hi; ++k) {
-      const int v = p[k];
-      p[k] = run;
-      run += v;
+    for (int a = 0; a < 5; ++a)
+#pragma unroll
+      for (int j = 0; j < R; ++j) v[a][j] = lo + j < nb ? bsum[a * ntiles + lo + j] : 0;
+    int local[5], ex[5], tot[5];
+#pragma unroll
+    for (int a = 0; a < 5; ++a) {
+      local[a] = 0;
+#pragma unroll
+      for (int j = 0; j < R; ++j) local[a] += v[a][j];
     }
-    totals[a] = tot;
+    block_excl_scan5<1024>(local, ex, tot, sh);
+#pragma unroll
+    for (int a = 0; a < 5; ++a) {
+      int run = ex[a] + static_cast<int>(carry[a]);
+#pragma unroll
+      for (int j = 0; j < R; ++j) {
+        if (lo + j < nb) bsum[a * ntiles + lo + j] = run;
+        run += v[a][j];
+      }
+      carry[a] += tot[a];
+    }
   }
   if (threadIdx.x != 0) return;
-  cscal[kCU] = totals[0];
-  cscal[kCValid] = totals[1];
-  cscal[kCNewReq] = totals[2];
-  cscal[kCNLong] = 0;
-  cscal[kCNUnits] = 0;
+  cscal[kCU] = carry[0];
+  cscal[kCValid] = carry[1];
+  cscal[kCNewReq] = carry[2];
+  cscal[kCNLong] = carry[3];
+  cscal[kCNUnits] = carry[4];
   const int64_t live = tscal[kTLive];
   const int64_t lim = min(tscal[kTLimit], tscal[kTRowCap]);
   const int64_t room = lim > live ? lim - live : 0;
-  const int64_t ins = totals[2] < room ? totals[2] : room;
+  const int64_t ins = carry[2] < room ? carry[2] : room;
   cscal[kCNew] = ins;
   cscal[kCBaseLive] = live;
-  cscal[kCTrunc] = totals[2] > room ? 1 : 0;
+  cscal[kCTrunc] = carry[2] > room ? 1 : 0;
   tscal[kTLive] = live + ins;
+  publish_live(h_live, tag, live + ins);
 }
 
 // After the host grew the table: reserve again from the same live count.
-__global__ void k_rereserve(int64_t* cscal, int64_t* tscal) {
+__global__ void k_rereserve(int64_t* cscal, int64_t* tscal, int64_t* h_live, int64_t tag) {
   const int64_t live = cscal[kCBaseLive], req = cscal[kCNewReq];
   const int64_t lim = min(tscal[kTLimit], tscal[kTRowCap]);
   const int64_t room = lim > live ? lim - live : 0;
@@ -302,7 +415,10 @@ __global__ void k_rereserve(int64_t* cscal, int64_t* tscal) {
   cscal[kCNew] = ins;
   cscal[kCTrunc] = req > room ? 1 : 0;
   tscal[kTLive] = live + ins;
+  publish_live(h_live, tag, live + ins);
 }
+
+__global__ void k_zero_scalars(int64_t* cscal) { cscal[threadIdx.x] = 0; }
 
 __global__ void k_scratch_clear(ScratchSlot* slots, int64_t n) {
   for (int64_t i = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x; i < n;
@@ -315,15 +431,16 @@ hipError_t launch_scratch_clear(ScratchSlot* slots, int64_t n, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_rereserve(const Work& w, const TableDev& t, hipStream_t s) {
-  k_rereserve<<<1, 1, 0, s>>>(w.scal, t.scal);
+hipError_t launch_rereserve(const Work& w, const TableDev& t, int64_t* h_live, int64_t tag, hipStream_t s) {
+  k_rereserve<<<1, 1, 0, s>>>(w.scal, t.scal, h_live, tag);
   return hipGetLastError();
 }
 
 hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const Scratch& sc, const TableDev& t, const Work& w,
-                              hipEvent_t* ev_local, hipEvent_t* ev_probe, hipStream_t s) {
+                              int64_t* h_live, int64_t tag, hipEvent_t* ev_local, hipEvent_t* ev_probe,
+                              hipStream_t s) {
   if (n <= 0) {
-    (void)hipMemsetAsync(w.scal, 0, sizeof(int64_t) * kCScalars, s);
+    k_zero_scalars<<<1, kCScalars, 0, s>>>(w.scal);
     return hipGetLastError();
   }
   const int64_t nb = (n + kRankTile - 1) / kRankTile;
@@ -334,7 +451,10 @@ hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const Scratch& s
   if (ev_probe && ev_probe[0]) (void)hipEventRecord(ev_probe[0], s);
   k_rank_probe<<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, sc, w.slot_of, n, w.bsum, w.ntiles);
   if (ev_probe && ev_probe[1]) (void)hipEventRecord(ev_probe[1], s);
-  k_scan3<<<1, 1024, 0, s>>>(w.bsum, nb, w.ntiles, w.scal, t.scal);
+  if (nb <= 1024) k_scan5<1><<<1, 1024, 0, s>>>(w.bsum, nb, w.ntiles, w.scal, t.scal, h_live, tag);
+  else if (nb <= 2048) k_scan5<2><<<1, 1024, 0, s>>>(w.bsum, nb, w.ntiles, w.scal, t.scal, h_live, tag);
+  else if (nb <= 4096) k_scan5<4><<<1, 1024, 0, s>>>(w.bsum, nb, w.ntiles, w.scal, t.scal, h_live, tag);
+  else k_scan5<8><<<1, 1024, 0, s>>>(w.bsum, nb, w.ntiles, w.scal, t.scal, h_live, tag);
   return hipGetLastError();
 }
 
@@ -344,29 +464,43 @@ hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const Scratch& s
 
 __global__ __launch_bounds__(kBlock) void k_compact_insert(TableDev t, Scratch sc, Work w,
                                                            const int64_t* __restrict__ values, int64_t n) {
-  __shared__ int sh[kBlock / kWave + 1];
+  __shared__ int sh[kBlock / kWave + 1][5];
   const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kRankTile + threadIdx.x * kRankItems;
+  const int b = blockIdx.x;
+  int pre[5];  // the tile's exclusive prefixes (first, count, new, hot, units)
+#pragma unroll
+  for (int a = 0; a < 5; ++a) pre[a] = w.bsum[a * w.ntiles + b];
   int s[4];
   load4(w.slot_of, i0, n, s);
   bool f[4];
   ScratchAux ax0[4];
-  int cf = 0, cc = 0, cn = 0;
+  int cf = 0, cc = 0, cn = 0, cl = 0, cu = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     f[k] = s[k] >= 0 && (s[k] & kFirstBit);
     s[k] &= kSlotMask;
-    if (f[k]) ax0[k] = sc.aux[s[k]];
+    ax0[k] = sc.aux[f[k] ? s[k] : 0];  // all four reads in flight together
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
     cf += f[k];
     cc += f[k] ? ax0[k].count : 0;
     cn += (f[k] && ax0[k].row < 0);
+    if (f[k] && ax0[k].count > kLong) {
+      cl += 1;
+      cu += unit_count(ax0[k].count);
+    }
   }
-  int tot;
-  const int ex_a = block_excl_scan<kBlock>(cf | (cn << 16), sh, tot);
-  const int ex_c = block_excl_scan<kBlock>(cc, sh, tot);
-  const int b = blockIdx.x;
-  int uid = w.bsum[b] + (ex_a & 0xFFFF);
-  int start = w.bsum[w.ntiles + b] + ex_c;
-  int64_t nr = w.bsum[2 * w.ntiles + b] + (ex_a >> 16);
+  // the tile's first occurrences get consecutive unique ids, segments, rows
+  // of new keys, hot-key indices and backward units
+  const int v[5] = {cf, cc, cn, cl, cu};
+  int ex[5], tot[5];
+  block_excl_scan5<kBlock>(v, ex, tot, sh);
+  int uid = pre[0] + ex[0];
+  int start = pre[1] + ex[1];
+  int64_t nr = pre[2] + ex[2];
+  int lnext = pre[3] + ex[3];
+  int unext = pre[4] + ex[4];
   const int64_t inserted = w.scal[kCNew];
   const int64_t live0 = w.scal[kCBaseLive];
   if (blockIdx.x == 0 && threadIdx.x == 0 && w.scal[kCTrunc]) atomicOr(reinterpret_cast<int*>(&t.scal[kTErr]), kErrFull);
@@ -378,16 +512,11 @@ __global__ __launch_bounds__(kBlock) void k_compact_insert(TableDev t, Scratch s
     w.unique[uid] = values[i0 + k];
     int li = -1, ush = 0;
     if (c > kLong) {
-      li = static_cast<int>(atomicAdd(reinterpret_cast<unsigned long long*>(&w.scal[kCNLong]), 1ull));
-      while ((c - 1) >> (ush + kUnitLog2) >= kMaxUnits) ++ush;  // ceil(c / (kUnit << ush)) <= kMaxUnits
-      const int usz = kUnit << ush;
-      const int units = (c + usz - 1) / usz;
-      const int us = static_cast<int>(
-          atomicAdd(reinterpret_cast<unsigned long long*>(&w.scal[kCNUnits]), static_cast<unsigned long long>(units)));
+      li = lnext++;
+      ush = unit_shift(c);
       w.long_u[li] = uid;
-      w.long_start[li] = us;
-      float4* gp = reinterpret_cast<float4*>(w.gpart + static_cast<int64_t>(li) * t.dim);
-      for (int j = 0; j < t.dim / 4; ++j) gp[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+      w.long_start[li] = unext;
+      unext += unit_count(c);
     }
     int64_t row = ax0[k].row;
     if (row < 0) {
@@ -429,15 +558,15 @@ __device__ inline float init_value(uint64_t z, int j, float lo, float span) {
 }
 
 // Lane groups of 16 write the rows of the inserted keys: w from the init
-// formula, optimizer state zero, 16 bytes per lane per store.
-__global__ __launch_bounds__(kBlock) void k_init_rows(TableDev t, Work w) {
+// formula, optimizer state zero, 16 bytes per lane per store.  Block `blk`
+// of `nblk` takes every nblk-th group of keys.
+__device__ inline void init_rows(const TableDev& t, const Work& w, int64_t blk, int64_t nblk) {
   constexpr int G = 16;
   const int lane = threadIdx.x % G, grp = threadIdx.x / G;
   const int64_t inserted = w.scal[kCNew];
   const int chunks = static_cast<int>(t.store.stride / 16);
   const int wbytes = t.dim * (t.row_dtype ? 2 : 4);
-  for (int64_t q = static_cast<int64_t>(blockIdx.x) * (kBlock / G) + grp; q < inserted;
-       q += static_cast<int64_t>(gridDim.x) * (kBlock / G)) {
+  for (int64_t q = blk * (kBlock / G) + grp; q < inserted; q += nblk * (kBlock / G)) {
     const int u = w.new_list[q];
     const int64_t row = w.useg[u].row;
     const uint64_t z = mix64(static_cast<uint64_t>(w.unique[u]) ^ mix64(t.seed));
@@ -473,18 +602,18 @@ __global__ __launch_bounds__(kBlock) void k_init_rows(TableDev t, Work w) {
 // (OCC) it also writes each occurrence's row and its position in the
 // occurrence list, and the descriptor of every backward unit of a hot key.
 template <bool OCC>
-__global__ __launch_bounds__(kBlock) void k_occ(Scratch sc, Work w, int64_t n) {
-  const int64_t i0 = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * 4;
+__device__ inline void occ_pass(const Scratch& sc, const Work& w, int64_t n, int64_t blk) {
+  const int64_t i0 = (blk * kBlock + threadIdx.x) * 4;
   if (i0 >= n) return;
   int s[4], rk[4];
   load4(w.slot_of, i0, n, s);
   load4(w.occ_rank, i0, n, rk);
   ScratchAux a[4];
 #pragma unroll
+  for (int k = 0; k < 4; ++k) a[k] = sc.aux[s[k] >= 0 ? (s[k] & kSlotMask) : 0];  // all in flight together
+#pragma unroll
   for (int k = 0; k < 4; ++k) {
-    if (s[k] >= 0) {
-      a[k] = sc.aux[s[k] & kSlotMask];
-    } else {
+    if (s[k] < 0) {
       a[k].row = -1;
       a[k].uid = -1;
       a[k].start = 0;
@@ -525,6 +654,16 @@ __global__ __launch_bounds__(kBlock) void k_occ(Scratch sc, Work w, int64_t n) {
   }
 }
 
+// The last pass of a lookup: blocks [0, occ_blocks) run the per-occurrence
+// pass, the others write the rows of the inserted keys (both only need the
+// compaction, so they share one launch).
+template <bool OCC>
+__global__ __launch_bounds__(kBlock) void k_occ_init(Scratch sc, TableDev t, Work w, int64_t n, int64_t occ_blocks) {
+  const int64_t b = blockIdx.x;
+  if (b < occ_blocks) occ_pass<OCC>(sc, w, n, b);
+  else init_rows(t, w, b - occ_blocks, static_cast<int64_t>(gridDim.x) - occ_blocks);
+}
+
 hipError_t launch_compact_insert(const int64_t* values, int64_t n, const Scratch& sc, const TableDev& t, const Work& w,
                                  bool occ_lists, hipEvent_t* ev_compact, hipEvent_t* ev_init, hipEvent_t* ev_occ,
                                  hipStream_t s) {
@@ -533,13 +672,16 @@ hipError_t launch_compact_insert(const int64_t* values, int64_t n, const Scratch
   if (ev_compact && ev_compact[0]) (void)hipEventRecord(ev_compact[0], s);
   k_compact_insert<<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, sc, w, values, n);
   if (ev_compact && ev_compact[1]) (void)hipEventRecord(ev_compact[1], s);
+  // one launch: the per-occurrence pass and the new rows (the init-rows and
+  // occurrence events both bracket it)
   if (ev_init && ev_init[0]) (void)hipEventRecord(ev_init[0], s);
-  k_init_rows<<<grid_for(n, kBlock / 16, 8192), kBlock, 0, s>>>(t, w);
-  if (ev_init && ev_init[1]) (void)hipEventRecord(ev_init[1], s);
   if (ev_occ && ev_occ[0]) (void)hipEventRecord(ev_occ[0], s);
-  if (occ_lists) k_occ<true><<<grid_for(n, kBlock * 4, 1ll << 31), kBlock, 0, s>>>(sc, w, n);
-  else k_occ<false><<<grid_for(n, kBlock * 4, 1ll << 31), kBlock, 0, s>>>(sc, w, n);
+  const int64_t ob = grid_for(n, kBlock * 4, 1ll << 31);
+  const int64_t ib = grid_for(n, kBlock / 16, 8192);
+  if (occ_lists) k_occ_init<true><<<static_cast<unsigned>(ob + ib), kBlock, 0, s>>>(sc, t, w, n, ob);
+  else k_occ_init<false><<<static_cast<unsigned>(ob + ib), kBlock, 0, s>>>(sc, t, w, n, ob);
   if (ev_occ && ev_occ[1]) (void)hipEventRecord(ev_occ[1], s);
+  if (ev_init && ev_init[1]) (void)hipEventRecord(ev_init[1], s);
   return hipGetLastError();
 }
 

@@ -34,16 +34,24 @@ constexpr int kRankTile = kBlock * kRankItems;  // 1024
 constexpr int kProbeBatch = 4;
 
 // Backward: a key with at most kLong occurrences is reduced by one lane
-// group; a longer ("hot") key is cut into units of kUnit positions whose
-// partial sums are added into a per-key partial row.
+// group; a longer ("hot") key is cut into units of kUnit positions, each
+// writing a partial sum row that one block per key then adds up.
 constexpr int kLong = 32;
 constexpr int kUnit = 32;
 constexpr int kUnitLog2 = 5;
 static_assert(kUnit == 1 << kUnitLog2, "kUnit is a power of two");
 // A key with more than kUnit * kMaxUnits occurrences gets units of
-// kUnit << shift positions, so no partial row receives more than kMaxUnits
-// atomic adds per element.
+// kUnit << shift positions, so no key has more than kMaxUnits partial rows.
 constexpr int kMaxUnits = 1024;
+__host__ __device__ inline int unit_shift(int count) {
+  int sh = 0;
+  while ((count - 1) >> (sh + kUnitLog2) >= kMaxUnits) ++sh;
+  return sh;
+}
+__host__ __device__ inline int unit_count(int count) {
+  const int usz = kUnit << unit_shift(count);
+  return (count + usz - 1) / usz;
+}
 
 // Grid of the grid-stride kernels that loop over a device-side count: 8
 // blocks of 256 threads per CU on 256 CUs.
@@ -160,9 +168,9 @@ struct Work {
   int32_t* long_u;      // [n/kLong + 1] unique id of each hot key
   int32_t* long_start;  // [n/kLong + 1] first backward unit of each hot key
   Unit* units;          // [2n/kUnit + 2] backward units of the hot keys
-  int32_t* bsum;        // [3 * ntiles] tile sums: first occurrences, their counts, new keys
+  int32_t* bsum;        // [5 * ntiles] tile sums: first occurrences, their counts, new keys, hot keys, units
   int64_t* scal;        // [kCScalars]
-  float* gpart;         // [(n/kLong + 1) * D] partial gradient rows of hot keys
+  float* gpart;         // [(2n/kUnit + 2) * D] partial gradient row of each backward unit
   int64_t ntiles;       // tiles of the rank passes (bsum stride)
 };
 
@@ -175,8 +183,12 @@ struct OptArgs {
 // launchers; all enqueue on `s` and return hipGetLastError()
 // ---------------------------------------------------------------------------
 // dedup + IDMap probe of first occurrences + 3-way scan (ends before the insert)
+// The scan also stores (tag << 48) | (live rows after the call) to h_live
+// (pinned host memory; may be null), so the host can refresh its bound on
+// the live count without a copy or an event.
 hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const Scratch& sc, const TableDev& t,
-                              const Work& w, hipEvent_t* ev_local, hipEvent_t* ev_probe, hipStream_t s);
+                              const Work& w, int64_t* h_live, int64_t tag, hipEvent_t* ev_local,
+                              hipEvent_t* ev_probe, hipStream_t s);
 // unique / segments / rows / IDMap insert / row init, then the per-occurrence
 // pass: inverse[], scratch release and, for a forward (occ_lists), each
 // occurrence's row and list position and the hot keys' backward units
@@ -186,7 +198,7 @@ hipError_t launch_compact_insert(const int64_t* values, int64_t n, const Scratch
 // set every scratch slot to empty
 hipError_t launch_scratch_clear(ScratchSlot* slots, int64_t n, hipStream_t s);
 // redo the row reservation of the last scan after the table has grown
-hipError_t launch_rereserve(const Work& w, const TableDev& t, hipStream_t s);
+hipError_t launch_rereserve(const Work& w, const TableDev& t, int64_t* h_live, int64_t tag, hipStream_t s);
 hipError_t launch_map_rows(const Work& w, int64_t n, int64_t* rows_out, int64_t* n_inserted, hipStream_t s);
 hipError_t launch_find(const TableDev& t, const int64_t* keys, int64_t n, int64_t* rows_out, hipStream_t s);
 hipError_t launch_pool(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int64_t bags, int mode,
