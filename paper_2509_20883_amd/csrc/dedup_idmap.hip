@@ -120,34 +120,37 @@ __device__ inline void block_excl_scan5(const int (&v)[5], int (&ex)[5], int (&t
 // pass 1: tile-local dedup in LDS, then the global scratch set
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(kBlock) void k_dedup_local(const int64_t* __restrict__ values, int64_t n, Scratch sc,
+template <int NT>
+__global__ __launch_bounds__(NT) void k_dedup_local(const int64_t* __restrict__ values, int64_t n, Scratch sc,
                                                         int32_t* __restrict__ slot_of, int32_t* __restrict__ occ_rank,
                                                         int* err) {
+  constexpr int TILE = NT * kDedupItems;  // occurrences per block
+  constexpr int SLOTS = 2 * TILE;         // LDS hash slots (load <= 0.5)
   // lkey: the key, then (read only by the slot's owner in between) its
   // scratch slot; lcnt: the count, then the global rank base of the tile's
   // occurrences of the key
-  __shared__ unsigned long long lkey[kDedupLdsSlots];
-  __shared__ unsigned int lmin[kDedupLdsSlots];
-  __shared__ unsigned int lcnt[kDedupLdsSlots];
-  __shared__ short ldense[kDedupTile];  // the tile's distinct keys: dense index -> LDS slot
-  __shared__ int sh[kBlock / kWave + 1];
+  __shared__ unsigned long long lkey[SLOTS];
+  __shared__ unsigned int lmin[SLOTS];
+  __shared__ unsigned int lcnt[SLOTS];
+  __shared__ short ldense[TILE];  // the tile's distinct keys: dense index -> LDS slot
+  __shared__ int sh[NT / kWave + 1];
   const int tid = threadIdx.x;
-  for (int s = tid; s < kDedupLdsSlots; s += kBlock) {
+  for (int s = tid; s < SLOTS; s += NT) {
     lkey[s] = kEncEmpty;
     lmin[s] = 0xFFFFFFFFu;
     lcnt[s] = 0u;
   }
   // every load is issued before the first wait (n > 0: indices are clamped)
-  const int64_t base = static_cast<int64_t>(blockIdx.x) * kDedupTile;
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * TILE;
   int64_t raw[kDedupItems];
 #pragma unroll
-  for (int k = 0; k < kDedupItems; ++k) raw[k] = values[min(base + k * kBlock + tid, n - 1)];
+  for (int k = 0; k < kDedupItems; ++k) raw[k] = values[min(base + k * NT + tid, n - 1)];
   __syncthreads();
   int ls[kDedupItems];
   unsigned int lr[kDedupItems];
 #pragma unroll
   for (int k = 0; k < kDedupItems; ++k) {
-    const int64_t i = base + k * kBlock + tid;
+    const int64_t i = base + k * NT + tid;
     const unsigned long long e = static_cast<unsigned long long>(raw[k]) ^ kSign;
     ls[k] = -1;
     lr[k] = 0;
@@ -156,11 +159,11 @@ __global__ __launch_bounds__(kBlock) void k_dedup_local(const int64_t* __restric
       atomicOr(err, kErrKey);
       continue;
     }
-    unsigned int h = static_cast<unsigned int>(mix64(e) >> 40) & (kDedupLdsSlots - 1);
-    while (true) {  // at most kDedupTile keys in twice as many slots: terminates
+    unsigned int h = static_cast<unsigned int>(mix64(e) >> 40) & (SLOTS - 1);
+    while (true) {  // at most TILE keys in twice as many slots: terminates
       const unsigned long long old = atomicCAS(&lkey[h], kEncEmpty, e);
       if (old == kEncEmpty || old == e) break;
-      h = (h + 1) & (kDedupLdsSlots - 1);
+      h = (h + 1) & (SLOTS - 1);
     }
     atomicMin(&lmin[h], static_cast<unsigned int>(i));
     lr[k] = atomicAdd(&lcnt[h], 1u);
@@ -169,12 +172,12 @@ __global__ __launch_bounds__(kBlock) void k_dedup_local(const int64_t* __restric
   __syncthreads();
   // Dense list of the occupied slots, so a wavefront's global phase runs as
   // few rounds as the tile has distinct keys per thread (not one per slot).
-  constexpr int kOwn = kDedupLdsSlots / kBlock;
+  constexpr int kOwn = SLOTS / NT;
   int occ = 0;
 #pragma unroll
   for (int j = 0; j < kOwn; ++j) occ += lkey[tid * kOwn + j] != kEncEmpty;
   int d;
-  int at = block_excl_scan<kBlock>(occ, sh, d);
+  int at = block_excl_scan<NT>(occ, sh, d);
 #pragma unroll
   for (int j = 0; j < kOwn; ++j)
     if (lkey[tid * kOwn + j] != kEncEmpty) ldense[at++] = static_cast<short>(tid * kOwn + j);
@@ -185,13 +188,13 @@ __global__ __launch_bounds__(kBlock) void k_dedup_local(const int64_t* __restric
   // lower the stored first position if this tile's is smaller (it only ever
   // decreases, so a stale read errs on the side of the atomic); add the
   // tile's count, whose old value is the rank base of the tile's occurrences.
-  constexpr int kPer = kDedupTile / kBlock;
+  constexpr int kPer = TILE / NT;
   int sl[kPer];
   unsigned long long ke[kPer];
   ScratchSlot cur[kPer];
 #pragma unroll
   for (int r = 0; r < kPer; ++r) {
-    const int q = tid + r * kBlock;
+    const int q = tid + r * NT;
     sl[r] = q < d ? ldense[q] : -1;
     ke[r] = sl[r] >= 0 ? lkey[sl[r]] : kEncEmpty;
   }
@@ -241,7 +244,7 @@ __global__ __launch_bounds__(kBlock) void k_dedup_local(const int64_t* __restric
   __syncthreads();
 #pragma unroll
   for (int k = 0; k < kDedupItems; ++k) {
-    const int64_t i = base + k * kBlock + tid;
+    const int64_t i = base + k * NT + tid;
     if (i >= n) continue;
     const int g = ls[k] >= 0 ? static_cast<int>(static_cast<long long>(lkey[ls[k]])) : -1;
     const bool cand = g >= 0 && lmin[ls[k]] == static_cast<unsigned int>(i);
@@ -445,7 +448,8 @@ hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const Scratch& s
   }
   const int64_t nb = (n + kRankTile - 1) / kRankTile;
   if (ev_local && ev_local[0]) (void)hipEventRecord(ev_local[0], s);
-  k_dedup_local<<<grid_for(n, kDedupTile, 1ll << 31), kBlock, 0, s>>>(values, n, sc, w.slot_of, w.occ_rank,
+  k_dedup_local<kDedupThreads><<<grid_for(n, kDedupThreads * kDedupItems, 1ll << 31), kDedupThreads, 0, s>>>(
+      values, n, sc, w.slot_of, w.occ_rank,
                                                                      reinterpret_cast<int*>(t.scal + kTErr));
   if (ev_local && ev_local[1]) (void)hipEventRecord(ev_local[1], s);
   if (ev_probe && ev_probe[0]) (void)hipEventRecord(ev_probe[0], s);

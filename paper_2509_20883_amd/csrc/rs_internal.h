@@ -19,10 +19,10 @@ constexpr unsigned long long kEncEmpty = 0ull;
 constexpr unsigned long long kEncTomb = 1ull;
 
 // Dedup: a block dedups a tile of occurrences in LDS before touching the
-// global scratch table, so a hot key costs one global atomic per tile.
+// global scratch table, so a key costs one global insert per tile it occurs
+// in: 1024 threads x 4 occurrences per tile, 8192 LDS hash slots (136 KB).
 constexpr int kDedupItems = 4;
-constexpr int kDedupTile = kBlock * kDedupItems;  // 1024 occurrences
-constexpr int kDedupLdsSlots = 2 * kDedupTile;    // load <= 0.5
+constexpr int kDedupThreads = 1024;
 
 // Tile of the two passes that rank first occurrences (4 consecutive items
 // per thread: many resident waves for these latency-bound passes).
