@@ -46,7 +46,7 @@ bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
 // Workspace layout of one forward: every array sized by the upper bound n.
 struct Layout {
   size_t slot_of, occ_rank, inverse, occ_row, occ_pos, unique, useg, rows, new_list, occ_ref, long_u, long_start,
-      units, bsum, scal, gpart, total;
+      units, bsum, csum, scal, gpart, total;
   int64_t ntiles;
 };
 
@@ -71,11 +71,12 @@ Layout make_layout(int64_t n, int dim) {
   L.useg = take(sizeof(Seg) * n1);
   L.rows = take(8 * n1);
   L.new_list = take(4 * n1);
-  L.occ_ref = take(4 * n1);
+  L.occ_ref = take(8 * n1);  // int32 per position, or {int32, float} for mean pooling
   L.long_u = take(4 * nlong);
   L.long_start = take(4 * nlong);
   L.units = take(sizeof(Unit) * nunit);
   L.bsum = take(4 * 5 * static_cast<size_t>(L.ntiles));
+  L.csum = take(4 * 5 * static_cast<size_t>(L.ntiles / kScanChunk + 1));
   L.scal = take(8 * kCScalars);
   L.gpart = take(4 * nunit * static_cast<size_t>(dim));
   L.total = off;
@@ -95,10 +96,12 @@ Work make_work(void* base, const Layout& L) {
   w.rows = reinterpret_cast<int64_t*>(b + L.rows);
   w.new_list = reinterpret_cast<int32_t*>(b + L.new_list);
   w.occ_ref = reinterpret_cast<int32_t*>(b + L.occ_ref);
+  w.occ_rs = reinterpret_cast<int2*>(b + L.occ_ref);
   w.long_u = reinterpret_cast<int32_t*>(b + L.long_u);
   w.long_start = reinterpret_cast<int32_t*>(b + L.long_start);
   w.units = reinterpret_cast<Unit*>(b + L.units);
   w.bsum = reinterpret_cast<int32_t*>(b + L.bsum);
+  w.csum = reinterpret_cast<int32_t*>(b + L.csum);
   w.scal = reinterpret_cast<int64_t*>(b + L.scal);
   w.gpart = reinterpret_cast<float*>(b + L.gpart);
   w.ntiles = L.ntiles;

@@ -71,10 +71,17 @@ __device__ inline void sum_positions(const Work& w, const GT* __restrict__ grad,
   constexpr int NR = (kUnit + LANES - 1) / LANES;  // positions per lane
   constexpr int kBatch = E == 4 ? 16 : 8;          // gradient rows in flight
   int myref[NR];
+  float mysc[NR];
 #pragma unroll
   for (int k = 0; k < NR; ++k) {
     const int q = k * LANES + lane;
-    myref[k] = q < cnt ? w.occ_ref[p0 + q] : -1;
+    if (MODE == 1) {
+      const int2 rs = q < cnt ? w.occ_rs[p0 + q] : make_int2(-1, 0);
+      myref[k] = rs.x;
+      mysc[k] = __int_as_float(rs.y);
+    } else {
+      myref[k] = q < cnt ? w.occ_ref[p0 + q] : -1;
+    }
   }
 #pragma unroll
   for (int q0 = 0; q0 < kUnit; q0 += kBatch) {
@@ -99,8 +106,8 @@ __device__ inline void sum_positions(const Work& w, const GT* __restrict__ grad,
     if (MODE == 1) {
 #pragma unroll
       for (int j = 0; j < kBatch; ++j) {
-        if (ref[j] < 0) continue;
-        const float sc = 1.0f / static_cast<float>(offsets[ref[j] + 1] - offsets[ref[j]]);
+        const int q = q0 + j;
+        const float sc = LANES > 1 ? __shfl(mysc[q / LANES], q % LANES, LANES) : mysc[q];
 #pragma unroll
         for (int k = 0; k < E; ++k) x[j][k] *= sc;
       }
@@ -112,7 +119,94 @@ __device__ inline void sum_positions(const Work& w, const GT* __restrict__ grad,
   }
 }
 
-// Keys with at most kLong occurrences, one lane group each; block `blk` of
+// Sum of the gradient rows of K segments of the occurrence list
+// ([st[k], st[k] + ct[k]), ct[k] <= kLong), taken as one sequence of at most
+// K * kLong positions: the lanes load the positions' gradient-row indices
+// together, share them by shuffles, and read the rows kBatch at a time, each
+// added into its segment's accumulator.
+template <typename GT, int E, int LANES, int MODE, int K>
+__device__ inline void sum_segments(const Work& w, const GT* __restrict__ grad, const int (&st)[K], const int (&ct)[K],
+                                    int lane, float (&acc)[K][E]) {
+  constexpr int D = LANES * E;
+  constexpr int MAXP = K * kLong;
+  constexpr int NR = (MAXP + LANES - 1) / LANES;  // positions per lane
+  constexpr int kBatch = E == 4 ? 16 : 8;          // gradient rows in flight
+  int pre[K + 1];
+  pre[0] = 0;
+#pragma unroll
+  for (int k = 0; k < K; ++k) pre[k + 1] = pre[k] + ct[k];
+  const int T = pre[K];
+  int myref[NR];
+  float mysc[NR];
+#pragma unroll
+  for (int j = 0; j < NR; ++j) {
+    const int tq = j * LANES + lane;
+    int kk = 0;
+#pragma unroll
+    for (int k = 1; k < K; ++k) kk += tq >= pre[k];
+    const bool valid = tq < T;
+    int sk = st[0], pk = 0;  // select, not a runtime index (keeps st / pre in registers)
+#pragma unroll
+    for (int k = 1; k < K; ++k)
+      if (kk == k) {
+        sk = st[k];
+        pk = pre[k];
+      }
+    const int p = valid ? sk + (tq - pk) : 0;
+    if (MODE == 1) {
+      const int2 rs = valid ? w.occ_rs[p] : make_int2(-1, 0);
+      myref[j] = rs.x;
+      mysc[j] = __int_as_float(rs.y);
+    } else {
+      myref[j] = valid ? w.occ_ref[p] : -1;
+    }
+  }
+#pragma unroll
+  for (int q0 = 0; q0 < MAXP; q0 += kBatch) {
+    if (q0 >= T) break;
+    int ref[kBatch], kq[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int tq = q0 + j;
+      const int r = LANES > 1 ? __shfl(myref[tq / LANES], tq % LANES, LANES) : myref[tq];
+      ref[j] = tq < T ? r : -1;
+      int kk = 0;
+#pragma unroll
+      for (int k = 1; k < K; ++k) kk += tq >= pre[k];
+      kq[j] = kk;
+    }
+    float x[kBatch][E];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      if (ref[j] >= 0) {
+        load_vals<GT, E>(grad + static_cast<int64_t>(ref[j]) * D + lane * E, x[j]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e) x[j][e] = 0.f;
+      }
+    }
+    if (MODE == 1) {
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const int tq = q0 + j;
+        const float sc = LANES > 1 ? __shfl(mysc[tq / LANES], tq % LANES, LANES) : mysc[tq];
+#pragma unroll
+        for (int e = 0; e < E; ++e) x[j][e] *= sc;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j)
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const bool hit = kq[j] == k;  // a select per accumulator, not an indexed access
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[k][e] += hit ? x[j][e] : 0.f;
+      }
+  }
+}
+
+// Keys with at most kLong occurrences: a lane group takes kShortKeys
+// consecutive keys per iteration (their loads interleaved); block `blk` of
 // `nblk` takes every nblk-th group of keys.
 template <typename WT, typename GT, int LANES, int MODE, bool FUSED>
 __device__ inline void bwd_short(const TableDev& t, const Work& w, const int64_t* __restrict__ offsets,
@@ -121,26 +215,42 @@ __device__ inline void bwd_short(const TableDev& t, const Work& w, const int64_t
   constexpr int E = 16 / static_cast<int>(sizeof(GT));
   constexpr int GPB = kBlock / LANES;
   constexpr int D = LANES * E;
+  constexpr int K = E == 4 ? kShortKeys : 1;  // bf16 gradient rows: one key (register budget)
   const int lane = threadIdx.x % LANES;
   const int grp = threadIdx.x / LANES;
   const int64_t U = w.scal[kCU];
-  for (int64_t u = blk * GPB + grp; u < U; u += nblk * GPB) {
-    const Seg sg = w.useg[u];
-    if (sg.count > kLong) continue;  // a hot key: k_bwd_long
-    RowFrag<WT, E> fr;
-    uint8_t* rp = nullptr;
-    if (FUSED && sg.row >= 0) {
-      rp = t.store.row(sg.row);
-      fr.load(rp, lane, D, t.nstate);  // in flight while the gradients are read
-    }
-    float acc[E];
+  for (int64_t u0 = (blk * GPB + grp) * K; u0 < U; u0 += nblk * GPB * K) {
+    Seg sg[K];
 #pragma unroll
-    for (int k = 0; k < E; ++k) acc[k] = 0.f;
-    sum_positions<GT, E, LANES, MODE>(w, grad, offsets, sg.start, sg.count, lane, acc);
+    for (int k = 0; k < K; ++k) sg[k] = w.useg[min(u0 + k, U - 1)];
+    int st[K], ct[K];
+    bool act[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      act[k] = u0 + k < U && sg[k].count <= kLong;  // hot keys: k_bwd_long
+      st[k] = sg[k].start;
+      ct[k] = act[k] ? sg[k].count : 0;
+    }
+    RowFrag<WT, E> fr[K];
     if (FUSED) {
-      if (rp) fr.update_store(rp, lane, D, acc, o);
-    } else {
-      store_vals<float, E>(grad_unique + u * D + lane * E, acc);
+#pragma unroll
+      for (int k = 0; k < K; ++k)  // in flight while the gradients are read
+        if (act[k] && sg[k].row >= 0) fr[k].load(t.store.row(sg[k].row), lane, D, t.nstate);
+    }
+    float acc[K][E];
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[k][e] = 0.f;
+    sum_segments<GT, E, LANES, MODE, K>(w, grad, st, ct, lane, acc);
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      if (!act[k]) continue;
+      if (FUSED) {
+        if (sg[k].row >= 0) fr[k].update_store(t.store.row(sg[k].row), lane, D, acc[k], o);
+      } else {
+        store_vals<float, E>(grad_unique + (u0 + k) * D + lane * E, acc[k]);
+      }
     }
   }
 }

@@ -34,11 +34,16 @@ __device__ inline int64_t idmap_lookup_at(const TableDev& t, unsigned long long 
     Slot sl[kProbeBatch];
 #pragma unroll
     for (int k = 0; k < kProbeBatch; ++k) sl[k] = t.slots[(h + k) & t.cap_mask];
+    int64_t r = -1;
+    bool fin = false;
 #pragma unroll
-    for (int k = 0; k < kProbeBatch; ++k) {
-      if (sl[k].key == e) return sl[k].row;
-      if (sl[k].key == kEncEmpty) return -1;
+    for (int k = 0; k < kProbeBatch; ++k) {  // selects only: the batch stays in registers
+      const bool hit = !fin && sl[k].key == e;
+      const bool empty = !fin && sl[k].key == kEncEmpty;
+      r = hit ? sl[k].row : r;
+      fin = fin || hit || empty;
     }
+    if (fin) return r;
     h = (h + kProbeBatch) & t.cap_mask;
   }
   return -1;
@@ -270,10 +275,12 @@ __device__ inline void load4(const int32_t* __restrict__ p, int64_t i0, int64_t 
   }
 }
 
-__global__ __launch_bounds__(kBlock) void k_rank_probe(TableDev t, Scratch sc, int32_t* __restrict__ slot_of,
-                                                       int64_t n, int32_t* __restrict__ bsum, int64_t ntiles) {
-  __shared__ int sh[kBlock / kWave + 1][5];
-  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kRankTile + threadIdx.x * kRankItems;
+template <int NT>
+__global__ __launch_bounds__(NT) void k_rank_probe(TableDev t, Scratch sc, int32_t* __restrict__ slot_of,
+                                                   int64_t n, int32_t* __restrict__ bsum, int64_t ntiles,
+                                                   int64_t* cscal) {
+  __shared__ int sh[NT / kWave + 1][5];
+  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * NT * kRankItems + threadIdx.x * kRankItems;
   int s[4];
   load4(slot_of, i0, n, s);
   // every load of a step is issued before its results are waited for: the
@@ -316,14 +323,11 @@ __global__ __launch_bounds__(kBlock) void k_rank_probe(TableDev t, Scratch sc, i
     int64_t r = -1;
     bool done = false;
 #pragma unroll
-    for (int q = 0; q < kProbeBatch; ++q) {
-      if (done) continue;
-      if (pb[k][q].key == ss[k].key) {
-        r = pb[k][q].row;
-        done = true;
-      } else if (pb[k][q].key == kEncEmpty) {
-        done = true;
-      }
+    for (int q = 0; q < kProbeBatch; ++q) {  // selects only: the batch stays in registers
+      const bool hit = !done && pb[k][q].key == ss[k].key;
+      const bool empty = !done && pb[k][q].key == kEncEmpty;
+      r = hit ? pb[k][q].row : r;
+      done = done || hit || empty;
     }
     if (!done) r = idmap_lookup_at(t, ss[k].key, (h[k] + kProbeBatch) & t.cap_mask, kProbeBatch);
     ScratchAux* ax = &sc.aux[s[k] & kSlotMask];
@@ -343,8 +347,12 @@ __global__ __launch_bounds__(kBlock) void k_rank_probe(TableDev t, Scratch sc, i
   }
   const int v[5] = {cf, c, nw, nl, nu};
   int ex[5], tot[5];
-  block_excl_scan5<kBlock>(v, ex, tot, sh);
-  if (threadIdx.x < 5) bsum[threadIdx.x * ntiles + blockIdx.x] = tot[threadIdx.x];
+  block_excl_scan5<NT>(v, ex, tot, sh);
+  if (threadIdx.x == 0) {
+#pragma unroll
+    for (int a = 0; a < 5; ++a) bsum[a * ntiles + blockIdx.x] = tot[a];
+    if (blockIdx.x == 0) cscal[kCScanDone] = 0;  // the scan's completion counter
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -359,52 +367,91 @@ __device__ inline void publish_live(int64_t* h_live, int64_t tag, int64_t live) 
   }
 }
 
-// One block scans the five tile-sum arrays (thread t owns R consecutive
-// tiles of each round of 1024 R tiles; all 5 R loads in flight together).
+// Scan of the five tile-sum arrays: block c scans chunk c (kScanChunk tiles,
+// R per thread) in place and stores the chunk's totals; the last block to
+// finish (a counter, no waiting) scans the chunk totals in place, reserves
+// the rows of the new keys and publishes the live count.  A tile's prefix is
+// then bsum[a][tile] + csum[a][tile / kScanChunk].
 template <int R>
 __global__ __launch_bounds__(1024) void k_scan5(int32_t* __restrict__ bsum, int64_t nb, int64_t ntiles,
-                                                int64_t* cscal, int64_t* tscal, int64_t* h_live, int64_t tag) {
+                                                int32_t* __restrict__ csum, int64_t nch, int64_t* cscal,
+                                                int64_t* tscal, int64_t* h_live, int64_t tag) {
+  static_assert(1024 * R == kScanChunk, "one chunk per block");
   __shared__ int sh[1024 / kWave + 1][5];
-  int64_t carry[5] = {0, 0, 0, 0, 0};
-  for (int64_t r0 = 0; r0 < nb; r0 += 1024 * R) {
-    const int64_t lo = r0 + static_cast<int64_t>(threadIdx.x) * R;
-    int v[5][R];
+  __shared__ bool last;
+  const int64_t c = blockIdx.x;
+  const int64_t lo = c * kScanChunk + static_cast<int64_t>(threadIdx.x) * R;
+  int v[5][R];
 #pragma unroll
-    for (int a = 0; a < 5; ++a)
+  for (int a = 0; a < 5; ++a)
 #pragma unroll
-      for (int j = 0; j < R; ++j) v[a][j] = lo + j < nb ? bsum[a * ntiles + lo + j] : 0;
-    int local[5], ex[5], tot[5];
+    for (int j = 0; j < R; ++j) v[a][j] = lo + j < nb ? bsum[a * ntiles + lo + j] : 0;
+  int local[5], ex[5], tot[5];
 #pragma unroll
-    for (int a = 0; a < 5; ++a) {
-      local[a] = 0;
+  for (int a = 0; a < 5; ++a) {
+    local[a] = 0;
 #pragma unroll
-      for (int j = 0; j < R; ++j) local[a] += v[a][j];
+    for (int j = 0; j < R; ++j) local[a] += v[a][j];
+  }
+  block_excl_scan5<1024>(local, ex, tot, sh);
+#pragma unroll
+  for (int a = 0; a < 5; ++a) {
+    int run = ex[a];
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      if (lo + j < nb) bsum[a * ntiles + lo + j] = run;
+      run += v[a][j];
     }
-    block_excl_scan5<1024>(local, ex, tot, sh);
+  }
+  if (threadIdx.x == 0) {
 #pragma unroll
-    for (int a = 0; a < 5; ++a) {
-      int run = ex[a] + static_cast<int>(carry[a]);
+    for (int a = 0; a < 5; ++a) csum[a * nch + c] = tot[a];
+    __threadfence();
+    const unsigned long long done =
+        atomicAdd(reinterpret_cast<unsigned long long*>(&cscal[kCScanDone]), 1ull);
+    last = done == static_cast<unsigned long long>(nch - 1);
+  }
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  // the last block: exclusive scan of the chunk totals (nch <= 1024 R)
+  int cv[5][R];
+  const int64_t clo = static_cast<int64_t>(threadIdx.x) * R;
 #pragma unroll
-      for (int j = 0; j < R; ++j) {
-        if (lo + j < nb) bsum[a * ntiles + lo + j] = run;
-        run += v[a][j];
-      }
-      carry[a] += tot[a];
+  for (int a = 0; a < 5; ++a)
+#pragma unroll
+    for (int j = 0; j < R; ++j)
+      cv[a][j] = clo + j < nch ? __hip_atomic_load(&csum[a * nch + clo + j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+#pragma unroll
+  for (int a = 0; a < 5; ++a) {
+    local[a] = 0;
+#pragma unroll
+    for (int j = 0; j < R; ++j) local[a] += cv[a][j];
+  }
+  block_excl_scan5<1024>(local, ex, tot, sh);
+#pragma unroll
+  for (int a = 0; a < 5; ++a) {
+    int run = ex[a];
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      if (clo + j < nch) csum[a * nch + clo + j] = run;
+      run += cv[a][j];
     }
   }
   if (threadIdx.x != 0) return;
-  cscal[kCU] = carry[0];
-  cscal[kCValid] = carry[1];
-  cscal[kCNewReq] = carry[2];
-  cscal[kCNLong] = carry[3];
-  cscal[kCNUnits] = carry[4];
+  cscal[kCScanDone] = 0;  // ready for the next call on this workspace
+  cscal[kCU] = tot[0];
+  cscal[kCValid] = tot[1];
+  cscal[kCNewReq] = tot[2];
+  cscal[kCNLong] = tot[3];
+  cscal[kCNUnits] = tot[4];
   const int64_t live = tscal[kTLive];
   const int64_t lim = min(tscal[kTLimit], tscal[kTRowCap]);
   const int64_t room = lim > live ? lim - live : 0;
-  const int64_t ins = carry[2] < room ? carry[2] : room;
+  const int64_t ins = tot[2] < room ? tot[2] : room;
   cscal[kCNew] = ins;
   cscal[kCBaseLive] = live;
-  cscal[kCTrunc] = carry[2] > room ? 1 : 0;
+  cscal[kCTrunc] = tot[2] > room ? 1 : 0;
   tscal[kTLive] = live + ins;
   publish_live(h_live, tag, live + ins);
 }
@@ -453,12 +500,12 @@ hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const Scratch& s
                                                                      reinterpret_cast<int*>(t.scal + kTErr));
   if (ev_local && ev_local[1]) (void)hipEventRecord(ev_local[1], s);
   if (ev_probe && ev_probe[0]) (void)hipEventRecord(ev_probe[0], s);
-  k_rank_probe<<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, sc, w.slot_of, n, w.bsum, w.ntiles);
+  k_rank_probe<kBlock><<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, sc, w.slot_of, n, w.bsum, w.ntiles,
+                                                                   w.scal);
   if (ev_probe && ev_probe[1]) (void)hipEventRecord(ev_probe[1], s);
-  if (nb <= 1024) k_scan5<1><<<1, 1024, 0, s>>>(w.bsum, nb, w.ntiles, w.scal, t.scal, h_live, tag);
-  else if (nb <= 2048) k_scan5<2><<<1, 1024, 0, s>>>(w.bsum, nb, w.ntiles, w.scal, t.scal, h_live, tag);
-  else if (nb <= 4096) k_scan5<4><<<1, 1024, 0, s>>>(w.bsum, nb, w.ntiles, w.scal, t.scal, h_live, tag);
-  else k_scan5<8><<<1, 1024, 0, s>>>(w.bsum, nb, w.ntiles, w.scal, t.scal, h_live, tag);
+  const int64_t nch = (nb + kScanChunk - 1) / kScanChunk;
+  k_scan5<kScanChunk / 1024><<<static_cast<unsigned>(nch), 1024, 0, s>>>(w.bsum, nb, w.ntiles, w.csum, nch, w.scal,
+                                                                          t.scal, h_live, tag);
   return hipGetLastError();
 }
 
@@ -466,14 +513,16 @@ hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const Scratch& s
 // pass 3: unique ids, segments, rows, IDMap inserts
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(kBlock) void k_compact_insert(TableDev t, Scratch sc, Work w,
-                                                           const int64_t* __restrict__ values, int64_t n) {
-  __shared__ int sh[kBlock / kWave + 1][5];
-  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kRankTile + threadIdx.x * kRankItems;
+template <int NT>
+__global__ __launch_bounds__(NT) void k_compact_insert(TableDev t, Scratch sc, Work w,
+                                                       const int64_t* __restrict__ values, int64_t n) {
+  __shared__ int sh[NT / kWave + 1][5];
+  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * NT * kRankItems + threadIdx.x * kRankItems;
   const int b = blockIdx.x;
   int pre[5];  // the tile's exclusive prefixes (first, count, new, hot, units)
+  const int64_t nch = (static_cast<int64_t>(gridDim.x) + kScanChunk - 1) / kScanChunk;
 #pragma unroll
-  for (int a = 0; a < 5; ++a) pre[a] = w.bsum[a * w.ntiles + b];
+  for (int a = 0; a < 5; ++a) pre[a] = w.bsum[a * w.ntiles + b] + w.csum[a * nch + b / kScanChunk];
   int s[4];
   load4(w.slot_of, i0, n, s);
   bool f[4];
@@ -499,7 +548,7 @@ __global__ __launch_bounds__(kBlock) void k_compact_insert(TableDev t, Scratch s
   // of new keys, hot-key indices and backward units
   const int v[5] = {cf, cc, cn, cl, cu};
   int ex[5], tot[5];
-  block_excl_scan5<kBlock>(v, ex, tot, sh);
+  block_excl_scan5<NT>(v, ex, tot, sh);
   int uid = pre[0] + ex[0];
   int start = pre[1] + ex[1];
   int64_t nr = pre[2] + ex[2];
@@ -674,7 +723,7 @@ hipError_t launch_compact_insert(const int64_t* values, int64_t n, const Scratch
   if (n <= 0) return hipSuccess;
   const int64_t nb = (n + kRankTile - 1) / kRankTile;
   if (ev_compact && ev_compact[0]) (void)hipEventRecord(ev_compact[0], s);
-  k_compact_insert<<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, sc, w, values, n);
+  k_compact_insert<kBlock><<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, sc, w, values, n);
   if (ev_compact && ev_compact[1]) (void)hipEventRecord(ev_compact[1], s);
   // one launch: the per-occurrence pass and the new rows (the init-rows and
   // occurrence events both bracket it)

@@ -9,9 +9,8 @@
 // loads, one lane group of D*sizeof(row)/16 lanes per row, and write the
 // gradient row each position of the occurrence list will read (occ_ref).
 //
-// A lane group handles kBags bags at once: their load chains (offsets ->
-// occurrence row -> row data) are interleaved so a wavefront keeps
-// 4 x (64 / lanes) rows in flight even for single-id bags.
+// A lane group handles kBags bags at once and requests up to kChunk rows of
+// them together, for single-id and long bags alike.
 #include "device_common.h"
 
 namespace rs {
@@ -20,18 +19,44 @@ constexpr int kBags = 4;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-template <typename WT, int LANES, int MODE>
+// acc += the E row elements held raw in v (16 bytes of the row)
+template <typename WT, int E>
+__device__ inline void add_raw(float (&acc)[E], const uint4& v);
+template <>
+__device__ inline void add_raw<float, 4>(float (&acc)[4], const uint4& v) {
+  acc[0] += __uint_as_float(v.x);
+  acc[1] += __uint_as_float(v.y);
+  acc[2] += __uint_as_float(v.z);
+  acc[3] += __uint_as_float(v.w);
+}
+template <>
+__device__ inline void add_raw<uint16_t, 8>(float (&acc)[8], const uint4& v) {
+  const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    acc[2 * k] += __uint_as_float(u[k] << 16);
+    acc[2 * k + 1] += __uint_as_float(u[k] & 0xFFFF0000u);
+  }
+}
+
+// A lane group pools kBags consecutive bags.  Their positions, taken as one
+// concatenated sequence, are processed in chunks of C: the lanes load the
+// chunk's occurrence rows and list positions together (each lane a few
+// positions), then every row of the chunk is requested before any is added,
+// so a group keeps C rows in flight whether the bags hold one id or hundreds
+// (C = 4 for batches of mostly single-id bags, 16 otherwise).
+template <typename WT, int LANES, int MODE, int C>
 __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64_t* __restrict__ offsets, int64_t n,
                                                  int64_t bags, float* __restrict__ out) {
   constexpr int E = 16 / static_cast<int>(sizeof(WT));
   constexpr int D = LANES * E;
   constexpr int GPB = kBlock / LANES;
+  constexpr int J = (C + LANES - 1) / LANES;  // chunk positions per lane
   const int lane = threadIdx.x % LANES;
   const int grp = threadIdx.x / LANES;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * GPB * kBags;
   for (int64_t g0 = (static_cast<int64_t>(blockIdx.x) * GPB + grp) * kBags; g0 < bags; g0 += stride) {
     int64_t b[kBags], e[kBags];
-    int64_t maxlen = 0;
     if constexpr (LANES > kBags) {
       // lanes 0..kBags of the group load offsets[g0 .. g0+kBags] together
       const int64_t gq = g0 + min(lane, kBags);
@@ -49,49 +74,72 @@ __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64
         e[q] = g0 + q < bags ? offsets[g0 + q + 1] : 0;
       }
     }
+    int64_t pre[kBags + 1];
+    pre[0] = 0;
 #pragma unroll
     for (int q = 0; q < kBags; ++q) {
       // CSR bounds clamped to [0, n]: malformed offsets cannot read out of range
       const bool ok = g0 + q < bags;
       b[q] = ok ? min(max(b[q], int64_t(0)), n) : 0;
       e[q] = ok ? min(max(e[q], b[q]), n) : 0;
-      maxlen = max(maxlen, e[q] - b[q]);
+      pre[q + 1] = pre[q] + (e[q] - b[q]);
     }
+    const int64_t total = pre[kBags];
     float acc[kBags][E];
 #pragma unroll
     for (int q = 0; q < kBags; ++q)
 #pragma unroll
       for (int k = 0; k < E; ++k) acc[q][k] = 0.f;
-    for (int64_t tt = 0; tt < maxlen; ++tt) {
-      int64_t r[kBags];
-      int pos[kBags];
+    for (int64_t t0 = 0; t0 < total; t0 += C) {
+      int64_t rr[J];
+      int pp[J], qq[J];
 #pragma unroll
-      for (int q = 0; q < kBags; ++q) {
-        const bool act = b[q] + tt < e[q];
-        r[q] = act ? w.occ_row[b[q] + tt] : -1;
-        pos[q] = act ? w.occ_pos[b[q] + tt] : -1;
+      for (int j = 0; j < J; ++j) {
+        const int c = lane + j * LANES;
+        const int64_t tt = t0 + c;
+        const bool valid = c < C && tt < total;
+        int q = 0;
+#pragma unroll
+        for (int k = 1; k < kBags; ++k) q += tt >= pre[k];
+        const int64_t p = valid ? b[q] + (tt - pre[q]) : 0;  // total > 0: position 0 exists
+        rr[j] = w.occ_row[p];
+        pp[j] = w.occ_pos[p];
+        if (!valid) {
+          rr[j] = -1;
+          pp[j] = -1;
+        }
+        qq[j] = q;
       }
-      float x[kBags][E];
+      // the occurrence's place in its key's segment of the occurrence list
+      // receives the gradient row it will read in the backward (and, for
+      // mean pooling, the scale 1 / bag length)
 #pragma unroll
-      for (int q = 0; q < kBags; ++q) {
-        if (r[q] >= 0) {
-          load_vals<WT, E>(reinterpret_cast<const WT*>(t.store.row(r[q])) + lane * E, x[q]);
+      for (int j = 0; j < J; ++j) {
+        if (pp[j] < 0) continue;
+        if (MODE == 1) {
+          int64_t len = 0;
+#pragma unroll
+          for (int q = 0; q < kBags; ++q)
+            if (qq[j] == q) len = e[q] - b[q];
+          w.occ_rs[pp[j]] = make_int2(static_cast<int>(g0 + qq[j]), __float_as_int(1.0f / static_cast<float>(len)));
         } else {
-#pragma unroll
-          for (int k = 0; k < E; ++k) x[q][k] = 0.f;
+          w.occ_ref[pp[j]] = static_cast<int>(g0 + qq[j]);
         }
       }
-      if (lane == 0) {
-        // the occurrence's place in its key's segment of the occurrence list
-        // receives the gradient row it will read in the backward
+      uint4 x[C];
+      int xq[C];
 #pragma unroll
-        for (int q = 0; q < kBags; ++q)
-          if (pos[q] >= 0) w.occ_ref[pos[q]] = static_cast<int>(g0 + q);
+      for (int c = 0; c < C; ++c) {
+        const int64_t r = LANES > 1 ? __shfl(rr[c / LANES], c % LANES, LANES) : rr[c];
+        xq[c] = LANES > 1 ? __shfl(qq[c / LANES], c % LANES, LANES) : qq[c];
+        x[c] = make_uint4(0u, 0u, 0u, 0u);
+        if (r >= 0) x[c] = *reinterpret_cast<const uint4*>(t.store.row(r) + lane * 16);
       }
 #pragma unroll
-      for (int q = 0; q < kBags; ++q)
+      for (int c = 0; c < C; ++c)
 #pragma unroll
-        for (int k = 0; k < E; ++k) acc[q][k] += x[q][k];
+        for (int q = 0; q < kBags; ++q)
+          if (xq[c] == q) add_raw<WT, E>(acc[q], x[c]);
     }
 #pragma unroll
     for (int q = 0; q < kBags; ++q) {
@@ -173,12 +221,18 @@ static hipError_t pool_mode(const TableDev& t, const Work& w, const int64_t* off
     const int64_t nch = (pad_len + TCH - 1) / TCH;
     k_pool_none<WT, LANES><<<grid_for(bags * nch, 1, 1 << 20), kBlock, 0, s>>>(t, w, offsets, n, bags, pad_len,
                                                                              static_cast<WT*>(out), mask);
-  } else if (mode == 1) {
-    k_pool<WT, LANES, 1><<<grid_for(bags, GPB * kBags, 1 << 20), kBlock, 0, s>>>(t, w, offsets, n, bags,
-                                                                                 static_cast<float*>(out));
   } else {
-    k_pool<WT, LANES, 0><<<grid_for(bags, GPB * kBags, 1 << 20), kBlock, 0, s>>>(t, w, offsets, n, bags,
-                                                                                 static_cast<float*>(out));
+    // mostly single-id bags (n <= 2 bags): 4-row chunks cover a group's bags
+    const bool few = n <= 2 * bags;
+    const unsigned g = grid_for(bags, GPB * kBags, 1 << 20);
+    float* o = static_cast<float*>(out);
+    if (mode == 1) {
+      if (few) k_pool<WT, LANES, 1, 4><<<g, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
+      else k_pool<WT, LANES, 1, 16><<<g, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
+    } else {
+      if (few) k_pool<WT, LANES, 0, 4><<<g, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
+      else k_pool<WT, LANES, 0, 16><<<g, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
+    }
   }
   return hipGetLastError();
 }

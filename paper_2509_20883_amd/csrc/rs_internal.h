@@ -28,6 +28,8 @@ constexpr int kDedupThreads = 1024;
 // per thread: many resident waves for these latency-bound passes).
 constexpr int kRankItems = 4;
 constexpr int kRankTile = kBlock * kRankItems;  // 1024
+// Tiles per block of the tile-sum scan.
+constexpr int kScanChunk = 2048;
 
 // Open addressing with linear probing; a lookup reads kProbeBatch
 // consecutive IDMap slots (64 bytes) per round trip.
@@ -37,6 +39,7 @@ constexpr int kProbeBatch = 4;
 // group; a longer ("hot") key is cut into units of kUnit positions, each
 // writing a partial sum row that one block per key then adds up.
 constexpr int kLong = 32;
+constexpr int kShortKeys = 2;  // short keys a lane group reduces together (fp32 gradients)
 constexpr int kUnit = 32;
 constexpr int kUnitLog2 = 5;
 static_assert(kUnit == 1 << kUnitLog2, "kUnit is a power of two");
@@ -72,7 +75,8 @@ enum : int {
   kCNLong = 5,     // keys with more than kLong occurrences
   kCNUnits = 6,    // backward units of those keys
   kCTrunc = 7,     // 1 if some keys not found had no room (latched as RS_EFULL)
-  kCScalars = 8
+  kCScanDone = 8,  // blocks of the tile-sum scan that have finished
+  kCScalars = 9
 };
 
 __host__ __device__ inline uint64_t mix64(uint64_t z) {
@@ -165,10 +169,12 @@ struct Work {
   int64_t* rows;        // [n]
   int32_t* new_list;    // [n] unique id of the k-th inserted key
   int32_t* occ_ref;     // [n] gradient row of each position of the occurrence list
+  int2* occ_rs;         // [n] mean pooling, same memory: {gradient row, bits of 1 / bag length}
   int32_t* long_u;      // [n/kLong + 1] unique id of each hot key
   int32_t* long_start;  // [n/kLong + 1] first backward unit of each hot key
   Unit* units;          // [2n/kUnit + 2] backward units of the hot keys
   int32_t* bsum;        // [5 * ntiles] tile sums: first occurrences, their counts, new keys, hot keys, units
+  int32_t* csum;        // [5 * (ntiles / kScanChunk + 1)] the same per chunk of tiles
   int64_t* scal;        // [kCScalars]
   float* gpart;         // [(2n/kUnit + 2) * D] partial gradient row of each backward unit
   int64_t ntiles;       // tiles of the rank passes (bsum stride)
