@@ -13,13 +13,13 @@
  *
  * Conventions shared by every entry point
  *  - All array arguments are DEVICE pointers owned by the caller, unless a
- *    comment says "host".  The table object (IDMap + Blocks + dedup scratch)
- *    is owned by the library.
+ *    comment says "host".  The table object (IDMap + Blocks) is owned by the
+ *    library.
  *  - Every call that takes an `rs_stream` only enqueues work on that HIP
  *    stream (a hipStream_t; NULL = the null stream) and returns without
  *    waiting, except where a comment says it synchronizes.  Calls on one
  *    table must be issued in stream order from one host thread: the table's
- *    scratch and counters are shared by its calls.
+ *    counters are shared by its calls.
  *  - Sizes and counts that depend on the data (the number of unique ids U,
  *    the number of inserted ids) stay on the device; buffers are sized by
  *    the upper bound n.
@@ -61,8 +61,8 @@ typedef enum { RS_ADAGRAD = 0, RS_ADAM = 1 } rs_optim;
 typedef struct rs_table rs_table; /* opaque, library-owned */
 typedef void* rs_stream;          /* hipStream_t */
 
-/* Device-memory allocator used for the table's IDMap, dedup scratch and
- * internal workspace.  NULL as the allocator argument means hipMalloc /
+/* Device-memory allocator used for the table's IDMap and internal
+ * workspace.  NULL as the allocator argument means hipMalloc /
  * hipFree.  A free callback is only invoked after the table's work has
  * completed.  The Blocks (rows + optimizer state) are physical chunks
  * (hipMemCreate) mapped into one reserved virtual range, so that rows never
@@ -210,8 +210,8 @@ rs_status lookup_pool_fwd(rs_table* t, const int64_t* values, const int64_t* off
  * lookup_prepare: everything of lookup_pool_fwd except the gather + pool:
  * dedup, IDMap find-or-insert, row init of new keys, and the per-occurrence
  * bookkeeping, into ctx (same arguments and errors as lookup_pool_fwd
- * minus out / mask).  It reads and writes only the IDMap, the table's dedup
- * scratch, the rows of the keys it inserts and ctx -- never a row that
+ * minus out / mask).  It reads and writes only the IDMap, the rows of the
+ * keys it inserts and ctx -- never a row that
  * already existed -- so it may run while an earlier batch's
  * lookup_pool_prepared / backward / optimizer are still running on another
  * stream.  Prepares of one table must be issued in order on one stream.
@@ -254,8 +254,10 @@ rs_status lookup_pool_bwd_opt(rs_table* t, const rs_ctx* ctx, const void* grad_o
  * the call's stream immediately before / after every launch of the named
  * kernel (NULL, NULL clears it).  For measurement only. */
 typedef enum {
-  RS_K_DEDUP_LOCAL = 0,    /* tile dedup + scratch set                          */
-  RS_K_RANK_PROBE = 1,     /* first occurrences + IDMap probe                   */
+  RS_K_TILE_DEDUP = 0,     /* tile dedup in LDS, records per hash partition     */
+  RS_K_PARTITION = 1,      /* per-partition dedup + IDMap probe, then the
+                              first-occurrence tile sums and their scan
+                              (several kernels)                                 */
   RS_K_COMPACT_INSERT = 2, /* unique ids, segments, rows, IDMap inserts         */
   RS_K_INIT_ROWS = 3,      /* same launch as RS_K_OCC (it writes the new rows)  */
   RS_K_POOL = 4,           /* gather + pool (and the occurrence list)           */

@@ -45,25 +45,37 @@ bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
 
 // Workspace layout of one forward: every array sized by the upper bound n.
 struct Layout {
-  size_t slot_of, occ_rank, inverse, occ_row, occ_pos, unique, useg, rows, new_list, occ_ref, long_u, long_start,
-      units, bsum, csum, scal, gpart, total;
+  size_t occ_word, firstkey, trec, nrec, pcnt, pcsum, prec, psrc, ptmp, kinfo, inverse, occ_row, occ_pos, unique,
+      useg, rows, new_list, occ_ref, long_u, long_start, units, bsum, csum, scal, gpart, total;
   int64_t ntiles;
+  FrontGeom g;
 };
 
 Layout make_layout(int64_t n, int dim) {
   const size_t n1 = static_cast<size_t>(n > 0 ? n : 1);
-  const size_t nlong = n1 / kLong + 1;             // keys with > kLong occurrences
-  const size_t nunit = 2 * (n1 / kUnit) + 2;       // >= sum over them of ceil(count / kUnit)
+  const size_t nlong = n1 / kLong + 1;        // keys with > kLong occurrences
+  const size_t nunit = 2 * (n1 / kUnit) + 2;  // >= sum over them of ceil(count / kUnit)
   Layout L{};
   L.ntiles = static_cast<int64_t>(n1 / kRankTile + 2);
+  L.g = front_geom(n);
+  const size_t nrecs = static_cast<size_t>(L.g.nblk) * static_cast<size_t>(L.g.rcap);
+  const size_t npc = static_cast<size_t>(L.g.P) * static_cast<size_t>(L.g.nblk);
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
     off += align_up(bytes);
     return o;
   };
-  L.slot_of = take(4 * n1);
-  L.occ_rank = take(4 * n1);
+  L.occ_word = take(4 * n1);
+  L.firstkey = take(4 * n1);
+  L.trec = take(sizeof(TileRec) * nrecs);  // also the records' results (int2 each)
+  L.nrec = take(4 * static_cast<size_t>(L.g.nblk));
+  L.pcnt = take(4 * npc);
+  L.pcsum = take(4 * (npc / kScanChunk + 1));
+  L.prec = take(sizeof(PartRec) * n1);
+  L.psrc = take(4 * n1);
+  L.ptmp = take(8 * n1);
+  L.kinfo = take(sizeof(KeyInfo) * n1);
   L.inverse = take(4 * n1);
   L.occ_row = take(8 * n1);
   L.occ_pos = take(4 * n1);
@@ -86,8 +98,17 @@ Layout make_layout(int64_t n, int dim) {
 Work make_work(void* base, const Layout& L) {
   uint8_t* b = static_cast<uint8_t*>(base);
   Work w;
-  w.slot_of = reinterpret_cast<int32_t*>(b + L.slot_of);
-  w.occ_rank = reinterpret_cast<int32_t*>(b + L.occ_rank);
+  w.occ_word = reinterpret_cast<uint32_t*>(b + L.occ_word);
+  w.firstkey = reinterpret_cast<int32_t*>(b + L.firstkey);
+  w.trec = reinterpret_cast<TileRec*>(b + L.trec);
+  w.recres = reinterpret_cast<int2*>(b + L.trec);
+  w.nrec = reinterpret_cast<int32_t*>(b + L.nrec);
+  w.pcnt = reinterpret_cast<int32_t*>(b + L.pcnt);
+  w.pcsum = reinterpret_cast<int32_t*>(b + L.pcsum);
+  w.prec = reinterpret_cast<PartRec*>(b + L.prec);
+  w.psrc = reinterpret_cast<int32_t*>(b + L.psrc);
+  w.ptmp = reinterpret_cast<int2*>(b + L.ptmp);
+  w.kinfo = reinterpret_cast<KeyInfo*>(b + L.kinfo);
   w.inverse = reinterpret_cast<int32_t*>(b + L.inverse);
   w.occ_row = reinterpret_cast<int64_t*>(b + L.occ_row);
   w.occ_pos = reinterpret_cast<int32_t*>(b + L.occ_pos);
@@ -105,13 +126,13 @@ Work make_work(void* base, const Layout& L) {
   w.scal = reinterpret_cast<int64_t*>(b + L.scal);
   w.gpart = reinterpret_cast<float*>(b + L.gpart);
   w.ntiles = L.ntiles;
+  w.g = L.g;
   return w;
 }
 
 const char* err_text(int bits) {
   if (bits & kErrKey) return "a reserved key (INT64_MIN or INT64_MIN+1) was in the input";
   if (bits & kErrFull) return "the table is full (auto_grow is off): some keys were not inserted";
-  if (bits & kErrScratch) return "dedup scratch table overflow";
   if (bits & kErrProbe) return "IDMap probe found no free slot";
   return "device error";
 }
@@ -144,10 +165,6 @@ struct rs_table {
   int64_t rows_prov = 0;
   // device scalars
   int64_t* d_scal = nullptr;
-  // dedup scratch
-  ScratchSlot* s_slot = nullptr;
-  ScratchAux* s_aux = nullptr;
-  int64_t s_cap = 0;
   // host view of the live count: an upper bound.  Every insert call gets a
   // 16-bit tag; its scan kernel stores (tag << 48) | exact live count into
   // h_pin[0], and bound_after[tag % kTags] remembers the host's bound right
@@ -197,7 +214,6 @@ struct rs_table {
     t.span = d.init_hi - d.init_lo;  // fp32 subtraction
     return t;
   }
-  Scratch scratch() const { return Scratch{s_slot, s_aux, static_cast<uint64_t>(s_cap - 1)}; }
   hipEvent_t* ev(int k) { return (kev[k][0] || kev[k][1]) ? kev[k] : nullptr; }
 };
 
@@ -218,27 +234,6 @@ rs_status take_latched(rs_table* t) {
   const int64_t zero = 0;
   RS_HIP(hipMemcpy(t->d_scal + kTErr, &zero, sizeof(int64_t), hipMemcpyHostToDevice));
   return fail(err_status(static_cast<int>(e)), err_text(static_cast<int>(e)));
-}
-
-// Ensure the dedup scratch has >= 2n slots (load <= 0.5); it is cleared once
-// here and then returned to empty by every call that used it.
-rs_status ensure_scratch(rs_table* t, int64_t n, hipStream_t s) {
-  int64_t want = 4096;
-  while (want < 2 * n) want <<= 1;
-  if (t->s_cap >= want) return RS_OK;
-  RS_HIP(hipStreamSynchronize(s));
-  t->release(t->s_slot);
-  t->release(t->s_aux);
-  t->s_slot = static_cast<ScratchSlot*>(t->alloc(sizeof(ScratchSlot) * want));
-  t->s_aux = static_cast<ScratchAux*>(t->alloc(sizeof(ScratchAux) * want));
-  if (!t->s_slot || !t->s_aux) {
-    t->s_cap = 0;
-    return fail(RS_ENOMEM, "allocation of the dedup scratch failed");
-  }
-  t->s_cap = want;
-  // empty slot = {key 0, first 0xFFFFFFFF, cnt 0}
-  RS_HIP(launch_scratch_clear(t->s_slot, want, s));
-  return RS_OK;
 }
 
 // Map Blocks chunks until `rows` rows fit.
@@ -339,12 +334,9 @@ int64_t next_tag(rs_table* t) {
 // table first when it may not have room).
 rs_status dedup_and_insert(rs_table* t, const int64_t* values, int64_t n, const Work& w, bool occ_lists,
                            hipStream_t s) {
-  rs_status st = ensure_scratch(t, n, s);
-  if (st != RS_OK) return st;
-  const Scratch sc = t->scratch();
+  rs_status st = RS_OK;
   const int64_t tag = next_tag(t);
-  RS_HIP(launch_dedup_probe(values, n, sc, t->dev(), w, t->h_pin, tag, t->ev(RS_K_DEDUP_LOCAL),
-                            t->ev(RS_K_RANK_PROBE), s));
+  RS_HIP(launch_dedup_probe(values, n, t->dev(), w, t->h_pin, tag, t->ev(RS_K_TILE_DEDUP), t->ev(RS_K_PARTITION), s));
   refresh_bound(t);
   const int64_t bound = t->live_bound + n;
   if (bound > t->limit || bound > t->rows_prov) {
@@ -367,7 +359,7 @@ rs_status dedup_and_insert(rs_table* t, const int64_t* values, int64_t n, const 
     t->live_bound = bound;
     t->bound_after[tag % rs_table::kTags] = t->live_bound;
   }
-  RS_HIP(launch_compact_insert(values, n, sc, t->dev(), w, occ_lists, t->ev(RS_K_COMPACT_INSERT),
+  RS_HIP(launch_compact_insert(values, n, t->dev(), w, occ_lists, t->ev(RS_K_COMPACT_INSERT),
                                t->ev(RS_K_INIT_ROWS), t->ev(RS_K_OCC), s));
   return RS_OK;
 }
@@ -503,8 +495,6 @@ rs_status ht_destroy(rs_table* t) {
   for (hipMemGenericAllocationHandle_t h : t->chunks) (void)hipMemRelease(h);
   if (t->va_base) (void)hipMemAddressFree(t->va_base, t->va_size);
   t->release(t->d_scal);
-  t->release(t->s_slot);
-  t->release(t->s_aux);
   t->release(t->iws);
   if (t->h_pin) (void)hipHostFree(t->h_pin);
   delete t;

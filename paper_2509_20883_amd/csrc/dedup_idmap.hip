@@ -2,23 +2,30 @@
 //
 // RecIS keeps a two-tier store: an IDMap from feature id to an offset and
 // Blocks holding the rows ("Optimization for Memory Bound"); ids are
-// deduplicated before the lookup ("ids partition").  One forward runs:
-//   k_dedup_local    per 1024-occurrence tile: LDS dedup, then one global
-//                    scratch insert per distinct key of the tile (atomicMin of
-//                    its first position, atomicAdd of its count; the value the
-//                    atomicAdd returns ranks the tile's occurrences of the key)
-//   k_rank_probe     first occurrences probe the IDMap; tile sums of
-//                    (first occurrences, their counts, keys not found, hot
-//                    keys, backward units of the hot keys)
-//   k_scan5          one block scans the five tile-sum arrays and reserves
-//                    the rows of the new keys
-//   k_compact_insert unique ids in first-occurrence order, occurrence-list
+// deduplicated before the lookup ("ids partition").  The dedup gives the
+// unique keys in first-occurrence order.  It uses no global atomics (on this
+// GPU they serialise at the memory side): keys are grouped by a hash
+// partition instead, so every key is counted by exactly one block in LDS.
+//   k_tile_dedup     per block, consecutive tiles of 4096 occurrences: LDS
+//                    dedup; one record per distinct key of a tile (key, first
+//                    position and count in the tile) with its rank among the
+//                    block's records of the key's hash partition
+//   k_scan_parts     exclusive scan of the (partition, block) record counts
+//   k_part_scatter   records into partition-major order
+//   k_part_dedup     one block per partition: LDS dedup of its records (first
+//                    position = min, count = sum, rank base of each record),
+//                    the key's IDMap probe, and a marker at its first position
+//   k_first_sums     per tile of positions: sums over the first occurrences
+//                    (keys, counts, keys not found, hot keys, backward units)
+//   k_scan5          scan of those tile sums; reserves the rows of new keys
+//   k_compact        unique ids in first-occurrence order, occurrence-list
 //                    segments, rows; new keys claim an IDMap slot
 //   k_occ_init       per occurrence: unique id (inverse), row, position in the
-//                    occurrence list, hot-key backward units; releases the
-//                    scratch slots.  Its other blocks write the initial rows
-//                    of the new keys
+//                    occurrence list, hot-key backward units.  Its other
+//                    blocks write the initial rows of the new keys
 #include "device_common.h"
+
+#include <algorithm>
 
 namespace rs {
 
@@ -77,19 +84,6 @@ __device__ inline int64_t idmap_claim(const TableDev& t, unsigned long long e) {
   return -1;
 }
 
-// Slot of an encoded key in the scratch set: read first, compare-and-swap only
-// an empty slot (a hot key, already present, costs no atomic here).
-__device__ inline int64_t scratch_claim(const Scratch& sc, unsigned long long e) {
-  uint64_t h = scratch_hash(e) & sc.mask;
-  for (uint64_t probed = 0; probed <= sc.mask; ++probed) {
-    unsigned long long cur = sc.slot[h].key;
-    if (cur == kEncEmpty) cur = atomicCAS(&sc.slot[h].key, kEncEmpty, e);
-    if (cur == kEncEmpty || cur == e) return static_cast<int64_t>(h);
-    h = (h + 1) & sc.mask;
-  }
-  return -1;
-}
-
 // Exclusive block scan of five values per thread at once (two barriers).
 template <int NT>
 __device__ inline void block_excl_scan5(const int (&v)[5], int (&ex)[5], int (&tot)[5], int (*sh)[5]) {
@@ -121,145 +115,335 @@ __device__ inline void block_excl_scan5(const int (&v)[5], int (&ex)[5], int (&t
   __syncthreads();
 }
 
+__device__ inline uint32_t part_of(unsigned long long e, int logP) {
+  return logP == 0 ? 0u : static_cast<uint32_t>(part_hash(e) >> (64 - logP));
+}
+
 // ---------------------------------------------------------------------------
-// pass 1: tile-local dedup in LDS, then the global scratch set
+// pass 1: tile dedup in LDS; one record per distinct key of a tile
 // ---------------------------------------------------------------------------
 
 template <int NT>
-__global__ __launch_bounds__(NT) void k_dedup_local(const int64_t* __restrict__ values, int64_t n, Scratch sc,
-                                                        int32_t* __restrict__ slot_of, int32_t* __restrict__ occ_rank,
-                                                        int* err) {
-  constexpr int TILE = NT * kDedupItems;  // occurrences per block
-  constexpr int SLOTS = 2 * TILE;         // LDS hash slots (load <= 0.5)
-  // lkey: the key, then (read only by the slot's owner in between) its
-  // scratch slot; lcnt: the count, then the global rank base of the tile's
-  // occurrences of the key
+__global__ __launch_bounds__(NT) void k_tile_dedup(const int64_t* __restrict__ values, int64_t n, Work w, int* err) {
+  constexpr int TILE = NT * kDedupItems;
+  constexpr int SLOTS = 2 * TILE;  // LDS hash slots (load <= 0.5)
+  static_assert(TILE == kDedupTile, "tile size");
+  // lmin: the key's first position in the tile, then the key's record index
   __shared__ unsigned long long lkey[SLOTS];
   __shared__ unsigned int lmin[SLOTS];
   __shared__ unsigned int lcnt[SLOTS];
-  __shared__ short ldense[TILE];  // the tile's distinct keys: dense index -> LDS slot
+  __shared__ short ldense[TILE];          // the tile's distinct keys: dense index -> LDS slot
+  __shared__ unsigned int lpc[kMaxParts];  // the block's records per partition
   __shared__ int sh[NT / kWave + 1];
+  const FrontGeom g = w.g;
   const int tid = threadIdx.x;
-  for (int s = tid; s < SLOTS; s += NT) {
-    lkey[s] = kEncEmpty;
-    lmin[s] = 0xFFFFFFFFu;
-    lcnt[s] = 0u;
+  const int64_t blk = blockIdx.x;
+  for (int q = tid; q < g.P; q += NT) lpc[q] = 0u;
+  if (blk == 0 && tid == 0) {  // completion counters of the two scans of this call
+    w.scal[kCScanDone] = 0;
+    w.scal[kCPartDone] = 0;
   }
-  // every load is issued before the first wait (n > 0: indices are clamped)
-  const int64_t base = static_cast<int64_t>(blockIdx.x) * TILE;
-  int64_t raw[kDedupItems];
+  const int64_t t0 = blk * g.R;
+  const int64_t t1 = min(t0 + g.R, g.ntiles);
+  TileRec* rec = w.trec + blk * g.rcap;
+  // the next tile's ids are loaded while this one is processed (n > 0:
+  // indices are clamped)
+  int64_t nxt[kDedupItems];
 #pragma unroll
-  for (int k = 0; k < kDedupItems; ++k) raw[k] = values[min(base + k * NT + tid, n - 1)];
-  __syncthreads();
-  int ls[kDedupItems];
-  unsigned int lr[kDedupItems];
+  for (int k = 0; k < kDedupItems; ++k) nxt[k] = values[min(t0 * TILE + k * NT + tid, n - 1)];
+  unsigned int nrec = 0;
+  for (int64_t tile = t0; tile < t1; ++tile) {
+    const int64_t base = tile * TILE;
+    int64_t raw[kDedupItems];
 #pragma unroll
-  for (int k = 0; k < kDedupItems; ++k) {
-    const int64_t i = base + k * NT + tid;
-    const unsigned long long e = static_cast<unsigned long long>(raw[k]) ^ kSign;
-    ls[k] = -1;
-    lr[k] = 0;
-    if (i >= n) continue;
-    if (e <= kEncTomb) {
-      atomicOr(err, kErrKey);
-      continue;
+    for (int k = 0; k < kDedupItems; ++k) raw[k] = nxt[k];
+    if (tile + 1 < t1) {
+#pragma unroll
+      for (int k = 0; k < kDedupItems; ++k) nxt[k] = values[min(base + TILE + k * NT + tid, n - 1)];
     }
-    unsigned int h = static_cast<unsigned int>(mix64(e) >> 40) & (SLOTS - 1);
-    while (true) {  // at most TILE keys in twice as many slots: terminates
-      const unsigned long long old = atomicCAS(&lkey[h], kEncEmpty, e);
-      if (old == kEncEmpty || old == e) break;
-      h = (h + 1) & (SLOTS - 1);
+    for (int q = tid; q < SLOTS; q += NT) {
+      lkey[q] = kEncEmpty;
+      lmin[q] = 0xFFFFFFFFu;
+      lcnt[q] = 0u;
     }
-    atomicMin(&lmin[h], static_cast<unsigned int>(i));
-    lr[k] = atomicAdd(&lcnt[h], 1u);
-    ls[k] = static_cast<int>(h);
-  }
-  __syncthreads();
-  // Dense list of the occupied slots, so a wavefront's global phase runs as
-  // few rounds as the tile has distinct keys per thread (not one per slot).
-  constexpr int kOwn = SLOTS / NT;
-  int occ = 0;
+    __syncthreads();
+    int ls[kDedupItems];
+    unsigned int lr[kDedupItems];
 #pragma unroll
-  for (int j = 0; j < kOwn; ++j) occ += lkey[tid * kOwn + j] != kEncEmpty;
-  int d;
-  int at = block_excl_scan<NT>(occ, sh, d);
-#pragma unroll
-  for (int j = 0; j < kOwn; ++j)
-    if (lkey[tid * kOwn + j] != kEncEmpty) ldense[at++] = static_cast<short>(tid * kOwn + j);
-  __syncthreads();
-  // Global phase, each step issued for all of a thread's keys before its
-  // results are waited for: read the key's scratch slot; claim it with a
-  // compare-and-swap if empty (a hot key, already present, costs no atomic);
-  // lower the stored first position if this tile's is smaller (it only ever
-  // decreases, so a stale read errs on the side of the atomic); add the
-  // tile's count, whose old value is the rank base of the tile's occurrences.
-  constexpr int kPer = TILE / NT;
-  int sl[kPer];
-  unsigned long long ke[kPer];
-  ScratchSlot cur[kPer];
-#pragma unroll
-  for (int r = 0; r < kPer; ++r) {
-    const int q = tid + r * NT;
-    sl[r] = q < d ? ldense[q] : -1;
-    ke[r] = sl[r] >= 0 ? lkey[sl[r]] : kEncEmpty;
-  }
-#pragma unroll
-  for (int r = 0; r < kPer; ++r) cur[r] = sc.slot[scratch_hash(ke[r]) & sc.mask];  // idle lanes: one shared line
-  int64_t gs[kPer];
-  unsigned long long old[kPer];
-#pragma unroll
-  for (int r = 0; r < kPer; ++r) {
-    old[r] = cur[r].key;
-    if (sl[r] >= 0 && cur[r].key == kEncEmpty)
-      old[r] = atomicCAS(&sc.slot[scratch_hash(ke[r]) & sc.mask].key, kEncEmpty, ke[r]);
-  }
-#pragma unroll
-  for (int r = 0; r < kPer; ++r) {
-    gs[r] = -1;
-    if (sl[r] < 0) continue;
-    if (old[r] == ke[r] || old[r] == kEncEmpty) {
-      gs[r] = static_cast<int64_t>(scratch_hash(ke[r]) & sc.mask);
-      if (old[r] == kEncEmpty) cur[r].first = 0xFFFFFFFFu;  // claimed here: always take the atomicMin
+    for (int k = 0; k < kDedupItems; ++k) {
+      const int64_t i = base + k * NT + tid;
+      const unsigned long long e = static_cast<unsigned long long>(raw[k]) ^ kSign;
+      ls[k] = -1;
+      lr[k] = 0;
+      if (i >= n) continue;
+      if (e <= kEncTomb) {
+        atomicOr(err, kErrKey);
+        continue;
+      }
+      unsigned int h = static_cast<unsigned int>(mix64(e) >> 40) & (SLOTS - 1);
+      while (true) {  // at most TILE keys in twice as many slots: terminates
+        const unsigned long long old = atomicCAS(&lkey[h], kEncEmpty, e);
+        if (old == kEncEmpty || old == e) break;
+        h = (h + 1) & (SLOTS - 1);
+      }
+      atomicMin(&lmin[h], static_cast<unsigned int>(i));
+      lr[k] = atomicAdd(&lcnt[h], 1u);
+      ls[k] = static_cast<int>(h);
     }
+    __syncthreads();
+    // dense list of the occupied slots
+    constexpr int kOwn = SLOTS / NT;
+    int occ = 0;
+#pragma unroll
+    for (int j = 0; j < kOwn; ++j) occ += lkey[tid * kOwn + j] != kEncEmpty;
+    int d;
+    int at = block_excl_scan<NT>(occ, sh, d);
+#pragma unroll
+    for (int j = 0; j < kOwn; ++j)
+      if (lkey[tid * kOwn + j] != kEncEmpty) ldense[at++] = static_cast<short>(tid * kOwn + j);
+    __syncthreads();
+    // one record per distinct key (nrec + d <= the block's occurrences <= rcap)
+    for (int q = tid; q < d; q += NT) {
+      const int sl = ldense[q];
+      const unsigned long long e = lkey[sl];
+      const unsigned int pr = atomicAdd(&lpc[part_of(e, g.logP)], 1u);
+      rec[nrec + q] = TileRec{e, lmin[sl], (pr << 12) | (lcnt[sl] - 1u)};
+      lmin[sl] = nrec + static_cast<unsigned int>(q);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kDedupItems; ++k) {
+      const int64_t i = base + k * NT + tid;
+      if (i >= n) continue;
+      w.occ_word[i] = ls[k] < 0 ? kOccRejected : ((lmin[ls[k]] << 12) | lr[k]);
+      w.firstkey[i] = -1;
+    }
+    nrec += static_cast<unsigned int>(d);
+    __syncthreads();  // the next tile clears the LDS
   }
+  for (int q = tid; q < g.P; q += NT) w.pcnt[static_cast<int64_t>(q) * g.nblk + blk] = static_cast<int>(lpc[q]);
+  if (tid == 0) w.nrec[blk] = static_cast<int>(nrec);
+}
+
+// ---------------------------------------------------------------------------
+// pass 2: exclusive scan of the (partition, block) record counts
+// ---------------------------------------------------------------------------
+
+// Block c scans chunk c (kScanChunk counts) in place and stores its total;
+// the last block to finish (a counter, no waiting) scans the chunk totals in
+// place and stores the number of records.  The offset of entry x is then
+// a[x] + csum[x / kScanChunk].
+__global__ __launch_bounds__(1024) void k_scan_parts(int32_t* __restrict__ a, int64_t na, int32_t* __restrict__ csum,
+                                                     int64_t nch, int64_t* cscal) {
+  constexpr int R = kScanChunk / 1024;
+  __shared__ int sh[1024 / kWave + 1];
+  __shared__ bool last;
+  const int64_t c = blockIdx.x;
+  const int64_t lo = c * kScanChunk + static_cast<int64_t>(threadIdx.x) * R;
+  int v[R];
+  int local = 0;
 #pragma unroll
-  for (int r = 0; r < kPer; ++r) {
-    if (sl[r] < 0 || gs[r] >= 0) continue;
-    gs[r] = scratch_claim(sc, ke[r]);  // collision: probe on (rare)
-    cur[r].first = 0xFFFFFFFFu;
-    if (gs[r] < 0) atomicOr(err, kErrScratch);
+  for (int j = 0; j < R; ++j) {
+    v[j] = lo + j < na ? a[lo + j] : 0;
+    local += v[j];
   }
-  unsigned int mn[kPer], cn[kPer], gb[kPer];
+  int tot;
+  int run = block_excl_scan<1024>(local, sh, tot);
 #pragma unroll
-  for (int r = 0; r < kPer; ++r) {
-    mn[r] = sl[r] >= 0 ? lmin[sl[r]] : 0u;
-    cn[r] = sl[r] >= 0 ? lcnt[sl[r]] : 0u;
+  for (int j = 0; j < R; ++j) {
+    if (lo + j < na) a[lo + j] = run;
+    run += v[j];
   }
-#pragma unroll
-  for (int r = 0; r < kPer; ++r)
-    if (gs[r] >= 0 && cur[r].first > mn[r]) atomicMin(&sc.slot[gs[r]].first, mn[r]);
-#pragma unroll
-  for (int r = 0; r < kPer; ++r) gb[r] = gs[r] >= 0 ? atomicAdd(&sc.slot[gs[r]].cnt, cn[r]) : 0u;
-#pragma unroll
-  for (int r = 0; r < kPer; ++r) {
-    if (sl[r] < 0) continue;
-    lkey[sl[r]] = static_cast<unsigned long long>(gs[r]);
-    lcnt[sl[r]] = gb[r];
+  if (threadIdx.x == 0) {
+    csum[c] = tot;
+    __threadfence();
+    const unsigned long long done = atomicAdd(reinterpret_cast<unsigned long long*>(&cscal[kCPartDone]), 1ull);
+    last = done == static_cast<unsigned long long>(nch - 1);
   }
   __syncthreads();
+  if (!last) return;
+  __threadfence();
+  const int64_t clo = static_cast<int64_t>(threadIdx.x) * R;  // nch <= 1024 R
+  local = 0;
 #pragma unroll
-  for (int k = 0; k < kDedupItems; ++k) {
-    const int64_t i = base + k * NT + tid;
-    if (i >= n) continue;
-    const int g = ls[k] >= 0 ? static_cast<int>(static_cast<long long>(lkey[ls[k]])) : -1;
-    const bool cand = g >= 0 && lmin[ls[k]] == static_cast<unsigned int>(i);
-    slot_of[i] = g < 0 ? -1 : (g | (cand ? kCandBit : 0));
-    occ_rank[i] = g >= 0 ? static_cast<int>(lcnt[ls[k]] + lr[k]) : 0;
+  for (int j = 0; j < R; ++j) {
+    v[j] = clo + j < nch ? __hip_atomic_load(&csum[clo + j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+    local += v[j];
+  }
+  run = block_excl_scan<1024>(local, sh, tot);
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    if (clo + j < nch) csum[clo + j] = run;
+    run += v[j];
+  }
+  if (threadIdx.x == 0) {
+    cscal[kCRecords] = tot;
+    cscal[kCPartDone] = 0;
+  }
+}
+
+__device__ inline int64_t part_offset(const Work& w, int64_t x) {
+  return static_cast<int64_t>(w.pcnt[x]) + w.pcsum[x / kScanChunk];
+}
+
+// ---------------------------------------------------------------------------
+// pass 3: records into partition-major order (grid: x over a block's
+// records, y = dedup block)
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kBlock) void k_part_scatter(Work w) {
+  const FrontGeom g = w.g;
+  const int64_t b = blockIdx.y;
+  const int64_t nr = w.nrec[b];
+  for (int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j < nr;
+       j += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const TileRec r = w.trec[b * g.rcap + j];
+    const int64_t x = static_cast<int64_t>(part_of(r.key, g.logP)) * g.nblk + b;
+    const int64_t dest = part_offset(w, x) + (r.meta >> 12);
+    w.prec[dest] = PartRec{r.key, r.tmin, (r.meta & 0xFFFu) + 1u};
+    w.psrc[dest] = static_cast<int>(b * g.rcap + j);
   }
 }
 
 // ---------------------------------------------------------------------------
-// pass 2: first occurrences probe the IDMap; tile sums
+// pass 4: one block per partition: LDS dedup of its records, IDMap probe
+// ---------------------------------------------------------------------------
+
+// Resolve a probe batch read at the key's home slot; continue the probe if
+// the batch neither holds the key nor an empty slot.
+__device__ inline int64_t resolve_probe(const TableDev& t, unsigned long long e, uint64_t h,
+                                        const Slot (&pb)[kProbeBatch]) {
+  int64_t r = -1;
+  bool done = false;
+#pragma unroll
+  for (int q = 0; q < kProbeBatch; ++q) {  // selects only: the batch stays in registers
+    const bool hit = !done && pb[q].key == e;
+    const bool empty = !done && pb[q].key == kEncEmpty;
+    r = hit ? pb[q].row : r;
+    done = done || hit || empty;
+  }
+  if (!done) r = idmap_lookup_at(t, e, (h + kProbeBatch) & t.cap_mask, kProbeBatch);
+  return r;
+}
+
+// Records of the partition are taken in sweeps of at most kPartSweep (by a
+// hash of the key), so a sweep's distinct keys fit the LDS table; if one
+// does not (a skewed hash), the partition starts again with twice as many
+// sweeps.  Key indices of the partition are lo + (dense index), all < hi.
+__global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w, int64_t n) {
+  constexpr int NT = kPartThreads, S = kPartSlots, OWN = S / NT;
+  constexpr int kMaxSweeps = 1 << 10;
+  __shared__ unsigned long long ckey[S];
+  __shared__ unsigned int cfirst[S];
+  __shared__ unsigned int ccnt[S];  // count, then the key's dense index
+  __shared__ short cdense[S];       // dense index -> slot
+  __shared__ int sh[NT / kWave + 1];
+  __shared__ int ovf;
+  const FrontGeom g = w.g;
+  const int tid = threadIdx.x;
+  const int p = blockIdx.x;
+  const int64_t lo = part_offset(w, static_cast<int64_t>(p) * g.nblk);
+  const int64_t hi = p + 1 < g.P ? part_offset(w, static_cast<int64_t>(p + 1) * g.nblk) : w.scal[kCRecords];
+  if (hi <= lo) return;  // the whole block: before any barrier
+  int nsw = static_cast<int>(min<int64_t>((hi - lo + kPartSweep - 1) / kPartSweep, kMaxSweeps));
+  int64_t dbase = 0;
+  int s = 0;
+  while (s < nsw) {
+    for (int q = tid; q < S; q += NT) {
+      ckey[q] = kEncEmpty;
+      cfirst[q] = 0xFFFFFFFFu;
+      ccnt[q] = 0u;
+    }
+    if (tid == 0) ovf = 0;
+    __syncthreads();
+    for (int64_t r = lo + tid; r < hi; r += NT) {
+      const PartRec x = w.prec[r];
+      const uint64_t h = part_hash(x.key);
+      if (nsw > 1 && static_cast<int>((h & 0xFFFFFull) % static_cast<uint64_t>(nsw)) != s) continue;
+      unsigned int sl = static_cast<unsigned int>(h >> 20) & (S - 1);
+      bool ok = false;
+      for (int probes = 0; probes < S; ++probes) {
+        const unsigned long long old = atomicCAS(&ckey[sl], kEncEmpty, x.key);
+        if (old == kEncEmpty || old == x.key) {
+          ok = true;
+          break;
+        }
+        sl = (sl + 1) & (S - 1);
+      }
+      if (!ok) {
+        ovf = 1;
+        continue;
+      }
+      atomicMin(&cfirst[sl], x.tmin);
+      const unsigned int rb = atomicAdd(&ccnt[sl], x.tcnt);
+      w.ptmp[r] = make_int2(static_cast<int>(sl), static_cast<int>(rb));
+    }
+    __syncthreads();
+    if (ovf) {
+      __syncthreads();  // every thread has read ovf
+      if (nsw >= kMaxSweeps) {
+        if (tid == 0) atomicOr(reinterpret_cast<int*>(&t.scal[kTErr]), kErrProbe);
+        return;
+      }
+      nsw *= 2;
+      s = 0;
+      dbase = 0;
+      continue;
+    }
+    // dense numbering of the occupied slots
+    int occ = 0;
+#pragma unroll
+    for (int j = 0; j < OWN; ++j) occ += ckey[tid * OWN + j] != kEncEmpty;
+    int d;
+    int at = block_excl_scan<NT>(occ, sh, d);
+#pragma unroll
+    for (int j = 0; j < OWN; ++j)
+      if (ckey[tid * OWN + j] != kEncEmpty) cdense[at++] = static_cast<short>(tid * OWN + j);
+    __syncthreads();
+    // one key per dense index: its IDMap probe (idle lanes read one shared
+    // line), key info, and the marker at its first position
+    for (int q0 = 0; q0 < d; q0 += NT) {
+      const int q = q0 + tid;
+      const bool act = q < d;
+      const int sl = act ? cdense[q] : 0;
+      const unsigned long long e = act ? ckey[sl] : kEncEmpty;
+      const uint64_t h = act ? (idmap_hash(e) & t.cap_mask) : 0;
+      Slot pb[kProbeBatch];
+#pragma unroll
+      for (int k = 0; k < kProbeBatch; ++k) pb[k] = t.slots[(h + k) & t.cap_mask];
+      if (act) {
+        const int64_t kidx = lo + dbase + q;
+        KeyInfo ki;
+        ki.row = resolve_probe(t, e, h, pb);
+        ki.first = static_cast<int>(cfirst[sl]);
+        ki.count = static_cast<int>(ccnt[sl]);
+        ki.uid = -1;
+        ki.start = 0;
+        ki.long_idx = -1;
+        ki.pad = 0;
+        w.kinfo[kidx] = ki;
+        if (cfirst[sl] < static_cast<uint64_t>(n)) w.firstkey[cfirst[sl]] = static_cast<int>(kidx);
+        ccnt[sl] = static_cast<unsigned int>(q);
+      }
+    }
+    __syncthreads();
+    // each record of the sweep: its key index and rank base
+    for (int64_t r = lo + tid; r < hi; r += NT) {
+      if (nsw > 1) {
+        const uint64_t h = part_hash(w.prec[r].key);
+        if (static_cast<int>((h & 0xFFFFFull) % static_cast<uint64_t>(nsw)) != s) continue;
+      }
+      const int2 tp = w.ptmp[r];
+      w.recres[w.psrc[r]] = make_int2(static_cast<int>(lo + dbase + ccnt[tp.x]), tp.y);
+    }
+    dbase += d;
+    ++s;
+    __syncthreads();  // the next sweep clears the LDS
+  }
+}
+
+// ---------------------------------------------------------------------------
+// pass 5: tile sums over the first occurrences
 // ---------------------------------------------------------------------------
 
 __device__ inline void load4(const int32_t* __restrict__ p, int64_t i0, int64_t n, int (&v)[4]) {
@@ -275,74 +459,31 @@ __device__ inline void load4(const int32_t* __restrict__ p, int64_t i0, int64_t 
   }
 }
 
+// Key info of key index k (k >= 0), or of index 0 for an idle lane (read,
+// never used: every load of a step is issued before its results are waited for).
+__device__ inline KeyInfo key_info(const Work& w, int k, int64_t n) {
+  return w.kinfo[min(max(k, 0), static_cast<int>(n - 1))];
+}
+
 template <int NT>
-__global__ __launch_bounds__(NT) void k_rank_probe(TableDev t, Scratch sc, int32_t* __restrict__ slot_of,
-                                                   int64_t n, int32_t* __restrict__ bsum, int64_t ntiles,
-                                                   int64_t* cscal) {
+__global__ __launch_bounds__(NT) void k_first_sums(Work w, int64_t n) {
   __shared__ int sh[NT / kWave + 1][5];
-  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * NT * kRankItems + threadIdx.x * kRankItems;
-  int s[4];
-  load4(slot_of, i0, n, s);
-  // every load of a step is issued before its results are waited for: the
-  // scratch slots of the tile-local firsts (other lanes read one shared
-  // slot), then the first IDMap probe batch of every first occurrence
-  bool f[4];
-  ScratchSlot ss[4];
+  const int64_t i0 = (static_cast<int64_t>(blockIdx.x) * NT + threadIdx.x) * kRankItems;
+  int f[4];
+  load4(w.firstkey, i0, n, f);
+  KeyInfo ki[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) ki[k] = key_info(w, f[k], n);
+  int cf = 0, c = 0, nw = 0, nl = 0, nu = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const bool cand = s[k] >= 0 && (s[k] & kCandBit);
-    ss[k] = sc.slot[cand ? (s[k] & kSlotMask) : 0];
-    f[k] = cand;
-  }
-  int c = 0, cf = 0, nl = 0, nu = 0;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    f[k] = f[k] && ss[k].first == static_cast<unsigned int>(i0 + k);
-    if (f[k]) {
-      const int ck = static_cast<int>(ss[k].cnt);
-      cf += 1;
-      c += ck;
-      if (ck > kLong) {
-        nl += 1;
-        nu += unit_count(ck);
-      }
-    }
-  }
-  uint64_t h[4];
-  Slot pb[4][kProbeBatch];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    h[k] = f[k] ? idmap_hash(ss[k].key) & t.cap_mask : 0;
-#pragma unroll
-    for (int q = 0; q < kProbeBatch; ++q) pb[k][q] = t.slots[(h[k] + q) & t.cap_mask];
-  }
-  int nw = 0;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    if (!f[k]) continue;
-    int64_t r = -1;
-    bool done = false;
-#pragma unroll
-    for (int q = 0; q < kProbeBatch; ++q) {  // selects only: the batch stays in registers
-      const bool hit = !done && pb[k][q].key == ss[k].key;
-      const bool empty = !done && pb[k][q].key == kEncEmpty;
-      r = hit ? pb[k][q].row : r;
-      done = done || hit || empty;
-    }
-    if (!done) r = idmap_lookup_at(t, ss[k].key, (h[k] + kProbeBatch) & t.cap_mask, kProbeBatch);
-    ScratchAux* ax = &sc.aux[s[k] & kSlotMask];
-    ax->row = r;
-    ax->count = static_cast<int>(ss[k].cnt);
-    nw += r < 0;
-  }
-  // the first occurrences are marked so the next pass reads only their keys
-  if (cf) {
-    if (i0 + 4 <= n) {
-      *reinterpret_cast<int4*>(slot_of + i0) = make_int4(f[0] ? s[0] | kFirstBit : s[0], f[1] ? s[1] | kFirstBit : s[1],
-                                                          f[2] ? s[2] | kFirstBit : s[2], f[3] ? s[3] | kFirstBit : s[3]);
-    } else {
-      for (int k = 0; k < 4 && i0 + k < n; ++k)
-        if (f[k]) slot_of[i0 + k] = s[k] | kFirstBit;
+    if (f[k] < 0) continue;
+    cf += 1;
+    c += ki[k].count;
+    nw += ki[k].row < 0;
+    if (ki[k].count > kLong) {
+      nl += 1;
+      nu += unit_count(ki[k].count);
     }
   }
   const int v[5] = {cf, c, nw, nl, nu};
@@ -350,8 +491,7 @@ __global__ __launch_bounds__(NT) void k_rank_probe(TableDev t, Scratch sc, int32
   block_excl_scan5<NT>(v, ex, tot, sh);
   if (threadIdx.x == 0) {
 #pragma unroll
-    for (int a = 0; a < 5; ++a) bsum[a * ntiles + blockIdx.x] = tot[a];
-    if (blockIdx.x == 0) cscal[kCScanDone] = 0;  // the scan's completion counter
+    for (int a = 0; a < 5; ++a) w.bsum[a * w.ntiles + blockIdx.x] = tot[a];
   }
 }
 
@@ -470,52 +610,60 @@ __global__ void k_rereserve(int64_t* cscal, int64_t* tscal, int64_t* h_live, int
 
 __global__ void k_zero_scalars(int64_t* cscal) { cscal[threadIdx.x] = 0; }
 
-__global__ void k_scratch_clear(ScratchSlot* slots, int64_t n) {
-  for (int64_t i = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x; i < n;
-       i += static_cast<int64_t>(gridDim.x) * kBlock)
-    slots[i] = ScratchSlot{kEncEmpty, 0xFFFFFFFFu, 0u};
-}
-
-hipError_t launch_scratch_clear(ScratchSlot* slots, int64_t n, hipStream_t s) {
-  k_scratch_clear<<<grid_for(n, kBlock, 65536), kBlock, 0, s>>>(slots, n);
-  return hipGetLastError();
-}
-
 hipError_t launch_rereserve(const Work& w, const TableDev& t, int64_t* h_live, int64_t tag, hipStream_t s) {
   k_rereserve<<<1, 1, 0, s>>>(w.scal, t.scal, h_live, tag);
   return hipGetLastError();
 }
 
-hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const Scratch& sc, const TableDev& t, const Work& w,
-                              int64_t* h_live, int64_t tag, hipEvent_t* ev_local, hipEvent_t* ev_probe,
-                              hipStream_t s) {
+FrontGeom front_geom(int64_t n) {
+  FrontGeom g;
+  const int64_t n1 = n > 0 ? n : 1;
+  g.ntiles = (n1 + kDedupTile - 1) / kDedupTile;
+  g.R = std::min<int64_t>(kMaxTilesPerBlock, (g.ntiles + 255) / 256);
+  g.nblk = (g.ntiles + g.R - 1) / g.R;
+  g.rcap = g.R * kDedupTile;
+  g.P = 1;
+  g.logP = 0;
+  while (g.P < kMaxParts && static_cast<int64_t>(g.P) * 2048 < n1) {
+    g.P <<= 1;
+    ++g.logP;
+  }
+  return g;
+}
+
+hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const TableDev& t, const Work& w, int64_t* h_live,
+                              int64_t tag, hipEvent_t* ev_tile, hipEvent_t* ev_part, hipStream_t s) {
   if (n <= 0) {
     k_zero_scalars<<<1, kCScalars, 0, s>>>(w.scal);
     return hipGetLastError();
   }
+  const FrontGeom& g = w.g;
+  if (ev_tile && ev_tile[0]) (void)hipEventRecord(ev_tile[0], s);
+  k_tile_dedup<kDedupThreads><<<static_cast<unsigned>(g.nblk), kDedupThreads, 0, s>>>(
+      values, n, w, reinterpret_cast<int*>(t.scal + kTErr));
+  if (ev_tile && ev_tile[1]) (void)hipEventRecord(ev_tile[1], s);
+  if (ev_part && ev_part[0]) (void)hipEventRecord(ev_part[0], s);
+  const int64_t na = static_cast<int64_t>(g.P) * g.nblk;
+  const int64_t nchp = (na + kScanChunk - 1) / kScanChunk;
+  k_scan_parts<<<static_cast<unsigned>(nchp), 1024, 0, s>>>(w.pcnt, na, w.pcsum, nchp, w.scal);
+  k_part_scatter<<<dim3(static_cast<unsigned>((g.rcap + 4 * kBlock - 1) / (4 * kBlock)), static_cast<unsigned>(g.nblk)),
+                   kBlock, 0, s>>>(w);
+  k_part_dedup<<<static_cast<unsigned>(g.P), kPartThreads, 0, s>>>(t, w, n);
   const int64_t nb = (n + kRankTile - 1) / kRankTile;
-  if (ev_local && ev_local[0]) (void)hipEventRecord(ev_local[0], s);
-  k_dedup_local<kDedupThreads><<<grid_for(n, kDedupThreads * kDedupItems, 1ll << 31), kDedupThreads, 0, s>>>(
-      values, n, sc, w.slot_of, w.occ_rank,
-                                                                     reinterpret_cast<int*>(t.scal + kTErr));
-  if (ev_local && ev_local[1]) (void)hipEventRecord(ev_local[1], s);
-  if (ev_probe && ev_probe[0]) (void)hipEventRecord(ev_probe[0], s);
-  k_rank_probe<kBlock><<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, sc, w.slot_of, n, w.bsum, w.ntiles,
-                                                                   w.scal);
-  if (ev_probe && ev_probe[1]) (void)hipEventRecord(ev_probe[1], s);
+  k_first_sums<kBlock><<<static_cast<unsigned>(nb), kBlock, 0, s>>>(w, n);
   const int64_t nch = (nb + kScanChunk - 1) / kScanChunk;
   k_scan5<kScanChunk / 1024><<<static_cast<unsigned>(nch), 1024, 0, s>>>(w.bsum, nb, w.ntiles, w.csum, nch, w.scal,
                                                                           t.scal, h_live, tag);
+  if (ev_part && ev_part[1]) (void)hipEventRecord(ev_part[1], s);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// pass 3: unique ids, segments, rows, IDMap inserts
+// pass 7: unique ids, segments, rows, IDMap inserts
 // ---------------------------------------------------------------------------
 
 template <int NT>
-__global__ __launch_bounds__(NT) void k_compact_insert(TableDev t, Scratch sc, Work w,
-                                                       const int64_t* __restrict__ values, int64_t n) {
+__global__ __launch_bounds__(NT) void k_compact(TableDev t, Work w, const int64_t* __restrict__ values, int64_t n) {
   __shared__ int sh[NT / kWave + 1][5];
   const int64_t i0 = static_cast<int64_t>(blockIdx.x) * NT * kRankItems + threadIdx.x * kRankItems;
   const int b = blockIdx.x;
@@ -523,25 +671,21 @@ __global__ __launch_bounds__(NT) void k_compact_insert(TableDev t, Scratch sc, W
   const int64_t nch = (static_cast<int64_t>(gridDim.x) + kScanChunk - 1) / kScanChunk;
 #pragma unroll
   for (int a = 0; a < 5; ++a) pre[a] = w.bsum[a * w.ntiles + b] + w.csum[a * nch + b / kScanChunk];
-  int s[4];
-  load4(w.slot_of, i0, n, s);
-  bool f[4];
-  ScratchAux ax0[4];
+  int f[4];
+  load4(w.firstkey, i0, n, f);
+  KeyInfo ki[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) ki[k] = key_info(w, f[k], n);  // all four reads in flight together
   int cf = 0, cc = 0, cn = 0, cl = 0, cu = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    f[k] = s[k] >= 0 && (s[k] & kFirstBit);
-    s[k] &= kSlotMask;
-    ax0[k] = sc.aux[f[k] ? s[k] : 0];  // all four reads in flight together
-  }
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    cf += f[k];
-    cc += f[k] ? ax0[k].count : 0;
-    cn += (f[k] && ax0[k].row < 0);
-    if (f[k] && ax0[k].count > kLong) {
+    if (f[k] < 0) continue;
+    cf += 1;
+    cc += ki[k].count;
+    cn += ki[k].row < 0;
+    if (ki[k].count > kLong) {
       cl += 1;
-      cu += unit_count(ax0[k].count);
+      cu += unit_count(ki[k].count);
     }
   }
   // the tile's first occurrences get consecutive unique ids, segments, rows
@@ -559,22 +703,21 @@ __global__ __launch_bounds__(NT) void k_compact_insert(TableDev t, Scratch sc, W
   if (blockIdx.x == 0 && threadIdx.x == 0 && w.scal[kCTrunc]) atomicOr(reinterpret_cast<int*>(&t.scal[kTErr]), kErrFull);
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    if (!f[k]) continue;
-    const int c = ax0[k].count;
-    const unsigned long long ekey = static_cast<unsigned long long>(values[i0 + k]) ^ kSign;
-    w.unique[uid] = values[i0 + k];
-    int li = -1, ush = 0;
+    if (f[k] < 0) continue;
+    const int c = ki[k].count;
+    const int64_t key = values[i0 + k];
+    w.unique[uid] = key;
+    int li = -1;
     if (c > kLong) {
       li = lnext++;
-      ush = unit_shift(c);
       w.long_u[li] = uid;
       w.long_start[li] = unext;
       unext += unit_count(c);
     }
-    int64_t row = ax0[k].row;
+    int64_t row = ki[k].row;
     if (row < 0) {
       if (nr < inserted) {
-        const int64_t slot = idmap_claim(t, ekey);
+        const int64_t slot = idmap_claim(t, static_cast<unsigned long long>(key) ^ kSign);
         if (slot >= 0) {
           row = live0 + nr;
           t.slots[slot].row = row;
@@ -587,15 +730,12 @@ __global__ __launch_bounds__(NT) void k_compact_insert(TableDev t, Scratch sc, W
     }
     w.rows[uid] = row;
     w.useg[uid] = Seg{row, start, c};
-    ScratchAux ax;
-    ax.row = row;
-    ax.start = start;
-    ax.uid = uid;
-    ax.count = c;
-    ax.long_idx = li;
-    ax.unit_shift = ush;
-    ax.pad = 0;
-    sc.aux[s[k]] = ax;
+    KeyInfo o = ki[k];
+    o.row = row;
+    o.uid = uid;
+    o.start = start;
+    o.long_idx = li;
+    w.kinfo[f[k]] = o;
     ++uid;
     start += c;
   }
@@ -650,41 +790,45 @@ __device__ inline void init_rows(const TableDev& t, const Work& w, int64_t blk, 
 }
 
 // The per-occurrence pass: inverse[i] = unique id of occurrence i (-1 for a
-// rejected key), and the occurrence of rank 0 of each key returns its scratch
-// slot to empty, so the scratch never needs a full clear.  For a forward
-// (OCC) it also writes each occurrence's row and its position in the
-// occurrence list, and the descriptor of every backward unit of a hot key.
+// rejected key).  For a forward (OCC) it also writes each occurrence's row
+// and its position in the occurrence list (the key's segment start + the
+// record's rank base + the rank inside the tile), and the descriptor of
+// every backward unit of a hot key.
 template <bool OCC>
-__device__ inline void occ_pass(const Scratch& sc, const Work& w, int64_t n, int64_t blk) {
+__device__ inline void occ_pass(const Work& w, int64_t n, int64_t blk) {
   const int64_t i0 = (blk * kBlock + threadIdx.x) * 4;
   if (i0 >= n) return;
-  int s[4], rk[4];
-  load4(w.slot_of, i0, n, s);
-  load4(w.occ_rank, i0, n, rk);
-  ScratchAux a[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) a[k] = sc.aux[s[k] >= 0 ? (s[k] & kSlotMask) : 0];  // all in flight together
+  const FrontGeom g = w.g;
+  int ow[4];
+  load4(reinterpret_cast<const int32_t*>(w.occ_word), i0, n, ow);  // -1 = kOccRejected past n
+  int2 rr[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    if (s[k] < 0) {
+    const uint32_t o = static_cast<uint32_t>(ow[k]);
+    const int64_t src = o == kOccRejected ? 0 : ((i0 + k) >> kDedupTileLog2) / g.R * g.rcap + (o >> 12);
+    rr[k] = w.recres[src];  // all in flight together
+  }
+  KeyInfo a[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) a[k] = key_info(w, rr[k].x, n);
+  int pos[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t o = static_cast<uint32_t>(ow[k]);
+    if (o == kOccRejected) {
       a[k].row = -1;
       a[k].uid = -1;
-      a[k].start = 0;
-      a[k].long_idx = -1;
+      pos[k] = -1;
+      continue;
     }
-  }
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    if (s[k] < 0 || i0 + k >= n) continue;
-    if (rk[k] == 0) sc.slot[s[k] & kSlotMask] = ScratchSlot{kEncEmpty, 0xFFFFFFFFu, 0u};
+    const int rk = rr[k].y + static_cast<int>(o & 0xFFFu);
+    pos[k] = a[k].start + rk;
     if (OCC && a[k].long_idx >= 0) {
-      const int sh = a[k].unit_shift;
+      const int sh = unit_shift(a[k].count);
       const int usz = kUnit << sh;
-      if ((rk[k] & (usz - 1)) == 0) {
-        const int p = a[k].start + rk[k];
-        w.units[w.long_start[a[k].long_idx] + (rk[k] >> (kUnitLog2 + sh))] =
-            Unit{a[k].long_idx, p, min(p + usz, a[k].start + a[k].count), 0};
-      }
+      if ((rk & (usz - 1)) == 0)
+        w.units[w.long_start[a[k].long_idx] + (rk >> (kUnitLog2 + sh))] =
+            Unit{a[k].long_idx, pos[k], min(pos[k] + usz, a[k].start + a[k].count), 0};
     }
   }
   if (i0 + 4 <= n) {
@@ -692,16 +836,14 @@ __device__ inline void occ_pass(const Scratch& sc, const Work& w, int64_t n, int
     if (OCC) {
       *reinterpret_cast<longlong2*>(w.occ_row + i0) = make_longlong2(a[0].row, a[1].row);
       *reinterpret_cast<longlong2*>(w.occ_row + i0 + 2) = make_longlong2(a[2].row, a[3].row);
-      *reinterpret_cast<int4*>(w.occ_pos + i0) =
-          make_int4(s[0] >= 0 ? a[0].start + rk[0] : -1, s[1] >= 0 ? a[1].start + rk[1] : -1,
-                    s[2] >= 0 ? a[2].start + rk[2] : -1, s[3] >= 0 ? a[3].start + rk[3] : -1);
+      *reinterpret_cast<int4*>(w.occ_pos + i0) = make_int4(pos[0], pos[1], pos[2], pos[3]);
     }
   } else {
     for (int k = 0; k < 4 && i0 + k < n; ++k) {
       w.inverse[i0 + k] = a[k].uid;
       if (OCC) {
         w.occ_row[i0 + k] = a[k].row;
-        w.occ_pos[i0 + k] = s[k] >= 0 ? a[k].start + rk[k] : -1;
+        w.occ_pos[i0 + k] = pos[k];
       }
     }
   }
@@ -711,19 +853,18 @@ __device__ inline void occ_pass(const Scratch& sc, const Work& w, int64_t n, int
 // pass, the others write the rows of the inserted keys (both only need the
 // compaction, so they share one launch).
 template <bool OCC>
-__global__ __launch_bounds__(kBlock) void k_occ_init(Scratch sc, TableDev t, Work w, int64_t n, int64_t occ_blocks) {
+__global__ __launch_bounds__(kBlock) void k_occ_init(TableDev t, Work w, int64_t n, int64_t occ_blocks) {
   const int64_t b = blockIdx.x;
-  if (b < occ_blocks) occ_pass<OCC>(sc, w, n, b);
+  if (b < occ_blocks) occ_pass<OCC>(w, n, b);
   else init_rows(t, w, b - occ_blocks, static_cast<int64_t>(gridDim.x) - occ_blocks);
 }
 
-hipError_t launch_compact_insert(const int64_t* values, int64_t n, const Scratch& sc, const TableDev& t, const Work& w,
-                                 bool occ_lists, hipEvent_t* ev_compact, hipEvent_t* ev_init, hipEvent_t* ev_occ,
-                                 hipStream_t s) {
+hipError_t launch_compact_insert(const int64_t* values, int64_t n, const TableDev& t, const Work& w, bool occ_lists,
+                                 hipEvent_t* ev_compact, hipEvent_t* ev_init, hipEvent_t* ev_occ, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   const int64_t nb = (n + kRankTile - 1) / kRankTile;
   if (ev_compact && ev_compact[0]) (void)hipEventRecord(ev_compact[0], s);
-  k_compact_insert<kBlock><<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, sc, w, values, n);
+  k_compact<kBlock><<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, w, values, n);
   if (ev_compact && ev_compact[1]) (void)hipEventRecord(ev_compact[1], s);
   // one launch: the per-occurrence pass and the new rows (the init-rows and
   // occurrence events both bracket it)
@@ -731,8 +872,8 @@ hipError_t launch_compact_insert(const int64_t* values, int64_t n, const Scratch
   if (ev_occ && ev_occ[0]) (void)hipEventRecord(ev_occ[0], s);
   const int64_t ob = grid_for(n, kBlock * 4, 1ll << 31);
   const int64_t ib = grid_for(n, kBlock / 16, 8192);
-  if (occ_lists) k_occ_init<true><<<static_cast<unsigned>(ob + ib), kBlock, 0, s>>>(sc, t, w, n, ob);
-  else k_occ_init<false><<<static_cast<unsigned>(ob + ib), kBlock, 0, s>>>(sc, t, w, n, ob);
+  if (occ_lists) k_occ_init<true><<<static_cast<unsigned>(ob + ib), kBlock, 0, s>>>(t, w, n, ob);
+  else k_occ_init<false><<<static_cast<unsigned>(ob + ib), kBlock, 0, s>>>(t, w, n, ob);
   if (ev_occ && ev_occ[1]) (void)hipEventRecord(ev_occ[1], s);
   if (ev_init && ev_init[1]) (void)hipEventRecord(ev_init[1], s);
   return hipGetLastError();

@@ -18,14 +18,26 @@ constexpr uint64_t kSign = 0x8000000000000000ull;
 constexpr unsigned long long kEncEmpty = 0ull;
 constexpr unsigned long long kEncTomb = 1ull;
 
-// Dedup: a block dedups a tile of occurrences in LDS before touching the
-// global scratch table, so a key costs one global insert per tile it occurs
-// in: 1024 threads x 4 occurrences per tile, 8192 LDS hash slots (136 KB).
+// Dedup, pass 1: a block dedups tiles of kDedupTile occurrences in LDS
+// (1024 threads x 4 occurrences, 8192 LDS hash slots) and writes one record
+// per distinct key of a tile, with the key's hash partition.
 constexpr int kDedupItems = 4;
 constexpr int kDedupThreads = 1024;
+constexpr int kDedupTile = kDedupThreads * kDedupItems;  // 4096
+constexpr int kDedupTileLog2 = 12;
+static_assert(kDedupTile == 1 << kDedupTileLog2, "tile is a power of two");
+// A dedup block takes at most kMaxTilesPerBlock consecutive tiles, so a
+// record index inside a block fits 19 bits (occ_word = index << 12 | rank).
+constexpr int kMaxTilesPerBlock = 128;
+// Hash partitions of the records (a power of two); the per-partition dedup
+// handles one partition per block with kPartSlots LDS hash slots.
+constexpr int kMaxParts = 4096;
+constexpr int kPartThreads = 512;
+constexpr int kPartSlots = 4096;
+constexpr int kPartSweep = 3072;  // records per LDS sweep (load <= 0.75)
 
-// Tile of the two passes that rank first occurrences (4 consecutive items
-// per thread: many resident waves for these latency-bound passes).
+// Tile of the passes over positions (4 consecutive items per thread: many
+// resident waves for these latency-bound passes).
 constexpr int kRankItems = 4;
 constexpr int kRankTile = kBlock * kRankItems;  // 1024
 // Tiles per block of the tile-sum scan.
@@ -61,7 +73,7 @@ __host__ __device__ inline int unit_count(int count) {
 constexpr int kResident = 2048;
 
 // Latched device error bits.
-enum : int { kErrKey = 1, kErrFull = 2, kErrScratch = 4, kErrProbe = 8 };
+enum : int { kErrKey = 1, kErrFull = 2, kErrProbe = 8 };
 
 // Table-resident device scalars.
 enum : int { kTLive = 0, kTLimit = 1, kTRowCap = 2, kTErr = 3, kTExport = 4, kTScalars = 8 };
@@ -76,7 +88,9 @@ enum : int {
   kCNUnits = 6,    // backward units of those keys
   kCTrunc = 7,     // 1 if some keys not found had no room (latched as RS_EFULL)
   kCScanDone = 8,  // blocks of the tile-sum scan that have finished
-  kCScalars = 9
+  kCPartDone = 9,  // blocks of the partition-count scan that have finished
+  kCRecords = 10,  // dedup records (tile-distinct keys)
+  kCScalars = 11
 };
 
 __host__ __device__ inline uint64_t mix64(uint64_t z) {
@@ -85,9 +99,9 @@ __host__ __device__ inline uint64_t mix64(uint64_t z) {
   return z ^ (z >> 31);
 }
 
-// Bucket hashes of the IDMap and of the dedup scratch (different salts).
+// Hashes of the IDMap buckets and of the dedup partitions (different salts).
 __device__ inline uint64_t idmap_hash(unsigned long long e) { return mix64(e ^ 0x2545F4914F6CDD1Dull); }
-__device__ inline uint64_t scratch_hash(unsigned long long e) { return mix64(e ^ 0x5BD1E9955BD1E995ull); }
+__device__ inline uint64_t part_hash(unsigned long long e) { return mix64(e ^ 0x5BD1E9955BD1E995ull); }
 
 struct alignas(16) Slot {
   unsigned long long key;  // encoded key
@@ -115,35 +129,45 @@ struct TableDev {
   float lo, span;  // init: fma(u, span, lo)
 };
 
-// Per-table dedup scratch: an open-addressing set of one call's keys, as two
-// arrays of structs so that every pass touches one cache sector per key.
-struct alignas(16) ScratchSlot {
-  unsigned long long key;  // encoded key (0: empty)
-  unsigned int first;      // first position of the key in the batch
-  unsigned int cnt;        // occurrences of the key
-};
-struct alignas(32) ScratchAux {
-  long long row;  // IDMap row (found by the probe pass, or assigned)
-  int start;      // first position of the key's segment of the occurrence list
-  int uid;        // unique id (first-occurrence order)
-  int count;      // occurrences
-  int long_idx;   // hot-key index, -1 if count <= kLong
-  int unit_shift; // hot key: backward units of kUnit << unit_shift positions
-  int pad;
-};
-struct Scratch {
-  ScratchSlot* slot;
-  ScratchAux* aux;
-  uint64_t mask;  // slots - 1
+// Geometry of the dedup passes for n occurrences (a pure function of n).
+struct FrontGeom {
+  int64_t ntiles;  // tiles of kDedupTile occurrences
+  int64_t R;       // tiles per dedup block (<= kMaxTilesPerBlock)
+  int64_t nblk;    // dedup blocks
+  int64_t rcap;    // record capacity of one dedup block (R * kDedupTile)
+  int P;           // hash partitions (power of two <= kMaxParts)
+  int logP;
 };
 
-// slot_of[i]: scratch slot of occurrence i (< 2^29 slots); kCandBit marks
-// the occurrence at its tile's first position of the key (only those can be
-// the key's first occurrence in the batch), kFirstBit the key's first
-// occurrence once known; -1 for a rejected key.
-constexpr int kCandBit = 1 << 30;
-constexpr int kFirstBit = 1 << 29;
-constexpr int kSlotMask = kFirstBit - 1;
+// Record of one distinct key of a dedup tile.  meta = (rank of the record
+// among its block's records of the same partition) << 12 | (count - 1).
+struct alignas(16) TileRec {
+  unsigned long long key;  // encoded key
+  unsigned int tmin;       // first position of the key in the tile
+  unsigned int meta;
+};
+
+// The same record moved into partition-major order.
+struct alignas(16) PartRec {
+  unsigned long long key;
+  unsigned int tmin;
+  unsigned int tcnt;  // occurrences of the key in the tile
+};
+
+// One distinct key of the call, indexed by its key index (a slot of the
+// partition-major record range of its partition).
+struct alignas(32) KeyInfo {
+  long long row;  // Blocks row (-1: not found / could not be inserted)
+  int first;      // first position of the key in the batch
+  int count;      // occurrences
+  int uid;        // unique id (first-occurrence order)
+  int start;      // first position of the key's segment of the occurrence list
+  int long_idx;   // hot-key index, -1 if count <= kLong
+  int pad;
+};
+
+// occ_word of a rejected (reserved) key
+constexpr uint32_t kOccRejected = 0xFFFFFFFFu;
 
 // Per-unique segment descriptor: the key's row, and where its occurrences
 // start in the occurrence list and how many there are.
@@ -159,8 +183,17 @@ struct alignas(16) Unit {
 
 // Workspace arrays of one forward (and its backward).
 struct Work {
-  int32_t* slot_of;     // [n] scratch slot per occurrence (| kCandBit)
-  int32_t* occ_rank;    // [n] rank of the occurrence among those of its key
+  uint32_t* occ_word;   // [n] dedup record index (in its block) << 12 | rank in the tile
+  int32_t* firstkey;    // [n] key index at the key's first position, else -1
+  TileRec* trec;        // [nblk * rcap] records of the dedup tiles, per block
+  int2* recres;         // [nblk * rcap] (same memory as trec) {key index, rank base} per record
+  int32_t* nrec;        // [nblk] records per dedup block
+  int32_t* pcnt;        // [P * nblk] records per (partition, block); scanned in place
+  int32_t* pcsum;       // [P * nblk / kScanChunk + 1] the same per chunk
+  PartRec* prec;        // [n] records in partition-major order
+  int32_t* psrc;        // [n] record index each partition-major record came from
+  int2* ptmp;           // [n] per partition-major record: LDS slot, rank base
+  KeyInfo* kinfo;       // [n] per key index
   int32_t* inverse;     // [n]
   int64_t* occ_row;     // [n] Blocks row of each occurrence (-1: none)
   int32_t* occ_pos;     // [n] position of each occurrence in the occurrence list
@@ -177,7 +210,8 @@ struct Work {
   int32_t* csum;        // [5 * (ntiles / kScanChunk + 1)] the same per chunk of tiles
   int64_t* scal;        // [kCScalars]
   float* gpart;         // [(2n/kUnit + 2) * D] partial gradient row of each backward unit
-  int64_t ntiles;       // tiles of the rank passes (bsum stride)
+  int64_t ntiles;       // tiles of the position passes (bsum stride)
+  FrontGeom g;
 };
 
 struct OptArgs {
@@ -188,21 +222,21 @@ struct OptArgs {
 // ---------------------------------------------------------------------------
 // launchers; all enqueue on `s` and return hipGetLastError()
 // ---------------------------------------------------------------------------
-// dedup + IDMap probe of first occurrences + 3-way scan (ends before the insert)
-// The scan also stores (tag << 48) | (live rows after the call) to h_live
-// (pinned host memory; may be null), so the host can refresh its bound on
-// the live count without a copy or an event.
-hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const Scratch& sc, const TableDev& t,
-                              const Work& w, int64_t* h_live, int64_t tag, hipEvent_t* ev_local,
-                              hipEvent_t* ev_probe, hipStream_t s);
+// Geometry of the dedup passes for n occurrences.
+FrontGeom front_geom(int64_t n);
+// Dedup of the call's keys in first-occurrence order and the IDMap probe
+// (ends before the insert): tile dedup, partition-count scan, scatter into
+// partitions, per-partition dedup + probe, tile sums of the first
+// occurrences and their scan.  The scan also stores (tag << 48) | (live rows
+// after the call) to h_live (pinned host memory; may be null), so the host
+// can refresh its bound on the live count without a copy or an event.
+hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const TableDev& t, const Work& w, int64_t* h_live,
+                              int64_t tag, hipEvent_t* ev_tile, hipEvent_t* ev_part, hipStream_t s);
 // unique / segments / rows / IDMap insert / row init, then the per-occurrence
-// pass: inverse[], scratch release and, for a forward (occ_lists), each
-// occurrence's row and list position and the hot keys' backward units
-hipError_t launch_compact_insert(const int64_t* values, int64_t n, const Scratch& sc, const TableDev& t,
-                                 const Work& w, bool occ_lists, hipEvent_t* ev_compact, hipEvent_t* ev_init,
-                                 hipEvent_t* ev_occ, hipStream_t s);
-// set every scratch slot to empty
-hipError_t launch_scratch_clear(ScratchSlot* slots, int64_t n, hipStream_t s);
+// pass: inverse[] and, for a forward (occ_lists), each occurrence's row and
+// list position and the hot keys' backward units
+hipError_t launch_compact_insert(const int64_t* values, int64_t n, const TableDev& t, const Work& w, bool occ_lists,
+                                 hipEvent_t* ev_compact, hipEvent_t* ev_init, hipEvent_t* ev_occ, hipStream_t s);
 // redo the row reservation of the last scan after the table has grown
 hipError_t launch_rereserve(const Work& w, const TableDev& t, int64_t* h_live, int64_t tag, hipStream_t s);
 hipError_t launch_map_rows(const Work& w, int64_t n, int64_t* rows_out, int64_t* n_inserted, hipStream_t s);

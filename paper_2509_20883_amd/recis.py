@@ -26,7 +26,7 @@ F32, BF16 = 0, 1
 ADAGRAD, ADAM = 0, 1
 # kernel ids of rs_set_kernel_events ("occ" and "init_rows" bracket the same
 # launch; "bwd_long" brackets the hot-key unit sums and their finish)
-KERNELS = {"dedup_local": 0, "rank_probe": 1, "compact_insert": 2, "init_rows": 3, "pool": 4,
+KERNELS = {"tile_dedup": 0, "partition": 1, "compact_insert": 2, "init_rows": 3, "pool": 4,
            "bwd_short": 5, "bwd_long": 6, "opt": 7, "occ": 8}
 
 
