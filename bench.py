@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--pipelined", action="store_true",
                     help="run the next batch's lookup_prepare on a second stream while the current batch pools and "
                          "runs its backward (default: one stream)")
+    ap.add_argument("--gen-workers", type=int, default=16,
+                    help="processes drawing the input batches before the GPU is touched (1: in-process, e.g. under "
+                         "a profiler)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (scales HBM byte counters)")
     return ap.parse_args()
@@ -150,13 +153,13 @@ def progress(msg: str):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def host_batches(k: int, nsteps: int):
+def host_batches(k: int, nsteps: int, workers: int = 16):
     """Every step's batch, drawn by a pool of forked worker processes before
     the GPU is touched (the draws are seeded per step, so the result does
     not depend on the number of workers)."""
     import multiprocessing as mp
 
-    nw = max(1, min(16, os.cpu_count() or 1, nsteps))
+    nw = max(1, min(workers, os.cpu_count() or 1, nsteps))
     out = [None] * nsteps
     t0 = time.time()
     if nw == 1:
@@ -230,7 +233,7 @@ def main():
     w = W.workload(a.workload)
     nsteps = a.warmup + a.steps
     t_setup = time.time()
-    hb = host_batches(a.workload, nsteps)  # before the GPU is initialised (forked workers)
+    hb = host_batches(a.workload, nsteps, a.gen_workers)  # before the GPU is initialised (forked workers)
 
     import torch
 

@@ -45,7 +45,7 @@ bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
 
 // Workspace layout of one forward: every array sized by the upper bound n.
 struct Layout {
-  size_t occ_word, firstkey, trec, nrec, pcnt, pcsum, prec, psrc, ptmp, kinfo, inverse, occ_row, occ_pos, unique,
+  size_t occ_word, firstkey, trec, srec, pcnt, poff, ptmp, kinfo, inverse, occ_row, occ_pos, unique,
       useg, rows, new_list, occ_ref, long_u, long_start, units, bsum, csum, scal, gpart, total;
   int64_t ntiles;
   FrontGeom g;
@@ -69,13 +69,11 @@ Layout make_layout(int64_t n, int dim) {
   L.occ_word = take(4 * n1);
   L.firstkey = take(4 * n1);
   L.trec = take(sizeof(TileRec) * nrecs);  // also the records' results (int2 each)
-  L.nrec = take(4 * static_cast<size_t>(L.g.nblk));
+  L.srec = take(sizeof(TileRec) * nrecs);
   L.pcnt = take(4 * npc);
-  L.pcsum = take(4 * (npc / kScanChunk + 1));
-  L.prec = take(sizeof(PartRec) * n1);
-  L.psrc = take(4 * n1);
-  L.ptmp = take(8 * n1);
-  L.kinfo = take(sizeof(KeyInfo) * n1);
+  L.poff = take(4 * npc);
+  L.ptmp = take(8 * nrecs);
+  L.kinfo = take(sizeof(KeyInfo) * nrecs);
   L.inverse = take(4 * n1);
   L.occ_row = take(8 * n1);
   L.occ_pos = take(4 * n1);
@@ -102,13 +100,12 @@ Work make_work(void* base, const Layout& L) {
   w.firstkey = reinterpret_cast<int32_t*>(b + L.firstkey);
   w.trec = reinterpret_cast<TileRec*>(b + L.trec);
   w.recres = reinterpret_cast<int2*>(b + L.trec);
-  w.nrec = reinterpret_cast<int32_t*>(b + L.nrec);
+  w.srec = reinterpret_cast<TileRec*>(b + L.srec);
   w.pcnt = reinterpret_cast<int32_t*>(b + L.pcnt);
-  w.pcsum = reinterpret_cast<int32_t*>(b + L.pcsum);
-  w.prec = reinterpret_cast<PartRec*>(b + L.prec);
-  w.psrc = reinterpret_cast<int32_t*>(b + L.psrc);
+  w.poff = reinterpret_cast<int32_t*>(b + L.poff);
   w.ptmp = reinterpret_cast<int2*>(b + L.ptmp);
   w.kinfo = reinterpret_cast<KeyInfo*>(b + L.kinfo);
+  w.nkeyidx = L.g.nblk * L.g.rcap;
   w.inverse = reinterpret_cast<int32_t*>(b + L.inverse);
   w.occ_row = reinterpret_cast<int64_t*>(b + L.occ_row);
   w.occ_pos = reinterpret_cast<int32_t*>(b + L.occ_pos);
@@ -287,12 +284,15 @@ rs_status rehash(rs_table* t, int64_t new_cap, hipStream_t s) {
   return RS_OK;
 }
 
-// Grow (when allowed) so that `live_need` keys fit the IDMap and the Blocks;
-// `batch` (the ids of the call) sizes the Blocks headroom.
+// Grow (when allowed) so that `live_need` keys fit the IDMap and the Blocks.
+// `batch` (the ids of the call) sizes the headroom: the IDMap is doubled
+// until another call of `batch` ids would fit as well, so the host's upper
+// bound on the live count (live + ids of the call) does not force a
+// synchronization on every call of a batch larger than the free room.
 rs_status grow_for(rs_table* t, int64_t live_need, int64_t batch, hipStream_t s) {
   if (t->d.auto_grow) {
     int64_t c = t->cap;
-    while (static_cast<double>(live_need) > static_cast<double>(t->d.max_load) * static_cast<double>(c)) c <<= 1;
+    while (static_cast<double>(live_need + batch) > static_cast<double>(t->d.max_load) * static_cast<double>(c)) c <<= 1;
     if (c != t->cap) {
       rs_status st = rehash(t, c, s);
       if (st != RS_OK) return st;

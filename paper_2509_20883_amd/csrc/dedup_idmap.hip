@@ -8,13 +8,12 @@
 // partition instead, so every key is counted by exactly one block in LDS.
 //   k_tile_dedup     per block, consecutive tiles of 4096 occurrences: LDS
 //                    dedup; one record per distinct key of a tile (key, first
-//                    position and count in the tile) with its rank among the
-//                    block's records of the key's hash partition
-//   k_scan_parts     exclusive scan of the (partition, block) record counts
-//   k_part_scatter   records into partition-major order
-//   k_part_dedup     one block per partition: LDS dedup of its records (first
-//                    position = min, count = sum, rank base of each record),
-//                    the key's IDMap probe, and a marker at its first position
+//                    position and count in the tile); at the end the block
+//                    copies its records into partition order
+//   k_part_dedup     one block per partition, reading its records from every
+//                    dedup block: LDS dedup (first position = min, count =
+//                    sum, rank base of each record), the key's IDMap probe,
+//                    and a marker at its first position
 //   k_first_sums     per tile of positions: sums over the first occurrences
 //                    (keys, counts, keys not found, hot keys, backward units)
 //   k_scan5          scan of those tile sums; reserves the rows of new keys
@@ -139,10 +138,7 @@ __global__ __launch_bounds__(NT) void k_tile_dedup(const int64_t* __restrict__ v
   const int tid = threadIdx.x;
   const int64_t blk = blockIdx.x;
   for (int q = tid; q < g.P; q += NT) lpc[q] = 0u;
-  if (blk == 0 && tid == 0) {  // completion counters of the two scans of this call
-    w.scal[kCScanDone] = 0;
-    w.scal[kCPartDone] = 0;
-  }
+  if (blk == 0 && tid == 0) w.scal[kCScanDone] = 0;  // completion counter of this call's scan
   const int64_t t0 = blk * g.R;
   const int64_t t1 = min(t0 + g.R, g.ntiles);
   TileRec* rec = w.trec + blk * g.rcap;
@@ -161,10 +157,12 @@ __global__ __launch_bounds__(NT) void k_tile_dedup(const int64_t* __restrict__ v
 #pragma unroll
       for (int k = 0; k < kDedupItems; ++k) nxt[k] = values[min(base + TILE + k * NT + tid, n - 1)];
     }
-    for (int q = tid; q < SLOTS; q += NT) {
-      lkey[q] = kEncEmpty;
-      lmin[q] = 0xFFFFFFFFu;
-      lcnt[q] = 0u;
+    if (tile == t0) {  // later tiles find the table cleared by their predecessor
+      for (int q = tid; q < SLOTS; q += NT) {
+        lkey[q] = kEncEmpty;
+        lmin[q] = 0xFFFFFFFFu;
+        lcnt[q] = 0u;
+      }
     }
     __syncthreads();
     int ls[kDedupItems];
@@ -219,94 +217,59 @@ __global__ __launch_bounds__(NT) void k_tile_dedup(const int64_t* __restrict__ v
       w.firstkey[i] = -1;
     }
     nrec += static_cast<unsigned int>(d);
-    __syncthreads();  // the next tile clears the LDS
+    __syncthreads();
+    // empty the occupied slots for the next tile
+    for (int q = tid; q < d; q += NT) {
+      const int sl = ldense[q];
+      lkey[sl] = kEncEmpty;
+      lmin[sl] = 0xFFFFFFFFu;
+      lcnt[sl] = 0u;
+    }
   }
-  for (int q = tid; q < g.P; q += NT) w.pcnt[static_cast<int64_t>(q) * g.nblk + blk] = static_cast<int>(lpc[q]);
-  if (tid == 0) w.nrec[blk] = static_cast<int>(nrec);
-}
-
-// ---------------------------------------------------------------------------
-// pass 2: exclusive scan of the (partition, block) record counts
-// ---------------------------------------------------------------------------
-
-// Block c scans chunk c (kScanChunk counts) in place and stores its total;
-// the last block to finish (a counter, no waiting) scans the chunk totals in
-// place and stores the number of records.  The offset of entry x is then
-// a[x] + csum[x / kScanChunk].
-__global__ __launch_bounds__(1024) void k_scan_parts(int32_t* __restrict__ a, int64_t na, int32_t* __restrict__ csum,
-                                                     int64_t nch, int64_t* cscal) {
-  constexpr int R = kScanChunk / 1024;
-  __shared__ int sh[1024 / kWave + 1];
-  __shared__ bool last;
-  const int64_t c = blockIdx.x;
-  const int64_t lo = c * kScanChunk + static_cast<int64_t>(threadIdx.x) * R;
-  int v[R];
-  int local = 0;
+  // the block's records per partition and their offsets in partition order
+  // (in place in lpc), then the partition-ordered copy of the records
+  constexpr int PPT = kMaxParts / NT;
+  int c[PPT];
+  int loc = 0;
 #pragma unroll
-  for (int j = 0; j < R; ++j) {
-    v[j] = lo + j < na ? a[lo + j] : 0;
-    local += v[j];
+  for (int j = 0; j < PPT; ++j) {
+    const int q = tid * PPT + j;
+    c[j] = q < g.P ? static_cast<int>(lpc[q]) : 0;
+    loc += c[j];
   }
   int tot;
-  int run = block_excl_scan<1024>(local, sh, tot);
+  int run = block_excl_scan<NT>(loc, sh, tot);
 #pragma unroll
-  for (int j = 0; j < R; ++j) {
-    if (lo + j < na) a[lo + j] = run;
-    run += v[j];
-  }
-  if (threadIdx.x == 0) {
-    csum[c] = tot;
-    __threadfence();
-    const unsigned long long done = atomicAdd(reinterpret_cast<unsigned long long*>(&cscal[kCPartDone]), 1ull);
-    last = done == static_cast<unsigned long long>(nch - 1);
+  for (int j = 0; j < PPT; ++j) {
+    const int q = tid * PPT + j;
+    if (q < g.P) {
+      w.pcnt[blk * g.P + q] = c[j];
+      w.poff[blk * g.P + q] = run;
+      lpc[q] = static_cast<unsigned int>(run);
+    }
+    run += c[j];
   }
   __syncthreads();
-  if (!last) return;
-  __threadfence();
-  const int64_t clo = static_cast<int64_t>(threadIdx.x) * R;  // nch <= 1024 R
-  local = 0;
+  TileRec* srt = w.srec + blk * g.rcap;
+  constexpr int U8 = 8;  // records in flight per thread
+  for (unsigned int j0 = tid; j0 < nrec; j0 += U8 * NT) {
+    TileRec r[U8];
 #pragma unroll
-  for (int j = 0; j < R; ++j) {
-    v[j] = clo + j < nch ? __hip_atomic_load(&csum[clo + j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
-    local += v[j];
-  }
-  run = block_excl_scan<1024>(local, sh, tot);
+    for (int u = 0; u < U8; ++u) {
+      const unsigned int j = j0 + u * NT;
+      if (j < nrec) r[u] = rec[j];
+    }
 #pragma unroll
-  for (int j = 0; j < R; ++j) {
-    if (clo + j < nch) csum[clo + j] = run;
-    run += v[j];
-  }
-  if (threadIdx.x == 0) {
-    cscal[kCRecords] = tot;
-    cscal[kCPartDone] = 0;
-  }
-}
-
-__device__ inline int64_t part_offset(const Work& w, int64_t x) {
-  return static_cast<int64_t>(w.pcnt[x]) + w.pcsum[x / kScanChunk];
-}
-
-// ---------------------------------------------------------------------------
-// pass 3: records into partition-major order (grid: x over a block's
-// records, y = dedup block)
-// ---------------------------------------------------------------------------
-
-__global__ __launch_bounds__(kBlock) void k_part_scatter(Work w) {
-  const FrontGeom g = w.g;
-  const int64_t b = blockIdx.y;
-  const int64_t nr = w.nrec[b];
-  for (int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j < nr;
-       j += static_cast<int64_t>(gridDim.x) * kBlock) {
-    const TileRec r = w.trec[b * g.rcap + j];
-    const int64_t x = static_cast<int64_t>(part_of(r.key, g.logP)) * g.nblk + b;
-    const int64_t dest = part_offset(w, x) + (r.meta >> 12);
-    w.prec[dest] = PartRec{r.key, r.tmin, (r.meta & 0xFFFu) + 1u};
-    w.psrc[dest] = static_cast<int>(b * g.rcap + j);
+    for (int u = 0; u < U8; ++u) {
+      const unsigned int j = j0 + u * NT;
+      if (j < nrec)
+        srt[lpc[part_of(r[u].key, g.logP)] + (r[u].meta >> 12)] = TileRec{r[u].key, r[u].tmin, (j << 12) | (r[u].meta & 0xFFFu)};
+    }
   }
 }
 
 // ---------------------------------------------------------------------------
-// pass 4: one block per partition: LDS dedup of its records, IDMap probe
+// pass 2: one block per partition: LDS dedup of its records, IDMap probe
 // ---------------------------------------------------------------------------
 
 // Resolve a probe batch read at the key's home slot; continue the probe if
@@ -326,57 +289,198 @@ __device__ inline int64_t resolve_probe(const TableDev& t, unsigned long long e,
   return r;
 }
 
-// Records of the partition are taken in sweeps of at most kPartSweep (by a
-// hash of the key), so a sweep's distinct keys fit the LDS table; if one
-// does not (a skewed hash), the partition starts again with twice as many
-// sweeps.  Key indices of the partition are lo + (dense index), all < hi.
+// The partition's records are read from every dedup block's
+// partition-ordered copy (segment b: cnt[b] records at off[b]).  A key's
+// index is the position of the record that entered it into the LDS table.
+// A partition of at most kPartSlots records is done in one pass with each
+// thread's records in registers (its distinct keys always fit the table);
+// a larger one in sweeps of at most kPartSweep records by a hash of the key,
+// and if a sweep's keys do not fit (a skewed hash) the partition starts
+// again with twice as many sweeps.
+__device__ inline void probe_store_keys(const TableDev& t, const Work& w, int64_t n, int d, const short* cdense,
+                                        const unsigned long long* ckey, const unsigned int* cfirst,
+                                        const unsigned int* ccnt, const unsigned int* cpos) {
+  constexpr int NT = kPartThreads;
+  constexpr int KP = 4;  // keys per thread per round: their probe batches in flight together
+  for (int q0 = 0; q0 < d; q0 += KP * NT) {
+    int sl[KP];
+    unsigned long long e[KP];
+    uint64_t h[KP];
+    Slot pb[KP][kProbeBatch];
+#pragma unroll
+    for (int u = 0; u < KP; ++u) {
+      const int q = q0 + u * NT + static_cast<int>(threadIdx.x);
+      sl[u] = q < d ? cdense[q] : -1;
+      e[u] = sl[u] >= 0 ? ckey[sl[u]] : kEncEmpty;
+      h[u] = sl[u] >= 0 ? (idmap_hash(e[u]) & t.cap_mask) : 0;  // idle lanes read one shared line
+#pragma unroll
+      for (int k = 0; k < kProbeBatch; ++k) pb[u][k] = t.slots[(h[u] + k) & t.cap_mask];
+    }
+#pragma unroll
+    for (int u = 0; u < KP; ++u) {
+      if (sl[u] < 0) continue;
+      const unsigned int kidx = cpos[sl[u]];
+      KeyInfo ki;
+      ki.row = resolve_probe(t, e[u], h[u], pb[u]);
+      ki.first = static_cast<int>(cfirst[sl[u]]);
+      ki.count = static_cast<int>(ccnt[sl[u]]);
+      ki.uid = -1;
+      ki.start = 0;
+      ki.long_idx = -1;
+      ki.pad = 0;
+      w.kinfo[kidx] = ki;
+      if (cfirst[sl[u]] < static_cast<uint64_t>(n)) w.firstkey[cfirst[sl[u]]] = static_cast<int>(kidx);
+    }
+  }
+}
+
+// Enter key e into the LDS table (linear probing from slot h); the thread
+// that enters it records `pos` as the key index.  Returns the slot, or -1
+// if every slot holds another key.
+__device__ inline int lds_insert(unsigned long long* ckey, unsigned int* cpos, unsigned long long e, uint64_t hh,
+                                 int pos) {
+  constexpr int S = kPartSlots;
+  unsigned int sl = static_cast<unsigned int>(hh >> 20) & (S - 1);
+  for (int probes = 0; probes < S; ++probes) {
+    const unsigned long long old = atomicCAS(&ckey[sl], kEncEmpty, e);
+    if (old == kEncEmpty) cpos[sl] = static_cast<unsigned int>(pos);
+    if (old == kEncEmpty || old == e) return static_cast<int>(sl);
+    sl = (sl + 1) & (S - 1);
+  }
+  return -1;
+}
+
 __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w, int64_t n) {
-  constexpr int NT = kPartThreads, S = kPartSlots, OWN = S / NT;
+  constexpr int NT = kPartThreads, S = kPartSlots, OWN = S / NT, K = kPartPer;
   constexpr int kMaxSweeps = 1 << 10;
+  constexpr int BPT = (kMaxDedupBlocks + NT - 1) / NT;
   __shared__ unsigned long long ckey[S];
   __shared__ unsigned int cfirst[S];
-  __shared__ unsigned int ccnt[S];  // count, then the key's dense index
+  __shared__ unsigned int ccnt[S];
+  __shared__ unsigned int cpos[S];  // key index (position of the record that entered the key)
   __shared__ short cdense[S];       // dense index -> slot
+  __shared__ int cpre[kMaxDedupBlocks];   // exclusive prefix of the segment sizes
+  __shared__ int cbase[kMaxDedupBlocks];  // position of each segment
   __shared__ int sh[NT / kWave + 1];
   __shared__ int ovf;
   const FrontGeom g = w.g;
   const int tid = threadIdx.x;
   const int p = blockIdx.x;
-  const int64_t lo = part_offset(w, static_cast<int64_t>(p) * g.nblk);
-  const int64_t hi = p + 1 < g.P ? part_offset(w, static_cast<int64_t>(p + 1) * g.nblk) : w.scal[kCRecords];
-  if (hi <= lo) return;  // the whole block: before any barrier
-  int nsw = static_cast<int>(min<int64_t>((hi - lo + kPartSweep - 1) / kPartSweep, kMaxSweeps));
-  int64_t dbase = 0;
-  int s = 0;
-  while (s < nsw) {
-    for (int q = tid; q < S; q += NT) {
-      ckey[q] = kEncEmpty;
-      cfirst[q] = 0xFFFFFFFFu;
-      ccnt[q] = 0u;
+  // the partition's segments (thread tid holds blocks tid*BPT ...)
+  int cn[BPT];
+  int loc = 0;
+#pragma unroll
+  for (int j = 0; j < BPT; ++j) {
+    const int b = tid * BPT + j;
+    cn[j] = b < g.nblk ? w.pcnt[static_cast<int64_t>(b) * g.P + p] : 0;
+    if (b < g.nblk) cbase[b] = static_cast<int>(b * g.rcap) + w.poff[static_cast<int64_t>(b) * g.P + p];
+    loc += cn[j];
+  }
+  int nr;
+  int run = block_excl_scan<NT>(loc, sh, nr);
+#pragma unroll
+  for (int j = 0; j < BPT; ++j) {
+    const int b = tid * BPT + j;
+    if (b < g.nblk) cpre[b] = run;
+    run += cn[j];
+  }
+  for (int q = tid; q < S; q += NT) {
+    ckey[q] = kEncEmpty;
+    cfirst[q] = 0xFFFFFFFFu;
+    ccnt[q] = 0u;
+  }
+  __syncthreads();
+  if (nr == 0) return;  // the whole block
+  const int nb = static_cast<int>(g.nblk);
+  // position of the fr-th record of the partition: the last segment whose
+  // prefix is <= fr (empty segments share their successor's prefix)
+  auto rec_pos = [&](int fr) {
+    int lo = 0, hi = nb;  // cpre[lo] <= fr; the answer is in [lo, hi)
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (cpre[mid] <= fr) lo = mid;
+      else hi = mid;
     }
+    return cbase[lo] + (fr - cpre[lo]);
+  };
+  auto dense_list = [&]() {
+    int occ = 0;
+#pragma unroll
+    for (int j = 0; j < OWN; ++j) occ += ckey[tid * OWN + j] != kEncEmpty;
+    int d;
+    int at = block_excl_scan<NT>(occ, sh, d);
+#pragma unroll
+    for (int j = 0; j < OWN; ++j)
+      if (ckey[tid * OWN + j] != kEncEmpty) cdense[at++] = static_cast<short>(tid * OWN + j);
+    __syncthreads();
+    return d;
+  };
+
+  if (nr <= NT * K) {
+    // one pass: the thread's records tid, tid + NT, ... stay in registers
+    int pos[K];
+    TileRec x[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) pos[k] = tid + k * NT < nr ? rec_pos(tid + k * NT) : -1;
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+      if (pos[k] >= 0) x[k] = w.srec[pos[k]];
+    int sl[K];
+    unsigned int rb[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      sl[k] = -1;
+      rb[k] = 0;
+      if (pos[k] < 0) continue;
+      sl[k] = lds_insert(ckey, cpos, x[k].key, part_hash(x[k].key), pos[k]);  // nr <= S: always found
+      if (sl[k] < 0) {
+        pos[k] = -1;
+        continue;
+      }
+      atomicMin(&cfirst[sl[k]], x[k].tmin);
+      rb[k] = atomicAdd(&ccnt[sl[k]], (x[k].meta & 0xFFFu) + 1u);
+    }
+    __syncthreads();
+    const int d = dense_list();
+    probe_store_keys(t, w, n, d, cdense, ckey, cfirst, ccnt, cpos);
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      if (pos[k] < 0) continue;
+      const int64_t src = (static_cast<int64_t>(pos[k]) / g.rcap) * g.rcap + (x[k].meta >> 12);
+      w.recres[src] = make_int2(static_cast<int>(cpos[sl[k]]), static_cast<int>(rb[k]));
+    }
+    return;
+  }
+
+  // sweeps (rare: a partition far above the average size)
+  int nsw = min((nr + kPartSweep - 1) / kPartSweep, kMaxSweeps);
+  int s = 0;
+  bool fresh = true;  // the table is clear
+  while (s < nsw) {
+    if (!fresh) {
+      for (int q = tid; q < S; q += NT) {
+        ckey[q] = kEncEmpty;
+        cfirst[q] = 0xFFFFFFFFu;
+        ccnt[q] = 0u;
+      }
+    }
+    fresh = false;
     if (tid == 0) ovf = 0;
     __syncthreads();
-    for (int64_t r = lo + tid; r < hi; r += NT) {
-      const PartRec x = w.prec[r];
+    for (int fr = tid; fr < nr; fr += NT) {
+      const int pos = rec_pos(fr);
+      const TileRec x = w.srec[pos];
       const uint64_t h = part_hash(x.key);
-      if (nsw > 1 && static_cast<int>((h & 0xFFFFFull) % static_cast<uint64_t>(nsw)) != s) continue;
-      unsigned int sl = static_cast<unsigned int>(h >> 20) & (S - 1);
-      bool ok = false;
-      for (int probes = 0; probes < S; ++probes) {
-        const unsigned long long old = atomicCAS(&ckey[sl], kEncEmpty, x.key);
-        if (old == kEncEmpty || old == x.key) {
-          ok = true;
-          break;
-        }
-        sl = (sl + 1) & (S - 1);
-      }
-      if (!ok) {
+      if (static_cast<int>((h & 0xFFFFFull) % static_cast<uint64_t>(nsw)) != s) continue;
+      const int sl = lds_insert(ckey, cpos, x.key, h, pos);
+      if (sl < 0) {
         ovf = 1;
         continue;
       }
       atomicMin(&cfirst[sl], x.tmin);
-      const unsigned int rb = atomicAdd(&ccnt[sl], x.tcnt);
-      w.ptmp[r] = make_int2(static_cast<int>(sl), static_cast<int>(rb));
+      const unsigned int rb = atomicAdd(&ccnt[sl], (x.meta & 0xFFFu) + 1u);
+      w.ptmp[pos] = make_int2(static_cast<int>(((x.meta >> 12) << 12) | static_cast<unsigned int>(sl)),
+                              static_cast<int>(rb));
     }
     __syncthreads();
     if (ovf) {
@@ -387,56 +491,18 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
       }
       nsw *= 2;
       s = 0;
-      dbase = 0;
       continue;
     }
-    // dense numbering of the occupied slots
-    int occ = 0;
-#pragma unroll
-    for (int j = 0; j < OWN; ++j) occ += ckey[tid * OWN + j] != kEncEmpty;
-    int d;
-    int at = block_excl_scan<NT>(occ, sh, d);
-#pragma unroll
-    for (int j = 0; j < OWN; ++j)
-      if (ckey[tid * OWN + j] != kEncEmpty) cdense[at++] = static_cast<short>(tid * OWN + j);
-    __syncthreads();
-    // one key per dense index: its IDMap probe (idle lanes read one shared
-    // line), key info, and the marker at its first position
-    for (int q0 = 0; q0 < d; q0 += NT) {
-      const int q = q0 + tid;
-      const bool act = q < d;
-      const int sl = act ? cdense[q] : 0;
-      const unsigned long long e = act ? ckey[sl] : kEncEmpty;
-      const uint64_t h = act ? (idmap_hash(e) & t.cap_mask) : 0;
-      Slot pb[kProbeBatch];
-#pragma unroll
-      for (int k = 0; k < kProbeBatch; ++k) pb[k] = t.slots[(h + k) & t.cap_mask];
-      if (act) {
-        const int64_t kidx = lo + dbase + q;
-        KeyInfo ki;
-        ki.row = resolve_probe(t, e, h, pb);
-        ki.first = static_cast<int>(cfirst[sl]);
-        ki.count = static_cast<int>(ccnt[sl]);
-        ki.uid = -1;
-        ki.start = 0;
-        ki.long_idx = -1;
-        ki.pad = 0;
-        w.kinfo[kidx] = ki;
-        if (cfirst[sl] < static_cast<uint64_t>(n)) w.firstkey[cfirst[sl]] = static_cast<int>(kidx);
-        ccnt[sl] = static_cast<unsigned int>(q);
-      }
+    const int d = dense_list();
+    probe_store_keys(t, w, n, d, cdense, ckey, cfirst, ccnt, cpos);
+    for (int fr = tid; fr < nr; fr += NT) {
+      const int pos = rec_pos(fr);
+      const uint64_t h = part_hash(w.srec[pos].key);
+      if (static_cast<int>((h & 0xFFFFFull) % static_cast<uint64_t>(nsw)) != s) continue;
+      const int2 tp = w.ptmp[pos];
+      const int64_t src = (static_cast<int64_t>(pos) / g.rcap) * g.rcap + (static_cast<uint32_t>(tp.x) >> 12);
+      w.recres[src] = make_int2(static_cast<int>(cpos[tp.x & 0xFFF]), tp.y);
     }
-    __syncthreads();
-    // each record of the sweep: its key index and rank base
-    for (int64_t r = lo + tid; r < hi; r += NT) {
-      if (nsw > 1) {
-        const uint64_t h = part_hash(w.prec[r].key);
-        if (static_cast<int>((h & 0xFFFFFull) % static_cast<uint64_t>(nsw)) != s) continue;
-      }
-      const int2 tp = w.ptmp[r];
-      w.recres[w.psrc[r]] = make_int2(static_cast<int>(lo + dbase + ccnt[tp.x]), tp.y);
-    }
-    dbase += d;
     ++s;
     __syncthreads();  // the next sweep clears the LDS
   }
@@ -461,8 +527,8 @@ __device__ inline void load4(const int32_t* __restrict__ p, int64_t i0, int64_t 
 
 // Key info of key index k (k >= 0), or of index 0 for an idle lane (read,
 // never used: every load of a step is issued before its results are waited for).
-__device__ inline KeyInfo key_info(const Work& w, int k, int64_t n) {
-  return w.kinfo[min(max(k, 0), static_cast<int>(n - 1))];
+__device__ inline KeyInfo key_info(const Work& w, int k) {
+  return w.kinfo[min(max(k, 0), static_cast<int>(w.nkeyidx - 1))];
 }
 
 template <int NT>
@@ -473,7 +539,7 @@ __global__ __launch_bounds__(NT) void k_first_sums(Work w, int64_t n) {
   load4(w.firstkey, i0, n, f);
   KeyInfo ki[4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) ki[k] = key_info(w, f[k], n);
+  for (int k = 0; k < 4; ++k) ki[k] = key_info(w, f[k]);
   int cf = 0, c = 0, nw = 0, nl = 0, nu = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
@@ -543,39 +609,44 @@ __global__ __launch_bounds__(1024) void k_scan5(int32_t* __restrict__ bsum, int6
       run += v[a][j];
     }
   }
-  if (threadIdx.x == 0) {
+  if (nch == 1) {
+    // one chunk: its totals are the totals (no chunk scan, no counter)
+    if (threadIdx.x < 5) csum[threadIdx.x] = 0;
+  } else {
+    if (threadIdx.x == 0) {
 #pragma unroll
-    for (int a = 0; a < 5; ++a) csum[a * nch + c] = tot[a];
+      for (int a = 0; a < 5; ++a) csum[a * nch + c] = tot[a];
+      __threadfence();
+      const unsigned long long done =
+          atomicAdd(reinterpret_cast<unsigned long long*>(&cscal[kCScanDone]), 1ull);
+      last = done == static_cast<unsigned long long>(nch - 1);
+    }
+    __syncthreads();
+    if (!last) return;
     __threadfence();
-    const unsigned long long done =
-        atomicAdd(reinterpret_cast<unsigned long long*>(&cscal[kCScanDone]), 1ull);
-    last = done == static_cast<unsigned long long>(nch - 1);
-  }
-  __syncthreads();
-  if (!last) return;
-  __threadfence();
-  // the last block: exclusive scan of the chunk totals (nch <= 1024 R)
-  int cv[5][R];
-  const int64_t clo = static_cast<int64_t>(threadIdx.x) * R;
+    // the last block: exclusive scan of the chunk totals (nch <= 1024 R)
+    int cv[5][R];
+    const int64_t clo = static_cast<int64_t>(threadIdx.x) * R;
 #pragma unroll
-  for (int a = 0; a < 5; ++a)
+    for (int a = 0; a < 5; ++a)
 #pragma unroll
-    for (int j = 0; j < R; ++j)
-      cv[a][j] = clo + j < nch ? __hip_atomic_load(&csum[a * nch + clo + j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+      for (int j = 0; j < R; ++j)
+        cv[a][j] = clo + j < nch ? __hip_atomic_load(&csum[a * nch + clo + j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
 #pragma unroll
-  for (int a = 0; a < 5; ++a) {
-    local[a] = 0;
+    for (int a = 0; a < 5; ++a) {
+      local[a] = 0;
 #pragma unroll
-    for (int j = 0; j < R; ++j) local[a] += cv[a][j];
-  }
-  block_excl_scan5<1024>(local, ex, tot, sh);
+      for (int j = 0; j < R; ++j) local[a] += cv[a][j];
+    }
+    block_excl_scan5<1024>(local, ex, tot, sh);
 #pragma unroll
-  for (int a = 0; a < 5; ++a) {
-    int run = ex[a];
+    for (int a = 0; a < 5; ++a) {
+      int run = ex[a];
 #pragma unroll
-    for (int j = 0; j < R; ++j) {
-      if (clo + j < nch) csum[a * nch + clo + j] = run;
-      run += cv[a][j];
+      for (int j = 0; j < R; ++j) {
+        if (clo + j < nch) csum[a * nch + clo + j] = run;
+        run += cv[a][j];
+      }
     }
   }
   if (threadIdx.x != 0) return;
@@ -624,7 +695,9 @@ FrontGeom front_geom(int64_t n) {
   g.rcap = g.R * kDedupTile;
   g.P = 1;
   g.logP = 0;
-  while (g.P < kMaxParts && static_cast<int64_t>(g.P) * 2048 < n1) {
+  // about 4096 ids (some 1500-2000 records) per partition: the partitions of
+  // a batch up to ~3M ids are all resident at once (3 blocks per CU)
+  while (g.P < kMaxParts && static_cast<int64_t>(g.P) * 4096 < n1) {
     g.P <<= 1;
     ++g.logP;
   }
@@ -638,16 +711,12 @@ hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const TableDev& 
     return hipGetLastError();
   }
   const FrontGeom& g = w.g;
+  if (g.nblk > kMaxDedupBlocks) return hipErrorInvalidValue;
   if (ev_tile && ev_tile[0]) (void)hipEventRecord(ev_tile[0], s);
   k_tile_dedup<kDedupThreads><<<static_cast<unsigned>(g.nblk), kDedupThreads, 0, s>>>(
       values, n, w, reinterpret_cast<int*>(t.scal + kTErr));
   if (ev_tile && ev_tile[1]) (void)hipEventRecord(ev_tile[1], s);
   if (ev_part && ev_part[0]) (void)hipEventRecord(ev_part[0], s);
-  const int64_t na = static_cast<int64_t>(g.P) * g.nblk;
-  const int64_t nchp = (na + kScanChunk - 1) / kScanChunk;
-  k_scan_parts<<<static_cast<unsigned>(nchp), 1024, 0, s>>>(w.pcnt, na, w.pcsum, nchp, w.scal);
-  k_part_scatter<<<dim3(static_cast<unsigned>((g.rcap + 4 * kBlock - 1) / (4 * kBlock)), static_cast<unsigned>(g.nblk)),
-                   kBlock, 0, s>>>(w);
   k_part_dedup<<<static_cast<unsigned>(g.P), kPartThreads, 0, s>>>(t, w, n);
   const int64_t nb = (n + kRankTile - 1) / kRankTile;
   k_first_sums<kBlock><<<static_cast<unsigned>(nb), kBlock, 0, s>>>(w, n);
@@ -675,7 +744,7 @@ __global__ __launch_bounds__(NT) void k_compact(TableDev t, Work w, const int64_
   load4(w.firstkey, i0, n, f);
   KeyInfo ki[4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) ki[k] = key_info(w, f[k], n);  // all four reads in flight together
+  for (int k = 0; k < 4; ++k) ki[k] = key_info(w, f[k]);  // all four reads in flight together
   int cf = 0, cc = 0, cn = 0, cl = 0, cu = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
@@ -810,7 +879,7 @@ __device__ inline void occ_pass(const Work& w, int64_t n, int64_t blk) {
   }
   KeyInfo a[4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) a[k] = key_info(w, rr[k].x, n);
+  for (int k = 0; k < 4; ++k) a[k] = key_info(w, rr[k].x);
   int pos[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {

@@ -27,14 +27,20 @@ constexpr int kDedupTile = kDedupThreads * kDedupItems;  // 4096
 constexpr int kDedupTileLog2 = 12;
 static_assert(kDedupTile == 1 << kDedupTileLog2, "tile is a power of two");
 // A dedup block takes at most kMaxTilesPerBlock consecutive tiles, so a
-// record index inside a block fits 19 bits (occ_word = index << 12 | rank).
+// record index inside a block fits 19 bits (occ_word = index << 12 | rank),
+// and there are at most kMaxDedupBlocks dedup blocks (n <= 2^28).
 constexpr int kMaxTilesPerBlock = 128;
-// Hash partitions of the records (a power of two); the per-partition dedup
-// handles one partition per block with kPartSlots LDS hash slots.
+constexpr int kMaxDedupBlocks = 512;
+// Hash partitions of the records (a power of two); one block per partition
+// dedups its records in an LDS table of kPartSlots slots.  A partition of at
+// most kPartThreads * kPartPer (= kPartSlots) records is processed with every
+// record of a thread in registers; a larger one in sweeps of at most
+// kPartSweep records (a key's records share a sweep).
 constexpr int kMaxParts = 4096;
-constexpr int kPartThreads = 512;
-constexpr int kPartSlots = 4096;
-constexpr int kPartSweep = 3072;  // records per LDS sweep (load <= 0.75)
+constexpr int kPartThreads = 256;
+constexpr int kPartSlots = 2048;
+constexpr int kPartPer = kPartSlots / kPartThreads;  // 8
+constexpr int kPartSweep = kPartSlots * 3 / 4;       // LDS load <= 0.75
 
 // Tile of the passes over positions (4 consecutive items per thread: many
 // resident waves for these latency-bound passes).
@@ -88,9 +94,7 @@ enum : int {
   kCNUnits = 6,    // backward units of those keys
   kCTrunc = 7,     // 1 if some keys not found had no room (latched as RS_EFULL)
   kCScanDone = 8,  // blocks of the tile-sum scan that have finished
-  kCPartDone = 9,  // blocks of the partition-count scan that have finished
-  kCRecords = 10,  // dedup records (tile-distinct keys)
-  kCScalars = 11
+  kCScalars = 9
 };
 
 __host__ __device__ inline uint64_t mix64(uint64_t z) {
@@ -139,23 +143,19 @@ struct FrontGeom {
   int logP;
 };
 
-// Record of one distinct key of a dedup tile.  meta = (rank of the record
-// among its block's records of the same partition) << 12 | (count - 1).
+// Record of one distinct key of a dedup tile.  Written in tile order with
+// meta = (rank of the record among its block's records of the same
+// partition) << 12 | (count - 1); the block then copies its records into
+// partition order with meta = (tile-order index) << 12 | (count - 1).
 struct alignas(16) TileRec {
   unsigned long long key;  // encoded key
   unsigned int tmin;       // first position of the key in the tile
   unsigned int meta;
 };
 
-// The same record moved into partition-major order.
-struct alignas(16) PartRec {
-  unsigned long long key;
-  unsigned int tmin;
-  unsigned int tcnt;  // occurrences of the key in the tile
-};
-
-// One distinct key of the call, indexed by its key index (a slot of the
-// partition-major record range of its partition).
+// One distinct key of the call, indexed by its key index: the position (in
+// the partition-ordered record copies) of the record that entered the key
+// into its partition's LDS table.
 struct alignas(32) KeyInfo {
   long long row;  // Blocks row (-1: not found / could not be inserted)
   int first;      // first position of the key in the batch
@@ -185,15 +185,14 @@ struct alignas(16) Unit {
 struct Work {
   uint32_t* occ_word;   // [n] dedup record index (in its block) << 12 | rank in the tile
   int32_t* firstkey;    // [n] key index at the key's first position, else -1
-  TileRec* trec;        // [nblk * rcap] records of the dedup tiles, per block
+  TileRec* trec;        // [nblk * rcap] records of the dedup tiles, per block, tile order
   int2* recres;         // [nblk * rcap] (same memory as trec) {key index, rank base} per record
-  int32_t* nrec;        // [nblk] records per dedup block
-  int32_t* pcnt;        // [P * nblk] records per (partition, block); scanned in place
-  int32_t* pcsum;       // [P * nblk / kScanChunk + 1] the same per chunk
-  PartRec* prec;        // [n] records in partition-major order
-  int32_t* psrc;        // [n] record index each partition-major record came from
-  int2* ptmp;           // [n] per partition-major record: LDS slot, rank base
-  KeyInfo* kinfo;       // [n] per key index
+  TileRec* srec;        // [nblk * rcap] the same records per block in partition order
+  int32_t* pcnt;        // [nblk * P] records per (block, partition)
+  int32_t* poff;        // [nblk * P] their offsets in the block's partition-ordered copy
+  int2* ptmp;           // [nblk * rcap] per partition-ordered record: (tile-order index << 12 | LDS slot), rank base
+  KeyInfo* kinfo;       // [nblk * rcap] per key index
+  int64_t nkeyidx;      // nblk * rcap (key indices are below it)
   int32_t* inverse;     // [n]
   int64_t* occ_row;     // [n] Blocks row of each occurrence (-1: none)
   int32_t* occ_pos;     // [n] position of each occurrence in the occurrence list
