@@ -69,7 +69,7 @@ __device__ inline void sum_positions(const Work& w, const GT* __restrict__ grad,
                                      int p0, int cnt, int lane, float (&acc)[E]) {
   constexpr int D = LANES * E;
   constexpr int NR = (kUnit + LANES - 1) / LANES;  // positions per lane
-  constexpr int kBatch = E == 4 ? 16 : 8;          // gradient rows in flight
+  constexpr int kBatch = 8;                        // gradient rows in flight (a small batch: more resident waves)
   int myref[NR];
   float mysc[NR];
 #pragma unroll
@@ -364,7 +364,9 @@ static hipError_t bwd_launch(const TableDev& t, const Work& w, const int64_t* of
   k_bwd_short<WT, GT, LANES, MODE, FUSED><<<grid_for(n, GPB, kResident), kBlock, 0, s>>>(t, w, offsets, g, gu, o);
   if (ev_s && ev_s[1]) (void)hipEventRecord(ev_s[1], s);
   if (ev_l && ev_l[0]) (void)hipEventRecord(ev_l[0], s);
-  k_bwd_long<GT, LANES, MODE><<<grid_for(2 * (n / kUnit) + 2, GPB, kResident), kBlock, 0, s>>>(w, offsets, g);
+  // one lane group per possible unit (the device-side count is at most
+  // 2n/kUnit + 2): no group takes a second unit while others are idle
+  k_bwd_long<GT, LANES, MODE><<<grid_for(2 * (n / kUnit) + 2, GPB), kBlock, 0, s>>>(w, offsets, g);
   k_bwd_long_finish<WT, E, LANES, FUSED><<<grid_for(n / kLong + 1, 1, 4 * kResident), kBlock, 0, s>>>(t, w, gu, o);
   if (ev_l && ev_l[1]) (void)hipEventRecord(ev_l[1], s);
   return hipGetLastError();

@@ -15,7 +15,6 @@
 
 namespace rs {
 
-constexpr int kBags = 4;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -45,7 +44,7 @@ __device__ inline void add_raw<uint16_t, 8>(float (&acc)[8], const uint4& v) {
 // positions), then every row of the chunk is requested before any is added,
 // so a group keeps C rows in flight whether the bags hold one id or hundreds
 // (C = 4 for batches of mostly single-id bags, 16 otherwise).
-template <typename WT, int LANES, int MODE, int C>
+template <typename WT, int LANES, int MODE, int C, int kBags>
 __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64_t* __restrict__ offsets, int64_t n,
                                                  int64_t bags, float* __restrict__ out) {
   constexpr int E = 16 / static_cast<int>(sizeof(WT));
@@ -222,16 +221,17 @@ static hipError_t pool_mode(const TableDev& t, const Work& w, const int64_t* off
     k_pool_none<WT, LANES><<<grid_for(bags * nch, 1, 1 << 20), kBlock, 0, s>>>(t, w, offsets, n, bags, pad_len,
                                                                              static_cast<WT*>(out), mask);
   } else {
-    // mostly single-id bags (n <= 2 bags): 4-row chunks cover a group's bags
+    // mostly single-id bags (n <= 2 bags): a lane group takes 8 bags and
+    // requests their rows together; longer bags: 4 bags, 16-row chunks
     const bool few = n <= 2 * bags;
-    const unsigned g = grid_for(bags, GPB * kBags, 1 << 20);
     float* o = static_cast<float*>(out);
+    const unsigned gf = grid_for(bags, GPB * 8, 1 << 20), gm = grid_for(bags, GPB * 4, 1 << 20);
     if (mode == 1) {
-      if (few) k_pool<WT, LANES, 1, 4><<<g, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
-      else k_pool<WT, LANES, 1, 16><<<g, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
+      if (few) k_pool<WT, LANES, 1, 8, 8><<<gf, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
+      else k_pool<WT, LANES, 1, 16, 4><<<gm, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
     } else {
-      if (few) k_pool<WT, LANES, 0, 4><<<g, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
-      else k_pool<WT, LANES, 0, 16><<<g, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
+      if (few) k_pool<WT, LANES, 0, 8, 8><<<gf, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
+      else k_pool<WT, LANES, 0, 16, 4><<<gm, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
     }
   }
   return hipGetLastError();
