@@ -238,6 +238,39 @@ def test_all_distinct_and_extreme_keys():
     _custom_batch_parity(w, vals, off)
 
 
+def _mix64(z):
+    """splitmix64 finaliser on uint64 numpy arrays (the dedup's partition hash)."""
+    with np.errstate(over="ignore"):
+        z = (z ^ (z >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
+        z = (z ^ (z >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
+        return z ^ (z >> np.uint64(31))
+
+
+def test_partition_sweeps_and_restart():
+    """Partitions with more records than the per-partition LDS table (2048
+    slots) are deduped in sweeps: random distinct keys (several partitions of
+    ~3000 records), and keys crafted so that every one falls in the first of
+    three sweeps, which overflows the table and restarts the partition with
+    more sweeps (white-box: the keys are picked with the partition hash)."""
+    _log("partition sweeps")
+    w = W.workload(0)
+    g = np.random.default_rng(11)
+    vals = np.unique(g.integers(-2**62, 2**62, size=12000, dtype=np.int64))
+    g.shuffle(vals)
+    vals = np.concatenate([vals, vals[:500]])      # some repeats across tiles
+    off = np.concatenate([np.arange(0, len(vals), 4), [len(vals)]]).astype(np.int64)
+    _custom_batch_parity(w, vals, off)
+    cand = np.unique(g.integers(-2**62, 2**62, size=40000, dtype=np.int64))
+    e = cand.view(np.uint64) ^ np.uint64(1 << 63)
+    h = _mix64(e ^ np.uint64(0x5BD1E9955BD1E995))
+    sel = cand[(h & np.uint64(0xFFFFF)) % np.uint64(3) == 0][:4000]
+    assert sel.size == 4000
+    g.shuffle(sel)
+    vals = np.concatenate([sel, sel[:96]])           # 4096 ids: one tile, one partition, 4000 records
+    off = np.concatenate([np.arange(0, len(vals), 3), [len(vals)]]).astype(np.int64)
+    _custom_batch_parity(w, vals, off, steps=2)
+
+
 def test_padded_bag_longer_than_pad_len():
     _log("padded truncation")
     w = W.workload(3, mini=True)
