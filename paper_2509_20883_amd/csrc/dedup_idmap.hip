@@ -291,15 +291,17 @@ __device__ inline int64_t resolve_probe(const TableDev& t, unsigned long long e,
 
 // The partition's records are read from every dedup block's
 // partition-ordered copy (segment b: cnt[b] records at off[b]).  A key's
-// index is the position of the record that entered it into the LDS table.
+// index is the position of its first record (the one holding its first
+// position), so the keys of a feature get indices in the feature's own
+// dedup blocks and the passes that follow read their key info close by.
 // A partition of at most kPartSlots records is done in one pass with each
 // thread's records in registers (its distinct keys always fit the table);
 // a larger one in sweeps of at most kPartSweep records by a hash of the key,
 // and if a sweep's keys do not fit (a skewed hash) the partition starts
 // again with twice as many sweeps.
 __device__ inline void probe_store_keys(const TableDev& t, const Work& w, int64_t n, int d, const short* cdense,
-                                        const unsigned long long* ckey, const unsigned int* cfirst,
-                                        const unsigned int* ccnt, const unsigned int* cpos) {
+                                        const unsigned long long* ckey, const unsigned long long* cfp,
+                                        const unsigned int* ccnt) {
   constexpr int NT = kPartThreads;
   constexpr int KP = 4;  // keys per thread per round: their probe batches in flight together
   for (int q0 = 0; q0 < d; q0 += KP * NT) {
@@ -319,31 +321,30 @@ __device__ inline void probe_store_keys(const TableDev& t, const Work& w, int64_
 #pragma unroll
     for (int u = 0; u < KP; ++u) {
       if (sl[u] < 0) continue;
-      const unsigned int kidx = cpos[sl[u]];
+      const unsigned long long fp = cfp[sl[u]];
+      const unsigned int kidx = static_cast<unsigned int>(fp);
+      const unsigned int first = static_cast<unsigned int>(fp >> 32);
       KeyInfo ki;
       ki.row = resolve_probe(t, e[u], h[u], pb[u]);
-      ki.first = static_cast<int>(cfirst[sl[u]]);
+      ki.first = static_cast<int>(first);
       ki.count = static_cast<int>(ccnt[sl[u]]);
       ki.uid = -1;
       ki.start = 0;
       ki.long_idx = -1;
       ki.pad = 0;
       w.kinfo[kidx] = ki;
-      if (cfirst[sl[u]] < static_cast<uint64_t>(n)) w.firstkey[cfirst[sl[u]]] = static_cast<int>(kidx);
+      if (first < static_cast<uint64_t>(n)) w.firstkey[first] = static_cast<int>(kidx);
     }
   }
 }
 
-// Enter key e into the LDS table (linear probing from slot h); the thread
-// that enters it records `pos` as the key index.  Returns the slot, or -1
-// if every slot holds another key.
-__device__ inline int lds_insert(unsigned long long* ckey, unsigned int* cpos, unsigned long long e, uint64_t hh,
-                                 int pos) {
+// Enter key e into the LDS table (linear probing from slot h).  Returns the
+// slot, or -1 if every slot holds another key.
+__device__ inline int lds_insert(unsigned long long* ckey, unsigned long long e, uint64_t hh) {
   constexpr int S = kPartSlots;
   unsigned int sl = static_cast<unsigned int>(hh >> 20) & (S - 1);
   for (int probes = 0; probes < S; ++probes) {
     const unsigned long long old = atomicCAS(&ckey[sl], kEncEmpty, e);
-    if (old == kEncEmpty) cpos[sl] = static_cast<unsigned int>(pos);
     if (old == kEncEmpty || old == e) return static_cast<int>(sl);
     sl = (sl + 1) & (S - 1);
   }
@@ -355,10 +356,11 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
   constexpr int kMaxSweeps = 1 << 10;
   constexpr int BPT = (kMaxDedupBlocks + NT - 1) / NT;
   __shared__ unsigned long long ckey[S];
-  __shared__ unsigned int cfirst[S];
+  // (first position << 32 | position of the record holding it): the minimum
+  // over the key's records gives the key's first position and its key index
+  __shared__ unsigned long long cfp[S];
   __shared__ unsigned int ccnt[S];
-  __shared__ unsigned int cpos[S];  // key index (position of the record that entered the key)
-  __shared__ short cdense[S];       // dense index -> slot
+  __shared__ short cdense[S];  // dense index -> slot
   __shared__ int cpre[kMaxDedupBlocks];   // exclusive prefix of the segment sizes
   __shared__ int cbase[kMaxDedupBlocks];  // position of each segment
   __shared__ int sh[NT / kWave + 1];
@@ -386,7 +388,7 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
   }
   for (int q = tid; q < S; q += NT) {
     ckey[q] = kEncEmpty;
-    cfirst[q] = 0xFFFFFFFFu;
+    cfp[q] = ~0ull;
     ccnt[q] = 0u;
   }
   __syncthreads();
@@ -432,22 +434,22 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
       sl[k] = -1;
       rb[k] = 0;
       if (pos[k] < 0) continue;
-      sl[k] = lds_insert(ckey, cpos, x[k].key, part_hash(x[k].key), pos[k]);  // nr <= S: always found
+      sl[k] = lds_insert(ckey, x[k].key, part_hash(x[k].key));  // nr <= S: always found
       if (sl[k] < 0) {
         pos[k] = -1;
         continue;
       }
-      atomicMin(&cfirst[sl[k]], x[k].tmin);
+      atomicMin(&cfp[sl[k]], (static_cast<unsigned long long>(x[k].tmin) << 32) | static_cast<unsigned int>(pos[k]));
       rb[k] = atomicAdd(&ccnt[sl[k]], (x[k].meta & 0xFFFu) + 1u);
     }
     __syncthreads();
     const int d = dense_list();
-    probe_store_keys(t, w, n, d, cdense, ckey, cfirst, ccnt, cpos);
+    probe_store_keys(t, w, n, d, cdense, ckey, cfp, ccnt);
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       if (pos[k] < 0) continue;
       const int64_t src = (static_cast<int64_t>(pos[k]) / g.rcap) * g.rcap + (x[k].meta >> 12);
-      w.recres[src] = make_int2(static_cast<int>(cpos[sl[k]]), static_cast<int>(rb[k]));
+      w.recres[src] = make_int2(static_cast<int>(static_cast<unsigned int>(cfp[sl[k]])), static_cast<int>(rb[k]));
     }
     return;
   }
@@ -460,7 +462,7 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
     if (!fresh) {
       for (int q = tid; q < S; q += NT) {
         ckey[q] = kEncEmpty;
-        cfirst[q] = 0xFFFFFFFFu;
+        cfp[q] = ~0ull;
         ccnt[q] = 0u;
       }
     }
@@ -472,12 +474,12 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
       const TileRec x = w.srec[pos];
       const uint64_t h = part_hash(x.key);
       if (static_cast<int>((h & 0xFFFFFull) % static_cast<uint64_t>(nsw)) != s) continue;
-      const int sl = lds_insert(ckey, cpos, x.key, h, pos);
+      const int sl = lds_insert(ckey, x.key, h);
       if (sl < 0) {
         ovf = 1;
         continue;
       }
-      atomicMin(&cfirst[sl], x.tmin);
+      atomicMin(&cfp[sl], (static_cast<unsigned long long>(x.tmin) << 32) | static_cast<unsigned int>(pos));
       const unsigned int rb = atomicAdd(&ccnt[sl], (x.meta & 0xFFFu) + 1u);
       w.ptmp[pos] = make_int2(static_cast<int>(((x.meta >> 12) << 12) | static_cast<unsigned int>(sl)),
                               static_cast<int>(rb));
@@ -494,14 +496,14 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
       continue;
     }
     const int d = dense_list();
-    probe_store_keys(t, w, n, d, cdense, ckey, cfirst, ccnt, cpos);
+    probe_store_keys(t, w, n, d, cdense, ckey, cfp, ccnt);
     for (int fr = tid; fr < nr; fr += NT) {
       const int pos = rec_pos(fr);
       const uint64_t h = part_hash(w.srec[pos].key);
       if (static_cast<int>((h & 0xFFFFFull) % static_cast<uint64_t>(nsw)) != s) continue;
       const int2 tp = w.ptmp[pos];
       const int64_t src = (static_cast<int64_t>(pos) / g.rcap) * g.rcap + (static_cast<uint32_t>(tp.x) >> 12);
-      w.recres[src] = make_int2(static_cast<int>(cpos[tp.x & 0xFFF]), tp.y);
+      w.recres[src] = make_int2(static_cast<int>(static_cast<unsigned int>(cfp[tp.x & 0xFFF])), tp.y);
     }
     ++s;
     __syncthreads();  // the next sweep clears the LDS

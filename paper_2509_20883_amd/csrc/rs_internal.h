@@ -154,8 +154,7 @@ struct alignas(16) TileRec {
 };
 
 // One distinct key of the call, indexed by its key index: the position (in
-// the partition-ordered record copies) of the record that entered the key
-// into its partition's LDS table.
+// the partition-ordered record copies) of the key's first record.
 struct alignas(32) KeyInfo {
   long long row;  // Blocks row (-1: not found / could not be inserted)
   int first;      // first position of the key in the batch

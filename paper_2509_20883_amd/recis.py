@@ -309,8 +309,8 @@ class Table:
 
     def set_kernel_events(self, kernel: str, start, stop):
         """Record torch.cuda.Event `start` / `stop` around every launch of `kernel`."""
-        if start is not None:
-            # torch creates the underlying hipEvent_t on first record()
+        if start is not None and (not start.cuda_event or not stop.cuda_event):
+            # torch creates the underlying hipEvent_t on its first record()
             start.record()
             stop.record()
         s = None if start is None else C.c_void_p(start.cuda_event)

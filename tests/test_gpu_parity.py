@@ -356,8 +356,9 @@ def test_pipelined_prepare_matches_serial():
         assert torch.equal(ctx_a[s].unique(U), ctx_b[s].unique(U))
         assert torch.equal(ctx_a[s].inverse(), ctx_b[s].inverse())
         assert torch.equal(ctx_a[s].rows(U), ctx_b[s].rows(U))
-        # hot-key partial sums use fp32 atomics (order varies): later steps may
-        # differ by an ulp of the updated rows
+        # a key's occurrences are listed in an order that varies between runs
+        # (ranks come from LDS arrival order), and so does the fp32 summation
+        # order of its gradient: later steps may differ by an ulp of the rows
         torch.testing.assert_close(outs_b[s], outs_a[s], rtol=1e-4, atol=2e-6)
     ka, ra = ga.export()
     kb, rb = gb.export()
