@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(HERE, "liboracle.so")
 OK, EINVAL, ENOMEM, EFULL, EKEY = 0, 1, 2, 3, 4
 SUM, MEAN, NONE = 0, 1, 2
 F32, BF16 = 0, 1
-ADAGRAD, ADAM = 0, 1
+ADAGRAD, ADAM, ADAMW, ADAM_TF = 0, 1, 2, 3
 
 _lib = None
 
@@ -63,10 +63,10 @@ def lib():
         L.or_backward.restype = i32
         L.or_backward.argtypes = [p, i64, p, i64, i32, i32, i64, p, p]
         L.or_optimizer.restype = i32
-        L.or_optimizer.argtypes = [p, p, i64, p, C.c_double, C.c_double, C.c_double, C.c_double]
+        L.or_optimizer.argtypes = [p, p, i64, p, C.c_double, C.c_double, C.c_double, C.c_double, C.c_double]
         L.or_step.restype = i32
         L.or_step.argtypes = [p, p, p, i64, i64, i32, i64, p, C.c_double, C.c_double, C.c_double,
-                              C.c_double, p, p, p, p]
+                              C.c_double, C.c_double, p, p, p, p]
         _lib = L
     return _lib
 
@@ -135,7 +135,7 @@ class Table:
 
     @property
     def nstate(self):
-        return 2 if self.opt == ADAM else 1
+        return 1 if self.opt == ADAGRAD else 2
 
     def size(self) -> int:
         return int(lib().or_size(self.h))
@@ -196,12 +196,13 @@ class Table:
         return dict(status=st, out=out, mask=mask, unique=uniq[:u].copy(), inverse=inv[:n].copy(),
                     rows=rows[:u].copy(), U=u, n_new=int(nn[0]))
 
-    def optimizer(self, rows, grad, lr, eps=1e-8, beta1=0.9, beta2=0.999):
+    def optimizer(self, rows, grad, lr, eps=1e-8, beta1=0.9, beta2=0.999, weight_decay=0.0):
         r = _c(rows, np.int64)
         g = _c(grad, np.float32)
-        return lib().or_optimizer(self.h, _p(r), r.size, _p(g), lr, eps, beta1, beta2)
+        return lib().or_optimizer(self.h, _p(r), r.size, _p(g), lr, eps, beta1, beta2, weight_decay)
 
-    def step(self, values, offsets, mode, grad, lr, eps=1e-8, beta1=0.9, beta2=0.999, pad_len=0):
+    def step(self, values, offsets, mode, grad, lr, eps=1e-8, beta1=0.9, beta2=0.999, pad_len=0,
+             weight_decay=0.0):
         v = _c(values, np.int64)
         off = _c(offsets, np.int64)
         g = _c(grad, np.float32)
@@ -214,6 +215,6 @@ class Table:
             mask = None
         U = np.zeros(1, dtype=np.int64)
         nn = np.zeros(1, dtype=np.int64)
-        st = lib().or_step(self.h, _p(v), _p(off), n, bags, mode, pad_len, _p(g), lr, eps, beta1, beta2,
+        st = lib().or_step(self.h, _p(v), _p(off), n, bags, mode, pad_len, _p(g), lr, eps, beta1, beta2, weight_decay,
                            _p(out), _p(mask), _p(U), _p(nn))
         return dict(status=st, out=out, mask=mask, U=int(U[0]), n_new=int(nn[0]))

@@ -16,8 +16,12 @@
 //   forward        per bag: sum / mean of its rows, or a padded copy
 //   backward       per unique key: sum of the upstream gradients of every
 //                  occurrence (scaled by 1/len for mean)
-//   optimizer      Adagrad (Duchi et al. 2011) or Adam (Kingma & Ba 2015,
-//                  Algorithm 1) on the touched rows only
+//   optimizer      Adagrad (Duchi et al. 2011), Adam (Kingma & Ba 2015,
+//                  Algorithm 1), AdamW (Adam with decoupled weight decay,
+//                  Loshchilov & Hutter 2019; the paper names SparseAdamW) or
+//                  Adam in the reordered form with epsilon-hat (Kingma & Ba
+//                  2015, end of section 2; TensorFlow's Adam) on the touched
+//                  rows only
 //
 // Sums and optimizer arithmetic are carried in fp64; stored rows and state
 // are fp32 (or bf16 rows, rounded to nearest even) because the storage type
@@ -39,7 +43,7 @@ namespace {
 constexpr int ST_OK = 0, ST_EINVAL = 1, ST_EFULL = 3, ST_EKEY = 4;
 constexpr int SUM = 0, MEAN = 1, NONE = 2;
 constexpr int F32 = 0, BF16 = 1;
-constexpr int ADAGRAD = 0, ADAM = 1;
+constexpr int ADAGRAD = 0, ADAM = 1, ADAMW = 2, ADAM_TF = 3;
 constexpr int64_t KEY_EMPTY = std::numeric_limits<int64_t>::min();   // reserved
 constexpr int64_t KEY_TOMB = std::numeric_limits<int64_t>::min() + 1; // reserved
 
@@ -93,7 +97,7 @@ struct Table {
   int64_t t = 0;                               // Adam step count (table-global)
 
   int64_t live() const { return static_cast<int64_t>(idmap.size()); }
-  int nstate() const { return opt == ADAM ? 2 : 1; }
+  int nstate() const { return opt == ADAGRAD ? 1 : 2; }
 
   float get_w(int64_t r, int j) const {
     return row_dtype == BF16 ? bf16_to_f32(wb[r * dim + j]) : w[r * dim + j];
@@ -109,7 +113,7 @@ struct Table {
       if (row_dtype == BF16) wb.push_back(bf16_rne(vals[j]));
       else w.push_back(vals[j]);
       s1.push_back(0.0f);
-      if (opt == ADAM) s2.push_back(0.0f);
+      if (opt != ADAGRAD) s2.push_back(0.0f);
     }
     return r;
   }
@@ -178,7 +182,7 @@ void or_init_row(uint64_t seed, int64_t key, int dim, float lo, float hi, float*
 }
 
 void* or_create(int dim, int row_dtype, int opt, float lo, float hi, uint64_t seed, int64_t max_live) {
-  if (dim <= 0 || (row_dtype != F32 && row_dtype != BF16) || (opt != ADAGRAD && opt != ADAM)) return nullptr;
+  if (dim <= 0 || (row_dtype != F32 && row_dtype != BF16) || opt < ADAGRAD || opt > ADAM_TF) return nullptr;
   Table* T = new Table;
   T->dim = dim;
   T->row_dtype = row_dtype;
@@ -342,19 +346,24 @@ int or_backward(const int64_t* offsets, int64_t bags, const int32_t* inverse, in
 //   Adam:    t += 1 once per call (table-global step);
 //            m = b1 m + (1-b1) g;  v = b2 v + (1-b2) g^2;
 //            w -= lr * (m / (1-b1^t)) / (sqrt(v / (1-b2^t)) + eps)
+//   AdamW:   the Adam step applied to w - lr * wd * w (decoupled decay of
+//            the touched row, then the moment update and step)
+//   Adam (epsilon-hat form): the same moments; lr_t = lr * sqrt(1-b2^t) / (1-b1^t);
+//            w -= lr_t * m / (sqrt(v) + eps)
 // Arithmetic in fp64 from the stored fp32 state; results stored as fp32
 // state and fp32 (or bf16, via fp32 then round-to-nearest-even) rows.
 // rows[u] < 0 is skipped.  grad is fp32 [U, dim].
 int or_optimizer(void* h, const int64_t* rows, int64_t U, const float* grad, double lr, double eps,
-                 double beta1, double beta2) {
+                 double beta1, double beta2, double weight_decay) {
   Table* T = static_cast<Table*>(h);
   const int D = T->dim;
   double bc1 = 1.0, bc2 = 1.0;
-  if (T->opt == ADAM) {
+  if (T->opt != ADAGRAD) {
     T->t += 1;
     bc1 = 1.0 - std::pow(beta1, static_cast<double>(T->t));
     bc2 = 1.0 - std::pow(beta2, static_cast<double>(T->t));
   }
+  const double lr_t = lr * std::sqrt(bc2) / bc1;
   for (int64_t u = 0; u < U; ++u) {
     const int64_t r = rows[u];
     if (r < 0) continue;
@@ -368,7 +377,12 @@ int or_optimizer(void* h, const int64_t* rows, int64_t U, const float* grad, dou
       } else {
         const double m = beta1 * static_cast<double>(T->s1[r * D + j]) + (1.0 - beta1) * g;
         const double v = beta2 * static_cast<double>(T->s2[r * D + j]) + (1.0 - beta2) * g * g;
-        w -= lr * (m / bc1) / (std::sqrt(v / bc2) + eps);
+        if (T->opt == ADAM_TF) {
+          w -= lr_t * m / (std::sqrt(v) + eps);
+        } else {
+          if (T->opt == ADAMW) w -= lr * weight_decay * w;
+          w -= lr * (m / bc1) / (std::sqrt(v / bc2) + eps);
+        }
         T->s1[r * D + j] = static_cast<float>(m);
         T->s2[r * D + j] = static_cast<float>(v);
       }
@@ -382,7 +396,7 @@ int or_optimizer(void* h, const int64_t* rows, int64_t U, const float* grad, dou
 // fp32 (the method's grad_unique dtype), then the optimizer.
 int or_step(void* h, const int64_t* values, const int64_t* offsets, int64_t n, int64_t bags, int mode,
             int64_t pad_len, const float* grad, double lr, double eps, double beta1, double beta2,
-            double* out, uint8_t* mask, int64_t* U_out, int64_t* n_new_out) {
+            double weight_decay, double* out, uint8_t* mask, int64_t* U_out, int64_t* n_new_out) {
   Table* T = static_cast<Table*>(h);
   std::vector<int64_t> uniq(static_cast<size_t>(n > 0 ? n : 1)), rows(static_cast<size_t>(n > 0 ? n : 1));
   std::vector<int32_t> inv(static_cast<size_t>(n > 0 ? n : 1));
@@ -395,7 +409,7 @@ int or_step(void* h, const int64_t* values, const int64_t* offsets, int64_t n, i
   or_backward(offsets, bags, inv.data(), U, D, mode, pad_len, grad, gu.data());
   std::vector<float> g32(gu.size());
   for (size_t k = 0; k < gu.size(); ++k) g32[k] = static_cast<float>(gu[k]);
-  or_optimizer(h, rows.data(), U, g32.data(), lr, eps, beta1, beta2);
+  or_optimizer(h, rows.data(), U, g32.data(), lr, eps, beta1, beta2, weight_decay);
   return st;
 }
 

@@ -411,6 +411,77 @@ def test_adam_matches_torch_sparse_adam_multi_step_lazy():
     np.testing.assert_allclose(W, p.detach().numpy(), rtol=1e-5, atol=1e-9)
 
 
+def test_adamw_matches_torch_adamw_multi_step():
+    """AdamW (decoupled weight decay, the paper's SparseAdamW) against
+    torch.optim.AdamW in fp64: every row is touched every step (then the lazy
+    update equals the dense one); a partially touched step leaves the other
+    rows, and their state, untouched (no decay either)."""
+    D, V = 4, 6
+    g = np.random.default_rng(33)
+    T = O.Table(D, opt=O.ADAMW, seed=9)
+    keys = np.arange(V, dtype=np.int64) + 2000
+    _, rows, _ = T.find_or_insert(keys)
+    _, W0, _ = T.read_rows(keys)
+    p = torch.nn.Parameter(torch.from_numpy(W0.astype(np.float64)))
+    lr, wd = 0.1, 0.1  # steps of ~lr: decay before vs after the step differ by ~1e-3
+    opt = torch.optim.AdamW([p], lr=lr, betas=(0.9, 0.999), eps=1e-8, weight_decay=wd)
+    for step in range(5):
+        G = g.standard_normal((V, D)).astype(np.float32)
+        T.optimizer(rows, G, lr, 1e-8, 0.9, 0.999, weight_decay=wd)
+        p.grad = torch.from_numpy(G.astype(np.float64))
+        opt.step()
+    _, W, _ = T.read_rows(keys)
+    np.testing.assert_allclose(W, p.detach().numpy(), rtol=1e-5, atol=1e-9)
+    # lazy: untouched rows keep their value (no decay) and state
+    _, before, sb = T.read_rows(keys)
+    T.optimizer(rows[:2], g.standard_normal((2, D)).astype(np.float32), lr, 1e-8, 0.9, 0.999, weight_decay=wd)
+    _, after, sa = T.read_rows(keys)
+    assert np.array_equal(before[2:], after[2:]) and np.array_equal(sb[2:], sa[2:])
+    assert not np.array_equal(before[:2], after[:2])
+
+
+def test_adam_eps_hat_form_identity_and_first_step():
+    """Adam in the reordered form (lr_t = lr sqrt(1-b2^t) / (1-b1^t),
+    w -= lr_t m / (sqrt(v) + eps_hat)) is Algorithm 1 with eps = eps_hat /
+    sqrt(1-b2^t) (same moments); its first step from zero moments is
+    w - lr sqrt(1-b2) g / (sqrt(1-b2) |g| + eps_hat)."""
+    D, V = 8, 5
+    g = np.random.default_rng(34)
+    keys = np.arange(V, dtype=np.int64) + 3000
+    lr, b1, b2, eps_hat = 2e-3, 0.9, 0.999, 1e-3
+    # first step, closed form
+    T = O.Table(D, opt=O.ADAM_TF, seed=10)
+    _, rows, _ = T.find_or_insert(keys)
+    _, W0, _ = T.read_rows(keys)
+    G = g.standard_normal((V, D)).astype(np.float32)
+    T.optimizer(rows, G, lr, eps_hat, b1, b2)
+    _, W1, S1 = T.read_rows(keys)
+    Gd = G.astype(np.float64)
+    ref = W0.astype(np.float64) - lr * np.sqrt(1 - b2) * Gd / (np.sqrt(1 - b2) * np.abs(Gd) + eps_hat)
+    np.testing.assert_allclose(W1, ref, rtol=2e-7, atol=1e-12)
+    np.testing.assert_allclose(S1[:, 0], (1 - b1) * Gd, rtol=1e-6)
+    np.testing.assert_allclose(S1[:, 1], (1 - b2) * Gd * Gd, rtol=1e-6)
+    # a later step from a random state: equal to Algorithm 1 with eps = eps_hat / sqrt(1 - b2^t)
+    t = 7
+    m = (0.1 * g.standard_normal((V, D))).astype(np.float32)
+    v = (0.01 * np.abs(g.standard_normal((V, D)))).astype(np.float32)
+    A = O.Table(D, opt=O.ADAM_TF, seed=10)
+    B = O.Table(D, opt=O.ADAM, seed=10)
+    for X in (A, B):
+        X.find_or_insert(keys)
+        X.write_rows(keys, W0, np.stack([m, v], axis=1))
+        X.t = t - 1
+    G = g.standard_normal((V, D)).astype(np.float32)
+    A.optimizer(rows, G, lr, eps_hat, b1, b2)
+    B.optimizer(rows, G, lr, eps_hat / np.sqrt(1 - b2 ** t), b1, b2)
+    _, WA, SA = A.read_rows(keys)
+    _, WB, SB = B.read_rows(keys)
+    assert np.array_equal(SA, SB)
+    ulp = np.spacing(np.abs(WB).astype(np.float32)).astype(np.float64)
+    assert (np.abs(WA.astype(np.float64) - WB) <= ulp).all()
+    assert not np.array_equal(WA, W0)
+
+
 def test_step_is_forward_backward_optimizer():
     g = np.random.default_rng(41)
     vals, off = _tiny_batch(g, 40, 6, 25)
