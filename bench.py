@@ -44,6 +44,8 @@ def parse():
     ap.add_argument("--pipelined", action="store_true",
                     help="run the next batch's lookup_prepare on a second stream while the current batch pools and "
                          "runs its backward (default: one stream)")
+    ap.add_argument("--optimizer", choices=["adagrad", "adam", "adamw", "adam-eps-hat"], default=None,
+                    help="run the workload with another row-sparse optimizer (adamw: weight decay 0.01)")
     ap.add_argument("--gen-workers", type=int, default=16,
                     help="processes drawing the input batches before the GPU is touched (1: in-process, e.g. under "
                          "a profiler)")
@@ -84,7 +86,7 @@ def kernel_source_hash(kernel: str) -> str:
 
 def row_bytes(w):
     R = w.dim * (2 if w.row_dtype == 1 else 4)
-    S = w.dim * 4 * (2 if w.opt == 1 else 1)
+    S = w.dim * 4 * (1 if w.opt == 0 else 2)
     return R, S
 
 
@@ -211,7 +213,8 @@ def cpu_baseline(w, target_s):
                 ot.find_or_insert(uk[np.isin(uk, pool_keys, assume_unique=True)])
             present.update(uk.tolist())
         t0 = time.perf_counter()
-        ot.step(b.values, b.offsets, w.mode, grad, w.lr, w.eps, w.beta1, w.beta2, pad_len=w.pad_len)
+        ot.step(b.values, b.offsets, w.mode, grad, w.lr, w.eps, w.beta1, w.beta2, pad_len=w.pad_len,
+                weight_decay=w.weight_decay)
         secs += time.perf_counter() - t0
         ids += b.n
         steps += 1
@@ -231,6 +234,10 @@ def main():
     from paper_2509_20883_amd import workloads as W
 
     w = W.workload(a.workload)
+    if a.optimizer:
+        w.opt = ["adagrad", "adam", "adamw", "adam-eps-hat"].index(a.optimizer)
+        if w.opt == 2:
+            w.weight_decay = 0.01
     nsteps = a.warmup + a.steps
     t_setup = time.time()
     hb = host_batches(a.workload, nsteps, a.gen_workers)  # before the GPU is initialised (forked workers)
@@ -314,9 +321,9 @@ def main():
         table.forward(v, o, w.mode, pad_len=w.pad_len, ctx=c, out=ob, mask=mb)
         if a.unfused:
             table.backward(c, grad_of(i), gu)
-            table.optimizer_step(c, gu, w.lr, w.eps, w.beta1, w.beta2)
+            table.optimizer_step(c, gu, w.lr, w.eps, w.beta1, w.beta2, w.weight_decay)
         else:
-            table.backward_optimizer(c, grad_of(i), w.lr, w.eps, w.beta1, w.beta2)
+            table.backward_optimizer(c, grad_of(i), w.lr, w.eps, w.beta1, w.beta2, w.weight_decay)
         if ring < nsteps:
             stepscal[i].copy_(c.scalars())
 
@@ -395,9 +402,9 @@ def main():
             table.pool(ctxs[i], out=ob, mask=mb)
             if a.unfused:
                 table.backward(ctxs[i], grad_of(i), gu)
-                table.optimizer_step(ctxs[i], gu, w.lr, w.eps, w.beta1, w.beta2)
+                table.optimizer_step(ctxs[i], gu, w.lr, w.eps, w.beta1, w.beta2, w.weight_decay)
             else:
-                table.backward_optimizer(ctxs[i], grad_of(i), w.lr, w.eps, w.beta1, w.beta2)
+                table.backward_optimizer(ctxs[i], grad_of(i), w.lr, w.eps, w.beta1, w.beta2, w.weight_decay)
     else:
         for j in range(a.steps):
             set_events(j)

@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define RS_VERSION 1
+#define RS_VERSION 2
 
 typedef enum {
   RS_OK = 0,
@@ -56,7 +56,17 @@ typedef enum {
 
 typedef enum { RS_POOL_SUM = 0, RS_POOL_MEAN = 1, RS_POOL_NONE = 2 } rs_pool;
 typedef enum { RS_F32 = 0, RS_BF16 = 1 } rs_dtype;
-typedef enum { RS_ADAGRAD = 0, RS_ADAM = 1 } rs_optim;
+/* Row-sparse optimizers (every one keeps fp32 state beside the row: Adagrad
+ * one accumulator per element, the Adam family two moments per element).
+ *  RS_ADAGRAD: Duchi et al. 2011.
+ *  RS_ADAM:    Kingma & Ba 2015, Algorithm 1 (the paper's SparseAdam).
+ *  RS_ADAMW:   Adam with decoupled weight decay (Loshchilov & Hutter 2019;
+ *              the paper's SparseAdamW): the touched row first decays by
+ *              lr * weight_decay * w, then takes the Adam step.
+ *  RS_ADAM_TF: Adam in the reordered form with epsilon-hat (Kingma & Ba
+ *              2015, end of section 2; the form TensorFlow implements, which
+ *              the paper's TF-compatible optimizers follow). */
+typedef enum { RS_ADAGRAD = 0, RS_ADAM = 1, RS_ADAMW = 2, RS_ADAM_TF = 3 } rs_optim;
 
 typedef struct rs_table rs_table; /* opaque, library-owned */
 typedef void* rs_stream;          /* hipStream_t */
@@ -91,12 +101,15 @@ typedef struct {
   int32_t reserved0;
 } rs_table_desc;
 
-/* Optimizer hyper-parameters.  Adagrad uses lr, eps; Adam uses all four.
- * Given in double: the kernels take fp32 constants that the library derives
- * in double (lr, eps, beta, 1 - beta, bias corrections), so 1 - beta2 does
- * not inherit the fp32 rounding error of beta2. */
+/* Optimizer hyper-parameters.  Adagrad uses lr, eps; the Adam family lr,
+ * eps (epsilon-hat for RS_ADAM_TF), beta1, beta2; RS_ADAMW also
+ * weight_decay.  Given in double: the kernels take fp32 constants that the
+ * library derives in double (lr, eps, beta, 1 - beta, bias corrections,
+ * lr * weight_decay), so 1 - beta2 does not inherit the fp32 rounding error
+ * of beta2. */
 typedef struct {
   double lr, eps, beta1, beta2;
+  double weight_decay;
 } rs_opt_params;
 
 /* Forward context: the caller provides the workspace; lookup_pool_fwd fills
@@ -239,6 +252,9 @@ rs_status lookup_pool_bwd(rs_table* t, const rs_ctx* ctx, const void* grad_out, 
  *   Adagrad: acc += g*g;  w -= lr * g / (sqrt(acc) + eps)
  *   Adam:    t += 1 (once per call, table-global);  m = b1*m + (1-b1)*g;
  *            v = b2*v + (1-b2)*g*g;  w -= lr * (m/(1-b1^t)) / (sqrt(v/(1-b2^t)) + eps)
+ *   AdamW:   w -= lr * weight_decay * w, then the Adam step
+ *   Adam (epsilon-hat): the same moments;  w -= lr_t * m / (sqrt(v) + eps)
+ *            with lr_t = lr * sqrt(1-b2^t) / (1-b1^t)
  * Arithmetic in fp32; bf16 rows are widened, updated, and rounded to nearest
  * even.  grad_unique [n, D] fp32 as written by lookup_pool_bwd. */
 rs_status sparse_opt_step(rs_table* t, const rs_ctx* ctx, const float* grad_unique,

@@ -193,7 +193,7 @@ struct rs_table {
     if (custom) a.free(p, a.ctx);
     else (void)hipFree(p);
   }
-  int nstate() const { return d.optimizer == RS_ADAM ? 2 : 1; }
+  int nstate() const { return d.optimizer == RS_ADAGRAD ? 1 : 2; }
   int wbytes() const { return d.row_dtype == RS_BF16 ? 2 : 4; }
 
   TableDev dev() const {
@@ -377,10 +377,15 @@ OptArgs make_opt(rs_table* t, const rs_opt_params* p) {
   o.omb2 = static_cast<float>(1.0 - p->beta2);
   o.bc1 = 1.0f;
   o.bc2 = 1.0f;
-  if (o.opt == RS_ADAM) {
+  o.wdlr = static_cast<float>(p->lr * p->weight_decay);
+  o.lrt = static_cast<float>(p->lr);
+  if (o.opt != RS_ADAGRAD) {
     t->adam_t += 1;
-    o.bc1 = static_cast<float>(1.0 - std::pow(p->beta1, static_cast<double>(t->adam_t)));
-    o.bc2 = static_cast<float>(1.0 - std::pow(p->beta2, static_cast<double>(t->adam_t)));
+    const double bc1 = 1.0 - std::pow(p->beta1, static_cast<double>(t->adam_t));
+    const double bc2 = 1.0 - std::pow(p->beta2, static_cast<double>(t->adam_t));
+    o.bc1 = static_cast<float>(bc1);
+    o.bc2 = static_cast<float>(bc2);
+    o.lrt = static_cast<float>(p->lr * std::sqrt(bc2) / bc1);
   }
   return o;
 }
@@ -408,7 +413,7 @@ rs_status ht_create(const rs_table_desc* d, const rs_allocator* a, rs_stream str
   *out = nullptr;
   if (!valid_dim(d->dim)) return fail(RS_EINVAL, "dim must be 8, 16, 32, 64, 128 or 256");
   if (d->row_dtype != RS_F32 && d->row_dtype != RS_BF16) return fail(RS_EINVAL, "bad row_dtype");
-  if (d->optimizer != RS_ADAGRAD && d->optimizer != RS_ADAM) return fail(RS_EINVAL, "bad optimizer");
+  if (d->optimizer < RS_ADAGRAD || d->optimizer > RS_ADAM_TF) return fail(RS_EINVAL, "bad optimizer");
   if (!is_pow2(d->capacity_slots) || d->capacity_slots < 16 || d->capacity_slots > (int64_t(1) << 40))
     return fail(RS_EINVAL, "capacity_slots must be a power of two in [16, 2^40]");
   if (!(d->max_load > 0.0f && d->max_load <= 0.9f)) return fail(RS_EINVAL, "max_load must be in (0, 0.9]");

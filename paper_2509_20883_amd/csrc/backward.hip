@@ -37,6 +37,8 @@ struct RowFrag {
   }
   // Adagrad: acc += g^2; w -= lr g / (sqrt(acc) + eps).
   // Adam:    m = b1 m + (1-b1) g; v = b2 v + (1-b2) g^2; w -= lr (m/bc1) / (sqrt(v/bc2) + eps).
+  // AdamW:   w -= (lr wd) w, then the Adam step.
+  // Adam, epsilon-hat form: the same moments; w -= lr_t m / (sqrt(v) + eps).
   __device__ inline void update_store(uint8_t* row, int lane, int dim, const float (&g)[E], const OptArgs& o) {
     float* p = reinterpret_cast<float*>(row + static_cast<int64_t>(dim) * sizeof(WT)) + lane * E;
     if (o.opt == 0) {
@@ -51,7 +53,12 @@ struct RowFrag {
       for (int k = 0; k < E; ++k) {
         s1[k] = o.beta1 * s1[k] + o.omb1 * g[k];
         s2[k] = o.beta2 * s2[k] + o.omb2 * g[k] * g[k];
-        w[k] = w[k] - o.lr * (s1[k] / o.bc1) / (__builtin_sqrtf(s2[k] / o.bc2) + o.eps);
+        if (o.opt == 3) {
+          w[k] = w[k] - o.lrt * s1[k] / (__builtin_sqrtf(s2[k]) + o.eps);
+        } else {
+          if (o.opt == 2) w[k] = w[k] - o.wdlr * w[k];
+          w[k] = w[k] - o.lr * (s1[k] / o.bc1) / (__builtin_sqrtf(s2[k] / o.bc2) + o.eps);
+        }
       }
       store_vals<float, E>(p, s1);
       store_vals<float, E>(p + dim, s2);
@@ -401,7 +408,7 @@ hipError_t launch_bwd(const TableDev& t, const Work& w, const int64_t* offsets, 
                       float* grad_unique, const OptArgs* opt, hipEvent_t* ev_short, hipEvent_t* ev_long,
                       hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  const OptArgs o = opt ? *opt : OptArgs{0, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 1.f, 1.f};
+  const OptArgs o = opt ? *opt : OptArgs{0, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 1.f, 1.f, 0.f, 0.f};
   if (opt)
     return t.row_dtype ? bwd_mode<uint16_t, true>(t, w, offsets, n, mode, grad, grad_unique, o, ev_short, ev_long, s)
                        : bwd_mode<float, true>(t, w, offsets, n, mode, grad, grad_unique, o, ev_short, ev_long, s);

@@ -213,8 +213,10 @@ struct Work {
 };
 
 struct OptArgs {
-  int opt;  // 0 adagrad, 1 adam
+  int opt;  // 0 adagrad, 1 adam, 2 adamw, 3 adam (epsilon-hat form)
   float lr, eps, beta1, beta2, omb1, omb2, bc1, bc2;  // omb = 1 - beta, all derived in double
+  float wdlr;  // lr * weight_decay (adamw)
+  float lrt;   // lr * sqrt(1 - beta2^t) / (1 - beta1^t) (epsilon-hat form)
 };
 
 // ---------------------------------------------------------------------------

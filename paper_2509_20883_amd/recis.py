@@ -23,7 +23,7 @@ OK, EINVAL, ENOMEM, EFULL, EKEY, EHIP = 0, 1, 2, 3, 4, 5
 STATUS_NAMES = {0: "RS_OK", 1: "RS_EINVAL", 2: "RS_ENOMEM", 3: "RS_EFULL", 4: "RS_EKEY", 5: "RS_EHIP"}
 SUM, MEAN, NONE = 0, 1, 2
 F32, BF16 = 0, 1
-ADAGRAD, ADAM = 0, 1
+ADAGRAD, ADAM, ADAMW, ADAM_TF = 0, 1, 2, 3
 # kernel ids of rs_set_kernel_events ("occ" and "init_rows" bracket the same
 # launch; "bwd_long" brackets the hot-key unit sums and their finish)
 KERNELS = {"tile_dedup": 0, "partition": 1, "compact_insert": 2, "init_rows": 3, "pool": 4,
@@ -44,7 +44,8 @@ class TableDesc(C.Structure):
 
 
 class OptParams(C.Structure):
-    _fields_ = [("lr", C.c_double), ("eps", C.c_double), ("beta1", C.c_double), ("beta2", C.c_double)]
+    _fields_ = [("lr", C.c_double), ("eps", C.c_double), ("beta1", C.c_double), ("beta2", C.c_double),
+                ("weight_decay", C.c_double)]
 
 
 class RsCtx(C.Structure):
@@ -163,7 +164,7 @@ class Table:
         _check(lib().ht_create(C.byref(d), None, _stream(), C.byref(h)))
         self.h = h
         self.dim, self.row_dtype, self.optimizer = dim, row_dtype, optimizer
-        self.nstate = 2 if optimizer == ADAM else 1
+        self.nstate = 1 if optimizer == ADAGRAD else 2
         self.device = torch.device("cuda", torch.cuda.current_device())
 
     def close(self):
@@ -297,14 +298,14 @@ class Table:
         return grad_unique
 
     def optimizer_step(self, ctx: Ctx, grad_unique: torch.Tensor, lr: float, eps: float = 1e-8,
-                       beta1: float = 0.9, beta2: float = 0.999):
-        p = OptParams(lr, eps, beta1, beta2)
+                       beta1: float = 0.9, beta2: float = 0.999, weight_decay: float = 0.0):
+        p = OptParams(lr, eps, beta1, beta2, weight_decay)
         _check(lib().sparse_opt_step(self.h, C.byref(ctx.c), _ptr(grad_unique), C.byref(p), _stream()))
 
     def backward_optimizer(self, ctx: Ctx, grad_out: torch.Tensor, lr: float, eps: float = 1e-8,
-                           beta1: float = 0.9, beta2: float = 0.999):
+                           beta1: float = 0.9, beta2: float = 0.999, weight_decay: float = 0.0):
         g = self._grad(ctx, grad_out)
-        p = OptParams(lr, eps, beta1, beta2)
+        p = OptParams(lr, eps, beta1, beta2, weight_decay)
         _check(lib().lookup_pool_bwd_opt(self.h, C.byref(ctx.c), _ptr(g), C.byref(p), _stream()))
 
     def set_kernel_events(self, kernel: str, start, stop):

@@ -143,7 +143,7 @@ def zipf_ranks(n: int, V: int, s: float, g: np.random.Generator) -> np.ndarray:
 
 SUM, MEAN, NONE = 0, 1, 2
 F32, BF16 = 0, 1
-ADAGRAD, ADAM = 0, 1
+ADAGRAD, ADAM, ADAMW, ADAM_TF = 0, 1, 2, 3
 
 
 @dataclasses.dataclass
@@ -172,6 +172,7 @@ class Workload:
     eps: float = 1e-8
     beta1: float = 0.9
     beta2: float = 0.999
+    weight_decay: float = 0.0
     prepop: str = "none"  # "none", "frac90", "all", "pool"
     grad_dtype: int = F32
     steps: int = 1
@@ -414,6 +415,6 @@ def prepop_count(w: Workload) -> int:
 def describe(w: Workload) -> dict:
     return {"workload": w.name, "batch": w.batch, "features": w.n_features, "dim": w.dim,
             "row_dtype": "bf16" if w.row_dtype == BF16 else "f32",
-            "optimizer": "adam" if w.opt == ADAM else "adagrad",
+            "optimizer": ["adagrad", "adam", "adamw", "adam-eps-hat"][w.opt],
             "pooling": ["sum", "mean", "none"][w.mode], "zipf_s": w.zipf_s,
             "vocab_total": int(sum(w.vocab)) if w.vocab else int(w.pool0), "mini": w.mini}

@@ -73,7 +73,7 @@ def bf16_ulp(x: np.ndarray) -> np.ndarray:
     return 2.0 ** (e - 7)
 
 
-def opt_bounds(opt, row_dtype, w0, s0, g, dg, lr, eps, b1, b2, t, w_ref):
+def opt_bounds(opt, row_dtype, w0, s0, g, dg, lr, eps, b1, b2, t, w_ref, wd=0.0):
     """Error bounds of an fp32 optimizer step against the fp64 oracle.
 
     Each fp32 operation is allowed 1e-6 of the magnitude of its terms (about
@@ -99,11 +99,21 @@ def opt_bounds(opt, row_dtype, w0, s0, g, dg, lr, eps, b1, b2, t, w_ref):
         v1 = b2 * s0[:, 1] + (1 - b2) * g * g
         b_m = 1e-6 * (b1 * np.abs(s0[:, 0]) + (1 - b1) * ag) + (1 - b1) * dg + 1e-37
         b_v = 1e-6 * (b2 * s0[:, 1] + (1 - b2) * g * g) + (1 - b2) * (2 * ag * dg + dg * dg) + 1e-37
-        mh, vh = np.abs(m1) / bc1, v1 / bc2
-        sq = np.sqrt(vh)
-        dsq = np.minimum((b_v / bc2) / np.maximum(2 * sq, 1e-30), np.sqrt(b_v / bc2))
-        upd = lr * mh / (sq + eps)
-        d_upd = lr * ((b_m / bc1) / (sq + eps) + mh * dsq / (sq + eps) ** 2) + 1e-6 * upd
+        if opt == O.ADAM_TF:
+            # w -= lr_t m / (sqrt(v) + eps), lr_t = lr sqrt(bc2) / bc1
+            lrt = lr * np.sqrt(bc2) / bc1
+            sq = np.sqrt(v1)
+            dsq = np.minimum(b_v / np.maximum(2 * sq, 1e-30), np.sqrt(b_v))
+            upd = lrt * np.abs(m1) / (sq + eps)
+            d_upd = lrt * (b_m / (sq + eps) + np.abs(m1) * dsq / (sq + eps) ** 2) + 1e-6 * upd
+        else:
+            mh, vh = np.abs(m1) / bc1, v1 / bc2
+            sq = np.sqrt(vh)
+            dsq = np.minimum((b_v / bc2) / np.maximum(2 * sq, 1e-30), np.sqrt(b_v / bc2))
+            upd = lr * mh / (sq + eps)
+            d_upd = lr * ((b_m / bc1) / (sq + eps) + mh * dsq / (sq + eps) ** 2) + 1e-6 * upd
+            if opt == O.ADAMW:  # w -= (lr wd) w first: one more rounded product
+                d_upd = d_upd + 1e-6 * lr * wd * np.abs(w0)
         b_state = np.stack([b_m, b_v], axis=1)
     if row_dtype == O.BF16:
         b_w = np.maximum(1e-2 * np.abs(w_ref) + 1e-6, 1.01 * bf16_ulp(w_ref)) + d_upd
@@ -169,13 +179,14 @@ def run_step_parity(w: W.Workload, gt: R.Table, ot: O.Table, batch: W.Batch, gra
     gu_abs = O.backward(off, ref["inverse"], U, w.dim, w.mode, pad, np.abs(gfin))
     assert_sum_close(gu_gpu, gu_ref, gu_abs, what=f"step {step} grad_unique")
     # optimizer, stage-wise: oracle starts from the GPU's pre-state and grads
-    gt.optimizer_step(ctx, gu, w.lr, w.eps, w.beta1, w.beta2)
+    gt.optimizer_step(ctx, gu, w.lr, w.eps, w.beta1, w.beta2, w.weight_decay)
     w1, s1 = gt.read_rows(ctx.rows(U))
     w1, s1 = w1.cpu().numpy(), s1.cpu().numpy()
     ot.write_rows(ref["unique"], w0, s0)
-    ot.optimizer(ref["rows"], gu_gpu, w.lr, w.eps, w.beta1, w.beta2)
+    ot.optimizer(ref["rows"], gu_gpu, w.lr, w.eps, w.beta1, w.beta2, weight_decay=w.weight_decay)
     _, w1_ref, s1_ref = ot.read_rows(ref["unique"])
-    bounds = opt_bounds(w.opt, w.row_dtype, w0, s0, gu_gpu, 0.0, w.lr, w.eps, w.beta1, w.beta2, ot.t, w1_ref)
+    bounds = opt_bounds(w.opt, w.row_dtype, w0, s0, gu_gpu, 0.0, w.lr, w.eps, w.beta1, w.beta2, ot.t, w1_ref,
+                        w.weight_decay)
     assert_opt_close(w1, s1, w1_ref, s1_ref, bounds, what=f"step {step} optimizer")
     # the next step starts both sides from the GPU's updated rows (stage-wise
     # parity: fp32 vs fp64 optimizer rounding is not carried into later steps)

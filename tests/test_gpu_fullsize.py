@@ -143,7 +143,7 @@ def _check_update(w, b, grad, uniq, inv, sel, w0, s0, w1, s1):
     _, w0_ref, s0_ref = ot.read_rows(uniq[sel])
     assert np.array_equal(w0, w0_ref) and np.array_equal(s0, s0_ref), "rows before the update differ"
     g32 = gu.astype(np.float32)
-    ot.optimizer(rows_o, g32, w.lr, w.eps, w.beta1, w.beta2)
+    ot.optimizer(rows_o, g32, w.lr, w.eps, w.beta1, w.beta2, weight_decay=w.weight_decay)
     _, w1_ref, s1_ref = ot.read_rows(uniq[sel])
     dg = 1e-5 * gabs + np.abs(gu) * 2.0 ** -23
     bounds = opt_bounds(w.opt, w.row_dtype, w0, s0, g32, dg, w.lr, w.eps, w.beta1, w.beta2, ot.t, w1_ref)

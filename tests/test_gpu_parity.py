@@ -162,8 +162,8 @@ def _fused_vs_unfused(w, b, grad):
     U = int(ca.scalars()[0].item())
     w0, s0 = [x.cpu().numpy() for x in ga.read_rows(ca.rows(U))]
     gu = ga.backward(ca, gdev)
-    ga.optimizer_step(ca, gu, w.lr, w.eps, w.beta1, w.beta2)
-    gb.backward_optimizer(cb, gdev, w.lr, w.eps, w.beta1, w.beta2)
+    ga.optimizer_step(ca, gu, w.lr, w.eps, w.beta1, w.beta2, w.weight_decay)
+    gb.backward_optimizer(cb, gdev, w.lr, w.eps, w.beta1, w.beta2, w.weight_decay)
     wa, sa = [x.cpu().numpy() for x in ga.read_rows(ca.rows(U))]
     wb, sb = [x.cpu().numpy() for x in gb.read_rows(cb.rows(U))]
     ga.check()
@@ -174,7 +174,7 @@ def _fused_vs_unfused(w, b, grad):
     gfin = np.where(np.isfinite(grad), grad, 0).astype(np.float32)
     gabs = O.backward(b.offsets, inv, U, w.dim, w.mode, pad, np.abs(gfin))
     bounds = P.opt_bounds(w.opt, w.row_dtype, w0, s0, gu[:U].cpu().numpy(), 2e-5 * gabs, w.lr, w.eps,
-                          w.beta1, w.beta2, 1, wa)
+                          w.beta1, w.beta2, 1, wa, w.weight_decay)
     ga.close()
     gb.close()
     return wa, sa, wb, sb, bounds
@@ -187,6 +187,37 @@ def test_fused_bwd_opt_equals_two_calls(k):
     b = W.make_batch(w, 0)
     grad = W.make_grad(w, b, 0)
     wa, sa, wb, sb, bounds = _fused_vs_unfused(w, b, grad)
+    P.assert_opt_close(wb, sb, wa, sa, bounds, what="fused vs unfused")
+
+
+def _variant(opt, row_dtype):
+    """The single-hot workload (reduced) with another optimizer / row dtype."""
+    w = W.workload(1, mini=True)
+    w.opt, w.row_dtype = opt, row_dtype
+    if opt == O.ADAMW:
+        w.lr, w.weight_decay = 1e-2, 0.05
+    if opt == O.ADAM_TF:
+        w.lr, w.eps = 1e-2, 1e-7
+    return w
+
+
+@pytest.mark.parametrize("opt,row_dtype", [(O.ADAMW, O.F32), (O.ADAMW, O.BF16), (O.ADAM_TF, O.F32),
+                                           (O.ADAM_TF, O.BF16)])
+def test_optimizer_variants_step_parity(opt, row_dtype):
+    """AdamW (decoupled weight decay) and Adam in the epsilon-hat form: step
+    parity over three steps (stage-wise, two-call path), then the fused
+    backward + optimizer against the two calls."""
+    w = _variant(opt, row_dtype)
+    _log("optimizer variant", opt, row_dtype)
+    gt, ot = P.gpu_table(w), P.oracle_table(w)
+    P.prepopulate(w, gt, ot)
+    for step in range(3):
+        b = W.make_batch(w, step)
+        P.run_step_parity(w, gt, ot, b, W.make_grad(w, b, step), step)
+    gt.check()
+    gt.close()
+    b = W.make_batch(w, 0)
+    wa, sa, wb, sb, bounds = _fused_vs_unfused(w, b, W.make_grad(w, b, 0))
     P.assert_opt_close(wb, sb, wa, sa, bounds, what="fused vs unfused")
 
 
