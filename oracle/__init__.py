@@ -50,6 +50,8 @@ def lib():
         L.or_set_step_count.argtypes = [p, i64]
         L.or_dedup.restype = i64
         L.or_dedup.argtypes = [p, i64, p, p]
+        L.or_ids_partition.restype = i64
+        L.or_ids_partition.argtypes = [p, i64, i32, u64, p, p, p, p]
         L.or_find_or_insert.restype = i32
         L.or_find_or_insert.argtypes = [p, p, i64, p, p]
         L.or_read_rows.restype = i64
@@ -107,6 +109,23 @@ def dedup(values: np.ndarray):
     if U < 0:
         return -U, None, None
     return OK, u[:U].copy(), inv[:n].copy()
+
+
+def ids_partition(values: np.ndarray, nshards: int, owner_seed: int = 0):
+    """Dedup + split by owner shard: (keys int64[U], shard_offsets int64[G+1],
+    inverse int32[N], n_rejected).  Shard s holds keys[offsets[s]:offsets[s+1]],
+    in first-occurrence order; owner(k) = mix64(k ^ owner_seed) mod G."""
+    v = _c(values, np.int64)
+    n = v.size
+    keys = np.empty(max(n, 1), dtype=np.int64)
+    offs = np.empty(max(nshards, 0) + 1, dtype=np.int64)
+    inv = np.empty(max(n, 1), dtype=np.int32)
+    rej = np.zeros(1, dtype=np.int64)
+    U = lib().or_ids_partition(_p(v), n, int(nshards), owner_seed & 0xFFFFFFFFFFFFFFFF, _p(keys), _p(offs),
+                               _p(inv), _p(rej))
+    if U < 0:
+        raise ValueError("ids_partition: invalid arguments")
+    return keys[:U].copy(), offs.copy(), inv[:n].copy(), int(rej[0])
 
 
 def backward(offsets, inverse, U, dim, mode, pad_len, grad):

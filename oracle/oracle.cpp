@@ -16,6 +16,7 @@
 //   forward        per bag: sum / mean of its rows, or a padded copy
 //   backward       per unique key: sum of the upstream gradients of every
 //                  occurrence (scaled by 1/len for mean)
+//   ids partition  dedup + split of the distinct keys by owner shard
 //   optimizer      Adagrad (Duchi et al. 2011), Adam (Kingma & Ba 2015,
 //                  Algorithm 1), AdamW (Adam with decoupled weight decay,
 //                  Loshchilov & Hutter 2019; the paper names SparseAdamW) or
@@ -204,6 +205,55 @@ int64_t or_dedup(const int64_t* values, int64_t n, int64_t* unique_out, int32_t*
   for (int64_t i = 0; i < n; ++i)
     if (reserved(values[i])) return -ST_EKEY;
   return dedup(values, n, unique_out, inverse_out);
+}
+
+// Ids partition ("Ids Partition" in Benchmark of Operators; "Request Merging
+// & Sharding" in Load Balancing): the batch's ids are deduplicated and split
+// by the shard that owns them, so that each shard can be sent its own ids.
+// Reading taken (the paper names no owner function): the owner of key k among
+// G shards is mix64(uint64(k) XOR owner_seed) mod G; the output lists the
+// distinct keys shard by shard (shard 0 first), each shard's keys in the
+// order of their first occurrence in the batch.  shard_offsets[s] is where
+// shard s starts (shard_offsets[G] = U); inverse_out[i] is the output
+// position of values[i].  A reserved key (INT64_MIN, INT64_MIN+1) takes no
+// part: its inverse is -1 and *n_rejected counts it.
+// Returns U, or -ST_EINVAL for G < 1.
+int64_t or_ids_partition(const int64_t* values, int64_t n, int32_t nshards, uint64_t owner_seed, int64_t* keys_out,
+                         int64_t* shard_offsets, int32_t* inverse_out, int64_t* n_rejected) {
+  if (nshards < 1 || n < 0) return -ST_EINVAL;
+  // 1. distinct keys in first-occurrence order
+  std::unordered_map<int64_t, int64_t> first_index;  // key -> index in `order`
+  std::vector<int64_t> order;
+  int64_t rejected = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    if (reserved(values[i])) {
+      ++rejected;
+      continue;
+    }
+    if (first_index.find(values[i]) == first_index.end()) {
+      first_index.emplace(values[i], static_cast<int64_t>(order.size()));
+      order.push_back(values[i]);
+    }
+  }
+  // 2. shard by shard, that shard's keys in first-occurrence order
+  std::unordered_map<int64_t, int64_t> out_pos;
+  int64_t U = 0;
+  for (int32_t s = 0; s < nshards; ++s) {
+    shard_offsets[s] = U;
+    for (int64_t k : order) {
+      const uint64_t owner = mix64(static_cast<uint64_t>(k) ^ owner_seed) % static_cast<uint64_t>(nshards);
+      if (owner != static_cast<uint64_t>(s)) continue;
+      keys_out[U] = k;
+      out_pos.emplace(k, U);
+      ++U;
+    }
+  }
+  shard_offsets[nshards] = U;
+  // 3. each id's position in the output
+  for (int64_t i = 0; i < n; ++i)
+    inverse_out[i] = reserved(values[i]) ? -1 : static_cast<int32_t>(out_pos.at(values[i]));
+  if (n_rejected) *n_rejected = rejected;
+  return U;
 }
 
 int or_find_or_insert(void* h, const int64_t* keys, int64_t n, int64_t* rows_out, int64_t* n_inserted) {

@@ -199,6 +199,114 @@ def test_dedup_rejects_reserved_keys():
     assert st == O.OK and len(u) == 3
 
 
+# --------------------------------------------------------------------------- ids partition
+
+
+def _s64(x):
+    x &= M64
+    return x - (1 << 64) if x >= 1 << 63 else x
+
+
+def _partition_brute(seq, G, seed):
+    """Distinct keys sorted by (owner, first position): a sort, not the
+    oracle's shard-by-shard scan; owners from the pinned mix64."""
+    first = {}
+    for i, k in enumerate(seq.tolist()):
+        first.setdefault(k, i)
+    own = {k: O.mix64((k & M64) ^ seed) % G for k in first}
+    keys = sorted(first, key=lambda k: (own[k], first[k]))
+    offs = [0] * (G + 1)
+    for k in keys:
+        offs[own[k] + 1] += 1
+    offs = np.cumsum(offs)
+    pos = {k: j for j, k in enumerate(keys)}
+    return np.array(keys, dtype=np.int64), offs, np.array([pos[k] for k in seq.tolist()], dtype=np.int32)
+
+
+def test_ids_partition_owner_pinned_to_published_vectors():
+    # keys whose owner hash input is a splitmix64 state with a published
+    # output: owner = that output mod G (G = 3 and 4 catch a mask for a mod
+    # and a dropped seed)
+    seed, vals = _vectors()
+    oseed = 0xA5A5F00DCAFE1234
+    states = [(seed + (j + 1) * GAMMA) & M64 for j in range(len(vals))]
+    ks = [_s64(z ^ oseed) for z in states]
+    order = [2, 0, 2, 4, 1, 3, 0, 1, 4, 4]
+    seq = np.array([ks[j] for j in order], dtype=np.int64)
+    for G in (3, 4):
+        keys, offs, inv, rej = O.ids_partition(seq, G, oseed)
+        own = {ks[j]: vals[j] % G for j in range(len(vals))}
+        firstpos = {}
+        for i, j in enumerate(order):
+            firstpos.setdefault(ks[j], i)
+        want = sorted(firstpos, key=lambda k: (own[k], firstpos[k]))
+        assert keys.tolist() == want and rej == 0
+        for s_ in range(G):
+            seg = keys[offs[s_]:offs[s_ + 1]].tolist()
+            assert all(own[k] == s_ for k in seg)
+        assert offs[0] == 0 and offs[G] == len(want)
+        assert np.array_equal(keys[inv], seq)
+
+
+def test_ids_partition_brute_force_small():
+    g = np.random.default_rng(21)
+    for trial in range(60):
+        n = int(g.integers(0, 40))
+        alphabet = g.integers(-2**63 + 2, 2**63 - 1, size=int(g.integers(1, 12)), dtype=np.int64)
+        seq = alphabet[g.integers(0, len(alphabet), size=n)] if n else np.zeros(0, dtype=np.int64)
+        G = int(g.choice([1, 2, 3, 5, 8, 16]))
+        seed = int(g.integers(0, 2**63)) * 2 + trial % 2
+        keys, offs, inv, rej = O.ids_partition(seq, G, seed)
+        ek, eo, ei = _partition_brute(seq, G, seed)
+        assert np.array_equal(keys, ek) and np.array_equal(offs, eo) and np.array_equal(inv, ei) and rej == 0
+
+
+def test_ids_partition_one_shard_is_dedup():
+    g = np.random.default_rng(5)
+    seq = g.zipf(1.2, size=20000).astype(np.int64) * 7919 - 3
+    keys, offs, inv, _ = O.ids_partition(seq, 1, 123)
+    st, u, uinv = O.dedup(seq)
+    assert st == O.OK
+    assert np.array_equal(keys, u) and np.array_equal(inv, uinv)
+    assert offs.tolist() == [0, len(u)]
+
+
+def test_ids_partition_invariants_large():
+    g = np.random.default_rng(8)
+    seq = (g.zipf(1.1, size=60000).astype(np.int64) * 1_000_003) ^ 0x5555
+    G = 8
+    keys, offs, inv, rej = O.ids_partition(seq, G, 99)
+    assert rej == 0
+    assert np.array_equal(keys[inv], seq)                          # reconstruction
+    assert len(np.unique(keys)) == len(keys)                       # distinct
+    assert np.array_equal(np.sort(keys), np.unique(seq))           # same set
+    assert offs[0] == 0 and offs[-1] == len(keys) and np.all(np.diff(offs) >= 0)
+    first = np.full(len(keys), len(seq))
+    np.minimum.at(first, inv, np.arange(len(seq)))
+    for s_ in range(G):
+        lo, hi = offs[s_], offs[s_ + 1]
+        assert all(O.mix64((int(k) & M64) ^ 99) % G == s_ for k in keys[lo:hi][:200])
+        assert np.all(np.diff(first[lo:hi]) > 0)                   # first-occurrence order in a shard
+    # a good owner hash spreads the distinct keys evenly (chi-square, 7 dof)
+    cnt = np.diff(offs)
+    exp = len(keys) / G
+    assert ((cnt - exp) ** 2 / exp).sum() < 30
+
+
+def test_ids_partition_reserved_keys_and_empty():
+    lo = np.iinfo(np.int64).min
+    seq = np.array([4, lo, 9, lo + 1, 4, lo], dtype=np.int64)
+    keys, offs, inv, rej = O.ids_partition(seq, 2, 0)
+    assert rej == 3
+    assert sorted(keys.tolist()) == [4, 9]
+    assert inv[1] == -1 and inv[3] == -1 and inv[5] == -1
+    assert keys[inv[0]] == 4 and keys[inv[2]] == 9 and inv[4] == inv[0]
+    keys, offs, inv, rej = O.ids_partition(np.zeros(0, dtype=np.int64), 5, 1)
+    assert len(keys) == 0 and offs.tolist() == [0] * 6 and len(inv) == 0 and rej == 0
+    with pytest.raises(ValueError):
+        O.ids_partition(seq, 0, 0)
+
+
 # --------------------------------------------------------------------------- find-or-insert
 
 
