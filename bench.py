@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--gen-workers", type=int, default=16,
                     help="processes drawing the input batches before the GPU is touched (1: in-process, e.g. under "
                          "a profiler)")
+    ap.add_argument("--op", choices=["step", "ids-partition"], default="step",
+                    help="ids-partition: time the fused dedup + owner split alone on its one-million-id input")
+    ap.add_argument("--shards", type=int, default=None, help="owner shards of --op ids-partition (default 8)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (scales HBM byte counters)")
     return ap.parse_args()
@@ -223,6 +226,87 @@ def cpu_baseline(w, target_s):
                       f"{int(ids)} ids), {secs:.1f} s of single-threaded step time"}
 
 
+IDS_METRIC = "ids partition (dedup + split by owner shard) IDs/sec and achieved HBM GB/s vs peak, 1 MI355X"
+
+
+def ids_partition_bytes(n: int, U: int, G: int) -> int:
+    """Algorithmic bytes of one ids partition: ids read once; distinct keys,
+    shard offsets, the inverse and the two info words written once."""
+    return 8 * n + 8 * U + 8 * (G + 1) + 4 * n + 16
+
+
+def bench_ids_partition(a):
+    from paper_2509_20883_amd import workloads as W
+
+    G = a.shards or W.IDS_PARTITION_SHARDS
+    seed = W.IDS_PARTITION_SEED
+    nring = 4
+    host = [W.ids_partition_values(step=s) for s in range(nring)]
+    import torch
+
+    from paper_2509_20883_amd import recis as R
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    vals = [torch.from_numpy(v).to(dev) for v in host]
+    n = int(max(v.numel() for v in vals))
+    part = R.IdsPartition()
+    keys = torch.empty(n, dtype=torch.int64, device=dev)
+    offs = torch.empty(G + 1, dtype=torch.int64, device=dev)
+    inv = torch.empty(n, dtype=torch.int32, device=dev)
+    infos = torch.zeros(a.warmup + a.steps, 2, dtype=torch.int64, device=dev)
+    for i in range(a.warmup):
+        part(vals[i % nring], G, seed, keys, offs, inv, infos[i])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for j in range(a.steps):
+        i = a.warmup + j
+        part(vals[i % nring], G, seed, keys, offs, inv, infos[i])
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / a.steps
+    info = infos.cpu().numpy()
+    if np.any(info[:, 1] != 0):
+        raise RuntimeError(f"ids_partition reported error bits {info[:, 1].tolist()}")
+    Us = [int(info[a.warmup + j, 0]) for j in range(a.steps)]
+    ns = [int(vals[(a.warmup + j) % nring].numel()) for j in range(a.steps)]
+    byts = float(np.mean([ids_partition_bytes(nn, U, G) for nn, U in zip(ns, Us)]))
+    achieved = byts / (ms * 1e-3) / 1e9
+    res = {
+        "metric": IDS_METRIC,
+        "value": float(np.mean(ns)) / (ms * 1e-3),
+        "unit": "IDs/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic (26 single-hot Zipf(1.05) features, 4 batches resident in HBM, used in turn)",
+        "config": {"workload": "ids-partition-1M", "ids": int(np.mean(ns)), "shards": G, "U_mean": float(np.mean(Us))},
+        "roofline": {"bound": "hbm", "kernel": "ids_partition (whole call)", "achieved": achieved,
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "kernel_ms": ms, "kernel_bytes_alg": byts},
+    }
+    if not a.no_cpu_baseline:
+        import oracle as O
+
+        t0 = time.perf_counter()
+        calls = 0
+        while calls == 0 or time.perf_counter() - t0 < a.cpu_seconds:
+            O.ids_partition(host[calls % nring], G, seed)
+            calls += 1
+        dt = time.perf_counter() - t0
+        cpu = {"value": calls * float(np.mean([h.size for h in host])) / dt, "unit": "IDs/s", "cores": 1,
+               "kind": "oracle", "sample": f"{calls} whole calls on the same inputs"}
+        cpu["gpu_speedup"] = res["value"] / cpu["value"]
+        res["cpu_baseline"] = cpu
+    print(json.dumps(res), flush=True)
+
+
 def main():
     a = parse()
     if a.copy_calibration:
@@ -231,6 +315,9 @@ def main():
     if a.gpus != 1:
         print(json.dumps({"error": "single-GPU build: run with --gpus 1 (the multi-GPU path is a design only)"}))
         sys.exit(2)
+    if a.op == "ids-partition":
+        bench_ids_partition(a)
+        return
     from paper_2509_20883_amd import workloads as W
 
     w = W.workload(a.workload)

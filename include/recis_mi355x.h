@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define RS_VERSION 2
+#define RS_VERSION 3
 
 typedef enum {
   RS_OK = 0,
@@ -265,6 +265,34 @@ rs_status sparse_opt_step(rs_table* t, const rs_ctx* ctx, const float* grad_uniq
  * out.  Same results as the two calls (up to fp32 summation order). */
 rs_status lookup_pool_bwd_opt(rs_table* t, const rs_ctx* ctx, const void* grad_out,
                               const rs_opt_params* p, rs_stream stream);
+
+/* Ids partition ("Ids Partition" among the benchmarked operators; "Request
+ * Merging & Sharding" under Load Balancing): the batch's ids deduplicated and
+ * split by the shard that owns them, in one call, before the exchange of
+ * each shard's ids.  No table is involved.
+ *   owner(k) = mix64((uint64_t)k ^ owner_seed) mod nshards, with mix64 the
+ *   splitmix64 output function (Steele, Lea & Flood 2014).
+ * Outputs (device, caller-owned):
+ *   keys_out [n] int64: the U distinct keys, shard 0's first, each shard's
+ *                keys in the order of their first occurrence in values;
+ *                entries past U are unspecified
+ *   shard_offsets [nshards+1] int64: shard s holds
+ *                keys_out[shard_offsets[s] .. shard_offsets[s+1]);
+ *                shard_offsets[nshards] = U
+ *   inverse [n] int32: keys_out[inverse[i]] == values[i]; -1 for a reserved
+ *                key (INT64_MIN, INT64_MIN+1), which takes no part
+ *   info [2] int64: {U, error bits}: bit 0 (1) a reserved key was skipped;
+ *                bit 3 (8) an internal dedup pass overflowed (outputs
+ *                invalid; not expected for any input)
+ * values [n] int64, n <= 2^28; 1 <= nshards <= 1024.  workspace: device,
+ * 256-byte aligned, >= ids_partition_workspace_bytes(n, nshards) bytes,
+ * reusable by the next call once this one has completed in stream order.
+ * Enqueues on `stream` and returns without waiting.  Errors: RS_EINVAL
+ * (sizes, null pointers, workspace), RS_EHIP. */
+size_t ids_partition_workspace_bytes(int64_t n, int32_t nshards);
+rs_status ids_partition(const int64_t* values, int64_t n, int32_t nshards, uint64_t owner_seed, int64_t* keys_out,
+                        int64_t* shard_offsets, int32_t* inverse, int64_t* info, void* workspace,
+                        size_t workspace_bytes, rs_stream stream);
 
 /* Kernel timing hook: from now on, hipEvent_t `start` / `stop` are recorded on
  * the call's stream immediately before / after every launch of the named

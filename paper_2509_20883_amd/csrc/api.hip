@@ -127,6 +127,62 @@ Work make_work(void* base, const Layout& L) {
   return w;
 }
 
+// Workspace layout of one ids partition: the dedup passes' arrays (no
+// IDMap), the owner counts and their scan, scalars.
+struct PartLayout {
+  size_t occ_word, firstkey, trec, srec, pcnt, poff, ptmp, kinfo, hist, csum, cscal, pscal, total;
+  FrontGeom g;
+  OwnerGeom og;
+};
+
+PartLayout make_part_layout(int64_t n, int G) {
+  const size_t n1 = static_cast<size_t>(n > 0 ? n : 1);
+  PartLayout L{};
+  L.g = front_geom(n);
+  L.og = owner_geom(n, G);
+  const size_t nrecs = static_cast<size_t>(L.g.nblk) * static_cast<size_t>(L.g.rcap);
+  const size_t npc = static_cast<size_t>(L.g.P) * static_cast<size_t>(L.g.nblk);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align_up(bytes);
+    return o;
+  };
+  L.occ_word = take(4 * n1);
+  L.firstkey = take(4 * n1);
+  L.trec = take(sizeof(TileRec) * nrecs);
+  L.srec = take(sizeof(TileRec) * nrecs);
+  L.pcnt = take(4 * npc);
+  L.poff = take(4 * npc);
+  L.ptmp = take(8 * nrecs);
+  L.kinfo = take(sizeof(KeyInfo) * nrecs);
+  L.hist = take(4 * static_cast<size_t>(L.og.len));
+  L.csum = take(4 * static_cast<size_t>(L.og.nch));
+  L.cscal = take(8 * kCScalars);
+  L.pscal = take(8 * kPScalars);
+  L.total = off;
+  return L;
+}
+
+Work make_part_work(void* base, const PartLayout& L, int32_t* inverse) {
+  uint8_t* b = static_cast<uint8_t*>(base);
+  Work w{};
+  w.occ_word = reinterpret_cast<uint32_t*>(b + L.occ_word);
+  w.firstkey = reinterpret_cast<int32_t*>(b + L.firstkey);
+  w.trec = reinterpret_cast<TileRec*>(b + L.trec);
+  w.recres = reinterpret_cast<int2*>(b + L.trec);
+  w.srec = reinterpret_cast<TileRec*>(b + L.srec);
+  w.pcnt = reinterpret_cast<int32_t*>(b + L.pcnt);
+  w.poff = reinterpret_cast<int32_t*>(b + L.poff);
+  w.ptmp = reinterpret_cast<int2*>(b + L.ptmp);
+  w.kinfo = reinterpret_cast<KeyInfo*>(b + L.kinfo);
+  w.nkeyidx = L.g.nblk * L.g.rcap;
+  w.inverse = inverse;
+  w.scal = reinterpret_cast<int64_t*>(b + L.cscal);
+  w.g = L.g;
+  return w;
+}
+
 const char* err_text(int bits) {
   if (bits & kErrKey) return "a reserved key (INT64_MIN or INT64_MIN+1) was in the input";
   if (bits & kErrFull) return "the table is full (auto_grow is off): some keys were not inserted";
@@ -509,6 +565,29 @@ rs_status ht_destroy(rs_table* t) {
 size_t lookup_workspace_bytes(int64_t n, int64_t /*bags*/, int64_t /*pad_len*/, const rs_table* t) {
   if (!t || n < 0) return 0;
   return make_layout(n, t->d.dim).total;
+}
+
+size_t ids_partition_workspace_bytes(int64_t n, int32_t nshards) {
+  if (n < 0 || n > (int64_t(1) << 28) || nshards < 1 || nshards > kMaxShards) return 0;
+  return make_part_layout(n, nshards).total;
+}
+
+rs_status ids_partition(const int64_t* values, int64_t n, int32_t nshards, uint64_t owner_seed, int64_t* keys_out,
+                        int64_t* shard_offsets, int32_t* inverse, int64_t* info, void* workspace,
+                        size_t workspace_bytes, rs_stream stream) {
+  if (n < 0 || n > (int64_t(1) << 28)) return fail(RS_EINVAL, "n must be in [0, 2^28]");
+  if (nshards < 1 || nshards > kMaxShards) return fail(RS_EINVAL, "nshards must be in [1, 1024]");
+  if (!shard_offsets || !info) return fail(RS_EINVAL, "null shard_offsets or info");
+  if (n > 0 && (!values || !keys_out || !inverse)) return fail(RS_EINVAL, "null values, keys_out or inverse");
+  const PartLayout L = make_part_layout(n, nshards);
+  if (!workspace || workspace_bytes < L.total) return fail(RS_EINVAL, "workspace missing or too small");
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return fail(RS_EINVAL, "workspace must be 256-byte aligned");
+  uint8_t* b = static_cast<uint8_t*>(workspace);
+  const Work w = make_part_work(workspace, L, inverse);
+  RS_HIP(launch_ids_partition(values, n, nshards, owner_seed, w, L.og, reinterpret_cast<int32_t*>(b + L.hist),
+                              reinterpret_cast<int32_t*>(b + L.csum), reinterpret_cast<int64_t*>(b + L.pscal),
+                              keys_out, shard_offsets, info, static_cast<hipStream_t>(stream)));
+  return RS_OK;
 }
 
 rs_status ht_find_or_insert(rs_table* t, const int64_t* keys, int64_t n, int64_t* rows_out, int64_t* n_inserted_dev,

@@ -315,8 +315,10 @@ __device__ inline void probe_store_keys(const TableDev& t, const Work& w, int64_
       sl[u] = q < d ? cdense[q] : -1;
       e[u] = sl[u] >= 0 ? ckey[sl[u]] : kEncEmpty;
       h[u] = sl[u] >= 0 ? (idmap_hash(e[u]) & t.cap_mask) : 0;  // idle lanes read one shared line
+      if (t.slots) {
 #pragma unroll
-      for (int k = 0; k < kProbeBatch; ++k) pb[u][k] = t.slots[(h[u] + k) & t.cap_mask];
+        for (int k = 0; k < kProbeBatch; ++k) pb[u][k] = t.slots[(h[u] + k) & t.cap_mask];
+      }
     }
 #pragma unroll
     for (int u = 0; u < KP; ++u) {
@@ -325,7 +327,7 @@ __device__ inline void probe_store_keys(const TableDev& t, const Work& w, int64_
       const unsigned int kidx = static_cast<unsigned int>(fp);
       const unsigned int first = static_cast<unsigned int>(fp >> 32);
       KeyInfo ki;
-      ki.row = resolve_probe(t, e[u], h[u], pb[u]);
+      ki.row = t.slots ? resolve_probe(t, e[u], h[u], pb[u]) : 0;  // no table: nothing to probe
       ki.first = static_cast<int>(first);
       ki.count = static_cast<int>(ccnt[sl[u]]);
       ki.uid = -1;
@@ -706,20 +708,27 @@ FrontGeom front_geom(int64_t n) {
   return g;
 }
 
-hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const TableDev& t, const Work& w, int64_t* h_live,
-                              int64_t tag, hipEvent_t* ev_tile, hipEvent_t* ev_part, hipStream_t s) {
-  if (n <= 0) {
-    k_zero_scalars<<<1, kCScalars, 0, s>>>(w.scal);
-    return hipGetLastError();
-  }
+hipError_t launch_dedup_keys(const int64_t* values, int64_t n, const TableDev& t, const Work& w, hipEvent_t* ev_tile,
+                             hipEvent_t* ev_part, hipStream_t s) {
   const FrontGeom& g = w.g;
-  if (g.nblk > kMaxDedupBlocks) return hipErrorInvalidValue;
+  if (n <= 0 || g.nblk > kMaxDedupBlocks) return hipErrorInvalidValue;
   if (ev_tile && ev_tile[0]) (void)hipEventRecord(ev_tile[0], s);
   k_tile_dedup<kDedupThreads><<<static_cast<unsigned>(g.nblk), kDedupThreads, 0, s>>>(
       values, n, w, reinterpret_cast<int*>(t.scal + kTErr));
   if (ev_tile && ev_tile[1]) (void)hipEventRecord(ev_tile[1], s);
   if (ev_part && ev_part[0]) (void)hipEventRecord(ev_part[0], s);
   k_part_dedup<<<static_cast<unsigned>(g.P), kPartThreads, 0, s>>>(t, w, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const TableDev& t, const Work& w, int64_t* h_live,
+                              int64_t tag, hipEvent_t* ev_tile, hipEvent_t* ev_part, hipStream_t s) {
+  if (n <= 0) {
+    k_zero_scalars<<<1, kCScalars, 0, s>>>(w.scal);
+    return hipGetLastError();
+  }
+  const hipError_t e = launch_dedup_keys(values, n, t, w, ev_tile, ev_part, s);
+  if (e != hipSuccess) return e;
   const int64_t nb = (n + kRankTile - 1) / kRankTile;
   k_first_sums<kBlock><<<static_cast<unsigned>(nb), kBlock, 0, s>>>(w, n);
   const int64_t nch = (nb + kScanChunk - 1) / kScanChunk;
@@ -918,6 +927,14 @@ __device__ inline void occ_pass(const Work& w, int64_t n, int64_t blk) {
       }
     }
   }
+}
+
+__global__ __launch_bounds__(kBlock) void k_inverse(Work w, int64_t n) { occ_pass<false>(w, n, blockIdx.x); }
+
+hipError_t launch_inverse(const Work& w, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  k_inverse<<<grid_for(n, kBlock * 4, 1ll << 31), kBlock, 0, s>>>(w, n);
+  return hipGetLastError();
 }
 
 // The last pass of a lookup: blocks [0, occ_blocks) run the per-occurrence

@@ -1,0 +1,244 @@
+// Ids partition (gfx950): dedup of a batch of ids fused with the split of the
+// distinct ids by the shard that owns them (RecIS, "Ids Partition" among the
+// benchmarked operators; "Request Merging & Sharding": requests are
+// deduplicated and sharded by id before the all-to-all).
+//
+// owner(k) = mix64(uint64(k) ^ seed) mod G.  Output: the distinct keys shard
+// by shard, each shard's keys in first-occurrence order, the shard offsets,
+// and each id's position in that list.
+//
+// Passes (the first two are the lookup's dedup passes with no IDMap):
+//   k_tile_dedup, k_part_dedup   key index, first position and count of
+//                                every distinct key; a marker at its first
+//                                position
+//   k_owner_hist     per block of positions: distinct keys (first
+//                    occurrences) per owner, in LDS
+//   k_scan_flat      exclusive scan of those counts in (shard, block) order
+//   k_owner_scatter  per block, in position order: stable rank of each first
+//                    occurrence among its shard's (wave ballots on the owner
+//                    bits), key to its output slot, slot into the key's info
+//   k_inverse        per id: the output slot of its key
+#include "device_common.h"
+
+#include <algorithm>
+
+namespace rs {
+
+__device__ inline uint32_t owner_of(int64_t key, uint64_t seed, uint32_t G, uint32_t gmask) {
+  const uint64_t h = mix64(static_cast<uint64_t>(key) ^ seed);
+  // G a power of two: the mask is the same residue
+  return gmask ? static_cast<uint32_t>(h & gmask) : static_cast<uint32_t>(h % G);
+}
+
+OwnerGeom owner_geom(int64_t n, int G) {
+  OwnerGeom og;
+  const int64_t n1 = n > 0 ? n : 1;
+  // rank tiles per block: enough that the count table (G per block) stays
+  // small next to the ids and fits one two-level scan
+  int64_t need = std::max<int64_t>((G + 63) / 64, (static_cast<int64_t>(G) * n1 + (1ll << 32) - 1) >> 32);
+  og.ch = 1;
+  while (og.ch < need) og.ch <<= 1;
+  og.nb = (n1 + og.ch * kRankTile - 1) / (og.ch * kRankTile);
+  og.len = static_cast<int64_t>(G) * og.nb;
+  og.nch = (og.len + kScanChunk - 1) / kScanChunk;
+  og.nbits = 0;
+  while ((1 << og.nbits) < G) ++og.nbits;
+  og.gmask = (G & (G - 1)) == 0 ? static_cast<uint32_t>(G - 1) : 0u;
+  return og;
+}
+
+// Four ids of rank tile b (strided by the block size: position order is
+// item-major, then thread) and their first-occurrence markers.
+__device__ inline void load_tile(const int32_t* __restrict__ firstkey, const int64_t* __restrict__ values, int64_t n,
+                                 int64_t b, int (&f)[kRankItems], int64_t (&v)[kRankItems]) {
+#pragma unroll
+  for (int k = 0; k < kRankItems; ++k) {
+    const int64_t i = b + k * kBlock + threadIdx.x;
+    f[k] = i < n ? firstkey[i] : -1;
+    v[k] = i < n ? values[i] : 0;
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_owner_hist(const int32_t* __restrict__ firstkey,
+                                                       const int64_t* __restrict__ values, int64_t n, int G,
+                                                       uint64_t seed, OwnerGeom og, int32_t* __restrict__ hist) {
+  __shared__ int lh[kMaxShards];
+  for (int q = threadIdx.x; q < G; q += kBlock) lh[q] = 0;
+  __syncthreads();
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * og.ch * kRankTile;
+  for (int64_t c = 0; c < og.ch; ++c) {
+    const int64_t b = base + c * kRankTile;
+    if (b >= n) break;  // block-uniform
+    int f[kRankItems];
+    int64_t v[kRankItems];
+    load_tile(firstkey, values, n, b, f, v);
+#pragma unroll
+    for (int k = 0; k < kRankItems; ++k)
+      if (f[k] >= 0) atomicAdd(&lh[owner_of(v[k], seed, G, og.gmask)], 1);
+  }
+  __syncthreads();
+  for (int q = threadIdx.x; q < G; q += kBlock) hist[static_cast<int64_t>(q) * og.nb + blockIdx.x] = lh[q];
+}
+
+// In-place exclusive scan of a[0, len): block c scans chunk c and stores its
+// total; the last block to finish (a counter, no waiting) scans the chunk
+// totals (nch <= kScanChunk).  An element's prefix is then
+// a[j] + csum[j / kScanChunk]; the grand total goes to *total.
+template <int R>
+__global__ __launch_bounds__(1024) void k_scan_flat(int32_t* __restrict__ a, int64_t len, int32_t* __restrict__ csum,
+                                                    int64_t nch, int64_t* counter, int64_t* total) {
+  static_assert(1024 * R == kScanChunk, "one chunk per block");
+  __shared__ int sh[1024 / kWave + 1];
+  __shared__ bool last;
+  const int64_t c = blockIdx.x;
+  const int64_t lo = c * kScanChunk + static_cast<int64_t>(threadIdx.x) * R;
+  int v[R];
+  int loc = 0;
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    v[j] = lo + j < len ? a[lo + j] : 0;
+    loc += v[j];
+  }
+  int tot;
+  int run = block_excl_scan<1024>(loc, sh, tot);
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    if (lo + j < len) a[lo + j] = run;
+    run += v[j];
+  }
+  if (nch == 1) {
+    if (threadIdx.x == 0) {
+      csum[0] = 0;
+      *total = tot;
+    }
+    return;
+  }
+  if (threadIdx.x == 0) {
+    csum[c] = tot;
+    __threadfence();
+    const unsigned long long done = atomicAdd(reinterpret_cast<unsigned long long*>(counter), 1ull);
+    last = done == static_cast<unsigned long long>(nch - 1);
+  }
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  const int64_t clo = static_cast<int64_t>(threadIdx.x) * R;
+  int cv[R];
+  loc = 0;
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    cv[j] = clo + j < nch ? __hip_atomic_load(&csum[clo + j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+    loc += cv[j];
+  }
+  run = block_excl_scan<1024>(loc, sh, tot);
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    if (clo + j < nch) csum[clo + j] = run;
+    run += cv[j];
+  }
+  if (threadIdx.x == 0) {
+    *counter = 0;  // ready for the next call on this workspace
+    *total = tot;
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_owner_scatter(Work w, const int64_t* __restrict__ values, int64_t n, int G,
+                                                          uint64_t seed, OwnerGeom og, const int32_t* __restrict__ hist,
+                                                          const int32_t* __restrict__ csum, const int64_t* pscal,
+                                                          int64_t* __restrict__ keys_out,
+                                                          int64_t* __restrict__ shard_offsets, int64_t* info) {
+  constexpr int NW = kBlock / kWave;
+  __shared__ int run[kMaxShards];     // next output slot of each shard
+  __shared__ int wc[NW][kMaxShards];  // this round's first occurrences per (wave, shard)
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+  const int64_t blk = blockIdx.x;
+  for (int q = tid; q < G; q += kBlock) {
+    const int64_t j = static_cast<int64_t>(q) * og.nb + blk;
+    const int p = hist[j] + csum[j / kScanChunk];
+    run[q] = p;
+#pragma unroll
+    for (int u = 0; u < NW; ++u) wc[u][q] = 0;
+    if (blk == 0) shard_offsets[q] = p;
+  }
+  if (blk == 0 && tid == 0) {
+    const int64_t U = pscal[kPTotal];
+    shard_offsets[G] = U;
+    info[0] = U;
+    info[1] = pscal[kTErr];
+  }
+  __syncthreads();
+  const uint64_t below = (1ull << lane) - 1ull;
+  const int64_t base = blk * og.ch * kRankTile;
+  for (int64_t c = 0; c < og.ch; ++c) {
+    const int64_t b = base + c * kRankTile;
+    if (b >= n) break;  // block-uniform
+    int f[kRankItems];
+    int64_t v[kRankItems];
+    load_tile(w.firstkey, values, n, b, f, v);
+    uint32_t own[kRankItems];
+#pragma unroll
+    for (int k = 0; k < kRankItems; ++k) own[k] = f[k] >= 0 ? owner_of(v[k], seed, G, og.gmask) : 0u;
+    // item k of every thread, in position order: waves 0..NW-1, lanes 0..63
+#pragma unroll
+    for (int k = 0; k < kRankItems; ++k) {
+      const bool valid = f[k] >= 0;
+      // lanes of this wave whose first occurrence has the same owner
+      uint64_t peers = __ballot(valid);
+      for (int bit = 0; bit < og.nbits; ++bit) {
+        const bool on = (own[k] >> bit) & 1u;
+        const uint64_t bb = __ballot(on);
+        peers &= on ? bb : ~bb;
+      }
+      const int cnt = __popcll(peers);
+      const bool leader = valid && (peers & below) == 0ull;
+      if (leader) wc[wid][own[k]] = cnt;
+      __syncthreads();
+      if (valid) {
+        int pos = run[own[k]] + __popcll(peers & below);
+        for (int u = 0; u < wid; ++u) pos += wc[u][own[k]];
+        keys_out[pos] = v[k];
+        w.kinfo[f[k]].uid = pos;
+      }
+      __syncthreads();
+      if (leader) {
+        atomicAdd(&run[own[k]], cnt);
+        wc[wid][own[k]] = 0;
+      }
+      __syncthreads();
+    }
+  }
+}
+
+__global__ void k_ids_init(int64_t* pscal, int64_t n, int G, int64_t* shard_offsets, int64_t* info) {
+  const int tid = threadIdx.x;
+  if (tid < kPScalars) pscal[tid] = 0;
+  if (n > 0) return;
+  for (int q = tid; q <= G; q += blockDim.x) shard_offsets[q] = 0;
+  if (tid == 0) {
+    info[0] = 0;
+    info[1] = 0;
+  }
+}
+
+hipError_t launch_ids_partition(const int64_t* values, int64_t n, int G, uint64_t seed, const Work& w,
+                                const OwnerGeom& og, int32_t* hist, int32_t* csum, int64_t* pscal, int64_t* keys_out,
+                                int64_t* shard_offsets, int64_t* info, hipStream_t s) {
+  if (G < 1 || G > kMaxShards || og.nch > kScanChunk) return hipErrorInvalidValue;
+  k_ids_init<<<1, kBlock, 0, s>>>(pscal, n, G, shard_offsets, info);
+  if (n <= 0) return hipGetLastError();
+  // no IDMap: the dedup passes probe nothing; their error bits go to pscal
+  TableDev t{};
+  t.scal = pscal;
+  hipError_t e = launch_dedup_keys(values, n, t, w, nullptr, nullptr, s);
+  if (e != hipSuccess) return e;
+  k_owner_hist<<<static_cast<unsigned>(og.nb), kBlock, 0, s>>>(w.firstkey, values, n, G, seed, og, hist);
+  k_scan_flat<kScanChunk / 1024><<<static_cast<unsigned>(og.nch), 1024, 0, s>>>(hist, og.len, csum, og.nch,
+                                                                                pscal + kPCounter, pscal + kPTotal);
+  k_owner_scatter<<<static_cast<unsigned>(og.nb), kBlock, 0, s>>>(w, values, n, G, seed, og, hist, csum, pscal,
+                                                                  keys_out, shard_offsets, info);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_inverse(w, n, s);
+}
+
+}  // namespace rs

@@ -5,7 +5,8 @@ used here only for device memory and the current HIP stream.  There is no
 fallback: if the library is not built, or no GPU is present, calls raise.
 
 Names follow the C ABI (include/recis_mi355x.h): ht_create, ht_find_or_insert,
-lookup_pool_fwd, lookup_pool_bwd, sparse_opt_step, lookup_pool_bwd_opt.
+lookup_pool_fwd, lookup_pool_bwd, sparse_opt_step, lookup_pool_bwd_opt,
+ids_partition.
 """
 from __future__ import annotations
 
@@ -89,6 +90,8 @@ def lib() -> C.CDLL:
         "sparse_opt_step": (C.c_int, [p, C.POINTER(RsCtx), p, C.POINTER(OptParams), p]),
         "lookup_pool_bwd_opt": (C.c_int, [p, C.POINTER(RsCtx), p, C.POINTER(OptParams), p]),
         "rs_set_kernel_events": (C.c_int, [p, i32, p, p]),
+        "ids_partition_workspace_bytes": (C.c_size_t, [i64, i32]),
+        "ids_partition": (C.c_int, [p, i64, i32, C.c_uint64, p, p, p, p, p, C.c_size_t, p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -150,6 +153,50 @@ class Ctx:
 
     def rows(self, U: int) -> torch.Tensor:
         return self._view(self.c.rows, U, torch.int64)
+
+
+def ids_partition_workspace_bytes(n: int, nshards: int) -> int:
+    return int(lib().ids_partition_workspace_bytes(n, nshards))
+
+
+class IdsPartition:
+    """Ids partition (dedup + split by owner shard) with a reusable workspace.
+
+    ``__call__(values, nshards, owner_seed)`` enqueues the call on the current
+    stream and returns device tensors (keys int64 [n], shard_offsets int64
+    [nshards+1], inverse int32 [n], info int64 [2] = {U, error bits}); the
+    first U keys are valid, shard s holds keys[offsets[s]:offsets[s+1]].
+    """
+
+    def __init__(self):
+        self.ws: Optional[torch.Tensor] = None
+
+    def __call__(self, values: torch.Tensor, nshards: int, owner_seed: int = 0, keys=None, shard_offsets=None,
+                 inverse=None, info=None):
+        v = _dev(values, torch.int64)
+        n = v.numel()
+        need = ids_partition_workspace_bytes(n, nshards)
+        if need == 0:
+            raise RecisError(EINVAL, "n must be in [0, 2^28] and nshards in [1, 1024]")
+        if self.ws is None or self.ws.numel() < need:
+            self.ws = torch.empty(need, dtype=torch.uint8, device=v.device)
+        if keys is None:
+            keys = torch.empty(max(n, 1), dtype=torch.int64, device=v.device)
+        if shard_offsets is None:
+            shard_offsets = torch.empty(nshards + 1, dtype=torch.int64, device=v.device)
+        if inverse is None:
+            inverse = torch.empty(max(n, 1), dtype=torch.int32, device=v.device)
+        if info is None:
+            info = torch.empty(2, dtype=torch.int64, device=v.device)
+        _check(lib().ids_partition(_ptr(v), n, nshards, owner_seed & 0xFFFFFFFFFFFFFFFF, _ptr(keys),
+                                   _ptr(shard_offsets), _ptr(inverse), _ptr(info), _ptr(self.ws), self.ws.numel(),
+                                   _stream()))
+        return keys[:max(n, 0)], shard_offsets, inverse[:n], info
+
+
+def ids_partition(values: torch.Tensor, nshards: int, owner_seed: int = 0):
+    """One-off ids partition (allocates its workspace); see IdsPartition."""
+    return IdsPartition()(values, nshards, owner_seed)
 
 
 class Table:

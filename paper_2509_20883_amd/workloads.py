@@ -418,3 +418,22 @@ def describe(w: Workload) -> dict:
             "optimizer": ["adagrad", "adam", "adamw", "adam-eps-hat"][w.opt],
             "pooling": ["sum", "mean", "none"][w.mode], "zipf_s": w.zipf_s,
             "vocab_total": int(sum(w.vocab)) if w.vocab else int(w.pool0), "mini": w.mini}
+
+
+# ---------------------------------------------------------------------------
+# ids partition input
+# ---------------------------------------------------------------------------
+
+# The paper benchmarks its fused ids partition on one million ids.  The
+# stand-in: the 26 single-hot features of workload 1 (Zipf 1.05 over
+# log-uniform vocabularies, feature id in the high bits) at 38462 bags, i.e.
+# 1,000,012 ids of one merged same-dim request, split over the 8 GPUs of one
+# node.
+IDS_PARTITION_BATCH = 38462
+IDS_PARTITION_SHARDS = 8
+IDS_PARTITION_SEED = 0x0DDBA11CAFEF00D5
+
+
+def ids_partition_values(step: int = 0, batch: int = IDS_PARTITION_BATCH) -> np.ndarray:
+    """The ids of one ids-partition call (int64, feature-major)."""
+    return make_batch(workload(1), step, batch=batch).values
