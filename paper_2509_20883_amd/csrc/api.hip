@@ -130,7 +130,7 @@ Work make_work(void* base, const Layout& L) {
 // Workspace layout of one ids partition: the dedup passes' arrays (no
 // IDMap), the owner counts and their scan, scalars.
 struct PartLayout {
-  size_t occ_word, firstkey, trec, srec, pcnt, poff, ptmp, kinfo, hist, csum, cscal, pscal, total;
+  size_t occ_word, firstkey, trec, srec, pcnt, poff, ptmp, kslot, hist, csum, cscal, pscal, total;
   FrontGeom g;
   OwnerGeom og;
 };
@@ -155,7 +155,7 @@ PartLayout make_part_layout(int64_t n, int G) {
   L.pcnt = take(4 * npc);
   L.poff = take(4 * npc);
   L.ptmp = take(8 * nrecs);
-  L.kinfo = take(sizeof(KeyInfo) * nrecs);
+  L.kslot = take(4 * nrecs);
   L.hist = take(4 * static_cast<size_t>(L.og.len));
   L.csum = take(4 * static_cast<size_t>(L.og.nch));
   L.cscal = take(8 * kCScalars);
@@ -175,7 +175,7 @@ Work make_part_work(void* base, const PartLayout& L, int32_t* inverse) {
   w.pcnt = reinterpret_cast<int32_t*>(b + L.pcnt);
   w.poff = reinterpret_cast<int32_t*>(b + L.poff);
   w.ptmp = reinterpret_cast<int2*>(b + L.ptmp);
-  w.kinfo = reinterpret_cast<KeyInfo*>(b + L.kinfo);
+  w.kinfo = nullptr;  // no key info: only first-occurrence markers and key indices
   w.nkeyidx = L.g.nblk * L.g.rcap;
   w.inverse = inverse;
   w.scal = reinterpret_cast<int64_t*>(b + L.cscal);
@@ -585,8 +585,9 @@ rs_status ids_partition(const int64_t* values, int64_t n, int32_t nshards, uint6
   uint8_t* b = static_cast<uint8_t*>(workspace);
   const Work w = make_part_work(workspace, L, inverse);
   RS_HIP(launch_ids_partition(values, n, nshards, owner_seed, w, L.og, reinterpret_cast<int32_t*>(b + L.hist),
-                              reinterpret_cast<int32_t*>(b + L.csum), reinterpret_cast<int64_t*>(b + L.pscal),
-                              keys_out, shard_offsets, info, static_cast<hipStream_t>(stream)));
+                              reinterpret_cast<int32_t*>(b + L.csum), reinterpret_cast<int32_t*>(b + L.kslot),
+                              reinterpret_cast<int64_t*>(b + L.pscal), keys_out, shard_offsets, info,
+                              static_cast<hipStream_t>(stream)));
   return RS_OK;
 }
 

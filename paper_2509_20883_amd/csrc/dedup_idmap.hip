@@ -326,15 +326,17 @@ __device__ inline void probe_store_keys(const TableDev& t, const Work& w, int64_
       const unsigned long long fp = cfp[sl[u]];
       const unsigned int kidx = static_cast<unsigned int>(fp);
       const unsigned int first = static_cast<unsigned int>(fp >> 32);
-      KeyInfo ki;
-      ki.row = t.slots ? resolve_probe(t, e[u], h[u], pb[u]) : 0;  // no table: nothing to probe
-      ki.first = static_cast<int>(first);
-      ki.count = static_cast<int>(ccnt[sl[u]]);
-      ki.uid = -1;
-      ki.start = 0;
-      ki.long_idx = -1;
-      ki.pad = 0;
-      w.kinfo[kidx] = ki;
+      if (w.kinfo) {  // null: only the first-occurrence markers are wanted
+        KeyInfo ki;
+        ki.row = t.slots ? resolve_probe(t, e[u], h[u], pb[u]) : 0;  // no table: nothing to probe
+        ki.first = static_cast<int>(first);
+        ki.count = static_cast<int>(ccnt[sl[u]]);
+        ki.uid = -1;
+        ki.start = 0;
+        ki.long_idx = -1;
+        ki.pad = 0;
+        w.kinfo[kidx] = ki;
+      }
       if (first < static_cast<uint64_t>(n)) w.firstkey[first] = static_cast<int>(kidx);
     }
   }
@@ -927,14 +929,6 @@ __device__ inline void occ_pass(const Work& w, int64_t n, int64_t blk) {
       }
     }
   }
-}
-
-__global__ __launch_bounds__(kBlock) void k_inverse(Work w, int64_t n) { occ_pass<false>(w, n, blockIdx.x); }
-
-hipError_t launch_inverse(const Work& w, int64_t n, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  k_inverse<<<grid_for(n, kBlock * 4, 1ll << 31), kBlock, 0, s>>>(w, n);
-  return hipGetLastError();
 }
 
 // The last pass of a lookup: blocks [0, occ_blocks) run the per-occurrence

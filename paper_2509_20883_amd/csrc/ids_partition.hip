@@ -13,11 +13,13 @@
 //                                position
 //   k_owner_hist     per block of positions: distinct keys (first
 //                    occurrences) per owner, in LDS
-//   k_scan_flat      exclusive scan of those counts in (shard, block) order
+//   k_scan_one / k_scan_flat  exclusive scan of those counts in (shard,
+//                    block) order (one block, or chunks + a last-block pass)
 //   k_owner_scatter  per block, in position order: stable rank of each first
 //                    occurrence among its shard's (wave ballots on the owner
-//                    bits), key to its output slot, slot into the key's info
-//   k_inverse        per id: the output slot of its key
+//                    bits), key to its output slot, slot by key index
+//   k_ids_inverse    per id: the output slot of its key (id -> record -> key
+//                    index -> slot)
 #include "device_common.h"
 
 #include <algorithm>
@@ -33,12 +35,15 @@ __device__ inline uint32_t owner_of(int64_t key, uint64_t seed, uint32_t G, uint
 OwnerGeom owner_geom(int64_t n, int G) {
   OwnerGeom og;
   const int64_t n1 = n > 0 ? n : 1;
-  // rank tiles per block: enough that the count table (G per block) stays
-  // small next to the ids and fits one two-level scan
-  int64_t need = std::max<int64_t>((G + 63) / 64, (static_cast<int64_t>(G) * n1 + (1ll << 32) - 1) >> 32);
+  // rank tiles per block: as few as keep the count table (G per block) at
+  // most a quarter of the ids (or 16384 counts) and within one two-level scan
+  const int64_t cap = std::min<int64_t>(std::max<int64_t>(n1 / 4, 16384), int64_t(kScanChunk) * kScanChunk);
   og.ch = 1;
-  while (og.ch < need) og.ch <<= 1;
-  og.nb = (n1 + og.ch * kRankTile - 1) / (og.ch * kRankTile);
+  og.nb = (n1 + kRankTile - 1) / kRankTile;
+  while (static_cast<int64_t>(G) * og.nb > cap) {
+    og.ch <<= 1;
+    og.nb = (n1 + og.ch * kRankTile - 1) / (og.ch * kRankTile);
+  }
   og.len = static_cast<int64_t>(G) * og.nb;
   og.nch = (og.len + kScanChunk - 1) / kScanChunk;
   og.nbits = 0;
@@ -142,9 +147,52 @@ __global__ __launch_bounds__(1024) void k_scan_flat(int32_t* __restrict__ a, int
   }
 }
 
+// One-block exclusive scan of a[0, len), len <= 1024 R, in place; the chunk
+// offsets csum[0, nch) are all zero, so prefixes read as in k_scan_flat.
+// Wave w owns elements [64 R w, 64 R (w + 1)): its j-th row of 64 is one
+// coalesced load, scanned across the lanes and chained over the rows.
+template <int R>
+__global__ __launch_bounds__(1024) void k_scan_one(int32_t* __restrict__ a, int64_t len, int32_t* __restrict__ csum,
+                                                   int64_t nch, int64_t* total) {
+  constexpr int NW = 1024 / kWave;
+  __shared__ int sh[NW + 1];
+  const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+  const int64_t base = static_cast<int64_t>(wid) * R * kWave + lane;
+  int v[R];
+#pragma unroll
+  for (int j = 0; j < R; ++j) v[j] = base + j * kWave < len ? a[base + j * kWave] : 0;
+  int ex[R];
+  int run = 0;  // the wave's total over rows < j
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const int inc = wave_incl_scan(v[j]);
+    ex[j] = run + inc - v[j];
+    run += __shfl(inc, kWave - 1, kWave);
+  }
+  if (lane == 0) sh[wid] = run;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int r = 0;
+    for (int q = 0; q < NW; ++q) {
+      const int t = sh[q];
+      sh[q] = r;
+      r += t;
+    }
+    sh[NW] = r;
+  }
+  __syncthreads();
+  const int off = sh[wid];
+#pragma unroll
+  for (int j = 0; j < R; ++j)
+    if (base + j * kWave < len) a[base + j * kWave] = off + ex[j];
+  if (threadIdx.x < nch) csum[threadIdx.x] = 0;
+  if (threadIdx.x == 0) *total = sh[NW];
+}
+
 __global__ __launch_bounds__(kBlock) void k_owner_scatter(Work w, const int64_t* __restrict__ values, int64_t n, int G,
                                                           uint64_t seed, OwnerGeom og, const int32_t* __restrict__ hist,
-                                                          const int32_t* __restrict__ csum, const int64_t* pscal,
+                                                          const int32_t* __restrict__ csum,
+                                                          int32_t* __restrict__ kslot, const int64_t* pscal,
                                                           int64_t* __restrict__ keys_out,
                                                           int64_t* __restrict__ shard_offsets, int64_t* info) {
   constexpr int NW = kBlock / kWave;
@@ -197,7 +245,7 @@ __global__ __launch_bounds__(kBlock) void k_owner_scatter(Work w, const int64_t*
         int pos = run[own[k]] + __popcll(peers & below);
         for (int u = 0; u < wid; ++u) pos += wc[u][own[k]];
         keys_out[pos] = v[k];
-        w.kinfo[f[k]].uid = pos;
+        kslot[f[k]] = pos;
       }
       __syncthreads();
       if (leader) {
@@ -206,6 +254,42 @@ __global__ __launch_bounds__(kBlock) void k_owner_scatter(Work w, const int64_t*
       }
       __syncthreads();
     }
+  }
+}
+
+// inverse[i] = output slot of occurrence i's key: its dedup record (from the
+// occurrence word), the record's key index, that key's slot; -1 for a
+// rejected (reserved) key.
+__global__ __launch_bounds__(kBlock) void k_ids_inverse(Work w, const int32_t* __restrict__ kslot, int64_t n) {
+  const int64_t i0 = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * 4;
+  if (i0 >= n) return;
+  const FrontGeom g = w.g;
+  uint32_t o[4];
+  if (i0 + 4 <= n) {
+    const uint4 a = *reinterpret_cast<const uint4*>(w.occ_word + i0);
+    o[0] = a.x;
+    o[1] = a.y;
+    o[2] = a.z;
+    o[3] = a.w;
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) o[k] = i0 + k < n ? w.occ_word[i0 + k] : kOccRejected;
+  }
+  int kid[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {  // all four record reads in flight together
+    const bool rej = o[k] == kOccRejected;
+    const int64_t src = rej ? 0 : ((i0 + k) >> kDedupTileLog2) / g.R * g.rcap + (o[k] >> 12);
+    const int x = w.recres[src].x;
+    kid[k] = rej ? -1 : x;
+  }
+  int pos[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) pos[k] = kid[k] < 0 ? -1 : kslot[kid[k]];
+  if (i0 + 4 <= n) {
+    *reinterpret_cast<int4*>(w.inverse + i0) = make_int4(pos[0], pos[1], pos[2], pos[3]);
+  } else {
+    for (int k = 0; k < 4 && i0 + k < n; ++k) w.inverse[i0 + k] = pos[k];
   }
 }
 
@@ -221,8 +305,8 @@ __global__ void k_ids_init(int64_t* pscal, int64_t n, int G, int64_t* shard_offs
 }
 
 hipError_t launch_ids_partition(const int64_t* values, int64_t n, int G, uint64_t seed, const Work& w,
-                                const OwnerGeom& og, int32_t* hist, int32_t* csum, int64_t* pscal, int64_t* keys_out,
-                                int64_t* shard_offsets, int64_t* info, hipStream_t s) {
+                                const OwnerGeom& og, int32_t* hist, int32_t* csum, int32_t* kslot, int64_t* pscal,
+                                int64_t* keys_out, int64_t* shard_offsets, int64_t* info, hipStream_t s) {
   if (G < 1 || G > kMaxShards || og.nch > kScanChunk) return hipErrorInvalidValue;
   k_ids_init<<<1, kBlock, 0, s>>>(pscal, n, G, shard_offsets, info);
   if (n <= 0) return hipGetLastError();
@@ -232,13 +316,16 @@ hipError_t launch_ids_partition(const int64_t* values, int64_t n, int G, uint64_
   hipError_t e = launch_dedup_keys(values, n, t, w, nullptr, nullptr, s);
   if (e != hipSuccess) return e;
   k_owner_hist<<<static_cast<unsigned>(og.nb), kBlock, 0, s>>>(w.firstkey, values, n, G, seed, og, hist);
-  k_scan_flat<kScanChunk / 1024><<<static_cast<unsigned>(og.nch), 1024, 0, s>>>(hist, og.len, csum, og.nch,
-                                                                                pscal + kPCounter, pscal + kPTotal);
-  k_owner_scatter<<<static_cast<unsigned>(og.nb), kBlock, 0, s>>>(w, values, n, G, seed, og, hist, csum, pscal,
-                                                                  keys_out, shard_offsets, info);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  return launch_inverse(w, n, s);
+  constexpr int kOneBlock = 16;  // counts per thread of the one-block scan
+  if (og.len <= 1024 * kOneBlock)
+    k_scan_one<kOneBlock><<<1, 1024, 0, s>>>(hist, og.len, csum, og.nch, pscal + kPTotal);
+  else
+    k_scan_flat<kScanChunk / 1024><<<static_cast<unsigned>(og.nch), 1024, 0, s>>>(hist, og.len, csum, og.nch,
+                                                                                  pscal + kPCounter, pscal + kPTotal);
+  k_owner_scatter<<<static_cast<unsigned>(og.nb), kBlock, 0, s>>>(w, values, n, G, seed, og, hist, csum, kslot,
+                                                                  pscal, keys_out, shard_offsets, info);
+  k_ids_inverse<<<grid_for(n, kBlock * 4, 1ll << 31), kBlock, 0, s>>>(w, kslot, n);
+  return hipGetLastError();
 }
 
 }  // namespace rs

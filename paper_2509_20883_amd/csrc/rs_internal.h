@@ -248,23 +248,23 @@ FrontGeom front_geom(int64_t n);
 // can refresh its bound on the live count without a copy or an event.
 hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const TableDev& t, const Work& w, int64_t* h_live,
                               int64_t tag, hipEvent_t* ev_tile, hipEvent_t* ev_part, hipStream_t s);
-// The first two dedup passes only (tile dedup, per-partition dedup; with
-// t.slots == nullptr no IDMap is probed and every key gets row 0): key info
-// of every distinct key and the first-occurrence markers.  n > 0.
+// The first two dedup passes only (tile dedup, per-partition dedup): the
+// first-occurrence markers, each record's key index and, unless w.kinfo is
+// null, the key info of every distinct key (t.slots null: no IDMap probe,
+// row 0).  n > 0.
 hipError_t launch_dedup_keys(const int64_t* values, int64_t n, const TableDev& t, const Work& w, hipEvent_t* ev_tile,
                              hipEvent_t* ev_part, hipStream_t s);
-// inverse[i] = kinfo[key index of occurrence i].uid (-1 for a rejected key)
-hipError_t launch_inverse(const Work& w, int64_t n, hipStream_t s);
 // Geometry of the ids partition's owner passes.
 OwnerGeom owner_geom(int64_t n, int G);
-// Ids partition of n ids into G shards: the dedup passes on w (no IDMap),
-// owner counts (hist [og.len]), their scan (csum [og.nch]), the stable
-// scatter of the distinct keys into keys_out, shard_offsets [G+1] and
+// Ids partition of n ids into G shards: the dedup passes on w (no IDMap, no
+// key info), owner counts (hist [og.len]), their scan (csum [og.nch]), the
+// stable scatter of the distinct keys into keys_out and of their output
+// slots into kslot [per key index], shard_offsets [G+1] and
 // info [2] = {distinct keys, error bits}, then w.inverse [n].  pscal holds
 // kPScalars scalars.
 hipError_t launch_ids_partition(const int64_t* values, int64_t n, int G, uint64_t seed, const Work& w,
-                                const OwnerGeom& og, int32_t* hist, int32_t* csum, int64_t* pscal, int64_t* keys_out,
-                                int64_t* shard_offsets, int64_t* info, hipStream_t s);
+                                const OwnerGeom& og, int32_t* hist, int32_t* csum, int32_t* kslot, int64_t* pscal,
+                                int64_t* keys_out, int64_t* shard_offsets, int64_t* info, hipStream_t s);
 // unique / segments / rows / IDMap insert / row init, then the per-occurrence
 // pass: inverse[] and, for a forward (occ_lists), each occurrence's row and
 // list position and the hot keys' backward units
