@@ -52,6 +52,10 @@ def lib():
         L.or_dedup.argtypes = [p, i64, p, p]
         L.or_ids_partition.restype = i64
         L.or_ids_partition.argtypes = [p, i64, i32, u64, p, p, p, p]
+        L.or_bucketize.restype = i32
+        L.or_bucketize.argtypes = [p, p, i32, p, p, p]
+        L.or_mod.restype = i32
+        L.or_mod.argtypes = [p, p, i32, p, p]
         L.or_find_or_insert.restype = i32
         L.or_find_or_insert.argtypes = [p, p, i64, p, p]
         L.or_read_rows.restype = i64
@@ -126,6 +130,30 @@ def ids_partition(values: np.ndarray, nshards: int, owner_seed: int = 0):
     if U < 0:
         raise ValueError("ids_partition: invalid arguments")
     return keys[:U].copy(), offs.copy(), inv[:n].copy(), int(rej[0])
+
+
+def bucketize(values, col_offsets, boundaries, bnd_offsets) -> np.ndarray:
+    """Bucket of every value of every column (int64), TF Bucketize semantics."""
+    v = _c(values, np.float32)
+    co = _c(col_offsets, np.int64)
+    b = _c(boundaries, np.float32)
+    bo = _c(bnd_offsets, np.int64)
+    out = np.empty(max(v.size, 1), dtype=np.int64)
+    if lib().or_bucketize(_p(v), _p(co), co.size - 1, _p(b if b.size else np.zeros(1, np.float32)), _p(bo),
+                          _p(out)) != 0:
+        raise ValueError("bucketize: invalid arguments")
+    return out[:v.size].copy()
+
+
+def mod(values, col_offsets, moduli) -> np.ndarray:
+    """Floor modulus of every id by its column's modulus (int64)."""
+    v = _c(values, np.int64)
+    co = _c(col_offsets, np.int64)
+    m = _c(moduli, np.int64)
+    out = np.empty(max(v.size, 1), dtype=np.int64)
+    if lib().or_mod(_p(v), _p(co), co.size - 1, _p(m if m.size else np.zeros(1, np.int64)), _p(out)) != 0:
+        raise ValueError("mod: invalid arguments")
+    return out[:v.size].copy()
 
 
 def backward(offsets, inverse, U, dim, mode, pad_len, grad):

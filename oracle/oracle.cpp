@@ -17,6 +17,7 @@
 //   backward       per unique key: sum of the upstream gradients of every
 //                  occurrence (scaled by 1/len for mean)
 //   ids partition  dedup + split of the distinct keys by owner shard
+//   bucketize/mod  feature transforms fused over many columns
 //   optimizer      Adagrad (Duchi et al. 2011), Adam (Kingma & Ba 2015,
 //                  Algorithm 1), AdamW (Adam with decoupled weight decay,
 //                  Loshchilov & Hutter 2019; the paper names SparseAdamW) or
@@ -254,6 +255,45 @@ int64_t or_ids_partition(const int64_t* values, int64_t n, int32_t nshards, uint
     inverse_out[i] = reserved(values[i]) ? -1 : static_cast<int32_t>(out_pos.at(values[i]));
   if (n_rejected) *n_rejected = rejected;
   return U;
+}
+
+// Bucketize, fused over columns ("Bucketize and Mod" in Benchmark of
+// Operators; the Feature Engine turns a float feature such as a price into
+// an id by its bucket).  Column c holds values[col_off[c] .. col_off[c+1])
+// and its nondecreasing boundaries bnd[bnd_off[c] .. bnd_off[c+1]).
+// Reading taken (the paper names the operator only): TensorFlow's Bucketize,
+// bucket = the number of boundaries b with b <= x (so boundaries[k-1] <= x <
+// boundaries[k] gives k); a NaN compares false and lands in bucket 0.
+// Returns 0, or -ST_EINVAL for bad offsets.
+int or_bucketize(const float* values, const int64_t* col_off, int32_t ncols, const float* bnd,
+                 const int64_t* bnd_off, int64_t* out) {
+  if (ncols < 0 || col_off[0] != 0 || bnd_off[0] != 0) return -ST_EINVAL;
+  for (int32_t c = 0; c < ncols; ++c) {
+    if (col_off[c + 1] < col_off[c] || bnd_off[c + 1] < bnd_off[c]) return -ST_EINVAL;
+    for (int64_t i = col_off[c]; i < col_off[c + 1]; ++i) {
+      int64_t k = 0;
+      for (int64_t j = bnd_off[c]; j < bnd_off[c + 1]; ++j)
+        if (bnd[j] <= values[i]) ++k;
+      out[i] = k;
+    }
+  }
+  return 0;
+}
+
+// Mod, fused over columns (same passage): column c's ids map to x mod m_c
+// with m_c > 0.  Reading taken: the floor modulus (result in [0, m_c), also
+// for a negative id), so the result is a valid bucket id.
+int or_mod(const int64_t* values, const int64_t* col_off, int32_t ncols, const int64_t* moduli, int64_t* out) {
+  if (ncols < 0 || col_off[0] != 0) return -ST_EINVAL;
+  for (int32_t c = 0; c < ncols; ++c) {
+    if (col_off[c + 1] < col_off[c] || moduli[c] <= 0) return -ST_EINVAL;
+    for (int64_t i = col_off[c]; i < col_off[c + 1]; ++i) {
+      int64_t r = values[i] % moduli[c];
+      if (r < 0) r += moduli[c];
+      out[i] = r;
+    }
+  }
+  return 0;
 }
 
 int or_find_or_insert(void* h, const int64_t* keys, int64_t n, int64_t* rows_out, int64_t* n_inserted) {

@@ -307,6 +307,59 @@ def test_ids_partition_reserved_keys_and_empty():
         O.ids_partition(seq, 0, 0)
 
 
+# --------------------------------------------------------------------------- bucketize / mod
+
+
+def _columns(g, ncols, lo, hi):
+    sizes = g.integers(lo, hi, size=ncols)
+    off = np.zeros(ncols + 1, dtype=np.int64)
+    np.cumsum(sizes, out=off[1:])
+    return off
+
+
+def test_bucketize_matches_searchsorted_right_and_tf_examples():
+    # TensorFlow's documented example: boundaries [0, 10, 100],
+    # input [[-5, 10000], [150, 10], [5, 100]] -> [[0, 3], [3, 2], [1, 3]]
+    out = O.bucketize(np.array([-5, 10000, 150, 10, 5, 100], np.float32), np.array([0, 6]),
+                      np.array([0, 10, 100], np.float32), np.array([0, 3]))
+    assert out.tolist() == [0, 3, 3, 2, 1, 3]
+    g = np.random.default_rng(31)
+    coff = _columns(g, 40, 0, 300)
+    nb = g.integers(0, 50, size=40)
+    boff = np.zeros(41, dtype=np.int64)
+    np.cumsum(nb, out=boff[1:])
+    bnd = np.concatenate([np.sort(g.choice(np.linspace(-5, 5, 41), size=k).astype(np.float32)) for k in nb]
+                         + [np.zeros(0, np.float32)])
+    vals = g.choice(np.linspace(-6, 6, 121), size=int(coff[-1])).astype(np.float32)  # hits boundaries exactly
+    vals[::17] = np.nan
+    vals[5::23] = -0.0
+    out = O.bucketize(vals, coff, bnd, boff)
+    for c in range(40):
+        v = vals[coff[c]:coff[c + 1]]
+        b = bnd[boff[c]:boff[c + 1]]
+        want = np.searchsorted(b, v, side="right")
+        want[np.isnan(v)] = 0
+        assert np.array_equal(out[coff[c]:coff[c + 1]], want)
+
+
+def test_mod_matches_numpy_floor_mod():
+    g = np.random.default_rng(32)
+    coff = _columns(g, 30, 0, 400)
+    mods = g.integers(1, 10**6, size=30)
+    mods[0], mods[1] = 1, (1 << 62) + 7
+    vals = g.integers(-2**63, 2**63 - 1, size=int(coff[-1]), dtype=np.int64)
+    vals[:3] = [np.iinfo(np.int64).min, -1, np.iinfo(np.int64).max]
+    out = O.mod(vals, coff, mods)
+    for c in range(30):
+        v = vals[coff[c]:coff[c + 1]]
+        assert np.array_equal(out[coff[c]:coff[c + 1]], np.mod(v, np.int64(mods[c])))
+    # by hand: Python's % is the floor modulus
+    out = O.mod(np.array([-7, 7, -1, 0, 12], np.int64), np.array([0, 5]), np.array([5]))
+    assert out.tolist() == [-7 % 5, 7 % 5, -1 % 5, 0, 12 % 5]
+    with pytest.raises(ValueError):
+        O.mod(np.array([1], np.int64), np.array([0, 1]), np.array([0]))
+
+
 # --------------------------------------------------------------------------- find-or-insert
 
 
