@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define RS_VERSION 3
+#define RS_VERSION 4
 
 typedef enum {
   RS_OK = 0,
@@ -293,6 +293,30 @@ size_t ids_partition_workspace_bytes(int64_t n, int32_t nshards);
 rs_status ids_partition(const int64_t* values, int64_t n, int32_t nshards, uint64_t owner_seed, int64_t* keys_out,
                         int64_t* shard_offsets, int32_t* inverse, int64_t* info, void* workspace,
                         size_t workspace_bytes, rs_stream stream);
+
+/* Feature transforms fused over many columns, one launch for all of them
+ * ("Bucketize and Mod" among the benchmarked operators: models hold dozens
+ * to hundreds of such columns).  The columns are one flat array of n
+ * elements; column c holds [col_offsets[c], col_offsets[c+1]) (int64
+ * [ncols+1], col_offsets[0] = 0, nondecreasing, col_offsets[ncols] = n).
+ *
+ * fused_bucketize: values fp32 [n] -> out int64 [n], out[i] = the number of
+ *   boundaries b of i's column with b <= values[i] (TensorFlow's Bucketize:
+ *   boundaries[k-1] <= x < boundaries[k] gives k; a NaN gives 0).  Column c's
+ *   boundaries are boundaries[bnd_offsets[c] .. bnd_offsets[c+1]), fp32,
+ *   nondecreasing and not NaN (int64 [ncols+1] offsets, bnd_offsets[0] = 0).
+ * fused_mod: values int64 [n] -> out int64 [n], out[i] = values[i] mod m in
+ *   [0, m) (floor modulus) with m = moduli[column of i] (int64 [ncols],
+ *   m > 0; a modulus <= 0 gives -1).
+ * All arrays are device arrays.  The offsets are read by the kernels; the
+ * caller guarantees the layout above (validate != 0 checks it, and the
+ * moduli, on the host: it copies them back, so it synchronizes).  Errors:
+ * RS_EINVAL (sizes, null pointers, a layout validate rejects), RS_EHIP. */
+rs_status fused_bucketize(const float* values, int64_t n, const int64_t* col_offsets, int32_t ncols,
+                          const float* boundaries, const int64_t* bnd_offsets, int64_t* out, int32_t validate,
+                          rs_stream stream);
+rs_status fused_mod(const int64_t* values, int64_t n, const int64_t* col_offsets, int32_t ncols,
+                    const int64_t* moduli, int64_t* out, int32_t validate, rs_stream stream);
 
 /* Kernel timing hook: from now on, hipEvent_t `start` / `stop` are recorded on
  * the call's stream immediately before / after every launch of the named

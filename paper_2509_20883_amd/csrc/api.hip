@@ -591,6 +591,62 @@ rs_status ids_partition(const int64_t* values, int64_t n, int32_t nshards, uint6
   return RS_OK;
 }
 
+namespace {
+
+// Host check of column offsets (and their boundary offsets / moduli): copies
+// them back, so it synchronizes.
+rs_status check_columns(const int64_t* col_off, int32_t ncols, int64_t n, const int64_t* bnd_off,
+                        const int64_t* moduli, hipStream_t s) {
+  std::vector<int64_t> co(static_cast<size_t>(ncols) + 1), aux(bnd_off ? ncols + 1 : moduli ? ncols : 0);
+  RS_HIP(hipStreamSynchronize(s));
+  RS_HIP(hipMemcpy(co.data(), col_off, sizeof(int64_t) * co.size(), hipMemcpyDeviceToHost));
+  if (!aux.empty())
+    RS_HIP(hipMemcpy(aux.data(), bnd_off ? bnd_off : moduli, sizeof(int64_t) * aux.size(), hipMemcpyDeviceToHost));
+  if (co[0] != 0 || co[ncols] != n) return fail(RS_EINVAL, "column offsets must start at 0 and end at n");
+  for (int32_t c = 0; c < ncols; ++c)
+    if (co[c + 1] < co[c]) return fail(RS_EINVAL, "column offsets must be nondecreasing");
+  if (bnd_off) {
+    if (aux[0] != 0) return fail(RS_EINVAL, "boundary offsets must start at 0");
+    for (int32_t c = 0; c < ncols; ++c)
+      if (aux[c + 1] < aux[c]) return fail(RS_EINVAL, "boundary offsets must be nondecreasing");
+  }
+  if (moduli)
+    for (int32_t c = 0; c < ncols; ++c)
+      if (aux[c] <= 0) return fail(RS_EINVAL, "moduli must be > 0");
+  return RS_OK;
+}
+
+}  // namespace
+
+rs_status fused_bucketize(const float* values, int64_t n, const int64_t* col_offsets, int32_t ncols,
+                          const float* boundaries, const int64_t* bnd_offsets, int64_t* out, int32_t validate,
+                          rs_stream stream) {
+  if (n < 0 || n >= (int64_t(1) << 40)) return fail(RS_EINVAL, "n must be in [0, 2^40)");
+  if (ncols < 1 || !col_offsets || !bnd_offsets) return fail(RS_EINVAL, "need ncols >= 1 and both offset arrays");
+  if (n > 0 && (!values || !out)) return fail(RS_EINVAL, "null values or out");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (validate) {
+    const rs_status st = check_columns(col_offsets, ncols, n, bnd_offsets, nullptr, s);
+    if (st != RS_OK) return st;
+  }
+  RS_HIP(launch_bucketize(values, n, col_offsets, ncols, boundaries, bnd_offsets, out, s));
+  return RS_OK;
+}
+
+rs_status fused_mod(const int64_t* values, int64_t n, const int64_t* col_offsets, int32_t ncols,
+                    const int64_t* moduli, int64_t* out, int32_t validate, rs_stream stream) {
+  if (n < 0 || n >= (int64_t(1) << 40)) return fail(RS_EINVAL, "n must be in [0, 2^40)");
+  if (ncols < 1 || !col_offsets || !moduli) return fail(RS_EINVAL, "need ncols >= 1, offsets and moduli");
+  if (n > 0 && (!values || !out)) return fail(RS_EINVAL, "null values or out");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (validate) {
+    const rs_status st = check_columns(col_offsets, ncols, n, nullptr, moduli, s);
+    if (st != RS_OK) return st;
+  }
+  RS_HIP(launch_mod(values, n, col_offsets, ncols, moduli, out, s));
+  return RS_OK;
+}
+
 rs_status ht_find_or_insert(rs_table* t, const int64_t* keys, int64_t n, int64_t* rows_out, int64_t* n_inserted_dev,
                             rs_stream stream) {
   if (!t) return fail(RS_EINVAL, "null table");

@@ -281,6 +281,12 @@ hipError_t launch_bwd(const TableDev& t, const Work& w, const int64_t* offsets, 
                       hipEvent_t* ev_long, hipStream_t s);
 hipError_t launch_opt(const TableDev& t, const Work& w, int64_t n, const float* grad_unique, const OptArgs& opt,
                       hipEvent_t* ev, hipStream_t s);
+// Feature transforms fused over ncols columns of one flat array of n
+// elements (column c: [col_off[c], col_off[c+1])).
+hipError_t launch_bucketize(const float* values, int64_t n, const int64_t* col_off, int ncols, const float* bnd,
+                            const int64_t* bnd_off, int64_t* out, hipStream_t s);
+hipError_t launch_mod(const int64_t* values, int64_t n, const int64_t* col_off, int ncols, const int64_t* moduli,
+                      int64_t* out, hipStream_t s);
 hipError_t launch_rehash(const Slot* old_slots, int64_t old_cap, const TableDev& t, hipStream_t s);
 hipError_t launch_export(const TableDev& t, int64_t cap_slots, int64_t* keys, int64_t* rows, int64_t cap,
                          int64_t* n_dev, hipStream_t s);

@@ -6,7 +6,7 @@ fallback: if the library is not built, or no GPU is present, calls raise.
 
 Names follow the C ABI (include/recis_mi355x.h): ht_create, ht_find_or_insert,
 lookup_pool_fwd, lookup_pool_bwd, sparse_opt_step, lookup_pool_bwd_opt,
-ids_partition.
+ids_partition, fused_bucketize, fused_mod.
 """
 from __future__ import annotations
 
@@ -92,6 +92,8 @@ def lib() -> C.CDLL:
         "rs_set_kernel_events": (C.c_int, [p, i32, p, p]),
         "ids_partition_workspace_bytes": (C.c_size_t, [i64, i32]),
         "ids_partition": (C.c_int, [p, i64, i32, C.c_uint64, p, p, p, p, p, C.c_size_t, p]),
+        "fused_bucketize": (C.c_int, [p, i64, p, i32, p, p, p, i32, p]),
+        "fused_mod": (C.c_int, [p, i64, p, i32, p, p, i32, p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -197,6 +199,34 @@ class IdsPartition:
 def ids_partition(values: torch.Tensor, nshards: int, owner_seed: int = 0):
     """One-off ids partition (allocates its workspace); see IdsPartition."""
     return IdsPartition()(values, nshards, owner_seed)
+
+
+def fused_bucketize(values: torch.Tensor, col_offsets: torch.Tensor, boundaries: torch.Tensor,
+                    bnd_offsets: torch.Tensor, out: Optional[torch.Tensor] = None,
+                    validate: bool = False) -> torch.Tensor:
+    """Bucket (int64) of every fp32 value of every column; one launch."""
+    v = _dev(values, torch.float32)
+    co = _dev(col_offsets, torch.int64)
+    b = _dev(boundaries, torch.float32)
+    bo = _dev(bnd_offsets, torch.int64)
+    if out is None:
+        out = torch.empty(v.numel(), dtype=torch.int64, device=v.device)
+    _check(lib().fused_bucketize(_ptr(v), v.numel(), _ptr(co), co.numel() - 1, _ptr(b), _ptr(bo), _ptr(out),
+                                 int(validate), _stream()))
+    return out
+
+
+def fused_mod(values: torch.Tensor, col_offsets: torch.Tensor, moduli: torch.Tensor,
+              out: Optional[torch.Tensor] = None, validate: bool = False) -> torch.Tensor:
+    """Floor modulus (int64) of every id by its column's modulus; one launch."""
+    v = _dev(values, torch.int64)
+    co = _dev(col_offsets, torch.int64)
+    m = _dev(moduli, torch.int64)
+    if out is None:
+        out = torch.empty(v.numel(), dtype=torch.int64, device=v.device)
+    _check(lib().fused_mod(_ptr(v), v.numel(), _ptr(co), co.numel() - 1, _ptr(m), _ptr(out), int(validate),
+                           _stream()))
+    return out
 
 
 class Table:

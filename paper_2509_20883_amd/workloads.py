@@ -437,3 +437,54 @@ IDS_PARTITION_SEED = 0x0DDBA11CAFEF00D5
 def ids_partition_values(step: int = 0, batch: int = IDS_PARTITION_BATCH) -> np.ndarray:
     """The ids of one ids-partition call (int64, feature-major)."""
     return make_batch(workload(1), step, batch=batch).values
+
+
+# ---------------------------------------------------------------------------
+# feature-transform columns (bucketize, mod)
+# ---------------------------------------------------------------------------
+
+# The paper benchmarks its fused bucketize and mod on 100 columns of 10,000
+# values each.  Stand-ins: log-normal float features (prices) with 63
+# boundaries per column at the column distribution's quantiles (rounded to
+# cents, so some values hit a boundary exactly); int64 ids (Zipf ranks through
+# the 40-bit bijection, some negative) with a modulus per column drawn
+# log-uniformly in [1e2, 1e7].
+FEATURE_COLUMNS = 100
+FEATURE_VALUES = 10_000
+FEATURE_BOUNDS = 63
+
+
+def _col_offsets(sizes: np.ndarray) -> np.ndarray:
+    off = np.zeros(len(sizes) + 1, dtype=np.int64)
+    np.cumsum(sizes, out=off[1:])
+    return off
+
+
+def bucketize_columns(ncols: int = FEATURE_COLUMNS, nvals=FEATURE_VALUES, nbounds=FEATURE_BOUNDS, step: int = 0):
+    """(values fp32 [n], col_offsets int64 [ncols+1], boundaries fp32, bnd_offsets int64 [ncols+1]).
+    ``nvals`` / ``nbounds`` may be ints or per-column arrays."""
+    g = rng(40, step)
+    sizes = np.broadcast_to(np.asarray(nvals, dtype=np.int64), (ncols,)).copy()
+    nb = np.broadcast_to(np.asarray(nbounds, dtype=np.int64), (ncols,)).copy()
+    vals, bnds = [], []
+    for c in range(ncols):
+        mu, sigma = g.uniform(0.0, 6.0), g.uniform(0.3, 1.5)
+        x = np.round(g.lognormal(mu, sigma, size=int(sizes[c])), 2).astype(np.float32)
+        q = np.quantile(g.lognormal(mu, sigma, size=4096), np.linspace(0, 1, int(nb[c]) + 2)[1:-1]) if nb[c] else []
+        vals.append(x)
+        bnds.append(np.sort(np.round(np.asarray(q, dtype=np.float64), 2)).astype(np.float32))
+    return (np.concatenate(vals) if vals else np.zeros(0, np.float32), _col_offsets(sizes),
+            np.concatenate(bnds) if bnds else np.zeros(0, np.float32), _col_offsets(nb))
+
+
+def mod_columns(ncols: int = FEATURE_COLUMNS, nvals=FEATURE_VALUES, step: int = 0):
+    """(values int64 [n], col_offsets int64 [ncols+1], moduli int64 [ncols])."""
+    g = rng(41, step)
+    sizes = np.broadcast_to(np.asarray(nvals, dtype=np.int64), (ncols,)).copy()
+    vals = []
+    for c in range(ncols):
+        ids = rank_to_id(zipf_ranks(int(sizes[c]), 10**6, 1.1, g), 7919 * c + 11)
+        sign = np.where(g.random(int(sizes[c])) < 0.1, -1, 1)
+        vals.append(ids * sign)
+    moduli = np.round(10.0 ** g.uniform(2.0, 7.0, size=ncols)).astype(np.int64)
+    return (np.concatenate(vals).astype(np.int64) if vals else np.zeros(0, np.int64), _col_offsets(sizes), moduli)
