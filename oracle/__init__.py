@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "liboracle.so")
 
 OK, EINVAL, ENOMEM, EFULL, EKEY = 0, 1, 2, 3, 4
-SUM, MEAN, NONE = 0, 1, 2
+SUM, MEAN, NONE, TAIL = 0, 1, 2, 3
 F32, BF16 = 0, 1
 ADAGRAD, ADAM, ADAMW, ADAM_TF = 0, 1, 2, 3
 
@@ -226,7 +226,7 @@ class Table:
         v = _c(values, np.int64)
         off = _c(offsets, np.int64)
         n, bags = v.size, off.size - 1
-        if mode == NONE:
+        if mode in (NONE, TAIL):
             out = np.zeros((bags, pad_len, self.dim), dtype=np.float64)
             mask = np.zeros((bags, pad_len), dtype=np.uint8)
         else:
@@ -254,7 +254,7 @@ class Table:
         off = _c(offsets, np.int64)
         g = _c(grad, np.float32)
         n, bags = v.size, off.size - 1
-        if mode == NONE:
+        if mode in (NONE, TAIL):
             out = np.zeros((bags, pad_len, self.dim), dtype=np.float64)
             mask = np.zeros((bags, pad_len), dtype=np.uint8)
         else:

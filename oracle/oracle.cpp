@@ -43,7 +43,7 @@
 namespace {
 
 constexpr int ST_OK = 0, ST_EINVAL = 1, ST_EFULL = 3, ST_EKEY = 4;
-constexpr int SUM = 0, MEAN = 1, NONE = 2;
+constexpr int SUM = 0, MEAN = 1, NONE = 2, TAIL = 3;
 constexpr int F32 = 0, BF16 = 1;
 constexpr int ADAGRAD = 0, ADAM = 1, ADAMW = 2, ADAM_TF = 3;
 constexpr int64_t KEY_EMPTY = std::numeric_limits<int64_t>::min();   // reserved
@@ -359,6 +359,9 @@ int64_t or_export(void* h, int64_t* keys, int64_t* rows, int64_t cap) {
 //   MEAN: out[g]       = that sum / len(g); an empty bag gives 0
 //   NONE: out[g][t]    = row of the t-th id of bag g for t < min(len, L), else 0;
 //         mask[g][t]   = t < len
+//   TAIL: the same with the last min(len, L) ids of the bag: out[g][t] = row of
+//         id skip + t, skip = max(len - L, 0) (the sequence tile of the
+//         Reduction Operations, concatenating a sequence's most recent rows)
 // Dedup and find-or-insert run first (new keys are inserted during the
 // forward, so new rows are initialised before use).  A row of -1 (a failed
 // insert in a bounded table) contributes a zero vector.
@@ -369,7 +372,7 @@ int or_forward(void* h, const int64_t* values, const int64_t* offsets, int64_t n
   if (n < 0 || bags < 0 || offsets[0] != 0 || offsets[bags] != n) return ST_EINVAL;
   for (int64_t g = 0; g < bags; ++g)
     if (offsets[g + 1] < offsets[g]) return ST_EINVAL;
-  if (mode == NONE && pad_len <= 0) return ST_EINVAL;
+  if ((mode == NONE || mode == TAIL) && pad_len <= 0) return ST_EINVAL;
   const int64_t U = or_dedup(values, n, unique_out, inverse_out);
   if (U < 0) return ST_EKEY;
   int64_t nn = 0;
@@ -379,11 +382,12 @@ int or_forward(void* h, const int64_t* values, const int64_t* offsets, int64_t n
   const int D = T->dim;
   for (int64_t g = 0; g < bags; ++g) {
     const int64_t b = offsets[g], e = offsets[g + 1], len = e - b;
-    if (mode == NONE) {
+    if (mode == NONE || mode == TAIL) {
+      const int64_t skip = mode == TAIL && len > pad_len ? len - pad_len : 0;
       for (int64_t t = 0; t < pad_len; ++t) {
         double* o = out + (g * pad_len + t) * D;
         mask[g * pad_len + t] = static_cast<uint8_t>(t < len);
-        const int64_t r = t < len ? rows_out[inverse_out[b + t]] : -1;
+        const int64_t r = t < len ? rows_out[inverse_out[b + skip + t]] : -1;
         for (int j = 0; j < D; ++j) o[j] = r >= 0 ? static_cast<double>(T->get_w(r, j)) : 0.0;
       }
       continue;
@@ -404,20 +408,22 @@ int or_forward(void* h, const int64_t* values, const int64_t* offsets, int64_t n
 // Backward (workflow, backward update: gradients are aggregated per
 // retained forward offset).  grad_unique[u] = sum over occurrences i of key u
 // of scale(g(i)) * grad[g(i)], scale = 1 (sum) or 1/len (mean); padded mode
-// sums grad[g][t] over the positions t < min(len, L) holding key u.  Masked
-// positions are never read.  Sums in fp64.
+// sums grad[g][t] over the positions t < min(len, L) holding key u (tail
+// mode: id skip + t holds slot t).  Masked positions are never read.  Sums
+// in fp64.
 int or_backward(const int64_t* offsets, int64_t bags, const int32_t* inverse, int64_t U, int dim,
                 int mode, int64_t pad_len, const float* grad, double* grad_unique) {
   for (int64_t k = 0; k < U * dim; ++k) grad_unique[k] = 0.0;
   for (int64_t g = 0; g < bags; ++g) {
     const int64_t b = offsets[g], e = offsets[g + 1], len = e - b;
+    const int64_t skip = mode == TAIL && len > pad_len ? len - pad_len : 0;
     for (int64_t i = b; i < e; ++i) {
       const int64_t u = inverse[i];
       if (u < 0) continue;
       double* gu = grad_unique + u * dim;
-      if (mode == NONE) {
-        const int64_t t = i - b;
-        if (t >= pad_len) continue;
+      if (mode == NONE || mode == TAIL) {
+        const int64_t t = i - b - skip;
+        if (t < 0 || t >= pad_len) continue;
         const float* gr = grad + (g * pad_len + t) * dim;
         for (int j = 0; j < dim; ++j) gu[j] += static_cast<double>(gr[j]);
       } else {

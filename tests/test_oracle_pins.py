@@ -460,6 +460,66 @@ def test_padded_gather_and_mask():
                 assert r["mask"][gi, t] == 0 and np.all(r["out"][gi, t] == 0)
 
 
+def test_sequence_tile_tail_is_the_concat_of_the_last_rows():
+    g = np.random.default_rng(12)
+    vals, off = _tiny_batch(g, 25, 16, 30)
+    L, D = 6, 4
+    T = O.Table(D, seed=5)
+    r = T.forward(vals, off, O.TAIL, pad_len=L)
+    assert r["status"] == O.OK
+    lens = np.diff(off)
+    # definition: row g of the [B, L*D] tile is the concatenation of the rows
+    # of the bag's last min(len, L) ids, zero-padded to L*D
+    for gi in range(len(lens)):
+        ids = vals[off[gi]:off[gi + 1]][-L:] if lens[gi] else vals[:0]
+        _, Wg, _ = T.read_rows(ids) if ids.size else (0, np.zeros((0, D), np.float32), 0)
+        want = np.zeros(L * D)
+        want[:ids.size * D] = Wg.astype(np.float64).reshape(-1)
+        assert np.array_equal(r["out"].reshape(len(lens), L * D)[gi], want)
+        assert r["mask"][gi].tolist() == [1] * min(lens[gi], L) + [0] * (L - min(lens[gi], L))
+    # the same as the head copy of a batch cut to each bag's last L ids
+    cut = [vals[off[gi]:off[gi + 1]][-L:] for gi in range(len(lens))]
+    off2 = np.zeros_like(off)
+    np.cumsum([c.size for c in cut], out=off2[1:])
+    r2 = O.Table(D, seed=5).forward(np.concatenate(cut), off2, O.NONE, pad_len=L)
+    assert np.array_equal(r["out"], r2["out"]) and np.array_equal(r["mask"], r2["mask"])
+    # ids cut off the front are still looked up (inserted)
+    assert T.size() == len(np.unique(vals))
+
+
+def test_backward_adjoint_identity_tail_tile():
+    g = np.random.default_rng(14)
+    vals, off = _tiny_batch(g, 30, 14, 20)
+    L, D = 5, 3
+    st, u, inv = O.dedup(vals)
+    U = len(u)
+    W = g.standard_normal((U, D))
+    G = g.standard_normal((len(off) - 1, L, D)).astype(np.float32)
+    lens = np.diff(off)
+    fw = np.zeros((len(off) - 1, L, D))
+    for gi in range(len(lens)):
+        skip = max(lens[gi] - L, 0)
+        for t in range(min(lens[gi], L)):
+            fw[gi, t] = W[inv[off[gi] + skip + t]]
+    Gn = G.copy()
+    Gn[np.arange(L)[None, :] >= lens[:, None]] = np.nan
+    gu = O.backward(off, inv, U, D, O.TAIL, L, Gn)
+    assert np.all(np.isfinite(gu))
+    lhs = float((fw * G.astype(np.float64)).sum())
+    rhs = float((W * gu).sum())
+    assert abs(lhs - rhs) <= 1e-12 * max(1.0, abs(lhs))
+    # the ids cut off the front get no gradient
+    front = np.zeros(U, bool)
+    for gi in range(len(lens)):
+        for i in range(off[gi], off[gi] + max(lens[gi] - L, 0)):
+            front[inv[i]] = True
+    kept = np.zeros(U, bool)
+    for gi in range(len(lens)):
+        for i in range(off[gi] + max(lens[gi] - L, 0), off[gi + 1]):
+            kept[inv[i]] = True
+    assert np.all(gu[front & ~kept] == 0)
+
+
 # --------------------------------------------------------------------------- backward
 
 
