@@ -98,7 +98,7 @@ def b_alg(w, N, G, U, Nnew):
     """Algorithmic HBM bytes of one step (every array moved once; rows of
     duplicate ids counted once)."""
     R, S = row_bytes(w)
-    if w.mode == 2:
+    if w.mode in (2, 3):
         L = w.pad_len
         out = G * L * R + G * L            # padded rows + mask
         grad = N * R                       # valid positions only (lengths <= L here)
@@ -133,13 +133,13 @@ def kernel_bytes(w, kernel, N, G, ks):
     R, S = row_bytes(w)
     U = ks["U"]
     if kernel == "pool":
-        out = G * w.pad_len * R + G * w.pad_len if w.mode == 2 else G * w.dim * 4
+        out = G * w.pad_len * R + G * w.pad_len if w.mode in (2, 3) else G * w.dim * 4
         # offsets, inverse, occurrence ranks, row ids, segment descriptors,
         # unique rows, output, occurrence list
         return 8 * (G + 1) + 4 * N + 4 * N + 8 * U + 16 * U + R * U + out + 4 * N
     if kernel == "bwd_short":
         Us, Ns = ks["U_short"], ks["N_short"]
-        gr = R if w.mode == 2 else w.dim * 4
+        gr = R if w.mode in (2, 3) else w.dim * 4
         # segment descriptors, occurrence list, one upstream gradient row per
         # occurrence, row + state read-modify-write
         return 16 * U + 4 * Ns + gr * Ns + 2 * (R + S) * Us
@@ -194,7 +194,7 @@ def cpu_baseline(w, target_s):
     steps = 0
     while secs < target_s and steps < 50:
         b = W.make_batch(w, steps)
-        if w.mode == 2:
+        if w.mode in (2, 3):
             grad = W.make_grad(w, b, steps)
         else:
             grad = np.random.default_rng(steps).standard_normal((b.bags, w.dim)).astype(np.float32)
@@ -441,7 +441,7 @@ def main():
             host_values[s] = bv
         batches.append((torch.from_numpy(bv).to(dev), torch.from_numpy(bo).to(dev), nb, gb))
         if s < 4:
-            if w.mode == 2:
+            if w.mode in (2, 3):
                 shape = (gb, w.pad_len, w.dim)
                 gdt = torch.bfloat16 if w.row_dtype == 1 else torch.float32
             else:
@@ -453,7 +453,7 @@ def main():
     ctxs = [R.Ctx() for _ in range(ring)]
     stepscal = torch.zeros(nsteps, 4, dtype=torch.int64, device=dev)
     maxb = max(b[3] for b in batches)
-    if w.mode == 2:
+    if w.mode in (2, 3):
         odt = torch.bfloat16 if w.row_dtype == 1 else torch.float32
         out = torch.empty(maxb, w.pad_len, w.dim, dtype=odt, device=dev)
         mask = torch.empty(maxb, w.pad_len, dtype=torch.uint8, device=dev)

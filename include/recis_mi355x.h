@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define RS_VERSION 4
+#define RS_VERSION 5
 
 typedef enum {
   RS_OK = 0,
@@ -54,7 +54,12 @@ typedef enum {
   RS_EHIP = 5    /* a HIP runtime call failed                               */
 } rs_status;
 
-typedef enum { RS_POOL_SUM = 0, RS_POOL_MEAN = 1, RS_POOL_NONE = 2 } rs_pool;
+/* Pooling of a bag ("Reduction Operations": sum, mean, tile).  The two
+ * padded copies are the sequence tile: viewed as [bags, pad_len * D], a
+ * bag's row is the concatenation of its rows.  RS_POOL_NONE keeps the first
+ * pad_len ids of a longer bag, RS_POOL_TILE_TAIL its last pad_len (the most
+ * recent behaviours), both in their order from slot 0, zero after. */
+typedef enum { RS_POOL_SUM = 0, RS_POOL_MEAN = 1, RS_POOL_NONE = 2, RS_POOL_TILE_TAIL = 3 } rs_pool;
 typedef enum { RS_F32 = 0, RS_BF16 = 1 } rs_dtype;
 /* Row-sparse optimizers (every one keeps fp32 state beside the row: Adagrad
  * one accumulator per element, the Adam family two moments per element).
@@ -209,6 +214,9 @@ size_t lookup_workspace_bytes(int64_t n, int64_t bags, int64_t pad_len, const rs
  *                the t-th id of bag g for t < min(len, pad_len), else 0;
  *                mask uint8 [bags, pad_len] = (t < len).  Ids past pad_len
  *                are looked up (and inserted) but not copied.
+ *  RS_POOL_TILE_TAIL: the same with the bag's last min(len, pad_len) ids:
+ *                out[g][t] = row of id skip + t, skip = max(len - pad_len, 0);
+ *                the skipped ids are looked up (and inserted) but not copied.
  * New keys are inserted (and initialised) before the gather.
  * validate != 0 also checks the CSR offsets on the host (copies them back:
  * slow, synchronizing).  Errors: RS_EINVAL (sizes, workspace, mode),
@@ -242,7 +250,8 @@ rs_status lookup_pool_prepared(rs_table* t, rs_ctx* ctx, void* out, uint8_t* mas
  * (none; positions with mask 0 are never read).
  * grad_unique [n, D] fp32: row u (< U) receives
  *   sum over occurrences i of unique u of scale(bag(i)) * grad_out[bag(i)]
- * (scale 1 for sum, 1/len for mean; padded: grad_out[g][t] for t < pad_len). */
+ * (scale 1 for sum, 1/len for mean; padded: grad_out[g][t] for the id copied
+ * to slot t; ids that were not copied contribute nothing). */
 rs_status lookup_pool_bwd(rs_table* t, const rs_ctx* ctx, const void* grad_out, float* grad_unique,
                           rs_stream stream);
 

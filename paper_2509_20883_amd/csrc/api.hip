@@ -43,6 +43,8 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
 
+bool padded_mode(int32_t mode) { return mode == RS_POOL_NONE || mode == RS_POOL_TILE_TAIL; }
+
 // Workspace layout of one forward: every array sized by the upper bound n.
 struct Layout {
   size_t occ_word, firstkey, trec, srec, pcnt, poff, ptmp, kinfo, inverse, occ_row, occ_pos, unique,
@@ -744,9 +746,9 @@ rs_status lookup_prepare(rs_table* t, const int64_t* values, const int64_t* offs
   if (!t || !ctx) return fail(RS_EINVAL, "null table or context");
   if (n < 0 || n > (int64_t(1) << 28)) return fail(RS_EINVAL, "n must be in [0, 2^28]");
   if (bags < 0 || bags >= (int64_t(1) << 31)) return fail(RS_EINVAL, "bags must be in [0, 2^31)");
-  if (mode != RS_POOL_SUM && mode != RS_POOL_MEAN && mode != RS_POOL_NONE) return fail(RS_EINVAL, "bad pooling mode");
-  if (mode == RS_POOL_NONE) {
-    if (pad_len <= 0) return fail(RS_EINVAL, "pad_len must be > 0 for RS_POOL_NONE");
+  if (mode != RS_POOL_SUM && mode != RS_POOL_MEAN && !padded_mode(mode)) return fail(RS_EINVAL, "bad pooling mode");
+  if (padded_mode(mode)) {
+    if (pad_len <= 0) return fail(RS_EINVAL, "pad_len must be > 0 for the padded modes");
     if (bags * pad_len >= (int64_t(1) << 31)) return fail(RS_EINVAL, "bags * pad_len must be < 2^31");
   }
   if (!offsets || (n > 0 && !values)) return fail(RS_EINVAL, "null input");
@@ -771,7 +773,7 @@ rs_status lookup_prepare(rs_table* t, const int64_t* values, const int64_t* offs
   ctx->offsets = offsets;
   ctx->n = n;
   ctx->bags = bags;
-  ctx->pad_len = mode == RS_POOL_NONE ? pad_len : 0;
+  ctx->pad_len = padded_mode(mode) ? pad_len : 0;
   ctx->mode = mode;
   ctx->dim = t->d.dim;
   rs_status st = dedup_and_insert(t, values, n, w, true, s);
@@ -785,7 +787,7 @@ rs_status lookup_pool_prepared(rs_table* t, rs_ctx* ctx, void* out, uint8_t* mas
   if (!t || !ctx) return fail(RS_EINVAL, "null table or context");
   if (ctx->table != t || ctx->priv[0] < 1) return fail(RS_EINVAL, "context was not prepared on this table");
   if (ctx->bags > 0 && !out) return fail(RS_EINVAL, "null output");
-  if (ctx->mode == RS_POOL_NONE && ctx->bags > 0 && !mask) return fail(RS_EINVAL, "null mask");
+  if (padded_mode(ctx->mode) && ctx->bags > 0 && !mask) return fail(RS_EINVAL, "null mask");
   const Work w = ctx_work(ctx);
   RS_HIP(launch_pool(t->dev(), w, ctx->offsets, ctx->n, ctx->bags, ctx->mode, ctx->pad_len, out, mask,
                      t->ev(RS_K_POOL), static_cast<hipStream_t>(stream)));
@@ -797,7 +799,7 @@ rs_status lookup_pool_fwd(rs_table* t, const int64_t* values, const int64_t* off
                           int32_t mode, int64_t pad_len, void* out, uint8_t* mask, rs_ctx* ctx, int32_t validate,
                           rs_stream stream) {
   if (bags > 0 && !out) return fail(RS_EINVAL, "null output");
-  if (mode == RS_POOL_NONE && bags > 0 && !mask) return fail(RS_EINVAL, "null mask");
+  if (padded_mode(mode) && bags > 0 && !mask) return fail(RS_EINVAL, "null mask");
   rs_status st = lookup_prepare(t, values, offsets, n, bags, mode, pad_len, ctx, validate, stream);
   if (st != RS_OK) return st;
   return lookup_pool_prepared(t, ctx, out, mask, stream);

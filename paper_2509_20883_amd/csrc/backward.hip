@@ -399,7 +399,7 @@ template <typename WT, bool FUSED>
 static hipError_t bwd_mode(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int mode,
                            const void* grad, float* gu, const OptArgs& o, hipEvent_t* es, hipEvent_t* el,
                            hipStream_t s) {
-  if (mode == 2) return bwd_dim<WT, WT, 0, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
+  if (mode == 2 || mode == 3) return bwd_dim<WT, WT, 0, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
   if (mode == 1) return bwd_dim<WT, float, 1, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
   return bwd_dim<WT, float, 0, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
 }

@@ -163,8 +163,8 @@ __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64
 // positions, with their loads issued together.
 template <typename WT, int LANES>
 __global__ __launch_bounds__(kBlock) void k_pool_none(TableDev t, Work w, const int64_t* __restrict__ offsets,
-                                                      int64_t n, int64_t bags, int64_t L, WT* __restrict__ out,
-                                                      uint8_t* __restrict__ mask) {
+                                                      int64_t n, int64_t bags, int64_t L, bool tail,
+                                                      WT* __restrict__ out, uint8_t* __restrict__ mask) {
   constexpr int E = 16 / static_cast<int>(sizeof(WT));
   constexpr int D = LANES * E;
   constexpr int GPB = kBlock / LANES;
@@ -177,14 +177,16 @@ __global__ __launch_bounds__(kBlock) void k_pool_none(TableDev t, Work w, const 
     const int64_t g = blk / nch, c = blk % nch;
     const int64_t b = min(max(offsets[g], int64_t(0)), n);
     const int64_t len = min(max(offsets[g + 1], b), n) - b;
+    // the copied window: ids [skip, skip + min(len, L)) of the bag
+    const int64_t skip = tail && len > L ? len - L : 0;
     int64_t tp[K], r[K];
     int pos[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       tp[k] = c * TCH + grp + k * GPB;
       const bool act = tp[k] < L && tp[k] < len;
-      r[k] = act ? w.occ_row[b + tp[k]] : -1;
-      pos[k] = act ? w.occ_pos[b + tp[k]] : -1;
+      r[k] = act ? w.occ_row[b + skip + tp[k]] : -1;
+      pos[k] = act ? w.occ_pos[b + skip + tp[k]] : -1;
     }
     uint4 v[K];
 #pragma unroll
@@ -201,9 +203,10 @@ __global__ __launch_bounds__(kBlock) void k_pool_none(TableDev t, Work w, const 
       }
     }
     if (c == 0 && lane == 0) {
-      // ids past pad_len: in the occurrence list (the key is touched) but
-      // without a gradient row
-      for (int64_t tpos = L + grp; tpos < len; tpos += GPB) {
+      // ids outside the window (past L, or before skip): in the occurrence
+      // list (the key is touched) but without a gradient row
+      const int64_t x0 = tail ? 0 : L, x1 = tail ? skip : len;
+      for (int64_t tpos = x0 + grp; tpos < x1; tpos += GPB) {
         const int pp = w.occ_pos[b + tpos];
         if (pp >= 0) w.occ_ref[pp] = -1;
       }
@@ -215,11 +218,11 @@ template <typename WT, int LANES>
 static hipError_t pool_mode(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int64_t bags,
                             int mode, int64_t pad_len, void* out, uint8_t* mask, hipStream_t s) {
   constexpr int GPB = kBlock / LANES;
-  if (mode == 2) {
+  if (mode == 2 || mode == 3) {
     constexpr int TCH = GPB > 64 ? GPB : 64;
     const int64_t nch = (pad_len + TCH - 1) / TCH;
     k_pool_none<WT, LANES><<<grid_for(bags * nch, 1, 1 << 20), kBlock, 0, s>>>(t, w, offsets, n, bags, pad_len,
-                                                                             static_cast<WT*>(out), mask);
+                                                                             mode == 3, static_cast<WT*>(out), mask);
   } else {
     // mostly single-id bags (n <= 2 bags): a lane group takes 8 bags and
     // requests their rows together; longer bags: 4 bags, 16-row chunks

@@ -22,7 +22,7 @@ HEADER = os.path.join(os.path.dirname(PKG), "include", "recis_mi355x.h")
 
 OK, EINVAL, ENOMEM, EFULL, EKEY, EHIP = 0, 1, 2, 3, 4, 5
 STATUS_NAMES = {0: "RS_OK", 1: "RS_EINVAL", 2: "RS_ENOMEM", 3: "RS_EFULL", 4: "RS_EKEY", 5: "RS_EHIP"}
-SUM, MEAN, NONE = 0, 1, 2
+SUM, MEAN, NONE, TAIL = 0, 1, 2, 3
 F32, BF16 = 0, 1
 ADAGRAD, ADAM, ADAMW, ADAM_TF = 0, 1, 2, 3
 # kernel ids of rs_set_kernel_events ("occ" and "init_rows" bracket the same
@@ -315,7 +315,7 @@ class Table:
         n, bags = v.numel(), o.numel() - 1
         ctx = ctx or Ctx()
         ctx.ensure(self.workspace_bytes(n, bags, pad_len), v.device)
-        if mode == NONE:
+        if mode in (NONE, TAIL):
             odt = torch.bfloat16 if self.row_dtype == BF16 else torch.float32
             if out is None:
                 out = torch.empty(bags, pad_len, self.dim, dtype=odt, device=v.device)
@@ -346,7 +346,7 @@ class Table:
         """Second half of the forward: gather + pool of a prepared ctx."""
         c = ctx.c
         dev = ctx.ws.device
-        if c.mode == NONE:
+        if c.mode in (NONE, TAIL):
             odt = torch.bfloat16 if self.row_dtype == BF16 else torch.float32
             if out is None:
                 out = torch.empty(c.bags, c.pad_len, self.dim, dtype=odt, device=dev)
@@ -359,7 +359,7 @@ class Table:
 
     def _grad(self, ctx: Ctx, grad_out: torch.Tensor) -> torch.Tensor:
         c = ctx.c
-        if c.mode == NONE:
+        if c.mode in (NONE, TAIL):
             want, dt = c.bags * c.pad_len * self.dim, (torch.bfloat16 if self.row_dtype == BF16 else torch.float32)
         else:
             want, dt = c.bags * self.dim, torch.float32

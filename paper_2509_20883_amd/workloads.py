@@ -141,7 +141,13 @@ def zipf_ranks(n: int, V: int, s: float, g: np.random.Generator) -> np.ndarray:
 # configurations
 # ---------------------------------------------------------------------------
 
-SUM, MEAN, NONE = 0, 1, 2
+SUM, MEAN, NONE, TAIL = 0, 1, 2, 3
+
+
+def padded(mode: int) -> bool:
+    """The padded copies: head (first L ids) and tail (last L ids, the sequence tile)."""
+    return mode in (NONE, TAIL)
+
 F32, BF16 = 0, 1
 ADAGRAD, ADAM, ADAMW, ADAM_TF = 0, 1, 2, 3
 
@@ -227,6 +233,13 @@ def workload(k: int, mini: bool = False) -> Workload:
                      batch=32768, n_features=200, vocab=[], zipf_s=1.2, lengths="mixed",
                      namespaced=True, capacity_slots=1 << 25, lr=1e-3, eps=1e-8, prepop="pool",
                      pool0=20_000_000, fresh_per_step=300_000, n_single=150, steps=100)
+    elif k == 5:
+        # the sequence tile of the Reduction Operations benchmark (one million
+        # ids of dim 16): 8000 behaviour sequences of U{16..234} ids (mean
+        # 125), each tiled as the concatenation of its most recent 128 rows
+        w = Workload("seq-tile-1M-d16-tail128-adagrad", 5, dim=16, row_dtype=F32, opt=ADAGRAD, mode=TAIL,
+                     batch=8000, n_features=1, vocab=[1_000_000], zipf_s=1.2, lengths="uniform:16:234",
+                     namespaced=False, capacity_slots=1 << 21, pad_len=128, lr=0.01, eps=1e-8)
     else:
         raise ValueError(f"no workload {k}")
     w.seed = seed64(k)
@@ -247,6 +260,9 @@ def workload(k: int, mini: bool = False) -> Workload:
             w.steps = 3
         if k in (1, 2):
             w.capacity_slots = 1 << 20
+        if k == 5:
+            w.pad_len = 48
+            w.capacity_slots = 1 << 16
         w.block_rows = 1 << 14
     return w
 
@@ -353,7 +369,7 @@ def make_grad(w: Workload, b: Batch, step: int = 0, nan_in_masked: bool = False)
     sequence mode ``[G, L, D]`` as fp32 values already rounded to bf16 when the
     gradient dtype is bf16 (returned as float32 holding bf16-representable values)."""
     g = rng(w.index, 100 + int(w.mini), step)
-    if w.mode == NONE:
+    if padded(w.mode):
         L = w.pad_len
         x = g.standard_normal((b.bags, L, w.dim), dtype=np.float32)
         if w.grad_dtype == BF16:
@@ -416,7 +432,7 @@ def describe(w: Workload) -> dict:
     return {"workload": w.name, "batch": w.batch, "features": w.n_features, "dim": w.dim,
             "row_dtype": "bf16" if w.row_dtype == BF16 else "f32",
             "optimizer": ["adagrad", "adam", "adamw", "adam-eps-hat"][w.opt],
-            "pooling": ["sum", "mean", "none"][w.mode], "zipf_s": w.zipf_s,
+            "pooling": ["sum", "mean", "none", "tile-tail"][w.mode], "pad_len": w.pad_len, "zipf_s": w.zipf_s,
             "vocab_total": int(sum(w.vocab)) if w.vocab else int(w.pool0), "mini": w.mini}
 
 

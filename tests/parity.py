@@ -140,7 +140,7 @@ def run_step_parity(w: W.Workload, gt: R.Table, ot: O.Table, batch: W.Batch, gra
                     check_rows_exact: bool = True):
     """One step on both sides; compares every stage.  Returns (U, n_new)."""
     v, off = batch.values, batch.offsets
-    pad = w.pad_len if w.mode == O.NONE else 0
+    pad = w.pad_len if w.mode in (O.NONE, O.TAIL) else 0
     out, mask, ctx = gt.forward(to_dev(v), to_dev(off), w.mode, pad_len=pad)
     torch.cuda.synchronize()
     ref = ot.forward(v, off, w.mode, pad_len=pad)
@@ -161,7 +161,7 @@ def run_step_parity(w: W.Workload, gt: R.Table, ot: O.Table, batch: W.Batch, gra
     # rows found or inserted this step hold the same bits on both sides
     assert np.array_equal(w0, w0_ref) and np.array_equal(s0, s0_ref), "rows before the optimizer differ"
     # forward output
-    if w.mode == O.NONE:
+    if w.mode in (O.NONE, O.TAIL):
         o = out.float().cpu().numpy()
         assert np.array_equal(o, ref["out"].astype(np.float32)), "padded gather differs"
         assert np.array_equal(mask.cpu().numpy(), ref["mask"]), "mask differs"
@@ -170,7 +170,7 @@ def run_step_parity(w: W.Workload, gt: R.Table, ot: O.Table, batch: W.Batch, gra
         assert_sum_close(out.cpu().numpy(), ref["out"], scale, what=f"step {step} pooled")
     # backward (per-unique sums), stage-wise
     gdev = to_dev(grad)
-    if w.mode == O.NONE and w.row_dtype == O.BF16:
+    if w.mode in (O.NONE, O.TAIL) and w.row_dtype == O.BF16:
         gdev = gdev.to(torch.bfloat16)
     gu = gt.backward(ctx, gdev)
     gu_gpu = gu[:U].cpu().numpy()

@@ -111,11 +111,11 @@ def _check_outputs(w, b, out, mask, g):
     bags = _sample_bags(b, g)
     vals, off = _sub_batch(b, bags)
     ot = _oracle(w)
-    pad = w.pad_len if w.mode == O.NONE else 0
+    pad = w.pad_len if w.mode in (O.NONE, O.TAIL) else 0
     ref = ot.forward(vals, off, w.mode, pad_len=pad)
     assert ref["status"] == O.OK
     sel = torch.from_numpy(bags).cuda()
-    if w.mode == O.NONE:
+    if w.mode in (O.NONE, O.TAIL):
         o = out.index_select(0, sel).float().cpu().numpy()
         assert np.array_equal(o, ref["out"].astype(np.float32)), "padded gather of sampled bags differs"
         assert np.array_equal(mask.index_select(0, sel).cpu().numpy(), ref["mask"]), "mask differs"
@@ -133,7 +133,7 @@ def _check_update(w, b, grad, uniq, inv, sel, w0, s0, w1, s1):
     remap = np.full(U, -1, dtype=np.int32)
     remap[sel] = np.arange(sel.size, dtype=np.int32)
     inv_s = np.where(inv >= 0, remap[np.maximum(inv, 0)], -1).astype(np.int32)
-    pad = w.pad_len if w.mode == O.NONE else 0
+    pad = w.pad_len if w.mode in (O.NONE, O.TAIL) else 0
     gu = O.backward(b.offsets, inv_s, sel.size, w.dim, w.mode, pad, grad)
     gfin = np.where(np.isfinite(grad), grad, 0).astype(np.float32)
     gabs = O.backward(b.offsets, inv_s, sel.size, w.dim, w.mode, pad, np.abs(gfin))
@@ -150,7 +150,7 @@ def _check_update(w, b, grad, uniq, inv, sel, w0, s0, w1, s1):
     assert_opt_close(w1, s1, w1_ref, s1_ref, bounds, what="fused backward + optimizer (sampled ids)")
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4])
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
 def test_fullsize_step(k):
     """One full-size step of workload k (first step after pre-population)."""
     w = W.workload(k)
@@ -164,9 +164,9 @@ def test_fullsize_step(k):
         grad = W.make_grad(w, b, 0)
         v, off = to_dev(b.values), to_dev(b.offsets)
         gdev = to_dev(grad)
-        if w.mode == O.NONE and w.row_dtype == O.BF16:
+        if w.mode in (O.NONE, O.TAIL) and w.row_dtype == O.BF16:
             gdev = gdev.to(torch.bfloat16)
-        out, mask, ctx = gt.forward(v, off, w.mode, pad_len=w.pad_len if w.mode == O.NONE else 0)
+        out, mask, ctx = gt.forward(v, off, w.mode, pad_len=w.pad_len if w.mode in (O.NONE, O.TAIL) else 0)
         torch.cuda.synchronize()
         U, uniq, inv, rows = _check_integers(w, gt, ctx, b, live0, prepop)
         counts = np.bincount(inv[inv >= 0], minlength=U)

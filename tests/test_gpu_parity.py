@@ -132,7 +132,7 @@ def test_rehash_keeps_contents():
 # --------------------------------------------------------------------------- step parity
 
 
-@pytest.mark.parametrize("k", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("k", [0, 1, 2, 3, 4, 5])
 def test_step_parity_workloads(k):
     w = W.workload(k, mini=(k != 0))
     _log("step parity", w.name, "mini" if w.mini else "full")
@@ -141,7 +141,7 @@ def test_step_parity_workloads(k):
     steps = 3 if k in (0, 4) else 2
     for step in range(steps):
         b = W.make_batch(w, step)
-        grad = W.make_grad(w, b, step, nan_in_masked=(w.mode == O.NONE))
+        grad = W.make_grad(w, b, step, nan_in_masked=(w.mode in (O.NONE, O.TAIL)))
         U, nn = P.run_step_parity(w, gt, ot, b, grad, step)
         _log(f"  step {step}: N={b.n} bags={b.bags} U={U} new={nn}")
     gt.check()
@@ -153,9 +153,9 @@ def _fused_vs_unfused(w, b, grad):
     ga, gb = P.gpu_table(w), P.gpu_table(w)
     P.prepopulate(w, ga)
     P.prepopulate(w, gb)
-    pad = w.pad_len if w.mode == O.NONE else 0
+    pad = w.pad_len if w.mode in (O.NONE, O.TAIL) else 0
     gdev = P.to_dev(grad)
-    if w.mode == O.NONE and w.row_dtype == O.BF16:
+    if w.mode in (O.NONE, O.TAIL) and w.row_dtype == O.BF16:
         gdev = gdev.to(torch.bfloat16)
     _, _, ca = ga.forward(P.to_dev(b.values), P.to_dev(b.offsets), w.mode, pad_len=pad)
     _, _, cb = gb.forward(P.to_dev(b.values), P.to_dev(b.offsets), w.mode, pad_len=pad)
@@ -180,7 +180,7 @@ def _fused_vs_unfused(w, b, grad):
     return wa, sa, wb, sb, bounds
 
 
-@pytest.mark.parametrize("k", [0, 2, 3])
+@pytest.mark.parametrize("k", [0, 2, 3, 5])
 def test_fused_bwd_opt_equals_two_calls(k):
     w = W.workload(k, mini=(k != 0))
     _log("fused vs unfused", w.name)
@@ -230,7 +230,7 @@ def _custom_batch_parity(w, values, offsets, steps=1, seed=0):
                 n_features=1, batch=len(offsets) - 1)
     g = np.random.default_rng(seed)
     for step in range(steps):
-        if w.mode == O.NONE:
+        if w.mode in (O.NONE, O.TAIL):
             grad = W.bf16_representable(g.standard_normal((b.bags, w.pad_len, w.dim)).astype(np.float32))
         else:
             grad = g.standard_normal((b.bags, w.dim)).astype(np.float32)
@@ -246,6 +246,21 @@ def test_empty_batch_and_empty_bags():
     _custom_batch_parity(w, [5, 6, 5], [0, 0, 2, 2, 3, 3])
     w2 = W.workload(2, mini=True)
     _custom_batch_parity(w2, [5, 6, 5, 9], [0, 0, 3, 3, 4])
+
+
+def test_sequence_tile_tail_edges():
+    """Tail tile: bags shorter than, equal to and longer than the pad length,
+    empty bags, a key only in the cut-off front of a bag, repeats."""
+    _log("tile tail edges")
+    w = W.workload(5, mini=True)
+    w.pad_len = 5
+    vals = [1, 2, 3, 4, 5, 6, 7, 8,   9, 10,   11, 12, 13, 14, 15,   99, 98, 97, 1, 2, 3, 3, 3]
+    offs = [0, 0, 8, 10, 10, 15, 23]
+    _custom_batch_parity(w, vals, offs, steps=2, seed=3)
+    w.pad_len = 1
+    _custom_batch_parity(w, vals, offs, steps=1, seed=4)
+    w.pad_len = 300                                  # more than one position chunk, never truncating
+    _custom_batch_parity(w, vals, offs, steps=1, seed=5)
 
 
 def test_hot_key_spanning_many_chunks():
