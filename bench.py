@@ -76,7 +76,7 @@ def copy_calibration():
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "ms": ms, "GBps": 2 * n / (ms * 1e-3) / 1e9}))
 
 
-KERNEL_SOURCES = {"pool": "pool.hip", "bwd_short": "backward.hip"}
+KERNEL_SOURCES = {"pool": "pool.hip", "bwd_short": "backward.hip", "bwd_long": "backward.hip"}
 
 
 def kernel_source_hash(kernel: str) -> str:
@@ -94,14 +94,15 @@ def row_bytes(w):
     return R, S
 
 
-def b_alg(w, N, G, U, Nnew):
+def b_alg(w, N, G, U, Nnew, V=None):
     """Algorithmic HBM bytes of one step (every array moved once; rows of
-    duplicate ids counted once)."""
+    duplicate ids counted once).  V: ids inside the padded modes' copied
+    windows (sum over bags of min(len, pad_len))."""
     R, S = row_bytes(w)
     if w.mode in (2, 3):
         L = w.pad_len
         out = G * L * R + G * L            # padded rows + mask
-        grad = N * R                       # valid positions only (lengths <= L here)
+        grad = (N if V is None else V) * R  # gradient rows of the copied ids only
     else:
         out = G * w.dim * 4
         grad = G * w.dim * 4
@@ -118,31 +119,55 @@ def unit_count(c: int, unit: int = 32, max_units: int = 1024) -> int:
     return (c + usz - 1) // usz
 
 
-def key_stats(values: np.ndarray, long_threshold: int = 32):
-    """Host-side split of a batch into short keys (<= 32 occurrences) and hot keys."""
-    _, cnt = np.unique(values, return_counts=True)
+def window_mask(w, offsets: np.ndarray, n: int):
+    """Positions whose id is copied by a padded mode (all positions otherwise)."""
+    if w.mode not in (2, 3):
+        return None
+    lens = np.diff(offsets)
+    t = np.arange(n) - np.repeat(offsets[:-1], lens)           # position inside the bag
+    skip = np.repeat(np.maximum(lens - w.pad_len, 0), lens) if w.mode == 3 else 0
+    return (t >= skip) & (t < skip + w.pad_len)
+
+
+def key_stats(values: np.ndarray, window=None, long_threshold: int = 32):
+    """Host-side split of a batch into short keys (<= 32 occurrences) and hot
+    keys; Nw_* count the occurrences that carry a gradient row (inside the
+    padded modes' windows)."""
+    uk, inv, cnt = np.unique(values, return_inverse=True, return_counts=True)
+    cw = cnt if window is None else np.bincount(inv[window], minlength=uk.size)
     hot = cnt > long_threshold
     return {"U": int(cnt.size), "U_short": int((~hot).sum()), "N_short": int(cnt[~hot].sum()),
             "U_long": int(hot.sum()), "N_long": int(cnt[hot].sum()),
+            "Nw_short": int(cw[~hot].sum()), "Nw_long": int(cw[hot].sum()), "V": int(cw.sum()),
             "units": int(sum(unit_count(int(c)) for c in cnt[hot]))}
 
 
 def kernel_bytes(w, kernel, N, G, ks):
-    """Algorithmic bytes of one launch of the two largest kernels (each array
+    """Algorithmic bytes of one launch of the largest kernels (each array
     element the kernel must touch, counted once; rows of duplicate ids once)."""
     R, S = row_bytes(w)
     U = ks["U"]
+    gr = R if w.mode in (2, 3) else w.dim * 4
     if kernel == "pool":
-        out = G * w.pad_len * R + G * w.pad_len if w.mode in (2, 3) else G * w.dim * 4
+        if w.mode in (2, 3):
+            V = ks["V"]
+            # offsets, row id + list position of each copied id, padded rows
+            # + mask, unique rows, the list entries of all ids
+            return 8 * (G + 1) + 12 * V + G * w.pad_len * R + G * w.pad_len + R * U + 4 * N
         # offsets, inverse, occurrence ranks, row ids, segment descriptors,
         # unique rows, output, occurrence list
-        return 8 * (G + 1) + 4 * N + 4 * N + 8 * U + 16 * U + R * U + out + 4 * N
+        return 8 * (G + 1) + 4 * N + 4 * N + 8 * U + 16 * U + R * U + G * w.dim * 4 + 4 * N
     if kernel == "bwd_short":
-        Us, Ns = ks["U_short"], ks["N_short"]
-        gr = R if w.mode in (2, 3) else w.dim * 4
+        Us, Ns, Nw = ks["U_short"], ks["N_short"], ks["Nw_short"]
         # segment descriptors, occurrence list, one upstream gradient row per
-        # occurrence, row + state read-modify-write
-        return 16 * U + 4 * Ns + gr * Ns + 2 * (R + S) * Us
+        # occurrence that has one, row + state read-modify-write
+        return 16 * U + 4 * Ns + gr * Nw + 2 * (R + S) * Us
+    if kernel == "bwd_long":
+        Ul, Nl, Nw, nu = ks["U_long"], ks["N_long"], ks["Nw_long"], ks["units"]
+        # unit sums: unit descriptors, occurrence list, gradient rows, one
+        # partial row written per unit; finish: partial rows read, row + state
+        # read-modify-write of each hot key
+        return 16 * nu + 4 * Nl + gr * Nw + 4 * w.dim * nu + 4 * w.dim * nu + 2 * (R + S) * Ul
     raise KeyError(kernel)
 
 
@@ -432,13 +457,16 @@ def main():
     gen.manual_seed(2509)
     stat_steps = set(np.linspace(a.warmup, nsteps - 1, num=min(a.steps, 5)).round().astype(int).tolist()) \
         if a.steps > 30 else set(range(a.warmup, nsteps))
-    host_values = {}
+    host_values, host_windows = {}, {}
     for s in range(nsteps):
         bv, bo = hb[s]
         hb[s] = None
         nb, gb = int(bv.shape[0]), int(bo.shape[0] - 1)
+        win = window_mask(w, bo, nb)
+        if win is not None:
+            host_windows[s] = int(win.sum())
         if s in stat_steps:
-            host_values[s] = bv
+            host_values[s] = (bv, win)
         batches.append((torch.from_numpy(bv).to(dev), torch.from_numpy(bo).to(dev), nb, gb))
         if s < 4:
             if w.mode in (2, 3):
@@ -505,13 +533,14 @@ def main():
             prof[k].append(e0.elapsed_time(e1))
     for k in names:
         table.set_kernel_events(k, None, None)
-    # the dominant kernel: the larger of the pool and the short-key backward by
-    # their median time over the warm-up steps after the first (cold) one
+    # the dominant kernel: the largest of the pool, the short-key backward and
+    # the hot-key backward (unit sums + finish) by their median time over the
+    # warm-up steps after the first (cold) one
     def wmed(k):
         v = prof[k][1:] if len(prof[k]) > 1 else prof[k]
         return float(np.median(v)) if v else 0.0
 
-    dom = max(("pool", "bwd_short"), key=wmed)
+    dom = max(("pool", "bwd_short", "bwd_long"), key=wmed)
     cands = (dom,)
     # timed region: K steps, the dominant kernel bracketed by HIP events on the
     # step's stream in every 4th step (a timing event costs ~6 us of idle GPU
@@ -588,9 +617,11 @@ def main():
         U, Nnew = int(sc[0]), int(sc[1])
         _, _, n, g = batches[i]
         tot_ids += n
-        tot_bytes += b_alg(w, n, g, U, Nnew)
+        V = host_windows.get(i)
+        tot_bytes += b_alg(w, n, g, U, Nnew, V)
         if i in host_values:  # every timed step, or 5 evenly spaced ones in long runs
-            dom_b.append(kernel_bytes(w, dom, n, g, key_stats(host_values[i])))
+            hv, hw = host_values[i]
+            dom_b.append(kernel_bytes(w, dom, n, g, key_stats(hv, hw)))
         Us.append(U)
         news.append(Nnew)
     dom_bytes = float(np.mean(dom_b)) * a.steps

@@ -76,7 +76,9 @@ __device__ inline void sum_positions(const Work& w, const GT* __restrict__ grad,
                                      int p0, int cnt, int lane, float (&acc)[E]) {
   constexpr int D = LANES * E;
   constexpr int NR = (kUnit + LANES - 1) / LANES;  // positions per lane
-  constexpr int kBatch = 8;                        // gradient rows in flight (a small batch: more resident waves)
+  // gradient rows in flight: a small batch keeps more waves resident; narrow
+  // rows (<= 4 lanes) take a whole unit's rows (128 values per lane) at once
+  constexpr int kBatch = LANES <= 4 ? 128 / E : 8;
   int myref[NR];
   float mysc[NR];
 #pragma unroll
@@ -100,16 +102,14 @@ __device__ inline void sum_positions(const Work& w, const GT* __restrict__ grad,
       const int r = LANES > 1 ? __shfl(myref[q / LANES], q % LANES, LANES) : myref[q];
       ref[j] = q < cnt ? r : -1;
     }
+    uint4 raw[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j)  // every load issued before any is used
+      raw[j] = ref[j] >= 0 ? load_raw16(grad + static_cast<int64_t>(ref[j]) * D + lane * E)
+                           : make_uint4(0u, 0u, 0u, 0u);
     float x[kBatch][E];
 #pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      if (ref[j] >= 0) {
-        load_vals<GT, E>(grad + static_cast<int64_t>(ref[j]) * D + lane * E, x[j]);
-      } else {
-#pragma unroll
-        for (int k = 0; k < E; ++k) x[j][k] = 0.f;
-      }
-    }
+    for (int j = 0; j < kBatch; ++j) widen16<GT, E>(raw[j], x[j]);
     if (MODE == 1) {
 #pragma unroll
       for (int j = 0; j < kBatch; ++j) {
@@ -182,16 +182,14 @@ __device__ inline void sum_segments(const Work& w, const GT* __restrict__ grad, 
       for (int k = 1; k < K; ++k) kk += tq >= pre[k];
       kq[j] = kk;
     }
+    uint4 raw[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j)  // every load issued before any is used
+      raw[j] = ref[j] >= 0 ? load_raw16(grad + static_cast<int64_t>(ref[j]) * D + lane * E)
+                           : make_uint4(0u, 0u, 0u, 0u);
     float x[kBatch][E];
 #pragma unroll
-    for (int j = 0; j < kBatch; ++j) {
-      if (ref[j] >= 0) {
-        load_vals<GT, E>(grad + static_cast<int64_t>(ref[j]) * D + lane * E, x[j]);
-      } else {
-#pragma unroll
-        for (int e = 0; e < E; ++e) x[j][e] = 0.f;
-      }
-    }
+    for (int j = 0; j < kBatch; ++j) widen16<GT, E>(raw[j], x[j]);
     if (MODE == 1) {
 #pragma unroll
       for (int j = 0; j < kBatch; ++j) {

@@ -118,6 +118,32 @@ __device__ inline void load_vals<uint16_t, 4>(const uint16_t* __restrict__ p, fl
   v[3] = __uint_as_float(a.y & 0xFFFF0000u);
 }
 
+// The 16 bytes of a row fragment as raw bits, and their E fp32 values: a
+// batch of loads is issued as raw loads first and widened afterwards, so no
+// load waits for the one before it (a widening inside a conditional load
+// would make the compiler wait for each load in turn).
+__device__ inline uint4 load_raw16(const void* __restrict__ p) { return *reinterpret_cast<const uint4*>(p); }
+
+template <typename T, int E>
+__device__ inline void widen16(const uint4& a, float (&v)[E]);
+
+template <>
+__device__ inline void widen16<float, 4>(const uint4& a, float (&v)[4]) {
+  v[0] = __uint_as_float(a.x);
+  v[1] = __uint_as_float(a.y);
+  v[2] = __uint_as_float(a.z);
+  v[3] = __uint_as_float(a.w);
+}
+template <>
+__device__ inline void widen16<uint16_t, 8>(const uint4& a, float (&v)[8]) {
+  const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    v[2 * k] = __uint_as_float(w[k] << 16);
+    v[2 * k + 1] = __uint_as_float(w[k] & 0xFFFF0000u);
+  }
+}
+
 template <typename T, int E>
 __device__ inline void store_vals(T* __restrict__ p, const float (&v)[E]);
 
