@@ -775,6 +775,9 @@ __global__ __launch_bounds__(NT) void k_compact(TableDev t, Work w, const int64_
   const int v[5] = {cf, cc, cn, cl, cu};
   int ex[5], tot[5];
   block_excl_scan5<NT>(v, ex, tot, sh);
+  int64_t keys[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) keys[k] = f[k] >= 0 ? values[i0 + k] : 0;  // all in flight together
   int uid = pre[0] + ex[0];
   int start = pre[1] + ex[1];
   int64_t nr = pre[2] + ex[2];
@@ -787,7 +790,7 @@ __global__ __launch_bounds__(NT) void k_compact(TableDev t, Work w, const int64_
   for (int k = 0; k < 4; ++k) {
     if (f[k] < 0) continue;
     const int c = ki[k].count;
-    const int64_t key = values[i0 + k];
+    const int64_t key = keys[k];
     w.unique[uid] = key;
     int li = -1;
     if (c > kLong) {
