@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(HERE, "liboracle.so")
 OK, EINVAL, ENOMEM, EFULL, EKEY = 0, 1, 2, 3, 4
 SUM, MEAN, NONE, TAIL = 0, 1, 2, 3
 F32, BF16 = 0, 1
-ADAGRAD, ADAM, ADAMW, ADAM_TF = 0, 1, 2, 3
+ADAGRAD, ADAM, ADAMW, ADAM_TF, ADAGRAD_RW, ADAM_RW = 0, 1, 2, 3, 4, 5
 
 _lib = None
 
@@ -182,7 +182,17 @@ class Table:
 
     @property
     def nstate(self):
-        return 1 if self.opt == ADAGRAD else 2
+        """Per-element state vectors (row-wise optimizers: their vectors; the
+        row scalar is extra)."""
+        return {ADAGRAD: 1, ADAGRAD_RW: 0, ADAM_RW: 1}.get(self.opt, 2)
+
+    @property
+    def state_shape(self):
+        """Shape of one row's state: (nstate, dim), or (state elements,) for
+        the row-wise optimizers ([acc] or [m (dim) | v])."""
+        if self.opt in (ADAGRAD_RW, ADAM_RW):
+            return (self.nstate * self.dim + 1,)
+        return (self.nstate, self.dim)
 
     def size(self) -> int:
         return int(lib().or_size(self.h))
@@ -205,7 +215,7 @@ class Table:
     def read_rows(self, keys):
         k = _c(keys, np.int64)
         w = np.full((k.size, self.dim), np.nan, dtype=np.float32)
-        s = np.full((k.size, self.nstate, self.dim), np.nan, dtype=np.float32)
+        s = np.full((k.size, *self.state_shape), np.nan, dtype=np.float32)
         found = lib().or_read_rows(self.h, _p(k), k.size, _p(w), _p(s))
         return int(found), w, s
 

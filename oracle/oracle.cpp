@@ -22,8 +22,9 @@
 //                  Algorithm 1), AdamW (Adam with decoupled weight decay,
 //                  Loshchilov & Hutter 2019; the paper names SparseAdamW) or
 //                  Adam in the reordered form with epsilon-hat (Kingma & Ba
-//                  2015, end of section 2; TensorFlow's Adam) on the touched
-//                  rows only
+//                  2015, end of section 2; TensorFlow's Adam), or the
+//                  row-wise (one scalar per row) Adagrad / Adam, on the
+//                  touched rows only
 //
 // Sums and optimizer arithmetic are carried in fp64; stored rows and state
 // are fp32 (or bf16 rows, rounded to nearest even) because the storage type
@@ -45,7 +46,7 @@ namespace {
 constexpr int ST_OK = 0, ST_EINVAL = 1, ST_EFULL = 3, ST_EKEY = 4;
 constexpr int SUM = 0, MEAN = 1, NONE = 2, TAIL = 3;
 constexpr int F32 = 0, BF16 = 1;
-constexpr int ADAGRAD = 0, ADAM = 1, ADAMW = 2, ADAM_TF = 3;
+constexpr int ADAGRAD = 0, ADAM = 1, ADAMW = 2, ADAM_TF = 3, ADAGRAD_RW = 4, ADAM_RW = 5;
 constexpr int64_t KEY_EMPTY = std::numeric_limits<int64_t>::min();   // reserved
 constexpr int64_t KEY_TOMB = std::numeric_limits<int64_t>::min() + 1; // reserved
 
@@ -96,10 +97,24 @@ struct Table {
   std::vector<float> w;                        // Blocks, fp32 rows  [live, dim]
   std::vector<uint16_t> wb;                    // Blocks, bf16 rows  [live, dim]
   std::vector<float> s1, s2;                   // Adagrad acc | Adam m, v   [live, dim]
+  std::vector<float> sr;                       // row-wise Adagrad acc | row-wise Adam v  [live]
   int64_t t = 0;                               // Adam step count (table-global)
 
   int64_t live() const { return static_cast<int64_t>(idmap.size()); }
-  int nstate() const { return opt == ADAGRAD ? 1 : 2; }
+  // per-element state vectors, and whether one scalar per row follows them
+  int nvec() const { return opt == ADAGRAD ? 1 : opt == ADAGRAD_RW ? 0 : opt == ADAM_RW ? 1 : 2; }
+  bool row_scalar() const { return opt == ADAGRAD_RW || opt == ADAM_RW; }
+  bool adam_family() const { return opt != ADAGRAD && opt != ADAGRAD_RW; }
+  int state_elems() const { return nvec() * dim + (row_scalar() ? 1 : 0); }
+  // state element e of row r: [s1 (dim) | s2 (dim) | row scalar], as present
+  float get_s(int64_t r, int e) const {
+    if (e < nvec() * dim) return e < dim ? s1[r * dim + e] : s2[r * dim + e - dim];
+    return sr[r];
+  }
+  void put_s(int64_t r, int e, float v) {
+    if (e < nvec() * dim) (e < dim ? s1[r * dim + e] : s2[r * dim + e - dim]) = v;
+    else sr[r] = v;
+  }
 
   float get_w(int64_t r, int j) const {
     return row_dtype == BF16 ? bf16_to_f32(wb[r * dim + j]) : w[r * dim + j];
@@ -114,9 +129,10 @@ struct Table {
     for (int j = 0; j < dim; ++j) {
       if (row_dtype == BF16) wb.push_back(bf16_rne(vals[j]));
       else w.push_back(vals[j]);
-      s1.push_back(0.0f);
-      if (opt != ADAGRAD) s2.push_back(0.0f);
+      if (nvec() >= 1) s1.push_back(0.0f);
+      if (nvec() == 2) s2.push_back(0.0f);
     }
+    if (row_scalar()) sr.push_back(0.0f);
     return r;
   }
 };
@@ -184,7 +200,7 @@ void or_init_row(uint64_t seed, int64_t key, int dim, float lo, float hi, float*
 }
 
 void* or_create(int dim, int row_dtype, int opt, float lo, float hi, uint64_t seed, int64_t max_live) {
-  if (dim <= 0 || (row_dtype != F32 && row_dtype != BF16) || opt < ADAGRAD || opt > ADAM_TF) return nullptr;
+  if (dim <= 0 || (row_dtype != F32 && row_dtype != BF16) || opt < ADAGRAD || opt > ADAM_RW) return nullptr;
   Table* T = new Table;
   T->dim = dim;
   T->row_dtype = row_dtype;
@@ -300,24 +316,22 @@ int or_find_or_insert(void* h, const int64_t* keys, int64_t n, int64_t* rows_out
   return find_or_insert(static_cast<Table*>(h), keys, n, rows_out, n_inserted);
 }
 
-// Row contents by key (w as fp32 values; state [nstate, dim] per key).
+// Row contents by key (w as fp32 values; state_elems() state floats per key:
+// [acc] / [m | v] per element, or the row-wise [acc] / [m (dim) | v]).
 // Returns the number of keys found; absent keys leave their output untouched.
 int64_t or_read_rows(void* h, const int64_t* keys, int64_t n, float* w_out, float* state_out) {
   Table* T = static_cast<Table*>(h);
-  const int D = T->dim, S = T->nstate();
+  const int D = T->dim, S = T->state_elems();
   int64_t found = 0;
   for (int64_t i = 0; i < n; ++i) {
     auto it = T->idmap.find(keys[i]);
     if (it == T->idmap.end()) continue;
     ++found;
     const int64_t r = it->second;
-    for (int j = 0; j < D; ++j) {
+    for (int j = 0; j < D; ++j)
       if (w_out) w_out[i * D + j] = T->get_w(r, j);
-      if (state_out) {
-        state_out[(i * S + 0) * D + j] = T->s1[r * D + j];
-        if (S == 2) state_out[(i * S + 1) * D + j] = T->s2[r * D + j];
-      }
-    }
+    for (int e = 0; e < S; ++e)
+      if (state_out) state_out[i * S + e] = T->get_s(r, e);
   }
   return found;
 }
@@ -326,16 +340,13 @@ int64_t or_read_rows(void* h, const int64_t* keys, int64_t n, float* w_out, floa
 // oracle from a given table state.  w values are rounded to the row dtype.
 void or_write_rows(void* h, const int64_t* keys, int64_t n, const float* w_in, const float* state_in) {
   Table* T = static_cast<Table*>(h);
-  const int D = T->dim, S = T->nstate();
+  const int D = T->dim, S = T->state_elems();
   std::vector<float> zero(D, 0.0f);
   for (int64_t i = 0; i < n; ++i) {
     auto it = T->idmap.find(keys[i]);
     int64_t r = (it == T->idmap.end()) ? T->append(keys[i], zero.data()) : it->second;
-    for (int j = 0; j < D; ++j) {
-      T->put_w(r, j, w_in[i * D + j]);
-      T->s1[r * D + j] = state_in ? state_in[(i * S + 0) * D + j] : 0.0f;
-      if (S == 2) T->s2[r * D + j] = state_in ? state_in[(i * S + 1) * D + j] : 0.0f;
-    }
+    for (int j = 0; j < D; ++j) T->put_w(r, j, w_in[i * D + j]);
+    for (int e = 0; e < S; ++e) T->put_s(r, e, state_in ? state_in[i * S + e] : 0.0f);
   }
 }
 
@@ -446,6 +457,12 @@ int or_backward(const int64_t* offsets, int64_t bags, const int32_t* inverse, in
 //            the touched row, then the moment update and step)
 //   Adam (epsilon-hat form): the same moments; lr_t = lr * sqrt(1-b2^t) / (1-b1^t);
 //            w -= lr_t * m / (sqrt(v) + eps)
+//   Row-wise state (one scalar per row instead of one per element; the
+//   memory-saving form of embedding-table optimizers, as in FBGEMM), with
+//   ms = mean over the row of g^2:
+//   Row-wise Adagrad: acc += ms;  w -= lr * g / (sqrt(acc) + eps)
+//   Row-wise Adam:    m per element as in Adam; v = b2 v + (1-b2) ms per
+//            row;  w -= lr * (m / (1-b1^t)) / (sqrt(v / (1-b2^t)) + eps)
 // Arithmetic in fp64 from the stored fp32 state; results stored as fp32
 // state and fp32 (or bf16, via fp32 then round-to-nearest-even) rows.
 // rows[u] < 0 is skipped.  grad is fp32 [U, dim].
@@ -454,7 +471,7 @@ int or_optimizer(void* h, const int64_t* rows, int64_t U, const float* grad, dou
   Table* T = static_cast<Table*>(h);
   const int D = T->dim;
   double bc1 = 1.0, bc2 = 1.0;
-  if (T->opt != ADAGRAD) {
+  if (T->adam_family()) {
     T->t += 1;
     bc1 = 1.0 - std::pow(beta1, static_cast<double>(T->t));
     bc2 = 1.0 - std::pow(beta2, static_cast<double>(T->t));
@@ -463,6 +480,34 @@ int or_optimizer(void* h, const int64_t* rows, int64_t U, const float* grad, dou
   for (int64_t u = 0; u < U; ++u) {
     const int64_t r = rows[u];
     if (r < 0) continue;
+    if (T->row_scalar()) {
+      // one accumulator per row from the mean of the squared gradient
+      double ms = 0.0;
+      for (int j = 0; j < D; ++j) {
+        const double g = static_cast<double>(grad[u * D + j]);
+        ms += g * g;
+      }
+      ms /= static_cast<double>(D);
+      if (T->opt == ADAGRAD_RW) {
+        const double acc = static_cast<double>(T->sr[r]) + ms;
+        const double step = lr / (std::sqrt(acc) + eps);
+        for (int j = 0; j < D; ++j)
+          T->put_w(r, j, static_cast<float>(static_cast<double>(T->get_w(r, j)) -
+                                            step * static_cast<double>(grad[u * D + j])));
+        T->sr[r] = static_cast<float>(acc);
+      } else {
+        const double v = beta2 * static_cast<double>(T->sr[r]) + (1.0 - beta2) * ms;
+        const double den = std::sqrt(v / bc2) + eps;
+        for (int j = 0; j < D; ++j) {
+          const double g = static_cast<double>(grad[u * D + j]);
+          const double m = beta1 * static_cast<double>(T->s1[r * D + j]) + (1.0 - beta1) * g;
+          T->put_w(r, j, static_cast<float>(static_cast<double>(T->get_w(r, j)) - lr * (m / bc1) / den));
+          T->s1[r * D + j] = static_cast<float>(m);
+        }
+        T->sr[r] = static_cast<float>(v);
+      }
+      continue;
+    }
     for (int j = 0; j < D; ++j) {
       const double g = static_cast<double>(grad[u * D + j]);
       double w = static_cast<double>(T->get_w(r, j));

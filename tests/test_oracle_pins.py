@@ -719,3 +719,100 @@ def test_step_is_forward_backward_optimizer():
     _, wa, sa = A.read_rows(rb["unique"])
     _, wb, sb = B.read_rows(rb["unique"])
     assert np.array_equal(wa, wb) and np.array_equal(sa, sb)
+
+
+# --------------------------------------------------------------------------- row-wise state
+
+
+def test_rowwise_adagrad_dim1_matches_torch_adagrad():
+    """With one element per row the row mean of g^2 is g^2: row-wise Adagrad
+    is Adagrad (Duchi et al. 2011), here torch.optim.Adagrad over lazy steps."""
+    V = 6
+    g = np.random.default_rng(41)
+    T = O.Table(1, opt=O.ADAGRAD_RW, seed=3)
+    keys = np.arange(V, dtype=np.int64) * 7
+    _, rows, _ = T.find_or_insert(keys)
+    _, W0, _ = T.read_rows(keys)
+    p = torch.nn.Parameter(torch.from_numpy(W0.astype(np.float64)))
+    opt = torch.optim.Adagrad([p], lr=0.05, eps=1e-8, initial_accumulator_value=0.0)
+    for step in range(5):
+        touched = np.sort(g.choice(V, size=3, replace=False))
+        G = g.standard_normal((3, 1)).astype(np.float32)
+        T.optimizer(rows[touched], G, 0.05, 1e-8)
+        dense = torch.zeros(V, 1, dtype=torch.float64)
+        dense[touched] = torch.from_numpy(G.astype(np.float64))
+        p.grad = dense
+        opt.step()
+    _, W, S = T.read_rows(keys)
+    np.testing.assert_allclose(W, p.detach().numpy(), rtol=1e-6, atol=1e-8)
+    np.testing.assert_allclose(S[:, 0], opt.state[p]["sum"].numpy()[:, 0], rtol=1e-6)
+
+
+def test_rowwise_adam_dim1_matches_torch_sparse_adam():
+    V = 5
+    g = np.random.default_rng(42)
+    T = O.Table(1, opt=O.ADAM_RW, seed=4)
+    keys = np.arange(V, dtype=np.int64) + 50
+    _, rows, _ = T.find_or_insert(keys)
+    _, W0, _ = T.read_rows(keys)
+    p = torch.nn.Parameter(torch.from_numpy(W0.astype(np.float64)))
+    opt = torch.optim.SparseAdam([p], lr=1e-2, betas=(0.9, 0.999), eps=1e-8)
+    for step in range(6):
+        touched = np.sort(g.choice(V, size=2, replace=False))
+        G = g.standard_normal((2, 1)).astype(np.float32)
+        T.optimizer(rows[touched], G, 1e-2, 1e-8, 0.9, 0.999)
+        idx = torch.from_numpy(touched.astype(np.int64))[None, :]
+        p.grad = torch.sparse_coo_tensor(idx, torch.from_numpy(G.astype(np.float64)), (V, 1))
+        opt.step()
+    _, W, _ = T.read_rows(keys)
+    assert T.t == 6
+    np.testing.assert_allclose(W, p.detach().numpy(), rtol=1e-5, atol=1e-9)
+
+
+@pytest.mark.parametrize("rw,ew", [(O.ADAGRAD_RW, O.ADAGRAD), (O.ADAM_RW, O.ADAM)])
+def test_rowwise_with_constant_row_gradients_equals_elementwise(rw, ew):
+    """A gradient constant across each row has mean(g^2) = g_j^2 for every j,
+    so the row-wise and the element-wise optimizers take the same steps (a
+    dropped 1/dim or a per-element accumulator fails this at dim 8)."""
+    D, V = 8, 6
+    g = np.random.default_rng(43 + rw)
+    keys = np.arange(V, dtype=np.int64) + 700
+    A, B = O.Table(D, opt=rw, seed=5), O.Table(D, opt=ew, seed=5)
+    _, rows, _ = A.find_or_insert(keys)
+    B.find_or_insert(keys)
+    for step in range(4):
+        touched = np.sort(g.choice(V, size=4, replace=False))
+        G = np.repeat(g.standard_normal((4, 1)), D, axis=1).astype(np.float32)
+        A.optimizer(rows[touched], G, 0.02, 1e-8, 0.9, 0.999)
+        B.optimizer(rows[touched], G, 0.02, 1e-8, 0.9, 0.999)
+    _, WA, SA = A.read_rows(keys)
+    _, WB, SB = B.read_rows(keys)
+    np.testing.assert_allclose(WA, WB, rtol=1e-6, atol=1e-9)
+    if rw == O.ADAGRAD_RW:
+        np.testing.assert_allclose(SA[:, 0], SB[:, 0, 0], rtol=1e-6)
+    else:
+        np.testing.assert_allclose(SA[:, :D], SB[:, 0], rtol=1e-6)    # m per element
+        np.testing.assert_allclose(SA[:, D], SB[:, 1, 0], rtol=1e-6)  # v per row
+
+
+def test_rowwise_first_step_closed_form_and_layout():
+    D = 4
+    G = np.array([[3.0, -4.0, 0.0, 0.0]], dtype=np.float32)      # mean g^2 = 25 / 4
+    T = O.Table(D, opt=O.ADAGRAD_RW, seed=6)
+    _, rows, _ = T.find_or_insert(np.array([9], dtype=np.int64))
+    _, w0, s0 = T.read_rows(np.array([9], dtype=np.int64))
+    assert s0.shape == (1, 1) and s0[0, 0] == 0
+    T.optimizer(rows, G, 0.1, 0.0)
+    _, w1, s1 = T.read_rows(np.array([9], dtype=np.int64))
+    assert s1[0, 0] == 6.25
+    np.testing.assert_allclose(w1, w0.astype(np.float64) - 0.1 * G / 2.5, rtol=1.2e-7, atol=1e-12)  # fp32 storage
+    # row-wise Adam keeps [m (dim) | v] and its first step is lr * g / sqrt(mean g^2)
+    T = O.Table(D, opt=O.ADAM_RW, seed=6)
+    _, rows, _ = T.find_or_insert(np.array([9], dtype=np.int64))
+    _, w0, s0 = T.read_rows(np.array([9], dtype=np.int64))
+    assert s0.shape == (1, D + 1)
+    T.optimizer(rows, G, 0.1, 0.0, 0.9, 0.999)
+    _, w1, s1 = T.read_rows(np.array([9], dtype=np.int64))
+    np.testing.assert_allclose(s1[0, :D], 0.1 * G[0], rtol=1e-6)
+    np.testing.assert_allclose(s1[0, D], 0.001 * 6.25, rtol=1e-6)
+    np.testing.assert_allclose(w1, w0.astype(np.float64) - 0.1 * G / 2.5, rtol=1e-6, atol=1e-12)
