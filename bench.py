@@ -28,6 +28,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
+OPTIMIZERS = ["adagrad", "adam", "adamw", "adam-eps-hat", "adagrad-rowwise", "adam-rowwise"]
 METRIC = "embedding step IDs/sec (fwd+bwd+opt) and achieved HBM GB/s vs peak, 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
 
@@ -44,7 +45,7 @@ def parse():
     ap.add_argument("--pipelined", action="store_true",
                     help="run the next batch's lookup_prepare on a second stream while the current batch pools and "
                          "runs its backward (default: one stream)")
-    ap.add_argument("--optimizer", choices=["adagrad", "adam", "adamw", "adam-eps-hat"], default=None,
+    ap.add_argument("--optimizer", choices=OPTIMIZERS, default=None,
                     help="run the workload with another row-sparse optimizer (adamw: weight decay 0.01)")
     ap.add_argument("--gen-workers", type=int, default=16,
                     help="processes drawing the input batches before the GPU is touched (1: in-process, e.g. under "
@@ -89,8 +90,9 @@ def kernel_source_hash(kernel: str) -> str:
 
 
 def row_bytes(w):
+    """Row bytes of w and of its optimizer state (the state's fp32 elements)."""
     R = w.dim * (2 if w.row_dtype == 1 else 4)
-    S = w.dim * 4 * (1 if w.opt == 0 else 2)
+    S = 4 * {0: w.dim, 4: 1, 5: w.dim + 1}.get(w.opt, 2 * w.dim)
     return R, S
 
 
@@ -421,7 +423,7 @@ def main():
 
     w = W.workload(a.workload)
     if a.optimizer:
-        w.opt = ["adagrad", "adam", "adamw", "adam-eps-hat"].index(a.optimizer)
+        w.opt = OPTIMIZERS.index(a.optimizer)
         if w.opt == 2:
             w.weight_decay = 0.01
     nsteps = a.warmup + a.steps

@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define RS_VERSION 5
+#define RS_VERSION 6
 
 typedef enum {
   RS_OK = 0,
@@ -62,7 +62,8 @@ typedef enum {
 typedef enum { RS_POOL_SUM = 0, RS_POOL_MEAN = 1, RS_POOL_NONE = 2, RS_POOL_TILE_TAIL = 3 } rs_pool;
 typedef enum { RS_F32 = 0, RS_BF16 = 1 } rs_dtype;
 /* Row-sparse optimizers (every one keeps fp32 state beside the row: Adagrad
- * one accumulator per element, the Adam family two moments per element).
+ * one accumulator per element, the Adam family two moments per element; the
+ * row-wise forms one scalar per row in place of a per-element vector).
  *  RS_ADAGRAD: Duchi et al. 2011.
  *  RS_ADAM:    Kingma & Ba 2015, Algorithm 1 (the paper's SparseAdam).
  *  RS_ADAMW:   Adam with decoupled weight decay (Loshchilov & Hutter 2019;
@@ -70,8 +71,18 @@ typedef enum { RS_F32 = 0, RS_BF16 = 1 } rs_dtype;
  *              lr * weight_decay * w, then takes the Adam step.
  *  RS_ADAM_TF: Adam in the reordered form with epsilon-hat (Kingma & Ba
  *              2015, end of section 2; the form TensorFlow implements, which
- *              the paper's TF-compatible optimizers follow). */
-typedef enum { RS_ADAGRAD = 0, RS_ADAM = 1, RS_ADAMW = 2, RS_ADAM_TF = 3 } rs_optim;
+ *              the paper's TF-compatible optimizers follow).
+ *  RS_ADAGRAD_ROWWISE: one accumulator per row, fed the row mean of g^2
+ *              (the memory-saving form of embedding-table Adagrad).
+ *  RS_ADAM_ROWWISE: m per element, v per row from the row mean of g^2. */
+typedef enum {
+  RS_ADAGRAD = 0,
+  RS_ADAM = 1,
+  RS_ADAMW = 2,
+  RS_ADAM_TF = 3,
+  RS_ADAGRAD_ROWWISE = 4,
+  RS_ADAM_ROWWISE = 5
+} rs_optim;
 
 typedef struct rs_table rs_table; /* opaque, library-owned */
 typedef void* rs_stream;          /* hipStream_t */
@@ -189,8 +200,10 @@ rs_status ht_export(rs_table* t, int64_t* keys, int64_t* rows, int64_t cap, int6
                     rs_stream stream);
 
 /* Read rows by row id: w_out [n, D] fp32 (bf16 rows widened exactly),
- * state_out [n, S, D] fp32 with S = 1 (Adagrad accumulator) or 2 (Adam m, v);
- * either may be NULL.  Rows outside [0, live) give NaN. */
+ * state_out [n, SE] fp32, the row's state in storage order: Adagrad [acc (D)]
+ * (SE = D), the Adam family [m (D) | v (D)] (SE = 2D), row-wise Adagrad
+ * [acc] (SE = 1), row-wise Adam [m (D) | v] (SE = D + 1); either may be NULL.
+ * Rows outside [0, live) give NaN. */
 rs_status ht_read_rows(rs_table* t, const int64_t* rows, int64_t n, float* w_out, float* state_out,
                        rs_stream stream);
 
@@ -264,6 +277,10 @@ rs_status lookup_pool_bwd(rs_table* t, const rs_ctx* ctx, const void* grad_out, 
  *   AdamW:   w -= lr * weight_decay * w, then the Adam step
  *   Adam (epsilon-hat): the same moments;  w -= lr_t * m / (sqrt(v) + eps)
  *            with lr_t = lr * sqrt(1-b2^t) / (1-b1^t)
+ *   Row-wise, with ms = (sum over the row of g*g) / dim:
+ *     Adagrad: acc += ms;  w -= lr * g / (sqrt(acc) + eps)
+ *     Adam:    t += 1;  m = b1*m + (1-b1)*g;  v = b2*v + (1-b2)*ms (per row);
+ *              w -= lr * (m/(1-b1^t)) / (sqrt(v/(1-b2^t)) + eps)
  * Arithmetic in fp32; bf16 rows are widened, updated, and rounded to nearest
  * even.  grad_unique [n, D] fp32 as written by lookup_pool_bwd. */
 rs_status sparse_opt_step(rs_table* t, const rs_ctx* ctx, const float* grad_unique,

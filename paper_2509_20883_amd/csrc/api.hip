@@ -251,7 +251,12 @@ struct rs_table {
     if (custom) a.free(p, a.ctx);
     else (void)hipFree(p);
   }
-  int nstate() const { return d.optimizer == RS_ADAGRAD ? 1 : 2; }
+  // per-element state vectors, the row scalar of the row-wise optimizers
+  int nstate() const {
+    return d.optimizer == RS_ADAGRAD ? 1 : d.optimizer == RS_ADAGRAD_ROWWISE ? 0 : d.optimizer == RS_ADAM_ROWWISE ? 1 : 2;
+  }
+  int rowscalar() const { return d.optimizer == RS_ADAGRAD_ROWWISE || d.optimizer == RS_ADAM_ROWWISE ? 1 : 0; }
+  int state_elems() const { return nstate() * d.dim + rowscalar(); }
   int wbytes() const { return d.row_dtype == RS_BF16 ? 2 : 4; }
 
   TableDev dev() const {
@@ -264,6 +269,7 @@ struct rs_table {
     t.dim = d.dim;
     t.row_dtype = d.row_dtype;
     t.nstate = nstate();
+    t.rowscalar = rowscalar();
     t.seed = d.seed;
     t.lo = d.init_lo;
     t.span = d.init_hi - d.init_lo;  // fp32 subtraction
@@ -437,7 +443,7 @@ OptArgs make_opt(rs_table* t, const rs_opt_params* p) {
   o.bc2 = 1.0f;
   o.wdlr = static_cast<float>(p->lr * p->weight_decay);
   o.lrt = static_cast<float>(p->lr);
-  if (o.opt != RS_ADAGRAD) {
+  if (o.opt != RS_ADAGRAD && o.opt != RS_ADAGRAD_ROWWISE) {  // the Adam family
     t->adam_t += 1;
     const double bc1 = 1.0 - std::pow(p->beta1, static_cast<double>(t->adam_t));
     const double bc2 = 1.0 - std::pow(p->beta2, static_cast<double>(t->adam_t));
@@ -471,7 +477,7 @@ rs_status ht_create(const rs_table_desc* d, const rs_allocator* a, rs_stream str
   *out = nullptr;
   if (!valid_dim(d->dim)) return fail(RS_EINVAL, "dim must be 8, 16, 32, 64, 128 or 256");
   if (d->row_dtype != RS_F32 && d->row_dtype != RS_BF16) return fail(RS_EINVAL, "bad row_dtype");
-  if (d->optimizer < RS_ADAGRAD || d->optimizer > RS_ADAM_TF) return fail(RS_EINVAL, "bad optimizer");
+  if (d->optimizer < RS_ADAGRAD || d->optimizer > RS_ADAM_ROWWISE) return fail(RS_EINVAL, "bad optimizer");
   if (!is_pow2(d->capacity_slots) || d->capacity_slots < 16 || d->capacity_slots > (int64_t(1) << 40))
     return fail(RS_EINVAL, "capacity_slots must be a power of two in [16, 2^40]");
   if (!(d->max_load > 0.0f && d->max_load <= 0.9f)) return fail(RS_EINVAL, "max_load must be in (0, 0.9]");
@@ -491,7 +497,8 @@ rs_status ht_create(const rs_table_desc* d, const rs_allocator* a, rs_stream str
     delete t;
     return fail(RS_EHIP, "hipGetDevice failed");
   }
-  t->stride = static_cast<int64_t>(d->dim) * (t->wbytes() + 4 * t->nstate());
+  t->stride = static_cast<int64_t>(d->dim) * t->wbytes() + 4 * t->state_elems();
+  t->stride = (t->stride + 15) / 16 * 16;  // 16-byte row fragments
   t->cap = d->capacity_slots;
   t->limit = static_cast<int64_t>(std::floor(static_cast<double>(d->max_load) * static_cast<double>(t->cap)));
   t->slots = static_cast<Slot*>(t->alloc(sizeof(Slot) * static_cast<size_t>(t->cap)));
@@ -717,7 +724,7 @@ rs_status ht_read_rows(rs_table* t, const int64_t* rows, int64_t n, float* w_out
     // no Blocks yet: every row is out of range
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (n > 0 && w_out) RS_HIP(hipMemsetAsync(w_out, 0xFF, sizeof(float) * n * t->d.dim, s));
-    if (n > 0 && state_out) RS_HIP(hipMemsetAsync(state_out, 0xFF, sizeof(float) * n * t->d.dim * t->nstate(), s));
+    if (n > 0 && state_out) RS_HIP(hipMemsetAsync(state_out, 0xFF, sizeof(float) * n * t->state_elems(), s));
     return RS_OK;
   }
   RS_HIP(launch_read_rows(t->dev(), rows, n, w_out, state_out, static_cast<hipStream_t>(stream)));

@@ -25,23 +25,62 @@
 
 namespace rs {
 
-// Optimizer state of E consecutive elements [lane*E, lane*E + E) of a row.
+// Sum of v over the LANES lanes of a lane group (every lane gets it).
+template <int LANES>
+__device__ inline float group_sum(float v) {
+#pragma unroll
+  for (int d = LANES / 2; d >= 1; d >>= 1) v += __shfl_xor(v, d, LANES);
+  return v;
+}
+
+// Optimizer state of E consecutive elements [lane*E, lane*E + E) of a row,
+// and the row's state scalar (row-wise optimizers).
 template <typename WT, int E>
 struct RowFrag {
-  float w[E], s1[E], s2[E];
-  __device__ inline void load(const uint8_t* row, int lane, int dim, int nstate) {
+  float w[E], s1[E], s2[E], sr;
+  __device__ inline void load(const uint8_t* row, int lane, int dim, int nstate, int rowscalar) {
     load_vals<WT, E>(reinterpret_cast<const WT*>(row) + lane * E, w);
-    const float* p = reinterpret_cast<const float*>(row + static_cast<int64_t>(dim) * sizeof(WT)) + lane * E;
-    load_vals<float, E>(p, s1);
-    if (nstate == 2) load_vals<float, E>(p + dim, s2);
+    const float* base = reinterpret_cast<const float*>(row + static_cast<int64_t>(dim) * sizeof(WT));
+    if (nstate >= 1) load_vals<float, E>(base + lane * E, s1);
+    if (nstate == 2) load_vals<float, E>(base + dim + lane * E, s2);
+    sr = rowscalar ? base[nstate * dim] : 0.f;  // the same word for the whole lane group
   }
   // Adagrad: acc += g^2; w -= lr g / (sqrt(acc) + eps).
   // Adam:    m = b1 m + (1-b1) g; v = b2 v + (1-b2) g^2; w -= lr (m/bc1) / (sqrt(v/bc2) + eps).
   // AdamW:   w -= (lr wd) w, then the Adam step.
   // Adam, epsilon-hat form: the same moments; w -= lr_t m / (sqrt(v) + eps).
+  // Row-wise (ms = the row mean of g^2, summed over the lane group):
+  //   Adagrad: acc += ms; w -= lr g / (sqrt(acc) + eps)
+  //   Adam:    m per element as above; v = b2 v + (1-b2) ms per row;
+  //            w -= lr (m/bc1) / (sqrt(v/bc2) + eps)
+  // All lanes of the group call it together (the row-wise sum shuffles).
+  template <int LANES>
   __device__ inline void update_store(uint8_t* row, int lane, int dim, const float (&g)[E], const OptArgs& o) {
-    float* p = reinterpret_cast<float*>(row + static_cast<int64_t>(dim) * sizeof(WT)) + lane * E;
-    if (o.opt == 0) {
+    float* base = reinterpret_cast<float*>(row + static_cast<int64_t>(dim) * sizeof(WT));
+    float* p = base + lane * E;
+    if (o.opt >= 4) {
+      float ss = 0.f;
+#pragma unroll
+      for (int k = 0; k < E; ++k) ss += g[k] * g[k];
+      const float ms = group_sum<LANES>(ss) / static_cast<float>(dim);
+      if (o.opt == 4) {
+        sr = sr + ms;
+        const float step = o.lr / (__builtin_sqrtf(sr) + o.eps);
+#pragma unroll
+        for (int k = 0; k < E; ++k) w[k] = w[k] - step * g[k];
+        if (lane == 0) base[0] = sr;
+      } else {
+        sr = o.beta2 * sr + o.omb2 * ms;
+        const float den = __builtin_sqrtf(sr / o.bc2) + o.eps;
+#pragma unroll
+        for (int k = 0; k < E; ++k) {
+          s1[k] = o.beta1 * s1[k] + o.omb1 * g[k];
+          w[k] = w[k] - o.lr * (s1[k] / o.bc1) / den;
+        }
+        store_vals<float, E>(p, s1);
+        if (lane == 0) base[dim] = sr;
+      }
+    } else if (o.opt == 0) {
 #pragma unroll
       for (int k = 0; k < E; ++k) {
         s1[k] = s1[k] + g[k] * g[k];
@@ -240,7 +279,7 @@ __device__ inline void bwd_short(const TableDev& t, const Work& w, const int64_t
     if (FUSED) {
 #pragma unroll
       for (int k = 0; k < K; ++k)  // in flight while the gradients are read
-        if (act[k] && sg[k].row >= 0) fr[k].load(t.store.row(sg[k].row), lane, D, t.nstate);
+        if (act[k] && sg[k].row >= 0) fr[k].load(t.store.row(sg[k].row), lane, D, t.nstate, t.rowscalar);
     }
     float acc[K][E];
 #pragma unroll
@@ -252,7 +291,7 @@ __device__ inline void bwd_short(const TableDev& t, const Work& w, const int64_t
     for (int k = 0; k < K; ++k) {
       if (!act[k]) continue;
       if (FUSED) {
-        if (sg[k].row >= 0) fr[k].update_store(t.store.row(sg[k].row), lane, D, acc[k], o);
+        if (sg[k].row >= 0) fr[k].template update_store<LANES>(t.store.row(sg[k].row), lane, D, acc[k], o);
       } else {
         store_vals<float, E>(grad_unique + (u0 + k) * D + lane * E, acc[k]);
       }
@@ -316,7 +355,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_long_finish(TableDev t, Work w, 
     uint8_t* rp = nullptr;
     if (FUSED && grp == 0 && sg.row >= 0) {
       rp = t.store.row(sg.row);
-      fr.load(rp, lane, D, t.nstate);  // in flight while the partial rows are read
+      fr.load(rp, lane, D, t.nstate, t.rowscalar);  // in flight while the partial rows are read
     }
     float acc[E];
 #pragma unroll
@@ -347,7 +386,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_long_finish(TableDev t, Work w, 
 #pragma unroll
       for (int q = 0; q < E; ++q) acc[q] = red[0][lane * E + q];
       if (FUSED) {
-        if (rp) fr.update_store(rp, lane, D, acc, o);
+        if (rp) fr.template update_store<LANES>(rp, lane, D, acc, o);
       } else {
         store_vals<float, E>(grad_unique + static_cast<int64_t>(u) * D + lane * E, acc);
       }
@@ -431,10 +470,10 @@ __global__ __launch_bounds__(kBlock) void k_opt(TableDev t, Work w, const float*
     if (r < 0) continue;
     uint8_t* rp = t.store.row(r);
     RowFrag<WT, E> fr;
-    fr.load(rp, lane, D, t.nstate);
+    fr.load(rp, lane, D, t.nstate, t.rowscalar);
     float g[E];
     load_vals<float, E>(grad_unique + u * D + lane * E, g);
-    fr.update_store(rp, lane, D, g, o);
+    fr.template update_store<LANES>(rp, lane, D, g, o);
   }
 }
 

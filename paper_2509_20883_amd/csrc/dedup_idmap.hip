@@ -1057,8 +1057,11 @@ __global__ __launch_bounds__(kBlock) void k_read_rows(TableDev t, const int64_t*
       w_out[idx] = v;
     }
     if (state_out) {
+      // state_elems floats per row ([s0 | s1 | row scalar], as present); the
+      // thread of element j copies state floats j, j + dim, ...
+      const int se = t.nstate * t.dim + t.rowscalar;
       const float* sp = ok ? reinterpret_cast<const float*>(rp + static_cast<int64_t>(t.dim) * (t.row_dtype ? 2 : 4)) : nullptr;
-      for (int q = 0; q < t.nstate; ++q) state_out[(i * t.nstate + q) * t.dim + j] = ok ? sp[q * t.dim + j] : __builtin_nanf("");
+      for (int q = j; q < se; q += t.dim) state_out[i * se + q] = ok ? sp[q] : __builtin_nanf("");
     }
   }
 }

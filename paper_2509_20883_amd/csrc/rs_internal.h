@@ -130,7 +130,8 @@ struct alignas(16) Slot {
 
 // Blocks: physical chunks mapped back to back into one reserved virtual
 // range, so rows never move and row r is at base + r * stride; a row is
-// [w: D x row dtype | state0: D x fp32 | state1: D x fp32 (Adam)].
+// [w: D x row dtype | state0: D x fp32 | state1: D x fp32 (Adam) | row
+// scalar (row-wise optimizers)], padded to 16 bytes.
 struct RowStore {
   uint8_t* base;
   int64_t stride;  // bytes per row
@@ -144,7 +145,8 @@ struct TableDev {
   int64_t* scal;  // kT* scalars
   int dim;
   int row_dtype;  // 0 f32, 1 bf16
-  int nstate;     // 1 or 2
+  int nstate;     // per-element fp32 state vectors after w (0, 1 or 2)
+  int rowscalar;  // 1: one fp32 state scalar per row follows them (row-wise optimizers)
   uint64_t seed;
   float lo, span;  // init: fma(u, span, lo)
 };
@@ -229,7 +231,7 @@ struct Work {
 };
 
 struct OptArgs {
-  int opt;  // 0 adagrad, 1 adam, 2 adamw, 3 adam (epsilon-hat form)
+  int opt;  // 0 adagrad, 1 adam, 2 adamw, 3 adam (epsilon-hat form), 4 row-wise adagrad, 5 row-wise adam
   float lr, eps, beta1, beta2, omb1, omb2, bc1, bc2;  // omb = 1 - beta, all derived in double
   float wdlr;  // lr * weight_decay (adamw)
   float lrt;   // lr * sqrt(1 - beta2^t) / (1 - beta1^t) (epsilon-hat form)

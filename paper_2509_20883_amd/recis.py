@@ -24,7 +24,7 @@ OK, EINVAL, ENOMEM, EFULL, EKEY, EHIP = 0, 1, 2, 3, 4, 5
 STATUS_NAMES = {0: "RS_OK", 1: "RS_EINVAL", 2: "RS_ENOMEM", 3: "RS_EFULL", 4: "RS_EKEY", 5: "RS_EHIP"}
 SUM, MEAN, NONE, TAIL = 0, 1, 2, 3
 F32, BF16 = 0, 1
-ADAGRAD, ADAM, ADAMW, ADAM_TF = 0, 1, 2, 3
+ADAGRAD, ADAM, ADAMW, ADAM_TF, ADAGRAD_RW, ADAM_RW = 0, 1, 2, 3, 4, 5
 # kernel ids of rs_set_kernel_events ("occ" and "init_rows" bracket the same
 # launch; "bwd_long" brackets the hot-key unit sums and their finish)
 KERNELS = {"tile_dedup": 0, "partition": 1, "compact_insert": 2, "init_rows": 3, "pool": 4,
@@ -241,7 +241,10 @@ class Table:
         _check(lib().ht_create(C.byref(d), None, _stream(), C.byref(h)))
         self.h = h
         self.dim, self.row_dtype, self.optimizer = dim, row_dtype, optimizer
-        self.nstate = 1 if optimizer == ADAGRAD else 2
+        # per-element state vectors; the row-wise optimizers add one scalar per row
+        self.nstate = {ADAGRAD: 1, ADAGRAD_RW: 0, ADAM_RW: 1}.get(optimizer, 2)
+        self.state_shape = ((self.nstate * dim + 1,) if optimizer in (ADAGRAD_RW, ADAM_RW)
+                            else (self.nstate, dim))
         self.device = torch.device("cuda", torch.cuda.current_device())
 
     def close(self):
@@ -299,7 +302,7 @@ class Table:
     def read_rows(self, rows: torch.Tensor) -> Tuple[torch.Tensor, torch.Tensor]:
         r = _dev(rows, torch.int64)
         w = torch.empty(r.numel(), self.dim, dtype=torch.float32, device=r.device)
-        s = torch.empty(r.numel(), self.nstate, self.dim, dtype=torch.float32, device=r.device)
+        s = torch.empty(r.numel(), *self.state_shape, dtype=torch.float32, device=r.device)
         _check(lib().ht_read_rows(self.h, _ptr(r), r.numel(), _ptr(w), _ptr(s), _stream()))
         return w, s
 

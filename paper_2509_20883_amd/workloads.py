@@ -149,7 +149,7 @@ def padded(mode: int) -> bool:
     return mode in (NONE, TAIL)
 
 F32, BF16 = 0, 1
-ADAGRAD, ADAM, ADAMW, ADAM_TF = 0, 1, 2, 3
+ADAGRAD, ADAM, ADAMW, ADAM_TF, ADAGRAD_RW, ADAM_RW = 0, 1, 2, 3, 4, 5
 
 
 @dataclasses.dataclass
@@ -431,7 +431,7 @@ def prepop_count(w: Workload) -> int:
 def describe(w: Workload) -> dict:
     return {"workload": w.name, "batch": w.batch, "features": w.n_features, "dim": w.dim,
             "row_dtype": "bf16" if w.row_dtype == BF16 else "f32",
-            "optimizer": ["adagrad", "adam", "adamw", "adam-eps-hat"][w.opt],
+            "optimizer": ["adagrad", "adam", "adamw", "adam-eps-hat", "adagrad-rowwise", "adam-rowwise"][w.opt],
             "pooling": ["sum", "mean", "none", "tile-tail"][w.mode], "pad_len": w.pad_len, "zipf_s": w.zipf_s,
             "vocab_total": int(sum(w.vocab)) if w.vocab else int(w.pool0), "mini": w.mini}
 

@@ -85,7 +85,35 @@ def opt_bounds(opt, row_dtype, w0, s0, g, dg, lr, eps, b1, b2, t, w_ref, wd=0.0)
     w0, g, dg, w_ref = (np.asarray(x, f) for x in (w0, g, dg, w_ref))
     s0 = np.asarray(s0, f)
     ag = np.abs(g)
-    if opt == O.ADAGRAD:
+    if opt in (O.ADAGRAD_RW, O.ADAM_RW):
+        # the row mean of g^2: an fp32 tree sum over the row (a few roundings
+        # per level) plus the gradient's own uncertainty
+        D = g.shape[1]
+        ms = (g * g).mean(axis=1)
+        d_ms = 4e-6 * ms + (2 * ag * dg + dg * dg).mean(axis=1) + 1e-37
+        if opt == O.ADAGRAD_RW:
+            acc1 = s0[:, 0] + ms
+            b_acc = 1e-6 * acc1 + d_ms
+            sq = np.sqrt(acc1)
+            dsq = np.minimum(b_acc / np.maximum(2 * sq, 1e-30), np.sqrt(b_acc))
+            den = (sq + eps)[:, None]
+            upd = lr * ag / den
+            d_upd = lr * (dg / den + ag * dsq[:, None] / den ** 2) + 1e-6 * upd
+            b_state = b_acc[:, None]
+        else:
+            bc1, bc2 = 1.0 - b1 ** t, 1.0 - b2 ** t
+            m1 = b1 * s0[:, :D] + (1 - b1) * g
+            v1 = b2 * s0[:, D] + (1 - b2) * ms
+            b_m = 1e-6 * (b1 * np.abs(s0[:, :D]) + (1 - b1) * ag) + (1 - b1) * dg + 1e-37
+            b_v = 1e-6 * (b2 * s0[:, D] + (1 - b2) * ms) + (1 - b2) * d_ms
+            sq = np.sqrt(v1 / bc2)
+            dsq = np.minimum((b_v / bc2) / np.maximum(2 * sq, 1e-30), np.sqrt(b_v / bc2))
+            den = (sq + eps)[:, None]
+            mh = np.abs(m1) / bc1
+            upd = lr * mh / den
+            d_upd = lr * ((b_m / bc1) / den + mh * dsq[:, None] / den ** 2) + 1e-6 * upd
+            b_state = np.concatenate([b_m, b_v[:, None]], axis=1)
+    elif opt == O.ADAGRAD:
         acc1 = s0[:, 0] + g * g
         b_acc = 1e-6 * acc1 + 2 * ag * dg + dg * dg + 1e-37
         sq = np.sqrt(acc1)

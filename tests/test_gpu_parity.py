@@ -202,11 +202,13 @@ def _variant(opt, row_dtype):
 
 
 @pytest.mark.parametrize("opt,row_dtype", [(O.ADAMW, O.F32), (O.ADAMW, O.BF16), (O.ADAM_TF, O.F32),
-                                           (O.ADAM_TF, O.BF16)])
+                                           (O.ADAM_TF, O.BF16), (O.ADAGRAD_RW, O.F32), (O.ADAGRAD_RW, O.BF16),
+                                           (O.ADAM_RW, O.F32), (O.ADAM_RW, O.BF16)])
 def test_optimizer_variants_step_parity(opt, row_dtype):
-    """AdamW (decoupled weight decay) and Adam in the epsilon-hat form: step
-    parity over three steps (stage-wise, two-call path), then the fused
-    backward + optimizer against the two calls."""
+    """AdamW (decoupled weight decay), Adam in the epsilon-hat form and the
+    row-wise (one scalar per row) Adagrad and Adam: step parity over three
+    steps (stage-wise, two-call path), then the fused backward + optimizer
+    against the two calls."""
     w = _variant(opt, row_dtype)
     _log("optimizer variant", opt, row_dtype)
     gt, ot = P.gpu_table(w), P.oracle_table(w)
@@ -214,6 +216,27 @@ def test_optimizer_variants_step_parity(opt, row_dtype):
     for step in range(3):
         b = W.make_batch(w, step)
         P.run_step_parity(w, gt, ot, b, W.make_grad(w, b, step), step)
+    gt.check()
+    gt.close()
+    b = W.make_batch(w, 0)
+    wa, sa, wb, sb, bounds = _fused_vs_unfused(w, b, W.make_grad(w, b, 0))
+    P.assert_opt_close(wb, sb, wa, sa, bounds, what="fused vs unfused")
+
+
+@pytest.mark.parametrize("k,opt", [(0, O.ADAGRAD_RW), (3, O.ADAM_RW), (2, O.ADAGRAD_RW), (5, O.ADAM_RW)])
+def test_rowwise_optimizers_across_row_widths(k, opt):
+    """Row-wise state on rows of 2 to 16 lanes (dim 16 fp32, dim 128 bf16
+    padded, dim 32 bf16 mean, dim 16 tail tile): the row sum of g^2 crosses
+    the whole lane group, in the short-key, hot-key and two-call paths."""
+    w = W.workload(k, mini=(k != 0))
+    w.opt = opt
+    _log("row-wise", w.name, opt)
+    gt, ot = P.gpu_table(w), P.oracle_table(w)
+    P.prepopulate(w, gt, ot)
+    for step in range(2):
+        b = W.make_batch(w, step)
+        grad = W.make_grad(w, b, step, nan_in_masked=(w.mode in (O.NONE, O.TAIL)))
+        P.run_step_parity(w, gt, ot, b, grad, step)
     gt.check()
     gt.close()
     b = W.make_batch(w, 0)
