@@ -56,6 +56,12 @@ def lib():
         L.or_bucketize.argtypes = [p, p, i32, p, p, p]
         L.or_mod.restype = i32
         L.or_mod.argtypes = [p, p, i32, p, p]
+        L.or_evict.restype = i64
+        L.or_evict.argtypes = [p, C.c_uint32]
+        L.or_rows_allocated.restype = i64
+        L.or_rows_allocated.argtypes = [p]
+        L.or_clock.restype = C.c_uint32
+        L.or_clock.argtypes = [p]
         L.or_find_or_insert.restype = i32
         L.or_find_or_insert.argtypes = [p, p, i64, p, p]
         L.or_read_rows.restype = i64
@@ -196,6 +202,17 @@ class Table:
 
     def size(self) -> int:
         return int(lib().or_size(self.h))
+
+    def evict(self, max_age: int) -> int:
+        """Remove the keys not looked up in the last max_age calls (age > max_age)."""
+        return int(lib().or_evict(self.h, max_age & 0xFFFFFFFF))
+
+    def rows_allocated(self) -> int:
+        return int(lib().or_rows_allocated(self.h))
+
+    @property
+    def clock(self) -> int:
+        return int(lib().or_clock(self.h))
 
     @property
     def t(self) -> int:

@@ -11,8 +11,11 @@
 // Operators": dedup in ids partition, sum/mean reduction, gather, scatter):
 //
 //   dedup          unique keys in first-occurrence order + inverse index
-//   find-or-insert IDMap key -> row; a missing key gets the next row and a
-//                  deterministic initial value derived from (seed, key)
+//   find-or-insert IDMap key -> row; a missing key gets a free row (or the
+//                  next new one) and a deterministic initial value derived
+//                  from (seed, key)
+//   eviction       keys not looked up for more than a given number of calls
+//                  leave the table; their rows are reused
 //   forward        per bag: sum / mean of its rows, or a padded copy
 //   backward       per unique key: sum of the upstream gradients of every
 //                  occurrence (scaled by 1/len for mean)
@@ -99,6 +102,15 @@ struct Table {
   std::vector<float> s1, s2;                   // Adagrad acc | Adam m, v   [live, dim]
   std::vector<float> sr;                       // row-wise Adagrad acc | row-wise Adam v  [live]
   int64_t t = 0;                               // Adam step count (table-global)
+  // Eviction of stale features (Embedding Engine): every lookup call
+  // advances the clock; a row remembers its key and the clock of the last
+  // call that looked it up.  Freed rows form a stack that new keys take
+  // from (top first) before new rows are added.
+  int64_t nrows = 0;                           // rows ever allocated
+  std::vector<int64_t> row_key;                // key of each row (KEY_EMPTY: free)
+  std::vector<uint32_t> row_seen;              // clock of its last lookup
+  std::vector<int64_t> free_stack;             // free rows
+  uint32_t clock = 0;
 
   int64_t live() const { return static_cast<int64_t>(idmap.size()); }
   // per-element state vectors, and whether one scalar per row follows them
@@ -124,8 +136,10 @@ struct Table {
     else w[r * dim + j] = v;
   }
   int64_t append(int64_t key, const float* vals) {
-    const int64_t r = live();
+    const int64_t r = nrows++;
     idmap.emplace(key, r);
+    row_key.push_back(key);
+    row_seen.push_back(clock);
     for (int j = 0; j < dim; ++j) {
       if (row_dtype == BF16) wb.push_back(bf16_rne(vals[j]));
       else w.push_back(vals[j]);
@@ -133,6 +147,18 @@ struct Table {
       if (nvec() == 2) s2.push_back(0.0f);
     }
     if (row_scalar()) sr.push_back(0.0f);
+    return r;
+  }
+  // A new key's row: the top of the free stack (re-initialised), else a new one.
+  int64_t take_row(int64_t key, const float* vals) {
+    if (free_stack.empty()) return append(key, vals);
+    const int64_t r = free_stack.back();
+    free_stack.pop_back();
+    idmap.emplace(key, r);
+    row_key[r] = key;
+    row_seen[r] = clock;
+    for (int j = 0; j < dim; ++j) put_w(r, j, vals[j]);
+    for (int e = 0; e < state_elems(); ++e) put_s(r, e, 0.0f);
     return r;
   }
 };
@@ -173,6 +199,7 @@ int find_or_insert(Table* T, const int64_t* keys, int64_t n, int64_t* rows, int6
     auto it = T->idmap.find(keys[i]);
     if (it != T->idmap.end()) {
       rows[i] = it->second;
+      T->row_seen[it->second] = T->clock;
       continue;
     }
     if (T->max_live >= 0 && T->live() >= T->max_live) {
@@ -181,7 +208,7 @@ int find_or_insert(Table* T, const int64_t* keys, int64_t n, int64_t* rows, int6
       continue;
     }
     init_row(T->seed, keys[i], T->dim, T->lo, T->hi, tmp.data());
-    rows[i] = T->append(keys[i], tmp.data());
+    rows[i] = T->take_row(keys[i], tmp.data());
     ++added;
   }
   if (n_new) *n_new = added;
@@ -313,8 +340,29 @@ int or_mod(const int64_t* values, const int64_t* col_off, int32_t ncols, const i
 }
 
 int or_find_or_insert(void* h, const int64_t* keys, int64_t n, int64_t* rows_out, int64_t* n_inserted) {
+  static_cast<Table*>(h)->clock += 1;  // one lookup call
   return find_or_insert(static_cast<Table*>(h), keys, n, rows_out, n_inserted);
 }
+
+// Evict the stale features: every key whose age (clock now minus the clock
+// of its last lookup, modulo 2^32) exceeds max_age leaves the IDMap; its row
+// is pushed on the free stack (rows in ascending order).  Returns the count.
+int64_t or_evict(void* h, uint32_t max_age) {
+  Table* T = static_cast<Table*>(h);
+  int64_t count = 0;
+  for (int64_t r = 0; r < T->nrows; ++r) {
+    if (T->row_key[r] == KEY_EMPTY) continue;
+    if (static_cast<uint32_t>(T->clock - T->row_seen[r]) <= max_age) continue;
+    T->idmap.erase(T->row_key[r]);
+    T->row_key[r] = KEY_EMPTY;
+    T->free_stack.push_back(r);
+    ++count;
+  }
+  return count;
+}
+
+int64_t or_rows_allocated(void* h) { return static_cast<Table*>(h)->nrows; }
+uint32_t or_clock(void* h) { return static_cast<Table*>(h)->clock; }
 
 // Row contents by key (w as fp32 values; state_elems() state floats per key:
 // [acc] / [m | v] per element, or the row-wise [acc] / [m (dim) | v]).
@@ -387,6 +435,7 @@ int or_forward(void* h, const int64_t* values, const int64_t* offsets, int64_t n
   const int64_t U = or_dedup(values, n, unique_out, inverse_out);
   if (U < 0) return ST_EKEY;
   int64_t nn = 0;
+  T->clock += 1;  // one lookup call
   int st = find_or_insert(T, unique_out, U, rows_out, &nn);
   *U_out = U;
   *n_new_out = nn;

@@ -816,3 +816,70 @@ def test_rowwise_first_step_closed_form_and_layout():
     np.testing.assert_allclose(s1[0, :D], 0.1 * G[0], rtol=1e-6)
     np.testing.assert_allclose(s1[0, D], 0.001 * 6.25, rtol=1e-6)
     np.testing.assert_allclose(w1, w0.astype(np.float64) - 0.1 * G / 2.5, rtol=1e-6, atol=1e-12)
+
+
+# --------------------------------------------------------------------------- eviction
+
+
+def test_eviction_removes_exactly_the_stale_keys():
+    """Brute force: the test records, from its own inputs, the last call in
+    which each key was looked up; evict(max_age) must keep exactly the keys
+    with (calls so far - last call) <= max_age."""
+    g = np.random.default_rng(51)
+    T = O.Table(4, opt=O.ADAGRAD, seed=2)
+    last = {}
+    calls = 0
+    for step in range(12):
+        keys = g.integers(0, 60, size=int(g.integers(1, 25))).astype(np.int64)
+        if step % 3 == 0:
+            T.find_or_insert(keys)
+        else:
+            off = np.array([0, keys.size], dtype=np.int64)
+            assert T.forward(keys, off, O.SUM)["status"] == O.OK
+        calls += 1
+        for k in keys.tolist():
+            last[k] = calls
+        if step in (5, 9, 11):
+            max_age = int(g.integers(0, 4))
+            n = T.evict(max_age)
+            keep = {k for k, c in last.items() if calls - c <= max_age}
+            assert n == len(last) - len(keep)
+            last = {k: c for k, c in last.items() if k in keep}
+            ek, er = T.export()
+            assert set(ek.tolist()) == keep
+            assert T.size() == len(keep)
+            # rows of the live keys are distinct; live + free rows = rows allocated
+            assert len(set(er.tolist())) == er.size
+    assert T.clock == calls
+
+
+def test_evicted_rows_are_reused_top_of_stack_first_and_reinitialised():
+    D = 4
+    T = O.Table(D, opt=O.ADAM, seed=9)
+    st, rows, _ = T.find_or_insert(np.arange(10, dtype=np.int64))          # call 1: rows 0..9
+    assert rows.tolist() == list(range(10))
+    # update some rows so that stale values would show if a row leaked
+    T.optimizer(rows, np.ones((10, D), np.float32), 0.1, 1e-8, 0.9, 0.999)
+    keep = np.array([0, 1, 2, 4, 5, 6, 8], dtype=np.int64)
+    T.find_or_insert(keep)                                                   # call 2
+    assert T.evict(0) == 3                                                   # keys 3, 7, 9 age 1 > 0
+    st, rows, nn = T.find_or_insert(np.array([100, 101, 102, 103, 3], dtype=np.int64))
+    assert nn == 5
+    # the free stack holds 3, 7, 9 (pushed in row order): 9 is taken first
+    assert rows.tolist() == [9, 7, 3, 10, 11]
+    assert T.rows_allocated() == 12
+    _, w, s = T.read_rows(np.array([100, 101, 102, 103, 3], dtype=np.int64))
+    for i, k in enumerate([100, 101, 102, 103, 3]):
+        assert np.array_equal(w[i], O.init_row(9, k, D, -0.01, 0.01))       # fresh values, no leak
+        assert np.all(s[i] == 0)
+
+
+def test_eviction_max_age_zero_and_untouched_table():
+    T = O.Table(2, seed=1)
+    assert T.evict(5) == 0 and T.size() == 0
+    T.find_or_insert(np.array([1, 2, 3], dtype=np.int64))
+    T.find_or_insert(np.array([2], dtype=np.int64))
+    assert T.evict(1) == 0                       # ages 1, 0, 1
+    assert T.evict(0) == 2 and T.export()[0].tolist() == [2]
+    st, rows, _ = T.find_or_insert(np.array([1], dtype=np.int64))
+    assert rows.tolist() == [2]                  # rows 0 and 2 were freed (pushed 0, 2): 2 on top
