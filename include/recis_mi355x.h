@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define RS_VERSION 6
+#define RS_VERSION 7
 
 typedef enum {
   RS_OK = 0,
@@ -114,7 +114,9 @@ typedef struct {
                              of two >= 64                                        */
   int32_t auto_grow;      /* 1: rehash the IDMap (x2) and add Blocks on demand;
                              0: inserts beyond max_load*capacity fail (RS_EFULL) */
-  int32_t reserved0;
+  int32_t evictable;      /* 1: keep each row's key and the lookup clock of its
+                             last lookup (16 more bytes per row at most), so
+                             that ht_evict can drop stale keys; 0: no eviction */
 } rs_table_desc;
 
 /* Optimizer hyper-parameters.  Adagrad uses lr, eps; the Adam family lr,
@@ -186,6 +188,20 @@ rs_status ht_find(rs_table* t, const int64_t* keys, int64_t n, int64_t* rows_out
 /* Synchronize the stream and return the number of live keys (host pointer);
  * returns (and clears) any latched device error. */
 rs_status ht_size(rs_table* t, int64_t* live_host, rs_stream stream);
+
+/* Feature eviction (Embedding Engine: "evicting stale features during
+ * continuous training").  Every lookup call (ht_find_or_insert,
+ * lookup_prepare / lookup_pool_fwd) advances the table's lookup clock by
+ * one, and each key it looks up (found or inserted) records that clock.
+ * ht_evict removes every key whose age -- the current clock minus its
+ * recorded clock, modulo 2^32 -- exceeds max_age (max_age = 0 keeps only the
+ * keys of the latest lookup call): its IDMap slot becomes a tombstone (a
+ * later rehash drops it) and its row is pushed on a stack of free rows, in
+ * ascending row order.  New keys take free rows from the top of that stack
+ * (re-initialised exactly like a new row) before new rows are added.
+ * Only for tables created with evictable = 1 (else RS_EINVAL).  Synchronizes
+ * the stream; *n_evicted_host (may be NULL) receives the count. */
+rs_status ht_evict(rs_table* t, uint32_t max_age, int64_t* n_evicted_host, rs_stream stream);
 
 /* Synchronize the stream and return (and clear) any latched device error. */
 rs_status rs_table_check(rs_table* t, rs_stream stream);

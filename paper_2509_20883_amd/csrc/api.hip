@@ -220,6 +220,12 @@ struct rs_table {
   int64_t rows_prov = 0;
   // device scalars
   int64_t* d_scal = nullptr;
+  // eviction: row metadata offset (-1: none), the lookup clock (one tick per
+  // lookup call), the free-row stack (capacity rows_prov)
+  int meta_off = -1;
+  uint32_t clock = 0;
+  int64_t* free_rows = nullptr;
+  int64_t free_cap = 0;
   // host view of the live count: an upper bound.  Every insert call gets a
   // 16-bit tag; its scan kernel stores (tag << 48) | exact live count into
   // h_pin[0], and bound_after[tag % kTags] remembers the host's bound right
@@ -270,6 +276,9 @@ struct rs_table {
     t.row_dtype = d.row_dtype;
     t.nstate = nstate();
     t.rowscalar = rowscalar();
+    t.meta_off = meta_off;
+    t.clock = clock;
+    t.free_rows = free_rows;
     t.seed = d.seed;
     t.lo = d.init_lo;
     t.span = d.init_hi - d.init_lo;  // fp32 subtraction
@@ -327,6 +336,19 @@ rs_status provision_rows(rs_table* t, int64_t rows, hipStream_t s) {
     t->mapped += bytes;
   }
   t->rows_prov = static_cast<int64_t>(t->mapped / static_cast<size_t>(t->stride));
+  if (t->meta_off >= 0 && t->rows_prov > t->free_cap) {
+    // the free-row stack can hold every row
+    int64_t* nf = static_cast<int64_t*>(t->alloc(sizeof(int64_t) * static_cast<size_t>(t->rows_prov)));
+    if (!nf) return fail(RS_ENOMEM, "allocation of the free-row stack failed");
+    if (t->free_rows) {
+      RS_HIP(hipMemcpyAsync(nf, t->free_rows, sizeof(int64_t) * static_cast<size_t>(t->free_cap),
+                            hipMemcpyDeviceToDevice, s));
+      RS_HIP(hipStreamSynchronize(s));
+      t->release(t->free_rows);
+    }
+    t->free_rows = nf;
+    t->free_cap = t->rows_prov;
+  }
   return set_scalar(t, kTRowCap, t->rows_prov, s);
 }
 
@@ -343,30 +365,36 @@ rs_status rehash(rs_table* t, int64_t new_cap, hipStream_t s) {
   RS_HIP(launch_rehash(old, old_cap, t->dev(), s));
   rs_status st = set_scalar(t, kTLimit, t->limit, s);
   if (st != RS_OK) return st;
+  st = set_scalar(t, kTTomb, 0, s);  // the rehash leaves the tombstones behind
+  if (st != RS_OK) return st;
   RS_HIP(hipStreamSynchronize(s));
   t->release(old);
   return RS_OK;
 }
 
-// Grow (when allowed) so that `live_need` keys fit the IDMap and the Blocks.
-// `batch` (the ids of the call) sizes the headroom: the IDMap is doubled
-// until another call of `batch` ids would fit as well, so the host's upper
-// bound on the live count (live + ids of the call) does not force a
-// synchronization on every call of a batch larger than the free room.
-rs_status grow_for(rs_table* t, int64_t live_need, int64_t batch, hipStream_t s) {
+// Grow (when allowed) so that `keys_need` live keys fit the IDMap and
+// `rows_need` rows the Blocks.  `batch` (the ids of the call) sizes the
+// headroom: the IDMap is doubled until another call of `batch` ids would fit
+// as well, so the host's upper bound on the live count (live + ids of the
+// call) does not force a synchronization on every call of a batch larger
+// than the free room.  Tombstones (eviction) count against the key limit
+// until a rehash drops them: the IDMap is rehashed, at the same capacity if
+// that suffices, when they would not leave that room.
+rs_status grow_for(rs_table* t, int64_t keys_need, int64_t tombs, int64_t rows_need, int64_t batch, hipStream_t s) {
   if (t->d.auto_grow) {
+    const double ml = static_cast<double>(t->d.max_load);
     int64_t c = t->cap;
-    while (static_cast<double>(live_need + batch) > static_cast<double>(t->d.max_load) * static_cast<double>(c)) c <<= 1;
-    if (c != t->cap) {
+    while (static_cast<double>(keys_need + batch) > ml * static_cast<double>(c)) c <<= 1;
+    if (c != t->cap || static_cast<double>(keys_need + tombs + batch) > ml * static_cast<double>(c)) {
       rs_status st = rehash(t, c, s);
       if (st != RS_OK) return st;
     }
     // headroom: a quarter more rows and at least four batches' worth, so the
     // host's upper bound on live rows rarely forces a synchronization
-    const int64_t headroom = live_need + std::max(live_need / 4, 4 * batch) + t->d.block_rows;
+    const int64_t headroom = rows_need + std::max(rows_need / 4, 4 * batch) + t->d.block_rows;
     return provision_rows(t, headroom, s);
   }
-  return provision_rows(t, std::min(live_need, t->limit), s);
+  return provision_rows(t, std::min(rows_need, t->limit), s);
 }
 
 // Lower the host's bound on live rows with the newest count a scan kernel
@@ -407,15 +435,20 @@ rs_status dedup_and_insert(rs_table* t, const int64_t* values, int64_t n, const 
     // exact decision: read back U and live (one synchronization)
     RS_HIP(hipStreamSynchronize(s));
     // the scan already reserved rows for the keys not found (or as many as
-    // fitted): read the request and the live count before it
-    int64_t req = 0, live0 = 0;
-    RS_HIP(hipMemcpy(&req, w.scal + kCNewReq, sizeof(int64_t), hipMemcpyDeviceToHost));
-    RS_HIP(hipMemcpy(&live0, w.scal + kCBaseLive, sizeof(int64_t), hipMemcpyDeviceToHost));
-    st = grow_for(t, live0 + req, n, s);
+    // fitted): read the request and the counts before it
+    int64_t cs[kCScalars], ts[kTScalars];
+    RS_HIP(hipMemcpy(cs, w.scal, sizeof(cs), hipMemcpyDeviceToHost));
+    RS_HIP(hipMemcpy(ts, t->d_scal, sizeof(ts), hipMemcpyDeviceToHost));
+    const int64_t req = cs[kCNewReq];
+    const int64_t keys_need = cs[kCBaseKeys] + req;
+    const int64_t rows_need = cs[kCBaseLive] + std::max<int64_t>(req - cs[kCFreeTop], 0);
+    st = grow_for(t, keys_need, ts[kTTomb], rows_need, n, s);
     if (st != RS_OK) return st;
+    int64_t tombs = 0;
+    RS_HIP(hipMemcpy(&tombs, t->d_scal + kTTomb, sizeof(int64_t), hipMemcpyDeviceToHost));
     // redo the reservation against the grown table (published under a new
     // tag: the scan's count may predate the growth)
-    reset_bound(t, live0 + req);
+    reset_bound(t, std::max(keys_need + tombs, rows_need));
     const int64_t tag2 = next_tag(t);
     RS_HIP(launch_rereserve(w, t->dev(), t->h_pin, tag2, s));
     t->bound_after[tag2 % rs_table::kTags] = t->live_bound;
@@ -498,6 +531,11 @@ rs_status ht_create(const rs_table_desc* d, const rs_allocator* a, rs_stream str
     return fail(RS_EHIP, "hipGetDevice failed");
   }
   t->stride = static_cast<int64_t>(d->dim) * t->wbytes() + 4 * t->state_elems();
+  if (d->evictable) {
+    // {int64 key, uint32 clock of the last lookup} after the state
+    t->meta_off = static_cast<int>((t->stride + 7) / 8 * 8);
+    t->stride = t->meta_off + 12;
+  }
   t->stride = (t->stride + 15) / 16 * 16;  // 16-byte row fragments
   t->cap = d->capacity_slots;
   t->limit = static_cast<int64_t>(std::floor(static_cast<double>(d->max_load) * static_cast<double>(t->cap)));
@@ -566,6 +604,7 @@ rs_status ht_destroy(rs_table* t) {
   if (t->va_base) (void)hipMemAddressFree(t->va_base, t->va_size);
   t->release(t->d_scal);
   t->release(t->iws);
+  t->release(t->free_rows);
   if (t->h_pin) (void)hipHostFree(t->h_pin);
   delete t;
   return st;
@@ -675,6 +714,7 @@ rs_status ht_find_or_insert(rs_table* t, const int64_t* keys, int64_t n, int64_t
     if (!t->iws) return fail(RS_ENOMEM, "allocation of the insert workspace failed");
   }
   const Work w = make_work(t->iws, L);
+  t->clock += 1;  // one lookup call
   rs_status st = dedup_and_insert(t, keys, n, w, false, s);
   if (st != RS_OK) return st;
   RS_HIP(launch_map_rows(w, n, rows_out, n_inserted_dev, s));
@@ -693,8 +733,35 @@ rs_status ht_size(rs_table* t, int64_t* live_host, rs_stream stream) {
   if (!t || !live_host) return fail(RS_EINVAL, "null table or output");
   hipStream_t s = static_cast<hipStream_t>(stream);
   RS_HIP(hipStreamSynchronize(s));
-  RS_HIP(hipMemcpy(live_host, t->d_scal + kTLive, sizeof(int64_t), hipMemcpyDeviceToHost));
-  reset_bound(t, *live_host);
+  int64_t ts[kTScalars];
+  RS_HIP(hipMemcpy(ts, t->d_scal, sizeof(ts), hipMemcpyDeviceToHost));
+  *live_host = ts[kTKeys];
+  reset_bound(t, std::max(ts[kTKeys] + ts[kTTomb], ts[kTLive]));
+  return take_latched(t);
+}
+
+rs_status ht_evict(rs_table* t, uint32_t max_age, int64_t* n_evicted_host, rs_stream stream) {
+  if (!t) return fail(RS_EINVAL, "null table");
+  if (t->meta_off < 0) return fail(RS_EINVAL, "the table was created without eviction (evictable = 0)");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t nb = std::max<int64_t>(1, (t->rows_prov + kEvictRows - 1) / kEvictRows);
+  int32_t* bcount = static_cast<int32_t*>(t->alloc(sizeof(int32_t) * static_cast<size_t>(nb + 1)));
+  if (!bcount) return fail(RS_ENOMEM, "allocation of the eviction counts failed");
+  rs_status st = RS_OK;
+  if (t->rows_prov > 0) {
+    const hipError_t e = launch_evict(t->dev(), t->rows_prov, max_age, bcount, s);
+    if (e != hipSuccess) st = fail(RS_EHIP, std::string("eviction launch: ") + hipGetErrorString(e));
+  }
+  int64_t ts[kTScalars] = {};
+  int32_t n = 0;
+  if (st == RS_OK && (hipStreamSynchronize(s) != hipSuccess ||
+                      (t->rows_prov > 0 && hipMemcpy(&n, bcount + nb, sizeof(int32_t), hipMemcpyDeviceToHost) != hipSuccess) ||
+                      hipMemcpy(ts, t->d_scal, sizeof(ts), hipMemcpyDeviceToHost) != hipSuccess))
+    st = fail(RS_EHIP, "eviction read-back failed");
+  t->release(bcount);
+  if (st != RS_OK) return st;
+  reset_bound(t, std::max(ts[kTKeys] + ts[kTTomb], ts[kTLive]));
+  if (n_evicted_host) *n_evicted_host = n;
   return take_latched(t);
 }
 
@@ -783,6 +850,7 @@ rs_status lookup_prepare(rs_table* t, const int64_t* values, const int64_t* offs
   ctx->pad_len = padded_mode(mode) ? pad_len : 0;
   ctx->mode = mode;
   ctx->dim = t->d.dim;
+  t->clock += 1;  // one lookup call
   rs_status st = dedup_and_insert(t, values, n, w, true, s);
   if (st != RS_OK) return st;
   ctx->priv[0] = 1;

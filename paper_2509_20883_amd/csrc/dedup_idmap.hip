@@ -579,6 +579,30 @@ __device__ inline void publish_live(int64_t* h_live, int64_t tag, int64_t live) 
   }
 }
 
+// Rows for `req` keys not found, from `hw` rows allocated, `keys` live keys
+// and `F` free rows: as many as both the IDMap (its key limit counts the
+// tombstones) and the Blocks (free rows, then provisioned ones) allow.  The
+// first min(inserted, F) new keys take free rows.  The published count
+// bounds both the IDMap occupancy and the rows allocated.
+__device__ inline void reserve_rows(int64_t* cscal, int64_t* tscal, int64_t req, int64_t hw, int64_t keys, int64_t F,
+                                    int64_t* h_live, int64_t tag) {
+  const int64_t tombs = tscal[kTTomb];
+  const int64_t key_room = max(tscal[kTLimit] - keys - tombs, int64_t(0));
+  const int64_t row_room = F + max(tscal[kTRowCap] - hw, int64_t(0));
+  const int64_t ins = min(req, min(key_room, row_room));
+  const int64_t take = min(ins, F);
+  cscal[kCNew] = ins;
+  cscal[kCBaseLive] = hw;
+  cscal[kCBaseKeys] = keys;
+  cscal[kCFreeTop] = F;
+  cscal[kCFreeTake] = take;
+  cscal[kCTrunc] = req > ins ? 1 : 0;
+  tscal[kTLive] = hw + ins - take;
+  tscal[kTKeys] = keys + ins;
+  tscal[kTFree] = F - take;
+  publish_live(h_live, tag, max(keys + ins + tombs, hw + ins - take));
+}
+
 // Scan of the five tile-sum arrays: block c scans chunk c (kScanChunk tiles,
 // R per thread) in place and stores the chunk's totals; the last block to
 // finish (a counter, no waiting) scans the chunk totals in place, reserves
@@ -662,27 +686,12 @@ __global__ __launch_bounds__(1024) void k_scan5(int32_t* __restrict__ bsum, int6
   cscal[kCNewReq] = tot[2];
   cscal[kCNLong] = tot[3];
   cscal[kCNUnits] = tot[4];
-  const int64_t live = tscal[kTLive];
-  const int64_t lim = min(tscal[kTLimit], tscal[kTRowCap]);
-  const int64_t room = lim > live ? lim - live : 0;
-  const int64_t ins = tot[2] < room ? tot[2] : room;
-  cscal[kCNew] = ins;
-  cscal[kCBaseLive] = live;
-  cscal[kCTrunc] = tot[2] > room ? 1 : 0;
-  tscal[kTLive] = live + ins;
-  publish_live(h_live, tag, live + ins);
+  reserve_rows(cscal, tscal, tot[2], tscal[kTLive], tscal[kTKeys], tscal[kTFree], h_live, tag);
 }
 
-// After the host grew the table: reserve again from the same live count.
+// After the host grew the table: reserve again from the same counts.
 __global__ void k_rereserve(int64_t* cscal, int64_t* tscal, int64_t* h_live, int64_t tag) {
-  const int64_t live = cscal[kCBaseLive], req = cscal[kCNewReq];
-  const int64_t lim = min(tscal[kTLimit], tscal[kTRowCap]);
-  const int64_t room = lim > live ? lim - live : 0;
-  const int64_t ins = req < room ? req : room;
-  cscal[kCNew] = ins;
-  cscal[kCTrunc] = req > room ? 1 : 0;
-  tscal[kTLive] = live + ins;
-  publish_live(h_live, tag, live + ins);
+  reserve_rows(cscal, tscal, cscal[kCNewReq], cscal[kCBaseLive], cscal[kCBaseKeys], cscal[kCFreeTop], h_live, tag);
 }
 
 __global__ void k_zero_scalars(int64_t* cscal) { cscal[threadIdx.x] = 0; }
@@ -785,6 +794,7 @@ __global__ __launch_bounds__(NT) void k_compact(TableDev t, Work w, const int64_
   int unext = pre[4] + ex[4];
   const int64_t inserted = w.scal[kCNew];
   const int64_t live0 = w.scal[kCBaseLive];
+  const int64_t ftop = w.scal[kCFreeTop], ftake = w.scal[kCFreeTake];
   if (blockIdx.x == 0 && threadIdx.x == 0 && w.scal[kCTrunc]) atomicOr(reinterpret_cast<int*>(&t.scal[kTErr]), kErrFull);
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
@@ -804,7 +814,8 @@ __global__ __launch_bounds__(NT) void k_compact(TableDev t, Work w, const int64_
       if (nr < inserted) {
         const int64_t slot = idmap_claim(t, static_cast<unsigned long long>(key) ^ kSign);
         if (slot >= 0) {
-          row = live0 + nr;
+          // the first `ftake` new keys take free rows from the top of the stack
+          row = nr < ftake ? t.free_rows[ftop - 1 - nr] : live0 + (nr - ftake);
           t.slots[slot].row = row;
           w.new_list[nr] = uid;
         } else {
@@ -812,6 +823,9 @@ __global__ __launch_bounds__(NT) void k_compact(TableDev t, Work w, const int64_
         }
       }
       ++nr;
+    } else if (t.meta_off >= 0) {
+      // eviction: this call is the key's last lookup
+      *reinterpret_cast<uint32_t*>(t.store.row(row) + t.meta_off + 8) = t.clock;
     }
     w.rows[uid] = row;
     w.useg[uid] = Seg{row, start, c};
@@ -836,8 +850,9 @@ __device__ inline float init_value(uint64_t z, int j, float lo, float span) {
 }
 
 // Lane groups of 16 write the rows of the inserted keys: w from the init
-// formula, optimizer state zero, 16 bytes per lane per store.  Block `blk`
-// of `nblk` takes every nblk-th group of keys.
+// formula, optimizer state zero, and for eviction the key and this call's
+// clock; 16 bytes per lane per store.  Block `blk` of `nblk` takes every
+// nblk-th group of keys.
 __device__ inline void init_rows(const TableDev& t, const Work& w, int64_t blk, int64_t nblk) {
   constexpr int G = 16;
   const int lane = threadIdx.x % G, grp = threadIdx.x / G;
@@ -847,7 +862,8 @@ __device__ inline void init_rows(const TableDev& t, const Work& w, int64_t blk, 
   for (int64_t q = blk * (kBlock / G) + grp; q < inserted; q += nblk * (kBlock / G)) {
     const int u = w.new_list[q];
     const int64_t row = w.useg[u].row;
-    const uint64_t z = mix64(static_cast<uint64_t>(w.unique[u]) ^ mix64(t.seed));
+    const int64_t key = w.unique[u];
+    const uint64_t z = mix64(static_cast<uint64_t>(key) ^ mix64(t.seed));
     uint8_t* rp = t.store.row(row);
     for (int ch = lane; ch < chunks; ch += G) {
       const int off = ch * 16;
@@ -868,6 +884,17 @@ __device__ inline void init_rows(const TableDev& t, const Work& w, int64_t blk, 
                    (static_cast<uint32_t>(f32_to_bf16(init_value(z, j0 + 2 * k + 1, t.lo, t.span))) << 16);
           val = make_uint4(h[0], h[1], h[2], h[3]);
         }
+      }
+      if (t.meta_off >= 0 && off + 16 > t.meta_off && off < t.meta_off + 12) {
+        uint32_t v4[4] = {val.x, val.y, val.z, val.w};
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int b = off + 4 * q4 - t.meta_off;  // byte of the {key, clock} record
+          if (b == 0) v4[q4] = static_cast<uint32_t>(static_cast<uint64_t>(key));
+          if (b == 4) v4[q4] = static_cast<uint32_t>(static_cast<uint64_t>(key) >> 32);
+          if (b == 8) v4[q4] = t.clock;
+        }
+        val = make_uint4(v4[0], v4[1], v4[2], v4[3]);
       }
       *reinterpret_cast<uint4*>(rp + off) = val;
     }
@@ -961,6 +988,113 @@ hipError_t launch_compact_insert(const int64_t* values, int64_t n, const TableDe
   else k_occ_init<false><<<static_cast<unsigned>(ob + ib), kBlock, 0, s>>>(t, w, n, ob);
   if (ev_occ && ev_occ[1]) (void)hipEventRecord(ev_occ[1], s);
   if (ev_init && ev_init[1]) (void)hipEventRecord(ev_init[1], s);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// eviction of stale keys
+// ---------------------------------------------------------------------------
+
+// Slot index of an encoded key, or -1.
+__device__ inline int64_t idmap_slot_of(const TableDev& t, unsigned long long e) {
+  uint64_t h = idmap_hash(e) & t.cap_mask;
+  for (uint64_t probed = 0; probed <= t.cap_mask; ++probed) {
+    const unsigned long long k = t.slots[h].key;
+    if (k == e) return static_cast<int64_t>(h);
+    if (k == kEncEmpty) return -1;
+    h = (h + 1) & t.cap_mask;
+  }
+  return -1;
+}
+
+// Row r holds a key whose age (clock - clock of its last lookup, mod 2^32)
+// exceeds max_age.  Rows at or past the high-water mark hold nothing.
+__device__ inline bool stale_row(const TableDev& t, int64_t r, int64_t hw, uint32_t max_age, int64_t& key) {
+  key = INT64_MIN;
+  if (r >= hw) return false;
+  const uint8_t* m = t.store.row(r) + t.meta_off;
+  key = *reinterpret_cast<const int64_t*>(m);
+  const uint32_t seen = *reinterpret_cast<const uint32_t*>(m + 8);
+  return key != INT64_MIN && static_cast<uint32_t>(t.clock - seen) > max_age;
+}
+
+// Stale rows per block of kEvictRows rows (4 per thread).
+__global__ __launch_bounds__(kBlock) void k_evict_count(TableDev t, uint32_t max_age, int32_t* __restrict__ bcount) {
+  __shared__ int sh[kBlock / kWave + 1];
+  const int64_t hw = t.scal[kTLive];
+  int c = 0;
+#pragma unroll
+  for (int k = 0; k < kEvictRows / kBlock; ++k) {
+    int64_t key;
+    c += stale_row(t, static_cast<int64_t>(blockIdx.x) * kEvictRows + k * kBlock + threadIdx.x, hw, max_age, key);
+  }
+  const int tot = block_sum<kBlock>(c, sh);
+  if (threadIdx.x == 0) bcount[blockIdx.x] = tot;
+}
+
+// One block: exclusive scan of the nb block counts in place (chunks of 1024
+// with a running carry); the total goes to bcount[nb].
+__global__ __launch_bounds__(1024) void k_evict_scan(int32_t* __restrict__ bcount, int64_t nb) {
+  __shared__ int sh[1024 / kWave + 1];
+  int carry = 0;
+  for (int64_t base = 0; base < nb; base += 1024) {
+    const int64_t i = base + threadIdx.x;
+    const int v = i < nb ? bcount[i] : 0;
+    int tot;
+    const int ex = block_excl_scan<1024>(v, sh, tot);
+    if (i < nb) bcount[i] = carry + ex;
+    carry += tot;
+  }
+  if (threadIdx.x == 0) bcount[nb] = carry;
+}
+
+// The stale rows of a block, in row order: each is pushed on the free stack
+// (after the rows already there), its key is cleared and its IDMap slot
+// becomes a tombstone.
+__global__ __launch_bounds__(kBlock) void k_evict_apply(TableDev t, uint32_t max_age,
+                                                        const int32_t* __restrict__ bcount) {
+  __shared__ int sh[kBlock / kWave + 1];
+  constexpr int K = kEvictRows / kBlock;
+  const int64_t hw = t.scal[kTLive];
+  const int64_t F0 = t.scal[kTFree];
+  // thread tid owns rows r0 + tid*K ... + K-1: row order = thread order
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kEvictRows + static_cast<int64_t>(threadIdx.x) * K;
+  int64_t key[K];
+  bool st[K];
+  int c = 0;
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    st[k] = stale_row(t, r0 + k, hw, max_age, key[k]);
+    c += st[k];
+  }
+  int tot;
+  int pos = block_excl_scan<kBlock>(c, sh, tot);
+  const int64_t base = F0 + bcount[blockIdx.x];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    if (!st[k]) continue;
+    t.free_rows[base + pos++] = r0 + k;
+    *reinterpret_cast<int64_t*>(t.store.row(r0 + k) + t.meta_off) = INT64_MIN;
+    const int64_t slot = idmap_slot_of(t, static_cast<unsigned long long>(key[k]) ^ kSign);
+    if (slot >= 0) t.slots[slot].key = kEncTomb;
+    else atomicOr(reinterpret_cast<int*>(&t.scal[kTErr]), kErrProbe);
+  }
+}
+
+__global__ void k_evict_finish(int64_t* tscal, const int32_t* bcount, int64_t nb) {
+  const int64_t n = bcount[nb];
+  tscal[kTFree] += n;
+  tscal[kTKeys] -= n;
+  tscal[kTTomb] += n;
+}
+
+hipError_t launch_evict(const TableDev& t, int64_t rows_prov, uint32_t max_age, int32_t* bcount, hipStream_t s) {
+  if (t.meta_off < 0) return hipErrorInvalidValue;
+  const int64_t nb = std::max<int64_t>(1, (rows_prov + kEvictRows - 1) / kEvictRows);
+  k_evict_count<<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, max_age, bcount);
+  k_evict_scan<<<1, 1024, 0, s>>>(bcount, nb);
+  k_evict_apply<<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, max_age, bcount);
+  k_evict_finish<<<1, 1, 0, s>>>(t.scal, bcount, nb);
   return hipGetLastError();
 }
 

@@ -81,8 +81,21 @@ constexpr int kResident = 2048;
 // Latched device error bits.
 enum : int { kErrKey = 1, kErrFull = 2, kErrProbe = 8 };
 
-// Table-resident device scalars.
-enum : int { kTLive = 0, kTLimit = 1, kTRowCap = 2, kTErr = 3, kTExport = 4, kTScalars = 8 };
+// Table-resident device scalars: rows ever allocated (the high-water mark),
+// the IDMap key limit, rows provisioned, error bits, export counter, and for
+// eviction the free-row stack size, live keys and IDMap tombstones (without
+// eviction live keys = rows and the other two stay 0).
+enum : int {
+  kTLive = 0,
+  kTLimit = 1,
+  kTRowCap = 2,
+  kTErr = 3,
+  kTExport = 4,
+  kTFree = 5,
+  kTKeys = 6,
+  kTTomb = 7,
+  kTScalars = 8
+};
 // Per-call (context) device scalars.
 enum : int {
   kCU = 0,         // unique keys
@@ -94,7 +107,10 @@ enum : int {
   kCNUnits = 6,    // backward units of those keys
   kCTrunc = 7,     // 1 if some keys not found had no room (latched as RS_EFULL)
   kCScanDone = 8,  // blocks of the tile-sum scan that have finished
-  kCScalars = 9
+  kCBaseKeys = 9,  // live keys before the insert
+  kCFreeTop = 10,  // free-row stack size before the insert
+  kCFreeTake = 11, // inserted keys that take a free row (the first ones)
+  kCScalars = 12
 };
 
 // Ids partition: at most kMaxShards owner shards.  Its device scalars: the
@@ -131,7 +147,8 @@ struct alignas(16) Slot {
 // Blocks: physical chunks mapped back to back into one reserved virtual
 // range, so rows never move and row r is at base + r * stride; a row is
 // [w: D x row dtype | state0: D x fp32 | state1: D x fp32 (Adam) | row
-// scalar (row-wise optimizers)], padded to 16 bytes.
+// scalar (row-wise optimizers) | {key, clock of its last lookup} (tables
+// with eviction)], padded to 16 bytes.
 struct RowStore {
   uint8_t* base;
   int64_t stride;  // bytes per row
@@ -147,6 +164,9 @@ struct TableDev {
   int row_dtype;  // 0 f32, 1 bf16
   int nstate;     // per-element fp32 state vectors after w (0, 1 or 2)
   int rowscalar;  // 1: one fp32 state scalar per row follows them (row-wise optimizers)
+  int meta_off;   // eviction: byte offset of the row's {int64 key, uint32 clock}; -1: none
+  uint32_t clock; // eviction: the lookup clock of this call
+  int64_t* free_rows;  // eviction: the free-row stack
   uint64_t seed;
   float lo, span;  // init: fma(u, span, lo)
 };
@@ -289,6 +309,12 @@ hipError_t launch_bucketize(const float* values, int64_t n, const int64_t* col_o
                             const int64_t* bnd_off, int64_t* out, hipStream_t s);
 hipError_t launch_mod(const int64_t* values, int64_t n, const int64_t* col_off, int ncols, const int64_t* moduli,
                       int64_t* out, hipStream_t s);
+// Eviction of the keys whose age (clock - clock of their last lookup)
+// exceeds max_age: their IDMap slots become tombstones and their rows are
+// pushed on the free stack in row order.  bcount: one int per block of
+// kEvictRows rows; the evicted count is added to the table scalars.
+constexpr int kEvictRows = 1024;
+hipError_t launch_evict(const TableDev& t, int64_t rows_prov, uint32_t max_age, int32_t* bcount, hipStream_t s);
 hipError_t launch_rehash(const Slot* old_slots, int64_t old_cap, const TableDev& t, hipStream_t s);
 hipError_t launch_export(const TableDev& t, int64_t cap_slots, int64_t* keys, int64_t* rows, int64_t cap,
                          int64_t* n_dev, hipStream_t s);

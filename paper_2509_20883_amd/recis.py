@@ -41,7 +41,7 @@ class TableDesc(C.Structure):
     _fields_ = [("dim", C.c_int32), ("row_dtype", C.c_int32), ("optimizer", C.c_int32),
                 ("init_lo", C.c_float), ("init_hi", C.c_float), ("seed", C.c_uint64),
                 ("capacity_slots", C.c_int64), ("max_load", C.c_float), ("block_rows", C.c_int64),
-                ("auto_grow", C.c_int32), ("reserved0", C.c_int32)]
+                ("auto_grow", C.c_int32), ("evictable", C.c_int32)]
 
 
 class OptParams(C.Structure):
@@ -90,6 +90,7 @@ def lib() -> C.CDLL:
         "sparse_opt_step": (C.c_int, [p, C.POINTER(RsCtx), p, C.POINTER(OptParams), p]),
         "lookup_pool_bwd_opt": (C.c_int, [p, C.POINTER(RsCtx), p, C.POINTER(OptParams), p]),
         "rs_set_kernel_events": (C.c_int, [p, i32, p, p]),
+        "ht_evict": (C.c_int, [p, C.c_uint32, C.POINTER(i64), p]),
         "ids_partition_workspace_bytes": (C.c_size_t, [i64, i32]),
         "ids_partition": (C.c_int, [p, i64, i32, C.c_uint64, p, p, p, p, p, C.c_size_t, p]),
         "fused_bucketize": (C.c_int, [p, i64, p, i32, p, p, p, i32, p]),
@@ -234,9 +235,9 @@ class Table:
 
     def __init__(self, dim: int, row_dtype: int = F32, optimizer: int = ADAGRAD, init_lo: float = -0.01,
                  init_hi: float = 0.01, seed: int = 0, capacity_slots: int = 1 << 17, max_load: float = 0.75,
-                 block_rows: int = 1 << 16, auto_grow: bool = True):
+                 block_rows: int = 1 << 16, auto_grow: bool = True, evictable: bool = False):
         d = TableDesc(dim, row_dtype, optimizer, init_lo, init_hi, seed & 0xFFFFFFFFFFFFFFFF, capacity_slots,
-                      max_load, block_rows, int(bool(auto_grow)), 0)
+                      max_load, block_rows, int(bool(auto_grow)), int(bool(evictable)))
         h = C.c_void_p()
         _check(lib().ht_create(C.byref(d), None, _stream(), C.byref(h)))
         self.h = h
@@ -278,6 +279,12 @@ class Table:
     def size(self) -> int:
         v = C.c_int64()
         _check(lib().ht_size(self.h, C.byref(v), _stream()))
+        return v.value
+
+    def evict(self, max_age: int) -> int:
+        """Drop the keys not looked up in the last max_age lookup calls; returns the count."""
+        v = C.c_int64()
+        _check(lib().ht_evict(self.h, max_age & 0xFFFFFFFF, C.byref(v), _stream()))
         return v.value
 
     def check(self):
