@@ -50,6 +50,10 @@ def parse():
     ap.add_argument("--gen-workers", type=int, default=16,
                     help="processes drawing the input batches before the GPU is touched (1: in-process, e.g. under "
                          "a profiler)")
+    ap.add_argument("--evictable", action="store_true",
+                    help="create the table with eviction (each row keeps its key and last-lookup clock)")
+    ap.add_argument("--evict-age", type=int, default=-1,
+                    help="after the timed steps, time one ht_evict(max_age) on the table (implies --evictable)")
     ap.add_argument("--op", choices=["step", "ids-partition", "bucketize", "mod"], default="step",
                     help="ids-partition: time the fused dedup + owner split alone on its one-million-id input; "
                          "bucketize / mod: the fused feature transforms on 100 columns of 10,000 values")
@@ -436,8 +440,9 @@ def main():
 
     torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
+    evictable = a.evictable or a.evict_age >= 0
     table = R.Table(w.dim, w.row_dtype, w.opt, w.init_lo, w.init_hi, w.table_seed, w.capacity_slots, w.max_load,
-                    w.block_rows, auto_grow=True)
+                    w.block_rows, auto_grow=True, evictable=evictable)
     npre = 0
     for keys in W.prepop_keys(w):
         table.find_or_insert(torch.from_numpy(keys).to(dev))
@@ -608,6 +613,27 @@ def main():
     cand_ms = {k: float(np.mean([e0.elapsed_time(e1) for e0, e1 in cand_ev[k].values()])) for k in cands}
     total_ms = e_start.elapsed_time(e_stop)
     table.check()
+    eviction = None
+    if a.evict_age >= 0:
+        # one eviction over the whole table, after the timed steps: it reads
+        # every allocated row's {key, clock} record (12 bytes) and, per evicted
+        # key, writes its row's key, its free-stack entry and its IDMap slot
+        rows_before = table.size()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record()
+        n_ev = table.evict(a.evict_age)
+        ev1.record()
+        torch.cuda.synchronize()
+        ems = ev0.elapsed_time(ev1)
+        # rows allocated = live rows before the last step + the keys it inserted
+        # (no row has been freed before this first eviction)
+        last = (stepscal[-1] if ring < nsteps else ctxs[nsteps - 1].scalars()).cpu().numpy()
+        hw = int(last[3] + last[1])
+        ebytes = 12 * hw + n_ev * (8 + 8 + 16)
+        eviction = {"max_age": a.evict_age, "ms": ems, "keys_before": rows_before, "evicted": n_ev,
+                    "rows_scanned": hw, "bytes_alg": ebytes, "GBps_alg": ebytes / (ems * 1e-3) / 1e9}
+        progress(f"evicted {n_ev} of {rows_before} keys in {ems:.3f} ms")
 
     # per-step sizes (read after the timed region)
     tot_ids = tot_bytes = 0
@@ -664,6 +690,8 @@ def main():
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic, "kernel_ms": dom_ms,
                      "kernel_bytes_alg": dom_bytes / a.steps},
         "kernel_ms_warmup": {k: float(np.mean(v)) for k, v in prof.items() if v},
+        "evictable": evictable,
+        "eviction": eviction,
         "setup_s": setup_s,
     }
     if not a.no_cpu_baseline:
