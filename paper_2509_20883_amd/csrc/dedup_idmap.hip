@@ -819,6 +819,7 @@ __global__ __launch_bounds__(NT) void k_compact(TableDev t, Work w, const int64_
           t.slots[slot].row = row;
           w.new_list[nr] = uid;
         } else {
+          w.new_list[nr] = -1;  // no slot (cannot happen below the key limit): no row to initialise
           atomicOr(reinterpret_cast<int*>(&t.scal[kTErr]), kErrProbe);
         }
       }
@@ -861,6 +862,7 @@ __device__ inline void init_rows(const TableDev& t, const Work& w, int64_t blk, 
   const int wbytes = t.dim * (t.row_dtype ? 2 : 4);
   for (int64_t q = blk * (kBlock / G) + grp; q < inserted; q += nblk * (kBlock / G)) {
     const int u = w.new_list[q];
+    if (u < 0) continue;
     const int64_t row = w.useg[u].row;
     const int64_t key = w.unique[u];
     const uint64_t z = mix64(static_cast<uint64_t>(key) ^ mix64(t.seed));
