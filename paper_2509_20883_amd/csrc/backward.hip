@@ -176,7 +176,7 @@ __device__ inline void sum_segments(const Work& w, const GT* __restrict__ grad, 
   constexpr int D = LANES * E;
   constexpr int MAXP = K * kLong;
   constexpr int NR = (MAXP + LANES - 1) / LANES;  // positions per lane
-  constexpr int kBatch = E == 4 ? 16 : 8;          // gradient rows in flight
+  constexpr int kBatch = 8;  // gradient rows in flight (111 VGPRs for fp32 rows: 4 waves per SIMD)
   int pre[K + 1];
   pre[0] = 0;
 #pragma unroll

@@ -55,52 +55,54 @@ __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64
   const int grp = threadIdx.x / LANES;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * GPB * kBags;
   for (int64_t g0 = (static_cast<int64_t>(blockIdx.x) * GPB + grp) * kBags; g0 < bags; g0 += stride) {
-    int64_t b[kBags], e[kBags];
+    // positions fit 32 bits (n <= 2^28): fewer registers, more resident waves
+    int b[kBags], e[kBags];
     if constexpr (LANES > kBags) {
       // lanes 0..kBags of the group load offsets[g0 .. g0+kBags] together
       const int64_t gq = g0 + min(lane, kBags);
-      const int64_t ov = gq <= bags ? offsets[gq] : n;
+      const int ov = static_cast<int>(gq <= bags ? offsets[gq] : n);
 #pragma unroll
       for (int q = 0; q <= kBags; ++q) {
-        const int64_t x = __shfl(ov, q, LANES);
+        const int x = __shfl(ov, q, LANES);
         if (q < kBags) b[q] = x;
         if (q > 0) e[q - 1] = x;
       }
     } else {
 #pragma unroll
       for (int q = 0; q < kBags; ++q) {
-        b[q] = g0 + q < bags ? offsets[g0 + q] : 0;
-        e[q] = g0 + q < bags ? offsets[g0 + q + 1] : 0;
+        b[q] = g0 + q < bags ? static_cast<int>(offsets[g0 + q]) : 0;
+        e[q] = g0 + q < bags ? static_cast<int>(offsets[g0 + q + 1]) : 0;
       }
     }
-    int64_t pre[kBags + 1];
+    int pre[kBags + 1];
     pre[0] = 0;
+    const int n32 = static_cast<int>(n);
 #pragma unroll
     for (int q = 0; q < kBags; ++q) {
       // CSR bounds clamped to [0, n]: malformed offsets cannot read out of range
       const bool ok = g0 + q < bags;
-      b[q] = ok ? min(max(b[q], int64_t(0)), n) : 0;
-      e[q] = ok ? min(max(e[q], b[q]), n) : 0;
+      b[q] = ok ? min(max(b[q], 0), n32) : 0;
+      e[q] = ok ? min(max(e[q], b[q]), n32) : 0;
       pre[q + 1] = pre[q] + (e[q] - b[q]);
     }
-    const int64_t total = pre[kBags];
+    const int total = pre[kBags];
     float acc[kBags][E];
 #pragma unroll
     for (int q = 0; q < kBags; ++q)
 #pragma unroll
       for (int k = 0; k < E; ++k) acc[q][k] = 0.f;
-    for (int64_t t0 = 0; t0 < total; t0 += C) {
+    for (int t0 = 0; t0 < total; t0 += C) {
       int64_t rr[J];
       int pp[J], qq[J];
 #pragma unroll
       for (int j = 0; j < J; ++j) {
         const int c = lane + j * LANES;
-        const int64_t tt = t0 + c;
+        const int tt = t0 + c;
         const bool valid = c < C && tt < total;
         int q = 0;
 #pragma unroll
         for (int k = 1; k < kBags; ++k) q += tt >= pre[k];
-        const int64_t p = valid ? b[q] + (tt - pre[q]) : 0;  // total > 0: position 0 exists
+        const int p = valid ? b[q] + (tt - pre[q]) : 0;  // total > 0: position 0 exists
         rr[j] = w.occ_row[p];
         pp[j] = w.occ_pos[p];
         if (!valid) {
@@ -116,7 +118,7 @@ __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64
       for (int j = 0; j < J; ++j) {
         if (pp[j] < 0) continue;
         if (MODE == 1) {
-          int64_t len = 0;
+          int len = 0;
 #pragma unroll
           for (int q = 0; q < kBags; ++q)
             if (qq[j] == q) len = e[q] - b[q];
