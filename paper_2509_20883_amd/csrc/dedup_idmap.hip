@@ -356,7 +356,7 @@ __device__ inline int lds_insert(unsigned long long* ckey, unsigned long long e,
 }
 
 __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w, int64_t n) {
-  constexpr int NT = kPartThreads, S = kPartSlots, OWN = S / NT, K = kPartPer;
+  constexpr int NT = kPartThreads, S = kPartSlots, OWN = S / NT, K = kPartFast;
   constexpr int kMaxSweeps = 1 << 10;
   constexpr int BPT = (kMaxDedupBlocks + NT - 1) / NT;
   __shared__ unsigned long long ckey[S];
@@ -395,6 +395,7 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
     cfp[q] = ~0ull;
     ccnt[q] = 0u;
   }
+  if (tid == 0) ovf = 0;
   __syncthreads();
   if (nr == 0) return;  // the whole block
   const int nb = static_cast<int>(g.nblk);
@@ -422,8 +423,11 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
     return d;
   };
 
+  bool fresh = true;  // the LDS table is clear
   if (nr <= NT * K) {
     // one pass: the thread's records tid, tid + NT, ... stay in registers
+    // (up to kPartSlots records their keys always fit the table; beyond, a
+    // full table sends the partition to the sweeps)
     int pos[K];
     TileRec x[K];
 #pragma unroll
@@ -438,8 +442,9 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
       sl[k] = -1;
       rb[k] = 0;
       if (pos[k] < 0) continue;
-      sl[k] = lds_insert(ckey, x[k].key, part_hash(x[k].key));  // nr <= S: always found
+      sl[k] = lds_insert(ckey, x[k].key, part_hash(x[k].key));
       if (sl[k] < 0) {
+        ovf = 1;
         pos[k] = -1;
         continue;
       }
@@ -447,21 +452,24 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
       rb[k] = atomicAdd(&ccnt[sl[k]], (x[k].meta & 0xFFFu) + 1u);
     }
     __syncthreads();
-    const int d = dense_list();
-    probe_store_keys(t, w, n, d, cdense, ckey, cfp, ccnt);
+    if (!ovf) {
+      const int d = dense_list();
+      probe_store_keys(t, w, n, d, cdense, ckey, cfp, ccnt);
 #pragma unroll
-    for (int k = 0; k < K; ++k) {
-      if (pos[k] < 0) continue;
-      const int64_t src = (static_cast<int64_t>(pos[k]) / g.rcap) * g.rcap + (x[k].meta >> 12);
-      w.recres[src] = make_int2(static_cast<int>(static_cast<unsigned int>(cfp[sl[k]])), static_cast<int>(rb[k]));
+      for (int k = 0; k < K; ++k) {
+        if (pos[k] < 0) continue;
+        const int64_t src = (static_cast<int64_t>(pos[k]) / g.rcap) * g.rcap + (x[k].meta >> 12);
+        w.recres[src] = make_int2(static_cast<int>(static_cast<unsigned int>(cfp[sl[k]])), static_cast<int>(rb[k]));
+      }
+      return;
     }
-    return;
+    fresh = false;
+    __syncthreads();  // every thread has read ovf before the sweeps reset it
   }
 
   // sweeps (rare: a partition far above the average size)
   int nsw = min((nr + kPartSweep - 1) / kPartSweep, kMaxSweeps);
   int s = 0;
-  bool fresh = true;  // the table is clear
   while (s < nsw) {
     if (!fresh) {
       for (int q = tid; q < S; q += NT) {

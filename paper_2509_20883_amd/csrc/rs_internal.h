@@ -33,13 +33,16 @@ constexpr int kMaxTilesPerBlock = 128;
 constexpr int kMaxDedupBlocks = 512;
 // Hash partitions of the records (a power of two); one block per partition
 // dedups its records in an LDS table of kPartSlots slots.  A partition of at
-// most kPartThreads * kPartPer (= kPartSlots) records is processed with every
-// record of a thread in registers; a larger one in sweeps of at most
-// kPartSweep records (a key's records share a sweep).
+// most kPartThreads * kPartFast records is processed with every record of a
+// thread in registers (unless its distinct keys overflow the table); a larger
+// one in sweeps of at most kPartSweep records (a key's records share a
+// sweep).
 constexpr int kMaxParts = 4096;
 constexpr int kPartThreads = 256;
 constexpr int kPartSlots = 2048;
-constexpr int kPartPer = kPartSlots / kPartThreads;  // 8
+// Records per thread of the register pass: partitions a little above
+// kPartSlots records (whose distinct keys still fit the table) stay there.
+constexpr int kPartFast = 10;
 constexpr int kPartSweep = kPartSlots * 3 / 4;       // LDS load <= 0.75
 
 // Tile of the passes over positions (4 consecutive items per thread: many

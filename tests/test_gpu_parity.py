@@ -318,7 +318,8 @@ def _mix64(z):
 def test_partition_sweeps_and_restart():
     """Partitions with more records than the per-partition LDS table (2048
     slots) are deduped in sweeps: random distinct keys (several partitions of
-    ~3000 records), and keys crafted so that every one falls in the first of
+    ~3000 records, and of ~2250 records whose keys overflow the table in the
+    register pass), and keys crafted so that every one falls in the first of
     three sweeps, which overflows the table and restarts the partition with
     more sweeps (white-box: the keys are picked with the partition hash)."""
     _log("partition sweeps")
@@ -327,6 +328,13 @@ def test_partition_sweeps_and_restart():
     vals = np.unique(g.integers(-2**62, 2**62, size=12000, dtype=np.int64))
     g.shuffle(vals)
     vals = np.concatenate([vals, vals[:500]])      # some repeats across tiles
+    off = np.concatenate([np.arange(0, len(vals), 4), [len(vals)]]).astype(np.int64)
+    _custom_batch_parity(w, vals, off)
+    # ~2250 distinct keys per partition (4 partitions): within the register
+    # pass's record count but above the table's 2048 slots, so the table
+    # fills and the partition goes to the sweeps
+    vals = np.unique(g.integers(-2**62, 2**62, size=9000, dtype=np.int64))
+    g.shuffle(vals)
     off = np.concatenate([np.arange(0, len(vals), 4), [len(vals)]]).astype(np.int64)
     _custom_batch_parity(w, vals, off)
     cand = np.unique(g.integers(-2**62, 2**62, size=40000, dtype=np.int64))
