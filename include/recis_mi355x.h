@@ -10,6 +10,10 @@
  * its backward workflow (per-id gradient aggregation using the offsets kept
  * from the forward pass, then a row-sparse Adagrad / Adam update of the rows
  * and their state in place — "Backward Update", "Optimizer", "Scatter").
+ * Beside the step: the sequence tile (a bag's rows concatenated, keeping its
+ * first or last ids), row-wise optimizer state, eviction of stale keys, the
+ * ids partition (dedup + split by owner shard) and the bucketize / mod
+ * feature transforms fused over columns.
  *
  * Conventions shared by every entry point
  *  - All array arguments are DEVICE pointers owned by the caller, unless a
@@ -27,7 +31,7 @@
  *    message for the last non-OK status of the calling thread is returned by
  *    rs_last_error().  Errors the kernels detect (a reserved key, a full
  *    table) are latched in the table and returned by the next synchronizing
- *    call (ht_size, ht_reserve, ht_destroy, rs_table_check).
+ *    call (ht_size, ht_reserve, ht_evict, ht_destroy, rs_table_check).
  *  - Keys are opaque int64.  INT64_MIN (empty) and INT64_MIN+1 (tombstone)
  *    are reserved; a key equal to either is rejected with RS_EKEY and does
  *    not take part in the step.
