@@ -203,7 +203,8 @@ rs_status ht_size(rs_table* t, int64_t* live_host, rs_stream stream);
  * later rehash drops it) and its row is pushed on a stack of free rows, in
  * ascending row order.  New keys take free rows from the top of that stack
  * (re-initialised exactly like a new row) before new rows are added.
- * Only for tables created with evictable = 1 (else RS_EINVAL).  Synchronizes
+ * Only for tables created with evictable = 1 and fewer than 2^31 rows
+ * provisioned (else RS_EINVAL).  Synchronizes
  * the stream; *n_evicted_host (may be NULL) receives the count. */
 rs_status ht_evict(rs_table* t, uint32_t max_age, int64_t* n_evicted_host, rs_stream stream);
 

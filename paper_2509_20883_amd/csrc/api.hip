@@ -743,6 +743,7 @@ rs_status ht_size(rs_table* t, int64_t* live_host, rs_stream stream) {
 rs_status ht_evict(rs_table* t, uint32_t max_age, int64_t* n_evicted_host, rs_stream stream) {
   if (!t) return fail(RS_EINVAL, "null table");
   if (t->meta_off < 0) return fail(RS_EINVAL, "the table was created without eviction (evictable = 0)");
+  if (t->rows_prov >= (int64_t(1) << 31)) return fail(RS_EINVAL, "eviction counts rows in 32 bits: fewer than 2^31 rows");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int64_t nb = std::max<int64_t>(1, (t->rows_prov + kEvictRows - 1) / kEvictRows);
   int32_t* bcount = static_cast<int32_t*>(t->alloc(sizeof(int32_t) * static_cast<size_t>(nb + 1)));
