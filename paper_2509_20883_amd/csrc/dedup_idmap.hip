@@ -189,16 +189,18 @@ __global__ __launch_bounds__(NT) void k_tile_dedup(const int64_t* __restrict__ v
       ls[k] = static_cast<int>(h);
     }
     __syncthreads();
-    // dense list of the occupied slots
+    // dense list of the occupied slots: thread tid owns slots tid + j * NT
+    // (consecutive lanes, consecutive slots: no bank conflicts), read once
     constexpr int kOwn = SLOTS / NT;
-    int occ = 0;
+    static_assert(kOwn <= 32, "occupancy mask");
+    unsigned int om = 0u;
 #pragma unroll
-    for (int j = 0; j < kOwn; ++j) occ += lkey[tid * kOwn + j] != kEncEmpty;
+    for (int j = 0; j < kOwn; ++j) om |= static_cast<unsigned int>(lkey[j * NT + tid] != kEncEmpty) << j;
     int d;
-    int at = block_excl_scan<NT>(occ, sh, d);
+    int at = block_excl_scan<NT>(__popc(om), sh, d);
 #pragma unroll
     for (int j = 0; j < kOwn; ++j)
-      if (lkey[tid * kOwn + j] != kEncEmpty) ldense[at++] = static_cast<short>(tid * kOwn + j);
+      if ((om >> j) & 1u) ldense[at++] = static_cast<short>(j * NT + tid);
     __syncthreads();
     // one record per distinct key (nrec + d <= the block's occurrences <= rcap)
     for (int q = tid; q < d; q += NT) {
@@ -410,15 +412,18 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
     }
     return cbase[lo] + (fr - cpre[lo]);
   };
+  // dense list of the occupied slots: thread tid owns slots tid + j * NT
+  // (consecutive lanes, consecutive slots: no bank conflicts), read once
+  static_assert(OWN <= 32, "occupancy mask");
   auto dense_list = [&]() {
-    int occ = 0;
+    unsigned int om = 0u;
 #pragma unroll
-    for (int j = 0; j < OWN; ++j) occ += ckey[tid * OWN + j] != kEncEmpty;
+    for (int j = 0; j < OWN; ++j) om |= static_cast<unsigned int>(ckey[j * NT + tid] != kEncEmpty) << j;
     int d;
-    int at = block_excl_scan<NT>(occ, sh, d);
+    int at = block_excl_scan<NT>(__popc(om), sh, d);
 #pragma unroll
     for (int j = 0; j < OWN; ++j)
-      if (ckey[tid * OWN + j] != kEncEmpty) cdense[at++] = static_cast<short>(tid * OWN + j);
+      if ((om >> j) & 1u) cdense[at++] = static_cast<short>(j * NT + tid);
     __syncthreads();
     return d;
   };
