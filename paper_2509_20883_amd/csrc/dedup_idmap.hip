@@ -127,10 +127,14 @@ __global__ __launch_bounds__(NT) void k_tile_dedup(const int64_t* __restrict__ v
   constexpr int TILE = NT * kDedupItems;
   constexpr int SLOTS = 2 * TILE;  // LDS hash slots (load <= 0.5)
   static_assert(TILE == kDedupTile, "tile size");
-  // lmin: the key's first position in the tile, then the key's record index
-  __shared__ unsigned long long lkey[SLOTS];
-  __shared__ unsigned int lmin[SLOTS];
-  __shared__ unsigned int lcnt[SLOTS];
+  // One LDS buffer: the hash table while the tiles are deduplicated (slot
+  // keys; lmin: the key's first position in the tile, then its record
+  // index; lcnt: its count), then the staging buffer of the partition-order
+  // copy (one 16-byte record per slot).
+  __shared__ TileRec lbuf[SLOTS];
+  unsigned long long* const lkey = reinterpret_cast<unsigned long long*>(lbuf);
+  unsigned int* const lmin = reinterpret_cast<unsigned int*>(lkey + SLOTS);
+  unsigned int* const lcnt = lmin + SLOTS;
   __shared__ short ldense[TILE];          // the tile's distinct keys: dense index -> LDS slot
   __shared__ unsigned int lpc[kMaxParts];  // the block's records per partition
   __shared__ int sh[NT / kWave + 1];
@@ -254,18 +258,37 @@ __global__ __launch_bounds__(NT) void k_tile_dedup(const int64_t* __restrict__ v
   __syncthreads();
   TileRec* srt = w.srec + blk * g.rcap;
   constexpr int U8 = 8;  // records in flight per thread
-  for (unsigned int j0 = tid; j0 < nrec; j0 += U8 * NT) {
-    TileRec r[U8];
+  // Record j goes to position lpc[partition] + rank of the partition order.
+  // Up to kStageChunks chunks of SLOTS positions: each chunk is assembled in
+  // LDS (every pass reads all records, L2-resident) and written out with
+  // coalesced full-line stores; a block with more records scatters them
+  // (runs of a few 16-byte records per partition: partial-line writes).
+  const unsigned int chunks = (nrec + SLOTS - 1) / SLOTS;
+  const bool staged = chunks <= static_cast<unsigned int>(kStageChunks);
+  for (unsigned int c = 0; c < (staged ? chunks : 1u); ++c) {
+    const unsigned int o0 = c * SLOTS;
+    const unsigned int o1 = min(o0 + static_cast<unsigned int>(SLOTS), nrec);
+    for (unsigned int j0 = tid; j0 < nrec; j0 += U8 * NT) {
+      TileRec r[U8];
 #pragma unroll
-    for (int u = 0; u < U8; ++u) {
-      const unsigned int j = j0 + u * NT;
-      if (j < nrec) r[u] = rec[j];
+      for (int u = 0; u < U8; ++u) {
+        const unsigned int j = j0 + u * NT;
+        if (j < nrec) r[u] = rec[j];
+      }
+#pragma unroll
+      for (int u = 0; u < U8; ++u) {
+        const unsigned int j = j0 + u * NT;
+        if (j >= nrec) continue;
+        const unsigned int o = lpc[part_of(r[u].key, g.logP)] + (r[u].meta >> 12);
+        const TileRec x{r[u].key, r[u].tmin, (j << 12) | (r[u].meta & 0xFFFu)};
+        if (!staged) srt[o] = x;
+        else if (o >= o0 && o < o1) lbuf[o - o0] = x;
+      }
     }
-#pragma unroll
-    for (int u = 0; u < U8; ++u) {
-      const unsigned int j = j0 + u * NT;
-      if (j < nrec)
-        srt[lpc[part_of(r[u].key, g.logP)] + (r[u].meta >> 12)] = TileRec{r[u].key, r[u].tmin, (j << 12) | (r[u].meta & 0xFFFu)};
+    if (staged) {
+      __syncthreads();
+      for (unsigned int o = o0 + tid; o < o1; o += NT) srt[o] = lbuf[o - o0];
+      __syncthreads();  // the next chunk reuses the buffer
     }
   }
 }
