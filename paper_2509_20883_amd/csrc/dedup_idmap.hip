@@ -122,6 +122,10 @@ __device__ inline uint32_t part_of(unsigned long long e, int logP) {
 // pass 1: tile dedup in LDS; one record per distinct key of a tile
 // ---------------------------------------------------------------------------
 
+// A dedup block whose records fill at most this many LDS chunks (8192
+// records each) writes their partition-order copy with coalesced stores.
+constexpr int kStageChunks = 4;
+
 template <int NT>
 __global__ __launch_bounds__(NT) void k_tile_dedup(const int64_t* __restrict__ values, int64_t n, Work w, int* err) {
   constexpr int TILE = NT * kDedupItems;

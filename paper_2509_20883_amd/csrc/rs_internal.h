@@ -30,9 +30,6 @@ static_assert(kDedupTile == 1 << kDedupTileLog2, "tile is a power of two");
 // record index inside a block fits 19 bits (occ_word = index << 12 | rank),
 // and there are at most kMaxDedupBlocks dedup blocks (n <= 2^28).
 constexpr int kMaxTilesPerBlock = 128;
-// A dedup block whose records fill at most this many LDS chunks (8192
-// records each) writes their partition-order copy with coalesced stores.
-constexpr int kStageChunks = 4;
 constexpr int kMaxDedupBlocks = 512;
 // Hash partitions of the records (a power of two); one block per partition
 // dedups its records in an LDS table of kPartSlots slots.  A partition of at
