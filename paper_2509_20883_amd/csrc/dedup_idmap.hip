@@ -262,15 +262,16 @@ __global__ __launch_bounds__(NT) void k_tile_dedup(const int64_t* __restrict__ v
   __syncthreads();
   TileRec* srt = w.srec + blk * g.rcap;
   constexpr int U8 = 8;  // records in flight per thread
-  // Record j goes to position lpc[partition] + rank of the partition order.
-  // Up to kStageChunks chunks of SLOTS positions: each chunk is assembled in
-  // LDS (every pass reads all records, L2-resident) and written out with
-  // coalesced full-line stores; a block with more records scatters them
-  // (runs of a few 16-byte records per partition: partial-line writes).
+  // Record j goes to position lpc[partition] + its rank in the partition.
+  // A block of at most kStageChunks chunks of SLOTS records assembles each
+  // chunk in LDS (every pass reads all of the block's records again) and
+  // writes it out with coalesced full-line stores; a larger block scatters
+  // the records (runs of a few 16-byte records per partition: partial-line
+  // writes, costly once the copies outgrow the memory-side cache).
   const unsigned int chunks = (nrec + SLOTS - 1) / SLOTS;
   const bool staged = chunks <= static_cast<unsigned int>(kStageChunks);
-  for (unsigned int c = 0; c < (staged ? chunks : 1u); ++c) {
-    const unsigned int o0 = c * SLOTS;
+  for (unsigned int ch = 0; ch < (staged ? chunks : 1u); ++ch) {
+    const unsigned int o0 = ch * SLOTS;
     const unsigned int o1 = min(o0 + static_cast<unsigned int>(SLOTS), nrec);
     for (unsigned int j0 = tid; j0 < nrec; j0 += U8 * NT) {
       TileRec r[U8];
