@@ -9,7 +9,11 @@ state, batch 65536, table pre-populated with 90% of the vocabulary.
 
 Prints ONE JSON line (rank 0, N = 1):
   value       = ID occurrences per second over the timed steps (whole job)
-  gbps        = algorithmic bytes per step / step time
+  gbps        = algorithmic bytes per step / step time (rows of duplicate ids
+                counted once); hbm_frac = gbps / 8 TB/s, frac_of_copy = gbps /
+                a plain 1 GiB device copy timed in the same run
+  gbps_effective_occ = the same with every occurrence's row counted (B_occ):
+                an effective bandwidth, not HBM traffic
   roofline    = the dominant kernel's algorithmic bytes / its HIP-event time
   cpu_baseline= the CPU oracle timed on a bounded sample of the same workload
 """
@@ -63,21 +67,30 @@ def parse():
     return ap.parse_args()
 
 
-def copy_calibration():
-    """A plain copy kernel of known size: 1 GiB read + 1 GiB written per launch."""
+def copy_ms(n: int = 1 << 30, reps: int = 5) -> float:
+    """Mean time (ms) of a plain device copy of n bytes (n read + n written)."""
     import torch
 
-    n = 1 << 30
     src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
     dst = torch.empty_like(src)
+    dst.copy_(src)  # first touch outside the timing
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
-    for _ in range(5):
+    for _ in range(reps):
         dst.copy_(src)
     e1.record()
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / 5
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    torch.cuda.empty_cache()
+    return ms
+
+
+def copy_calibration():
+    """A plain copy kernel of known size: 1 GiB read + 1 GiB written per launch."""
+    n = 1 << 30
+    ms = copy_ms(n)
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "ms": ms, "GBps": 2 * n / (ms * 1e-3) / 1e9}))
 
 
@@ -114,6 +127,14 @@ def b_alg(w, N, G, U, Nnew, V=None):
         grad = G * w.dim * 4
     return (8 * N + 8 * (G + 1) + 4 * N + 8 * U + 8 * U + 16 * U + 8 * U + 8 * U + Nnew * (16 + R + S)
             + 4 * N + R * U + out + grad + 4 * N + 2 * (R + S) * U)
+
+
+def b_occ(w, N, G, U, Nnew, V=None):
+    """B_occ: b_alg with the row of every gathered occurrence counted (no
+    reuse of a duplicate id's row), the traffic if no row came from a cache;
+    a bandwidth from it is an effective figure, not HBM traffic."""
+    R, _ = row_bytes(w)
+    return b_alg(w, N, G, U, Nnew, V) - R * U + R * (N if V is None else V)
 
 
 def unit_count(c: int, unit: int = 32, max_units: int = 1024) -> int:
@@ -503,6 +524,10 @@ def main():
     torch.cuda.synchronize()
     setup_s = time.time() - t_setup
     progress(f"setup done in {setup_s:.0f} s; {nsteps} steps")
+    # plain device copy in the same run (untimed for the step): the practical
+    # bandwidth the step's GB/s is also reported against
+    copy_gbps = 2 * (1 << 30) / (copy_ms(1 << 30) * 1e-3) / 1e9
+    progress(f"device copy: {copy_gbps:.0f} GB/s")
 
     def grad_of(i):
         g = batches[i][3]
@@ -636,7 +661,7 @@ def main():
         progress(f"evicted {n_ev} of {rows_before} keys in {ems:.3f} ms")
 
     # per-step sizes (read after the timed region)
-    tot_ids = tot_bytes = 0
+    tot_ids = tot_bytes = tot_occ = 0
     Us, news, dom_b = [], [], []
     scal = stepscal.cpu().numpy() if ring < nsteps else None
     for j in range(a.steps):
@@ -647,6 +672,7 @@ def main():
         tot_ids += n
         V = host_windows.get(i)
         tot_bytes += b_alg(w, n, g, U, Nnew, V)
+        tot_occ += b_occ(w, n, g, U, Nnew, V)
         if i in host_values:  # every timed step, or 5 evenly spaced ones in long runs
             hv, hw = host_values[i]
             dom_b.append(kernel_bytes(w, dom, n, g, key_stats(hv, hw)))
@@ -686,6 +712,10 @@ def main():
         "gbps": gbps,
         "hbm_frac": gbps / HBM_PEAK_GBPS,
         "bytes_alg_per_step": tot_bytes / a.steps,
+        "copy_gbps": copy_gbps,
+        "frac_of_copy": gbps / copy_gbps,
+        "bytes_occ_per_step": tot_occ / a.steps,
+        "gbps_effective_occ": tot_occ / (total_ms * 1e-3) / 1e9,
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic, "kernel_ms": dom_ms,
                      "kernel_bytes_alg": dom_bytes / a.steps},

@@ -147,3 +147,13 @@ def test_key_stats_and_kernel_bytes_by_hand():
 def test_ids_partition_bytes():
     B = _bench()
     assert B.ids_partition_bytes(100, 10, 8) == 800 + 80 + 72 + 400 + 16
+
+
+def test_b_occ_counts_every_gathered_row():
+    B = _bench()
+    w = W.workload(0)                                            # dim 16 fp32: 64-byte rows
+    R, _ = B.row_bytes(w)
+    # 100 ids over 30 unique keys: 70 re-read rows more than the algorithmic count
+    assert B.b_occ(w, 100, 10, 30, 5) - B.b_alg(w, 100, 10, 30, 5) == R * 70
+    w.mode, w.pad_len = W.NONE, 4                                # padded: only the copied window's rows
+    assert B.b_occ(w, 100, 10, 30, 5, V=40) - B.b_alg(w, 100, 10, 30, 5, V=40) == R * 10
