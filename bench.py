@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU time of the oracle sample")
     ap.add_argument("--unfused", action="store_true", help="lookup_pool_bwd + sparse_opt_step instead of the fused call")
+    ap.add_argument("--no-step-events", action="store_true",
+                    help="no timing event at the step boundaries (no per-step times, no median)")
     ap.add_argument("--pipelined", action="store_true",
                     help="run the next batch's lookup_prepare on a second stream while the current batch pools and "
                          "runs its backward (default: one stream)")
@@ -65,6 +67,20 @@ def parse():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (scales HBM byte counters)")
     return ap.parse_args()
+
+
+def host_cpu() -> dict:
+    """The host the CPU baseline ran on: its logical CPUs and CPU model."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"host_nproc": os.cpu_count(), "host_cpu_model": model}
 
 
 def copy_ms(n: int = 1 << 30, reps: int = 5) -> float:
@@ -276,7 +292,7 @@ def cpu_baseline(w, target_s):
         steps += 1
     return {"value": ids / secs, "unit": "IDs/s", "cores": 1, "kind": "oracle",
             "sample": f"{steps} consecutive full steps (batch {w.batch} x {w.n_features} features, "
-                      f"{int(ids)} ids), {secs:.1f} s of single-threaded step time"}
+                      f"{int(ids)} ids), {secs:.1f} s of single-threaded step time", **host_cpu()}
 
 
 IDS_METRIC = "ids partition (dedup + split by owner shard) IDs/sec and achieved HBM GB/s vs peak, 1 MI355X"
@@ -354,7 +370,7 @@ def bench_ids_partition(a):
             calls += 1
         dt = time.perf_counter() - t0
         cpu = {"value": calls * float(np.mean([h.size for h in host])) / dt, "unit": "IDs/s", "cores": 1,
-               "kind": "oracle", "sample": f"{calls} whole calls on the same inputs"}
+               "kind": "oracle", "sample": f"{calls} whole calls on the same inputs", **host_cpu()}
         cpu["gpu_speedup"] = res["value"] / cpu["value"]
         res["cpu_baseline"] = cpu
     print(json.dumps(res), flush=True)
@@ -424,7 +440,7 @@ def bench_feature_op(a):
             calls += 1
         dt = time.perf_counter() - t0
         cpu = {"value": calls * n / dt, "unit": "values/s", "cores": 1, "kind": "oracle",
-               "sample": f"{calls} whole calls on the same inputs"}
+               "sample": f"{calls} whole calls on the same inputs", **host_cpu()}
         cpu["gpu_speedup"] = res["value"] / cpu["value"]
         res["cpu_baseline"] = cpu
     print(json.dumps(res), flush=True)
@@ -593,6 +609,8 @@ def main():
             e1.record()
     torch.cuda.synchronize()
     e_start, e_stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # step boundaries (serial schedule): per-step times for the median
+    step_ev = [torch.cuda.Event(enable_timing=True) for _ in range(a.steps)] if not a.no_step_events else []
     pipelined = a.pipelined
     e_start.record()
     if pipelined:
@@ -631,12 +649,18 @@ def main():
         for j in range(a.steps):
             set_events(j)
             step(a.warmup + j)
+            if step_ev and j + 1 < a.steps:
+                step_ev[j].record()
     e_stop.record()
     torch.cuda.synchronize()
     for k in cands:
         table.set_kernel_events(k, None, None)
     cand_ms = {k: float(np.mean([e0.elapsed_time(e1) for e0, e1 in cand_ev[k].values()])) for k in cands}
     total_ms = e_start.elapsed_time(e_stop)
+    step_ms = None
+    if step_ev and not pipelined:
+        bounds = [e_start] + step_ev[:a.steps - 1] + [e_stop]
+        step_ms = [bounds[j].elapsed_time(bounds[j + 1]) for j in range(a.steps)]
     table.check()
     eviction = None
     if a.evict_age >= 0:
@@ -700,6 +724,7 @@ def main():
         "steps": a.steps,
         "warmup": a.warmup,
         "ms_per_step": ms_per_step,
+        "ms_per_step_median": float(np.median(step_ms)) if step_ms else None,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
