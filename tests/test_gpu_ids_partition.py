@@ -52,7 +52,10 @@ def _zipf_ids(n, V, s, seed):
 
 
 @pytest.mark.parametrize("n,G", [(1, 1), (1, 8), (100, 3), (1024, 2), (1025, 8), (4097, 5), (70001, 8),
-                                 (70001, 1), (131072, 64), (250003, 1000), (250003, 1024), (40000, 7)])
+                                 (70001, 1), (131072, 64), (250003, 1000), (250003, 1024), (40000, 7),
+                                 # owner-count tables of 8256 and 12800 entries: past the histogram's
+                                 # own scan (at most 8192), scanned by one block of their own
+                                 (131073, 64), (131072, 100)])
 def test_ids_partition_matches_oracle(n, G):
     _log(f"ids_partition n={n} G={G}")
     part = R.IdsPartition()
