@@ -631,9 +631,9 @@ def main():
 
     dom = max(("pool", "bwd_short", "bwd_long"), key=wmed)
     cands = (dom,)
-    # timed region: K steps, the dominant kernel bracketed by HIP events on the
-    # step's stream in every 4th step (a timing event costs ~6 us of idle GPU
-    # on each side of the kernel; the others run without them)
+    # timed region: K steps, the dominant kernel timed in every 4th step by
+    # start / stop events that its launch hands to the dispatch (timestamps
+    # of the kernel's own execution on the step's stream)
     sampled = list(range(0, a.steps, 4))
     cand_ev = {k: {j: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for j in sampled}
                for k in cands}

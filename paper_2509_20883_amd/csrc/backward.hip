@@ -23,6 +23,8 @@
 // Without the optimizer (lookup_pool_bwd) the same kernels write grad_unique.
 #include "device_common.h"
 
+#include <hip/hip_ext.h>
+
 namespace rs {
 
 // Sum of v over the LANES lanes of a lane group (every lane gets it).
@@ -404,15 +406,18 @@ static hipError_t bwd_launch(const TableDev& t, const Work& w, const int64_t* of
   // grid-stride loops over device-side counts (U, units, hot keys): a grid
   // of at most kResident blocks per strategy keeps every CU busy without
   // dispatching wavefronts that would find no work
-  if (ev_s && ev_s[0]) (void)hipEventRecord(ev_s[0], s);
-  k_bwd_short<WT, GT, LANES, MODE, FUSED><<<grid_for(n, GPB, kResident), kBlock, 0, s>>>(t, w, offsets, g, gu, o);
-  if (ev_s && ev_s[1]) (void)hipEventRecord(ev_s[1], s);
-  if (ev_l && ev_l[0]) (void)hipEventRecord(ev_l[0], s);
+  // optional timing events are timestamped by the dispatches themselves
+  // (short keys: their kernel; hot keys: unit sums start to finish end)
+  hipEvent_t s0 = ev_s ? ev_s[0] : nullptr, s1 = ev_s ? ev_s[1] : nullptr;
+  hipEvent_t l0 = ev_l ? ev_l[0] : nullptr, l1 = ev_l ? ev_l[1] : nullptr;
+  hipExtLaunchKernelGGL((k_bwd_short<WT, GT, LANES, MODE, FUSED>), dim3(grid_for(n, GPB, kResident)), dim3(kBlock), 0,
+                        s, s0, s1, 0, t, w, offsets, g, gu, o);
   // one lane group per possible unit (the device-side count is at most
   // 2n/kUnit + 2): no group takes a second unit while others are idle
-  k_bwd_long<GT, LANES, MODE><<<grid_for(2 * (n / kUnit) + 2, GPB), kBlock, 0, s>>>(w, offsets, g);
-  k_bwd_long_finish<WT, E, LANES, FUSED><<<grid_for(n / kLong + 1, 1, 4 * kResident), kBlock, 0, s>>>(t, w, gu, o);
-  if (ev_l && ev_l[1]) (void)hipEventRecord(ev_l[1], s);
+  hipExtLaunchKernelGGL((k_bwd_long<GT, LANES, MODE>), dim3(grid_for(2 * (n / kUnit) + 2, GPB)), dim3(kBlock), 0, s,
+                        l0, nullptr, 0, w, offsets, g);
+  hipExtLaunchKernelGGL((k_bwd_long_finish<WT, E, LANES, FUSED>), dim3(grid_for(n / kLong + 1, 1, 4 * kResident)),
+                        dim3(kBlock), 0, s, nullptr, l1, 0, t, w, gu, o);
   return hipGetLastError();
 }
 

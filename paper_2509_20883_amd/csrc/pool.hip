@@ -13,6 +13,8 @@
 // them together, for single-id and long bags alike.
 #include "device_common.h"
 
+#include <hip/hip_ext.h>
+
 namespace rs {
 
 
@@ -216,15 +218,18 @@ __global__ __launch_bounds__(kBlock) void k_pool_none(TableDev t, Work w, const 
   }
 }
 
+// The launch takes optional start / stop events that the dispatch itself
+// timestamps (the kernel's own execution, no extra packets on the stream).
 template <typename WT, int LANES>
 static hipError_t pool_mode(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int64_t bags,
-                            int mode, int64_t pad_len, void* out, uint8_t* mask, hipStream_t s) {
+                            int mode, int64_t pad_len, void* out, uint8_t* mask, hipEvent_t e0, hipEvent_t e1,
+                            hipStream_t s) {
   constexpr int GPB = kBlock / LANES;
   if (mode == 2 || mode == 3) {
     constexpr int TCH = GPB > 64 ? GPB : 64;
     const int64_t nch = (pad_len + TCH - 1) / TCH;
-    k_pool_none<WT, LANES><<<grid_for(bags * nch, 1, 1 << 20), kBlock, 0, s>>>(t, w, offsets, n, bags, pad_len,
-                                                                             mode == 3, static_cast<WT*>(out), mask);
+    hipExtLaunchKernelGGL((k_pool_none<WT, LANES>), dim3(grid_for(bags * nch, 1, 1 << 20)), dim3(kBlock), 0, s, e0, e1,
+                          0, t, w, offsets, n, bags, pad_len, mode == 3, static_cast<WT*>(out), mask);
   } else {
     // mostly single-id bags (n <= 2 bags): a lane group takes 8 bags and
     // requests their rows together; longer bags: 4 bags, 16-row chunks
@@ -232,11 +237,19 @@ static hipError_t pool_mode(const TableDev& t, const Work& w, const int64_t* off
     float* o = static_cast<float*>(out);
     const unsigned gf = grid_for(bags, GPB * 8, 1 << 20), gm = grid_for(bags, GPB * 4, 1 << 20);
     if (mode == 1) {
-      if (few) k_pool<WT, LANES, 1, 8, 8><<<gf, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
-      else k_pool<WT, LANES, 1, 16, 4><<<gm, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
+      if (few)
+        hipExtLaunchKernelGGL((k_pool<WT, LANES, 1, 8, 8>), dim3(gf), dim3(kBlock), 0, s, e0, e1, 0, t, w, offsets, n,
+                              bags, o);
+      else
+        hipExtLaunchKernelGGL((k_pool<WT, LANES, 1, 16, 4>), dim3(gm), dim3(kBlock), 0, s, e0, e1, 0, t, w, offsets,
+                              n, bags, o);
     } else {
-      if (few) k_pool<WT, LANES, 0, 8, 8><<<gf, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
-      else k_pool<WT, LANES, 0, 16, 4><<<gm, kBlock, 0, s>>>(t, w, offsets, n, bags, o);
+      if (few)
+        hipExtLaunchKernelGGL((k_pool<WT, LANES, 0, 8, 8>), dim3(gf), dim3(kBlock), 0, s, e0, e1, 0, t, w, offsets, n,
+                              bags, o);
+      else
+        hipExtLaunchKernelGGL((k_pool<WT, LANES, 0, 16, 4>), dim3(gm), dim3(kBlock), 0, s, e0, e1, 0, t, w, offsets,
+                              n, bags, o);
     }
   }
   return hipGetLastError();
@@ -244,16 +257,16 @@ static hipError_t pool_mode(const TableDev& t, const Work& w, const int64_t* off
 
 template <typename WT>
 static hipError_t pool_dim(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int64_t bags, int mode,
-                           int64_t pad_len, void* out, uint8_t* mask, hipStream_t s) {
+                           int64_t pad_len, void* out, uint8_t* mask, hipEvent_t e0, hipEvent_t e1, hipStream_t s) {
   constexpr int E = 16 / static_cast<int>(sizeof(WT));
   switch (t.dim / E) {
-    case 1: return pool_mode<WT, 1>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
-    case 2: return pool_mode<WT, 2>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
-    case 4: return pool_mode<WT, 4>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
-    case 8: return pool_mode<WT, 8>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
-    case 16: return pool_mode<WT, 16>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
-    case 32: return pool_mode<WT, 32>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
-    case 64: return pool_mode<WT, 64>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
+    case 1: return pool_mode<WT, 1>(t, w, offsets, n, bags, mode, pad_len, out, mask, e0, e1, s);
+    case 2: return pool_mode<WT, 2>(t, w, offsets, n, bags, mode, pad_len, out, mask, e0, e1, s);
+    case 4: return pool_mode<WT, 4>(t, w, offsets, n, bags, mode, pad_len, out, mask, e0, e1, s);
+    case 8: return pool_mode<WT, 8>(t, w, offsets, n, bags, mode, pad_len, out, mask, e0, e1, s);
+    case 16: return pool_mode<WT, 16>(t, w, offsets, n, bags, mode, pad_len, out, mask, e0, e1, s);
+    case 32: return pool_mode<WT, 32>(t, w, offsets, n, bags, mode, pad_len, out, mask, e0, e1, s);
+    case 64: return pool_mode<WT, 64>(t, w, offsets, n, bags, mode, pad_len, out, mask, e0, e1, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -261,10 +274,9 @@ static hipError_t pool_dim(const TableDev& t, const Work& w, const int64_t* offs
 hipError_t launch_pool(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int64_t bags, int mode,
                        int64_t pad_len, void* out, uint8_t* mask, hipEvent_t* ev, hipStream_t s) {
   if (bags <= 0) return hipSuccess;
-  if (ev && ev[0]) (void)hipEventRecord(ev[0], s);
-  const hipError_t e = t.row_dtype ? pool_dim<uint16_t>(t, w, offsets, n, bags, mode, pad_len, out, mask, s)
-                                   : pool_dim<float>(t, w, offsets, n, bags, mode, pad_len, out, mask, s);
-  if (ev && ev[1]) (void)hipEventRecord(ev[1], s);
+  hipEvent_t e0 = ev ? ev[0] : nullptr, e1 = ev ? ev[1] : nullptr;
+  const hipError_t e = t.row_dtype ? pool_dim<uint16_t>(t, w, offsets, n, bags, mode, pad_len, out, mask, e0, e1, s)
+                                   : pool_dim<float>(t, w, offsets, n, bags, mode, pad_len, out, mask, e0, e1, s);
   return e;
 }
 
