@@ -365,9 +365,14 @@ rs_status fused_bucketize(const float* values, int64_t n, const int64_t* col_off
 rs_status fused_mod(const int64_t* values, int64_t n, const int64_t* col_offsets, int32_t ncols,
                     const int64_t* moduli, int64_t* out, int32_t validate, rs_stream stream);
 
-/* Kernel timing hook: from now on, hipEvent_t `start` / `stop` are recorded on
- * the call's stream immediately before / after every launch of the named
- * kernel (NULL, NULL clears it).  For measurement only. */
+/* Kernel timing hook: from now on, hipEvent_t `start` / `stop` time every
+ * launch of the named kernel (NULL, NULL clears it).  For RS_K_POOL,
+ * RS_K_BWD_SHORT and RS_K_BWD_LONG the events are handed to the launch and
+ * timestamped by the dispatch (the kernel's own execution; for RS_K_BWD_LONG
+ * from the unit sums' start to the finish's end); for the other kernels they
+ * are recorded on the call's stream immediately before / after the launch.
+ * The events must exist (created, e.g. recorded once) before the call that
+ * uses them.  For measurement only. */
 typedef enum {
   RS_K_TILE_DEDUP = 0,     /* tile dedup in LDS, records per hash partition     */
   RS_K_PARTITION = 1,      /* per-partition dedup + IDMap probe, then the
