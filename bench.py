@@ -64,6 +64,8 @@ def parse():
                     help="ids-partition: time the fused dedup + owner split alone on its one-million-id input; "
                          "bucketize / mod: the fused feature transforms on 100 columns of 10,000 values")
     ap.add_argument("--shards", type=int, default=None, help="owner shards of --op ids-partition (default 8)")
+    ap.add_argument("--ceilings", action="store_true",
+                    help="measure plain device read / write / copy / random-row gather bandwidth and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (scales HBM byte counters)")
     return ap.parse_args()
@@ -101,6 +103,45 @@ def copy_ms(n: int = 1 << 30, reps: int = 5) -> float:
     del src, dst
     torch.cuda.empty_cache()
     return ms
+
+
+def ceilings():
+    """Practical HBM ceilings of plain device operations on 2 GiB buffers
+    (torch's own kernels; bytes moved / median time of 5): sequential read
+    (a sum), streaming write (a fill), copy, and a gather of random 256-byte
+    rows into a contiguous output."""
+    import torch
+
+    n = 1 << 29  # fp32 elements: 2 GiB
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    rows = x.view(-1, 64)  # 256-byte rows
+    g = torch.Generator(device="cuda")
+    g.manual_seed(2509)
+    idx = torch.randint(0, rows.shape[0], (rows.shape[0] // 4,), device="cuda", generator=g)
+    out = torch.empty(idx.numel(), 64, dtype=torch.float32, device="cuda")
+    tests = {
+        "read (sum)": (lambda: x.sum(), 4 * n),
+        "write (fill)": (lambda: y.fill_(2.0), 4 * n),
+        "copy": (lambda: y.copy_(x), 8 * n),
+        "random 256-byte rows gathered (read + write)": (lambda: torch.index_select(rows, 0, idx, out=out),
+                                                          2 * 256 * idx.numel() + 8 * idx.numel()),
+    }
+    res = {}
+    for name, (fn, nbytes) in tests.items():
+        fn()
+        torch.cuda.synchronize()
+        ms = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        m = float(np.median(ms))
+        res[name] = {"bytes": nbytes, "ms": m, "GBps": nbytes / (m * 1e-3) / 1e9}
+    print(json.dumps({"ceilings": res, "peak_GBps": HBM_PEAK_GBPS}))
 
 
 def copy_calibration():
@@ -450,6 +491,9 @@ def main():
     a = parse()
     if a.copy_calibration:
         copy_calibration()
+        return
+    if a.ceilings:
+        ceilings()
         return
     if a.gpus != 1:
         print(json.dumps({"error": "single-GPU build: run with --gpus 1 (the multi-GPU path is a design only)"}))
