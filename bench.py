@@ -3,18 +3,21 @@
 One step = lookup_pool_fwd (dedup, IDMap find-or-insert with row init, fused
 gather + pool) + lookup_pool_bwd_opt (per-unique gradient sums fused with the
 row-sparse optimizer) over one batch of synthetic input already resident in
-HBM.  Default workload: 26 single-hot categorical features, each its own
-logical table (fused into one physical table), dim 64 fp32 rows with Adam
-state, batch 65536, table pre-populated with 90% of the vocabulary.
+HBM.  Default workload: the growing dynamic table -- 200 features (150
+single-hot, 50 multi-hot with Poisson(10) bags) in one hash table that starts
+at 2e7 live ids and takes 3e5 never-seen ids per step, dim 64 fp32 rows with
+Adam state, batch 32768, sum pooling; the IDMap is resized inside the run.
 
 Prints ONE JSON line (rank 0, N = 1):
   value       = ID occurrences per second over the timed steps (whole job)
   gbps        = algorithmic bytes per step / step time (rows of duplicate ids
                 counted once); hbm_frac = gbps / 8 TB/s, frac_of_copy = gbps /
-                a plain 1 GiB device copy timed in the same run
+                a 1 GiB device copy (the library's copy probe) timed in the
+                same run
   gbps_effective_occ = the same with every occurrence's row counted (B_occ):
                 an effective bandwidth, not HBM traffic
-  roofline    = the dominant kernel's algorithmic bytes / its HIP-event time
+  roofline    = the dominant kernel's algorithmic bytes (the step's byte terms
+                that kernel moves) / its HIP-event time
   cpu_baseline= the CPU oracle timed on a bounded sample of the same workload
 """
 from __future__ import annotations
@@ -40,9 +43,10 @@ HBM_PEAK_GBPS = 8000.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default: 100 for the growing table, whose run includes resizes; else 20)")
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", type=int, default=1)
+    ap.add_argument("--workload", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target CPU time of the oracle sample")
     ap.add_argument("--unfused", action="store_true", help="lookup_pool_bwd + sparse_opt_step instead of the fused call")
@@ -67,7 +71,11 @@ def parse():
     ap.add_argument("--ceilings", action="store_true",
                     help="measure plain device read / write / copy / random-row gather bandwidth and exit")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="only run a plain 1 GiB device-to-device copy 5 times (scales HBM byte counters)")
+                    help="only run the library's 1 GiB copy probe 5 times (scales HBM byte counters)")
+    ap.add_argument("--traffic-from", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR"),
+                    help="write profiles/traffic_<workload>*.{md,json} from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE "
+                         "output directories of a step run and of a --copy-calibration run (no GPU needed)")
+    ap.add_argument("--traffic-cmd", default="", help="the profiled command, recorded in the summary")
     return ap.parse_args()
 
 
@@ -85,70 +93,161 @@ def host_cpu() -> dict:
     return {"host_nproc": os.cpu_count(), "host_cpu_model": model}
 
 
-def copy_ms(n: int = 1 << 30, reps: int = 5) -> float:
-    """Mean time (ms) of a plain device copy of n bytes (n read + n written)."""
+def _probe_ms(fn, reps: int = 5) -> float:
+    """Median time (ms) of fn() over reps launches, each bracketed by events."""
     import torch
+
+    fn()
+    torch.cuda.synchronize()
+    ms = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms.append(e0.elapsed_time(e1))
+    return float(np.median(ms))
+
+
+def copy_ms(n: int = 1 << 30, reps: int = 5) -> float:
+    """Time (ms) of the library's copy probe over n bytes (n read + n written)."""
+    import torch
+
+    from paper_2509_20883_amd import recis as R
 
     src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
     dst = torch.empty_like(src)
-    dst.copy_(src)  # first touch outside the timing
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        dst.copy_(src)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / reps
+    ms = _probe_ms(lambda: R.bandwidth_probe("copy", src, dst), reps)
     del src, dst
     torch.cuda.empty_cache()
     return ms
 
 
 def ceilings():
-    """Practical HBM ceilings of plain device operations on 2 GiB buffers
-    (torch's own kernels; bytes moved / median time of 5): sequential read
-    (a sum), streaming write (a fill), copy, and a gather of random 256-byte
-    rows into a contiguous output."""
+    """Practical HBM ceilings of this GPU, from the library's bandwidth probes
+    (hand-written kernels with the step's access widths and launch shapes) on
+    2 GiB buffers: sequential read, streaming write, copy, a gather of random
+    256-byte rows into a streamed output, and a random read-modify-write of
+    768-byte rows (a dim-64 fp32 row with its two Adam moments).  Bytes moved /
+    median time of 5 launches."""
     import torch
 
-    n = 1 << 29  # fp32 elements: 2 GiB
-    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    from paper_2509_20883_amd import recis as R
+
+    nb = 1 << 31
+    x = torch.ones(nb // 4, dtype=torch.float32, device="cuda")
     y = torch.empty_like(x)
-    rows = x.view(-1, 64)  # 256-byte rows
+    sink = torch.zeros(4, dtype=torch.int32, device="cuda")
     g = torch.Generator(device="cuda")
     g.manual_seed(2509)
-    idx = torch.randint(0, rows.shape[0], (rows.shape[0] // 4,), device="cuda", generator=g)
-    out = torch.empty(idx.numel(), 64, dtype=torch.float32, device="cuda")
+    n_g = nb // 256 // 4  # a quarter of the 256-byte rows, gathered
+    idx_g = torch.randint(0, nb // 256, (n_g,), device="cuda", generator=g)
+    out = torch.empty(n_g * 64, dtype=torch.float32, device="cuda")
+    n_r = nb // 768 // 4  # a quarter of the 768-byte rows, updated (distinct rows)
+    idx_r = torch.randperm(nb // 768, device="cuda", generator=g)[:n_r]
     tests = {
-        "read (sum)": (lambda: x.sum(), 4 * n),
-        "write (fill)": (lambda: y.fill_(2.0), 4 * n),
-        "copy": (lambda: y.copy_(x), 8 * n),
-        "random 256-byte rows gathered (read + write)": (lambda: torch.index_select(rows, 0, idx, out=out),
-                                                          2 * 256 * idx.numel() + 8 * idx.numel()),
+        "read": (lambda: R.bandwidth_probe("read", x, sink), nb),
+        "write (streaming)": (lambda: R.bandwidth_probe("write", y), nb),
+        "copy": (lambda: R.bandwidth_probe("copy", x, y), 2 * nb),
+        "gather of random 256-byte rows (read + streamed write + index)":
+            (lambda: R.bandwidth_probe("gather", x, out, idx_g, row_bytes=256), (2 * 256 + 8) * n_g),
+        "read-modify-write of random 768-byte rows (+ index)":
+            (lambda: R.bandwidth_probe("rmw", x, None, idx_r, row_bytes=768), (2 * 768 + 8) * n_r),
     }
     res = {}
     for name, (fn, nbytes) in tests.items():
-        fn()
-        torch.cuda.synchronize()
-        ms = []
-        for _ in range(5):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            fn()
-            e1.record()
-            torch.cuda.synchronize()
-            ms.append(e0.elapsed_time(e1))
-        m = float(np.median(ms))
+        m = _probe_ms(fn)
         res[name] = {"bytes": nbytes, "ms": m, "GBps": nbytes / (m * 1e-3) / 1e9}
     print(json.dumps({"ceilings": res, "peak_GBps": HBM_PEAK_GBPS}))
 
 
 def copy_calibration():
-    """A plain copy kernel of known size: 1 GiB read + 1 GiB written per launch."""
+    """The library's copy probe over 1 GiB (1 GiB read + 1 GiB written per
+    launch), five launches: the reference for scaling HBM byte counters."""
     n = 1 << 30
     ms = copy_ms(n)
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "ms": ms, "GBps": 2 * n / (ms * 1e-3) / 1e9}))
+
+
+def _counter_rows(d: str):
+    """Rows of the counter_collection CSV under a rocprofv3 output directory."""
+    import csv
+    import glob
+
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise FileNotFoundError(f"no counter_collection.csv under {d}")
+    with open(files[0]) as fh:
+        return list(csv.DictReader(fh))
+
+
+# kernels whose last dispatch in a counter run is one step's launch, by the
+# name the roofline uses (the hot-key backward is its unit sums + finish)
+TRAFFIC_KERNELS = {"pool": ("rs::k_pool<", "rs::k_pool_none<"), "bwd_short": ("rs::k_bwd_short<",),
+                   "bwd_long": ("rs::k_bwd_long<", "rs::k_bwd_long_finish<")}
+
+
+def traffic_from(a):
+    """HBM bytes per launch from FETCH_SIZE / WRITE_SIZE (KiB per dispatch),
+    each scaled by what the same counter reads for the library's copy probe
+    of 1 GiB read + 1 GiB written; the step's kernels are taken at their last
+    dispatch (the last step of the profiled run)."""
+    from collections import defaultdict
+
+    from paper_2509_20883_amd import workloads as W
+
+    fdir, wdir, cfdir, cwdir = a.traffic_from
+    gib_kib = (1 << 30) / 1024
+
+    def calib(d):
+        vals = [float(r["Counter_Value"]) for r in _counter_rows(d) if "k_probe_copy" in r["Kernel_Name"]]
+        if not vals:
+            raise RuntimeError(f"no copy-probe dispatch in {d}")
+        return gib_kib / float(np.median(vals))
+
+    fs, ws = calib(cfdir), calib(cwdir)
+
+    def last(d):
+        by = defaultdict(list)
+        for r in _counter_rows(d):
+            name = r["Kernel_Name"].split("(")[0].replace("void ", "").strip()
+            by[name].append((int(r["Dispatch_Id"]), float(r["Counter_Value"])))
+        return {k: max(v)[1] * 1024 for k, v in by.items()}
+
+    F, Wr = last(fdir), last(wdir)
+    wl = W.describe(W.workload(a.workload))["workload"]
+    step = sorted((k for k in F if k.startswith("rs::") and "probe" not in k and "rehash" not in k
+                   and "map_rows" not in k and "k_occ_init<false>" not in k), key=lambda k: -(F[k] + Wr.get(k, 0)))
+    lines = [f"# HBM traffic per launch: {wl}", "",
+             "Counters `FETCH_SIZE` and `WRITE_SIZE` (KiB per dispatch), each in its own run, at the last step of", "",
+             "```", a.traffic_cmd or "(command not recorded)", "```", "",
+             "scaled by the same counters on the library's copy probe of 1 GiB read + 1 GiB written "
+             f"(`bench.py --copy-calibration`): fetch x{fs:.3f}, write x{ws:.3f}.  Converted by "
+             "`bench.py --traffic-from`.", "",
+             "| kernel | fetch MB | write MB |", "|---|---|---|"]
+    tf = tw = 0.0
+    for k in step:
+        f, x = F[k] * fs / 1e6, Wr.get(k, 0.0) * ws / 1e6
+        tf += f
+        tw += x
+        lines.append(f"| `{k}` | {f:.1f} | {x:.1f} |")
+    lines += [f"| step total | {tf:.0f} | {tw:.0f} |", ""]
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    with open(os.path.join(ROOT, "profiles", f"traffic_{wl}.md"), "w") as fh:
+        fh.write("\n".join(lines))
+    for kern, prefixes in TRAFFIC_KERNELS.items():
+        names = [k for k in step if k.startswith(prefixes)]
+        if not names:
+            continue
+        fb = sum(F[k] for k in names) * fs
+        wb = sum(Wr.get(k, 0.0) for k in names) * ws
+        rec = {"kernel": kern, "kernels": names, "workload": wl, "bytes_per_launch": fb + wb, "fetch_bytes": fb,
+               "write_bytes": wb, "fetch_scale": fs, "write_scale": ws, "kernel_source_hash": kernel_source_hash(kern),
+               "counters_from": f"profiles/traffic_{wl}.md"}
+        with open(os.path.join(ROOT, "profiles", f"traffic_{wl}_{kern}.json"), "w") as fh:
+            json.dump(rec, fh, indent=1)
+    print("\n".join(lines))
 
 
 KERNEL_SOURCES = {"pool": "pool.hip", "bwd_short": "backward.hip", "bwd_long": "backward.hip"}
@@ -213,45 +312,66 @@ def window_mask(w, offsets: np.ndarray, n: int):
     return (t >= skip) & (t < skip + w.pad_len)
 
 
-def key_stats(values: np.ndarray, window=None, long_threshold: int = 32):
+def key_stats(values: np.ndarray, offsets: np.ndarray, window=None, long_threshold: int = 32):
     """Host-side split of a batch into short keys (<= 32 occurrences) and hot
     keys; Nw_* count the occurrences that carry a gradient row (inside the
-    padded modes' windows)."""
+    padded modes' windows), Gb_* the distinct bags those occurrences lie in."""
     uk, inv, cnt = np.unique(values, return_inverse=True, return_counts=True)
+    inv = inv.reshape(-1)
     cw = cnt if window is None else np.bincount(inv[window], minlength=uk.size)
     hot = cnt > long_threshold
+    G = offsets.size - 1
+    bag = np.repeat(np.arange(G, dtype=np.int64), np.diff(offsets))
+    hot_occ = hot[inv]
+    carry = np.ones(values.size, dtype=bool) if window is None else window
+
+    def distinct_bags(sel):
+        return int(np.count_nonzero(np.bincount(bag[sel & carry], minlength=G)))
+
     return {"U": int(cnt.size), "U_short": int((~hot).sum()), "N_short": int(cnt[~hot].sum()),
             "U_long": int(hot.sum()), "N_long": int(cnt[hot].sum()),
             "Nw_short": int(cw[~hot].sum()), "Nw_long": int(cw[hot].sum()), "V": int(cw.sum()),
+            "Gb_short": distinct_bags(~hot_occ), "Gb_long": distinct_bags(hot_occ),
             "units": int(sum(unit_count(int(c)) for c in cnt[hot]))}
 
 
 def kernel_bytes(w, kernel, N, G, ks):
-    """Algorithmic bytes of one launch of the largest kernels (each array
-    element the kernel must touch, counted once; rows of duplicate ids once)."""
+    """Bytes of one launch of the largest kernels: (alg, impl).
+
+    alg: the step's algorithmic byte terms (the B_alg formula) that this
+    kernel moves -- pool: offsets, the inverse read, the row ids read, the
+    unique rows, the output; backward: the upstream gradient rows (each
+    gradient row once), the inverse read of the kernel's occurrences, the
+    row + state read-modify-write of its keys.  impl: every array element the
+    implementation touches, counted once (alg plus its own bookkeeping:
+    occurrence lists, segment descriptors, partial rows)."""
     R, S = row_bytes(w)
     U = ks["U"]
-    gr = R if w.mode in (2, 3) else w.dim * 4
+    padded = w.mode in (2, 3)
+    gr = R if padded else w.dim * 4
     if kernel == "pool":
-        if w.mode in (2, 3):
-            V = ks["V"]
-            # offsets, row id + list position of each copied id, padded rows
-            # + mask, unique rows, the list entries of all ids
-            return 8 * (G + 1) + 12 * V + G * w.pad_len * R + G * w.pad_len + R * U + 4 * N
-        # offsets, inverse, occurrence ranks, row ids, segment descriptors,
-        # unique rows, output, occurrence list
-        return 8 * (G + 1) + 4 * N + 4 * N + 8 * U + 16 * U + R * U + G * w.dim * 4 + 4 * N
+        out = G * w.pad_len * R + G * w.pad_len if padded else G * w.dim * 4
+        alg = 8 * (G + 1) + 4 * N + 8 * U + R * U + out
+        # the kernel reads each id's row id (8 B) and list position (4 B) and
+        # writes the list's gradient-row entry (4 B; 8 B with the mean scale)
+        ref = 8 if w.mode == 1 else 4
+        impl = 8 * (G + 1) + 12 * N + R * U + out + ref * N
+        return alg, impl
     if kernel == "bwd_short":
         Us, Ns, Nw = ks["U_short"], ks["N_short"], ks["Nw_short"]
-        # segment descriptors, occurrence list, one upstream gradient row per
-        # occurrence that has one, row + state read-modify-write
-        return 16 * U + 4 * Ns + gr * Nw + 2 * (R + S) * Us
+        grad_alg = gr * (Nw if padded else ks["Gb_short"])
+        alg = grad_alg + 4 * Ns + 2 * (R + S) * Us
+        # segment descriptors of every key, one gradient row per occurrence
+        impl = 16 * U + 4 * Ns + gr * Nw + 2 * (R + S) * Us
+        return alg, impl
     if kernel == "bwd_long":
         Ul, Nl, Nw, nu = ks["U_long"], ks["N_long"], ks["Nw_long"], ks["units"]
-        # unit sums: unit descriptors, occurrence list, gradient rows, one
-        # partial row written per unit; finish: partial rows read, row + state
-        # read-modify-write of each hot key
-        return 16 * nu + 4 * Nl + gr * Nw + 4 * w.dim * nu + 4 * w.dim * nu + 2 * (R + S) * Ul
+        grad_alg = gr * (Nw if padded else ks["Gb_long"])
+        alg = grad_alg + 4 * Nl + 2 * (R + S) * Ul
+        # unit descriptors, one gradient row per occurrence, one partial row
+        # written and read back per unit
+        impl = 16 * nu + 4 * Nl + gr * Nw + 2 * 4 * w.dim * nu + 2 * (R + S) * Ul
+        return alg, impl
     raise KeyError(kernel)
 
 
@@ -489,6 +609,9 @@ def bench_feature_op(a):
 
 def main():
     a = parse()
+    if a.traffic_from:
+        traffic_from(a)
+        return
     if a.copy_calibration:
         copy_calibration()
         return
@@ -507,6 +630,8 @@ def main():
     from paper_2509_20883_amd import workloads as W
 
     w = W.workload(a.workload)
+    if a.steps is None:
+        a.steps = 100 if a.workload == 4 else 20
     if a.optimizer:
         w.opt = OPTIMIZERS.index(a.optimizer)
         if w.opt == 2:
@@ -543,8 +668,9 @@ def main():
     batches, grads = [], []
     gen = torch.Generator(device=dev)
     gen.manual_seed(2509)
-    stat_steps = set(np.linspace(a.warmup, nsteps - 1, num=min(a.steps, 5)).round().astype(int).tolist()) \
-        if a.steps > 30 else set(range(a.warmup, nsteps))
+    # host-side key statistics (for the dominant kernel's bytes) of at most 5
+    # evenly spaced timed steps
+    stat_steps = set(np.linspace(a.warmup, nsteps - 1, num=min(a.steps, 5)).round().astype(int).tolist())
     host_values, host_windows = {}, {}
     for s in range(nsteps):
         bv, bo = hb[s]
@@ -554,7 +680,7 @@ def main():
         if win is not None:
             host_windows[s] = int(win.sum())
         if s in stat_steps:
-            host_values[s] = (bv, win)
+            host_values[s] = (bv, bo, win)
         batches.append((torch.from_numpy(bv).to(dev), torch.from_numpy(bo).to(dev), nb, gb))
         if s < 4:
             if w.mode in (2, 3):
@@ -697,6 +823,7 @@ def main():
     # step boundaries (serial schedule): per-step times for the median
     step_ev = [torch.cuda.Event(enable_timing=True) for _ in range(a.steps)] if not a.no_step_events else []
     pipelined = a.pipelined
+    caps = [table.capacity()]
     e_start.record()
     if pipelined:
         # the library records the dominant kernel's events at each launch; set
@@ -736,6 +863,9 @@ def main():
             step(a.warmup + j)
             if step_ev and j + 1 < a.steps:
                 step_ev[j].record()
+            # the host grows the IDMap inside the call when it must: its
+            # capacity after the call tells whether this step resized it
+            caps.append(table.capacity())
     e_stop.record()
     torch.cuda.synchronize()
     for k in cands:
@@ -783,18 +913,19 @@ def main():
         tot_bytes += b_alg(w, n, g, U, Nnew, V)
         tot_occ += b_occ(w, n, g, U, Nnew, V)
         if i in host_values:  # every timed step, or 5 evenly spaced ones in long runs
-            hv, hw = host_values[i]
-            dom_b.append(kernel_bytes(w, dom, n, g, key_stats(hv, hw)))
+            hv, ho, hw = host_values[i]
+            dom_b.append(kernel_bytes(w, dom, n, g, key_stats(hv, ho, hw)))
         Us.append(U)
         news.append(Nnew)
-    dom_bytes = float(np.mean(dom_b)) * a.steps
+    dom_alg = float(np.mean([b[0] for b in dom_b]))
+    dom_impl = float(np.mean([b[1] for b in dom_b]))
     dom_ms = cand_ms[dom]
     ms_per_step = total_ms / a.steps
     gbps = tot_bytes / (total_ms * 1e-3) / 1e9
-    achieved = dom_bytes / a.steps / (dom_ms * 1e-3) / 1e9
+    achieved = dom_alg / (dom_ms * 1e-3) / 1e9
 
     traffic = None
-    tpath = os.path.join(ROOT, "profiles", f"traffic_workload{a.workload}_{dom}.json")
+    tpath = os.path.join(ROOT, "profiles", f"traffic_{W.describe(w)['workload']}_{dom}.json")
     if os.path.exists(tpath):
         with open(tpath) as fh:
             tj = json.load(fh)
@@ -828,7 +959,12 @@ def main():
         "gbps_effective_occ": tot_occ / (total_ms * 1e-3) / 1e9,
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic, "kernel_ms": dom_ms,
-                     "kernel_bytes_alg": dom_bytes / a.steps},
+                     "kernel_bytes_alg": dom_alg, "kernel_bytes_impl": dom_impl,
+                     "kernel_bytes_bookkeeping": dom_impl - dom_alg},
+        "idmap_resize": {"capacity_slots_start": caps[0], "capacity_slots_end": caps[-1],
+                         "rehashes_in_window": sum(1 for x, y in zip(caps, caps[1:]) if y != x),
+                         "resize_in_window": caps[-1] != caps[0],
+                         "live_rows_end": table.size()} if not pipelined else None,
         "kernel_ms_warmup": {k: float(np.mean(v)) for k, v in prof.items() if v},
         "first_step": first_step,
         "evictable": evictable,

@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define RS_VERSION 7
+#define RS_VERSION 8
 
 typedef enum {
   RS_OK = 0,
@@ -389,6 +389,24 @@ typedef enum {
   RS_K_COUNT = 9
 } rs_kernel_id;
 rs_status rs_set_kernel_events(rs_table* t, int32_t kernel, void* start_event, void* stop_event);
+
+/* Bandwidth probes, for measurement only: plain device operations with the
+ * access widths and launch shapes of the step's kernels, so the step's
+ * bandwidth can be set against what this GPU delivers for each access
+ * pattern.  Enqueued on `stream`; the caller times them (events).
+ *  RS_PROBE_READ:   read n bytes of a (n a multiple of 16); b >= 4 bytes
+ *                   receives nothing unless the data hash to one value
+ *  RS_PROBE_WRITE:  write n bytes of a (a multiple of 16), streaming stores
+ *  RS_PROBE_COPY:   copy n bytes from a to b (a multiple of 16)
+ *  RS_PROBE_GATHER: b[i] = row idx[i] of a, for i < n, rows of row_bytes
+ *                   (16 times a power of two, at most 1024); indices outside
+ *                   [0, a_bytes / row_bytes) are skipped
+ *  RS_PROBE_RMW:    row idx[i] of a += 1.0f (every fp32 word), for i < n
+ * a_bytes / b_bytes: the buffers' sizes in bytes.  idx: device int64 [n].
+ * Errors: RS_EINVAL (kinds, sizes, null pointers), RS_EHIP. */
+typedef enum { RS_PROBE_READ = 0, RS_PROBE_WRITE = 1, RS_PROBE_COPY = 2, RS_PROBE_GATHER = 3, RS_PROBE_RMW = 4 } rs_probe_kind;
+rs_status rs_bandwidth_probe(int32_t kind, void* a, int64_t a_bytes, void* b, int64_t b_bytes, const int64_t* idx,
+                             int64_t n, int32_t row_bytes, rs_stream stream);
 
 #ifdef __cplusplus
 }

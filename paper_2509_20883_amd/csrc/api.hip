@@ -21,6 +21,10 @@
 
 using namespace rs;
 
+static_assert(RS_PROBE_READ == kProbeRead && RS_PROBE_WRITE == kProbeWrite && RS_PROBE_COPY == kProbeCopy &&
+                  RS_PROBE_GATHER == kProbeGather && RS_PROBE_RMW == kProbeRmw,
+              "probe kinds of the header and the kernels agree");
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -497,6 +501,9 @@ rs_status check_ctx(const rs_table* t, const rs_ctx* c) {
 
 Work ctx_work(const rs_ctx* c) { return make_work(c->workspace, make_layout(c->n, c->dim)); }
 
+// Rows of the upstream gradient of a forward (its output's rows).
+int64_t grad_rows(const rs_ctx* c) { return padded_mode(c->mode) ? c->bags * c->pad_len : c->bags; }
+
 }  // namespace
 
 extern "C" {
@@ -886,7 +893,7 @@ rs_status lookup_pool_bwd(rs_table* t, const rs_ctx* ctx, const void* grad_out, 
   if (st != RS_OK) return st;
   if (ctx->n > 0 && (!grad_out || !grad_unique)) return fail(RS_EINVAL, "null gradient");
   const Work w = ctx_work(ctx);
-  RS_HIP(launch_bwd(t->dev(), w, ctx->offsets, ctx->n, ctx->mode, grad_out, grad_unique, nullptr,
+  RS_HIP(launch_bwd(t->dev(), w, grad_rows(ctx), ctx->n, ctx->mode, grad_out, grad_unique, nullptr,
                     t->ev(RS_K_BWD_SHORT), t->ev(RS_K_BWD_LONG), static_cast<hipStream_t>(stream)));
   return RS_OK;
 }
@@ -911,8 +918,29 @@ rs_status lookup_pool_bwd_opt(rs_table* t, const rs_ctx* ctx, const void* grad_o
   if (ctx->n > 0 && !grad_out) return fail(RS_EINVAL, "null gradient");
   const OptArgs o = make_opt(t, p);
   const Work w = ctx_work(ctx);
-  RS_HIP(launch_bwd(t->dev(), w, ctx->offsets, ctx->n, ctx->mode, grad_out, nullptr, &o, t->ev(RS_K_BWD_SHORT),
+  RS_HIP(launch_bwd(t->dev(), w, grad_rows(ctx), ctx->n, ctx->mode, grad_out, nullptr, &o, t->ev(RS_K_BWD_SHORT),
                     t->ev(RS_K_BWD_LONG), static_cast<hipStream_t>(stream)));
+  return RS_OK;
+}
+
+rs_status rs_bandwidth_probe(int32_t kind, void* a, int64_t a_bytes, void* b, int64_t b_bytes, const int64_t* idx,
+                             int64_t n, int32_t row_bytes, rs_stream stream) {
+  if (!a || a_bytes <= 0 || n < 0) return fail(RS_EINVAL, "null or empty buffer a, or n < 0");
+  const bool rows = kind == RS_PROBE_GATHER || kind == RS_PROBE_RMW;
+  if (kind < RS_PROBE_READ || kind > RS_PROBE_RMW) return fail(RS_EINVAL, "bad probe kind");
+  if (!rows) {
+    if (n % 16 != 0 || n > a_bytes) return fail(RS_EINVAL, "n must be a multiple of 16 and at most a_bytes");
+    if ((kind == RS_PROBE_READ && (!b || b_bytes < 4)) || (kind == RS_PROBE_COPY && (!b || n > b_bytes)))
+      return fail(RS_EINVAL, "buffer b missing or too small");
+  } else {
+    const int lanes = row_bytes / 16;
+    if (row_bytes <= 0 || row_bytes % 16 != 0 || lanes > 64 || (lanes & (lanes - 1)) != 0 || row_bytes > a_bytes)
+      return fail(RS_EINVAL, "row_bytes must be 16 times a power of two up to 1024, at most a_bytes");
+    if (!idx) return fail(RS_EINVAL, "null idx");
+    if (kind == RS_PROBE_GATHER && (!b || n > b_bytes / row_bytes)) return fail(RS_EINVAL, "buffer b too small");
+  }
+  if (n == 0) return RS_OK;
+  RS_HIP(launch_probe(kind, a, a_bytes, b, idx, n, row_bytes, static_cast<hipStream_t>(stream)));
   return RS_OK;
 }
 

@@ -113,8 +113,8 @@ struct RowFrag {
 // indices together (one round trip), share them by shuffles, and then read
 // the gradient rows kBatch at a time.
 template <typename GT, int E, int LANES, int MODE>
-__device__ inline void sum_positions(const Work& w, const GT* __restrict__ grad, const int64_t* __restrict__ offsets,
-                                     int p0, int cnt, int lane, float (&acc)[E]) {
+__device__ inline void sum_positions(const Work& w, const GT* __restrict__ grad, uint32_t nref, int p0, int cnt,
+                                     int lane, float (&acc)[E]) {
   constexpr int D = LANES * E;
   constexpr int NR = (kUnit + LANES - 1) / LANES;  // positions per lane
   // gradient rows in flight: a small batch keeps more waves resident; narrow
@@ -141,7 +141,7 @@ __device__ inline void sum_positions(const Work& w, const GT* __restrict__ grad,
     for (int j = 0; j < kBatch; ++j) {
       const int q = q0 + j;
       const int r = LANES > 1 ? __shfl(myref[q / LANES], q % LANES, LANES) : myref[q];
-      ref[j] = q < cnt ? r : -1;
+      ref[j] = q < cnt && static_cast<uint32_t>(r) < nref ? r : -1;
     }
     uint4 raw[kBatch];
 #pragma unroll
@@ -173,8 +173,8 @@ __device__ inline void sum_positions(const Work& w, const GT* __restrict__ grad,
 // together, share them by shuffles, and read the rows kBatch at a time, each
 // added into its segment's accumulator.
 template <typename GT, int E, int LANES, int MODE, int K>
-__device__ inline void sum_segments(const Work& w, const GT* __restrict__ grad, const int (&st)[K], const int (&ct)[K],
-                                    int lane, float (&acc)[K][E]) {
+__device__ inline void sum_segments(const Work& w, const GT* __restrict__ grad, uint32_t nref, const int (&st)[K],
+                                    const int (&ct)[K], int lane, float (&acc)[K][E]) {
   constexpr int D = LANES * E;
   constexpr int MAXP = K * kLong;
   constexpr int NR = (MAXP + LANES - 1) / LANES;  // positions per lane
@@ -217,7 +217,7 @@ __device__ inline void sum_segments(const Work& w, const GT* __restrict__ grad, 
     for (int j = 0; j < kBatch; ++j) {
       const int tq = q0 + j;
       const int r = LANES > 1 ? __shfl(myref[tq / LANES], tq % LANES, LANES) : myref[tq];
-      ref[j] = tq < T ? r : -1;
+      ref[j] = tq < T && static_cast<uint32_t>(r) < nref ? r : -1;
       int kk = 0;
 #pragma unroll
       for (int k = 1; k < K; ++k) kk += tq >= pre[k];
@@ -255,8 +255,7 @@ __device__ inline void sum_segments(const Work& w, const GT* __restrict__ grad, 
 // consecutive keys per iteration (their loads interleaved); block `blk` of
 // `nblk` takes every nblk-th group of keys.
 template <typename WT, typename GT, int LANES, int MODE, bool FUSED>
-__device__ inline void bwd_short(const TableDev& t, const Work& w, const int64_t* __restrict__ offsets,
-                                 const GT* __restrict__ grad, float* __restrict__ grad_unique, const OptArgs& o,
+__device__ inline void bwd_short(const TableDev& t, const Work& w, uint32_t nref, const GT* __restrict__ grad, float* __restrict__ grad_unique, const OptArgs& o,
                                  int64_t blk, int64_t nblk) {
   constexpr int E = 16 / static_cast<int>(sizeof(GT));
   constexpr int GPB = kBlock / LANES;
@@ -288,7 +287,7 @@ __device__ inline void bwd_short(const TableDev& t, const Work& w, const int64_t
     for (int k = 0; k < K; ++k)
 #pragma unroll
       for (int e = 0; e < E; ++e) acc[k][e] = 0.f;
-    sum_segments<GT, E, LANES, MODE, K>(w, grad, st, ct, lane, acc);
+    sum_segments<GT, E, LANES, MODE, K>(w, grad, nref, st, ct, lane, acc);
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       if (!act[k]) continue;
@@ -304,8 +303,8 @@ __device__ inline void bwd_short(const TableDev& t, const Work& w, const int64_t
 // One lane group per backward unit of a hot key: the unit's partial sum is
 // written to its own partial row.
 template <typename GT, int LANES, int MODE>
-__device__ inline void bwd_units(const Work& w, const int64_t* __restrict__ offsets, const GT* __restrict__ grad,
-                                 int64_t blk, int64_t nblk) {
+__device__ inline void bwd_units(const Work& w, uint32_t nref, const GT* __restrict__ grad, int64_t blk,
+                                 int64_t nblk) {
   constexpr int E = 16 / static_cast<int>(sizeof(GT));
   constexpr int GPB = kBlock / LANES;
   constexpr int D = LANES * E;
@@ -318,7 +317,7 @@ __device__ inline void bwd_units(const Work& w, const int64_t* __restrict__ offs
 #pragma unroll
     for (int q = 0; q < E; ++q) acc[q] = 0.f;
     for (int p = un.p0; p < un.p1; p += kUnit)
-      sum_positions<GT, E, LANES, MODE>(w, grad, offsets, p, min(kUnit, un.p1 - p), lane, acc);
+      sum_positions<GT, E, LANES, MODE>(w, grad, nref, p, min(kUnit, un.p1 - p), lane, acc);
     store_vals<float, E>(w.gpart + unit * D + lane * E, acc);
   }
 }
@@ -327,16 +326,14 @@ __device__ inline void bwd_units(const Work& w, const int64_t* __restrict__ offs
 // in one launch measured slower: the hot-key units' scattered gradient reads
 // then compete with the short keys' row updates).
 template <typename WT, typename GT, int LANES, int MODE, bool FUSED>
-__global__ __launch_bounds__(kBlock) void k_bwd_short(TableDev t, Work w, const int64_t* __restrict__ offsets,
-                                                      const GT* __restrict__ grad, float* __restrict__ grad_unique,
+__global__ __launch_bounds__(kBlock) void k_bwd_short(TableDev t, Work w, uint32_t nref, const GT* __restrict__ grad, float* __restrict__ grad_unique,
                                                       OptArgs o) {
-  bwd_short<WT, GT, LANES, MODE, FUSED>(t, w, offsets, grad, grad_unique, o, blockIdx.x, gridDim.x);
+  bwd_short<WT, GT, LANES, MODE, FUSED>(t, w, nref, grad, grad_unique, o, blockIdx.x, gridDim.x);
 }
 
 template <typename GT, int LANES, int MODE>
-__global__ __launch_bounds__(kBlock) void k_bwd_long(Work w, const int64_t* __restrict__ offsets,
-                                                     const GT* __restrict__ grad) {
-  bwd_units<GT, LANES, MODE>(w, offsets, grad, blockIdx.x, gridDim.x);
+__global__ __launch_bounds__(kBlock) void k_bwd_long(Work w, uint32_t nref, const GT* __restrict__ grad) {
+  bwd_units<GT, LANES, MODE>(w, nref, grad, blockIdx.x, gridDim.x);
 }
 
 template <typename WT, int E, int LANES, bool FUSED>
@@ -398,7 +395,7 @@ __global__ __launch_bounds__(kBlock) void k_bwd_long_finish(TableDev t, Work w, 
 }
 
 template <typename WT, typename GT, int LANES, int MODE, bool FUSED>
-static hipError_t bwd_launch(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, const void* grad,
+static hipError_t bwd_launch(const TableDev& t, const Work& w, uint32_t nref, int64_t n, const void* grad,
                              float* gu, const OptArgs& o, hipEvent_t* ev_s, hipEvent_t* ev_l, hipStream_t s) {
   constexpr int E = 16 / static_cast<int>(sizeof(GT));
   constexpr int GPB = kBlock / LANES;
@@ -411,51 +408,51 @@ static hipError_t bwd_launch(const TableDev& t, const Work& w, const int64_t* of
   hipEvent_t s0 = ev_s ? ev_s[0] : nullptr, s1 = ev_s ? ev_s[1] : nullptr;
   hipEvent_t l0 = ev_l ? ev_l[0] : nullptr, l1 = ev_l ? ev_l[1] : nullptr;
   hipExtLaunchKernelGGL((k_bwd_short<WT, GT, LANES, MODE, FUSED>), dim3(grid_for(n, GPB, kResident)), dim3(kBlock), 0,
-                        s, s0, s1, 0, t, w, offsets, g, gu, o);
+                        s, s0, s1, 0, t, w, nref, g, gu, o);
   // one lane group per possible unit (the device-side count is at most
   // 2n/kUnit + 2): no group takes a second unit while others are idle
   hipExtLaunchKernelGGL((k_bwd_long<GT, LANES, MODE>), dim3(grid_for(2 * (n / kUnit) + 2, GPB)), dim3(kBlock), 0, s,
-                        l0, nullptr, 0, w, offsets, g);
+                        l0, nullptr, 0, w, nref, g);
   hipExtLaunchKernelGGL((k_bwd_long_finish<WT, E, LANES, FUSED>), dim3(grid_for(n / kLong + 1, 1, 4 * kResident)),
                         dim3(kBlock), 0, s, nullptr, l1, 0, t, w, gu, o);
   return hipGetLastError();
 }
 
 template <typename WT, typename GT, int MODE, bool FUSED>
-static hipError_t bwd_dim(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, const void* grad,
+static hipError_t bwd_dim(const TableDev& t, const Work& w, uint32_t nref, int64_t n, const void* grad,
                           float* gu, const OptArgs& o, hipEvent_t* es, hipEvent_t* el, hipStream_t s) {
   constexpr int E = 16 / static_cast<int>(sizeof(GT));
   switch (t.dim / E) {
-    case 1: return bwd_launch<WT, GT, 1, MODE, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
-    case 2: return bwd_launch<WT, GT, 2, MODE, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
-    case 4: return bwd_launch<WT, GT, 4, MODE, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
-    case 8: return bwd_launch<WT, GT, 8, MODE, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
-    case 16: return bwd_launch<WT, GT, 16, MODE, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
-    case 32: return bwd_launch<WT, GT, 32, MODE, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
-    case 64: return bwd_launch<WT, GT, 64, MODE, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
+    case 1: return bwd_launch<WT, GT, 1, MODE, FUSED>(t, w, nref, n, grad, gu, o, es, el, s);
+    case 2: return bwd_launch<WT, GT, 2, MODE, FUSED>(t, w, nref, n, grad, gu, o, es, el, s);
+    case 4: return bwd_launch<WT, GT, 4, MODE, FUSED>(t, w, nref, n, grad, gu, o, es, el, s);
+    case 8: return bwd_launch<WT, GT, 8, MODE, FUSED>(t, w, nref, n, grad, gu, o, es, el, s);
+    case 16: return bwd_launch<WT, GT, 16, MODE, FUSED>(t, w, nref, n, grad, gu, o, es, el, s);
+    case 32: return bwd_launch<WT, GT, 32, MODE, FUSED>(t, w, nref, n, grad, gu, o, es, el, s);
+    case 64: return bwd_launch<WT, GT, 64, MODE, FUSED>(t, w, nref, n, grad, gu, o, es, el, s);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <typename WT, bool FUSED>
-static hipError_t bwd_mode(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int mode,
+static hipError_t bwd_mode(const TableDev& t, const Work& w, uint32_t nref, int64_t n, int mode,
                            const void* grad, float* gu, const OptArgs& o, hipEvent_t* es, hipEvent_t* el,
                            hipStream_t s) {
-  if (mode == 2 || mode == 3) return bwd_dim<WT, WT, 0, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
-  if (mode == 1) return bwd_dim<WT, float, 1, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
-  return bwd_dim<WT, float, 0, FUSED>(t, w, offsets, n, grad, gu, o, es, el, s);
+  if (mode == 2 || mode == 3) return bwd_dim<WT, WT, 0, FUSED>(t, w, nref, n, grad, gu, o, es, el, s);
+  if (mode == 1) return bwd_dim<WT, float, 1, FUSED>(t, w, nref, n, grad, gu, o, es, el, s);
+  return bwd_dim<WT, float, 0, FUSED>(t, w, nref, n, grad, gu, o, es, el, s);
 }
 
-hipError_t launch_bwd(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int mode, const void* grad,
+hipError_t launch_bwd(const TableDev& t, const Work& w, int64_t nref, int64_t n, int mode, const void* grad,
                       float* grad_unique, const OptArgs* opt, hipEvent_t* ev_short, hipEvent_t* ev_long,
                       hipStream_t s) {
   if (n <= 0) return hipSuccess;
   const OptArgs o = opt ? *opt : OptArgs{0, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 1.f, 1.f, 0.f, 0.f};
   if (opt)
-    return t.row_dtype ? bwd_mode<uint16_t, true>(t, w, offsets, n, mode, grad, grad_unique, o, ev_short, ev_long, s)
-                       : bwd_mode<float, true>(t, w, offsets, n, mode, grad, grad_unique, o, ev_short, ev_long, s);
-  return t.row_dtype ? bwd_mode<uint16_t, false>(t, w, offsets, n, mode, grad, grad_unique, o, ev_short, ev_long, s)
-                     : bwd_mode<float, false>(t, w, offsets, n, mode, grad, grad_unique, o, ev_short, ev_long, s);
+    return t.row_dtype ? bwd_mode<uint16_t, true>(t, w, static_cast<uint32_t>(nref), n, mode, grad, grad_unique, o, ev_short, ev_long, s)
+                       : bwd_mode<float, true>(t, w, static_cast<uint32_t>(nref), n, mode, grad, grad_unique, o, ev_short, ev_long, s);
+  return t.row_dtype ? bwd_mode<uint16_t, false>(t, w, static_cast<uint32_t>(nref), n, mode, grad, grad_unique, o, ev_short, ev_long, s)
+                     : bwd_mode<float, false>(t, w, static_cast<uint32_t>(nref), n, mode, grad, grad_unique, o, ev_short, ev_long, s);
 }
 
 // ---------------------------------------------------------------------------

@@ -301,7 +301,11 @@ hipError_t launch_map_rows(const Work& w, int64_t n, int64_t* rows_out, int64_t*
 hipError_t launch_find(const TableDev& t, const int64_t* keys, int64_t n, int64_t* rows_out, hipStream_t s);
 hipError_t launch_pool(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int64_t bags, int mode,
                        int64_t pad_len, void* out, uint8_t* mask, hipEvent_t* ev, hipStream_t s);
-hipError_t launch_bwd(const TableDev& t, const Work& w, const int64_t* offsets, int64_t n, int mode,
+// Backward (+ optimizer when opt is set).  nref: rows of the upstream
+// gradient (bags, or bags * pad_len for the padded modes); an occurrence-list
+// entry outside [0, nref) -- left stale by offsets that do not cover every
+// position -- contributes nothing instead of reading out of bounds.
+hipError_t launch_bwd(const TableDev& t, const Work& w, int64_t nref, int64_t n, int mode,
                       const void* grad, float* grad_unique, const OptArgs* opt, hipEvent_t* ev_short,
                       hipEvent_t* ev_long, hipStream_t s);
 hipError_t launch_opt(const TableDev& t, const Work& w, int64_t n, const float* grad_unique, const OptArgs& opt,
@@ -318,6 +322,12 @@ hipError_t launch_mod(const int64_t* values, int64_t n, const int64_t* col_off, 
 // kEvictRows rows; the evicted count is added to the table scalars.
 constexpr int kEvictRows = 1024;
 hipError_t launch_evict(const TableDev& t, int64_t rows_prov, uint32_t max_age, int32_t* bcount, hipStream_t s);
+// Bandwidth probes (measurement references).  read / write / copy: n bytes
+// (a multiple of 16) of a (and b); gather / rmw: n random rows of row_bytes
+// of a (a_bytes long) by idx, gathered into b or updated in place.
+enum : int { kProbeRead = 0, kProbeWrite = 1, kProbeCopy = 2, kProbeGather = 3, kProbeRmw = 4 };
+hipError_t launch_probe(int kind, void* a, int64_t a_bytes, void* b, const int64_t* idx, int64_t n, int row_bytes,
+                        hipStream_t s);
 hipError_t launch_rehash(const Slot* old_slots, int64_t old_cap, const TableDev& t, hipStream_t s);
 hipError_t launch_export(const TableDev& t, int64_t cap_slots, int64_t* keys, int64_t* rows, int64_t cap,
                          int64_t* n_dev, hipStream_t s);

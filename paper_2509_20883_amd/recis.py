@@ -95,6 +95,7 @@ def lib() -> C.CDLL:
         "ids_partition": (C.c_int, [p, i64, i32, C.c_uint64, p, p, p, p, p, C.c_size_t, p]),
         "fused_bucketize": (C.c_int, [p, i64, p, i32, p, p, p, i32, p]),
         "fused_mod": (C.c_int, [p, i64, p, i32, p, p, i32, p]),
+        "rs_bandwidth_probe": (C.c_int, [i32, p, i64, p, i64, p, i64, i32, p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -228,6 +229,27 @@ def fused_mod(values: torch.Tensor, col_offsets: torch.Tensor, moduli: torch.Ten
     _check(lib().fused_mod(_ptr(v), v.numel(), _ptr(co), co.numel() - 1, _ptr(m), _ptr(out), int(validate),
                            _stream()))
     return out
+
+
+PROBES = {"read": 0, "write": 1, "copy": 2, "gather": 3, "rmw": 4}
+
+
+def bandwidth_probe(kind: str, a: torch.Tensor, b: Optional[torch.Tensor] = None, idx: Optional[torch.Tensor] = None,
+                    n: Optional[int] = None, row_bytes: int = 0):
+    """Enqueue one bandwidth probe (measurement reference) on the current stream.
+
+    read / write / copy: n bytes (default: all of a); gather / rmw: the rows
+    of row_bytes of a named by idx (int64), gathered into b or updated in place.
+    """
+    if not a.is_cuda or (b is not None and not b.is_cuda) or (idx is not None and not idx.is_cuda):
+        raise RecisError(EINVAL, "probe buffers must be on the GPU")
+    ab = a.numel() * a.element_size()
+    bb = 0 if b is None else b.numel() * b.element_size()
+    if idx is not None:
+        idx = _dev(idx, torch.int64)
+    if n is None:
+        n = idx.numel() if kind in ("gather", "rmw") else ab
+    _check(lib().rs_bandwidth_probe(PROBES[kind], _ptr(a), ab, _ptr(b), bb, _ptr(idx), n, row_bytes, _stream()))
 
 
 class Table:

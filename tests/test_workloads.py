@@ -129,17 +129,30 @@ def test_window_mask_head_and_tail():
 def test_key_stats_and_kernel_bytes_by_hand():
     B = _bench()
     vals = np.array([7] * 40 + [1, 2, 2, 3], dtype=np.int64)    # one hot key (40 ids), three short keys
-    ks = B.key_stats(vals)
+    # bags 0-3: ten 7s each; bag 4: [1]; bag 5: [2]; bag 6: [2, 3]; bags 7-9 empty
+    offs = np.array([0, 10, 20, 30, 40, 41, 42, 44, 44, 44, 44], dtype=np.int64)
+    G = offs.size - 1
+    ks = B.key_stats(vals, offs)
     assert (ks["U"], ks["U_long"], ks["N_long"], ks["U_short"], ks["N_short"]) == (4, 1, 40, 3, 4)
     assert ks["units"] == 2                                      # 40 ids in units of 32
-    w = W.workload(0)                                            # dim 16 fp32, Adagrad
+    assert (ks["Gb_long"], ks["Gb_short"]) == (4, 3)             # distinct bags of each kind of key
+    w = W.workload(0)                                            # dim 16 fp32, Adagrad, sum
     R, S = B.row_bytes(w)
     assert (R, S) == (64, 64)
-    G = 10
-    # short keys: segment descriptors of all keys, 4 list entries, 4 gradient rows, 3 row+state updates
-    assert B.kernel_bytes(w, "bwd_short", vals.size, G, ks) == 16 * 4 + 4 * 4 + 64 * 4 + 2 * (R + S) * 3
-    # hot keys: 2 units, 40 list entries and gradient rows, partial rows written and read, one update
-    assert B.kernel_bytes(w, "bwd_long", vals.size, G, ks) == 16 * 2 + 4 * 40 + 64 * 40 + 2 * 64 * 2 + 2 * (R + S)
+    N, U = vals.size, 4
+    # short keys: each of their 3 bags' gradient rows once, 4 inverse reads, 3 row+state updates;
+    # the implementation also reads every key's segment descriptor and one gradient row per id
+    assert B.kernel_bytes(w, "bwd_short", N, G, ks) == (64 * 3 + 4 * 4 + 2 * (R + S) * 3,
+                                                        16 * 4 + 4 * 4 + 64 * 4 + 2 * (R + S) * 3)
+    # hot key: its 4 bags' gradient rows, 40 inverse reads, one update; the implementation reads
+    # 2 unit descriptors, 40 gradient rows, and writes and reads 2 partial rows
+    assert B.kernel_bytes(w, "bwd_long", N, G, ks) == (64 * 4 + 4 * 40 + 2 * (R + S),
+                                                       16 * 2 + 4 * 40 + 64 * 40 + 2 * 4 * 16 * 2 + 2 * (R + S))
+    # pool: offsets, inverse, row ids, unique rows, output; the implementation reads a row id and
+    # a list position per id and writes one list entry per id
+    out = G * 16 * 4
+    assert B.kernel_bytes(w, "pool", N, G, ks) == (8 * (G + 1) + 4 * N + 8 * U + R * U + out,
+                                                   8 * (G + 1) + 12 * N + R * U + out + 4 * N)
     w.opt = 5                                                    # row-wise Adam: m per element + v per row
     assert B.row_bytes(w) == (64, 4 * 17)
 
