@@ -91,12 +91,16 @@ typedef enum {
 typedef struct rs_table rs_table; /* opaque, library-owned */
 typedef void* rs_stream;          /* hipStream_t */
 
-/* Device-memory allocator used for the table's IDMap and internal
- * workspace.  NULL as the allocator argument means hipMalloc /
- * hipFree.  A free callback is only invoked after the table's work has
- * completed.  The Blocks (rows + optimizer state) are physical chunks
- * (hipMemCreate) mapped into one reserved virtual range, so that rows never
- * move when the table grows; they do not go through the allocator. */
+/* Device-memory allocator for everything a table owns: the IDMap, the
+ * Blocks (rows + optimizer state) and internal workspace, so that a
+ * framework's caching allocator (PyTorch's) can back the table.  With an
+ * allocator the Blocks are separate allocations of block_rows rows each,
+ * found through a device table of their addresses; rows never move.  NULL
+ * as the allocator argument means hipMalloc / hipFree for the IDMap and
+ * workspace, and Blocks made of physical chunks (hipMemCreate) mapped back
+ * to back into one reserved virtual range (no address table).  alloc returns
+ * NULL on failure (the call then returns RS_ENOMEM).  A free callback is
+ * only invoked after the table's work has completed. */
 typedef struct {
   void* (*alloc)(size_t bytes, void* ctx);
   void (*free)(void* ptr, void* ctx);
@@ -399,7 +403,8 @@ rs_status rs_set_kernel_events(rs_table* t, int32_t kernel, void* start_event, v
  *  RS_PROBE_WRITE:  write n bytes of a (a multiple of 16), streaming stores
  *  RS_PROBE_COPY:   copy n bytes from a to b (a multiple of 16)
  *  RS_PROBE_GATHER: b[i] = row idx[i] of a, for i < n, rows of row_bytes
- *                   (16 times a power of two, at most 1024); indices outside
+ *                   (16 * 2^k * c bytes with 2^k <= 64 lanes and c <= 4 words
+ *                   per lane: 16 ... 4096); indices outside
  *                   [0, a_bytes / row_bytes) are skipped
  *  RS_PROBE_RMW:    row idx[i] of a += 1.0f (every fp32 word), for i < n
  * a_bytes / b_bytes: the buffers' sizes in bytes.  idx: device int64 [n].

@@ -13,7 +13,8 @@ import os
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "liboracle.so")
+# RS_ORACLE_LIB names another build of oracle.cpp (the sanitizer tier's)
+LIB_PATH = os.environ.get("RS_ORACLE_LIB") or os.path.join(HERE, "liboracle.so")
 
 OK, EINVAL, ENOMEM, EFULL, EKEY = 0, 1, 2, 3, 4
 SUM, MEAN, NONE, TAIL = 0, 1, 2, 3

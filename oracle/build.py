@@ -18,6 +18,18 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def build_sanitized(out: str, verbose: bool = False) -> str:
+    """The same source built with AddressSanitizer and UndefinedBehaviorSanitizer
+    (any finding aborts), for the sanitizer tier of the CPU tests."""
+    src = os.path.join(HERE, "oracle.cpp")
+    cmd = ["g++", "-O1", "-g", "-std=c++17", "-shared", "-fPIC", "-ffp-contract=off", "-fno-omit-frame-pointer",
+           "-fsanitize=address,undefined", "-fno-sanitize-recover=all", src, "-o", out]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    return out
+
+
 if __name__ == "__main__":
     build(verbose=True)
     sys.exit(0)

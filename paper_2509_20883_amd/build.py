@@ -19,14 +19,16 @@ HIPCC_FLAGS = [
 ]
 
 
-def build(verbose: bool = False, jobs: int = 4) -> str:
+def build(verbose: bool = False, jobs: int = 4, out: str = LIB, defines=()) -> str:
+    """Compile every source and link `out` (default: the in-tree library);
+    `defines` are extra -D options (tuning variants)."""
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
     objs = []
     procs = []
     for src in SOURCES:
-        obj = os.path.join(CSRC, src + ".o")
-        cmd = [hipcc, *HIPCC_FLAGS, "-c", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
-               os.path.join(CSRC, src), "-o", obj]
+        obj = out + "." + src + ".o"
+        cmd = [hipcc, *HIPCC_FLAGS, *[f"-D{d}" for d in defines], "-c", "-I", os.path.join(ROOT, "include"), "-I",
+               CSRC, os.path.join(CSRC, src), "-o", obj]
         cmd.remove("-shared")
         if verbose:
             print(" ".join(cmd), flush=True)
@@ -38,14 +40,14 @@ def build(verbose: bool = False, jobs: int = 4) -> str:
     for p in procs:
         if p.wait() != 0:
             raise RuntimeError("hipcc failed")
-    cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", LIB + ".tmp"]
+    cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", out + ".tmp"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(LIB + ".tmp", LIB)
+    os.replace(out + ".tmp", out)
     for o in objs:
         os.remove(o)
-    return LIB
+    return out
 
 
 if __name__ == "__main__":

@@ -220,6 +220,11 @@ struct rs_table {
   size_t mapped = 0;      // bytes mapped so far
   size_t chunk_bytes = 0; // block_rows * stride, rounded up to the mapping granularity
   std::vector<hipMemGenericAllocationHandle_t> chunks;
+  // Blocks from the caller's allocator: one allocation per chunk of
+  // block_rows rows, and a device table of their addresses
+  std::vector<void*> achunks;
+  uint8_t** d_chunk_tab = nullptr;
+  int64_t chunk_tab_cap = 0;
   int64_t stride = 0;
   int64_t rows_prov = 0;
   // device scalars
@@ -274,7 +279,11 @@ struct rs_table {
     t.slots = slots;
     t.cap_mask = static_cast<uint64_t>(cap - 1);
     t.store.base = va_base;
+    t.store.chunks = d_chunk_tab;
     t.store.stride = stride;
+    int sh = 0;
+    while ((int64_t(1) << sh) < d.block_rows) ++sh;
+    t.store.shift = sh;
     t.scal = d_scal;
     t.dim = d.dim;
     t.row_dtype = d.row_dtype;
@@ -310,11 +319,32 @@ rs_status take_latched(rs_table* t) {
   return fail(err_status(static_cast<int>(e)), err_text(static_cast<int>(e)));
 }
 
+// Add Blocks chunks from the caller's allocator until `rows` rows fit.
+rs_status provision_alloc_rows(rs_table* t, int64_t rows, hipStream_t s) {
+  while (t->rows_prov < rows) {
+    const int64_t c = static_cast<int64_t>(t->achunks.size());
+    if (c >= t->chunk_tab_cap) return fail(RS_ENOMEM, "table rows exceed the device's memory");
+    void* p = t->alloc(t->chunk_bytes);
+    if (!p) return fail(RS_ENOMEM, "the allocator returned NULL for a Blocks chunk");
+    t->achunks.push_back(p);
+    k_set_scalar<<<1, 1, 0, s>>>(reinterpret_cast<int64_t*>(t->d_chunk_tab) + c,
+                                 static_cast<int64_t>(reinterpret_cast<uintptr_t>(p)));
+    RS_HIP(hipGetLastError());
+    t->rows_prov += t->d.block_rows;
+  }
+  return RS_OK;
+}
+
 // Map Blocks chunks until `rows` rows fit.
 rs_status provision_rows(rs_table* t, int64_t rows, hipStream_t s) {
   if (rows <= t->rows_prov) return RS_OK;
   const size_t need = static_cast<size_t>(rows) * static_cast<size_t>(t->stride);
-  if (need > t->va_size) return fail(RS_ENOMEM, "table rows exceed the reserved Blocks address range");
+  if (t->custom) {
+    rs_status st = provision_alloc_rows(t, rows, s);
+    if (st != RS_OK) return st;
+  } else if (need > t->va_size) {
+    return fail(RS_ENOMEM, "table rows exceed the reserved Blocks address range");
+  }
   hipMemAllocationProp prop = {};
   prop.type = hipMemAllocationTypePinned;
   prop.location.type = hipMemLocationTypeDevice;
@@ -323,7 +353,7 @@ rs_status provision_rows(rs_table* t, int64_t rows, hipStream_t s) {
   acc.location.type = hipMemLocationTypeDevice;
   acc.location.id = t->device;
   acc.flags = hipMemAccessFlagsProtReadWrite;
-  while (t->mapped < need) {
+  while (!t->custom && t->mapped < need) {
     const size_t bytes = std::min(t->chunk_bytes, t->va_size - t->mapped);
     hipMemGenericAllocationHandle_t h;
     if (hipMemCreate(&h, bytes, &prop, 0) != hipSuccess) {
@@ -339,7 +369,7 @@ rs_status provision_rows(rs_table* t, int64_t rows, hipStream_t s) {
     t->chunks.push_back(h);
     t->mapped += bytes;
   }
-  t->rows_prov = static_cast<int64_t>(t->mapped / static_cast<size_t>(t->stride));
+  if (!t->custom) t->rows_prov = static_cast<int64_t>(t->mapped / static_cast<size_t>(t->stride));
   if (t->meta_off >= 0 && t->rows_prov > t->free_cap) {
     // the free-row stack can hold every row
     int64_t* nf = static_cast<int64_t*>(t->alloc(sizeof(int64_t) * static_cast<size_t>(t->rows_prov)));
@@ -447,7 +477,16 @@ rs_status dedup_and_insert(rs_table* t, const int64_t* values, int64_t n, const 
     const int64_t keys_need = cs[kCBaseKeys] + req;
     const int64_t rows_need = cs[kCBaseLive] + std::max<int64_t>(req - cs[kCFreeTop], 0);
     st = grow_for(t, keys_need, ts[kTTomb], rows_need, n, s);
-    if (st != RS_OK) return st;
+    if (st != RS_OK) {
+      // no memory to grow: undo the scan's row reservation, so the call
+      // leaves the table as it found it (nothing inserted)
+      const rs_status e1 = set_scalar(t, kTLive, cs[kCBaseLive], s);
+      const rs_status e2 = set_scalar(t, kTKeys, cs[kCBaseKeys], s);
+      const rs_status e3 = set_scalar(t, kTFree, cs[kCFreeTop], s);
+      if (e1 != RS_OK || e2 != RS_OK || e3 != RS_OK) return RS_EHIP;
+      reset_bound(t, std::max(cs[kCBaseKeys] + ts[kTTomb], cs[kCBaseLive]));
+      return st;  // grow_for's message stays the last error
+    }
     int64_t tombs = 0;
     RS_HIP(hipMemcpy(&tombs, t->d_scal + kTTomb, sizeof(int64_t), hipMemcpyDeviceToHost));
     // redo the reservation against the grown table (published under a new
@@ -568,6 +607,24 @@ rs_status ht_create(const rs_table_desc* d, const rs_allocator* a, rs_stream str
     }
     st = set_scalar(t, kTLimit, t->limit, s);
     if (st != RS_OK) break;
+    if (t->custom) {
+      // Blocks from the allocator: chunks of block_rows rows, at most as many
+      // as the device's memory holds, addressed through a device table
+      size_t total = 0;
+      if (hipDeviceTotalMem(&total, t->device) != hipSuccess) {
+        st = fail(RS_EHIP, "hipDeviceTotalMem failed");
+        break;
+      }
+      t->chunk_bytes = static_cast<size_t>(d->block_rows) * static_cast<size_t>(t->stride);
+      t->chunk_tab_cap = static_cast<int64_t>(total / t->chunk_bytes) + 1;
+      t->d_chunk_tab = static_cast<uint8_t**>(t->alloc(sizeof(uint8_t*) * static_cast<size_t>(t->chunk_tab_cap)));
+      if (!t->d_chunk_tab) {
+        st = fail(RS_ENOMEM, "allocation of the Blocks chunk table failed");
+        break;
+      }
+      if (hipStreamSynchronize(s) != hipSuccess) st = fail(RS_EHIP, "hipStreamSynchronize failed");
+      break;
+    }
     // reserve the Blocks address range: as many bytes as the device has
     hipMemAllocationProp prop = {};
     prop.type = hipMemAllocationTypePinned;
@@ -609,6 +666,8 @@ rs_status ht_destroy(rs_table* t) {
   if (t->mapped) (void)hipMemUnmap(t->va_base, t->mapped);
   for (hipMemGenericAllocationHandle_t h : t->chunks) (void)hipMemRelease(h);
   if (t->va_base) (void)hipMemAddressFree(t->va_base, t->va_size);
+  for (void* p : t->achunks) t->release(p);
+  t->release(t->d_chunk_tab);
   t->release(t->d_scal);
   t->release(t->iws);
   t->release(t->free_rows);
@@ -933,9 +992,8 @@ rs_status rs_bandwidth_probe(int32_t kind, void* a, int64_t a_bytes, void* b, in
     if ((kind == RS_PROBE_READ && (!b || b_bytes < 4)) || (kind == RS_PROBE_COPY && (!b || n > b_bytes)))
       return fail(RS_EINVAL, "buffer b missing or too small");
   } else {
-    const int lanes = row_bytes / 16;
-    if (row_bytes <= 0 || row_bytes % 16 != 0 || lanes > 64 || (lanes & (lanes - 1)) != 0 || row_bytes > a_bytes)
-      return fail(RS_EINVAL, "row_bytes must be 16 times a power of two up to 1024, at most a_bytes");
+    if (row_bytes <= 0 || row_bytes % 16 != 0 || probe_lanes(row_bytes / 16) == 0 || row_bytes > a_bytes)
+      return fail(RS_EINVAL, "row_bytes must be 16 * 2^k * c (c <= 4, 2^k <= 64) and at most a_bytes");
     if (!idx) return fail(RS_EINVAL, "null idx");
     if (kind == RS_PROBE_GATHER && (!b || n > b_bytes / row_bytes)) return fail(RS_EINVAL, "buffer b too small");
   }

@@ -9,8 +9,8 @@
 // loads, one lane group of D*sizeof(row)/16 lanes per row, and write the
 // gradient row each position of the occurrence list will read (occ_ref).
 //
-// A lane group handles kBags bags at once and requests up to kChunk rows of
-// them together, for single-id and long bags alike.
+// A lane group handles one bag per lane and requests 16 rows of them at a
+// time, for single-id and long bags alike.
 #include "device_common.h"
 
 #include <hip/hip_ext.h>
@@ -40,13 +40,31 @@ __device__ inline void add_raw<uint16_t, 8>(float (&acc)[8], const uint4& v) {
   }
 }
 
-// A lane group pools kBags consecutive bags.  Their positions, taken as one
-// concatenated sequence, are processed in chunks of C: the lanes load the
-// chunk's occurrence rows and list positions together (each lane a few
-// positions), then every row of the chunk is requested before any is added,
-// so a group keeps C rows in flight whether the bags hold one id or hundreds
-// (C = 4 for batches of mostly single-id bags, 16 otherwise).
-template <typename WT, int LANES, int MODE, int C, int kBags>
+// Inclusive scan of v over the LANES lanes of a lane group.
+template <int LANES>
+__device__ inline int64_t group_incl_scan(int64_t v, int lane) {
+#pragma unroll
+  for (int d = 1; d < LANES; d <<= 1) {
+    const int64_t t = __shfl_up(v, d, LANES);
+    if (lane >= d) v += t;
+  }
+  return v;
+}
+
+// A lane group of LANES lanes pools LANES consecutive bags (lane q owns bag
+// g0 + q).  Their positions, taken as one sequence, are read in chunks of C:
+// the lanes load the chunk's occurrence rows and list positions (J per
+// lane), the next chunk's are requested before this chunk's rows are used,
+// and all C rows of a chunk are requested before any is added -- C rows in
+// flight whether the bags hold one id or hundreds.  The rows are then added
+// in order into one running accumulator; a cursor over the bags' cumulative
+// lengths flushes a bag (one non-temporal row store) when the sequence passes
+// its end, so empty bags are flushed as zeros and no per-bag accumulators
+// are held.  The walk also writes each id's entry of the occurrence list.
+// For well-formed offsets (each bag starts where the previous one ends) the
+// sequence is positions offsets[g0] ... ; malformed offsets give wrong
+// sums, never an access outside [0, n).
+template <typename WT, int LANES, int MODE, int C>
 __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64_t* __restrict__ offsets, int64_t n,
                                                  int64_t bags, float* __restrict__ out) {
   constexpr int E = 16 / static_cast<int>(sizeof(WT));
@@ -55,112 +73,93 @@ __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64
   constexpr int J = (C + LANES - 1) / LANES;  // chunk positions per lane
   const int lane = threadIdx.x % LANES;
   const int grp = threadIdx.x / LANES;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * GPB * kBags;
-  for (int64_t g0 = (static_cast<int64_t>(blockIdx.x) * GPB + grp) * kBags; g0 < bags; g0 += stride) {
-    // positions fit 32 bits (n <= 2^28): fewer registers, more resident waves
-    int b[kBags], e[kBags];
-    if constexpr (LANES > kBags) {
-      // lanes 0..kBags of the group load offsets[g0 .. g0+kBags] together
-      const int64_t gq = g0 + min(lane, kBags);
-      const int ov = static_cast<int>(gq <= bags ? offsets[gq] : n);
+  const int64_t g0 = (static_cast<int64_t>(blockIdx.x) * GPB + grp) * LANES;
+  if (g0 >= bags) return;
+  const int nb = static_cast<int>(min(static_cast<int64_t>(LANES), bags - g0));
+  // this lane's bag, CSR bounds clamped to [0, n]; positions fit 32 bits (n <= 2^28)
+  const int n32 = static_cast<int>(n);
+  const int64_t gq = g0 + min(lane, nb - 1);
+  const int bq = min(max(static_cast<int>(offsets[gq]), 0), n32);
+  const int eq = min(max(static_cast<int>(offsets[gq + 1]), bq), n32);
+  const int len = lane < nb ? eq - bq : 0;
+  const int64_t cum = group_incl_scan<LANES>(len, lane);  // end of bag `lane` in the sequence
+  // at most n ids for well-formed offsets (malformed ones are cut there)
+  const int total = static_cast<int>(min(__shfl(cum, LANES - 1, LANES), static_cast<int64_t>(n32)));
+  const int p0 = __shfl(bq, 0, LANES);                     // the sequence starts at the first bag's start
+  int64_t rr[J];
+  int pp[J];
+  auto load_idx = [&](int t0) {
 #pragma unroll
-      for (int q = 0; q <= kBags; ++q) {
-        const int x = __shfl(ov, q, LANES);
-        if (q < kBags) b[q] = x;
-        if (q > 0) e[q - 1] = x;
-      }
-    } else {
-#pragma unroll
-      for (int q = 0; q < kBags; ++q) {
-        b[q] = g0 + q < bags ? static_cast<int>(offsets[g0 + q]) : 0;
-        e[q] = g0 + q < bags ? static_cast<int>(offsets[g0 + q + 1]) : 0;
+    for (int j = 0; j < J; ++j) {
+      const int c = lane + j * LANES;
+      const bool valid = c < C && t0 + c < total;
+      const int p = valid ? min(p0 + t0 + c, n32 - 1) : 0;  // total > 0: position 0 exists
+      rr[j] = w.occ_row[p];
+      pp[j] = w.occ_pos[p];
+      if (!valid) {
+        rr[j] = -1;
+        pp[j] = -1;
       }
     }
-    int pre[kBags + 1];
-    pre[0] = 0;
-    const int n32 = static_cast<int>(n);
+  };
+  float acc[E];
 #pragma unroll
-    for (int q = 0; q < kBags; ++q) {
-      // CSR bounds clamped to [0, n]: malformed offsets cannot read out of range
-      const bool ok = g0 + q < bags;
-      b[q] = ok ? min(max(b[q], 0), n32) : 0;
-      e[q] = ok ? min(max(e[q], b[q]), n32) : 0;
-      pre[q + 1] = pre[q] + (e[q] - b[q]);
+  for (int k = 0; k < E; ++k) acc[k] = 0.f;
+  int q = 0;                                   // the bag the running sum belongs to (< nb)
+  int64_t cq = __shfl(cum, 0, LANES);          // its end
+  int64_t bstart = 0;                          // its start
+  auto flush = [&]() {
+    // the pooled output is streamed out once: non-temporal stores
+    const int64_t blen = cq - bstart;
+    if (MODE == 1 && blen > 0) {
+      const float l = static_cast<float>(blen);
+#pragma unroll
+      for (int k = 0; k < E; ++k) acc[k] = acc[k] / l;
     }
-    const int total = pre[kBags];
-    float acc[kBags][E];
+    float* op = out + (g0 + q) * D + lane * E;
 #pragma unroll
-    for (int q = 0; q < kBags; ++q)
-#pragma unroll
-      for (int k = 0; k < E; ++k) acc[q][k] = 0.f;
-    for (int t0 = 0; t0 < total; t0 += C) {
-      int64_t rr[J];
-      int pp[J], qq[J];
-#pragma unroll
-      for (int j = 0; j < J; ++j) {
-        const int c = lane + j * LANES;
-        const int tt = t0 + c;
-        const bool valid = c < C && tt < total;
-        int q = 0;
-#pragma unroll
-        for (int k = 1; k < kBags; ++k) q += tt >= pre[k];
-        const int p = valid ? b[q] + (tt - pre[q]) : 0;  // total > 0: position 0 exists
-        rr[j] = w.occ_row[p];
-        pp[j] = w.occ_pos[p];
-        if (!valid) {
-          rr[j] = -1;
-          pp[j] = -1;
-        }
-        qq[j] = q;
-      }
-      // the occurrence's place in its key's segment of the occurrence list
-      // receives the gradient row it will read in the backward (and, for
-      // mean pooling, the scale 1 / bag length)
-#pragma unroll
-      for (int j = 0; j < J; ++j) {
-        if (pp[j] < 0) continue;
-        if (MODE == 1) {
-          int len = 0;
-#pragma unroll
-          for (int q = 0; q < kBags; ++q)
-            if (qq[j] == q) len = e[q] - b[q];
-          w.occ_rs[pp[j]] = make_int2(static_cast<int>(g0 + qq[j]), __float_as_int(1.0f / static_cast<float>(len)));
-        } else {
-          w.occ_ref[pp[j]] = static_cast<int>(g0 + qq[j]);
-        }
-      }
-      uint4 x[C];
-      int xq[C];
-#pragma unroll
-      for (int c = 0; c < C; ++c) {
-        const int64_t r = LANES > 1 ? __shfl(rr[c / LANES], c % LANES, LANES) : rr[c];
-        xq[c] = LANES > 1 ? __shfl(qq[c / LANES], c % LANES, LANES) : qq[c];
-        x[c] = make_uint4(0u, 0u, 0u, 0u);
-        if (r >= 0) x[c] = *reinterpret_cast<const uint4*>(t.store.row(r) + lane * 16);
-      }
-#pragma unroll
-      for (int c = 0; c < C; ++c)
-#pragma unroll
-        for (int q = 0; q < kBags; ++q)
-          if (xq[c] == q) add_raw<WT, E>(acc[q], x[c]);
+    for (int k = 0; k < E; k += 4) {
+      const f32x4 v = {acc[k], acc[k + 1], acc[k + 2], acc[k + 3]};
+      __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(op + k));
     }
 #pragma unroll
-    for (int q = 0; q < kBags; ++q) {
-      if (g0 + q >= bags) continue;
-      if (MODE == 1 && e[q] > b[q]) {
-        const float len = static_cast<float>(e[q] - b[q]);
+    for (int k = 0; k < E; ++k) acc[k] = 0.f;
+    ++q;
+    bstart = cq;
+    cq = __shfl(cum, min(q, LANES - 1), LANES);
+  };
+  if (total > 0) load_idx(0);
+  for (int t0 = 0; t0 < total; t0 += C) {
+    uint4 x[C];
 #pragma unroll
-        for (int k = 0; k < E; ++k) acc[q][k] = acc[q][k] / len;
-      }
-      // the pooled output is streamed out once: non-temporal stores
-      float* op = out + (g0 + q) * D + lane * E;
+    for (int c = 0; c < C; ++c) {
+      const int64_t r = LANES > 1 ? __shfl(rr[c / LANES], c % LANES, LANES) : rr[c];
+      x[c] = make_uint4(0u, 0u, 0u, 0u);
+      if (r >= 0) x[c] = *reinterpret_cast<const uint4*>(t.store.row(r) + lane * 16);
+    }
+    int cp[J];  // this chunk's list positions (the next chunk's indices replace rr / pp)
 #pragma unroll
-      for (int k = 0; k < E; k += 4) {
-        const f32x4 v = {acc[q][k], acc[q][k + 1], acc[q][k + 2], acc[q][k + 3]};
-        __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(op + k));
+    for (int j = 0; j < J; ++j) cp[j] = pp[j];
+    if (t0 + C < total) load_idx(t0 + C);
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      const int tt = t0 + c;
+      if (tt >= total) break;
+      while (q < nb && tt >= cq) flush();  // bags ending before this id (empty ones flush zeros)
+      // the id's place in its key's segment of the occurrence list receives
+      // the gradient row it will read in the backward (and, for mean
+      // pooling, the scale 1 / bag length)
+      if (lane == c % LANES && cp[c / LANES] >= 0) {
+        if (MODE == 1)
+          w.occ_rs[cp[c / LANES]] =
+              make_int2(static_cast<int>(g0 + q), __float_as_int(1.0f / static_cast<float>(max(cq - bstart, int64_t(1)))));
+        else
+          w.occ_ref[cp[c / LANES]] = static_cast<int>(g0 + q);
       }
+      add_raw<WT, E>(acc, x[c]);
     }
   }
+  while (q < nb) flush();  // the last bag and any empty bags after it
 }
 
 // Padded copy: block = (bag, TCH positions); a lane group copies TCH / groups
@@ -231,26 +230,15 @@ static hipError_t pool_mode(const TableDev& t, const Work& w, const int64_t* off
     hipExtLaunchKernelGGL((k_pool_none<WT, LANES>), dim3(grid_for(bags * nch, 1, 1 << 20)), dim3(kBlock), 0, s, e0, e1,
                           0, t, w, offsets, n, bags, pad_len, mode == 3, static_cast<WT*>(out), mask);
   } else {
-    // mostly single-id bags (n <= 2 bags): a lane group takes 8 bags and
-    // requests their rows together; longer bags: 4 bags, 16-row chunks
-    const bool few = n <= 2 * bags;
+    // one lane group per LANES bags (one bag per lane), 16 rows in flight
     float* o = static_cast<float*>(out);
-    const unsigned gf = grid_for(bags, GPB * 8, 1 << 20), gm = grid_for(bags, GPB * 4, 1 << 20);
-    if (mode == 1) {
-      if (few)
-        hipExtLaunchKernelGGL((k_pool<WT, LANES, 1, 8, 8>), dim3(gf), dim3(kBlock), 0, s, e0, e1, 0, t, w, offsets, n,
-                              bags, o);
-      else
-        hipExtLaunchKernelGGL((k_pool<WT, LANES, 1, 16, 4>), dim3(gm), dim3(kBlock), 0, s, e0, e1, 0, t, w, offsets,
-                              n, bags, o);
-    } else {
-      if (few)
-        hipExtLaunchKernelGGL((k_pool<WT, LANES, 0, 8, 8>), dim3(gf), dim3(kBlock), 0, s, e0, e1, 0, t, w, offsets, n,
-                              bags, o);
-      else
-        hipExtLaunchKernelGGL((k_pool<WT, LANES, 0, 16, 4>), dim3(gm), dim3(kBlock), 0, s, e0, e1, 0, t, w, offsets,
-                              n, bags, o);
-    }
+    const unsigned g = grid_for(bags, static_cast<int64_t>(GPB) * LANES, int64_t(1) << 31);
+    if (mode == 1)
+      hipExtLaunchKernelGGL((k_pool<WT, LANES, 1, 16>), dim3(g), dim3(kBlock), 0, s, e0, e1, 0, t, w, offsets, n, bags,
+                            o);
+    else
+      hipExtLaunchKernelGGL((k_pool<WT, LANES, 0, 16>), dim3(g), dim3(kBlock), 0, s, e0, e1, 0, t, w, offsets, n, bags,
+                            o);
   }
   return hipGetLastError();
 }

@@ -1,7 +1,7 @@
 // Bandwidth probes (gfx950): plain device operations that bound what the
 // embedding step's kernels can reach on this GPU, measured with the same
 // access widths and launch shapes (16-byte lane accesses, 256-thread blocks,
-// lane groups of row_bytes / 16 lanes per row).  They are measurement
+// lane groups of up to 64 lanes per row, each lane moving 16-byte words).  They are measurement
 // references only; no step uses them.
 //   kProbeRead    sequential read of `bytes` (every 16-byte word summed)
 //   kProbeWrite   sequential streaming write of `bytes` (non-temporal stores)
@@ -70,12 +70,15 @@ __global__ __launch_bounds__(kBlock) void k_probe_copy(const uint4* __restrict__
   }
 }
 
-// Lane groups of `lanes` lanes (row_bytes / 16), kRows rows in flight per group.
-// Indices outside [0, nrows) are skipped (their output row is not written).
+// Lane groups of `lanes` lanes, each lane moving nch 16-byte words of a row
+// (at lane * 16 + c * lanes * 16), kRows rows in flight per group.  Indices
+// outside [0, nrows) are skipped (their output row is not written).
+constexpr int kProbeMaxChunks = 4;
+
 template <int kRows>
 __global__ __launch_bounds__(kBlock) void k_probe_gather(const uint8_t* __restrict__ rows, int64_t nrows, int row_bytes,
-                                                         int lanes, const int64_t* __restrict__ idx, int64_t n,
-                                                         uint8_t* __restrict__ out) {
+                                                         int lanes, int nch, const int64_t* __restrict__ idx,
+                                                         int64_t n, uint8_t* __restrict__ out) {
   const int lane = threadIdx.x % lanes, grp = threadIdx.x / lanes, gpb = kBlock / lanes;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * gpb * kRows;
   for (int64_t i0 = (static_cast<int64_t>(blockIdx.x) * gpb + grp) * kRows; i0 < n; i0 += stride) {
@@ -85,22 +88,30 @@ __global__ __launch_bounds__(kBlock) void k_probe_gather(const uint8_t* __restri
       r[k] = i0 + k < n ? idx[i0 + k] : -1;
       if (r[k] >= nrows) r[k] = -1;
     }
-    uint4 v[kRows];
+    uint4 v[kRows][kProbeMaxChunks];
 #pragma unroll
     for (int k = 0; k < kRows; ++k)
-      v[k] = r[k] >= 0 ? *reinterpret_cast<const uint4*>(rows + r[k] * row_bytes + lane * 16) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int c = 0; c < kProbeMaxChunks; ++c)
+        v[k][c] = r[k] >= 0 && c < nch
+                      ? *reinterpret_cast<const uint4*>(rows + r[k] * row_bytes + (c * lanes + lane) * 16)
+                      : make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int k = 0; k < kRows; ++k) {
       if (r[k] < 0) continue;
-      const u32x4 x = {v[k].x, v[k].y, v[k].z, v[k].w};
-      __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(out + (i0 + k) * row_bytes + lane * 16));
+#pragma unroll
+      for (int c = 0; c < kProbeMaxChunks; ++c) {
+        if (c >= nch) continue;
+        const u32x4 x = {v[k][c].x, v[k][c].y, v[k][c].z, v[k][c].w};
+        __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(out + (i0 + k) * row_bytes + (c * lanes + lane) * 16));
+      }
     }
   }
 }
 
 template <int kRows>
 __global__ __launch_bounds__(kBlock) void k_probe_rmw(uint8_t* __restrict__ rows, int64_t nrows, int row_bytes, int lanes,
-                                                      const int64_t* __restrict__ idx, int64_t n) {
+                                                      int nch, const int64_t* __restrict__ idx, int64_t n) {
   const int lane = threadIdx.x % lanes, grp = threadIdx.x / lanes, gpb = kBlock / lanes;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * gpb * kRows;
   for (int64_t i0 = (static_cast<int64_t>(blockIdx.x) * gpb + grp) * kRows; i0 < n; i0 += stride) {
@@ -110,17 +121,32 @@ __global__ __launch_bounds__(kBlock) void k_probe_rmw(uint8_t* __restrict__ rows
       r[k] = i0 + k < n ? idx[i0 + k] : -1;
       if (r[k] >= nrows) r[k] = -1;
     }
-    float4 v[kRows];
+    float4 v[kRows][kProbeMaxChunks];
 #pragma unroll
     for (int k = 0; k < kRows; ++k)
-      if (r[k] >= 0) v[k] = *reinterpret_cast<const float4*>(rows + r[k] * row_bytes + lane * 16);
+#pragma unroll
+      for (int c = 0; c < kProbeMaxChunks; ++c)
+        if (r[k] >= 0 && c < nch)
+          v[k][c] = *reinterpret_cast<const float4*>(rows + r[k] * row_bytes + (c * lanes + lane) * 16);
 #pragma unroll
     for (int k = 0; k < kRows; ++k) {
       if (r[k] < 0) continue;
-      const float4 x = make_float4(v[k].x + 1.f, v[k].y + 1.f, v[k].z + 1.f, v[k].w + 1.f);
-      *reinterpret_cast<float4*>(rows + r[k] * row_bytes + lane * 16) = x;
+#pragma unroll
+      for (int c = 0; c < kProbeMaxChunks; ++c) {
+        if (c >= nch) continue;
+        const float4 x = make_float4(v[k][c].x + 1.f, v[k][c].y + 1.f, v[k][c].z + 1.f, v[k][c].w + 1.f);
+        *reinterpret_cast<float4*>(rows + r[k] * row_bytes + (c * lanes + lane) * 16) = x;
+      }
     }
   }
+}
+
+// Lanes per row for a row of w16 16-byte words: the largest power of two
+// <= 64 dividing w16 that leaves at most kProbeMaxChunks words per lane, or 0.
+int probe_lanes(int w16) {
+  for (int l = 64; l >= 1; l >>= 1)
+    if (w16 % l == 0) return w16 / l <= kProbeMaxChunks ? l : 0;
+  return 0;
 }
 
 hipError_t launch_probe(int kind, void* a, int64_t a_bytes, void* b, const int64_t* idx, int64_t n, int row_bytes,
@@ -141,15 +167,16 @@ hipError_t launch_probe(int kind, void* a, int64_t a_bytes, void* b, const int64
     case kProbeGather:
     case kProbeRmw: {
       constexpr int kRows = 8;
-      const int lanes = row_bytes / 16;
-      if (row_bytes % 16 != 0 || lanes < 1 || lanes > 64 || (lanes & (lanes - 1)) != 0) return hipErrorInvalidValue;
+      const int lanes = row_bytes % 16 == 0 ? probe_lanes(row_bytes / 16) : 0;
+      if (lanes == 0) return hipErrorInvalidValue;
+      const int nch = row_bytes / 16 / lanes;
       const unsigned g = grid_for(n, static_cast<int64_t>(kBlock / lanes) * kRows, int64_t(1) << 20);
       if (kind == kProbeGather)
         k_probe_gather<kRows><<<g, kBlock, 0, s>>>(static_cast<const uint8_t*>(a), a_bytes / row_bytes, row_bytes,
-                                                   lanes, idx, n, static_cast<uint8_t*>(b));
+                                                   lanes, nch, idx, n, static_cast<uint8_t*>(b));
       else
-        k_probe_rmw<kRows><<<g, kBlock, 0, s>>>(static_cast<uint8_t*>(a), a_bytes / row_bytes, row_bytes, lanes, idx,
-                                                n);
+        k_probe_rmw<kRows><<<g, kBlock, 0, s>>>(static_cast<uint8_t*>(a), a_bytes / row_bytes, row_bytes, lanes, nch,
+                                                idx, n);
       break;
     }
     default:

@@ -6,6 +6,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "recis_mi355x.h"
+
 namespace rs {
 
 constexpr int kBlock = 256;  // threads per block (4 waves)
@@ -147,15 +149,22 @@ struct alignas(16) Slot {
   long long row;
 };
 
-// Blocks: physical chunks mapped back to back into one reserved virtual
-// range, so rows never move and row r is at base + r * stride; a row is
-// [w: D x row dtype | state0: D x fp32 | state1: D x fp32 (Adam) | row
-// scalar (row-wise optimizers) | {key, clock of its last lookup} (tables
-// with eviction)], padded to 16 bytes.
+// Blocks: chunks of 2^shift rows that never move.  By default they are
+// physical chunks mapped back to back into one reserved virtual range, so
+// row r is at base + r * stride; a table whose memory comes from a caller's
+// allocator keeps a device table of chunk pointers instead (row r is row
+// r mod 2^shift of chunk r >> shift).  A row is [w: D x row dtype | state0:
+// D x fp32 | state1: D x fp32 (Adam) | row scalar (row-wise optimizers) |
+// {key, clock of its last lookup} (tables with eviction)], padded to 16 bytes.
 struct RowStore {
-  uint8_t* base;
-  int64_t stride;  // bytes per row
-  __device__ inline uint8_t* row(int64_t r) const { return base + r * stride; }
+  uint8_t* base;                   // the mapped range (null with a chunk table)
+  uint8_t* const* chunks;          // the chunk table, or null
+  int64_t stride;                  // bytes per row
+  int shift;                       // log2 of the rows per chunk
+  __device__ inline uint8_t* row(int64_t r) const {
+    if (chunks) return chunks[r >> shift] + (r & ((int64_t(1) << shift) - 1)) * stride;
+    return base + r * stride;
+  }
 };
 
 struct TableDev {
@@ -328,6 +337,8 @@ hipError_t launch_evict(const TableDev& t, int64_t rows_prov, uint32_t max_age, 
 enum : int { kProbeRead = 0, kProbeWrite = 1, kProbeCopy = 2, kProbeGather = 3, kProbeRmw = 4 };
 hipError_t launch_probe(int kind, void* a, int64_t a_bytes, void* b, const int64_t* idx, int64_t n, int row_bytes,
                         hipStream_t s);
+// Lanes per row of the row probes for rows of w16 16-byte words (0: not supported).
+int probe_lanes(int w16);
 hipError_t launch_rehash(const Slot* old_slots, int64_t old_cap, const TableDev& t, hipStream_t s);
 hipError_t launch_export(const TableDev& t, int64_t cap_slots, int64_t* keys, int64_t* rows, int64_t cap,
                          int64_t* n_dev, hipStream_t s);

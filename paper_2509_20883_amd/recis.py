@@ -17,7 +17,8 @@ from typing import Optional, Tuple
 import torch
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "librecis_mi355x.so")
+# RS_LIB names another build of the library (e.g. a variant being measured)
+LIB_PATH = os.environ.get("RS_LIB") or os.path.join(PKG, "librecis_mi355x.so")
 HEADER = os.path.join(os.path.dirname(PKG), "include", "recis_mi355x.h")
 
 OK, EINVAL, ENOMEM, EFULL, EKEY, EHIP = 0, 1, 2, 3, 4, 5
@@ -42,6 +43,46 @@ class TableDesc(C.Structure):
                 ("init_lo", C.c_float), ("init_hi", C.c_float), ("seed", C.c_uint64),
                 ("capacity_slots", C.c_int64), ("max_load", C.c_float), ("block_rows", C.c_int64),
                 ("auto_grow", C.c_int32), ("evictable", C.c_int32)]
+
+
+ALLOC_FN = C.CFUNCTYPE(C.c_void_p, C.c_size_t, C.c_void_p)
+FREE_FN = C.CFUNCTYPE(None, C.c_void_p, C.c_void_p)
+
+
+class Allocator(C.Structure):
+    _fields_ = [("alloc", ALLOC_FN), ("free", FREE_FN), ("ctx", C.c_void_p)]
+
+
+class TorchAllocator:
+    """rs_allocator backed by PyTorch's caching allocator (current stream).
+
+    fail_after: return NULL from the (fail_after + 1)-th allocation on (tests
+    of the RS_ENOMEM path)."""
+
+    def __init__(self, device=None, fail_after: Optional[int] = None):
+        self.device = torch.cuda.current_device() if device is None else device
+        self.fail_after = fail_after
+        self.calls = 0
+        self.live = {}
+        self._a = ALLOC_FN(self._alloc)
+        self._f = FREE_FN(self._free)
+        self.struct = Allocator(self._a, self._f, None)
+
+    def _alloc(self, nbytes, ctx):
+        self.calls += 1
+        if self.fail_after is not None and self.calls > self.fail_after:
+            return None
+        try:
+            p = torch.cuda.caching_allocator_alloc(int(nbytes), self.device)
+        except Exception:  # an exception must not cross the C callback
+            return None
+        self.live[p] = int(nbytes)
+        return p
+
+    def _free(self, ptr, ctx):
+        if ptr in self.live:
+            del self.live[ptr]
+            torch.cuda.caching_allocator_delete(ptr)
 
 
 class OptParams(C.Structure):
@@ -72,7 +113,7 @@ def lib() -> C.CDLL:
     sig = {
         "rs_version": (C.c_int, []),
         "rs_last_error": (C.c_char_p, []),
-        "ht_create": (C.c_int, [C.POINTER(TableDesc), p, p, C.POINTER(p)]),
+        "ht_create": (C.c_int, [C.POINTER(TableDesc), C.POINTER(Allocator), p, C.POINTER(p)]),
         "ht_destroy": (C.c_int, [p]),
         "ht_find_or_insert": (C.c_int, [p, p, i64, p, p, p]),
         "ht_find": (C.c_int, [p, p, i64, p, p]),
@@ -257,11 +298,13 @@ class Table:
 
     def __init__(self, dim: int, row_dtype: int = F32, optimizer: int = ADAGRAD, init_lo: float = -0.01,
                  init_hi: float = 0.01, seed: int = 0, capacity_slots: int = 1 << 17, max_load: float = 0.75,
-                 block_rows: int = 1 << 16, auto_grow: bool = True, evictable: bool = False):
+                 block_rows: int = 1 << 16, auto_grow: bool = True, evictable: bool = False,
+                 allocator: Optional[TorchAllocator] = None):
         d = TableDesc(dim, row_dtype, optimizer, init_lo, init_hi, seed & 0xFFFFFFFFFFFFFFFF, capacity_slots,
                       max_load, block_rows, int(bool(auto_grow)), int(bool(evictable)))
         h = C.c_void_p()
-        _check(lib().ht_create(C.byref(d), None, _stream(), C.byref(h)))
+        self.allocator = allocator  # kept alive for the table's lifetime (its callbacks free the memory)
+        _check(lib().ht_create(C.byref(d), C.byref(allocator.struct) if allocator else None, _stream(), C.byref(h)))
         self.h = h
         self.dim, self.row_dtype, self.optimizer = dim, row_dtype, optimizer
         # per-element state vectors; the row-wise optimizers add one scalar per row

@@ -73,17 +73,22 @@ def bf16_ulp(x: np.ndarray) -> np.ndarray:
     return 2.0 ** (e - 7)
 
 
-def opt_bounds(opt, row_dtype, w0, s0, g, dg, lr, eps, b1, b2, t, w_ref, wd=0.0):
+def opt_bounds(opt, row_dtype, w0, s0, g, dg, lr, eps, b1, b2, t, w_ref, wd=0.0, dw0=0.0, ds0=0.0):
     """Error bounds of an fp32 optimizer step against the fp64 oracle.
 
     Each fp32 operation is allowed 1e-6 of the magnitude of its terms (about
     16 units of fp32 rounding), so cancellation in m = b1*m + (1-b1)*g or in
     w - update is bounded by the terms, not the result; `dg` is an extra
     uncertainty of the gradient itself (0 when both sides use the same one),
-    propagated to first order.  Returns (bound_w, bound_state)."""
+    propagated to first order.  dw0 / ds0 (shapes of w0 / s0) bound how far
+    the GPU's starting row and state already are from the oracle's (earlier
+    steps without re-synchronisation; Adagrad and the Adam family): they are
+    carried through the step to first order.  Returns (bound_w, bound_state)."""
     f = np.float64
     w0, g, dg, w_ref = (np.asarray(x, f) for x in (w0, g, dg, w_ref))
     s0 = np.asarray(s0, f)
+    ds0 = np.broadcast_to(np.asarray(ds0, f), s0.shape)
+    dw0 = np.broadcast_to(np.asarray(dw0, f), w0.shape)
     ag = np.abs(g)
     if opt in (O.ADAGRAD_RW, O.ADAM_RW):
         # the row mean of g^2: an fp32 tree sum over the row (a few roundings
@@ -115,7 +120,7 @@ def opt_bounds(opt, row_dtype, w0, s0, g, dg, lr, eps, b1, b2, t, w_ref, wd=0.0)
             b_state = np.concatenate([b_m, b_v[:, None]], axis=1)
     elif opt == O.ADAGRAD:
         acc1 = s0[:, 0] + g * g
-        b_acc = 1e-6 * acc1 + 2 * ag * dg + dg * dg + 1e-37
+        b_acc = 1e-6 * acc1 + 2 * ag * dg + dg * dg + ds0[:, 0] + 1e-37
         sq = np.sqrt(acc1)
         dsq = np.minimum(b_acc / np.maximum(2 * sq, 1e-30), np.sqrt(b_acc))
         upd = lr * ag / (sq + eps)
@@ -125,8 +130,9 @@ def opt_bounds(opt, row_dtype, w0, s0, g, dg, lr, eps, b1, b2, t, w_ref, wd=0.0)
         bc1, bc2 = 1.0 - b1 ** t, 1.0 - b2 ** t
         m1 = b1 * s0[:, 0] + (1 - b1) * g
         v1 = b2 * s0[:, 1] + (1 - b2) * g * g
-        b_m = 1e-6 * (b1 * np.abs(s0[:, 0]) + (1 - b1) * ag) + (1 - b1) * dg + 1e-37
-        b_v = 1e-6 * (b2 * s0[:, 1] + (1 - b2) * g * g) + (1 - b2) * (2 * ag * dg + dg * dg) + 1e-37
+        b_m = 1e-6 * (b1 * np.abs(s0[:, 0]) + (1 - b1) * ag) + (1 - b1) * dg + b1 * ds0[:, 0] + 1e-37
+        b_v = (1e-6 * (b2 * s0[:, 1] + (1 - b2) * g * g) + (1 - b2) * (2 * ag * dg + dg * dg) + b2 * ds0[:, 1]
+               + 1e-37)
         if opt == O.ADAM_TF:
             # w -= lr_t m / (sqrt(v) + eps), lr_t = lr sqrt(bc2) / bc1
             lrt = lr * np.sqrt(bc2) / bc1
@@ -144,9 +150,9 @@ def opt_bounds(opt, row_dtype, w0, s0, g, dg, lr, eps, b1, b2, t, w_ref, wd=0.0)
                 d_upd = d_upd + 1e-6 * lr * wd * np.abs(w0)
         b_state = np.stack([b_m, b_v], axis=1)
     if row_dtype == O.BF16:
-        b_w = np.maximum(1e-2 * np.abs(w_ref) + 1e-6, 1.01 * bf16_ulp(w_ref)) + d_upd
+        b_w = np.maximum(1e-2 * np.abs(w_ref) + 1e-6, 1.01 * bf16_ulp(w_ref)) + d_upd + dw0
     else:
-        b_w = 1e-6 * np.maximum(np.maximum(np.abs(w0), np.abs(w_ref)), lr) + d_upd
+        b_w = 1e-6 * np.maximum(np.maximum(np.abs(w0), np.abs(w_ref)), lr) + d_upd + dw0
     return b_w, b_state
 
 
