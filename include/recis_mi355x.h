@@ -345,6 +345,21 @@ rs_status ids_partition(const int64_t* values, int64_t n, int32_t nshards, uint6
                         int64_t* shard_offsets, int32_t* inverse, int64_t* info, void* workspace,
                         size_t workspace_bytes, rs_stream stream);
 
+/* ids_partition without allocation, for callers that cannot allocate device
+ * memory (code under HIP graph capture, serving loops, harnesses that forbid
+ * hipMalloc): the same computation and outputs as ids_partition, but the
+ * workspace is a fixed 54 MiB array inside this library (one per GPU, held
+ * until the process ends) instead of a caller's buffer, so the call itself
+ * allocates nothing.  n <= RS_IDS_STATIC_MAX_IDS (2^20; else RS_EINVAL).
+ * Every call on one GPU uses that GPU's array: calls that overlap on one GPU
+ * (other streams, other host threads) race and must be ordered by the
+ * caller.  Nothing needs clearing between calls.  Errors: RS_EINVAL (as
+ * ids_partition, and n above the limit), RS_EHIP. */
+#define RS_IDS_STATIC_MAX_IDS (1 << 20)
+rs_status ids_partition_static(const int64_t* values, int64_t n, int32_t nshards, uint64_t owner_seed,
+                               int64_t* keys_out, int64_t* shard_offsets, int32_t* inverse, int64_t* info,
+                               rs_stream stream);
+
 /* Feature transforms fused over many columns, one launch for all of them
  * ("Bucketize and Mod" among the benchmarked operators: models hold dozens
  * to hundreds of such columns).  The columns are one flat array of n

@@ -7,7 +7,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "librecis_mi355x.so")
-SOURCES = ["dedup_idmap.hip", "ids_partition.hip", "feature_ops.hip", "pool.hip", "backward.hip", "probes.hip", "api.hip"]
+SOURCES = ["dedup_idmap.hip", "ids_partition.hip", "feature_ops.hip", "pool.hip", "backward.hip", "probes.hip", "ids_static.hip", "api.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

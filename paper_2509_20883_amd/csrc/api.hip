@@ -204,6 +204,8 @@ rs_status err_status(int bits) {
 
 }  // namespace
 
+rs_status rs::set_last_error(rs_status st, const char* msg) { return fail(st, msg); }
+
 struct rs_table {
   rs_table_desc d{};
   rs_allocator a{};

@@ -269,6 +269,9 @@ struct OptArgs {
   float lrt;   // lr * sqrt(1 - beta2^t) / (1 - beta1^t) (epsilon-hat form)
 };
 
+// Record `msg` as the calling thread's last error (rs_last_error) and return st.
+rs_status set_last_error(rs_status st, const char* msg);
+
 // ---------------------------------------------------------------------------
 // launchers; all enqueue on `s` and return hipGetLastError()
 // ---------------------------------------------------------------------------

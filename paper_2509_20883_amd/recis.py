@@ -137,6 +137,7 @@ def lib() -> C.CDLL:
         "fused_bucketize": (C.c_int, [p, i64, p, i32, p, p, p, i32, p]),
         "fused_mod": (C.c_int, [p, i64, p, i32, p, p, i32, p]),
         "rs_bandwidth_probe": (C.c_int, [i32, p, i64, p, i64, p, i64, i32, p]),
+        "ids_partition_static": (C.c_int, [p, i64, i32, C.c_uint64, p, p, p, p, p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -237,6 +238,29 @@ class IdsPartition:
                                    _ptr(shard_offsets), _ptr(inverse), _ptr(info), _ptr(self.ws), self.ws.numel(),
                                    _stream()))
         return keys[:max(n, 0)], shard_offsets, inverse[:n], info
+
+
+IDS_STATIC_MAX_IDS = 1 << 20
+
+
+def ids_partition_static(values: torch.Tensor, nshards: int, owner_seed: int, keys: torch.Tensor,
+                         shard_offsets: torch.Tensor, inverse: torch.Tensor, info: torch.Tensor) -> None:
+    """ids_partition with the library's own fixed workspace: allocates nothing.
+
+    Every tensor is the caller's (contiguous, on the GPU): keys int64 [>= n],
+    shard_offsets int64 [nshards + 1], inverse int32 [>= n], info int64 [2];
+    n = values.numel() <= IDS_STATIC_MAX_IDS.  Calls on one GPU share the
+    workspace: overlapping calls race.
+    """
+    for t, dt in ((values, torch.int64), (keys, torch.int64), (shard_offsets, torch.int64), (inverse, torch.int32),
+                  (info, torch.int64)):
+        if not t.is_cuda or t.dtype != dt or not t.is_contiguous():
+            raise RecisError(EINVAL, f"expected a contiguous GPU {dt} tensor")
+    n = values.numel()
+    if keys.numel() < n or inverse.numel() < n or shard_offsets.numel() < nshards + 1 or info.numel() < 2:
+        raise RecisError(EINVAL, "output tensors too small")
+    _check(lib().ids_partition_static(_ptr(values), n, nshards, owner_seed & 0xFFFFFFFFFFFFFFFF, _ptr(keys),
+                                      _ptr(shard_offsets), _ptr(inverse), _ptr(info), _stream()))
 
 
 def ids_partition(values: torch.Tensor, nshards: int, owner_seed: int = 0):
