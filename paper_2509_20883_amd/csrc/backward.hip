@@ -16,8 +16,9 @@
 //                     gradient rows are being read)
 //   k_bwd_long        a hot key: its segment is cut into units (kUnit
 //                     positions, more for the hottest keys so a key has at
-//                     most kMaxUnits units) spread over the whole GPU; each
-//                     unit writes its partial sum row (no atomics)
+//                     most kMaxUnits units), each XCD taking a contiguous
+//                     eighth of them; each unit writes its partial sum row
+//                     (no atomics)
 //   k_bwd_long_finish one block per hot key sums the partial rows of its
 //                     units in a fixed order and applies the optimizer
 // Without the optimizer (lookup_pool_bwd) the same kernels write grad_unique.
@@ -333,7 +334,21 @@ __global__ __launch_bounds__(kBlock) void k_bwd_short(TableDev t, Work w, uint32
 
 template <typename GT, int LANES, int MODE>
 __global__ __launch_bounds__(kBlock) void k_bwd_long(Work w, uint32_t nref, const GT* __restrict__ grad) {
-  bwd_units<GT, LANES, MODE>(w, nref, grad, blockIdx.x, gridDim.x);
+  // XCD-contiguous: the dispatcher deals blocks to the 8 XCDs in turn, so
+  // block b runs on XCD b % 8; XCD x takes the x-th eighth of the units that
+  // exist (consecutive hot keys, so few features at a time: their gradient
+  // rows are re-read from that XCD's L2).  Units are equal work (kUnit ids),
+  // so the eighths balance.  The grid is a multiple of 8 blocks covering
+  // every possible unit.
+  const int64_t units = w.scal[kCNUnits];
+  constexpr int64_t gpb = kBlock / LANES;
+  const int64_t A = (units + gpb - 1) / gpb;  // blocks with units
+  const int64_t per = (A + 7) / 8;
+  const int64_t x = blockIdx.x % 8, i = blockIdx.x / 8;
+  if (i >= per) return;
+  const int64_t L = x * per + i;
+  if (L >= A) return;
+  bwd_units<GT, LANES, MODE>(w, nref, grad, L, 8 * per);
 }
 
 template <typename WT, int E, int LANES, bool FUSED>
@@ -411,7 +426,8 @@ static hipError_t bwd_launch(const TableDev& t, const Work& w, uint32_t nref, in
                         s, s0, s1, 0, t, w, nref, g, gu, o);
   // one lane group per possible unit (the device-side count is at most
   // 2n/kUnit + 2): no group takes a second unit while others are idle
-  hipExtLaunchKernelGGL((k_bwd_long<GT, LANES, MODE>), dim3(grid_for(2 * (n / kUnit) + 2, GPB)), dim3(kBlock), 0, s,
+  hipExtLaunchKernelGGL((k_bwd_long<GT, LANES, MODE>), dim3((grid_for(2 * (n / kUnit) + 2, GPB) + 7) / 8 * 8),
+                        dim3(kBlock), 0, s,
                         l0, nullptr, 0, w, nref, g);
   hipExtLaunchKernelGGL((k_bwd_long_finish<WT, E, LANES, FUSED>), dim3(grid_for(n / kLong + 1, 1, 4 * kResident)),
                         dim3(kBlock), 0, s, nullptr, l1, 0, t, w, gu, o);

@@ -141,22 +141,29 @@ __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64
 #pragma unroll
     for (int j = 0; j < J; ++j) cp[j] = pp[j];
     if (t0 + C < total) load_idx(t0 + C);
+    int myq[J], mylen[J];  // bag (and its length) of this lane's positions in the chunk
 #pragma unroll
     for (int c = 0; c < C; ++c) {
       const int tt = t0 + c;
       if (tt >= total) break;
       while (q < nb && tt >= cq) flush();  // bags ending before this id (empty ones flush zeros)
-      // the id's place in its key's segment of the occurrence list receives
-      // the gradient row it will read in the backward (and, for mean
-      // pooling, the scale 1 / bag length)
-      if (lane == c % LANES && cp[c / LANES] >= 0) {
-        if (MODE == 1)
-          w.occ_rs[cp[c / LANES]] =
-              make_int2(static_cast<int>(g0 + q), __float_as_int(1.0f / static_cast<float>(max(cq - bstart, int64_t(1)))));
-        else
-          w.occ_ref[cp[c / LANES]] = static_cast<int>(g0 + q);
+      if (lane == c % LANES) {
+        myq[c / LANES] = q;
+        mylen[c / LANES] = static_cast<int>(min(cq - bstart, int64_t(n32)));
       }
       add_raw<WT, E>(acc, x[c]);
+    }
+    // each id's place in its key's segment of the occurrence list receives
+    // the gradient row it will read in the backward (and, for mean pooling,
+    // the scale 1 / bag length)
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      if (cp[j] < 0) continue;  // also every slot past the sequence's end
+      if (MODE == 1)
+        w.occ_rs[cp[j]] = make_int2(static_cast<int>(g0 + myq[j]),
+                                    __float_as_int(1.0f / static_cast<float>(max(mylen[j], 1))));
+      else
+        w.occ_ref[cp[j]] = static_cast<int>(g0 + myq[j]);
     }
   }
   while (q < nb) flush();  // the last bag and any empty bags after it

@@ -18,56 +18,34 @@ namespace rs {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// Blocks of the streaming probes: enough to cover every CU several times.
-constexpr int64_t kProbeGrid = 8192;
-constexpr int kProbeUnroll = 4;
+// The streaming probes make one pass: thread t of block b moves 16-byte word
+// b * 256 + t, so the blocks, dispatched in order, sweep the buffer once
+// (measured on this GPU: a grid-stride loop over 2048-8192 blocks writes at
+// 4.4-5.2 TB/s, one pass at 6.9-7.1 TB/s).
 
 __global__ __launch_bounds__(kBlock) void k_probe_read(const uint4* __restrict__ a, int64_t n16,
                                                        uint32_t* __restrict__ sink) {
-  uint32_t acc = 0;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-  int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  for (; i + (kProbeUnroll - 1) * stride < n16; i += kProbeUnroll * stride) {
-    uint4 v[kProbeUnroll];
-#pragma unroll
-    for (int u = 0; u < kProbeUnroll; ++u) v[u] = a[i + u * stride];
-#pragma unroll
-    for (int u = 0; u < kProbeUnroll; ++u) acc += v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
-  }
-  for (; i < n16; i += stride) {
-    const uint4 v = a[i];
-    acc += v.x ^ v.y ^ v.z ^ v.w;
-  }
-  // a store the compiler cannot drop; taken only for one specific sum
-  if (acc == 0x9E3779B9u) sink[0] = acc;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (i >= n16) return;
+  const uint4 v = a[i];
+  // a store the compiler cannot drop; taken only for one specific word
+  if ((v.x ^ v.y ^ v.z ^ v.w) == 0x9E3779B9u) sink[0] = v.x;
 }
 
 __global__ __launch_bounds__(kBlock) void k_probe_write(uint4* __restrict__ a, int64_t n16, uint32_t value) {
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (i >= n16) return;
   const u32x4 v = {value, value, value, value};
-  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n16; i += stride)
-    __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(a + i));
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(a + i));
 }
 
 __global__ __launch_bounds__(kBlock) void k_probe_copy(const uint4* __restrict__ a, uint4* __restrict__ b,
                                                        int64_t n16) {
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-  int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  for (; i + (kProbeUnroll - 1) * stride < n16; i += kProbeUnroll * stride) {
-    uint4 v[kProbeUnroll];
-#pragma unroll
-    for (int u = 0; u < kProbeUnroll; ++u) v[u] = a[i + u * stride];
-#pragma unroll
-    for (int u = 0; u < kProbeUnroll; ++u) {
-      const u32x4 x = {v[u].x, v[u].y, v[u].z, v[u].w};
-      __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(b + i + u * stride));
-    }
-  }
-  for (; i < n16; i += stride) {
-    const uint4 v = a[i];
-    const u32x4 x = {v.x, v.y, v.z, v.w};
-    __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(b + i));
-  }
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  if (i >= n16) return;
+  const uint4 v = a[i];
+  const u32x4 x = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(b + i));
 }
 
 // Lane groups of `lanes` lanes, each lane moving nch 16-byte words of a row
@@ -153,16 +131,16 @@ hipError_t launch_probe(int kind, void* a, int64_t a_bytes, void* b, const int64
                         hipStream_t s) {
   switch (kind) {
     case kProbeRead:
-      k_probe_read<<<grid_for(n / 16, kBlock * kProbeUnroll, kProbeGrid), kBlock, 0, s>>>(
-          static_cast<const uint4*>(a), n / 16, static_cast<uint32_t*>(b));
+      k_probe_read<<<grid_for(n / 16, kBlock, int64_t(1) << 31), kBlock, 0, s>>>(static_cast<const uint4*>(a), n / 16,
+                                                                                static_cast<uint32_t*>(b));
       break;
     case kProbeWrite:
-      k_probe_write<<<grid_for(n / 16, kBlock * kProbeUnroll, kProbeGrid), kBlock, 0, s>>>(static_cast<uint4*>(a),
-                                                                                          n / 16, 0x3F800000u);
+      k_probe_write<<<grid_for(n / 16, kBlock, int64_t(1) << 31), kBlock, 0, s>>>(static_cast<uint4*>(a), n / 16,
+                                                                                 0x3F800000u);
       break;
     case kProbeCopy:
-      k_probe_copy<<<grid_for(n / 16, kBlock * kProbeUnroll, kProbeGrid), kBlock, 0, s>>>(
-          static_cast<const uint4*>(a), static_cast<uint4*>(b), n / 16);
+      k_probe_copy<<<grid_for(n / 16, kBlock, int64_t(1) << 31), kBlock, 0, s>>>(static_cast<const uint4*>(a),
+                                                                                static_cast<uint4*>(b), n / 16);
       break;
     case kProbeGather:
     case kProbeRmw: {
@@ -170,7 +148,7 @@ hipError_t launch_probe(int kind, void* a, int64_t a_bytes, void* b, const int64
       const int lanes = row_bytes % 16 == 0 ? probe_lanes(row_bytes / 16) : 0;
       if (lanes == 0) return hipErrorInvalidValue;
       const int nch = row_bytes / 16 / lanes;
-      const unsigned g = grid_for(n, static_cast<int64_t>(kBlock / lanes) * kRows, int64_t(1) << 20);
+      const unsigned g = grid_for(n, static_cast<int64_t>(kBlock / lanes) * kRows, int64_t(1) << 31);  // one pass
       if (kind == kProbeGather)
         k_probe_gather<kRows><<<g, kBlock, 0, s>>>(static_cast<const uint8_t*>(a), a_bytes / row_bytes, row_bytes,
                                                    lanes, nch, idx, n, static_cast<uint8_t*>(b));
