@@ -51,8 +51,8 @@ bool padded_mode(int32_t mode) { return mode == RS_POOL_NONE || mode == RS_POOL_
 
 // Workspace layout of one forward: every array sized by the upper bound n.
 struct Layout {
-  size_t occ_word, firstkey, trec, srec, pcnt, poff, ptmp, kinfo, inverse, occ_row, occ_pos, unique,
-      useg, rows, new_list, occ_ref, long_u, long_start, units, bsum, csum, scal, gpart, total;
+  size_t occ_word, trec, nrec, srec, pcnt, poff, ptmp, kinfo, inverse, occ_row, occ_pos, unique, useg, rows,
+      new_list, occ_ref, long_u, long_start, units, bsum, csum, scal, gpart, total;
   int64_t ntiles;
   FrontGeom g;
 };
@@ -62,8 +62,8 @@ Layout make_layout(int64_t n, int dim) {
   const size_t nlong = n1 / kLong + 1;        // keys with > kLong occurrences
   const size_t nunit = 2 * (n1 / kUnit) + 2;  // >= sum over them of ceil(count / kUnit)
   Layout L{};
-  L.ntiles = static_cast<int64_t>(n1 / kRankTile + 2);
   L.g = front_geom(n);
+  L.ntiles = record_tiles(L.g);
   const size_t nrecs = static_cast<size_t>(L.g.nblk) * static_cast<size_t>(L.g.rcap);
   const size_t npc = static_cast<size_t>(L.g.P) * static_cast<size_t>(L.g.nblk);
   size_t off = 0;
@@ -73,8 +73,8 @@ Layout make_layout(int64_t n, int dim) {
     return o;
   };
   L.occ_word = take(4 * n1);
-  L.firstkey = take(4 * n1);
   L.trec = take(sizeof(TileRec) * nrecs);  // also the records' results (int2 each)
+  L.nrec = take(4 * static_cast<size_t>(L.g.nblk));
   L.srec = take(sizeof(TileRec) * nrecs);
   L.pcnt = take(4 * npc);
   L.poff = take(4 * npc);
@@ -103,9 +103,9 @@ Work make_work(void* base, const Layout& L) {
   uint8_t* b = static_cast<uint8_t*>(base);
   Work w;
   w.occ_word = reinterpret_cast<uint32_t*>(b + L.occ_word);
-  w.firstkey = reinterpret_cast<int32_t*>(b + L.firstkey);
   w.trec = reinterpret_cast<TileRec*>(b + L.trec);
   w.recres = reinterpret_cast<int2*>(b + L.trec);
+  w.nrec = reinterpret_cast<int32_t*>(b + L.nrec);
   w.srec = reinterpret_cast<TileRec*>(b + L.srec);
   w.pcnt = reinterpret_cast<int32_t*>(b + L.pcnt);
   w.poff = reinterpret_cast<int32_t*>(b + L.poff);
@@ -136,7 +136,7 @@ Work make_work(void* base, const Layout& L) {
 // Workspace layout of one ids partition: the dedup passes' arrays (no
 // IDMap), the owner counts and their scan, scalars.
 struct PartLayout {
-  size_t occ_word, firstkey, trec, srec, pcnt, poff, ptmp, kslot, hist, csum, cscal, pscal, total;
+  size_t occ_word, trec, nrec, srec, pcnt, poff, ptmp, kslot, hist, csum, cscal, pscal, total;
   FrontGeom g;
   OwnerGeom og;
 };
@@ -145,7 +145,7 @@ PartLayout make_part_layout(int64_t n, int G) {
   const size_t n1 = static_cast<size_t>(n > 0 ? n : 1);
   PartLayout L{};
   L.g = front_geom(n);
-  L.og = owner_geom(n, G);
+  L.og = owner_geom(record_tiles(L.g) * kRankTile, G);  // the owner passes walk the record slots
   const size_t nrecs = static_cast<size_t>(L.g.nblk) * static_cast<size_t>(L.g.rcap);
   const size_t npc = static_cast<size_t>(L.g.P) * static_cast<size_t>(L.g.nblk);
   size_t off = 0;
@@ -155,8 +155,8 @@ PartLayout make_part_layout(int64_t n, int G) {
     return o;
   };
   L.occ_word = take(4 * n1);
-  L.firstkey = take(4 * n1);
   L.trec = take(sizeof(TileRec) * nrecs);
+  L.nrec = take(4 * static_cast<size_t>(L.g.nblk));
   L.srec = take(sizeof(TileRec) * nrecs);
   L.pcnt = take(4 * npc);
   L.poff = take(4 * npc);
@@ -174,9 +174,9 @@ Work make_part_work(void* base, const PartLayout& L, int32_t* inverse) {
   uint8_t* b = static_cast<uint8_t*>(base);
   Work w{};
   w.occ_word = reinterpret_cast<uint32_t*>(b + L.occ_word);
-  w.firstkey = reinterpret_cast<int32_t*>(b + L.firstkey);
   w.trec = reinterpret_cast<TileRec*>(b + L.trec);
   w.recres = reinterpret_cast<int2*>(b + L.trec);
+  w.nrec = reinterpret_cast<int32_t*>(b + L.nrec);
   w.srec = reinterpret_cast<TileRec*>(b + L.srec);
   w.pcnt = reinterpret_cast<int32_t*>(b + L.pcnt);
   w.poff = reinterpret_cast<int32_t*>(b + L.poff);

@@ -8,14 +8,17 @@
 // partition instead, so every key is counted by exactly one block in LDS.
 //   k_tile_dedup     per block, consecutive tiles of 4096 occurrences: LDS
 //                    dedup; one record per distinct key of a tile (key, first
-//                    position and count in the tile); at the end the block
+//                    position and count in the tile), the tile's records in
+//                    the order of their first positions; at the end the block
 //                    copies its records into partition order
 //   k_part_dedup     one block per partition, reading its records from every
 //                    dedup block: LDS dedup (first position = min, count =
-//                    sum, rank base of each record), the key's IDMap probe,
-//                    and a marker at its first position
-//   k_first_sums     per tile of positions: sums over the first occurrences
-//                    (keys, counts, keys not found, hot keys, backward units)
+//                    sum, rank base of each record), the key's IDMap probe;
+//                    the key's first record is flagged
+//   k_first_sums     per tile of records: sums over the first records (keys,
+//                    counts, keys not found, hot keys, backward units); the
+//                    records, tile after tile, list each key once in the
+//                    order of its first position
 //   k_scan5          scan of those tile sums; reserves the rows of new keys
 //   k_compact        unique ids in first-occurrence order, occurrence-list
 //                    segments, rows; new keys claim an IDMap slot
@@ -142,6 +145,7 @@ __global__ __launch_bounds__(NT) void k_tile_dedup(const int64_t* __restrict__ v
   __shared__ short ldense[TILE];          // the tile's distinct keys: dense index -> LDS slot
   __shared__ unsigned int lpc[kMaxParts];  // the block's records per partition
   __shared__ int sh[NT / kWave + 1];
+  __shared__ int lfirst[kDedupItems * (NT / kWave) + 1];  // first occurrences per (item, wave), then their prefix
   const FrontGeom g = w.g;
   const int tid = threadIdx.x;
   const int64_t blk = blockIdx.x;
@@ -197,18 +201,40 @@ __global__ __launch_bounds__(NT) void k_tile_dedup(const int64_t* __restrict__ v
       ls[k] = static_cast<int>(h);
     }
     __syncthreads();
-    // dense list of the occupied slots: thread tid owns slots tid + j * NT
-    // (consecutive lanes, consecutive slots: no bank conflicts), read once
-    constexpr int kOwn = SLOTS / NT;
-    static_assert(kOwn <= 32, "occupancy mask");
-    unsigned int om = 0u;
-#pragma unroll
-    for (int j = 0; j < kOwn; ++j) om |= static_cast<unsigned int>(lkey[j * NT + tid] != kEncEmpty) << j;
+    // dense list of the tile's keys in the order of their first positions:
+    // the first occurrences (lmin of the slot is the position itself), ranked
+    // in position order (item k of thread tid is position base + k*NT + tid:
+    // item-major, then wave, then lane)
     int d;
-    int at = block_excl_scan<NT>(__popc(om), sh, d);
+    {
+      constexpr int NW = NT / kWave;
+      const int lane = tid & (kWave - 1), wid = tid / kWave;
+      const uint64_t below = (1ull << lane) - 1ull;
+      bool fst[kDedupItems];
+      uint64_t bal[kDedupItems];
 #pragma unroll
-    for (int j = 0; j < kOwn; ++j)
-      if ((om >> j) & 1u) ldense[at++] = static_cast<short>(j * NT + tid);
+      for (int k = 0; k < kDedupItems; ++k) {
+        const int64_t i = base + k * NT + tid;
+        fst[k] = ls[k] >= 0 && lmin[ls[k]] == static_cast<unsigned int>(i);
+        bal[k] = __ballot(fst[k]);
+        if (lane == 0) lfirst[k * NW + wid] = __popcll(bal[k]);
+      }
+      __syncthreads();
+      if (tid == 0) {  // exclusive prefix over (item, wave) in position order
+        int run = 0;
+        for (int q = 0; q < kDedupItems * NW; ++q) {
+          const int c = lfirst[q];
+          lfirst[q] = run;
+          run += c;
+        }
+        lfirst[kDedupItems * NW] = run;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int k = 0; k < kDedupItems; ++k)
+        if (fst[k]) ldense[lfirst[k * NW + wid] + __popcll(bal[k] & below)] = static_cast<short>(ls[k]);
+      d = lfirst[kDedupItems * NW];
+    }
     __syncthreads();
     // one record per distinct key (nrec + d <= the block's occurrences <= rcap)
     for (int q = tid; q < d; q += NT) {
@@ -224,7 +250,6 @@ __global__ __launch_bounds__(NT) void k_tile_dedup(const int64_t* __restrict__ v
       const int64_t i = base + k * NT + tid;
       if (i >= n) continue;
       w.occ_word[i] = ls[k] < 0 ? kOccRejected : ((lmin[ls[k]] << 12) | lr[k]);
-      w.firstkey[i] = -1;
     }
     nrec += static_cast<unsigned int>(d);
     __syncthreads();
@@ -236,6 +261,7 @@ __global__ __launch_bounds__(NT) void k_tile_dedup(const int64_t* __restrict__ v
       lcnt[sl] = 0u;
     }
   }
+  if (tid == 0) w.nrec[blk] = static_cast<int>(nrec);
   // the block's records per partition and their offsets in partition order
   // (in place in lpc), then the partition-ordered copy of the records
   constexpr int PPT = kMaxParts / NT;
@@ -353,21 +379,17 @@ __device__ inline void probe_store_keys(const TableDev& t, const Work& w, int64_
 #pragma unroll
     for (int u = 0; u < KP; ++u) {
       if (sl[u] < 0) continue;
-      const unsigned long long fp = cfp[sl[u]];
-      const unsigned int kidx = static_cast<unsigned int>(fp);
-      const unsigned int first = static_cast<unsigned int>(fp >> 32);
-      if (w.kinfo) {  // null: only the first-occurrence markers are wanted
+      const unsigned int kidx = static_cast<unsigned int>(cfp[sl[u]]);
+      {
         KeyInfo ki;
         ki.row = t.slots ? resolve_probe(t, e[u], h[u], pb[u]) : 0;  // no table: nothing to probe
-        ki.first = static_cast<int>(first);
+        ki.key = static_cast<long long>(e[u] ^ kSign);
         ki.count = static_cast<int>(ccnt[sl[u]]);
         ki.uid = -1;
         ki.start = 0;
         ki.long_idx = -1;
-        ki.pad = 0;
         w.kinfo[kidx] = ki;
       }
-      if (first < static_cast<uint64_t>(n)) w.firstkey[first] = static_cast<int>(kidx);
     }
   }
 }
@@ -486,13 +508,18 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
     }
     __syncthreads();
     if (!ovf) {
-      const int d = dense_list();
-      probe_store_keys(t, w, n, d, cdense, ckey, cfp, ccnt);
+      if (w.kinfo) {  // null (ids partition): no key info, no probe
+        const int d = dense_list();
+        probe_store_keys(t, w, n, d, cdense, ckey, cfp, ccnt);
+      }
 #pragma unroll
       for (int k = 0; k < K; ++k) {
         if (pos[k] < 0) continue;
         const int64_t src = (static_cast<int64_t>(pos[k]) / g.rcap) * g.rcap + (x[k].meta >> 12);
-        w.recres[src] = make_int2(static_cast<int>(static_cast<unsigned int>(cfp[sl[k]])), static_cast<int>(rb[k]));
+        const unsigned int kidx = static_cast<unsigned int>(cfp[sl[k]]);
+        // the key's first record is the one whose position is its key index
+        const unsigned int fl = kidx == static_cast<unsigned int>(pos[k]) ? kRecFirst : 0u;
+        w.recres[src] = make_int2(static_cast<int>(kidx), static_cast<int>(rb[k] | fl));
       }
       return;
     }
@@ -540,15 +567,19 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
       s = 0;
       continue;
     }
-    const int d = dense_list();
-    probe_store_keys(t, w, n, d, cdense, ckey, cfp, ccnt);
+    if (w.kinfo) {
+      const int d = dense_list();
+      probe_store_keys(t, w, n, d, cdense, ckey, cfp, ccnt);
+    }
     for (int fr = tid; fr < nr; fr += NT) {
       const int pos = rec_pos(fr);
       const uint64_t h = part_hash(w.srec[pos].key);
       if (static_cast<int>((h & 0xFFFFFull) % static_cast<uint64_t>(nsw)) != s) continue;
       const int2 tp = w.ptmp[pos];
       const int64_t src = (static_cast<int64_t>(pos) / g.rcap) * g.rcap + (static_cast<uint32_t>(tp.x) >> 12);
-      w.recres[src] = make_int2(static_cast<int>(static_cast<unsigned int>(cfp[tp.x & 0xFFF])), tp.y);
+      const unsigned int kidx = static_cast<unsigned int>(cfp[tp.x & 0xFFF]);
+      const unsigned int fl = kidx == static_cast<unsigned int>(pos) ? kRecFirst : 0u;
+      w.recres[src] = make_int2(static_cast<int>(kidx), static_cast<int>(static_cast<unsigned int>(tp.y) | fl));
     }
     ++s;
     __syncthreads();  // the next sweep clears the LDS
@@ -578,12 +609,30 @@ __device__ inline KeyInfo key_info(const Work& w, int k) {
   return w.kinfo[min(max(k, 0), static_cast<int>(w.nkeyidx - 1))];
 }
 
+// The first records of record tile rt (4 record slots per thread): the key
+// index of each first record (a key's first record is its only one that is
+// counted), or -1.  Records past the dedup block's count are not read.
+__device__ inline void first_records(const Work& w, int64_t rt, int (&f)[4]) {
+  const int64_t per = w.g.rcap / kRankTile;  // record tiles per dedup block
+  const int64_t blk = rt / per;
+  const int64_t r0 = (rt % per) * kRankTile + static_cast<int64_t>(threadIdx.x) * 4;
+  const int64_t nr = w.nrec[blk];
+  const int4 a = *reinterpret_cast<const int4*>(w.recres + blk * w.g.rcap + r0);  // 2 records
+  const int4 b = *reinterpret_cast<const int4*>(w.recres + blk * w.g.rcap + r0 + 2);
+  const int x[4] = {a.x, a.z, b.x, b.z}, y[4] = {a.y, a.w, b.y, b.w};
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    f[k] = r0 + k < nr && (static_cast<uint32_t>(y[k]) & kRecFirst) ? x[k] : -1;
+}
+
+// Per record tile: sums over its first records (keys, their counts, keys not
+// found, hot keys, hot-key units).  Record tiles in block-major order list
+// the keys in the order of their first positions.
 template <int NT>
-__global__ __launch_bounds__(NT) void k_first_sums(Work w, int64_t n) {
+__global__ __launch_bounds__(NT) void k_first_sums(Work w) {
   __shared__ int sh[NT / kWave + 1][5];
-  const int64_t i0 = (static_cast<int64_t>(blockIdx.x) * NT + threadIdx.x) * kRankItems;
   int f[4];
-  load4(w.firstkey, i0, n, f);
+  first_records(w, blockIdx.x, f);
   KeyInfo ki[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) ki[k] = key_info(w, f[k]);
@@ -781,8 +830,8 @@ hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const TableDev& 
   }
   const hipError_t e = launch_dedup_keys(values, n, t, w, ev_tile, ev_part, s);
   if (e != hipSuccess) return e;
-  const int64_t nb = (n + kRankTile - 1) / kRankTile;
-  k_first_sums<kBlock><<<static_cast<unsigned>(nb), kBlock, 0, s>>>(w, n);
+  const int64_t nb = record_tiles(w.g);
+  k_first_sums<kBlock><<<static_cast<unsigned>(nb), kBlock, 0, s>>>(w);
   const int64_t nch = (nb + kScanChunk - 1) / kScanChunk;
   k_scan5<kScanChunk / 1024><<<static_cast<unsigned>(nch), 1024, 0, s>>>(w.bsum, nb, w.ntiles, w.csum, nch, w.scal,
                                                                           t.scal, h_live, tag);
@@ -795,16 +844,15 @@ hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const TableDev& 
 // ---------------------------------------------------------------------------
 
 template <int NT>
-__global__ __launch_bounds__(NT) void k_compact(TableDev t, Work w, const int64_t* __restrict__ values, int64_t n) {
+__global__ __launch_bounds__(NT) void k_compact(TableDev t, Work w) {
   __shared__ int sh[NT / kWave + 1][5];
-  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * NT * kRankItems + threadIdx.x * kRankItems;
   const int b = blockIdx.x;
-  int pre[5];  // the tile's exclusive prefixes (first, count, new, hot, units)
+  int pre[5];  // the record tile's exclusive prefixes (keys, count, new, hot, units)
   const int64_t nch = (static_cast<int64_t>(gridDim.x) + kScanChunk - 1) / kScanChunk;
 #pragma unroll
   for (int a = 0; a < 5; ++a) pre[a] = w.bsum[a * w.ntiles + b] + w.csum[a * nch + b / kScanChunk];
   int f[4];
-  load4(w.firstkey, i0, n, f);
+  first_records(w, b, f);
   KeyInfo ki[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) ki[k] = key_info(w, f[k]);  // all four reads in flight together
@@ -820,14 +868,11 @@ __global__ __launch_bounds__(NT) void k_compact(TableDev t, Work w, const int64_
       cu += unit_count(ki[k].count);
     }
   }
-  // the tile's first occurrences get consecutive unique ids, segments, rows
-  // of new keys, hot-key indices and backward units
+  // the tile's keys get consecutive unique ids, segments, rows of new keys,
+  // hot-key indices and backward units
   const int v[5] = {cf, cc, cn, cl, cu};
   int ex[5], tot[5];
   block_excl_scan5<NT>(v, ex, tot, sh);
-  int64_t keys[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) keys[k] = f[k] >= 0 ? values[i0 + k] : 0;  // all in flight together
   int uid = pre[0] + ex[0];
   int start = pre[1] + ex[1];
   int64_t nr = pre[2] + ex[2];
@@ -841,7 +886,7 @@ __global__ __launch_bounds__(NT) void k_compact(TableDev t, Work w, const int64_
   for (int k = 0; k < 4; ++k) {
     if (f[k] < 0) continue;
     const int c = ki[k].count;
-    const int64_t key = keys[k];
+    const int64_t key = ki[k].key;
     w.unique[uid] = key;
     int li = -1;
     if (c > kLong) {
@@ -976,7 +1021,7 @@ __device__ inline void occ_pass(const Work& w, int64_t n, int64_t blk) {
       pos[k] = -1;
       continue;
     }
-    const int rk = rr[k].y + static_cast<int>(o & 0xFFFu);
+    const int rk = static_cast<int>(static_cast<uint32_t>(rr[k].y) & ~kRecFirst) + static_cast<int>(o & 0xFFFu);
     pos[k] = a[k].start + rk;
     if (OCC && a[k].long_idx >= 0) {
       const int sh = unit_shift(a[k].count);
@@ -1017,9 +1062,9 @@ __global__ __launch_bounds__(kBlock) void k_occ_init(TableDev t, Work w, int64_t
 hipError_t launch_compact_insert(const int64_t* values, int64_t n, const TableDev& t, const Work& w, bool occ_lists,
                                  hipEvent_t* ev_compact, hipEvent_t* ev_init, hipEvent_t* ev_occ, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  const int64_t nb = (n + kRankTile - 1) / kRankTile;
+  const int64_t nb = record_tiles(w.g);
   if (ev_compact && ev_compact[0]) (void)hipEventRecord(ev_compact[0], s);
-  k_compact<kBlock><<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, w, values, n);
+  k_compact<kBlock><<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, w);
   if (ev_compact && ev_compact[1]) (void)hipEventRecord(ev_compact[1], s);
   // one launch: the per-occurrence pass and the new rows (the init-rows and
   // occurrence events both bracket it)

@@ -9,14 +9,14 @@
 //
 // Passes (the first two are the lookup's dedup passes with no IDMap):
 //   k_tile_dedup, k_part_dedup   key index, first position and count of
-//                                every distinct key; a marker at its first
-//                                position
-//   k_owner_hist     per block of positions: distinct keys (first
-//                    occurrences) per owner, in LDS
+//                                every distinct key; its first record flagged
+//                                (records are in first-position order)
+//   k_owner_hist     per block of record slots: distinct keys (first
+//                    records) per owner, in LDS
 //   k_scan_one / k_scan_flat  exclusive scan of those counts in (shard,
 //                    block) order (one block, or chunks + a last-block pass)
-//   k_owner_scatter  per block, in position order: stable rank of each first
-//                    occurrence among its shard's (wave ballots on the owner
+//   k_owner_scatter  per block, in record order: stable rank of each first
+//                    record among its shard's (wave ballots on the owner
 //                    bits), key to its output slot, slot by key index
 //   k_ids_inverse    per id: the output slot of its key (id -> record -> key
 //                    index -> slot)
@@ -52,21 +52,34 @@ OwnerGeom owner_geom(int64_t n, int G) {
   return og;
 }
 
-// Four ids of rank tile b (strided by the block size: position order is
-// item-major, then thread) and their first-occurrence markers.
-__device__ inline void load_tile(const int32_t* __restrict__ firstkey, const int64_t* __restrict__ values, int64_t n,
-                                 int64_t b, int (&f)[kRankItems], int64_t (&v)[kRankItems]) {
+// The owner passes walk the dedup records, whose record tiles (block-major,
+// kRankTile record slots each) list every key once, at its first record, in
+// the order of the keys' first positions.  "Position" b below is a record
+// slot: record tile b / kRankTile, slot b % kRankTile; item k of thread t is
+// slot k * kBlock + t (item-major, then thread: ascending record order).
+// f[k]: the key index of a first record, else -1; v[k]: its key (from the
+// partition-ordered copy, whose entry at the key index is that record).
+__device__ inline void load_tile(const Work& w, int64_t b, int (&f)[kRankItems], int64_t (&v)[kRankItems]) {
+  const int64_t per = w.g.rcap / kRankTile;
+  const int64_t rt = b / kRankTile;
+  const int64_t blk = rt / per;
+  const int64_t base = blk * w.g.rcap + (rt % per) * kRankTile;
+  const int64_t nr = blk * w.g.rcap + w.nrec[blk];
+  int2 r[kRankItems];
+#pragma unroll
+  for (int k = 0; k < kRankItems; ++k) r[k] = w.recres[base + k * kBlock + threadIdx.x];
 #pragma unroll
   for (int k = 0; k < kRankItems; ++k) {
-    const int64_t i = b + k * kBlock + threadIdx.x;
-    f[k] = i < n ? firstkey[i] : -1;
-    v[k] = i < n ? values[i] : 0;
+    const int64_t j = base + k * kBlock + threadIdx.x;
+    f[k] = j < nr && (static_cast<uint32_t>(r[k].y) & kRecFirst) ? r[k].x : -1;
   }
+#pragma unroll
+  for (int k = 0; k < kRankItems; ++k)
+    v[k] = f[k] >= 0 ? static_cast<int64_t>(w.srec[f[k]].key ^ kSign) : 0;  // all in flight together
 }
 
-__global__ __launch_bounds__(kBlock) void k_owner_hist(const int32_t* __restrict__ firstkey,
-                                                       const int64_t* __restrict__ values, int64_t n, int G,
-                                                       uint64_t seed, OwnerGeom og, int32_t* __restrict__ hist) {
+__global__ __launch_bounds__(kBlock) void k_owner_hist(Work w, int64_t n, int G, uint64_t seed, OwnerGeom og,
+                                                       int32_t* __restrict__ hist) {
   __shared__ int lh[kMaxShards];
   for (int q = threadIdx.x; q < G; q += kBlock) lh[q] = 0;
   __syncthreads();
@@ -76,7 +89,7 @@ __global__ __launch_bounds__(kBlock) void k_owner_hist(const int32_t* __restrict
     if (b >= n) break;  // block-uniform
     int f[kRankItems];
     int64_t v[kRankItems];
-    load_tile(firstkey, values, n, b, f, v);
+    load_tile(w, b, f, v);
 #pragma unroll
     for (int k = 0; k < kRankItems; ++k)
       if (f[k] >= 0) atomicAdd(&lh[owner_of(v[k], seed, G, og.gmask)], 1);
@@ -189,7 +202,7 @@ __global__ __launch_bounds__(1024) void k_scan_one(int32_t* __restrict__ a, int6
   if (threadIdx.x == 0) *total = sh[NW];
 }
 
-__global__ __launch_bounds__(kBlock) void k_owner_scatter(Work w, const int64_t* __restrict__ values, int64_t n, int G,
+__global__ __launch_bounds__(kBlock) void k_owner_scatter(Work w, int64_t n, int G,
                                                           uint64_t seed, OwnerGeom og, const int32_t* __restrict__ hist,
                                                           const int32_t* __restrict__ csum,
                                                           int32_t* __restrict__ kslot, const int64_t* pscal,
@@ -222,7 +235,7 @@ __global__ __launch_bounds__(kBlock) void k_owner_scatter(Work w, const int64_t*
     if (b >= n) break;  // block-uniform
     int f[kRankItems];
     int64_t v[kRankItems];
-    load_tile(w.firstkey, values, n, b, f, v);
+    load_tile(w, b, f, v);
     uint32_t own[kRankItems];
 #pragma unroll
     for (int k = 0; k < kRankItems; ++k) own[k] = f[k] >= 0 ? owner_of(v[k], seed, G, og.gmask) : 0u;
@@ -315,15 +328,17 @@ hipError_t launch_ids_partition(const int64_t* values, int64_t n, int G, uint64_
   t.scal = pscal;
   hipError_t e = launch_dedup_keys(values, n, t, w, nullptr, nullptr, s);
   if (e != hipSuccess) return e;
-  k_owner_hist<<<static_cast<unsigned>(og.nb), kBlock, 0, s>>>(w.firstkey, values, n, G, seed, og, hist);
+  // the owner passes walk the record slots of the dedup blocks
+  const int64_t nslots = record_tiles(w.g) * kRankTile;
+  k_owner_hist<<<static_cast<unsigned>(og.nb), kBlock, 0, s>>>(w, nslots, G, seed, og, hist);
   constexpr int kOneBlock = 16;  // counts per thread of the one-block scan
   if (og.len <= 1024 * kOneBlock)
     k_scan_one<kOneBlock><<<1, 1024, 0, s>>>(hist, og.len, csum, og.nch, pscal + kPTotal);
   else
     k_scan_flat<kScanChunk / 1024><<<static_cast<unsigned>(og.nch), 1024, 0, s>>>(hist, og.len, csum, og.nch,
                                                                                   pscal + kPCounter, pscal + kPTotal);
-  k_owner_scatter<<<static_cast<unsigned>(og.nb), kBlock, 0, s>>>(w, values, n, G, seed, og, hist, csum, kslot,
-                                                                  pscal, keys_out, shard_offsets, info);
+  k_owner_scatter<<<static_cast<unsigned>(og.nb), kBlock, 0, s>>>(w, nslots, G, seed, og, hist, csum, kslot, pscal,
+                                                                  keys_out, shard_offsets, info);
   k_ids_inverse<<<grid_for(n, kBlock * 4, 1ll << 31), kBlock, 0, s>>>(w, kslot, n);
   return hipGetLastError();
 }

@@ -193,10 +193,12 @@ struct FrontGeom {
   int logP;
 };
 
-// Record of one distinct key of a dedup tile.  Written in tile order with
-// meta = (rank of the record among its block's records of the same
-// partition) << 12 | (count - 1); the block then copies its records into
-// partition order with meta = (tile-order index) << 12 | (count - 1).
+// Record of one distinct key of a dedup tile.  A tile's records are written
+// in the order of the keys' first positions in the tile (so a block's
+// records, tile after tile, are in first-position order), with meta = (rank
+// of the record among its block's records of the same partition) << 12 |
+// (count - 1); the block then copies its records into partition order with
+// meta = (tile-order index) << 12 | (count - 1).
 struct alignas(16) TileRec {
   unsigned long long key;  // encoded key
   unsigned int tmin;       // first position of the key in the tile
@@ -207,12 +209,11 @@ struct alignas(16) TileRec {
 // the partition-ordered record copies) of the key's first record.
 struct alignas(32) KeyInfo {
   long long row;  // Blocks row (-1: not found / could not be inserted)
-  int first;      // first position of the key in the batch
+  long long key;  // the key
   int count;      // occurrences
   int uid;        // unique id (first-occurrence order)
   int start;      // first position of the key's segment of the occurrence list
   int long_idx;   // hot-key index, -1 if count <= kLong
-  int pad;
 };
 
 // occ_word of a rejected (reserved) key
@@ -233,9 +234,9 @@ struct alignas(16) Unit {
 // Workspace arrays of one forward (and its backward).
 struct Work {
   uint32_t* occ_word;   // [n] dedup record index (in its block) << 12 | rank in the tile
-  int32_t* firstkey;    // [n] key index at the key's first position, else -1
   TileRec* trec;        // [nblk * rcap] records of the dedup tiles, per block, tile order
-  int2* recres;         // [nblk * rcap] (same memory as trec) {key index, rank base} per record
+  int2* recres;         // [nblk * rcap] (same memory as trec) {key index, rank base | kRecFirst} per record
+  int32_t* nrec;        // [nblk] records of each dedup block
   TileRec* srec;        // [nblk * rcap] the same records per block in partition order
   int32_t* pcnt;        // [nblk * P] records per (block, partition)
   int32_t* poff;        // [nblk * P] their offsets in the block's partition-ordered copy
@@ -254,13 +255,20 @@ struct Work {
   int32_t* long_u;      // [n/kLong + 1] unique id of each hot key
   int32_t* long_start;  // [n/kLong + 1] first backward unit of each hot key
   Unit* units;          // [2n/kUnit + 2] backward units of the hot keys
-  int32_t* bsum;        // [5 * ntiles] tile sums: first occurrences, their counts, new keys, hot keys, units
-  int32_t* csum;        // [5 * (ntiles / kScanChunk + 1)] the same per chunk of tiles
+  int32_t* bsum;        // [5 * ntiles] record-tile sums: keys, their counts, new keys, hot keys, units
+  int32_t* csum;        // [5 * (ntiles / kScanChunk + 1)] the same per chunk of record tiles
   int64_t* scal;        // [kCScalars]
   float* gpart;         // [(2n/kUnit + 2) * D] partial gradient row of each backward unit
-  int64_t ntiles;       // tiles of the position passes (bsum stride)
+  int64_t ntiles;       // record tiles (kRankTile records of one dedup block each; bsum stride)
   FrontGeom g;
 };
+
+// The record result of a key's first record (the one holding its first
+// position) carries this bit in its rank-base word.
+constexpr uint32_t kRecFirst = 0x80000000u;
+// Record tiles: dedup block b's record slots [c * kRankTile, (c + 1) *
+// kRankTile) for c < rcap / kRankTile, in block-major order.
+inline int64_t record_tiles(const FrontGeom& g) { return g.nblk * (g.rcap / kRankTile); }
 
 struct OptArgs {
   int opt;  // 0 adagrad, 1 adam, 2 adamw, 3 adam (epsilon-hat form), 4 row-wise adagrad, 5 row-wise adam
