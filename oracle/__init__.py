@@ -59,6 +59,8 @@ def lib():
         L.or_mod.argtypes = [p, p, i32, p, p]
         L.or_evict.restype = i64
         L.or_evict.argtypes = [p, C.c_uint32]
+        L.or_compact.restype = i64
+        L.or_compact.argtypes = [p]
         L.or_rows_allocated.restype = i64
         L.or_rows_allocated.argtypes = [p]
         L.or_clock.restype = C.c_uint32
@@ -207,6 +209,11 @@ class Table:
     def evict(self, max_age: int) -> int:
         """Remove the keys not looked up in the last max_age calls (age > max_age)."""
         return int(lib().or_evict(self.h, max_age & 0xFFFFFFFF))
+
+    def compact(self) -> int:
+        """Move the live rows above the live count into the free rows below it
+        (k-th above into k-th free below, both ascending); returns the rows moved."""
+        return int(lib().or_compact(self.h))
 
     def rows_allocated(self) -> int:
         return int(lib().or_rows_allocated(self.h))

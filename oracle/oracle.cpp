@@ -361,6 +361,48 @@ int64_t or_evict(void* h, uint32_t max_age) {
   return count;
 }
 
+// Compaction of the Blocks after eviction.  The paper sizes its Blocks
+// flexibly (they grow by appending memory blocks) and evicts stale
+// features, but gives no procedure for giving rows back; the reading taken:
+// with L live keys, each row r >= L that holds a key moves into a free row
+// below L -- the k-th such row in ascending order into the k-th free row
+// below L in ascending order -- with its values, optimizer state and
+// last-lookup clock, and the IDMap follows it.  Afterwards rows 0 .. L-1
+// hold every live key, no row is free, and L rows are allocated, so memory
+// past row L can be released.  Returns the number of rows moved.
+int64_t or_compact(void* h) {
+  Table* T = static_cast<Table*>(h);
+  const int64_t L = T->live();
+  std::vector<int64_t> holes, movers;
+  for (int64_t r = 0; r < L && r < T->nrows; ++r)
+    if (T->row_key[r] == KEY_EMPTY) holes.push_back(r);
+  for (int64_t r = L; r < T->nrows; ++r)
+    if (T->row_key[r] != KEY_EMPTY) movers.push_back(r);
+  if (holes.size() != movers.size()) return -1;  // cannot happen: both count the keys missing below L
+  for (size_t k = 0; k < movers.size(); ++k) {
+    const int64_t src = movers[k], dst = holes[k];
+    for (int j = 0; j < T->dim; ++j) {
+      if (T->row_dtype == BF16) T->wb[dst * T->dim + j] = T->wb[src * T->dim + j];
+      else T->w[dst * T->dim + j] = T->w[src * T->dim + j];
+    }
+    for (int e = 0; e < T->state_elems(); ++e) T->put_s(dst, e, T->get_s(src, e));
+    T->row_key[dst] = T->row_key[src];
+    T->row_seen[dst] = T->row_seen[src];
+    T->idmap[T->row_key[src]] = dst;
+  }
+  // rows L and beyond are gone
+  T->nrows = L;
+  T->row_key.resize(L);
+  T->row_seen.resize(L);
+  if (T->row_dtype == BF16) T->wb.resize(L * T->dim);
+  else T->w.resize(L * T->dim);
+  if (T->nvec() >= 1) T->s1.resize(L * T->dim);
+  if (T->nvec() == 2) T->s2.resize(L * T->dim);
+  if (T->row_scalar()) T->sr.resize(L);
+  T->free_stack.clear();
+  return static_cast<int64_t>(movers.size());
+}
+
 int64_t or_rows_allocated(void* h) { return static_cast<Table*>(h)->nrows; }
 uint32_t or_clock(void* h) { return static_cast<Table*>(h)->clock; }
 

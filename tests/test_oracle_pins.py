@@ -883,3 +883,70 @@ def test_eviction_max_age_zero_and_untouched_table():
     assert T.evict(0) == 2 and T.export()[0].tolist() == [2]
     st, rows, _ = T.find_or_insert(np.array([1], dtype=np.int64))
     assert rows.tolist() == [2]                  # rows 0 and 2 were freed (pushed 0, 2): 2 on top
+
+
+# --------------------------------------------------------------------------- compaction
+
+
+def test_compaction_moves_the_rows_above_the_live_count_into_the_holes_below():
+    """Explicit case: rows 0..7, keys 10..17; evict the keys of rows 1, 3, 6.
+    Live L = 5; holes below 5: rows 1, 3; rows holding keys at or above 5:
+    5, 7.  Row 5 (key 15) moves to row 1, row 7 (key 17) to row 3."""
+    D = 4
+    T = O.Table(D, opt=O.ADAM, seed=3)
+    keys = np.arange(10, 18, dtype=np.int64)
+    _, rows, _ = T.find_or_insert(keys)                                    # call 1: rows 0..7
+    assert rows.tolist() == list(range(8))
+    T.optimizer(rows, np.arange(8 * D, dtype=np.float32).reshape(8, D) - 5, 0.1, 1e-8, 0.9, 0.999)
+    T.find_or_insert(np.array([10, 12, 14, 15, 17], dtype=np.int64))      # call 2: 11, 13, 16 go stale
+    assert T.evict(0) == 3
+    _, w_before, s_before = T.read_rows(np.array([15, 17, 10, 12, 14], dtype=np.int64))
+    assert T.compact() == 2
+    ek, er = T.export()
+    got = dict(zip(ek.tolist(), er.tolist()))
+    assert got == {10: 0, 12: 2, 14: 4, 15: 1, 17: 3}
+    assert T.rows_allocated() == 5
+    _, w_after, s_after = T.read_rows(np.array([15, 17, 10, 12, 14], dtype=np.int64))
+    assert np.array_equal(w_before, w_after) and np.array_equal(s_before, s_after)   # rows move whole
+    # nothing is free any more: a new key takes row L
+    _, rows, nn = T.find_or_insert(np.array([99], dtype=np.int64))
+    assert rows.tolist() == [5] and nn == 1
+    # a compact table stays put
+    assert T.compact() == 0
+
+
+@pytest.mark.parametrize("opt,dtype", [(O.ADAGRAD, O.F32), (O.ADAM, O.BF16), (O.ADAM_RW, O.F32)])
+def test_compaction_brute_force(opt, dtype):
+    """Random churn, then compaction: the key set and every key's row
+    contents (values, state) are unchanged, the rows are exactly 0..L-1, the
+    rows below L that held a key keep it, and the moved rows pair the holes
+    and the rows at or above L in ascending order (checked against the
+    pre-compaction key -> row map)."""
+    g = np.random.default_rng(7)
+    D = 8
+    T = O.Table(D, row_dtype=dtype, opt=opt, seed=11)
+    for step in range(10):
+        keys = g.integers(0, 400, size=int(g.integers(20, 120))).astype(np.int64)
+        _, rows, _ = T.find_or_insert(keys)
+        T.optimizer(np.unique(rows), g.standard_normal((np.unique(rows).size, D)).astype(np.float32),
+                    0.05, 1e-8, 0.9, 0.999)
+        if step in (3, 6, 9):
+            T.evict(int(g.integers(0, 2)))
+    ek, er = T.export()
+    before = dict(zip(ek.tolist(), er.tolist()))
+    _, w0, s0 = T.read_rows(ek)
+    L = len(before)
+    holes = sorted(set(range(L)) - set(r for r in before.values() if r < L))
+    movers = sorted(r for r in before.values() if r >= L)
+    assert len(holes) == len(movers) and len(movers) > 0
+    moved = T.compact()
+    assert moved == len(movers)
+    ek2, er2 = T.export()
+    after = dict(zip(ek2.tolist(), er2.tolist()))
+    assert set(after) == set(before) and sorted(after.values()) == list(range(L))
+    dest = dict(zip(movers, holes))
+    for k, r in before.items():
+        assert after[k] == (dest[r] if r >= L else r)
+    _, w1, s1 = T.read_rows(ek)
+    assert np.array_equal(w0, w1) and np.array_equal(s0, s1)
+    assert T.rows_allocated() == L
