@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define RS_VERSION 8
+#define RS_VERSION 9
 
 typedef enum {
   RS_OK = 0,
@@ -197,8 +197,9 @@ rs_status ht_find(rs_table* t, const int64_t* keys, int64_t n, int64_t* rows_out
  * returns (and clears) any latched device error. */
 rs_status ht_size(rs_table* t, int64_t* live_host, rs_stream stream);
 
-/* Feature eviction (Embedding Engine: "evicting stale features during
- * continuous training").  Every lookup call (ht_find_or_insert,
+/* Feature eviction (Embedding Engine, Framework Components: the KV table
+ * drops features that went stale while training goes on).  Every lookup
+ * call (ht_find_or_insert,
  * lookup_prepare / lookup_pool_fwd) advances the table's lookup clock by
  * one, and each key it looks up (found or inserted) records that clock.
  * ht_evict removes every key whose age -- the current clock minus its
@@ -208,9 +209,28 @@ rs_status ht_size(rs_table* t, int64_t* live_host, rs_stream stream);
  * ascending row order.  New keys take free rows from the top of that stack
  * (re-initialised exactly like a new row) before new rows are added.
  * Only for tables created with evictable = 1 and fewer than 2^31 rows
- * provisioned (else RS_EINVAL).  Synchronizes
- * the stream; *n_evicted_host (may be NULL) receives the count. */
+ * provisioned (else RS_EINVAL).  Synchronizes the stream (only that one):
+ * the caller orders ht_evict after every outstanding pool, backward and
+ * optimizer call of the table on any stream, since a freed row may be handed
+ * to a new key by the next lookup.  *n_evicted_host (may be NULL) receives
+ * the count. */
 rs_status ht_evict(rs_table* t, uint32_t max_age, int64_t* n_evicted_host, rs_stream stream);
+
+/* Compaction of the Blocks after eviction (the Blocks grow by appending
+ * chunks of rows; this gives memory back once keys have been evicted).  With
+ * L live keys, every row at or above row L that holds a key moves -- values,
+ * optimizer state, key and last-lookup clock -- into a free row below L: the
+ * k-th such row in ascending row order into the k-th free row below L in
+ * ascending order; the IDMap follows the moved keys.  Afterwards rows 0 ..
+ * L-1 hold every live key, no row is free (new keys take rows L, L+1, ...),
+ * and the Blocks chunks wholly past row L are released (unmapped, or handed
+ * back to the table's allocator).  Row ids returned before the call
+ * (rows_out, ctx->rows) are no longer valid; the call must be ordered after
+ * all outstanding work of the table, and synchronizes the stream.
+ * *moved_host / *bytes_released_host (either may be NULL) receive the rows
+ * moved and the bytes of Blocks memory released.  Only for tables created
+ * with evictable = 1 (else RS_EINVAL).  Errors: RS_ENOMEM, RS_EHIP. */
+rs_status ht_compact(rs_table* t, int64_t* moved_host, int64_t* bytes_released_host, rs_stream stream);
 
 /* Synchronize the stream and return (and clear) any latched device error. */
 rs_status rs_table_check(rs_table* t, rs_stream stream);
@@ -269,11 +289,14 @@ rs_status lookup_pool_fwd(rs_table* t, const int64_t* values, const int64_t* off
  * lookup_prepare: everything of lookup_pool_fwd except the gather + pool:
  * dedup, IDMap find-or-insert, row init of new keys, and the per-occurrence
  * bookkeeping, into ctx (same arguments and errors as lookup_pool_fwd
- * minus out / mask).  It reads and writes only the IDMap, the rows of the
- * keys it inserts and ctx -- never a row that
- * already existed -- so it may run while an earlier batch's
- * lookup_pool_prepared / backward / optimizer are still running on another
- * stream.  Prepares of one table must be issued in order on one stream.
+ * minus out / mask).  It writes the IDMap, the rows of the keys it inserts
+ * and ctx; on a table with eviction it also records the lookup clock in the
+ * key record of every row it finds (bytes no pool, backward or optimizer
+ * touches).  New keys take new rows, or rows that ht_evict freed; so a
+ * prepare may run while an earlier batch's lookup_pool_prepared / backward /
+ * optimizer are still running on another stream, provided no ht_evict was
+ * issued after that batch's forward (its freed rows could still be in use).
+ * Prepares of one table must be issued in order on one stream.
  *
  * lookup_pool_prepared: the gather + pool of a prepared ctx.  The caller
  * orders it after the prepare (same stream, or an event) and after the
@@ -368,7 +391,8 @@ rs_status ids_partition_static(const int64_t* values, int64_t n, int32_t nshards
  *
  * fused_bucketize: values fp32 [n] -> out int64 [n], out[i] = the number of
  *   boundaries b of i's column with b <= values[i] (TensorFlow's Bucketize:
- *   boundaries[k-1] <= x < boundaries[k] gives k; a NaN gives 0).  Column c's
+ *   boundaries[k-1] <= x < boundaries[k] gives k; a NaN, below no boundary,
+ *   gives the number of boundaries).  Column c's
  *   boundaries are boundaries[bnd_offsets[c] .. bnd_offsets[c+1]), fp32,
  *   nondecreasing and not NaN (int64 [ncols+1] offsets, bnd_offsets[0] = 0).
  * fused_mod: values int64 [n] -> out int64 [n], out[i] = values[i] mod m in

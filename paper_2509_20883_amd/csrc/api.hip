@@ -834,6 +834,70 @@ rs_status ht_evict(rs_table* t, uint32_t max_age, int64_t* n_evicted_host, rs_st
   return take_latched(t);
 }
 
+rs_status ht_compact(rs_table* t, int64_t* moved_host, int64_t* bytes_released_host, rs_stream stream) {
+  if (!t) return fail(RS_EINVAL, "null table");
+  if (t->meta_off < 0) return fail(RS_EINVAL, "the table was created without eviction (evictable = 0)");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  RS_HIP(hipStreamSynchronize(s));
+  int64_t ts[kTScalars];
+  RS_HIP(hipMemcpy(ts, t->d_scal, sizeof(ts), hipMemcpyDeviceToHost));
+  const int64_t L = ts[kTKeys], hw = ts[kTLive];
+  int64_t moved = 0;
+  if (hw > L) {
+    const int64_t nb = (hw + kEvictRows - 1) / kEvictRows;
+    int32_t* cnt = static_cast<int32_t*>(t->alloc(sizeof(int32_t) * 2 * static_cast<size_t>(nb + 1)));
+    int64_t* lists = static_cast<int64_t*>(t->alloc(sizeof(int64_t) * 2 * static_cast<size_t>(hw - L)));
+    rs_status st = RS_OK;
+    if (!cnt || !lists) {
+      st = fail(RS_ENOMEM, "allocation of the compaction lists failed");
+    } else {
+      const hipError_t e = launch_compact_rows(t->dev(), L, hw, cnt, cnt + nb + 1, lists, lists + (hw - L), s);
+      int32_t h[2] = {0, 0};
+      if (e != hipSuccess || hipStreamSynchronize(s) != hipSuccess ||
+          hipMemcpy(&h[0], cnt + nb, sizeof(int32_t), hipMemcpyDeviceToHost) != hipSuccess ||
+          hipMemcpy(&h[1], cnt + nb + 1 + nb, sizeof(int32_t), hipMemcpyDeviceToHost) != hipSuccess)
+        st = fail(RS_EHIP, "compaction failed");
+      moved = std::min(h[0], h[1]);
+    }
+    t->release(cnt);
+    t->release(lists);
+    if (st != RS_OK) return st;
+  }
+  // give back the Blocks memory past row L (whole chunks)
+  int64_t released = 0;
+  if (t->custom) {
+    const size_t keep = static_cast<size_t>((L + t->d.block_rows - 1) / t->d.block_rows);
+    while (t->achunks.size() > keep) {
+      t->release(t->achunks.back());
+      t->achunks.pop_back();
+      released += static_cast<int64_t>(t->chunk_bytes);
+    }
+    t->rows_prov = static_cast<int64_t>(t->achunks.size()) * t->d.block_rows;
+  } else {
+    const size_t need = static_cast<size_t>(L) * static_cast<size_t>(t->stride);
+    const size_t keep = (need + t->chunk_bytes - 1) / t->chunk_bytes;
+    while (t->chunks.size() > keep) {
+      const size_t off = (t->chunks.size() - 1) * t->chunk_bytes;
+      if (hipMemUnmap(t->va_base + off, t->chunk_bytes) != hipSuccess ||
+          hipMemRelease(t->chunks.back()) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(RS_EHIP, "unmapping a Blocks chunk failed");
+      }
+      t->chunks.pop_back();
+      t->mapped -= t->chunk_bytes;
+      released += static_cast<int64_t>(t->chunk_bytes);
+    }
+    t->rows_prov = static_cast<int64_t>(t->mapped / static_cast<size_t>(t->stride));
+  }
+  rs_status st = set_scalar(t, kTRowCap, t->rows_prov, s);
+  if (st != RS_OK) return st;
+  RS_HIP(hipStreamSynchronize(s));
+  reset_bound(t, std::max(L + ts[kTTomb], L));
+  if (moved_host) *moved_host = moved;
+  if (bytes_released_host) *bytes_released_host = released;
+  return take_latched(t);
+}
+
 rs_status rs_table_check(rs_table* t, rs_stream stream) {
   if (!t) return fail(RS_EINVAL, "null table");
   RS_HIP(hipStreamSynchronize(static_cast<hipStream_t>(stream)));

@@ -1187,6 +1187,121 @@ hipError_t launch_evict(const TableDev& t, int64_t rows_prov, uint32_t max_age, 
 }
 
 // ---------------------------------------------------------------------------
+// compaction of the Blocks after eviction
+// ---------------------------------------------------------------------------
+
+// Row r holds a key (eviction writes INT64_MIN into a freed row's key field).
+__device__ inline bool row_holds_key(const TableDev& t, int64_t r) {
+  return *reinterpret_cast<const int64_t*>(t.store.row(r) + t.meta_off) != INT64_MIN;
+}
+
+// Per block of kEvictRows rows below the high-water mark hw: the free rows
+// below the live count L ("holes") and the rows at or above L that hold a key
+// ("movers").  Thread tid owns rows r0 + tid*K ... (row order = thread order).
+__global__ __launch_bounds__(kBlock) void k_compact_count(TableDev t, int64_t L, int64_t hw, int32_t* __restrict__ hc,
+                                                          int32_t* __restrict__ mc) {
+  __shared__ int sh[kBlock / kWave + 1];
+  constexpr int K = kEvictRows / kBlock;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kEvictRows + static_cast<int64_t>(threadIdx.x) * K;
+  int h = 0, m = 0;
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int64_t r = r0 + k;
+    if (r >= hw) continue;
+    const bool held = row_holds_key(t, r);
+    h += r < L && !held;
+    m += r >= L && held;
+  }
+  const int th = block_sum<kBlock>(h, sh);
+  __syncthreads();
+  const int tm = block_sum<kBlock>(m, sh);
+  if (threadIdx.x == 0) {
+    hc[blockIdx.x] = th;
+    mc[blockIdx.x] = tm;
+  }
+}
+
+// The holes and the movers of each block, in row order, at their ranks
+// (hc / mc hold the blocks' exclusive prefixes).
+__global__ __launch_bounds__(kBlock) void k_compact_list(TableDev t, int64_t L, int64_t hw,
+                                                         const int32_t* __restrict__ hc, const int32_t* __restrict__ mc,
+                                                         int64_t* __restrict__ hole_at, int64_t* __restrict__ src_at,
+                                                         int64_t cap) {
+  __shared__ int sh[kBlock / kWave + 1];
+  constexpr int K = kEvictRows / kBlock;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kEvictRows + static_cast<int64_t>(threadIdx.x) * K;
+  bool hole[K], mover[K];
+  int h = 0, m = 0;
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int64_t r = r0 + k;
+    const bool held = r < hw && row_holds_key(t, r);
+    hole[k] = r < hw && r < L && !held;
+    mover[k] = r >= L && held;
+    h += hole[k];
+    m += mover[k];
+  }
+  int tot;
+  int hp = hc[blockIdx.x] + block_excl_scan<kBlock>(h, sh, tot);
+  int mp = mc[blockIdx.x] + block_excl_scan<kBlock>(m, sh, tot);
+#pragma unroll
+  for (int k = 0; k < K; ++k) {  // both lists hold at most cap = hw - L rows
+    if (hole[k] && hp < cap) hole_at[hp] = r0 + k;
+    if (mover[k] && mp < cap) src_at[mp] = r0 + k;
+    hp += hole[k];
+    mp += mover[k];
+  }
+}
+
+// One wave per move: the k-th mover's row (values, state, key and clock)
+// is copied into the k-th hole, 16 bytes per lane, and its IDMap slot takes
+// the new row.  npairs: the device-side count (the movers' total).
+__global__ __launch_bounds__(kBlock) void k_compact_move(TableDev t, const int64_t* __restrict__ hole_at,
+                                                         const int64_t* __restrict__ src_at,
+                                                         const int32_t* __restrict__ nholes,
+                                                         const int32_t* __restrict__ nmovers, int64_t cap) {
+  const int lane = threadIdx.x & (kWave - 1);
+  // the two counts agree for a consistent table (both are the keys missing
+  // below L); the minimum keeps every index inside the lists regardless
+  const int64_t np = min(min(static_cast<int64_t>(*nholes), static_cast<int64_t>(*nmovers)), cap);
+  if (blockIdx.x == 0 && threadIdx.x == 0 && *nholes != *nmovers)
+    atomicOr(reinterpret_cast<int*>(&t.scal[kTErr]), kErrProbe);
+  const int words = static_cast<int>(t.store.stride / 16);
+  for (int64_t k = static_cast<int64_t>(blockIdx.x) * (kBlock / kWave) + threadIdx.x / kWave; k < np;
+       k += static_cast<int64_t>(gridDim.x) * (kBlock / kWave)) {
+    const int64_t src = src_at[k], dst = hole_at[k];
+    const uint4* sp = reinterpret_cast<const uint4*>(t.store.row(src));
+    uint4* dp = reinterpret_cast<uint4*>(t.store.row(dst));
+    for (int q = lane; q < words; q += kWave) dp[q] = sp[q];
+    if (lane == 0) {
+      const int64_t key = *reinterpret_cast<const int64_t*>(t.store.row(src) + t.meta_off);
+      const int64_t slot = idmap_slot_of(t, static_cast<unsigned long long>(key) ^ kSign);
+      if (slot >= 0) t.slots[slot].row = dst;
+      else atomicOr(reinterpret_cast<int*>(&t.scal[kTErr]), kErrProbe);
+    }
+  }
+}
+
+__global__ void k_compact_finish(int64_t* tscal, int64_t L) {
+  tscal[kTLive] = L;
+  tscal[kTFree] = 0;
+}
+
+hipError_t launch_compact_rows(const TableDev& t, int64_t L, int64_t hw, int32_t* hc, int32_t* mc, int64_t* hole_at,
+                               int64_t* src_at, hipStream_t s) {
+  if (t.meta_off < 0 || hw <= L) return hipErrorInvalidValue;
+  const int64_t nb = (hw + kEvictRows - 1) / kEvictRows;
+  k_compact_count<<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, L, hw, hc, mc);
+  k_evict_scan<<<1, 1024, 0, s>>>(hc, nb);  // exclusive prefixes; the totals at [nb]
+  k_evict_scan<<<1, 1024, 0, s>>>(mc, nb);
+  k_compact_list<<<static_cast<unsigned>(nb), kBlock, 0, s>>>(t, L, hw, hc, mc, hole_at, src_at, hw - L);
+  k_compact_move<<<grid_for(hw - L, kBlock / kWave, 8192), kBlock, 0, s>>>(t, hole_at, src_at, hc + nb, mc + nb,
+                                                                           hw - L);
+  k_compact_finish<<<1, 1, 0, s>>>(t.scal, L);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // find-or-insert results, find-only lookups, rehash, export, read-back
 // ---------------------------------------------------------------------------
 

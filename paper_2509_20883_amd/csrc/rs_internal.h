@@ -350,6 +350,13 @@ hipError_t launch_probe(int kind, void* a, int64_t a_bytes, void* b, const int64
                         hipStream_t s);
 // Lanes per row of the row probes for rows of w16 16-byte words (0: not supported).
 int probe_lanes(int w16);
+// Compaction after eviction: with L live keys and hw rows allocated, the
+// k-th row at or above L holding a key moves (whole: values, state, key,
+// clock) into the k-th free row below L, both in ascending order, and its
+// IDMap slot follows; then hw = L and no row is free.  hc, mc: ints for
+// ceil(hw / kEvictRows) + 1 blocks; hole_at, src_at: hw - L entries each.
+hipError_t launch_compact_rows(const TableDev& t, int64_t L, int64_t hw, int32_t* hc, int32_t* mc, int64_t* hole_at,
+                               int64_t* src_at, hipStream_t s);
 hipError_t launch_rehash(const Slot* old_slots, int64_t old_cap, const TableDev& t, hipStream_t s);
 hipError_t launch_export(const TableDev& t, int64_t cap_slots, int64_t* keys, int64_t* rows, int64_t cap,
                          int64_t* n_dev, hipStream_t s);

@@ -132,6 +132,7 @@ def lib() -> C.CDLL:
         "lookup_pool_bwd_opt": (C.c_int, [p, C.POINTER(RsCtx), p, C.POINTER(OptParams), p]),
         "rs_set_kernel_events": (C.c_int, [p, i32, p, p]),
         "ht_evict": (C.c_int, [p, C.c_uint32, C.POINTER(i64), p]),
+        "ht_compact": (C.c_int, [p, C.POINTER(i64), C.POINTER(i64), p]),
         "ids_partition_workspace_bytes": (C.c_size_t, [i64, i32]),
         "ids_partition": (C.c_int, [p, i64, i32, C.c_uint64, p, p, p, p, p, C.c_size_t, p]),
         "fused_bucketize": (C.c_int, [p, i64, p, i32, p, p, p, i32, p]),
@@ -375,6 +376,13 @@ class Table:
         v = C.c_int64()
         _check(lib().ht_evict(self.h, max_age & 0xFFFFFFFF, C.byref(v), _stream()))
         return v.value
+
+    def compact(self) -> Tuple[int, int]:
+        """Move the live rows above the live count into the free rows below it;
+        returns (rows moved, bytes of Blocks memory released).  Synchronizes."""
+        m, b = C.c_int64(), C.c_int64()
+        _check(lib().ht_compact(self.h, C.byref(m), C.byref(b), _stream()))
+        return m.value, b.value
 
     def check(self):
         _check(lib().rs_table_check(self.h, _stream()))

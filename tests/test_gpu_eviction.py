@@ -97,3 +97,70 @@ def test_evict_errors_and_empty():
     assert rows[:3].tolist() == [0, 1, 2] and np.all(rows[3:] == -1)
     t.check()
     t.close()
+
+
+def _same_contents(gt, ot):
+    rk, _ = ot.export()
+    wg, sg = gt.read_rows(gt.find(torch.from_numpy(rk).cuda()))
+    _, wr, sr = ot.read_rows(rk)
+    assert np.array_equal(wg.cpu().numpy(), wr) and np.array_equal(sg.cpu().numpy(), sr), "row contents differ"
+
+
+@pytest.mark.parametrize("k,opt,alloc", [(0, O.ADAGRAD, False), (2, O.ADAGRAD, False), (1, O.ADAM_RW, False),
+                                         (2, O.ADAGRAD, True)])
+def test_compaction_after_evictions_matches_oracle(k, opt, alloc):
+    """Steps, evictions, then compaction on both sides: the key -> row map is
+    bit-exact (the k-th row at or above the live count into the k-th free row
+    below it), every key's row contents are unchanged (the oracle holds the
+    GPU's rows: stage-wise parity resynchronises it), Blocks memory past the
+    live rows is released, and later steps (new keys at rows L, L+1, ...)
+    keep the step parity."""
+    w = W.workload(k, mini=(k != 0))
+    w.opt = opt
+    _log("compaction", w.name, "allocator" if alloc else "")
+    kw = dict(evictable=True, block_rows=1024)
+    if alloc:
+        kw["allocator"] = R.TorchAllocator()
+    gt, ot = P.gpu_table(w, **kw), P.oracle_table(w)
+    P.prepopulate(w, gt, ot)
+    for step in range(4):
+        b = W.make_batch(w, step)
+        P.run_step_parity(w, gt, ot, b, W.make_grad(w, b, step), step)
+        if step in (1, 2):
+            assert gt.evict(0) == ot.evict(0)
+    live = ot.size()
+    allocated = ot.rows_allocated()
+    moved, released = gt.compact()
+    assert moved == ot.compact()
+    _log(f"  live {live} rows {allocated}: moved {moved}, released {released} bytes")
+    _same_table(gt, ot)
+    _same_contents(gt, ot)
+    assert ot.rows_allocated() == live and released >= 0
+    for step in range(4, 6):
+        b = W.make_batch(w, step)
+        P.run_step_parity(w, gt, ot, b, W.make_grad(w, b, step), step)
+    _same_table(gt, ot)
+    assert gt.compact()[0] == ot.compact() == 0  # compact again: nothing free, nothing moves
+    gt.check()
+    gt.close()
+
+
+def test_compact_errors_and_trivial_cases():
+    t = R.Table(16, O.F32, O.ADAGRAD, capacity_slots=256, seed=1)
+    with pytest.raises(R.RecisError):
+        t.compact()                               # not evictable
+    t.close()
+    t = R.Table(16, O.F32, O.ADAM, capacity_slots=256, seed=1, evictable=True, block_rows=64)
+    assert t.compact() == (0, 0)                  # empty table
+    t.find_or_insert(torch.arange(200, dtype=torch.int64, device="cuda"))
+    assert t.compact()[0] == 0                    # nothing free: nothing moves
+    t.find_or_insert(torch.arange(100, 110, dtype=torch.int64, device="cuda"))
+    assert t.evict(0) == 190 and t.size() == 10   # keys 100..109 stay, at rows 100..109
+    moved, released = t.compact()
+    assert moved == 10 and released >= 0
+    rows = t.find(torch.arange(100, 110, dtype=torch.int64, device="cuda")).cpu().numpy()
+    assert rows.tolist() == list(range(10))       # row 100 + j -> hole j
+    t.find_or_insert(torch.arange(110, dtype=torch.int64, device="cuda"))
+    assert t.size() == 110
+    t.check()
+    t.close()
