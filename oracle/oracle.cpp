@@ -305,8 +305,10 @@ int64_t or_ids_partition(const int64_t* values, int64_t n, int32_t nshards, uint
 // an id by its bucket).  Column c holds values[col_off[c] .. col_off[c+1])
 // and its nondecreasing boundaries bnd[bnd_off[c] .. bnd_off[c+1]).
 // Reading taken (the paper names the operator only): TensorFlow's Bucketize,
-// bucket = the number of boundaries b with b <= x (so boundaries[k-1] <= x <
-// boundaries[k] gives k); a NaN compares false and lands in bucket 0.
+// an upper-bound search: bucket = the index of the first boundary b with
+// x < b, or the number of boundaries if there is none (so boundaries[k-1] <=
+// x < boundaries[k] gives k); a NaN is below no boundary and lands in the
+// last bucket.
 // Returns 0, or -ST_EINVAL for bad offsets.
 int or_bucketize(const float* values, const int64_t* col_off, int32_t ncols, const float* bnd,
                  const int64_t* bnd_off, int64_t* out) {
@@ -314,9 +316,8 @@ int or_bucketize(const float* values, const int64_t* col_off, int32_t ncols, con
   for (int32_t c = 0; c < ncols; ++c) {
     if (col_off[c + 1] < col_off[c] || bnd_off[c + 1] < bnd_off[c]) return -ST_EINVAL;
     for (int64_t i = col_off[c]; i < col_off[c + 1]; ++i) {
-      int64_t k = 0;
-      for (int64_t j = bnd_off[c]; j < bnd_off[c + 1]; ++j)
-        if (bnd[j] <= values[i]) ++k;
+      int64_t k = 0;  // first boundary above the value
+      while (bnd_off[c] + k < bnd_off[c + 1] && !(values[i] < bnd[bnd_off[c] + k])) ++k;
       out[i] = k;
     }
   }

@@ -31,14 +31,16 @@ __device__ inline int column_of(P off, int lo, int hi, int64_t i) {
   return lo;
 }
 
-// Number of b[0, nb) with b <= x (b nondecreasing); 0 for a NaN x.
+// Upper bound: the index of the first of b[0, nb) (nondecreasing) with
+// x < b, or nb -- the number of boundaries b <= x, and nb for a NaN x (which
+// compares below no boundary).
 template <typename P>
 __device__ inline int64_t upper_bound_f(P b, int64_t nb, float x) {
   int64_t lo = 0, hi = nb;
   while (lo < hi) {
     const int64_t mid = (lo + hi) >> 1;
-    if (b[mid] <= x) lo = mid + 1;
-    else hi = mid;
+    if (x < b[mid]) hi = mid;
+    else lo = mid + 1;
   }
   return lo;
 }

@@ -337,8 +337,7 @@ def test_bucketize_matches_searchsorted_right_and_tf_examples():
     for c in range(40):
         v = vals[coff[c]:coff[c + 1]]
         b = bnd[boff[c]:boff[c + 1]]
-        want = np.searchsorted(b, v, side="right")
-        want[np.isnan(v)] = 0
+        want = np.searchsorted(b, v, side="right")   # numpy orders NaN after every number
         assert np.array_equal(out[coff[c]:coff[c + 1]], want)
 
 
