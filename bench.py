@@ -76,6 +76,12 @@ def parse():
                     help="write profiles/traffic_<workload>*.{md,json} from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE "
                          "output directories of a step run and of a --copy-calibration run (no GPU needed)")
     ap.add_argument("--traffic-cmd", default="", help="the profiled command, recorded in the summary")
+    ap.add_argument("--trace-from", metavar="DIR",
+                    help="write profiles/step_kernels_<workload>.md from a rocprofv3 --kernel-trace --stats output "
+                         "directory of a step run: per-kernel time over the timed steps and the --stats table")
+    ap.add_argument("--counters-from", metavar="DIR",
+                    help="write profiles/l2_<workload>.md from a rocprofv3 --pmc TCC_HIT_sum TCC_MISS_sum "
+                         "TCC_ATOMIC_sum output directory (last dispatch of each step kernel)")
     return ap.parse_args()
 
 
@@ -247,6 +253,88 @@ def traffic_from(a):
                "counters_from": f"profiles/traffic_{wl}.md"}
         with open(os.path.join(ROOT, "profiles", f"traffic_{wl}_{kern}.json"), "w") as fh:
             json.dump(rec, fh, indent=1)
+    print("\n".join(lines))
+
+
+def _csv_rows(d: str, suffix: str):
+    import csv
+    import glob
+
+    files = glob.glob(os.path.join(d, "**", f"*{suffix}"), recursive=True)
+    if not files:
+        raise FileNotFoundError(f"no *{suffix} under {d}")
+    with open(files[0]) as fh:
+        return list(csv.DictReader(fh))
+
+
+def _kname(r) -> str:
+    return r["Kernel_Name"].split("(")[0].replace("void ", "").strip()
+
+
+def trace_from(a):
+    """Per-kernel time of the timed steps (their last a.steps launches of each
+    step kernel, from the kernel trace) and rocprofv3's --stats table."""
+    from collections import defaultdict
+
+    from paper_2509_20883_amd import workloads as W
+
+    wl = W.describe(W.workload(a.workload))["workload"]
+    rows = _csv_rows(a.trace_from, "kernel_trace.csv")
+    by = defaultdict(list)
+    for r in rows:
+        by[_kname(r)].append((int(r["Dispatch_Id"]), (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3))
+    step = {k: v for k, v in by.items() if k.startswith("rs::") and "probe" not in k and "rehash" not in k
+            and "map_rows" not in k and "k_occ_init<false>" not in k and "rereserve" not in k}
+    lines = [f"# Kernel time per step: {wl}", "", "Command (MI355X, repository root copied to `<repo>`):", "", "```",
+             a.traffic_cmd or "(command not recorded)", "```", "",
+             f"Converted by `bench.py --workload {a.workload} --steps {a.steps} --trace-from <dir>`.", "",
+             f"## Per step (the last {a.steps} launches of each step kernel: the timed steps)", "",
+             "| kernel | mean us | % of kernel time |", "|---|---|---|"]
+    means = {k: float(np.mean([t for _, t in sorted(v)[-a.steps:]])) for k, v in step.items()}
+    tot = sum(means.values())
+    for k in sorted(means, key=lambda k: -means[k]):
+        lines.append(f"| `{k}` | {means[k]:.1f} | {100 * means[k] / tot:.1f} |")
+    lines += [f"| sum | {tot:.1f} | |", "", "## rocprofv3 `--stats` (all launches of the run, set-up included)", "",
+              "| kernel | calls | avg us | min us | max us | % time |", "|---|---|---|---|---|---|"]
+    for r in _csv_rows(a.trace_from, "kernel_stats.csv")[:16]:
+        lines.append(f"| `{r['Name'].split('(')[0].replace('void ', '')[:70]}` | {r['Calls']} | "
+                     f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
+                     f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.1f} |")
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    with open(os.path.join(ROOT, "profiles", f"step_kernels_{wl}.md"), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def counters_from(a):
+    """L2 hit rate and atomics per step kernel (its last dispatch)."""
+    from collections import defaultdict
+
+    from paper_2509_20883_amd import workloads as W
+
+    wl = W.describe(W.workload(a.workload))["workload"]
+    last, vals = {}, defaultdict(dict)
+    rows = _csv_rows(a.counters_from, "counter_collection.csv")
+    for r in rows:
+        k, d = _kname(r), int(r["Dispatch_Id"])
+        last[k] = max(last.get(k, -1), d)
+    for r in rows:
+        k = _kname(r)
+        if int(r["Dispatch_Id"]) == last[k]:
+            vals[k][r["Counter_Name"]] = float(r["Counter_Value"])
+    lines = [f"# L2 hits and atomics per launch: {wl}", "", "Command (MI355X, repository root copied to `<repo>`):",
+             "", "```", a.traffic_cmd or "(command not recorded)", "```", "",
+             "Last dispatch of each step kernel (the last step); TCC_HIT / TCC_MISS are L2 requests over all "
+             f"channels, TCC_ATOMIC the atomics that reach L2.  Converted by `bench.py --counters-from`.", "",
+             "| kernel | L2 hits (M) | L2 misses (M) | hit rate | atomics (M) |", "|---|---|---|---|---|"]
+    for k, v in sorted(vals.items(), key=lambda kv: -(kv[1].get("TCC_HIT_sum", 0) + kv[1].get("TCC_MISS_sum", 0))):
+        if not k.startswith("rs::") or "probe" in k:
+            continue
+        h, m = v.get("TCC_HIT_sum", 0.0), v.get("TCC_MISS_sum", 0.0)
+        lines.append(f"| `{k}` | {h / 1e6:.1f} | {m / 1e6:.1f} | {h / max(h + m, 1):.2f} | "
+                     f"{v.get('TCC_ATOMIC_sum', 0.0) / 1e6:.2f} |")
+    with open(os.path.join(ROOT, "profiles", f"l2_{wl}.md"), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
 
@@ -611,6 +699,14 @@ def main():
     a = parse()
     if a.traffic_from:
         traffic_from(a)
+        return
+    if a.trace_from:
+        if a.steps is None:
+            a.steps = 100 if a.workload == 4 else 20
+        trace_from(a)
+        return
+    if a.counters_from:
+        counters_from(a)
         return
     if a.copy_calibration:
         copy_calibration()
