@@ -440,10 +440,10 @@ def kernel_bytes(w, kernel, N, G, ks):
     if kernel == "pool":
         out = G * w.pad_len * R + G * w.pad_len if padded else G * w.dim * 4
         alg = 8 * (G + 1) + 4 * N + 8 * U + R * U + out
-        # the kernel reads each id's row id (8 B) and list position (4 B) and
-        # writes the list's gradient-row entry (4 B; 8 B with the mean scale)
+        # the kernel reads each id's row id (8 B) and writes the id's gradient
+        # row (4 B; 8 B with the mean scale), both in id order
         ref = 8 if w.mode == 1 else 4
-        impl = 8 * (G + 1) + 12 * N + R * U + out + ref * N
+        impl = 8 * (G + 1) + 8 * N + R * U + out + ref * N
         return alg, impl
     if kernel == "bwd_short":
         Us, Ns, Nw = ks["U_short"], ks["N_short"], ks["Nw_short"]
@@ -862,7 +862,7 @@ def main():
         scratch.close()
 
     # untimed pass over the warm-up steps with per-kernel events: find the dominant kernel
-    names = ["tile_dedup", "partition", "compact_insert", "occ", "pool", "bwd_short", "bwd_long"]
+    names = ["tile_dedup", "partition", "compact_insert", "occ", "pool", "occ_list", "bwd_short", "bwd_long"]
     if a.unfused:
         names.append("opt")
     prof = {k: [] for k in names}

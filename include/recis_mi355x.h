@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define RS_VERSION 9
+#define RS_VERSION 10
 
 typedef enum {
   RS_OK = 0,
@@ -312,7 +312,10 @@ rs_status lookup_pool_prepared(rs_table* t, rs_ctx* ctx, void* out, uint8_t* mas
  * grad_unique [n, D] fp32: row u (< U) receives
  *   sum over occurrences i of unique u of scale(bag(i)) * grad_out[bag(i)]
  * (scale 1 for sum, 1/len for mean; padded: grad_out[g][t] for the id copied
- * to slot t; ids that were not copied contribute nothing). */
+ * to slot t; ids that were not copied contribute nothing).  Its first launch
+ * lays out the per-key occurrence list from the gradient row of each id that
+ * the ctx's pool wrote, so the pool precedes it; ids outside
+ * [offsets[0], offsets[bags]) contribute nothing. */
 rs_status lookup_pool_bwd(rs_table* t, const rs_ctx* ctx, const void* grad_out, float* grad_unique,
                           rs_stream stream);
 
@@ -423,13 +426,15 @@ typedef enum {
                               (several kernels)                                 */
   RS_K_COMPACT_INSERT = 2, /* unique ids, segments, rows, IDMap inserts         */
   RS_K_INIT_ROWS = 3,      /* same launch as RS_K_OCC (it writes the new rows)  */
-  RS_K_POOL = 4,           /* gather + pool (and the occurrence list)           */
+  RS_K_POOL = 4,           /* gather + pool (and each id's gradient row)        */
   RS_K_BWD_SHORT = 5,      /* per-key gradient sum (+ optimizer), short keys    */
   RS_K_BWD_LONG = 6,       /* hot keys: unit partial sums + finish (two kernels) */
   RS_K_OPT = 7,            /* optimizer from grad_unique (two-call path)        */
   RS_K_OCC = 8,            /* per-occurrence rows, list positions, inverse; the
                               same launch writes the rows of inserted keys      */
-  RS_K_COUNT = 9
+  RS_K_OCC_LIST = 9,       /* the backward's first launch: the occurrence list
+                              (each position's gradient row)                    */
+  RS_K_COUNT = 10
 } rs_kernel_id;
 rs_status rs_set_kernel_events(rs_table* t, int32_t kernel, void* start_event, void* stop_event);
 

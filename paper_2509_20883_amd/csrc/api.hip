@@ -52,7 +52,7 @@ bool padded_mode(int32_t mode) { return mode == RS_POOL_NONE || mode == RS_POOL_
 // Workspace layout of one forward: every array sized by the upper bound n.
 struct Layout {
   size_t occ_word, trec, nrec, srec, pcnt, poff, ptmp, kinfo, inverse, occ_row, occ_pos, unique, useg, rows,
-      new_list, occ_ref, long_u, long_start, units, bsum, csum, scal, gpart, total;
+      new_list, id_ref, occ_ref, long_u, long_start, units, bsum, csum, scal, gpart, total;
   int64_t ntiles;
   FrontGeom g;
 };
@@ -87,6 +87,7 @@ Layout make_layout(int64_t n, int dim) {
   L.useg = take(sizeof(Seg) * n1);
   L.rows = take(8 * n1);
   L.new_list = take(4 * n1);
+  L.id_ref = take(8 * n1);   // int32 per id, or {int32, float} for mean pooling
   L.occ_ref = take(8 * n1);  // int32 per position, or {int32, float} for mean pooling
   L.long_u = take(4 * nlong);
   L.long_start = take(4 * nlong);
@@ -119,6 +120,8 @@ Work make_work(void* base, const Layout& L) {
   w.useg = reinterpret_cast<Seg*>(b + L.useg);
   w.rows = reinterpret_cast<int64_t*>(b + L.rows);
   w.new_list = reinterpret_cast<int32_t*>(b + L.new_list);
+  w.id_ref = reinterpret_cast<int32_t*>(b + L.id_ref);
+  w.id_rs = reinterpret_cast<int2*>(b + L.id_ref);
   w.occ_ref = reinterpret_cast<int32_t*>(b + L.occ_ref);
   w.occ_rs = reinterpret_cast<int2*>(b + L.occ_ref);
   w.long_u = reinterpret_cast<int32_t*>(b + L.long_u);
@@ -1019,7 +1022,7 @@ rs_status lookup_pool_bwd(rs_table* t, const rs_ctx* ctx, const void* grad_out, 
   if (ctx->n > 0 && (!grad_out || !grad_unique)) return fail(RS_EINVAL, "null gradient");
   const Work w = ctx_work(ctx);
   RS_HIP(launch_bwd(t->dev(), w, grad_rows(ctx), ctx->n, ctx->mode, grad_out, grad_unique, nullptr,
-                    t->ev(RS_K_BWD_SHORT), t->ev(RS_K_BWD_LONG), static_cast<hipStream_t>(stream)));
+                    t->ev(RS_K_OCC_LIST), t->ev(RS_K_BWD_SHORT), t->ev(RS_K_BWD_LONG), static_cast<hipStream_t>(stream)));
   return RS_OK;
 }
 
@@ -1043,7 +1046,7 @@ rs_status lookup_pool_bwd_opt(rs_table* t, const rs_ctx* ctx, const void* grad_o
   if (ctx->n > 0 && !grad_out) return fail(RS_EINVAL, "null gradient");
   const OptArgs o = make_opt(t, p);
   const Work w = ctx_work(ctx);
-  RS_HIP(launch_bwd(t->dev(), w, grad_rows(ctx), ctx->n, ctx->mode, grad_out, nullptr, &o, t->ev(RS_K_BWD_SHORT),
+  RS_HIP(launch_bwd(t->dev(), w, grad_rows(ctx), ctx->n, ctx->mode, grad_out, nullptr, &o, t->ev(RS_K_OCC_LIST), t->ev(RS_K_BWD_SHORT),
                     t->ev(RS_K_BWD_LONG), static_cast<hipStream_t>(stream)));
   return RS_OK;
 }

@@ -409,6 +409,53 @@ __global__ __launch_bounds__(kBlock) void k_bwd_long_finish(TableDev t, Work w, 
   }
 }
 
+// The occurrence list the backward reads: position occ_pos[i] of id i
+// receives the gradient row the pool gave that id (id_ref; with the bag's
+// mean scale for mean pooling).  Ids outside the pooled range [lo, hi) get
+// no gradient row (-1); ids of a rejected key have no position.  Four
+// consecutive ids per thread, read with 16-byte loads.
+template <bool MEAN>
+__global__ __launch_bounds__(kBlock) void k_occ_list(Work w, int64_t n) {
+  const int64_t i0 = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * 4;
+  if (i0 >= n) return;
+  const int64_t lo = min(max(w.scal[kCIdLo], int64_t(0)), n);
+  const int64_t hi = min(max(w.scal[kCIdHi], lo), n);
+  int pos[4], ref[4], sc[4] = {0, 0, 0, 0};
+  if (i0 + 4 <= n) {
+    const int4 p = *reinterpret_cast<const int4*>(w.occ_pos + i0);
+    pos[0] = p.x; pos[1] = p.y; pos[2] = p.z; pos[3] = p.w;
+    if (MEAN) {
+      const int4 a = *reinterpret_cast<const int4*>(w.id_rs + i0);
+      const int4 b = *reinterpret_cast<const int4*>(w.id_rs + i0 + 2);
+      ref[0] = a.x; sc[0] = a.y; ref[1] = a.z; sc[1] = a.w;
+      ref[2] = b.x; sc[2] = b.y; ref[3] = b.z; sc[3] = b.w;
+    } else {
+      const int4 r = *reinterpret_cast<const int4*>(w.id_ref + i0);
+      ref[0] = r.x; ref[1] = r.y; ref[2] = r.z; ref[3] = r.w;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const bool v = i0 + k < n;
+      pos[k] = v ? w.occ_pos[i0 + k] : -1;
+      if (MEAN) {
+        const int2 a = v ? w.id_rs[i0 + k] : make_int2(-1, 0);
+        ref[k] = a.x;
+        sc[k] = a.y;
+      } else {
+        ref[k] = v ? w.id_ref[i0 + k] : -1;
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (pos[k] < 0) continue;
+    const bool in = i0 + k >= lo && i0 + k < hi;
+    if (MEAN) w.occ_rs[pos[k]] = in ? make_int2(ref[k], sc[k]) : make_int2(-1, 0);
+    else w.occ_ref[pos[k]] = in ? ref[k] : -1;
+  }
+}
+
 template <typename WT, typename GT, int LANES, int MODE, bool FUSED>
 static hipError_t bwd_launch(const TableDev& t, const Work& w, uint32_t nref, int64_t n, const void* grad,
                              float* gu, const OptArgs& o, hipEvent_t* ev_s, hipEvent_t* ev_l, hipStream_t s) {
@@ -460,9 +507,15 @@ static hipError_t bwd_mode(const TableDev& t, const Work& w, uint32_t nref, int6
 }
 
 hipError_t launch_bwd(const TableDev& t, const Work& w, int64_t nref, int64_t n, int mode, const void* grad,
-                      float* grad_unique, const OptArgs* opt, hipEvent_t* ev_short, hipEvent_t* ev_long,
-                      hipStream_t s) {
+                      float* grad_unique, const OptArgs* opt, hipEvent_t* ev_list, hipEvent_t* ev_short,
+                      hipEvent_t* ev_long, hipStream_t s) {
   if (n <= 0) return hipSuccess;
+  {
+    hipEvent_t e0 = ev_list ? ev_list[0] : nullptr, e1 = ev_list ? ev_list[1] : nullptr;
+    const dim3 grid(static_cast<unsigned>(grid_for(n, kBlock * 4, int64_t(1) << 31)));
+    if (mode == 1) hipExtLaunchKernelGGL((k_occ_list<true>), grid, dim3(kBlock), 0, s, e0, e1, 0, w, n);
+    else hipExtLaunchKernelGGL((k_occ_list<false>), grid, dim3(kBlock), 0, s, e0, e1, 0, w, n);
+  }
   const OptArgs o = opt ? *opt : OptArgs{0, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 1.f, 1.f, 0.f, 0.f};
   if (opt)
     return t.row_dtype ? bwd_mode<uint16_t, true>(t, w, static_cast<uint32_t>(nref), n, mode, grad, grad_unique, o, ev_short, ev_long, s)

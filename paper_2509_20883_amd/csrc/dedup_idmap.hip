@@ -625,12 +625,23 @@ __device__ inline void first_records(const Work& w, int64_t rt, int (&f)[4]) {
     f[k] = r0 + k < nr && (static_cast<uint32_t>(y[k]) & kRecFirst) ? x[k] : -1;
 }
 
+// Record tile rt lies wholly past its dedup block's records (a block's record
+// slots are sized for its ids, and distinct keys are fewer).
+__device__ inline bool empty_record_tile(const Work& w, int64_t rt) {
+  const int64_t per = w.g.rcap / kRankTile;
+  return (rt % per) * kRankTile >= w.nrec[rt / per];
+}
+
 // Per record tile: sums over its first records (keys, their counts, keys not
 // found, hot keys, hot-key units).  Record tiles in block-major order list
 // the keys in the order of their first positions.
 template <int NT>
 __global__ __launch_bounds__(NT) void k_first_sums(Work w) {
   __shared__ int sh[NT / kWave + 1][5];
+  if (empty_record_tile(w, blockIdx.x)) {  // block-uniform
+    if (threadIdx.x < 5) w.bsum[threadIdx.x * w.ntiles + blockIdx.x] = 0;
+    return;
+  }
   int f[4];
   first_records(w, blockIdx.x, f);
   KeyInfo ki[4];
@@ -847,6 +858,8 @@ template <int NT>
 __global__ __launch_bounds__(NT) void k_compact(TableDev t, Work w) {
   __shared__ int sh[NT / kWave + 1][5];
   const int b = blockIdx.x;
+  if (blockIdx.x == 0 && threadIdx.x == 0 && w.scal[kCTrunc]) atomicOr(reinterpret_cast<int*>(&t.scal[kTErr]), kErrFull);
+  if (empty_record_tile(w, b)) return;  // block-uniform: no keys, nothing to write
   int pre[5];  // the record tile's exclusive prefixes (keys, count, new, hot, units)
   const int64_t nch = (static_cast<int64_t>(gridDim.x) + kScanChunk - 1) / kScanChunk;
 #pragma unroll
@@ -881,7 +894,6 @@ __global__ __launch_bounds__(NT) void k_compact(TableDev t, Work w) {
   const int64_t inserted = w.scal[kCNew];
   const int64_t live0 = w.scal[kCBaseLive];
   const int64_t ftop = w.scal[kCFreeTop], ftake = w.scal[kCFreeTake];
-  if (blockIdx.x == 0 && threadIdx.x == 0 && w.scal[kCTrunc]) atomicOr(reinterpret_cast<int*>(&t.scal[kTErr]), kErrFull);
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     if (f[k] < 0) continue;

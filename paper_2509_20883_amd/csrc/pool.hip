@@ -4,10 +4,10 @@
 // is read at that offset and the rows of a bag are reduced (sum, mean) or
 // copied into a padded sequence ("Forward Pass", "Reduction Operations",
 // "Gather").  The lookup happened in the dedup passes, which also gave every
-// occurrence its row (occ_row) and its position in the occurrence list
-// (occ_pos); these kernels read each occurrence's row with 16-byte vector
-// loads, one lane group of D*sizeof(row)/16 lanes per row, and write the
-// gradient row each position of the occurrence list will read (occ_ref).
+// occurrence its row (occ_row); these kernels read each occurrence's row
+// with 16-byte vector loads, one lane group of D*sizeof(row)/16 lanes per
+// row, and write the gradient row of each id (id_ref, in id order), from
+// which the backward builds its occurrence list.
 //
 // A lane group handles one bag per lane and requests 16 rows of them at a
 // time, for single-id and long bags alike.
@@ -19,6 +19,14 @@ namespace rs {
 
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// The ids the bags cover, [offsets[0], offsets[bags]) clamped to [0, n]: the
+// backward gives ids outside it no gradient row.
+__device__ inline void record_pooled_range(const Work& w, const int64_t* offsets, int64_t n, int64_t bags) {
+  const int64_t lo = min(max(offsets[0], int64_t(0)), n);
+  w.scal[kCIdLo] = lo;
+  w.scal[kCIdHi] = min(max(offsets[bags], lo), n);
+}
 
 // acc += the E row elements held raw in v (16 bytes of the row)
 template <typename WT, int E>
@@ -60,7 +68,7 @@ __device__ inline int64_t group_incl_scan(int64_t v, int lane) {
 // in order into one running accumulator; a cursor over the bags' cumulative
 // lengths flushes a bag (one non-temporal row store) when the sequence passes
 // its end, so empty bags are flushed as zeros and no per-bag accumulators
-// are held.  The walk also writes each id's entry of the occurrence list.
+// are held.  The walk also writes each id's gradient row (its bag).
 // For well-formed offsets (each bag starts where the previous one ends) the
 // sequence is positions offsets[g0] ... ; malformed offsets give wrong
 // sums, never an access outside [0, n).
@@ -73,6 +81,7 @@ __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64
   constexpr int J = (C + LANES - 1) / LANES;  // chunk positions per lane
   const int lane = threadIdx.x % LANES;
   const int grp = threadIdx.x / LANES;
+  if (blockIdx.x == 0 && threadIdx.x == 0) record_pooled_range(w, offsets, n, bags);
   const int64_t g0 = (static_cast<int64_t>(blockIdx.x) * GPB + grp) * LANES;
   if (g0 >= bags) return;
   const int nb = static_cast<int>(min(static_cast<int64_t>(LANES), bags - g0));
@@ -87,7 +96,6 @@ __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64
   const int total = static_cast<int>(min(__shfl(cum, LANES - 1, LANES), static_cast<int64_t>(n32)));
   const int p0 = __shfl(bq, 0, LANES);                     // the sequence starts at the first bag's start
   int64_t rr[J];
-  int pp[J];
   auto load_idx = [&](int t0) {
 #pragma unroll
     for (int j = 0; j < J; ++j) {
@@ -95,11 +103,7 @@ __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64
       const bool valid = c < C && t0 + c < total;
       const int p = valid ? min(p0 + t0 + c, n32 - 1) : 0;  // total > 0: position 0 exists
       rr[j] = w.occ_row[p];
-      pp[j] = w.occ_pos[p];
-      if (!valid) {
-        rr[j] = -1;
-        pp[j] = -1;
-      }
+      if (!valid) rr[j] = -1;
     }
   };
   float acc[E];
@@ -137,10 +141,7 @@ __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64
       x[c] = make_uint4(0u, 0u, 0u, 0u);
       if (r >= 0) x[c] = *reinterpret_cast<const uint4*>(t.store.row(r) + lane * 16);
     }
-    int cp[J];  // this chunk's list positions (the next chunk's indices replace rr / pp)
-#pragma unroll
-    for (int j = 0; j < J; ++j) cp[j] = pp[j];
-    if (t0 + C < total) load_idx(t0 + C);
+    if (t0 + C < total) load_idx(t0 + C);  // the next chunk's row ids replace rr
     int myq[J], mylen[J];  // bag (and its length) of this lane's positions in the chunk
 #pragma unroll
     for (int c = 0; c < C; ++c) {
@@ -153,17 +154,19 @@ __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64
       }
       add_raw<WT, E>(acc, x[c]);
     }
-    // each id's place in its key's segment of the occurrence list receives
-    // the gradient row it will read in the backward (and, for mean pooling,
-    // the scale 1 / bag length)
+    // each id of the chunk: the gradient row it reads in the backward (and,
+    // for mean pooling, the scale 1 / bag length); consecutive lanes write
+    // consecutive ids
 #pragma unroll
     for (int j = 0; j < J; ++j) {
-      if (cp[j] < 0) continue;  // also every slot past the sequence's end
+      const int c = lane + j * LANES;
+      if (c >= C || t0 + c >= total || p0 + t0 + c >= n32) continue;
+      const int p = p0 + t0 + c;
       if (MODE == 1)
-        w.occ_rs[cp[j]] = make_int2(static_cast<int>(g0 + myq[j]),
-                                    __float_as_int(1.0f / static_cast<float>(max(mylen[j], 1))));
+        w.id_rs[p] = make_int2(static_cast<int>(g0 + myq[j]),
+                               __float_as_int(1.0f / static_cast<float>(max(mylen[j], 1))));
       else
-        w.occ_ref[cp[j]] = static_cast<int>(g0 + myq[j]);
+        w.id_ref[p] = static_cast<int>(g0 + myq[j]);
     }
   }
   while (q < nb) flush();  // the last bag and any empty bags after it
@@ -182,6 +185,7 @@ __global__ __launch_bounds__(kBlock) void k_pool_none(TableDev t, Work w, const 
   constexpr int K = TCH / GPB;               // positions per lane group
   const int lane = threadIdx.x % LANES;
   const int grp = threadIdx.x / LANES;
+  if (blockIdx.x == 0 && threadIdx.x == 0) record_pooled_range(w, offsets, n, bags);
   const int64_t nch = (L + TCH - 1) / TCH;
   for (int64_t blk = blockIdx.x; blk < bags * nch; blk += gridDim.x) {
     const int64_t g = blk / nch, c = blk % nch;
@@ -190,13 +194,11 @@ __global__ __launch_bounds__(kBlock) void k_pool_none(TableDev t, Work w, const 
     // the copied window: ids [skip, skip + min(len, L)) of the bag
     const int64_t skip = tail && len > L ? len - L : 0;
     int64_t tp[K], r[K];
-    int pos[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) {
       tp[k] = c * TCH + grp + k * GPB;
       const bool act = tp[k] < L && tp[k] < len;
       r[k] = act ? w.occ_row[b + skip + tp[k]] : -1;
-      pos[k] = act ? w.occ_pos[b + skip + tp[k]] : -1;
     }
     uint4 v[K];
 #pragma unroll
@@ -209,17 +211,14 @@ __global__ __launch_bounds__(kBlock) void k_pool_none(TableDev t, Work w, const 
       *reinterpret_cast<uint4*>(out + (g * L + tp[k]) * D + lane * E) = v[k];
       if (lane == 0) {
         mask[g * L + tp[k]] = tp[k] < len ? 1 : 0;
-        if (pos[k] >= 0) w.occ_ref[pos[k]] = static_cast<int>(g * L + tp[k]);
+        if (tp[k] < len) w.id_ref[b + skip + tp[k]] = static_cast<int>(g * L + tp[k]);
       }
     }
     if (c == 0 && lane == 0) {
       // ids outside the window (past L, or before skip): in the occurrence
       // list (the key is touched) but without a gradient row
       const int64_t x0 = tail ? 0 : L, x1 = tail ? skip : len;
-      for (int64_t tpos = x0 + grp; tpos < x1; tpos += GPB) {
-        const int pp = w.occ_pos[b + tpos];
-        if (pp >= 0) w.occ_ref[pp] = -1;
-      }
+      for (int64_t tpos = x0 + grp; tpos < x1; tpos += GPB) w.id_ref[b + tpos] = -1;
     }
   }
 }

@@ -115,7 +115,9 @@ enum : int {
   kCBaseKeys = 9,  // live keys before the insert
   kCFreeTop = 10,  // free-row stack size before the insert
   kCFreeTake = 11, // inserted keys that take a free row (the first ones)
-  kCScalars = 12
+  kCIdLo = 12,     // ids [lo, hi) lie in the pooled bags: offsets[0], offsets[bags]
+  kCIdHi = 13,     //   clamped to [0, n] (written by the pool)
+  kCScalars = 14
 };
 
 // Ids partition: at most kMaxShards owner shards.  Its device scalars: the
@@ -250,6 +252,8 @@ struct Work {
   Seg* useg;            // [n]
   int64_t* rows;        // [n]
   int32_t* new_list;    // [n] unique id of the k-th inserted key
+  int32_t* id_ref;      // [n] gradient row of each id (written by the pool; -1: none)
+  int2* id_rs;          // [n] mean pooling, same memory: {gradient row, bits of 1 / bag length}
   int32_t* occ_ref;     // [n] gradient row of each position of the occurrence list
   int2* occ_rs;         // [n] mean pooling, same memory: {gradient row, bits of 1 / bag length}
   int32_t* long_u;      // [n/kLong + 1] unique id of each hot key
@@ -326,8 +330,8 @@ hipError_t launch_pool(const TableDev& t, const Work& w, const int64_t* offsets,
 // entry outside [0, nref) -- left stale by offsets that do not cover every
 // position -- contributes nothing instead of reading out of bounds.
 hipError_t launch_bwd(const TableDev& t, const Work& w, int64_t nref, int64_t n, int mode,
-                      const void* grad, float* grad_unique, const OptArgs* opt, hipEvent_t* ev_short,
-                      hipEvent_t* ev_long, hipStream_t s);
+                      const void* grad, float* grad_unique, const OptArgs* opt, hipEvent_t* ev_list,
+                      hipEvent_t* ev_short, hipEvent_t* ev_long, hipStream_t s);
 hipError_t launch_opt(const TableDev& t, const Work& w, int64_t n, const float* grad_unique, const OptArgs& opt,
                       hipEvent_t* ev, hipStream_t s);
 // Feature transforms fused over ncols columns of one flat array of n

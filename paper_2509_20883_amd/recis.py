@@ -29,7 +29,7 @@ ADAGRAD, ADAM, ADAMW, ADAM_TF, ADAGRAD_RW, ADAM_RW = 0, 1, 2, 3, 4, 5
 # kernel ids of rs_set_kernel_events ("occ" and "init_rows" bracket the same
 # launch; "bwd_long" brackets the hot-key unit sums and their finish)
 KERNELS = {"tile_dedup": 0, "partition": 1, "compact_insert": 2, "init_rows": 3, "pool": 4,
-           "bwd_short": 5, "bwd_long": 6, "opt": 7, "occ": 8}
+           "bwd_short": 5, "bwd_long": 6, "opt": 7, "occ": 8, "occ_list": 9}
 
 
 class RecisError(RuntimeError):

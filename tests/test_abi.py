@@ -24,7 +24,7 @@ def test_library_exports_every_declared_symbol():
     lib = ctypes.CDLL(R.LIB_PATH)
     missing = [n for n in _declared() if not hasattr(lib, n)]
     assert not missing, missing
-    assert R.lib().rs_version() == 9
+    assert R.lib().rs_version() == 10
 
 
 def test_binding_struct_layouts_match_header(tmp_path):

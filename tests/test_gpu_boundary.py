@@ -3,8 +3,8 @@
   * validate = 1 rejects malformed CSR offsets with RS_EINVAL (host check,
     before any kernel is enqueued);
   * offsets that do not cover every id (validate = 0) give in-bounds work:
-    the covered bags pool correctly and the backward ignores the stale
-    occurrence-list entries of the uncovered ids;
+    the covered bags pool correctly and the backward gives the uncovered ids
+    no gradient row;
   * an allocator that returns NULL gives RS_ENOMEM, at creation and when the
     table has to grow, and the table stays consistent afterwards;
   * a table whose IDMap, Blocks and workspace all come from PyTorch's caching
@@ -48,13 +48,15 @@ def test_validate_rejects_malformed_offsets():
     gt.close()
 
 
-def test_offsets_not_covering_every_id_stay_in_bounds():
+@pytest.mark.parametrize("k", [0, 2])
+def test_offsets_not_covering_every_id_stay_in_bounds(k):
     """validate = 0 and offsets that leave ids outside every bag: the kernels
     stay in bounds (positions clamped to [0, n), occurrence-list entries
     outside the gradient rows skipped); covered bags pool exactly as
-    defined.  The workspace starts as random bytes."""
-    _log("uncovered ids without validation")
-    w = W.workload(0)
+    defined, and the backward sums over the covered ids only (the uncovered
+    ones contribute nothing).  The workspace starts as random bytes."""
+    w = W.workload(k, mini=(k != 0))
+    _log("uncovered ids without validation", w.name)
     b = W.make_batch(w, 0)
     off = b.offsets.copy()
     off[0] = off[1]      # the first bag's ids are in no bag
@@ -68,13 +70,18 @@ def test_offsets_not_covering_every_id_stay_in_bounds():
     ctx.ws.copy_(torch.randint(0, 256, ctx.ws.shape, dtype=torch.uint8, device="cuda", generator=g))
     out, _, ctx = gt.forward(P.to_dev(b.values), P.to_dev(off), w.mode, ctx=ctx)
     grad = W.make_grad(w, b, 0)
-    gt.backward_optimizer(ctx, P.to_dev(grad), w.lr, w.eps)
+    gu = gt.backward(ctx, P.to_dev(grad))
+    gt.optimizer_step(ctx, gu, w.lr, w.eps)
     torch.cuda.synchronize()
     gt.check()
     U = int(ctx.scalars()[0].item())
     st, u_ref, inv_ref = O.dedup(b.values)
     assert st == O.OK and U == u_ref.size
     assert np.array_equal(ctx.inverse().cpu().numpy(), inv_ref)
+    # the backward over the bags as given: ids outside them contribute nothing
+    gu_ref = O.backward(off, inv_ref, U, w.dim, w.mode, 0, grad)
+    gu_abs = O.backward(off, inv_ref, U, w.dim, w.mode, 0, np.abs(grad))
+    P.assert_sum_close(gu.cpu().numpy()[:U], gu_ref, gu_abs, what="gradient of the covered ids")
     # covered bags: the sum of the initial rows of their ids
     ot = P.oracle_table(w)
     ot.find_or_insert(u_ref)
@@ -87,6 +94,9 @@ def test_offsets_not_covering_every_id_stay_in_bounds():
     np.add.at(ref, bag, rows0[inv_ref[pos]].astype(np.float64))
     scale = np.zeros((b.bags, w.dim))
     np.add.at(scale, bag, np.abs(rows0[inv_ref[pos]].astype(np.float64)))
+    if w.mode == R.MEAN:
+        ref /= np.maximum(lens, 1)[:, None]
+        scale /= np.maximum(lens, 1)[:, None]
     P.assert_sum_close(o, ref, scale, what="covered bags")
     gt.close()
 

@@ -148,11 +148,11 @@ def test_key_stats_and_kernel_bytes_by_hand():
     # 2 unit descriptors, 40 gradient rows, and writes and reads 2 partial rows
     assert B.kernel_bytes(w, "bwd_long", N, G, ks) == (64 * 4 + 4 * 40 + 2 * (R + S),
                                                        16 * 2 + 4 * 40 + 64 * 40 + 2 * 4 * 16 * 2 + 2 * (R + S))
-    # pool: offsets, inverse, row ids, unique rows, output; the implementation reads a row id and
-    # a list position per id and writes one list entry per id
+    # pool: offsets, inverse, row ids, unique rows, output; the implementation reads a row id per
+    # id and writes each id's gradient row
     out = G * 16 * 4
     assert B.kernel_bytes(w, "pool", N, G, ks) == (8 * (G + 1) + 4 * N + 8 * U + R * U + out,
-                                                   8 * (G + 1) + 12 * N + R * U + out + 4 * N)
+                                                   8 * (G + 1) + 8 * N + R * U + out + 4 * N)
     w.opt = 5                                                    # row-wise Adam: m per element + v per row
     assert B.row_bytes(w) == (64, 4 * 17)
 
