@@ -412,17 +412,34 @@ __global__ __launch_bounds__(kBlock) void k_bwd_long_finish(TableDev t, Work w, 
 // The occurrence list the backward reads: position occ_pos[i] of id i
 // receives the gradient row the pool gave that id (id_ref; with the bag's
 // mean scale for mean pooling).  Ids outside the pooled range [lo, hi) get
-// no gradient row (-1); ids of a rejected key have no position.  Four
-// consecutive ids per thread, read with 16-byte loads.
+// no gradient row (-1); ids of a rejected key have no position.
+//
+// One block per dedup tile (kOccListNT threads, 4 ids each).  A record's ids
+// in the tile hold the consecutive positions [base, base + count) of its
+// key's segment, one per rank, so the block counting-sorts its ids by record
+// in LDS (the tile's records are a contiguous range of its dedup block's
+// list) and stores slot after slot: consecutive lanes write consecutive
+// positions along each record's run, instead of one scattered 4-byte store
+// per id.
+constexpr int kOccListNT = kDedupTile / 4;
+
 template <bool MEAN>
-__global__ __launch_bounds__(kBlock) void k_occ_list(Work w, int64_t n) {
-  const int64_t i0 = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) * 4;
-  if (i0 >= n) return;
+__global__ __launch_bounds__(kOccListNT) void k_occ_list(Work w, int64_t n) {
+  constexpr int T = kDedupTile;
+  __shared__ int cnt[T];  // per record of the tile: its ids, then its first slot
+  __shared__ int spos[T], sref[T];
+  __shared__ int ssc[MEAN ? T : 1];
+  __shared__ int wsh[kOccListNT / kWave + 1];
+  __shared__ int rlo_sh;
+  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * T + threadIdx.x * 4;
   const int64_t lo = min(max(w.scal[kCIdLo], int64_t(0)), n);
   const int64_t hi = min(max(w.scal[kCIdHi], lo), n);
+  uint32_t o[4];
   int pos[4], ref[4], sc[4] = {0, 0, 0, 0};
   if (i0 + 4 <= n) {
+    const int4 ow = *reinterpret_cast<const int4*>(w.occ_word + i0);
     const int4 p = *reinterpret_cast<const int4*>(w.occ_pos + i0);
+    o[0] = ow.x; o[1] = ow.y; o[2] = ow.z; o[3] = ow.w;
     pos[0] = p.x; pos[1] = p.y; pos[2] = p.z; pos[3] = p.w;
     if (MEAN) {
       const int4 a = *reinterpret_cast<const int4*>(w.id_rs + i0);
@@ -437,6 +454,7 @@ __global__ __launch_bounds__(kBlock) void k_occ_list(Work w, int64_t n) {
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const bool v = i0 + k < n;
+      o[k] = v ? w.occ_word[i0 + k] : kOccRejected;
       pos[k] = v ? w.occ_pos[i0 + k] : -1;
       if (MEAN) {
         const int2 a = v ? w.id_rs[i0 + k] : make_int2(-1, 0);
@@ -449,10 +467,70 @@ __global__ __launch_bounds__(kBlock) void k_occ_list(Work w, int64_t n) {
   }
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
+    if (i0 + k < lo || i0 + k >= hi) {
+      ref[k] = -1;
+      sc[k] = 0;
+    }
+    if (pos[k] < 0) o[k] = kOccRejected;  // no list entry
+  }
+  // the tile's first record
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    cnt[threadIdx.x * 4 + k] = 0;
+    spos[threadIdx.x * 4 + k] = -1;  // a slot no id fills is skipped
+  }
+  if (threadIdx.x == 0) rlo_sh = 0x7FFFFFFF;
+  __syncthreads();
+  int m = 0x7FFFFFFF;
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    if (o[k] != kOccRejected) m = min(m, static_cast<int>(o[k] >> 12));
+  if (m != 0x7FFFFFFF) atomicMin(&rlo_sh, m);
+  __syncthreads();
+  const int rlo = rlo_sh;
+  // ids per record, then each record's first slot (exclusive scan)
+  int d[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    d[k] = o[k] == kOccRejected ? -1 : static_cast<int>(o[k] >> 12) - rlo;
+    if (d[k] >= T) d[k] = -1;  // outside the tile's records: cannot happen, stored directly below
+    if (d[k] >= 0) atomicAdd(&cnt[d[k]], 1);
+  }
+  __syncthreads();
+  int c4[4], sum = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    c4[k] = cnt[threadIdx.x * 4 + k];
+    sum += c4[k];
+  }
+  int total;
+  int ex = block_excl_scan<kOccListNT>(sum, wsh, total);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    cnt[threadIdx.x * 4 + k] = ex;
+    ex += c4[k];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
     if (pos[k] < 0) continue;
-    const bool in = i0 + k >= lo && i0 + k < hi;
-    if (MEAN) w.occ_rs[pos[k]] = in ? make_int2(ref[k], sc[k]) : make_int2(-1, 0);
-    else w.occ_ref[pos[k]] = in ? ref[k] : -1;
+    const int slot = d[k] >= 0 ? cnt[d[k]] + static_cast<int>(o[k] & 0xFFFu) : T;
+    if (slot < T) {
+      spos[slot] = pos[k];
+      sref[slot] = ref[k];
+      if (MEAN) ssc[slot] = sc[k];
+    } else if (MEAN) {
+      w.occ_rs[pos[k]] = make_int2(ref[k], sc[k]);
+    } else {
+      w.occ_ref[pos[k]] = ref[k];
+    }
+  }
+  __syncthreads();
+  for (int s = threadIdx.x; s < min(total, T); s += kOccListNT) {
+    const int p = spos[s];
+    if (p < 0) continue;
+    if (MEAN) w.occ_rs[p] = make_int2(sref[s], ssc[s]);
+    else w.occ_ref[p] = sref[s];
   }
 }
 
@@ -512,9 +590,9 @@ hipError_t launch_bwd(const TableDev& t, const Work& w, int64_t nref, int64_t n,
   if (n <= 0) return hipSuccess;
   {
     hipEvent_t e0 = ev_list ? ev_list[0] : nullptr, e1 = ev_list ? ev_list[1] : nullptr;
-    const dim3 grid(static_cast<unsigned>(grid_for(n, kBlock * 4, int64_t(1) << 31)));
-    if (mode == 1) hipExtLaunchKernelGGL((k_occ_list<true>), grid, dim3(kBlock), 0, s, e0, e1, 0, w, n);
-    else hipExtLaunchKernelGGL((k_occ_list<false>), grid, dim3(kBlock), 0, s, e0, e1, 0, w, n);
+    const dim3 grid(static_cast<unsigned>((n + kDedupTile - 1) / kDedupTile));
+    if (mode == 1) hipExtLaunchKernelGGL((k_occ_list<true>), grid, dim3(kOccListNT), 0, s, e0, e1, 0, w, n);
+    else hipExtLaunchKernelGGL((k_occ_list<false>), grid, dim3(kOccListNT), 0, s, e0, e1, 0, w, n);
   }
   const OptArgs o = opt ? *opt : OptArgs{0, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 1.f, 1.f, 0.f, 0.f};
   if (opt)
