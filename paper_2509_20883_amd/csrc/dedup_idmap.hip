@@ -348,8 +348,12 @@ __device__ inline int64_t resolve_probe(const TableDev& t, unsigned long long e,
 // The partition's records are read from every dedup block's
 // partition-ordered copy (segment b: cnt[b] records at off[b]).  A key's
 // index is the position of its first record (the one holding its first
-// position), so the keys of a feature get indices in the feature's own
-// dedup blocks and the passes that follow read their key info close by.
+// position): for a lookup its tile-order position, so the key info of a
+// tile's first records lies together, in the order in which the
+// first-occurrence sums and the compaction read and write it, and the info
+// of a key seen once lies beside its ids' records; for the ids partition
+// (no key info) its position in the partition-ordered copy, whose entry
+// there holds the key.
 // A partition of at most kPartSlots records is done in one pass with each
 // thread's records in registers (its distinct keys always fit the table);
 // a larger one in sweeps of at most kPartSweep records by a hash of the key,
@@ -478,6 +482,11 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
     return d;
   };
 
+  // the key index a record would give its key (see above)
+  auto rec_index = [&](int pos, const TileRec& x) {
+    return w.kinfo ? static_cast<unsigned int>((pos / g.rcap) * g.rcap + (x.meta >> 12))
+                   : static_cast<unsigned int>(pos);
+  };
   bool fresh = true;  // the LDS table is clear
   if (nr <= NT * K) {
     // one pass: the thread's records tid, tid + NT, ... stay in registers
@@ -503,7 +512,7 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
         pos[k] = -1;
         continue;
       }
-      atomicMin(&cfp[sl[k]], (static_cast<unsigned long long>(x[k].tmin) << 32) | static_cast<unsigned int>(pos[k]));
+      atomicMin(&cfp[sl[k]], (static_cast<unsigned long long>(x[k].tmin) << 32) | rec_index(pos[k], x[k]));
       rb[k] = atomicAdd(&ccnt[sl[k]], (x[k].meta & 0xFFFu) + 1u);
     }
     __syncthreads();
@@ -517,8 +526,8 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
         if (pos[k] < 0) continue;
         const int64_t src = (static_cast<int64_t>(pos[k]) / g.rcap) * g.rcap + (x[k].meta >> 12);
         const unsigned int kidx = static_cast<unsigned int>(cfp[sl[k]]);
-        // the key's first record is the one whose position is its key index
-        const unsigned int fl = kidx == static_cast<unsigned int>(pos[k]) ? kRecFirst : 0u;
+        // the key's first record is the one whose index is its key index
+        const unsigned int fl = kidx == rec_index(pos[k], x[k]) ? kRecFirst : 0u;
         w.recres[src] = make_int2(static_cast<int>(kidx), static_cast<int>(rb[k] | fl));
       }
       return;
@@ -551,7 +560,7 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
         ovf = 1;
         continue;
       }
-      atomicMin(&cfp[sl], (static_cast<unsigned long long>(x.tmin) << 32) | static_cast<unsigned int>(pos));
+      atomicMin(&cfp[sl], (static_cast<unsigned long long>(x.tmin) << 32) | rec_index(pos, x));
       const unsigned int rb = atomicAdd(&ccnt[sl], (x.meta & 0xFFFu) + 1u);
       w.ptmp[pos] = make_int2(static_cast<int>(((x.meta >> 12) << 12) | static_cast<unsigned int>(sl)),
                               static_cast<int>(rb));
@@ -578,7 +587,8 @@ __global__ __launch_bounds__(kPartThreads) void k_part_dedup(TableDev t, Work w,
       const int2 tp = w.ptmp[pos];
       const int64_t src = (static_cast<int64_t>(pos) / g.rcap) * g.rcap + (static_cast<uint32_t>(tp.x) >> 12);
       const unsigned int kidx = static_cast<unsigned int>(cfp[tp.x & 0xFFF]);
-      const unsigned int fl = kidx == static_cast<unsigned int>(pos) ? kRecFirst : 0u;
+      const unsigned int ix = w.kinfo ? static_cast<unsigned int>(src) : static_cast<unsigned int>(pos);
+      const unsigned int fl = kidx == ix ? kRecFirst : 0u;
       w.recres[src] = make_int2(static_cast<int>(kidx), static_cast<int>(static_cast<unsigned int>(tp.y) | fl));
     }
     ++s;

@@ -207,8 +207,8 @@ struct alignas(16) TileRec {
   unsigned int meta;
 };
 
-// One distinct key of the call, indexed by its key index: the position (in
-// the partition-ordered record copies) of the key's first record.
+// One distinct key of the call, indexed by its key index: the tile-order
+// position (in the record lists) of the key's first record.
 struct alignas(32) KeyInfo {
   long long row;  // Blocks row (-1: not found / could not be inserted)
   long long key;  // the key
@@ -297,10 +297,12 @@ FrontGeom front_geom(int64_t n);
 // can refresh its bound on the live count without a copy or an event.
 hipError_t launch_dedup_probe(const int64_t* values, int64_t n, const TableDev& t, const Work& w, int64_t* h_live,
                               int64_t tag, hipEvent_t* ev_tile, hipEvent_t* ev_part, hipStream_t s);
-// The first two dedup passes only (tile dedup, per-partition dedup): the
-// first-occurrence markers, each record's key index and, unless w.kinfo is
-// null, the key info of every distinct key (t.slots null: no IDMap probe,
-// row 0).  n > 0.
+// The first two dedup passes only (tile dedup, per-partition dedup): each
+// record's key index with the key's first record flagged and, unless
+// w.kinfo is null, the key info of every distinct key (t.slots null: no
+// IDMap probe, row 0).  With w.kinfo null a key index is the first record's
+// position in the partition-ordered copies (whose entry there holds the
+// key).  n > 0.
 hipError_t launch_dedup_keys(const int64_t* values, int64_t n, const TableDev& t, const Work& w, hipEvent_t* ev_tile,
                              hipEvent_t* ev_part, hipStream_t s);
 // Geometry of the ids partition's owner passes.
