@@ -98,15 +98,15 @@ __device__ inline void block_excl_scan5(const int (&v)[5], int (&ex)[5], int (&t
     for (int a = 0; a < 5; ++a) sh[wid][a] = inc[a];
   }
   __syncthreads();
-  if (threadIdx.x < 5) {
-    const int a = threadIdx.x;
-    int run = 0;
-    for (int w = 0; w < NT / kWave; ++w) {
-      const int t = sh[w][a];
-      sh[w][a] = run;
-      run += t;
+  if (wid == 0) {  // one wave scans the per-wave totals of each value
+    static_assert(NT / kWave <= kWave, "one wave scans the per-wave totals");
+#pragma unroll
+    for (int a = 0; a < 5; ++a) {
+      const int t = lane < NT / kWave ? sh[lane][a] : 0;
+      const int i2 = wave_incl_scan(t);
+      if (lane < NT / kWave) sh[lane][a] = i2 - t;
+      if (lane == kWave - 1) sh[NT / kWave][a] = i2;
     }
-    sh[NT / kWave][a] = run;
   }
   __syncthreads();
 #pragma unroll
@@ -220,14 +220,12 @@ __global__ __launch_bounds__(NT) void k_tile_dedup(const int64_t* __restrict__ v
         if (lane == 0) lfirst[k * NW + wid] = __popcll(bal[k]);
       }
       __syncthreads();
-      if (tid == 0) {  // exclusive prefix over (item, wave) in position order
-        int run = 0;
-        for (int q = 0; q < kDedupItems * NW; ++q) {
-          const int c = lfirst[q];
-          lfirst[q] = run;
-          run += c;
-        }
-        lfirst[kDedupItems * NW] = run;
+      if (tid < kWave) {  // exclusive prefix over (item, wave) in position order: one wave's scan
+        static_assert(kDedupItems * NW <= kWave, "one wave scans the (item, wave) counts");
+        const int c = tid < kDedupItems * NW ? lfirst[tid] : 0;
+        const int inc = wave_incl_scan(c);
+        if (tid < kDedupItems * NW) lfirst[tid] = inc - c;
+        if (tid == kWave - 1) lfirst[kDedupItems * NW] = inc;
       }
       __syncthreads();
 #pragma unroll

@@ -42,14 +42,12 @@ __device__ inline int block_excl_scan(int v, int* sh, int& total) {
   const int inc = wave_incl_scan(v);
   if (lane == kWave - 1) sh[wid] = inc;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    int run = 0;
-    for (int w = 0; w < NT / kWave; ++w) {
-      const int t = sh[w];
-      sh[w] = run;
-      run += t;
-    }
-    sh[NT / kWave] = run;
+  if (wid == 0) {  // one wave scans the per-wave totals
+    static_assert(NT / kWave <= kWave, "one wave scans the per-wave totals");
+    const int t = lane < NT / kWave ? sh[lane] : 0;
+    const int i2 = wave_incl_scan(t);
+    if (lane < NT / kWave) sh[lane] = i2 - t;
+    if (lane == kWave - 1) sh[NT / kWave] = i2;
   }
   __syncthreads();
   const int ex = sh[wid] + inc - v;
@@ -65,8 +63,7 @@ __device__ inline int block_sum(int v, int* sh) {
   if (lane == 0) sh[wid] = v;
   __syncthreads();
   int t = 0;
-  if (threadIdx.x == 0)
-    for (int w = 0; w < NT / kWave; ++w) t += sh[w];
+  if (wid == 0) t = wave_sum(lane < NT / kWave ? sh[lane] : 0);
   return t;  // valid in thread 0
 }
 
