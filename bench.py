@@ -44,7 +44,8 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None,
-                    help="timed steps (default: 100 for the growing table, whose run includes resizes; else 20)")
+                    help="timed steps (default: 100 for the growing table, whose run includes resizes, and "
+                         "for --op ids-partition; 200 for --op bucketize | mod; else 20)")
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -718,9 +719,11 @@ def main():
         print(json.dumps({"error": "single-GPU build: run with --gpus 1 (the multi-GPU path is a design only)"}))
         sys.exit(2)
     if a.op == "ids-partition":
+        a.steps = 100 if a.steps is None else a.steps
         bench_ids_partition(a)
         return
     if a.op in ("bucketize", "mod"):
+        a.steps = 200 if a.steps is None else a.steps
         bench_feature_op(a)
         return
     from paper_2509_20883_amd import workloads as W
