@@ -315,7 +315,9 @@ rs_status lookup_pool_prepared(rs_table* t, rs_ctx* ctx, void* out, uint8_t* mas
  * to slot t; ids that were not copied contribute nothing).  Its first launch
  * lays out the per-key occurrence list from the gradient row of each id that
  * the ctx's pool wrote, so the pool precedes it; ids outside
- * [offsets[0], offsets[bags]) contribute nothing. */
+ * [offsets[0], offsets[bags]) contribute nothing.  The order of a key's
+ * occurrences in that list (so the fp32 summation order) is not fixed from
+ * run to run: sums may differ in their last bits between runs. */
 rs_status lookup_pool_bwd(rs_table* t, const rs_ctx* ctx, const void* grad_out, float* grad_unique,
                           rs_stream stream);
 
