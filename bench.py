@@ -195,6 +195,16 @@ TRAFFIC_KERNELS = {"pool": ("rs::k_pool<", "rs::k_pool_none<"), "bwd_short": ("r
                    "bwd_long": ("rs::k_bwd_long<", "rs::k_bwd_long_finish<")}
 
 
+def profile_label(a) -> str:
+    """The workload a profile covers: the step's workload name, or the
+    operator run by --op with its size."""
+    if a.op == "ids-partition":
+        return f"ids_partition_1M_{a.shards or 8}shards"
+    from paper_2509_20883_amd import workloads as W
+
+    return W.describe(W.workload(a.workload))["workload"]
+
+
 def traffic_from(a):
     """HBM bytes per launch from FETCH_SIZE / WRITE_SIZE (KiB per dispatch),
     each scaled by what the same counter reads for the library's copy probe
@@ -202,7 +212,6 @@ def traffic_from(a):
     dispatch (the last step of the profiled run)."""
     from collections import defaultdict
 
-    from paper_2509_20883_amd import workloads as W
 
     fdir, wdir, cfdir, cwdir = a.traffic_from
     gib_kib = (1 << 30) / 1024
@@ -223,11 +232,13 @@ def traffic_from(a):
         return {k: max(v)[1] * 1024 for k, v in by.items()}
 
     F, Wr = last(fdir), last(wdir)
-    wl = W.describe(W.workload(a.workload))["workload"]
+    wl = profile_label(a)
+    unit = "call" if a.op != "step" else "step"
     step = sorted((k for k in F if k.startswith("rs::") and "probe" not in k and "rehash" not in k
                    and "map_rows" not in k and "k_occ_init<false>" not in k), key=lambda k: -(F[k] + Wr.get(k, 0)))
     lines = [f"# HBM traffic per launch: {wl}", "",
-             "Counters `FETCH_SIZE` and `WRITE_SIZE` (KiB per dispatch), each in its own run, at the last step of", "",
+             f"Counters `FETCH_SIZE` and `WRITE_SIZE` (KiB per dispatch), each in its own run, at the last {unit} of",
+             "",
              "```", a.traffic_cmd or "(command not recorded)", "```", "",
              "scaled by the same counters on the library's copy probe of 1 GiB read + 1 GiB written "
              f"(`bench.py --copy-calibration`): fetch x{fs:.3f}, write x{ws:.3f}.  Converted by "
@@ -239,7 +250,7 @@ def traffic_from(a):
         tf += f
         tw += x
         lines.append(f"| `{k}` | {f:.1f} | {x:.1f} |")
-    lines += [f"| step total | {tf:.0f} | {tw:.0f} |", ""]
+    lines += [f"| {unit} total | {tf:.0f} | {tw:.0f} |", ""]
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
     with open(os.path.join(ROOT, "profiles", f"traffic_{wl}.md"), "w") as fh:
         fh.write("\n".join(lines))
@@ -277,19 +288,20 @@ def trace_from(a):
     step kernel, from the kernel trace) and rocprofv3's --stats table."""
     from collections import defaultdict
 
-    from paper_2509_20883_amd import workloads as W
 
-    wl = W.describe(W.workload(a.workload))["workload"]
+    wl = profile_label(a)
+    unit = "call" if a.op != "step" else "step"
     rows = _csv_rows(a.trace_from, "kernel_trace.csv")
     by = defaultdict(list)
     for r in rows:
         by[_kname(r)].append((int(r["Dispatch_Id"]), (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3))
     step = {k: v for k, v in by.items() if k.startswith("rs::") and "probe" not in k and "rehash" not in k
             and "map_rows" not in k and "k_occ_init<false>" not in k and "rereserve" not in k}
-    lines = [f"# Kernel time per step: {wl}", "", "Command (MI355X, repository root copied to `<repo>`):", "", "```",
+    how = f"--op {a.op} --shards {a.shards or 8}" if a.op == "ids-partition" else f"--workload {a.workload}"
+    lines = [f"# Kernel time per {unit}: {wl}", "", "Command (MI355X, repository root copied to `<repo>`):", "", "```",
              a.traffic_cmd or "(command not recorded)", "```", "",
-             f"Converted by `bench.py --workload {a.workload} --steps {a.steps} --trace-from <dir>`.", "",
-             f"## Per step (the last {a.steps} launches of each step kernel: the timed steps)", "",
+             f"Converted by `bench.py {how} --steps {a.steps} --trace-from <dir>`.", "",
+             f"## Per {unit} (the last {a.steps} launches of each kernel: the timed {unit}s)", "",
              "| kernel | mean us | % of kernel time |", "|---|---|---|"]
     means = {k: float(np.mean([t for _, t in sorted(v)[-a.steps:]])) for k, v in step.items()}
     tot = sum(means.values())
