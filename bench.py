@@ -454,16 +454,16 @@ def kernel_bytes(w, kernel, N, G, ks):
         out = G * w.pad_len * R + G * w.pad_len if padded else G * w.dim * 4
         alg = 8 * (G + 1) + 4 * N + 8 * U + R * U + out
         # the kernel reads each id's row id (8 B) and writes the id's gradient
-        # row (4 B; 8 B with the mean scale), both in id order
-        ref = 8 if w.mode == 1 else 4
-        impl = 8 * (G + 1) + 8 * N + R * U + out + ref * N
+        # row (4 B), both in id order
+        impl = 8 * (G + 1) + 8 * N + R * U + out + 4 * N
         return alg, impl
     if kernel == "bwd_short":
         Us, Ns, Nw = ks["U_short"], ks["N_short"], ks["Nw_short"]
         grad_alg = gr * (Nw if padded else ks["Gb_short"])
         alg = grad_alg + 4 * Ns + 2 * (R + S) * Us
         # segment descriptors of every key, one gradient row per occurrence
-        impl = 16 * U + 4 * Ns + gr * Nw + 2 * (R + S) * Us
+        # (mean pooling: the bag offsets for the scales)
+        impl = 16 * U + 4 * Ns + gr * Nw + 2 * (R + S) * Us + (8 * (G + 1) if w.mode == 1 else 0)
         return alg, impl
     if kernel == "bwd_long":
         Ul, Nl, Nw, nu = ks["U_long"], ks["N_long"], ks["Nw_long"], ks["units"]
@@ -471,7 +471,8 @@ def kernel_bytes(w, kernel, N, G, ks):
         alg = grad_alg + 4 * Nl + 2 * (R + S) * Ul
         # unit descriptors, one gradient row per occurrence, one partial row
         # written and read back per unit
-        impl = 16 * nu + 4 * Nl + gr * Nw + 2 * 4 * w.dim * nu + 2 * (R + S) * Ul
+        impl = (16 * nu + 4 * Nl + gr * Nw + 2 * 4 * w.dim * nu + 2 * (R + S) * Ul
+                + (8 * (G + 1) if w.mode == 1 else 0))
         return alg, impl
     raise KeyError(kernel)
 

@@ -87,8 +87,8 @@ Layout make_layout(int64_t n, int dim) {
   L.useg = take(sizeof(Seg) * n1);
   L.rows = take(8 * n1);
   L.new_list = take(4 * n1);
-  L.id_ref = take(8 * n1);   // int32 per id, or {int32, float} for mean pooling
-  L.occ_ref = take(8 * n1);  // int32 per position, or {int32, float} for mean pooling
+  L.id_ref = take(4 * n1);
+  L.occ_ref = take(4 * n1);
   L.long_u = take(4 * nlong);
   L.long_start = take(4 * nlong);
   L.units = take(sizeof(Unit) * nunit);
@@ -121,9 +121,8 @@ Work make_work(void* base, const Layout& L) {
   w.rows = reinterpret_cast<int64_t*>(b + L.rows);
   w.new_list = reinterpret_cast<int32_t*>(b + L.new_list);
   w.id_ref = reinterpret_cast<int32_t*>(b + L.id_ref);
-  w.id_rs = reinterpret_cast<int2*>(b + L.id_ref);
   w.occ_ref = reinterpret_cast<int32_t*>(b + L.occ_ref);
-  w.occ_rs = reinterpret_cast<int2*>(b + L.occ_ref);
+  w.offsets = nullptr;
   w.long_u = reinterpret_cast<int32_t*>(b + L.long_u);
   w.long_start = reinterpret_cast<int32_t*>(b + L.long_start);
   w.units = reinterpret_cast<Unit*>(b + L.units);
@@ -543,7 +542,11 @@ rs_status check_ctx(const rs_table* t, const rs_ctx* c) {
   return RS_OK;
 }
 
-Work ctx_work(const rs_ctx* c) { return make_work(c->workspace, make_layout(c->n, c->dim)); }
+Work ctx_work(const rs_ctx* c) {
+  Work w = make_work(c->workspace, make_layout(c->n, c->dim));
+  w.offsets = c->offsets;
+  return w;
+}
 
 // Rows of the upstream gradient of a forward (its output's rows).
 int64_t grad_rows(const rs_ctx* c) { return padded_mode(c->mode) ? c->bags * c->pad_len : c->bags; }

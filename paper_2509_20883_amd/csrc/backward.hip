@@ -109,6 +109,14 @@ struct RowFrag {
   }
 };
 
+// Mean pooling's scale of gradient row (bag) r: 1 / the bag's length, from
+// the forward's offsets (r < nref = bags; any other r contributes nothing).
+__device__ inline float mean_scale(const Work& w, int r, uint32_t nref) {
+  if (static_cast<uint32_t>(r) >= nref) return 0.f;
+  const int64_t len = w.offsets[r + 1] - w.offsets[r];
+  return 1.0f / static_cast<float>(max(len, int64_t(1)));
+}
+
 // Sum of the gradient rows of occurrence-list positions [p0, p0 + cnt),
 // cnt <= kUnit.  The lanes of the group load the positions' gradient-row
 // indices together (one round trip), share them by shuffles, and then read
@@ -126,13 +134,11 @@ __device__ inline void sum_positions(const Work& w, const GT* __restrict__ grad,
 #pragma unroll
   for (int k = 0; k < NR; ++k) {
     const int q = k * LANES + lane;
-    if (MODE == 1) {
-      const int2 rs = q < cnt ? w.occ_rs[p0 + q] : make_int2(-1, 0);
-      myref[k] = rs.x;
-      mysc[k] = __int_as_float(rs.y);
-    } else {
-      myref[k] = q < cnt ? w.occ_ref[p0 + q] : -1;
-    }
+    myref[k] = q < cnt ? w.occ_ref[p0 + q] : -1;
+  }
+  if (MODE == 1) {
+#pragma unroll
+    for (int k = 0; k < NR; ++k) mysc[k] = mean_scale(w, myref[k], nref);
   }
 #pragma unroll
   for (int q0 = 0; q0 < kUnit; q0 += kBatch) {
@@ -202,13 +208,11 @@ __device__ inline void sum_segments(const Work& w, const GT* __restrict__ grad, 
         pk = pre[k];
       }
     const int p = valid ? sk + (tq - pk) : 0;
-    if (MODE == 1) {
-      const int2 rs = valid ? w.occ_rs[p] : make_int2(-1, 0);
-      myref[j] = rs.x;
-      mysc[j] = __int_as_float(rs.y);
-    } else {
-      myref[j] = valid ? w.occ_ref[p] : -1;
-    }
+    myref[j] = valid ? w.occ_ref[p] : -1;
+  }
+  if (MODE == 1) {
+#pragma unroll
+    for (int j = 0; j < NR; ++j) mysc[j] = mean_scale(w, myref[j], nref);
   }
 #pragma unroll
   for (int q0 = 0; q0 < MAXP; q0 += kBatch) {
@@ -410,9 +414,9 @@ __global__ __launch_bounds__(kBlock) void k_bwd_long_finish(TableDev t, Work w, 
 }
 
 // The occurrence list the backward reads: position occ_pos[i] of id i
-// receives the gradient row the pool gave that id (id_ref; with the bag's
-// mean scale for mean pooling).  Ids outside the pooled range [lo, hi) get
-// no gradient row (-1); ids of a rejected key have no position.
+// receives the gradient row the pool gave that id (id_ref).  Ids outside
+// the pooled range [lo, hi) get no gradient row (-1); ids of a rejected key
+// have no position.
 //
 // One block per dedup tile (kOccListNT threads, 4 ids each).  A record's ids
 // in the tile hold the consecutive positions [base, base + count) of its
@@ -423,54 +427,36 @@ __global__ __launch_bounds__(kBlock) void k_bwd_long_finish(TableDev t, Work w, 
 // per id.
 constexpr int kOccListNT = kDedupTile / 4;
 
-template <bool MEAN>
 __global__ __launch_bounds__(kOccListNT) void k_occ_list(Work w, int64_t n) {
   constexpr int T = kDedupTile;
   __shared__ int cnt[T];  // per record of the tile: its ids, then its first slot
   __shared__ int spos[T], sref[T];
-  __shared__ int ssc[MEAN ? T : 1];
   __shared__ int wsh[kOccListNT / kWave + 1];
   __shared__ int rlo_sh;
   const int64_t i0 = static_cast<int64_t>(blockIdx.x) * T + threadIdx.x * 4;
   const int64_t lo = min(max(w.scal[kCIdLo], int64_t(0)), n);
   const int64_t hi = min(max(w.scal[kCIdHi], lo), n);
   uint32_t o[4];
-  int pos[4], ref[4], sc[4] = {0, 0, 0, 0};
+  int pos[4], ref[4];
   if (i0 + 4 <= n) {
     const int4 ow = *reinterpret_cast<const int4*>(w.occ_word + i0);
     const int4 p = *reinterpret_cast<const int4*>(w.occ_pos + i0);
+    const int4 r = *reinterpret_cast<const int4*>(w.id_ref + i0);
     o[0] = ow.x; o[1] = ow.y; o[2] = ow.z; o[3] = ow.w;
     pos[0] = p.x; pos[1] = p.y; pos[2] = p.z; pos[3] = p.w;
-    if (MEAN) {
-      const int4 a = *reinterpret_cast<const int4*>(w.id_rs + i0);
-      const int4 b = *reinterpret_cast<const int4*>(w.id_rs + i0 + 2);
-      ref[0] = a.x; sc[0] = a.y; ref[1] = a.z; sc[1] = a.w;
-      ref[2] = b.x; sc[2] = b.y; ref[3] = b.z; sc[3] = b.w;
-    } else {
-      const int4 r = *reinterpret_cast<const int4*>(w.id_ref + i0);
-      ref[0] = r.x; ref[1] = r.y; ref[2] = r.z; ref[3] = r.w;
-    }
+    ref[0] = r.x; ref[1] = r.y; ref[2] = r.z; ref[3] = r.w;
   } else {
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const bool v = i0 + k < n;
       o[k] = v ? w.occ_word[i0 + k] : kOccRejected;
       pos[k] = v ? w.occ_pos[i0 + k] : -1;
-      if (MEAN) {
-        const int2 a = v ? w.id_rs[i0 + k] : make_int2(-1, 0);
-        ref[k] = a.x;
-        sc[k] = a.y;
-      } else {
-        ref[k] = v ? w.id_ref[i0 + k] : -1;
-      }
+      ref[k] = v ? w.id_ref[i0 + k] : -1;
     }
   }
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    if (i0 + k < lo || i0 + k >= hi) {
-      ref[k] = -1;
-      sc[k] = 0;
-    }
+    if (i0 + k < lo || i0 + k >= hi) ref[k] = -1;
     if (pos[k] < 0) o[k] = kOccRejected;  // no list entry
   }
   // the tile's first record
@@ -518,9 +504,6 @@ __global__ __launch_bounds__(kOccListNT) void k_occ_list(Work w, int64_t n) {
     if (slot < T) {
       spos[slot] = pos[k];
       sref[slot] = ref[k];
-      if (MEAN) ssc[slot] = sc[k];
-    } else if (MEAN) {
-      w.occ_rs[pos[k]] = make_int2(ref[k], sc[k]);
     } else {
       w.occ_ref[pos[k]] = ref[k];
     }
@@ -529,8 +512,7 @@ __global__ __launch_bounds__(kOccListNT) void k_occ_list(Work w, int64_t n) {
   for (int s = threadIdx.x; s < min(total, T); s += kOccListNT) {
     const int p = spos[s];
     if (p < 0) continue;
-    if (MEAN) w.occ_rs[p] = make_int2(sref[s], ssc[s]);
-    else w.occ_ref[p] = sref[s];
+    w.occ_ref[p] = sref[s];
   }
 }
 
@@ -591,8 +573,7 @@ hipError_t launch_bwd(const TableDev& t, const Work& w, int64_t nref, int64_t n,
   {
     hipEvent_t e0 = ev_list ? ev_list[0] : nullptr, e1 = ev_list ? ev_list[1] : nullptr;
     const dim3 grid(static_cast<unsigned>((n + kDedupTile - 1) / kDedupTile));
-    if (mode == 1) hipExtLaunchKernelGGL((k_occ_list<true>), grid, dim3(kOccListNT), 0, s, e0, e1, 0, w, n);
-    else hipExtLaunchKernelGGL((k_occ_list<false>), grid, dim3(kOccListNT), 0, s, e0, e1, 0, w, n);
+    hipExtLaunchKernelGGL(k_occ_list, grid, dim3(kOccListNT), 0, s, e0, e1, 0, w, n);
   }
   const OptArgs o = opt ? *opt : OptArgs{0, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 1.f, 1.f, 0.f, 0.f};
   if (opt)

@@ -142,31 +142,22 @@ __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64
       if (r >= 0) x[c] = *reinterpret_cast<const uint4*>(t.store.row(r) + lane * 16);
     }
     if (t0 + C < total) load_idx(t0 + C);  // the next chunk's row ids replace rr
-    int myq[J], mylen[J];  // bag (and its length) of this lane's positions in the chunk
+    int myq[J];  // bag of this lane's positions in the chunk
 #pragma unroll
     for (int c = 0; c < C; ++c) {
       const int tt = t0 + c;
       if (tt >= total) break;
       while (q < nb && tt >= cq) flush();  // bags ending before this id (empty ones flush zeros)
-      if (lane == c % LANES) {
-        myq[c / LANES] = q;
-        mylen[c / LANES] = static_cast<int>(min(cq - bstart, int64_t(n32)));
-      }
+      if (lane == c % LANES) myq[c / LANES] = q;
       add_raw<WT, E>(acc, x[c]);
     }
-    // each id of the chunk: the gradient row it reads in the backward (and,
-    // for mean pooling, the scale 1 / bag length); consecutive lanes write
-    // consecutive ids
+    // each id of the chunk: the gradient row it reads in the backward (its
+    // bag); consecutive lanes write consecutive ids
 #pragma unroll
     for (int j = 0; j < J; ++j) {
       const int c = lane + j * LANES;
       if (c >= C || t0 + c >= total || p0 + t0 + c >= n32) continue;
-      const int p = p0 + t0 + c;
-      if (MODE == 1)
-        w.id_rs[p] = make_int2(static_cast<int>(g0 + myq[j]),
-                               __float_as_int(1.0f / static_cast<float>(max(mylen[j], 1))));
-      else
-        w.id_ref[p] = static_cast<int>(g0 + myq[j]);
+      w.id_ref[p0 + t0 + c] = static_cast<int>(g0 + myq[j]);
     }
   }
   while (q < nb) flush();  // the last bag and any empty bags after it

@@ -253,9 +253,8 @@ struct Work {
   int64_t* rows;        // [n]
   int32_t* new_list;    // [n] unique id of the k-th inserted key
   int32_t* id_ref;      // [n] gradient row of each id (written by the pool; -1: none)
-  int2* id_rs;          // [n] mean pooling, same memory: {gradient row, bits of 1 / bag length}
   int32_t* occ_ref;     // [n] gradient row of each position of the occurrence list
-  int2* occ_rs;         // [n] mean pooling, same memory: {gradient row, bits of 1 / bag length}
+  const int64_t* offsets;  // the forward's bag offsets (mean pooling: the backward's 1 / bag length)
   int32_t* long_u;      // [n/kLong + 1] unique id of each hot key
   int32_t* long_start;  // [n/kLong + 1] first backward unit of each hot key
   Unit* units;          // [2n/kUnit + 2] backward units of the hot keys
