@@ -150,6 +150,50 @@ def _check_update(w, b, grad, uniq, inv, sel, w0, s0, w1, s1):
     assert_opt_close(w1, s1, w1_ref, s1_ref, bounds, what="fused backward + optimizer (sampled ids)")
 
 
+def _check_outputs_from_rows(w, gt, b, out, inv, rows, g):
+    """Pooled outputs of sampled bags against the rows the GPU table holds
+    after the forward (any step: rows updated by earlier steps included)."""
+    bags = _sample_bags(b, g)
+    lens = np.diff(b.offsets)[bags]
+    pos = np.concatenate([np.arange(b.offsets[i], b.offsets[i + 1]) for i in bags]) if lens.sum() else \
+        np.zeros(0, dtype=np.int64)
+    bag_of = np.repeat(np.arange(bags.size), lens)
+    u = inv[pos]
+    wr, _ = gt.read_rows(to_dev(rows[u]))
+    wr = wr.cpu().numpy().astype(np.float64)
+    ref = np.zeros((bags.size, w.dim))
+    scale = np.zeros((bags.size, w.dim))
+    np.add.at(ref, bag_of, wr)
+    np.add.at(scale, bag_of, np.abs(wr))
+    if w.mode == O.MEAN:
+        ref /= np.maximum(lens, 1)[:, None]
+        scale /= np.maximum(lens, 1)[:, None]
+    got = out.index_select(0, torch.from_numpy(bags).cuda()).cpu().numpy()
+    assert_sum_close(got, ref, scale, what="pooled (sampled bags, rows read back)")
+
+
+def _check_update_from(w, b, grad, uniq, inv, sel, w0, s0, w1, s1, t0):
+    """The fused backward + optimizer of sampled unique ids, the oracle
+    starting from the rows and state the GPU held before it (step count t0)."""
+    U = uniq.size
+    remap = np.full(U, -1, dtype=np.int32)
+    remap[sel] = np.arange(sel.size, dtype=np.int32)
+    inv_s = np.where(inv >= 0, remap[np.maximum(inv, 0)], -1).astype(np.int32)
+    gu = O.backward(b.offsets, inv_s, sel.size, w.dim, w.mode, 0, grad)
+    gabs = O.backward(b.offsets, inv_s, sel.size, w.dim, w.mode, 0, np.abs(grad))
+    ot = _oracle(w)
+    st, rows_o, _ = ot.find_or_insert(uniq[sel])
+    assert st == O.OK
+    ot.write_rows(uniq[sel], w0, s0)
+    ot.t = t0
+    g32 = gu.astype(np.float32)
+    ot.optimizer(rows_o, g32, w.lr, w.eps, w.beta1, w.beta2, weight_decay=w.weight_decay)
+    _, w1_ref, s1_ref = ot.read_rows(uniq[sel])
+    dg = 1e-5 * gabs + np.abs(gu) * 2.0 ** -23
+    bounds = opt_bounds(w.opt, w.row_dtype, w0, s0, g32, dg, w.lr, w.eps, w.beta1, w.beta2, ot.t, w1_ref)
+    assert_opt_close(w1, s1, w1_ref, s1_ref, bounds, what=f"fused backward + optimizer (sampled ids, t {t0 + 1})")
+
+
 @pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
 def test_fullsize_step(k):
     """One full-size step of workload k (first step after pre-population)."""
@@ -186,8 +230,12 @@ def test_fullsize_step(k):
 
 def test_fullsize_growing_steps():
     """Consecutive full-size steps of the growing-table workload: each step's
-    integer results against the oracle's dedup and the set of keys seen so far."""
+    integer results against the oracle's dedup and the set of keys seen so
+    far; the pooled outputs of sampled bags and the fused update of sampled
+    unique ids against the oracle started from the rows the GPU holds after
+    each forward (so rows updated by the earlier steps are covered)."""
     w = W.workload(4)
+    g = np.random.default_rng(9100)
     gt = gpu_table(w)
     try:
         prepopulate(w, gt)
@@ -196,13 +244,19 @@ def test_fullsize_growing_steps():
         for step in range(3):
             live0 = gt.size()
             b = W.make_batch(w, step)
-            grad = to_dev(W.make_grad(w, b, step))
+            grad = W.make_grad(w, b, step)
             out, _, ctx = gt.forward(to_dev(b.values), to_dev(b.offsets), w.mode, ctx=ctx)
             torch.cuda.synchronize()
-            U, uniq, _, _ = _check_integers(w, gt, ctx, b, live0, seen)
-            gt.backward_optimizer(ctx, grad, w.lr, w.eps, w.beta1, w.beta2)
-            torch.cuda.synchronize()
+            U, uniq, inv, rows = _check_integers(w, gt, ctx, b, live0, seen)
             assert np.isfinite(out.cpu().numpy()).all()
+            _check_outputs_from_rows(w, gt, b, out, inv, rows, g)
+            counts = np.bincount(inv[inv >= 0], minlength=U)
+            sel = _sample_unique(counts, g)
+            rsel = to_dev(rows[sel])
+            w0, s0 = (x.cpu().numpy() for x in gt.read_rows(rsel))
+            gt.backward_optimizer(ctx, to_dev(grad), w.lr, w.eps, w.beta1, w.beta2)
+            w1, s1 = (x.cpu().numpy() for x in gt.read_rows(rsel))
+            _check_update_from(w, b, grad, uniq, inv, sel, w0, s0, w1, s1, step)
             seen = np.union1d(seen, uniq)
         gt.check()
     finally:
