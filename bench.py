@@ -35,6 +35,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
+# where the profile converters write their summaries (and the bench reads
+# the traffic records back)
+PROFILES = os.path.join(ROOT, "profiles")
 OPTIMIZERS = ["adagrad", "adam", "adamw", "adam-eps-hat", "adagrad-rowwise", "adam-rowwise"]
 METRIC = "embedding step IDs/sec (fwd+bwd+opt) and achieved HBM GB/s vs peak, 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
@@ -251,8 +254,8 @@ def traffic_from(a):
         tw += x
         lines.append(f"| `{k}` | {f:.1f} | {x:.1f} |")
     lines += [f"| {unit} total | {tf:.0f} | {tw:.0f} |", ""]
-    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
-    with open(os.path.join(ROOT, "profiles", f"traffic_{wl}.md"), "w") as fh:
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(os.path.join(PROFILES, f"traffic_{wl}.md"), "w") as fh:
         fh.write("\n".join(lines))
     for kern, prefixes in TRAFFIC_KERNELS.items():
         names = [k for k in step if k.startswith(prefixes)]
@@ -263,7 +266,7 @@ def traffic_from(a):
         rec = {"kernel": kern, "kernels": names, "workload": wl, "bytes_per_launch": fb + wb, "fetch_bytes": fb,
                "write_bytes": wb, "fetch_scale": fs, "write_scale": ws, "kernel_source_hash": kernel_source_hash(kern),
                "counters_from": f"profiles/traffic_{wl}.md"}
-        with open(os.path.join(ROOT, "profiles", f"traffic_{wl}_{kern}.json"), "w") as fh:
+        with open(os.path.join(PROFILES, f"traffic_{wl}_{kern}.json"), "w") as fh:
             json.dump(rec, fh, indent=1)
     print("\n".join(lines))
 
@@ -313,8 +316,8 @@ def trace_from(a):
         lines.append(f"| `{r['Name'].split('(')[0].replace('void ', '')[:70]}` | {r['Calls']} | "
                      f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
                      f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.1f} |")
-    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
-    with open(os.path.join(ROOT, "profiles", f"step_kernels_{wl}.md"), "w") as fh:
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(os.path.join(PROFILES, f"step_kernels_{wl}.md"), "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
@@ -323,9 +326,7 @@ def counters_from(a):
     """L2 hit rate and atomics per step kernel (its last dispatch)."""
     from collections import defaultdict
 
-    from paper_2509_20883_amd import workloads as W
-
-    wl = W.describe(W.workload(a.workload))["workload"]
+    wl = profile_label(a)
     last, vals = {}, defaultdict(dict)
     rows = _csv_rows(a.counters_from, "counter_collection.csv")
     for r in rows:
@@ -346,7 +347,8 @@ def counters_from(a):
         h, m = v.get("TCC_HIT_sum", 0.0), v.get("TCC_MISS_sum", 0.0)
         lines.append(f"| `{k}` | {h / 1e6:.1f} | {m / 1e6:.1f} | {h / max(h + m, 1):.2f} | "
                      f"{v.get('TCC_ATOMIC_sum', 0.0) / 1e6:.2f} |")
-    with open(os.path.join(ROOT, "profiles", f"l2_{wl}.md"), "w") as fh:
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(os.path.join(PROFILES, f"l2_{wl}.md"), "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
@@ -1048,7 +1050,7 @@ def main():
     achieved = dom_alg / (dom_ms * 1e-3) / 1e9
 
     traffic = None
-    tpath = os.path.join(ROOT, "profiles", f"traffic_{W.describe(w)['workload']}_{dom}.json")
+    tpath = os.path.join(PROFILES, f"traffic_{W.describe(w)['workload']}_{dom}.json")
     if os.path.exists(tpath):
         with open(tpath) as fh:
             tj = json.load(fh)
