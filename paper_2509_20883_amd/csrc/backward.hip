@@ -80,7 +80,7 @@ struct RowFrag {
           s1[k] = o.beta1 * s1[k] + o.omb1 * g[k];
           w[k] = w[k] - o.lr * (s1[k] / o.bc1) / den;
         }
-        store_vals<float, E>(p, s1);
+        store_vals_nt<float, E>(p, s1);
         if (lane == 0) base[dim] = sr;
       }
     } else if (o.opt == 0) {
@@ -89,7 +89,7 @@ struct RowFrag {
         s1[k] = s1[k] + g[k] * g[k];
         w[k] = w[k] - o.lr * g[k] / (__builtin_sqrtf(s1[k]) + o.eps);
       }
-      store_vals<float, E>(p, s1);
+      store_vals_nt<float, E>(p, s1);
     } else {
 #pragma unroll
       for (int k = 0; k < E; ++k) {
@@ -102,10 +102,10 @@ struct RowFrag {
           w[k] = w[k] - o.lr * (s1[k] / o.bc1) / (__builtin_sqrtf(s2[k] / o.bc2) + o.eps);
         }
       }
-      store_vals<float, E>(p, s1);
-      store_vals<float, E>(p + dim, s2);
+      store_vals_nt<float, E>(p, s1);
+      store_vals_nt<float, E>(p + dim, s2);
     }
-    store_vals<WT, E>(reinterpret_cast<WT*>(row) + lane * E, w);
+    store_vals_nt<WT, E>(reinterpret_cast<WT*>(row) + lane * E, w);
   }
 };
 

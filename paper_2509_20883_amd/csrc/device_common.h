@@ -170,6 +170,45 @@ __device__ inline void store_vals<uint16_t, 4>(uint16_t* __restrict__ p, const f
   *reinterpret_cast<uint2*>(p) = a;
 }
 
+// The same stores, non-temporal, for rows and optimizer state written by an
+// update: nothing reads them again in the step, and the lines leave the
+// caches at once instead of being written back under the next kernel.
+typedef float nt_f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t nt_u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t nt_u32x2 __attribute__((ext_vector_type(2)));
+
+template <typename T, int E>
+__device__ inline void store_vals_nt(T* __restrict__ p, const float (&v)[E]);
+
+template <>
+__device__ inline void store_vals_nt<float, 4>(float* __restrict__ p, const float (&v)[4]) {
+  const nt_f32x4 a = {v[0], v[1], v[2], v[3]};
+  __builtin_nontemporal_store(a, reinterpret_cast<nt_f32x4*>(p));
+}
+template <>
+__device__ inline void store_vals_nt<float, 8>(float* __restrict__ p, const float (&v)[8]) {
+  const nt_f32x4 a = {v[0], v[1], v[2], v[3]};
+  const nt_f32x4 b = {v[4], v[5], v[6], v[7]};
+  __builtin_nontemporal_store(a, reinterpret_cast<nt_f32x4*>(p));
+  __builtin_nontemporal_store(b, reinterpret_cast<nt_f32x4*>(p + 4));
+}
+template <>
+__device__ inline void store_vals_nt<uint16_t, 8>(uint16_t* __restrict__ p, const float (&v)[8]) {
+  nt_u32x4 a;
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    a[k] = static_cast<uint32_t>(f32_to_bf16(v[2 * k])) | (static_cast<uint32_t>(f32_to_bf16(v[2 * k + 1])) << 16);
+  __builtin_nontemporal_store(a, reinterpret_cast<nt_u32x4*>(p));
+}
+template <>
+__device__ inline void store_vals_nt<uint16_t, 4>(uint16_t* __restrict__ p, const float (&v)[4]) {
+  nt_u32x2 a;
+#pragma unroll
+  for (int k = 0; k < 2; ++k)
+    a[k] = static_cast<uint32_t>(f32_to_bf16(v[2 * k])) | (static_cast<uint32_t>(f32_to_bf16(v[2 * k + 1])) << 16);
+  __builtin_nontemporal_store(a, reinterpret_cast<nt_u32x2*>(p));
+}
+
 inline unsigned grid_for(int64_t work_items, int64_t per_block, int64_t cap = 1 << 20) {
   int64_t g = (work_items + per_block - 1) / per_block;
   if (g < 1) g = 1;
