@@ -247,7 +247,8 @@ __global__ __launch_bounds__(NT) void k_tile_dedup(const int64_t* __restrict__ v
     for (int k = 0; k < kDedupItems; ++k) {
       const int64_t i = base + k * NT + tid;
       if (i >= n) continue;
-      w.occ_word[i] = ls[k] < 0 ? kOccRejected : ((lmin[ls[k]] << 12) | lr[k]);
+      // read again only by the passes after the compaction: non-temporal
+      __builtin_nontemporal_store(ls[k] < 0 ? kOccRejected : ((lmin[ls[k]] << 12) | lr[k]), &w.occ_word[i]);
     }
     nrec += static_cast<unsigned int>(d);
     __syncthreads();
@@ -1052,11 +1053,13 @@ __device__ inline void occ_pass(const Work& w, int64_t n, int64_t blk) {
     }
   }
   if (i0 + 4 <= n) {
-    *reinterpret_cast<int4*>(w.inverse + i0) = make_int4(a[0].uid, a[1].uid, a[2].uid, a[3].uid);
+    // the inverse (the caller's) and the list positions (the backward's)
+    // are not read in the forward: non-temporal
+    store4_nt(w.inverse + i0, a[0].uid, a[1].uid, a[2].uid, a[3].uid);
     if (OCC) {
       *reinterpret_cast<longlong2*>(w.occ_row + i0) = make_longlong2(a[0].row, a[1].row);
       *reinterpret_cast<longlong2*>(w.occ_row + i0 + 2) = make_longlong2(a[2].row, a[3].row);
-      *reinterpret_cast<int4*>(w.occ_pos + i0) = make_int4(pos[0], pos[1], pos[2], pos[3]);
+      store4_nt(w.occ_pos + i0, pos[0], pos[1], pos[2], pos[3]);
     }
   } else {
     for (int k = 0; k < 4 && i0 + k < n; ++k) {

@@ -209,6 +209,14 @@ __device__ inline void store_vals_nt<uint16_t, 4>(uint16_t* __restrict__ p, cons
   __builtin_nontemporal_store(a, reinterpret_cast<nt_u32x2*>(p));
 }
 
+// Four int32 to a 16-byte-aligned p in one non-temporal store (per-id
+// results that no kernel reads soon).
+__device__ inline void store4_nt(int32_t* p, int a, int b, int c, int d) {
+  const nt_u32x4 v = {static_cast<uint32_t>(a), static_cast<uint32_t>(b), static_cast<uint32_t>(c),
+                      static_cast<uint32_t>(d)};
+  __builtin_nontemporal_store(v, reinterpret_cast<nt_u32x4*>(p));
+}
+
 inline unsigned grid_for(int64_t work_items, int64_t per_block, int64_t cap = 1 << 20) {
   int64_t g = (work_items + per_block - 1) / per_block;
   if (g < 1) g = 1;
