@@ -152,13 +152,13 @@ __global__ __launch_bounds__(kBlock) void k_pool(TableDev t, Work w, const int64
       add_raw<WT, E>(acc, x[c]);
     }
     // each id of the chunk: the gradient row it reads in the backward (its
-    // bag); consecutive lanes write consecutive ids, non-temporal (read only
-    // by the backward)
+    // bag); consecutive lanes write consecutive ids (plain stores: a narrow
+    // lane group writes only 16 bytes per chunk, which the L2 merges)
 #pragma unroll
     for (int j = 0; j < J; ++j) {
       const int c = lane + j * LANES;
       if (c >= C || t0 + c >= total || p0 + t0 + c >= n32) continue;
-      __builtin_nontemporal_store(static_cast<int>(g0 + myq[j]), &w.id_ref[p0 + t0 + c]);
+      w.id_ref[p0 + t0 + c] = static_cast<int>(g0 + myq[j]);
     }
   }
   while (q < nb) flush();  // the last bag and any empty bags after it
