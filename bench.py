@@ -72,6 +72,9 @@ def parse():
                     help="ids-partition: time the fused dedup + owner split alone on its one-million-id input; "
                          "bucketize / mod: the fused feature transforms on 100 columns of 10,000 values")
     ap.add_argument("--shards", type=int, default=None, help="owner shards of --op ids-partition (default 8)")
+    ap.add_argument("--ceilings-from", nargs="+", metavar="PATH",
+                    help="write profiles/ceilings_mi355x.md from a --ceilings JSON line [and its rocprofv3 "
+                         "--kernel-trace --stats output directory] (no GPU needed)")
     ap.add_argument("--ceilings", action="store_true",
                     help="measure plain device read / write / copy / random-row gather bandwidth and exit")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -170,6 +173,39 @@ def ceilings():
         m = _probe_ms(fn)
         res[name] = {"bytes": nbytes, "ms": m, "GBps": nbytes / (m * 1e-3) / 1e9}
     print(json.dumps({"ceilings": res, "peak_GBps": HBM_PEAK_GBPS}))
+
+
+def ceilings_from(a):
+    """profiles/ceilings_mi355x.md from the JSON line of a `--ceilings` run
+    and, if given, the rocprofv3 `--kernel-trace --stats` output of the same
+    command (the probe kernels' own durations)."""
+    with open(a.ceilings_from[0]) as fh:
+        d = json.loads([ln for ln in fh if ln.startswith("{")][-1])
+    peak = d["peak_GBps"]
+    lines = ["# Practical HBM ceilings of this MI355X: the library's probe kernels, 2 GiB buffers", "",
+             "Commands (repository root copied to `<repo>`):", "", "```", a.traffic_cmd or "(command not recorded)",
+             "```", "",
+             "`bench.py --ceilings` times each probe (`rs_bandwidth_probe`, `csrc/probes.hip`: 256-thread blocks, "
+             "16-byte lane accesses, one pass) with HIP events, the median of 5 launches after one untimed launch; "
+             "bytes moved / time.  Converted by `bench.py --ceilings-from`.", "",
+             "| operation | bytes per launch | ms | GB/s | % of 8 TB/s |", "|---|---|---|---|---|"]
+    for name, r in d["ceilings"].items():
+        lines.append(f"| {name} | {r['bytes']} | {r['ms']:.3f} | {r['GBps']:.0f} | {100 * r['GBps'] / peak:.1f} |")
+    if len(a.ceilings_from) > 1:
+        lines += ["", "The probe kernels in the rocprofv3 trace of the same command (every launch):", "",
+                  "| kernel | calls | avg us | min us | max us |", "|---|---|---|---|---|"]
+        for r in _csv_rows(a.ceilings_from[1], "kernel_stats.csv"):
+            name = r["Name"].split("(")[0].replace("void ", "")
+            if "k_probe" in name:
+                lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                             f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |")
+    lines += ["", "The read-modify-write probe writes its rows back with non-temporal stores, as the "
+              "optimizer's update does; the gather and the streaming write and copy store their outputs "
+              "non-temporally too.", ""]
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(os.path.join(PROFILES, "ceilings_mi355x.md"), "w") as fh:
+        fh.write("\n".join(lines))
+    print("\n".join(lines))
 
 
 def copy_calibration():
@@ -726,6 +762,9 @@ def main():
         return
     if a.copy_calibration:
         copy_calibration()
+        return
+    if a.ceilings_from:
+        ceilings_from(a)
         return
     if a.ceilings:
         ceilings()

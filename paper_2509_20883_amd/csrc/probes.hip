@@ -9,7 +9,8 @@
 //   kProbeGather  out[i] = rows[idx[i]] for n rows of row_bytes: random row
 //                 reads, one streamed output row per index
 //   kProbeRmw     rows[idx[i]] += 1 for n rows of row_bytes: random row
-//                 read-modify-write in place (as the optimizer does)
+//                 read-modify-write in place (as the optimizer does, the
+//                 write non-temporal)
 #include "device_common.h"
 
 #include <hip/hip_ext.h>
@@ -112,8 +113,9 @@ __global__ __launch_bounds__(kBlock) void k_probe_rmw(uint8_t* __restrict__ rows
 #pragma unroll
       for (int c = 0; c < kProbeMaxChunks; ++c) {
         if (c >= nch) continue;
-        const float4 x = make_float4(v[k][c].x + 1.f, v[k][c].y + 1.f, v[k][c].z + 1.f, v[k][c].w + 1.f);
-        *reinterpret_cast<float4*>(rows + r[k] * row_bytes + (c * lanes + lane) * 16) = x;
+        // written back non-temporally, as the optimizer's update is
+        const nt_f32x4 x = {v[k][c].x + 1.f, v[k][c].y + 1.f, v[k][c].z + 1.f, v[k][c].w + 1.f};
+        __builtin_nontemporal_store(x, reinterpret_cast<nt_f32x4*>(rows + r[k] * row_bytes + (c * lanes + lane) * 16));
       }
     }
   }

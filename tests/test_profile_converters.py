@@ -103,3 +103,19 @@ def test_l2_summary_takes_the_last_dispatch(tmp_path, out):
     B.counters_from(_args(workload=2, counters_from=str(d)))
     md = open(out / "l2_100-multi-hot-d32-bf16-mean-adagrad.md").read()
     assert "| `rs::k_compact<256>` | 3.0 | 1.0 | 0.75 | 2.00 |" in md
+
+
+def test_ceilings_summary(tmp_path, out):
+    j = tmp_path / "ceil.json"
+    j.write_text('noise\n{"ceilings": {"read": {"bytes": 2147483648, "ms": 0.325, "GBps": 6607.6}}, '
+                 '"peak_GBps": 8000.0}\n')
+    st = tmp_path / "st"
+    _write_csv(os.path.join(st, "x", "c_kernel_stats.csv"),
+               [{"Name": "rs::k_probe_read(args)", "Calls": 6, "AverageNs": 326000, "MinNs": 320000,
+                 "MaxNs": 340000, "Percentage": 50.0},
+                {"Name": "at::native::fill(args)", "Calls": 1, "AverageNs": 1000, "MinNs": 1000, "MaxNs": 1000,
+                 "Percentage": 1.0}])
+    B.ceilings_from(argparse.Namespace(ceilings_from=[str(j), str(st)], traffic_cmd="cmd"))
+    md = open(out / "ceilings_mi355x.md").read()
+    assert "| read | 2147483648 | 0.325 | 6608 | 82.6 |" in md
+    assert "| `rs::k_probe_read` | 6 | 326.00 | 320.00 | 340.00 |" in md and "fill" not in md
