@@ -241,7 +241,9 @@ def profile_label(a) -> str:
         return f"ids_partition_1M_{a.shards or 8}shards"
     from paper_2509_20883_amd import workloads as W
 
-    return W.describe(W.workload(a.workload))["workload"]
+    wl = W.describe(W.workload(a.workload))["workload"]
+    age = getattr(a, "evict_age", -1)
+    return f"{wl}_evictable_age{age}" if age is not None and age >= 0 else wl
 
 
 def traffic_from(a):
