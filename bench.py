@@ -239,6 +239,8 @@ def profile_label(a) -> str:
     operator run by --op with its size."""
     if a.op == "ids-partition":
         return f"ids_partition_1M_{a.shards or 8}shards"
+    if a.op in ("bucketize", "mod"):
+        return f"{a.op}_100x10000"
     from paper_2509_20883_amd import workloads as W
 
     wl = W.describe(W.workload(a.workload))["workload"]
@@ -338,7 +340,8 @@ def trace_from(a):
         by[_kname(r)].append((int(r["Dispatch_Id"]), (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3))
     step = {k: v for k, v in by.items() if k.startswith("rs::") and "probe" not in k and "rehash" not in k
             and "map_rows" not in k and "k_occ_init<false>" not in k and "rereserve" not in k}
-    how = f"--op {a.op} --shards {a.shards or 8}" if a.op == "ids-partition" else f"--workload {a.workload}"
+    how = (f"--op {a.op} --shards {a.shards or 8}" if a.op == "ids-partition" else
+           f"--op {a.op}" if a.op != "step" else f"--workload {a.workload}")
     lines = [f"# Kernel time per {unit}: {wl}", "", "Command (MI355X, repository root copied to `<repo>`):", "", "```",
              a.traffic_cmd or "(command not recorded)", "```", "",
              f"Converted by `bench.py {how} --steps {a.steps} --trace-from <dir>`.", "",
