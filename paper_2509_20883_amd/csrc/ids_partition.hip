@@ -184,14 +184,11 @@ __global__ __launch_bounds__(1024) void k_scan_one(int32_t* __restrict__ a, int6
   }
   if (lane == 0) sh[wid] = run;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    int r = 0;
-    for (int q = 0; q < NW; ++q) {
-      const int t = sh[q];
-      sh[q] = r;
-      r += t;
-    }
-    sh[NW] = r;
+  if (wid == 0) {  // one wave scans the per-wave totals
+    const int t = lane < NW ? sh[lane] : 0;
+    const int i2 = wave_incl_scan(t);
+    if (lane < NW) sh[lane] = i2 - t;
+    if (lane == kWave - 1) sh[NW] = i2;
   }
   __syncthreads();
   const int off = sh[wid];
