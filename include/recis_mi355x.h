@@ -258,8 +258,11 @@ rs_status ht_read_rows(rs_table* t, const int64_t* rows, int64_t n, float* w_out
  * Synchronizes; returns (and clears) any latched device error. */
 rs_status ht_reserve(rs_table* t, int64_t live_upper_bound, rs_stream stream);
 
-/* Workspace bytes lookup_pool_fwd needs for n ids in `bags` bags (pad_len is
- * used by RS_POOL_NONE, else ignored) on table t. */
+/* Workspace bytes lookup_pool_fwd needs for n ids on table t.  Every
+ * workspace array is sized by the ids (and the table's dim); bags and
+ * pad_len do not change the size in this version (per-bag data lives in the
+ * caller's offsets and output), and are taken so that a later version may
+ * size per-bag arrays without changing the call. */
 size_t lookup_workspace_bytes(int64_t n, int64_t bags, int64_t pad_len, const rs_table* t);
 
 /* Forward: dedup + find-or-insert + fused gather/pool.
