@@ -72,6 +72,10 @@ def parse():
                     help="ids-partition: time the fused dedup + owner split alone on its one-million-id input; "
                          "bucketize / mod: the fused feature transforms on 100 columns of 10,000 values")
     ap.add_argument("--shards", type=int, default=None, help="owner shards of --op ids-partition (default 8)")
+    ap.add_argument("--kernels-from", nargs=6,
+                    metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR", "CAL_WRITE_DIR", "CEIL_JSON"),
+                    help="write profiles/kernels_<workload>.md: each step kernel's time, traffic, real bandwidth and "
+                         "its probe ceiling (no GPU needed)")
     ap.add_argument("--ceilings-from", nargs="+", metavar="PATH",
                     help="write profiles/ceilings_mi355x.md from a --ceilings JSON line [and its rocprofv3 "
                          "--kernel-trace --stats output directory] (no GPU needed)")
@@ -173,6 +177,72 @@ def ceilings():
         m = _probe_ms(fn)
         res[name] = {"bytes": nbytes, "ms": m, "GBps": nbytes / (m * 1e-3) / 1e9}
     print(json.dumps({"ceilings": res, "peak_GBps": HBM_PEAK_GBPS}))
+
+
+# which probe ceiling bounds each step kernel's access pattern (none: the
+# dedup passes' mixed random accesses of 8-32 bytes have no probe of their own)
+KERNEL_CEILING = {
+    "rs::k_bwd_short<": "read-modify-write of random 768-byte rows (+ index)",
+    "rs::k_pool<": "gather of random 256-byte rows (read + streamed write + index)",
+    "rs::k_bwd_long<": "read",
+    "rs::k_occ_list": "copy",
+    "rs::k_occ_init<": "copy",
+}
+
+
+def kernels_from(a):
+    """profiles/kernels_<workload>.md: per step kernel, its mean time over the
+    timed steps (kernel trace), its HBM traffic per launch (FETCH_SIZE /
+    WRITE_SIZE scaled by the copy probe), the real bandwidth that makes, and
+    the probe ceiling of its access pattern (a --ceilings JSON line)."""
+    from collections import defaultdict
+
+    tdir, fdir, wdir, cfdir, cwdir, cjson = a.kernels_from
+    wl = profile_label(a)
+    by = defaultdict(list)
+    for r in _csv_rows(tdir, "kernel_trace.csv"):
+        by[_kname(r)].append((int(r["Dispatch_Id"]), (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3))
+    us = {k: float(np.mean([t for _, t in sorted(v)[-a.steps:]])) for k, v in by.items() if k.startswith("rs::")}
+    gib_kib = (1 << 30) / 1024
+
+    def calib(d):
+        return gib_kib / float(np.median([float(r["Counter_Value"]) for r in _counter_rows(d)
+                                          if "k_probe_copy" in r["Kernel_Name"]]))
+
+    def last(d):
+        m = defaultdict(list)
+        for r in _counter_rows(d):
+            m[_kname(r)].append((int(r["Dispatch_Id"]), float(r["Counter_Value"]) * 1024))
+        return {k: max(v)[1] for k, v in m.items()}
+
+    fs, ws = calib(cfdir), calib(cwdir)
+    F, Wr = last(fdir), last(wdir)
+    with open(cjson) as fh:
+        ceil = json.loads([ln for ln in fh if ln.startswith("{")][-1])["ceilings"]
+    lines = [f"# Step kernels against the bandwidth ceilings: {wl}", "",
+             "Per kernel: mean time over the timed steps (kernel trace), HBM bytes per launch at the last step "
+             f"(FETCH_SIZE x{fs:.3f}, WRITE_SIZE x{ws:.3f}, the copy probe's scale), the real bandwidth they make, and "
+             "the library probe whose access pattern the kernel shares (`bench.py --ceilings`).  Converted by "
+             "`bench.py --kernels-from` from the runs of these commands:", "", "```",
+             a.traffic_cmd or "(commands not recorded)", "```", "",
+             "| kernel | us | fetch MB | write MB | real GB/s | ceiling probe | probe GB/s | % of probe |",
+             "|---|---|---|---|---|---|---|---|"]
+    for k in sorted(us, key=lambda k: -us[k]):
+        if ("probe" in k or "rehash" in k or "rereserve" in k or "map_rows" in k or "k_occ_init<false>" in k
+                or k not in F):
+            continue
+        fb, wb = F[k] * fs, Wr.get(k, 0.0) * ws
+        gbps = (fb + wb) / (us[k] * 1e-6) / 1e9
+        probe = next((c for pre, c in KERNEL_CEILING.items() if k.startswith(pre)), None)
+        pg = ceil[probe]["GBps"] if probe in ceil else None
+        lines.append(f"| `{k}` | {us[k]:.1f} | {fb / 1e6:.1f} | {wb / 1e6:.1f} | {gbps:.0f} | "
+                     f"{probe or 'none (mixed random 8-32-byte accesses)'} | {f'{pg:.0f}' if pg else '-'} | "
+                     f"{f'{100 * gbps / pg:.0f}' if pg else '-'} |")
+    lines.append("")
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(os.path.join(PROFILES, f"kernels_{wl}.md"), "w") as fh:
+        fh.write("\n".join(lines))
+    print("\n".join(lines))
 
 
 def ceilings_from(a):
@@ -770,6 +840,11 @@ def main():
         return
     if a.ceilings_from:
         ceilings_from(a)
+        return
+    if a.kernels_from:
+        if a.steps is None:
+            a.steps = 20
+        kernels_from(a)
         return
     if a.ceilings:
         ceilings()

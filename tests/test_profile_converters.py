@@ -119,3 +119,26 @@ def test_ceilings_summary(tmp_path, out):
     md = open(out / "ceilings_mi355x.md").read()
     assert "| read | 2147483648 | 0.325 | 6608 | 82.6 |" in md
     assert "| `rs::k_probe_read` | 6 | 326.00 | 320.00 | 340.00 |" in md and "fill" not in md
+
+
+def test_kernel_table_joins_time_traffic_and_ceiling(tmp_path, out):
+    gib_kib = (1 << 30) / 1024
+    cf, cw = tmp_path / "cf", tmp_path / "cw"
+    _counters(cf, "FETCH_SIZE", {"rs::k_probe_copy": [gib_kib / 2]})
+    _counters(cw, "WRITE_SIZE", {"rs::k_probe_copy": [gib_kib]})
+    f, w = tmp_path / "f", tmp_path / "w"
+    kern = "rs::k_bwd_short<float, float, 16, 0, true>"
+    _counters(f, "FETCH_SIZE", {kern: [1.0, 2e6]})   # 2e6 KiB x2 = 4.096 GB
+    _counters(w, "WRITE_SIZE", {kern: [1.0, 1e6]})   # 1.024 GB
+    t = tmp_path / "t"
+    rows = [{"Dispatch_Id": j + 1, "Kernel_Name": f"void {kern}(args)", "Start_Timestamp": 0,
+             "End_Timestamp": 1_000_000} for j in range(3)]  # 1 ms each
+    _write_csv(os.path.join(t, "x", "b_kernel_trace.csv"), rows)
+    c = tmp_path / "c.json"
+    c.write_text('{"ceilings": {"read-modify-write of random 768-byte rows (+ index)": '
+                 '{"bytes": 1, "ms": 1, "GBps": 6400.0}}, "peak_GBps": 8000.0}\n')
+    B.kernels_from(_args(steps=2, kernels_from=[str(t), str(f), str(w), str(cf), str(cw), str(c)]))
+    md = open(out / "kernels_200-feat-growing-d64-adam.md").read()
+    # (4.096 + 1.024) GB in 1 ms = 5120 GB/s, 80% of the probe's 6400
+    assert f"| `{kern}` | 1000.0 | 4096.0 | 1024.0 | 5120 | read-modify-write of random 768-byte rows (+ index) " \
+           f"| 6400 | 80 |" in md
