@@ -184,6 +184,7 @@ def ceilings():
 KERNEL_CEILING = {
     "rs::k_bwd_short<": "read-modify-write of random 768-byte rows (+ index)",
     "rs::k_pool<": "gather of random 256-byte rows (read + streamed write + index)",
+    "rs::k_pool_none<": "gather of random 256-byte rows (read + streamed write + index)",
     "rs::k_bwd_long<": "read",
     "rs::k_occ_list": "copy",
     "rs::k_occ_init<": "copy",
